@@ -1,0 +1,170 @@
+/*
+ * kred: reductions over symbolic M x N kernel and distance matrices on one
+ * AMD Instinct MI355X (gfx950).  C ABI.
+ *
+ * The library evaluates Eq. (2) of Charlier et al., "Kernel Operations on the
+ * GPU, with Autodiff, without Memory Overflows" (arXiv:2004.11127, Sec. 2):
+ *
+ *     a_i = Reduction_{j = 0..N-1} F(p, x_i, y_j, b_j),   i = 0..M-1,
+ *
+ * for a fixed set of formulas F and the reductions Sec. 2 lists, without ever
+ * storing the M x N matrix (Sec. 2: no N-by-M buffer in device memory; memory
+ * stays linear in M + N).  The motivating case is Eq. (1), the Gaussian
+ * kernel sum a_i = sum_j exp(-|x_i - y_j|^2 / (2 sigma^2)) b_j.  Indices are
+ * 0-based (the paper counts i = 1..M, j = 1..N).
+ *
+ * Layout: every array is dense, contiguous, row-major fp32 (int32 for k-NN
+ * indices) in device memory of the context's device: x is M x D, y is N x D,
+ * b is N x E.  Pointers need 4-byte alignment.  The caller owns x, y, b and
+ * out; the library never frees or keeps them past the call.
+ *
+ * Errors: every argument is checked on the host before anything is launched;
+ * on any error nothing runs and out is untouched.  Launch failures return
+ * KRED_ERR_HIP.  Faults inside a kernel surface at the caller's next
+ * synchronisation.  The library never prints and never aborts.
+ *
+ * Concurrency: kred_run is asynchronous on `stream`.  A context owns scratch
+ * memory (column-split partials and packed copies of y and b) that calls on it
+ * reuse, so one context must not run on two streams at once; use one context
+ * per stream.
+ */
+#ifndef KRED_H
+#define KRED_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KRED_VERSION 1
+
+/* Formulas F (Sec. 2 "symbolic formula"; Eq. (1) is KRED_F_GAUSS). */
+typedef enum kred_formula {
+  KRED_F_GAUSS = 0,       /* k = exp(-|x - y|^2 / (2 sigma^2)), F = k b            (Eq. (1)) */
+  KRED_F_LAPLACE = 1,     /* k = exp(-|x - y| / sigma),         F = k b                      */
+  KRED_F_SQDIST = 2,      /* d = |x - y|^2,                     F = d b (sum) or d (arg-K-min) */
+  KRED_F_GAUSS_GRADX = 3, /* Eq. (1) and its gradient in x_i, fused (Sec. 2 "Backpropagation") */
+  KRED_F_SINKHORN = 4     /* s = g_j - |x - y|^2 / eps, with g_j passed in b          */
+} kred_formula;
+
+/* Reductions over j (Sec. 2: .sum(), .logsumexp(), .argKmin(K)). */
+typedef enum kred_reduction {
+  KRED_R_SUM = 0,
+  KRED_R_LSE = 1,
+  KRED_R_ARGKMIN = 2
+} kred_reduction;
+
+typedef enum kred_status {
+  KRED_OK = 0,
+  KRED_ERR_INVALID_ARG = 1,  /* a null pointer, a size or parameter out of range */
+  KRED_ERR_UNSUPPORTED = 2,  /* a (formula, reduction) pair the library does not provide */
+  KRED_ERR_NOMEM = 3,        /* scratch allocation failed */
+  KRED_ERR_HIP = 4,          /* a HIP runtime call or kernel launch failed */
+  KRED_ERR_NO_DEVICE = 5     /* no usable gfx950 device with that ordinal */
+} kred_status;
+
+/* flags */
+#define KRED_FLAG_PROFILE 1u  /* time the main kernel of each call with HIP events (kred_profile_collect) */
+
+/* Per-call parameters (the "parameters p" of Eq. (2)). */
+typedef struct kred_params {
+  float sigma;        /* kernel width for GAUSS, LAPLACE, GAUSS_GRADX; > 0, finite       */
+  float eps;          /* temperature for SINKHORN; > 0, finite                            */
+  int32_t K;          /* number of neighbours for ARGKMIN; 1 <= K <= min(N, 64)           */
+  int32_t col_blocks; /* j split into this many blocks reduced in a second pass; 0 = auto */
+  uint32_t flags;     /* KRED_FLAG_* */
+} kred_params;
+
+/* Limits */
+#define KRED_MAX_D 256
+#define KRED_MAX_E 64
+#define KRED_MAX_K 64
+#define KRED_MAX_COL_BLOCKS 256
+
+typedef struct kred_ctx kred_ctx;
+
+/*
+ * Create a context on HIP device `device` (ordinal as seen by the process).
+ * On success *ctx is set; release it with kred_destroy.  Allocates no device
+ * memory until a call needs scratch.  Returns KRED_ERR_INVALID_ARG if ctx is
+ * NULL, KRED_ERR_NO_DEVICE if the ordinal is invalid or not gfx950,
+ * KRED_ERR_NOMEM if the host allocation fails.
+ */
+kred_status kred_create(kred_ctx** ctx, int device);
+
+/* Free the context and its scratch memory (synchronises the device first).
+ * NULL is accepted and ignored. */
+kred_status kred_destroy(kred_ctx* ctx);
+
+/*
+ * Evaluate a_i = Reduction_j F(p, x_i, y_j, b_j) for i = 0..M-1 (Eq. (2)).
+ *
+ * Valid (formula, reduction) pairs and their operands:
+ *   (GAUSS | LAPLACE | SQDIST, SUM):  b is N x E, out is fp32 M x E:
+ *        out[i, e] = sum_j F(|x_i - y_j|^2) b[j, e].
+ *   (GAUSS_GRADX, SUM), E = 1:  b is N x 1, out is fp32 M x (1 + D):
+ *        out[i, 0]     = a_i = sum_j k_ij b_j                       (Eq. (1))
+ *        out[i, 1 + k] = sum_j k_ij b_j (y_jk - x_ik) / sigma^2 = d a_i / d x_ik.
+ *   (SINKHORN, LSE), E = 1:  b holds g (N x 1), out is fp32 M x 1:
+ *        out[i] = log sum_j exp(g_j - |x_i - y_j|^2 / eps)   (natural log).
+ *   (SQDIST, ARGKMIN):  b must be NULL and E is ignored (pass 0), out is int32
+ *        M x K: the indices j of the K smallest |x_i - y_j|^2, ascending by
+ *        (distance, index): equal distances keep the lower index first.
+ * Any other pair returns KRED_ERR_UNSUPPORTED.
+ *
+ * Ranges: 0 <= M, N <= 2^31 - 1; 1 <= D <= KRED_MAX_D; 1 <= E <= KRED_MAX_E
+ * for SUM; p->col_blocks in [0, KRED_MAX_COL_BLOCKS].  Inputs must be finite
+ * (NaN or Inf in x, y or b gives an undefined result).
+ * Edge cases: M = 0 returns KRED_OK and touches nothing.  N = 0 writes zeros
+ * (SUM) or -infinity (LSE); ARGKMIN with N = 0 fails since it needs K <= N.
+ *
+ * `stream` is a hipStream_t (NULL = the null stream of the context's device).
+ * The call is asynchronous: it returns once the kernels are enqueued.
+ * Scratch memory comes from the context and is grown with hipMalloc when a
+ * call needs more than it holds; no M x N buffer is ever allocated (scratch
+ * is O((M + N) (D + E)) plus O(M col_blocks (E + D + K))).
+ */
+kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
+                     int64_t M, int64_t N, int32_t D, int32_t E,
+                     const float* x, const float* y, const float* b, void* out,
+                     void* stream);
+
+/*
+ * Host-only argument check with the same rules kred_run applies (kred_run
+ * calls it first).  Touches no device and dereferences no array pointer, so
+ * it runs on machines without a GPU.  Returns KRED_OK or the error kred_run
+ * would return.
+ */
+kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p,
+                          int64_t M, int64_t N, int32_t D, int32_t E,
+                          const void* x, const void* y, const void* b, const void* out);
+
+/*
+ * Scratch bytes kred_run will need for this call (0 when none), or -1 when
+ * the arguments are invalid.  Host-only.
+ */
+int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* p,
+                           int64_t M, int64_t N, int32_t D, int32_t E);
+
+/*
+ * With KRED_FLAG_PROFILE set on calls, the context records a HIP event pair
+ * around the main reduction kernel of each call.  This waits for those
+ * events, returns the number of timed launches in *count and their summed
+ * duration in milliseconds in *total_ms, and forgets them.  Names the last
+ * timed kernel family in *kernel (static string; may be NULL).
+ */
+kred_status kred_profile_collect(kred_ctx* ctx, int32_t* count, double* total_ms,
+                                 const char** kernel);
+
+/* Static description of a status code. */
+const char* kred_strerror(kred_status s);
+
+/* KRED_VERSION of the built library. */
+int32_t kred_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KRED_H */

@@ -1,0 +1,166 @@
+"""kred oracle: fp64 CPU reference for the symbolic-matrix reductions.
+
+TEST INFRASTRUCTURE ONLY.  The tests, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` call it to check and to time the GPU
+library; the library itself never imports, links or runs anything here, and
+this package shares no code with it.
+
+The arithmetic lives in ``kred_oracle.c`` (plain C, fp64, OpenMP over rows);
+this module builds it with gcc on first use, converts fp32 inputs to fp64 and
+marshals arguments.  What each routine computes follows Charlier et al.,
+"Kernel Operations on the GPU, with Autodiff, without Memory Overflows"
+(arXiv:2004.11127): Eq. (1) (Gaussian kernel sum), Eq. (2) with the
+reductions of Sec. 2 (sum, log-sum-exp, arg-K-min), and the x-gradient of
+Eq. (1) (Sec. 2, "Backpropagation").  The C file's header lists the readings
+taken where the paper is silent.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "kred_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+GAUSS, LAPLACE, SQDIST = 0, 1, 2
+_FORMULAS = {"gauss": GAUSS, "laplace": LAPLACE, "sqdist": SQDIST}
+
+_dp = ctypes.POINTER(ctypes.c_double)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+
+
+def build(force: bool = False) -> str:
+    """Compile liboracle.so with gcc (-O2, OpenMP, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-fno-fast-math",
+               "-ffp-contract=off", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            build()
+            lib = ctypes.CDLL(_LIB)
+            lib.oracle_kernel_sum.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_int64,
+                                              ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                              _dp, _dp, _dp, _i64p, ctypes.c_int64, _dp, _dp]
+            lib.oracle_gauss_gradx.argtypes = [ctypes.c_double, ctypes.c_int64, ctypes.c_int64,
+                                               ctypes.c_int, _dp, _dp, _dp, _i64p,
+                                               ctypes.c_int64, _dp, _dp]
+            lib.oracle_sinkhorn_lse.argtypes = [ctypes.c_double, ctypes.c_int64, ctypes.c_int64,
+                                                ctypes.c_int, _dp, _dp, _dp, _i64p,
+                                                ctypes.c_int64, _dp, _dp]
+            lib.oracle_argkmin.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                           ctypes.c_int, _dp, _dp, _i64p, ctypes.c_int64,
+                                           _i64p, _dp]
+            for f in (lib.oracle_kernel_sum, lib.oracle_gauss_gradx, lib.oracle_sinkhorn_lse,
+                      lib.oracle_argkmin):
+                f.restype = ctypes.c_int
+            _lib = lib
+    return _lib
+
+
+def _f64(a, ncols=None):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+    if ncols is not None:
+        a = a.reshape(-1, ncols)
+    return a
+
+
+def _ptr(a, t=_dp):
+    return a.ctypes.data_as(t) if a is not None else None
+
+
+def _rows(rows, M):
+    if rows is None:
+        return None, M
+    r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+    if r.size and (r.min() < 0 or r.max() >= M):
+        raise ValueError("row index out of range")
+    return r, r.size
+
+
+def _check(rc):
+    if rc != 0:
+        raise ValueError("oracle rejected its arguments")
+
+
+def kernel_sum(formula, x, y, b, sigma=1.0, rows=None):
+    """Sum reduction, Eq. (2) with F = kernel(|x_i - y_j|^2) b_j (Eq. (1) for "gauss").
+
+    Returns (a, norm), each (nrows, E) float64; norm = sum_j |F b_j|.
+    """
+    fcode = _FORMULAS[formula]
+    x = _f64(x); y = _f64(y)
+    M, D = x.shape
+    N = y.shape[0]
+    b = np.asarray(b, dtype=np.float64)
+    E = b.shape[1] if b.ndim == 2 else 1
+    b = _f64(b, E)
+    r, nr = _rows(rows, M)
+    out = np.empty((nr, E)); norm = np.empty((nr, E))
+    _check(_load().oracle_kernel_sum(fcode, float(sigma), M, N, D, E, _ptr(x), _ptr(y),
+                                     _ptr(b), _ptr(r, _i64p), nr, _ptr(out), _ptr(norm)))
+    return out, norm
+
+
+def gauss_gradx(x, y, b, sigma, rows=None):
+    """Gaussian sum (E = 1) and its x-gradient.
+
+    Returns (out, norm), each (nrows, 1 + D): column 0 is a_i, columns 1..D are
+    g_i = sum_j k_ij b_j (y_j - x_i) / sigma^2; norm sums the absolute summands.
+    """
+    x = _f64(x); y = _f64(y)
+    M, D = x.shape
+    N = y.shape[0]
+    b = _f64(b).reshape(N)
+    r, nr = _rows(rows, M)
+    out = np.empty((nr, 1 + D)); norm = np.empty((nr, 1 + D))
+    _check(_load().oracle_gauss_gradx(float(sigma), M, N, D, _ptr(x), _ptr(y), _ptr(b),
+                                      _ptr(r, _i64p), nr, _ptr(out), _ptr(norm)))
+    return out, norm
+
+
+def sinkhorn_lse(x, y, g, eps, rows=None):
+    """Log-sum-exp reduction a_i = log sum_j exp(g_j - |x_i - y_j|^2 / eps).
+
+    Returns (a, m): a (nrows,) and the row maxima m_i = max_j s_ij.
+    """
+    x = _f64(x); y = _f64(y)
+    M, D = x.shape
+    N = y.shape[0]
+    g = _f64(g).reshape(N)
+    r, nr = _rows(rows, M)
+    out = np.empty(nr); mx = np.empty(nr)
+    _check(_load().oracle_sinkhorn_lse(float(eps), M, N, D, _ptr(x), _ptr(y), _ptr(g),
+                                       _ptr(r, _i64p), nr, _ptr(out), _ptr(mx)))
+    return out, mx
+
+
+def argkmin(x, y, K, rows=None):
+    """Arg-K-min: indices of the K smallest |x_i - y_j|^2, ascending by (distance, index).
+
+    Returns (idx int64 (nrows, K), dist float64 (nrows, K)).
+    """
+    x = _f64(x); y = _f64(y)
+    M, D = x.shape
+    N = y.shape[0]
+    if not (1 <= K <= min(N, 1024)):
+        raise ValueError("need 1 <= K <= min(N, 1024)")
+    r, nr = _rows(rows, M)
+    idx = np.empty((nr, K), dtype=np.int64); dist = np.empty((nr, K))
+    _check(_load().oracle_argkmin(M, N, D, int(K), _ptr(x), _ptr(y), _ptr(r, _i64p), nr,
+                                  _ptr(idx, _i64p), _ptr(dist)))
+    return idx, dist

@@ -1,0 +1,286 @@
+"""Pins for the fp64 oracle, checked against what the mathematics fixes (CPU only).
+
+The paper prints no worked numeric example, so the oracle is pinned by
+hand-derived two-point values (tests/golden/hand_values.json), closed forms
+that hold at any size (separable sums on Cartesian lattices, sigma -> infinity
+limits, the expanded squared-distance identity), invariants (linearity,
+translation and joint-permutation invariance, log-sum-exp shift), finite
+differences for the gradient, and brute-force sorting for arg-K-min.  Each
+check is chosen so that a plausible slip in the oracle (a dropped term, a
+wrong sign, scale or index, a transposed operand, a wrong tie-break) fails.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_values.json")
+
+
+@pytest.fixture(scope="module")
+def hv():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+def _a(v):
+    return np.asarray(v, dtype=np.float64)
+
+
+# ---------------------------------------------------------------- hand values
+
+def test_golden_file_matches_its_closed_forms(hv):
+    # The stored numbers are the closed forms written in each entry.
+    assert hv["gauss_two_point"]["value"] == pytest.approx(1 + 2 * math.exp(-0.5), rel=1e-15)
+    assert hv["gauss_two_point_scaled"]["value"] == pytest.approx(3 - math.exp(-2), rel=1e-15)
+    assert hv["laplace_two_point"]["value"] == pytest.approx(1 + 2 * math.exp(-1), rel=1e-15)
+    assert hv["lse_two_point"]["value"] == pytest.approx(math.log(2), rel=1e-15)
+
+
+@pytest.mark.parametrize("key,formula", [("gauss_two_point", "gauss"),
+                                         ("gauss_two_point_scaled", "gauss"),
+                                         ("laplace_two_point", "laplace"),
+                                         ("sqdist_two_point", "sqdist")])
+def test_sum_hand_values(oracle_mod, hv, key, formula):
+    c = hv[key]
+    a, n = oracle_mod.kernel_sum(formula, _a(c["x"]), _a(c["y"]), _a(c["b"]), sigma=c["sigma"])
+    assert a[0, 0] == pytest.approx(c["value"], rel=1e-14, abs=1e-14)
+
+
+def test_gradx_hand_value(oracle_mod, hv):
+    c = hv["gradx_one_point"]
+    out, norm = oracle_mod.gauss_gradx(_a(c["x"]), _a(c["y"]), _a(c["b"]), c["sigma"])
+    np.testing.assert_allclose(out[0], c["value"], rtol=1e-14, atol=1e-15)
+
+
+def test_lse_hand_value(oracle_mod, hv):
+    c = hv["lse_two_point"]
+    a, m = oracle_mod.sinkhorn_lse(_a(c["x"]), _a(c["y"]), _a(c["g"]), c["eps"])
+    assert a[0] == pytest.approx(c["value"], rel=1e-14)
+    assert m[0] == pytest.approx(0.0, abs=1e-15)
+
+
+def test_argkmin_hand_value(oracle_mod, hv):
+    c = hv["argkmin_small"]
+    idx, dist = oracle_mod.argkmin(_a(c["x"]), _a(c["y"]), c["K"])
+    assert idx[0].tolist() == c["value"]
+    np.testing.assert_array_equal(dist[0], [0.0, 1.0, 1.0, 1.0])
+
+
+# ---------------------------------------------------------- Gaussian closed forms
+
+def _lattice(axes):
+    g = np.meshgrid(*axes, indexing="ij")
+    return np.stack([t.ravel() for t in g], axis=1)
+
+
+@pytest.mark.parametrize("sigma", [0.07, 0.3, 1.7])
+def test_gauss_separable_lattice(oracle_mod, sigma):
+    # With b = 1 and y on a Cartesian lattice G1 x G2 x G3, Eq. (1) factorises:
+    # a(x) = prod_d sum_{t in G_d} exp(-(x_d - t)^2 / (2 sigma^2)).
+    # Axes of different lengths and spacings catch swapped coordinates.
+    axes = [np.linspace(-0.3, 0.9, 5), np.linspace(0.1, 0.4, 3), np.array([-1.0, 0.0, 0.5, 2.0])]
+    y = _lattice(axes)
+    rng = np.random.default_rng(1)
+    x = rng.uniform(-0.5, 1.0, (17, 3))
+    b = np.ones((y.shape[0], 1))
+    a, n = oracle_mod.kernel_sum("gauss", x, y, b, sigma=sigma)
+    want = np.ones(x.shape[0])
+    for d in range(3):
+        want *= np.exp(-(x[:, d:d + 1] - axes[d][None, :]) ** 2 / (2 * sigma ** 2)).sum(axis=1)
+    np.testing.assert_allclose(a[:, 0], want, rtol=1e-13)
+    np.testing.assert_allclose(n[:, 0], want, rtol=1e-13)  # all terms positive
+
+
+def test_gauss_separable_lattice_high_dim(oracle_mod):
+    # Same identity in D = 6 with a two-point axis per dimension (64 lattice points).
+    axes = [np.array([0.0, 0.1 * (d + 1)]) for d in range(6)]
+    y = _lattice(axes)
+    x = np.random.default_rng(2).normal(size=(5, 6)) * 0.2
+    a, _ = oracle_mod.kernel_sum("gauss", x, y, np.ones((64, 1)), sigma=0.25)
+    want = np.ones(5)
+    for d in range(6):
+        want *= np.exp(-(x[:, d:d + 1] - axes[d][None, :]) ** 2 / (2 * 0.25 ** 2)).sum(axis=1)
+    np.testing.assert_allclose(a[:, 0], want, rtol=1e-13)
+
+
+@pytest.mark.parametrize("formula", ["gauss", "laplace"])
+def test_sigma_to_infinity_gives_sum_of_b(oracle_mod, formula):
+    rng = np.random.default_rng(3)
+    x = rng.uniform(0, 1, (9, 3)); y = rng.uniform(0, 1, (31, 3)); b = rng.normal(size=(31, 2))
+    a, n = oracle_mod.kernel_sum(formula, x, y, b, sigma=1e9)
+    np.testing.assert_allclose(a, np.broadcast_to(b.sum(axis=0), a.shape), rtol=1e-7, atol=1e-8)
+    np.testing.assert_allclose(n, np.broadcast_to(np.abs(b).sum(axis=0), n.shape), rtol=1e-7)
+
+
+def test_linearity_translation_permutation(oracle_mod):
+    rng = np.random.default_rng(4)
+    x = rng.uniform(0, 1, (13, 3)); y = rng.uniform(0, 1, (40, 3))
+    b1 = rng.normal(size=(40, 3)); b2 = rng.normal(size=(40, 3))
+    a1, _ = oracle_mod.kernel_sum("gauss", x, y, b1, sigma=0.2)
+    a2, _ = oracle_mod.kernel_sum("gauss", x, y, b2, sigma=0.2)
+    a12, _ = oracle_mod.kernel_sum("gauss", x, y, 2.0 * b1 - 3.0 * b2, sigma=0.2)
+    np.testing.assert_allclose(a12, 2 * a1 - 3 * a2, rtol=1e-12, atol=1e-12)
+    t = np.array([[5.0, -2.0, 0.25]])
+    at, _ = oracle_mod.kernel_sum("gauss", x + t, y + t, b1, sigma=0.2)
+    np.testing.assert_allclose(at, a1, rtol=1e-10, atol=1e-12)
+    p = rng.permutation(40)
+    ap, _ = oracle_mod.kernel_sum("gauss", x, y[p], b1[p], sigma=0.2)
+    np.testing.assert_allclose(ap, a1, rtol=1e-12, atol=1e-13)
+
+
+def test_rows_subset_matches_full(oracle_mod):
+    rng = np.random.default_rng(5)
+    x = rng.uniform(0, 1, (50, 3)); y = rng.uniform(0, 1, (60, 3)); b = rng.normal(size=(60, 1))
+    full, _ = oracle_mod.kernel_sum("gauss", x, y, b, sigma=0.3)
+    rows = np.array([0, 7, 49, 23])
+    sub, _ = oracle_mod.kernel_sum("gauss", x, y, b, sigma=0.3, rows=rows)
+    np.testing.assert_array_equal(sub, full[rows])
+
+
+def test_empty_inputs(oracle_mod):
+    x = np.zeros((3, 2)); y = np.zeros((0, 2)); b = np.zeros((0, 4))
+    a, n = oracle_mod.kernel_sum("gauss", x, y, b, sigma=1.0)
+    assert a.shape == (3, 4) and not a.any() and not n.any()
+    l, _ = oracle_mod.sinkhorn_lse(x, y, np.zeros((0, 1)), 1.0)
+    assert np.all(np.isneginf(l))
+
+
+# ------------------------------------------------------------------ Laplace, SqDist
+
+def test_laplace_two_points_on_axis(oracle_mod):
+    # |x - y| = 2 and 0.5 on an axis: 1*exp(-2/0.5)... closed form per term.
+    x = _a([[1.0, 1.0]]); y = _a([[3.0, 1.0], [1.0, 0.5]]); b = _a([[1.0], [-4.0]])
+    a, n = oracle_mod.kernel_sum("laplace", x, y, b, sigma=0.5)
+    assert a[0, 0] == pytest.approx(math.exp(-4.0) - 4.0 * math.exp(-1.0), rel=1e-14)
+    assert n[0, 0] == pytest.approx(math.exp(-4.0) + 4.0 * math.exp(-1.0), rel=1e-14)
+
+
+def test_sqdist_sum_expanded_identity(oracle_mod):
+    # sum_j |x_i - y_j|^2 b_j = |x_i|^2 sum_j b_j - 2 <x_i, sum_j b_j y_j> + sum_j b_j |y_j|^2
+    rng = np.random.default_rng(6)
+    x = rng.normal(size=(11, 5)); y = rng.normal(size=(37, 5)); b = rng.normal(size=(37, 2))
+    a, _ = oracle_mod.kernel_sum("sqdist", x, y, b)
+    want = (np.sum(x * x, 1)[:, None] * b.sum(0)[None, :] - 2 * x @ (y.T @ b)
+            + (np.sum(y * y, 1)[:, None] * b).sum(0)[None, :])
+    np.testing.assert_allclose(a, want, rtol=1e-11, atol=1e-11)
+
+
+# ------------------------------------------------------------------------ gradient
+
+def test_gradx_column0_is_gauss_sum(oracle_mod):
+    rng = np.random.default_rng(7)
+    x = rng.uniform(0, 1, (8, 3)); y = rng.uniform(0, 1, (25, 3)); b = rng.normal(size=(25, 1))
+    out, norm = oracle_mod.gauss_gradx(x, y, b, 0.3)
+    a, n = oracle_mod.kernel_sum("gauss", x, y, b, sigma=0.3)
+    np.testing.assert_allclose(out[:, 0], a[:, 0], rtol=1e-14)
+    np.testing.assert_allclose(norm[:, 0], n[:, 0], rtol=1e-14)
+
+
+@pytest.mark.parametrize("sigma,D", [(0.3, 3), (0.05, 3), (1.1, 5)])
+def test_gradx_matches_finite_differences(oracle_mod, sigma, D):
+    # g_ik = d a_i / d x_ik: central differences of the oracle's own a_i, in fp64.
+    rng = np.random.default_rng(8)
+    x = rng.uniform(0, 1, (6, D)) * (4 * sigma); y = rng.uniform(0, 1, (30, D)) * (4 * sigma)
+    b = rng.normal(size=(30, 1))
+    out, norm = oracle_mod.gauss_gradx(x, y, b, sigma)
+    h = 1e-5 * sigma
+    for k in range(D):
+        xp = x.copy(); xp[:, k] += h
+        xm = x.copy(); xm[:, k] -= h
+        ap, _ = oracle_mod.kernel_sum("gauss", xp, y, b, sigma=sigma)
+        am, _ = oracle_mod.kernel_sum("gauss", xm, y, b, sigma=sigma)
+        fd = (ap[:, 0] - am[:, 0]) / (2 * h)
+        np.testing.assert_allclose(out[:, 1 + k], fd, rtol=1e-6, atol=1e-7 * norm[:, 1 + k].max())
+
+
+# ---------------------------------------------------------------------- log-sum-exp
+
+def test_lse_single_point(oracle_mod):
+    x = _a([[0.1, 0.2, 0.3], [1.0, 0.0, -1.0]]); y = _a([[0.0, 0.0, 0.0]]); g = _a([[0.7]])
+    a, _ = oracle_mod.sinkhorn_lse(x, y, g, 0.5)
+    want = 0.7 - np.sum(x ** 2, 1) / 0.5
+    np.testing.assert_allclose(a, want, rtol=1e-14)
+
+
+def test_lse_eps_to_infinity_is_logsumexp_of_g(oracle_mod):
+    rng = np.random.default_rng(9)
+    x = rng.uniform(0, 1, (5, 3)); y = rng.uniform(0, 1, (50, 3)); g = rng.normal(size=(50, 1))
+    a, _ = oracle_mod.sinkhorn_lse(x, y, g, 1e30)
+    np.testing.assert_allclose(a, np.logaddexp.reduce(g[:, 0]), rtol=1e-14)
+
+
+def test_lse_shift_and_large_offsets(oracle_mod):
+    rng = np.random.default_rng(10)
+    x = rng.uniform(0, 1, (7, 3)); y = rng.uniform(0, 1, (64, 3)); g = rng.normal(size=(64, 1))
+    a, m = oracle_mod.sinkhorn_lse(x, y, g, 0.01)
+    for c in (3.5, -1000.0, 1000.0):
+        ac, mc = oracle_mod.sinkhorn_lse(x, y, g + c, 0.01)
+        np.testing.assert_allclose(ac, a + c, rtol=1e-13, atol=1e-11)
+        np.testing.assert_allclose(mc, m + c, rtol=1e-13, atol=1e-11)
+    # log-sum-exp lies between the max and the max + log N
+    assert np.all(a >= m - 1e-12) and np.all(a <= m + math.log(64) + 1e-12)
+
+
+def test_lse_equals_log_of_gaussian_sum(oracle_mod):
+    # With g_j = log b_j (b > 0) and eps = 2 sigma^2 the two formulas coincide:
+    # log sum_j exp(log b_j - d/(2 sigma^2)) = log sum_j exp(-d/(2 sigma^2)) b_j.
+    rng = np.random.default_rng(11)
+    x = rng.uniform(0, 1, (9, 3)); y = rng.uniform(0, 1, (80, 3)); b = rng.uniform(0.1, 2.0, (80, 1))
+    sigma = 0.2
+    gs, _ = oracle_mod.kernel_sum("gauss", x, y, b, sigma=sigma)
+    l, _ = oracle_mod.sinkhorn_lse(x, y, np.log(b), 2 * sigma ** 2)
+    np.testing.assert_allclose(l, np.log(gs[:, 0]), rtol=1e-13)
+
+
+# ------------------------------------------------------------------------- arg-K-min
+
+def _brute_knn(x, y, K):
+    d = ((x[:, None, :] - y[None, :, :]) ** 2).sum(-1)
+    out = []
+    for i in range(x.shape[0]):
+        order = np.lexsort((np.arange(y.shape[0]), d[i]))  # primary: distance, then index
+        out.append(order[:K])
+    return np.array(out)
+
+
+@pytest.mark.parametrize("K", [1, 3, 10, 57])
+def test_argkmin_brute_force_with_ties(oracle_mod, K):
+    rng = np.random.default_rng(12)
+    # integer coordinates in a small box force many equal distances
+    x = rng.integers(-2, 3, (23, 4)).astype(np.float64)
+    y = rng.integers(-2, 3, (57, 4)).astype(np.float64)
+    idx, dist = oracle_mod.argkmin(x, y, K)
+    np.testing.assert_array_equal(idx, _brute_knn(x, y, K))
+    # distances non-decreasing, and equal distances in increasing index order
+    assert np.all(np.diff(dist, axis=1) >= 0)
+    same = np.diff(dist, axis=1) == 0
+    assert np.all(np.diff(idx, axis=1)[same] > 0)
+
+
+def test_argkmin_full_sort_and_self_neighbour(oracle_mod):
+    rng = np.random.default_rng(13)
+    y = rng.normal(size=(40, 3))
+    x = y[[5, 0, 39, 17]]
+    idx, dist = oracle_mod.argkmin(x, y, 40)
+    assert idx[:, 0].tolist() == [5, 0, 39, 17]
+    assert np.all(dist[:, 0] == 0)
+    np.testing.assert_array_equal(idx, _brute_knn(x, y, 40))
+    for r in range(4):
+        assert sorted(idx[r].tolist()) == list(range(40))
+
+
+def test_argkmin_duplicate_points_lowest_index_first(oracle_mod):
+    y = _a([[1, 1], [0, 0], [1, 1], [0, 0], [0, 0], [2, 2]])
+    idx, _ = oracle_mod.argkmin(_a([[0, 0]]), y, 5)
+    assert idx[0].tolist() == [1, 3, 4, 0, 2]
+
+
+def test_argkmin_rejects_bad_k(oracle_mod):
+    x = np.zeros((2, 2)); y = np.zeros((3, 2))
+    with pytest.raises(ValueError):
+        oracle_mod.argkmin(x, y, 4)
+    with pytest.raises(ValueError):
+        oracle_mod.argkmin(x, y, 0)
