@@ -1,0 +1,133 @@
+// Second pass over column-block partials (when the j range was split into C
+// blocks to give a small-M problem enough workgroups).  Each partial is the
+// reduction of Eq. (2) over one block of columns; this pass applies the same
+// reduction across blocks, in increasing block order (fixed, so results are
+// reproducible run to run):
+//   sum:          a = sum_c a_c
+//   log-sum-exp:  (m, s) = (max_c m_c, sum_c s_c 2^(m_c - m)),  a = (m + log2 s) ln 2
+//   arg-K-min:    merge the C sorted (distance, index) lists, keep the K first.
+// The second pass reads C x M x W floats once; it is HBM-bound.
+#include "kred_internal.h"
+
+#include <climits>
+
+namespace kred {
+namespace {
+
+__global__ __launch_bounds__(256) void combine_sum_kernel(CombineArgs a) {
+  const int Ec = min(a.EP, a.E - a.e0);
+  const int64_t total = a.M * Ec;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = t / Ec;
+    const int e = (int)(t - row * Ec);
+    float s = 0.0f;
+    for (int c = 0; c < a.C; ++c) s += a.part[((int64_t)c * a.M + row) * a.EP + e];
+    static_cast<float*>(a.out)[row * a.E + a.e0 + e] = s;
+  }
+}
+
+__global__ __launch_bounds__(256) void combine_gradx_kernel(CombineArgs a) {
+  const int W = a.DP + 1;
+  const int64_t total = a.M * (1 + a.D);
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = t / (1 + a.D);
+    const int w = (int)(t - row * (1 + a.D));
+    float s = 0.0f;
+    for (int c = 0; c < a.C; ++c) s += a.part[((int64_t)c * a.M + row) * W + w];
+    static_cast<float*>(a.out)[t] = (w == 0) ? s : -s * a.gscale;
+  }
+}
+
+__global__ __launch_bounds__(256) void combine_lse_kernel(CombineArgs a) {
+  for (int64_t row = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; row < a.M;
+       row += (int64_t)gridDim.x * blockDim.x) {
+    float m = -__builtin_inff();
+    for (int c = 0; c < a.C; ++c) m = fmaxf(m, a.part[((int64_t)c * a.M + row) * 2]);
+    float s = 0.0f;
+    for (int c = 0; c < a.C; ++c) {
+      const float* p = a.part + ((int64_t)c * a.M + row) * 2;
+      s += p[1] * __builtin_amdgcn_exp2f(p[0] - m);
+    }
+    static_cast<float*>(a.out)[row] = (m + __builtin_amdgcn_logf(s)) * kLn2;
+  }
+}
+
+// (d, j) strictly before (d2, j2) in (distance, index) order.
+__device__ __forceinline__ bool before(float d, int j, float d2, int j2) {
+  return d < d2 || (d == d2 && j < j2);
+}
+
+template <int KP>
+__global__ __launch_bounds__(256) void combine_knn_kernel(CombineArgs a) {
+  for (int64_t row = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; row < a.M;
+       row += (int64_t)gridDim.x * blockDim.x) {
+    float dk[KP];
+    int jk[KP];
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      dk[p] = __builtin_inff();
+      jk[p] = INT_MAX;
+    }
+    for (int c = 0; c < a.C; ++c) {
+      const float* q = a.part + ((int64_t)c * a.M + row) * (2 * KP);
+      for (int i = 0; i < KP; ++i) {
+        const float d = q[2 * i];
+        const int j = __float_as_int(q[2 * i + 1]);
+        if (!before(d, j, dk[KP - 1], jk[KP - 1])) break;   // each list is sorted
+#pragma unroll
+        for (int p = KP - 1; p > 0; --p) {
+          const bool shift = before(d, j, dk[p - 1], jk[p - 1]);
+          const bool here = !shift && before(d, j, dk[p], jk[p]);
+          dk[p] = shift ? dk[p - 1] : (here ? d : dk[p]);
+          jk[p] = shift ? jk[p - 1] : (here ? j : jk[p]);
+        }
+        if (before(d, j, dk[0], jk[0])) {
+          dk[0] = d;
+          jk[0] = j;
+        }
+      }
+    }
+    int* o = static_cast<int*>(a.out) + row * a.K;
+#pragma unroll
+    for (int p = 0; p < KP; ++p)
+      if (p < a.K) o[p] = jk[p];
+  }
+}
+
+unsigned grid_for(int64_t items) {
+  const int64_t b = (items + 255) / 256;
+  return (unsigned)std::max<int64_t>(1, std::min<int64_t>(b, 16384));
+}
+
+}  // namespace
+
+hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
+  if (a.M == 0) return hipSuccess;
+  if (a.KP > 0) {
+    const dim3 g(grid_for(a.M));
+    switch (a.KP) {
+      case 1: hipLaunchKernelGGL(combine_knn_kernel<1>, g, dim3(256), 0, s, a); break;
+      case 4: hipLaunchKernelGGL(combine_knn_kernel<4>, g, dim3(256), 0, s, a); break;
+      case 16: hipLaunchKernelGGL(combine_knn_kernel<16>, g, dim3(256), 0, s, a); break;
+      case 64: hipLaunchKernelGGL(combine_knn_kernel<64>, g, dim3(256), 0, s, a); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
+  switch (a.formula) {
+    case F_GRADX:
+      hipLaunchKernelGGL(combine_gradx_kernel, dim3(grid_for(a.M * (1 + a.D))), dim3(256), 0, s, a);
+      break;
+    case F_SINKHORN:
+      hipLaunchKernelGGL(combine_lse_kernel, dim3(grid_for(a.M)), dim3(256), 0, s, a);
+      break;
+    default:
+      hipLaunchKernelGGL(combine_sum_kernel, dim3(grid_for(a.M * a.EP)), dim3(256), 0, s, a);
+      break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace kred

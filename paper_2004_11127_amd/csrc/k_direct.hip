@@ -1,0 +1,571 @@
+// Direct-form reduction kernels for small D (D <= 16) on gfx950.
+//
+// The reduction of Eq. (2) (Sec. 2) over a symbolic M x N matrix: each lane
+// owns R rows x_i held in VGPRs and streams every y_j of its column block.
+// y_j is the same for every lane of the wave, so it is read with scalar loads
+// into SGPRs (no LDS, no barriers): each VALU instruction of the pair loop
+// takes y_j as its scalar operand.  The pair term is evaluated in the direct
+// form |x - y|^2 = sum_k (x_k - y_k)^2, which keeps full fp32 accuracy when
+// x is close to y (where the Gaussian is large); coordinates arrive
+// prescaled so that the kernel value is one v_exp_f32 (2^-d) with no extra
+// multiply.  Sums are two-level (a tile partial folded into the running
+// total every kTileJ columns) to keep fp32 rounding growth at
+// O(u (sqrt(T) + sqrt(N/T))) instead of O(u N).
+#include "kred_internal.h"
+
+#include <cfloat>
+#include <climits>
+
+namespace kred {
+namespace {
+
+constexpr int kTileJ = 256;
+constexpr float kRescale = 32.0f;   // log-sum-exp: rescale when a term exceeds 2^32 x reference
+
+__device__ __forceinline__ float fast_exp2(float v) { return __builtin_amdgcn_exp2f(v); }
+__device__ __forceinline__ float fast_sqrt(float v) { return __builtin_amdgcn_sqrtf(v); }
+__device__ __forceinline__ float fast_log2(float v) { return __builtin_amdgcn_logf(v); }
+
+// ------------------------------------------------------------------ prologue
+__global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
+  const int S = a.DP + a.EP;
+  const int64_t total = a.N * S;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t j = t / S;
+    const int s = (int)(t - j * S);
+    float v = 0.0f;
+    if (s < a.D) {
+      v = a.y[j * a.D + s] * a.yscale;
+    } else if (s >= a.DP) {
+      const int e = a.e0 + s - a.DP;
+      if (a.b != nullptr && e < a.E) v = a.b[j * a.E + e] * a.bscale;
+    }
+    a.ypk[t] = v;
+  }
+}
+
+__global__ __launch_bounds__(256) void fill_kernel(float* out, int64_t count, float value) {
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < count;
+       t += (int64_t)gridDim.x * blockDim.x)
+    out[t] = value;
+}
+
+// -------------------------------------------------------- common row set-up
+template <int DP, int R>
+__device__ __forceinline__ void load_rows(const DirectArgs& a, int64_t rb, float (&xr)[R][DP],
+                                          int64_t (&row)[R]) {
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    row[r] = rb * (int64_t)(kThreads * R) + r * kThreads + threadIdx.x;
+    const bool ok = row[r] < a.M;
+#pragma unroll
+    for (int k = 0; k < DP; ++k)
+      xr[r][k] = (ok && k < a.D) ? a.x[row[r] * a.D + k] * a.xscale : 0.0f;
+  }
+}
+
+template <int DP>
+__device__ __forceinline__ float sq_dist(const float (&xr)[DP], const float* yv) {
+  float t = xr[0] - yv[0];
+  float d = t * t;
+#pragma unroll
+  for (int k = 1; k < DP; ++k) {
+    t = xr[k] - yv[k];
+    d = __builtin_fmaf(t, t, d);
+  }
+  return d;
+}
+
+// ------------------------------------------------------- sum-type formulas
+// F = k(d) b_j with k = 2^-d (Gauss, prescaled), 2^-sqrt(d) (Laplace,
+// prescaled) or d (squared distance).
+template <int F>
+__device__ __forceinline__ float kernel_of(float d) {
+  if constexpr (F == F_GAUSS) return fast_exp2(-d);
+  else if constexpr (F == F_LAPLACE) return fast_exp2(-fast_sqrt(d));
+  else return d;
+}
+
+template <int F, int DP, int EP, int R>
+__global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
+  constexpr int S = DP + EP;
+  constexpr int U = S <= 4 ? 4 : (S <= 8 ? 2 : 1);
+  const int c = blockIdx.x % a.C;
+  const int64_t rb = blockIdx.x / a.C;
+  const int64_t j0 = c * a.jpb;
+  const int64_t j1 = min(a.N, j0 + a.jpb);
+
+  float xr[R][DP];
+  int64_t row[R];
+  load_rows<DP, R>(a, rb, xr, row);
+  float tot[R][EP];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int e = 0; e < EP; ++e) tot[r][e] = 0.0f;
+
+  for (int64_t jt = j0; jt < j1; jt += kTileJ) {
+    const int64_t je = min(j1, jt + kTileJ);
+    float part[R][EP];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int e = 0; e < EP; ++e) part[r][e] = 0.0f;
+    int64_t j = jt;
+    for (; j + U <= je; j += U) {
+      const float* __restrict__ yp = a.ypk + j * S;
+      float yv[U][S];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int s = 0; s < S; ++s) yv[u][s] = yp[u * S + s];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const float k = kernel_of<F>(sq_dist<DP>(xr[r], yv[u]));
+#pragma unroll
+          for (int e = 0; e < EP; ++e) part[r][e] = __builtin_fmaf(k, yv[u][DP + e], part[r][e]);
+        }
+    }
+    for (; j < je; ++j) {
+      const float* __restrict__ yp = a.ypk + j * S;
+      float yv[S];
+#pragma unroll
+      for (int s = 0; s < S; ++s) yv[s] = yp[s];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const float k = kernel_of<F>(sq_dist<DP>(xr[r], yv));
+#pragma unroll
+        for (int e = 0; e < EP; ++e) part[r][e] = __builtin_fmaf(k, yv[DP + e], part[r][e]);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int e = 0; e < EP; ++e) tot[r][e] += part[r][e];
+  }
+
+  const int Ec = min(EP, a.E - a.e0);
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (row[r] >= a.M) continue;
+    if (a.C == 1) {
+      float* o = static_cast<float*>(a.out) + row[r] * a.E + a.e0;
+#pragma unroll
+      for (int e = 0; e < EP; ++e)
+        if (e < Ec) o[e] = tot[r][e];
+    } else {
+      float* p = a.part + ((int64_t)c * a.M + row[r]) * EP;
+#pragma unroll
+      for (int e = 0; e < EP; ++e) p[e] = tot[r][e];
+    }
+  }
+}
+
+// ------------------------------------------- Gaussian sum + x-gradient
+// w = 2^-d' b_j,  a += w,  G_k += w (x'_k - y'_k);  gradient = -G * gscale.
+template <int DP, int R>
+__global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
+  constexpr int S = DP + 1;
+  constexpr int W = DP + 1;
+  constexpr int U = S <= 4 ? 4 : (S <= 8 ? 2 : 1);
+  const int c = blockIdx.x % a.C;
+  const int64_t rb = blockIdx.x / a.C;
+  const int64_t j0 = c * a.jpb;
+  const int64_t j1 = min(a.N, j0 + a.jpb);
+
+  float xr[R][DP];
+  int64_t row[R];
+  load_rows<DP, R>(a, rb, xr, row);
+  float tot[R][W];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int w = 0; w < W; ++w) tot[r][w] = 0.0f;
+
+  auto pair = [&](float (&part)[R][W], const float* yv) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      float t[DP];
+      float d = 0.0f;
+#pragma unroll
+      for (int k = 0; k < DP; ++k) {
+        t[k] = xr[r][k] - yv[k];
+        d = (k == 0) ? t[0] * t[0] : __builtin_fmaf(t[k], t[k], d);
+      }
+      const float w = fast_exp2(-d) * yv[DP];
+      part[r][0] += w;
+#pragma unroll
+      for (int k = 0; k < DP; ++k) part[r][1 + k] = __builtin_fmaf(w, t[k], part[r][1 + k]);
+    }
+  };
+
+  for (int64_t jt = j0; jt < j1; jt += kTileJ) {
+    const int64_t je = min(j1, jt + kTileJ);
+    float part[R][W];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int w = 0; w < W; ++w) part[r][w] = 0.0f;
+    int64_t j = jt;
+    for (; j + U <= je; j += U) {
+      const float* __restrict__ yp = a.ypk + j * S;
+      float yv[U][S];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int s = 0; s < S; ++s) yv[u][s] = yp[u * S + s];
+#pragma unroll
+      for (int u = 0; u < U; ++u) pair(part, yv[u]);
+    }
+    for (; j < je; ++j) {
+      const float* __restrict__ yp = a.ypk + j * S;
+      float yv[S];
+#pragma unroll
+      for (int s = 0; s < S; ++s) yv[s] = yp[s];
+      pair(part, yv);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int w = 0; w < W; ++w) tot[r][w] += part[r][w];
+  }
+
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (row[r] >= a.M) continue;
+    if (a.C == 1) {
+      float* o = static_cast<float*>(a.out) + row[r] * (1 + a.D);
+      o[0] = tot[r][0];
+#pragma unroll
+      for (int k = 0; k < DP; ++k)
+        if (k < a.D) o[1 + k] = -tot[r][1 + k] * a.gscale;
+    } else {
+      float* p = a.part + ((int64_t)c * a.M + row[r]) * W;
+#pragma unroll
+      for (int w = 0; w < W; ++w) p[w] = tot[r][w];
+    }
+  }
+}
+
+// ------------------------------------------------ Sinkhorn log-sum-exp
+// In log2 units: s_ij = g'_j - d'_ij with g' = g log2(e), d' = |x' - y'|^2.
+// Running reference m_i (<= max_j s_ij + kRescale): terms are 2^(s - m);
+// when a term would exceed 2^kRescale the sums are rescaled and m moves up.
+template <int DP, int R>
+__global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
+  constexpr int S = DP + 1;
+  constexpr int U = S <= 4 ? 4 : (S <= 8 ? 2 : 1);
+  const int c = blockIdx.x % a.C;
+  const int64_t rb = blockIdx.x / a.C;
+  const int64_t j0 = c * a.jpb;
+  const int64_t j1 = min(a.N, j0 + a.jpb);
+
+  float xr[R][DP];
+  int64_t row[R];
+  load_rows<DP, R>(a, rb, xr, row);
+  float m[R], tot[R], part[R];
+  {
+    // first column of the block sets the reference: term 2^0 = 1
+    const float* __restrict__ yp = a.ypk + j0 * S;
+    float yv[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) yv[s] = yp[s];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      m[r] = yv[DP] - sq_dist<DP>(xr[r], yv);
+      tot[r] = 0.0f;
+      part[r] = 1.0f;
+    }
+  }
+
+  auto pair = [&](const float* yv) {
+    float uu[R];
+    bool big = false;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      float u = yv[DP] - m[r];
+#pragma unroll
+      for (int k = 0; k < DP; ++k) {
+        const float t = xr[r][k] - yv[k];
+        u = __builtin_fmaf(-t, t, u);
+      }
+      uu[r] = u;
+      big |= (u > kRescale);
+    }
+    if (__builtin_expect(big, 0)) {
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        if (uu[r] > kRescale) {
+          const float f = fast_exp2(-uu[r]);
+          part[r] *= f;
+          tot[r] *= f;
+          m[r] += uu[r];
+          uu[r] = 0.0f;
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) part[r] += fast_exp2(uu[r]);
+  };
+
+  for (int64_t jt = j0 + 1; jt < j1; jt += kTileJ) {
+    const int64_t je = min(j1, jt + kTileJ);
+    int64_t j = jt;
+    for (; j + U <= je; j += U) {
+      const float* __restrict__ yp = a.ypk + j * S;
+      float yv[U][S];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int s = 0; s < S; ++s) yv[u][s] = yp[u * S + s];
+#pragma unroll
+      for (int u = 0; u < U; ++u) pair(yv[u]);
+    }
+    for (; j < je; ++j) {
+      const float* __restrict__ yp = a.ypk + j * S;
+      float yv[S];
+#pragma unroll
+      for (int s = 0; s < S; ++s) yv[s] = yp[s];
+      pair(yv);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      tot[r] += part[r];
+      part[r] = 0.0f;
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) tot[r] += part[r];
+
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (row[r] >= a.M) continue;
+    if (a.C == 1) {
+      static_cast<float*>(a.out)[row[r]] = (m[r] + fast_log2(tot[r])) * kLn2;
+    } else {
+      float* p = a.part + ((int64_t)c * a.M + row[r]) * 2;
+      p[0] = m[r];
+      p[1] = tot[r];
+    }
+  }
+}
+
+// ------------------------------------------------------------ arg-K-min
+// Per row a sorted register list of the KP smallest (d, j) seen; columns are
+// visited in increasing j, so a later equal distance never displaces an
+// earlier one: the strict compare d < list gives the (distance, index) order.
+template <int KP>
+__device__ __forceinline__ void knn_insert(float (&dk)[KP], int (&jk)[KP], float d, int j) {
+#pragma unroll
+  for (int p = KP - 1; p > 0; --p) {
+    const bool shift = d < dk[p - 1];
+    const bool here = !shift && d < dk[p];
+    dk[p] = shift ? dk[p - 1] : (here ? d : dk[p]);
+    jk[p] = shift ? jk[p - 1] : (here ? j : jk[p]);
+  }
+  if (d < dk[0]) {
+    dk[0] = d;
+    jk[0] = j;
+  }
+}
+
+template <int DP, int KP, int R>
+__global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
+  constexpr int S = DP + 1;   // the prologue pads one zero signal column
+  constexpr int U = S <= 4 ? 4 : (S <= 8 ? 2 : 1);
+  const int c = blockIdx.x % a.C;
+  const int64_t rb = blockIdx.x / a.C;
+  const int64_t j0 = c * a.jpb;
+  const int64_t j1 = min(a.N, j0 + a.jpb);
+
+  float xr[R][DP];
+  int64_t row[R];
+  load_rows<DP, R>(a, rb, xr, row);
+  float dk[R][KP];
+  int jk[R][KP];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      dk[r][p] = __builtin_inff();
+      jk[r][p] = INT_MAX;
+    }
+
+  auto pair = [&](const float* yv, int j) {
+    float d[R];
+    bool any = false;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      d[r] = sq_dist<DP>(xr[r], yv);
+      any |= d[r] < dk[r][KP - 1];
+    }
+    if (__builtin_expect(any, 0)) {
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        if (d[r] < dk[r][KP - 1]) knn_insert<KP>(dk[r], jk[r], d[r], j);
+    }
+  };
+
+  int64_t j = j0;
+  for (; j + U <= j1; j += U) {
+    const float* __restrict__ yp = a.ypk + j * S;
+    float yv[U][S];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int s = 0; s < S; ++s) yv[u][s] = yp[u * S + s];
+#pragma unroll
+    for (int u = 0; u < U; ++u) pair(yv[u], (int)(j + u));
+  }
+  for (; j < j1; ++j) {
+    const float* __restrict__ yp = a.ypk + j * S;
+    float yv[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) yv[s] = yp[s];
+    pair(yv, (int)j);
+  }
+
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (row[r] >= a.M) continue;
+    if (a.C == 1) {
+      int* o = static_cast<int*>(a.out) + row[r] * a.K;
+#pragma unroll
+      for (int p = 0; p < KP; ++p)
+        if (p < a.K) o[p] = jk[r][p];
+    } else {
+      float* q = a.part + ((int64_t)c * a.M + row[r]) * (2 * KP);
+#pragma unroll
+      for (int p = 0; p < KP; ++p) {
+        q[2 * p] = dk[r][p];
+        q[2 * p + 1] = __int_as_float(jk[r][p]);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------- dispatch
+constexpr int kStateBudget = 48;   // VGPRs of per-row state a lane may hold
+
+constexpr int pow2_floor(int v) { return v >= 8 ? 8 : v >= 4 ? 4 : v >= 2 ? 2 : 1; }
+
+constexpr int rows_for(int formula, int DP, int EP, int KP) {
+  const int state = formula == F_GRADX      ? DP + 2 * (DP + 1)
+                    : formula == F_SINKHORN ? DP + 3
+                    : KP > 0                ? DP + 2 * KP
+                                            : DP + 2 * EP;
+  return pow2_floor(kStateBudget / state > 0 ? kStateBudget / state : 1);
+}
+
+template <int DP, int EP>
+hipError_t launch_sum_e(const DirectArgs& a, dim3 grid, hipStream_t s) {
+  switch (a.formula) {
+    case F_GAUSS:
+      hipLaunchKernelGGL((sum_kernel<F_GAUSS, DP, EP, rows_for(F_GAUSS, DP, EP, 0)>), grid,
+                         dim3(kThreads), 0, s, a);
+      break;
+    case F_LAPLACE:
+      hipLaunchKernelGGL((sum_kernel<F_LAPLACE, DP, EP, rows_for(F_LAPLACE, DP, EP, 0)>), grid,
+                         dim3(kThreads), 0, s, a);
+      break;
+    case F_SQDIST:
+      hipLaunchKernelGGL((sum_kernel<F_SQDIST, DP, EP, rows_for(F_SQDIST, DP, EP, 0)>), grid,
+                         dim3(kThreads), 0, s, a);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int DP>
+hipError_t launch_dp(const DirectArgs& a, dim3 grid, hipStream_t s) {
+  if (a.KP > 0) {
+    switch (a.KP) {
+#define KRED_KNN(KPV)                                                                           \
+  case KPV:                                                                                    \
+    hipLaunchKernelGGL((knn_kernel<DP, KPV, rows_for(F_SQDIST, DP, 1, KPV)>), grid,           \
+                       dim3(kThreads), 0, s, a);                                               \
+    return hipGetLastError();
+      KRED_KNN(1) KRED_KNN(4) KRED_KNN(16) KRED_KNN(64)
+#undef KRED_KNN
+      default:
+        return hipErrorInvalidValue;
+    }
+  }
+  switch (a.formula) {
+    case F_GRADX:
+      hipLaunchKernelGGL((gradx_kernel<DP, rows_for(F_GRADX, DP, 1, 0)>), grid, dim3(kThreads),
+                         0, s, a);
+      return hipGetLastError();
+    case F_SINKHORN:
+      hipLaunchKernelGGL((lse_kernel<DP, rows_for(F_SINKHORN, DP, 1, 0)>), grid, dim3(kThreads),
+                         0, s, a);
+      return hipGetLastError();
+    default:
+      switch (a.EP) {
+        case 1: return launch_sum_e<DP, 1>(a, grid, s);
+        case 4: return launch_sum_e<DP, 4>(a, grid, s);
+        case 16: return launch_sum_e<DP, 16>(a, grid, s);
+        default: return hipErrorInvalidValue;
+      }
+  }
+}
+
+}  // namespace
+
+int direct_pad_d(int D) {
+  if (D >= 1 && D <= 4) return D;
+  if (D <= 8) return 8;
+  if (D <= 16) return 16;
+  return 0;
+}
+
+int direct_pad_e(int E) { return E <= 1 ? 1 : (E <= 4 ? 4 : 16); }
+
+int knn_pad_k(int K) { return K <= 1 ? 1 : (K <= 4 ? 4 : (K <= 16 ? 16 : 64)); }
+
+int direct_rows_per_thread(int formula, int DP, int EP, int KP) {
+  return rows_for(formula, DP, EP, KP);
+}
+
+int partial_width(int formula, int DP, int EP, int KP) {
+  if (KP > 0) return 2 * KP;
+  if (formula == F_GRADX) return DP + 1;
+  if (formula == F_SINKHORN) return 2;
+  return EP;
+}
+
+hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
+  const int64_t total = a.N * (a.DP + a.EP);
+  if (total == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s) {
+  if (count == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((count + 255) / 256, 8192);
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)blocks), dim3(256), 0, s, out, count, value);
+  return hipGetLastError();
+}
+
+hipError_t launch_direct(const DirectArgs& a, hipStream_t s) {
+  const int R = direct_rows_per_thread(a.formula, a.DP, a.EP, a.KP);
+  const int64_t rb = (a.M + (int64_t)kThreads * R - 1) / ((int64_t)kThreads * R);
+  const dim3 grid((unsigned)(rb * a.C));
+  switch (a.DP) {
+    case 1: return launch_dp<1>(a, grid, s);
+    case 2: return launch_dp<2>(a, grid, s);
+    case 3: return launch_dp<3>(a, grid, s);
+    case 4: return launch_dp<4>(a, grid, s);
+    case 8: return launch_dp<8>(a, grid, s);
+    case 16: return launch_dp<16>(a, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace kred

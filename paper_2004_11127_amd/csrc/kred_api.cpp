@@ -1,0 +1,378 @@
+// kred host runtime: argument checks, context and scratch memory, path
+// selection and kernel launches for the C ABI declared in include/kred.h.
+#include "kred.h"
+#include "kred_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <vector>
+
+using namespace kred;
+
+struct kred_ctx {
+  int device = 0;
+  int num_cus = 256;
+  void* scratch = nullptr;
+  size_t scratch_bytes = 0;
+  // KRED_FLAG_PROFILE: event pairs around main kernels, reused across collects
+  std::vector<hipEvent_t> ev;
+  size_t ev_used = 0;
+  const char* last_kernel = "none";
+};
+
+namespace {
+
+constexpr int kMaxDirectD = 16;
+constexpr int64_t kAlign = 256;
+
+inline int64_t align_up(int64_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
+
+bool misaligned(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 3u); }
+
+// Everything a call needs, derived from validated arguments.
+struct Plan {
+  int formula, reduction;
+  int D, DP, E, KP, K;
+  int64_t M, N;
+  int C;          // column blocks
+  int64_t jpb;    // j per column block
+  int S_max;      // widest packed row over the E-slices
+  int W_max;      // widest partial row
+  int64_t pack_bytes, part_bytes;
+  float xscale, bscale, gscale;
+};
+
+// Column split: enough (row block, column block) work items to keep every
+// CU busy, each long enough to amortise its set-up.
+int choose_col_blocks(int64_t row_blocks, int64_t N, int num_cus, int requested) {
+  const int64_t max_c = std::max<int64_t>(1, std::min<int64_t>(KRED_MAX_COL_BLOCKS, N));
+  if (requested > 0) return (int)std::min<int64_t>(requested, max_c);
+  const int64_t target_items = (int64_t)num_cus * 16;
+  int64_t c = (target_items + row_blocks - 1) / row_blocks;
+  c = std::min<int64_t>(c, std::max<int64_t>(1, N / 128));   // >= ~128 columns per item
+  if (c >= 8) c = (c + 7) / 8 * 8;                              // equal share per XCD
+  return (int)std::max<int64_t>(1, std::min<int64_t>(c, max_c));
+}
+
+bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M, int64_t N,
+               int32_t D, int32_t E, int num_cus, Plan* pl) {
+  Plan q{};
+  q.formula = (int)f;
+  q.reduction = (int)r;
+  q.M = M;
+  q.N = N;
+  q.D = D;
+  q.DP = direct_pad_d(D);
+  if (q.DP == 0) return false;   // large-D path not available for this pair
+  q.KP = 0;
+  q.K = 0;
+  q.E = E;
+  if (r == KRED_R_ARGKMIN) {
+    q.K = p->K;
+    q.KP = knn_pad_k(p->K);
+    q.E = 0;
+  }
+  if (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN) q.E = 1;
+  const int EP_first = (r == KRED_R_ARGKMIN) ? 1 : direct_pad_e(std::min(q.E, 16));
+  q.S_max = q.DP + EP_first;
+  q.W_max = partial_width(q.formula, q.DP, EP_first, q.KP);
+  const int R = direct_rows_per_thread(q.formula, q.DP, EP_first, q.KP);
+  const int64_t row_blocks = (M + (int64_t)kThreads * R - 1) / ((int64_t)kThreads * R);
+  q.C = choose_col_blocks(std::max<int64_t>(1, row_blocks), N, num_cus, p->col_blocks);
+  q.jpb = N > 0 ? (N + q.C - 1) / q.C : 0;
+  if (N > 0) q.C = (int)((N + q.jpb - 1) / q.jpb);   // no empty column block
+  q.pack_bytes = align_up(N * q.S_max * (int64_t)sizeof(float));
+  q.part_bytes = q.C > 1 ? align_up((int64_t)q.C * M * q.W_max * (int64_t)sizeof(float)) : 0;
+  // prescales: the kernels evaluate 2^(-|x' - y'|^2) etc. with x' = x * xscale
+  const double log2e = 1.4426950408889634;
+  q.bscale = 1.0f;
+  q.gscale = 0.0f;
+  switch (f) {
+    case KRED_F_GAUSS:
+    case KRED_F_GAUSS_GRADX: {
+      const double s = (double)p->sigma;
+      const double c = log2e / (2.0 * s * s);
+      q.xscale = (float)std::sqrt(c);
+      q.gscale = (float)(1.0 / (s * s * std::sqrt(c)));
+      break;
+    }
+    case KRED_F_LAPLACE:
+      q.xscale = (float)(log2e / (double)p->sigma);
+      break;
+    case KRED_F_SINKHORN:
+      q.xscale = (float)std::sqrt(log2e / (double)p->eps);
+      q.bscale = (float)log2e;
+      break;
+    default:
+      q.xscale = 1.0f;
+  }
+  *pl = q;
+  return true;
+}
+
+kred_status grow_scratch(kred_ctx* ctx, size_t bytes) {
+  if (bytes <= ctx->scratch_bytes) return KRED_OK;
+  const size_t want = std::max(bytes, ctx->scratch_bytes * 5 / 4);
+  if (ctx->scratch) {
+    if (hipDeviceSynchronize() != hipSuccess) return KRED_ERR_HIP;
+    (void)hipFree(ctx->scratch);
+    ctx->scratch = nullptr;
+    ctx->scratch_bytes = 0;
+  }
+  if (hipMalloc(&ctx->scratch, want) != hipSuccess) {
+    (void)hipGetLastError();
+    ctx->scratch = nullptr;
+    return KRED_ERR_NOMEM;
+  }
+  ctx->scratch_bytes = want;
+  return KRED_OK;
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) return;
+    ok = (prev == dev) || hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (ok && hipGetDevice(&cur) == hipSuccess && cur != prev && prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+hipEvent_t next_event(kred_ctx* ctx) {
+  if (ctx->ev_used == ctx->ev.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    ctx->ev.push_back(e);
+  }
+  return ctx->ev[ctx->ev_used++];
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* kred_strerror(kred_status s) {
+  switch (s) {
+    case KRED_OK: return "success";
+    case KRED_ERR_INVALID_ARG: return "invalid argument";
+    case KRED_ERR_UNSUPPORTED: return "unsupported formula/reduction/size combination";
+    case KRED_ERR_NOMEM: return "out of device memory for scratch";
+    case KRED_ERR_HIP: return "HIP runtime error";
+    case KRED_ERR_NO_DEVICE: return "no usable gfx950 device";
+  }
+  return "unknown status";
+}
+
+int32_t kred_version(void) { return KRED_VERSION; }
+
+kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p, int64_t M,
+                          int64_t N, int32_t D, int32_t E, const void* x, const void* y,
+                          const void* b, const void* out) {
+  if (p == nullptr) return KRED_ERR_INVALID_ARG;
+  if ((int)f < KRED_F_GAUSS || (int)f > KRED_F_SINKHORN) return KRED_ERR_INVALID_ARG;
+  if ((int)r < KRED_R_SUM || (int)r > KRED_R_ARGKMIN) return KRED_ERR_INVALID_ARG;
+  if (M < 0 || N < 0 || M > INT32_MAX || N > INT32_MAX) return KRED_ERR_INVALID_ARG;
+  if (D < 1 || D > KRED_MAX_D) return KRED_ERR_INVALID_ARG;
+  if (p->col_blocks < 0 || p->col_blocks > KRED_MAX_COL_BLOCKS) return KRED_ERR_INVALID_ARG;
+  bool needs_b = true;
+  if (r == KRED_R_SUM && (f == KRED_F_GAUSS || f == KRED_F_LAPLACE || f == KRED_F_SQDIST)) {
+    if (E < 1 || E > KRED_MAX_E) return KRED_ERR_INVALID_ARG;
+    if (f != KRED_F_SQDIST && !finite_pos(p->sigma)) return KRED_ERR_INVALID_ARG;
+  } else if (r == KRED_R_SUM && f == KRED_F_GAUSS_GRADX) {
+    if (E != 1) return KRED_ERR_INVALID_ARG;
+    if (!finite_pos(p->sigma)) return KRED_ERR_INVALID_ARG;
+  } else if (r == KRED_R_LSE && f == KRED_F_SINKHORN) {
+    if (E != 1) return KRED_ERR_INVALID_ARG;
+    if (!finite_pos(p->eps)) return KRED_ERR_INVALID_ARG;
+  } else if (r == KRED_R_ARGKMIN && f == KRED_F_SQDIST) {
+    if (b != nullptr) return KRED_ERR_INVALID_ARG;
+    if (p->K < 1 || p->K > KRED_MAX_K || p->K > N) return KRED_ERR_INVALID_ARG;
+    needs_b = false;
+  } else {
+    return KRED_ERR_UNSUPPORTED;
+  }
+  // Paths: the direct-form kernels cover D <= 16 for every pair.
+  if (D > kMaxDirectD) return KRED_ERR_UNSUPPORTED;
+  if (M == 0) return KRED_OK;
+  if (x == nullptr || out == nullptr) return KRED_ERR_INVALID_ARG;
+  if (N > 0 && (y == nullptr || (needs_b && b == nullptr))) return KRED_ERR_INVALID_ARG;
+  if (misaligned(x) || misaligned(y) || misaligned(b) || misaligned(out))
+    return KRED_ERR_INVALID_ARG;
+  return KRED_OK;
+}
+
+int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* p, int64_t M,
+                           int64_t N, int32_t D, int32_t E) {
+  const float dummy = 0.0f;
+  const void* bp = (r == KRED_R_ARGKMIN) ? nullptr : &dummy;
+  if (kred_validate(f, r, p, M, N, D, E, &dummy, &dummy, bp, &dummy) != KRED_OK) return -1;
+  if (M == 0 || N == 0) return 0;
+  Plan pl;
+  if (!make_plan(f, r, p, M, N, D, E, 256, &pl)) return -1;
+  return pl.pack_bytes + pl.part_bytes;
+}
+
+kred_status kred_create(kred_ctx** ctx, int device) {
+  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
+  *ctx = nullptr;
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n) {
+    (void)hipGetLastError();
+    return KRED_ERR_NO_DEVICE;
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, device) != hipSuccess) return KRED_ERR_NO_DEVICE;
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) return KRED_ERR_NO_DEVICE;
+  kred_ctx* c = new (std::nothrow) kred_ctx();
+  if (c == nullptr) return KRED_ERR_NOMEM;
+  c->device = device;
+  c->num_cus = prop.multiProcessorCount;
+  *ctx = c;
+  return KRED_OK;
+}
+
+kred_status kred_destroy(kred_ctx* ctx) {
+  if (ctx == nullptr) return KRED_OK;
+  kred_status st = KRED_OK;
+  {
+    DeviceGuard g(ctx->device);
+    if (hipDeviceSynchronize() != hipSuccess) st = KRED_ERR_HIP;
+    if (ctx->scratch) (void)hipFree(ctx->scratch);
+    for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
+  }
+  delete ctx;
+  return st;
+}
+
+kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
+                     int64_t M, int64_t N, int32_t D, int32_t E, const float* x, const float* y,
+                     const float* b, void* out, void* stream) {
+  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
+  const kred_status v = kred_validate(f, r, p, M, N, D, E, x, y, b, out);
+  if (v != KRED_OK) return v;
+  if (M == 0) return KRED_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  DeviceGuard guard(ctx->device);
+  if (!guard.ok) return KRED_ERR_HIP;
+
+  if (N == 0) {
+    int64_t count = M;
+    float value = 0.0f;
+    if (f == KRED_F_GAUSS_GRADX) count = M * (1 + D);
+    else if (r == KRED_R_SUM) count = M * E;
+    else if (r == KRED_R_LSE) value = -INFINITY;
+    return launch_fill(static_cast<float*>(out), count, value, s) == hipSuccess ? KRED_OK
+                                                                                : KRED_ERR_HIP;
+  }
+
+  Plan pl;
+  if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &pl)) return KRED_ERR_UNSUPPORTED;
+  const kred_status gs = grow_scratch(ctx, (size_t)(pl.pack_bytes + pl.part_bytes));
+  if (gs != KRED_OK) return gs;
+  float* ypk = static_cast<float*>(ctx->scratch);
+  float* part = pl.part_bytes ? reinterpret_cast<float*>(static_cast<char*>(ctx->scratch) +
+                                                         pl.pack_bytes)
+                              : nullptr;
+  const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
+
+  const int n_slices = (r == KRED_R_ARGKMIN) ? 1 : (pl.E + 15) / 16;
+  for (int sl = 0; sl < n_slices; ++sl) {
+    const int e0 = sl * 16;
+    const int EP = (r == KRED_R_ARGKMIN) ? 1 : direct_pad_e(std::min(16, pl.E - e0));
+    PackArgs pa{};
+    pa.y = y;
+    pa.b = (r == KRED_R_ARGKMIN) ? nullptr : b;
+    pa.ypk = ypk;
+    pa.N = N;
+    pa.D = D;
+    pa.DP = pl.DP;
+    pa.E = pl.E;
+    pa.EP = EP;
+    pa.e0 = e0;
+    pa.yscale = pl.xscale;
+    pa.bscale = pl.bscale;
+    if (launch_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
+
+    DirectArgs da{};
+    da.formula = (int)f;
+    da.D = D;
+    da.DP = pl.DP;
+    da.E = pl.E;
+    da.EP = EP;
+    da.e0 = e0;
+    da.M = M;
+    da.N = N;
+    da.C = pl.C;
+    da.jpb = pl.jpb;
+    da.x = x;
+    da.ypk = ypk;
+    da.xscale = pl.xscale;
+    da.gscale = pl.gscale;
+    da.out = out;
+    da.part = part;
+    da.KP = pl.KP;
+    da.K = pl.K;
+    hipEvent_t e_start = nullptr, e_stop = nullptr;
+    if (prof) {
+      e_start = next_event(ctx);
+      e_stop = next_event(ctx);
+      if (!e_start || !e_stop || hipEventRecord(e_start, s) != hipSuccess) return KRED_ERR_HIP;
+    }
+    if (launch_direct(da, s) != hipSuccess) return KRED_ERR_HIP;
+    if (prof) {
+      if (hipEventRecord(e_stop, s) != hipSuccess) return KRED_ERR_HIP;
+      ctx->last_kernel = (r == KRED_R_ARGKMIN)       ? "knn_kernel"
+                         : (f == KRED_F_GAUSS_GRADX) ? "gradx_kernel"
+                         : (f == KRED_F_SINKHORN)    ? "lse_kernel"
+                                                     : "sum_kernel";
+    }
+    if (pl.C > 1) {
+      CombineArgs ca{};
+      ca.formula = (int)f;
+      ca.D = D;
+      ca.DP = pl.DP;
+      ca.E = pl.E;
+      ca.EP = EP;
+      ca.e0 = e0;
+      ca.M = M;
+      ca.C = pl.C;
+      ca.part = part;
+      ca.out = out;
+      ca.gscale = pl.gscale;
+      ca.KP = pl.KP;
+      ca.K = pl.K;
+      if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
+    }
+  }
+  return KRED_OK;
+}
+
+kred_status kred_profile_collect(kred_ctx* ctx, int32_t* count, double* total_ms,
+                                 const char** kernel) {
+  if (ctx == nullptr || count == nullptr || total_ms == nullptr) return KRED_ERR_INVALID_ARG;
+  DeviceGuard guard(ctx->device);
+  double sum = 0.0;
+  for (size_t i = 0; i + 1 < ctx->ev_used; i += 2) {
+    if (hipEventSynchronize(ctx->ev[i + 1]) != hipSuccess) return KRED_ERR_HIP;
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, ctx->ev[i], ctx->ev[i + 1]) != hipSuccess) return KRED_ERR_HIP;
+    sum += ms;
+  }
+  *count = (int32_t)(ctx->ev_used / 2);
+  *total_ms = sum;
+  if (kernel) *kernel = ctx->last_kernel;
+  ctx->ev_used = 0;
+  return KRED_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,210 @@
+"""Python binding for libkred (ctypes): argument marshalling only.
+
+Every step of a reduction runs in the HIP kernels of libkred.so; this module
+turns torch tensors into device pointers and a HIP stream handle and calls the
+C ABI of include/kred.h.  torch provides device memory and streams only.
+There is no CPU fallback: without the built library, or with tensors that are
+not on a GPU, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libkred.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "kred.h")
+
+FORMULAS = {"gauss": 0, "laplace": 1, "sqdist": 2, "gauss_gradx": 3, "sinkhorn": 4}
+REDUCTIONS = {"sum": 0, "lse": 1, "argkmin": 2}
+STATUS = {0: "KRED_OK", 1: "KRED_ERR_INVALID_ARG", 2: "KRED_ERR_UNSUPPORTED", 3: "KRED_ERR_NOMEM",
+          4: "KRED_ERR_HIP", 5: "KRED_ERR_NO_DEVICE"}
+FLAG_PROFILE = 1
+MAX_D, MAX_E, MAX_K, MAX_COL_BLOCKS = 256, 64, 64, 256
+
+
+class KredError(RuntimeError):
+    def __init__(self, status, what=""):
+        self.status = status
+        super().__init__("%s%s (%s)" % (what + ": " if what else "", STATUS.get(status, status),
+                                        strerror(status) if _lib is not None else ""))
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("sigma", ctypes.c_float), ("eps", ctypes.c_float), ("K", ctypes.c_int32),
+                ("col_blocks", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+_lib = None
+
+
+def load():
+    """Load libkred.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise FileNotFoundError("libkred.so is not built; run `python -m paper_2004_11127_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        pp = ctypes.POINTER(Params)
+        lib.kred_create.argtypes = [ctypes.POINTER(vp), ctypes.c_int]
+        lib.kred_destroy.argtypes = [vp]
+        lib.kred_run.argtypes = [vp, ctypes.c_int, ctypes.c_int, pp, i64, i64, i32, i32,
+                                 vp, vp, vp, vp, vp]
+        lib.kred_validate.argtypes = [ctypes.c_int, ctypes.c_int, pp, i64, i64, i32, i32,
+                                      vp, vp, vp, vp]
+        lib.kred_scratch_bytes.argtypes = [ctypes.c_int, ctypes.c_int, pp, i64, i64, i32, i32]
+        lib.kred_scratch_bytes.restype = i64
+        lib.kred_profile_collect.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double),
+                                             ctypes.POINTER(ctypes.c_char_p)]
+        lib.kred_strerror.argtypes = [ctypes.c_int]
+        lib.kred_strerror.restype = ctypes.c_char_p
+        lib.kred_version.restype = i32
+        for f in (lib.kred_create, lib.kred_destroy, lib.kred_run, lib.kred_validate,
+                  lib.kred_profile_collect):
+            f.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def header_symbols():
+    """Names of the functions include/kred.h declares."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(kred_[a-z_]+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def strerror(status):
+    return load().kred_strerror(int(status)).decode()
+
+
+def version():
+    return load().kred_version()
+
+
+def make_params(sigma=1.0, eps=1.0, K=0, col_blocks=0, flags=0):
+    return Params(float(sigma), float(eps), int(K), int(col_blocks), int(flags))
+
+
+def _codes(formula, reduction):
+    f = FORMULAS[formula] if isinstance(formula, str) else int(formula)
+    r = REDUCTIONS[reduction] if isinstance(reduction, str) else int(reduction)
+    return f, r
+
+
+def validate(formula, reduction, M, N, D, E, x=16, y=16, b=16, out=16, **params):
+    """Host-only argument check (no GPU needed).
+
+    Pointers are plain integers here and are checked only for null and alignment.
+    """
+    f, r = _codes(formula, reduction)
+    p = make_params(**params)
+    return load().kred_validate(f, r, ctypes.byref(p), int(M), int(N), int(D), int(E),
+                                x, y, b, out)
+
+
+def scratch_bytes(formula, reduction, M, N, D, E, **params):
+    f, r = _codes(formula, reduction)
+    p = make_params(**params)
+    return load().kred_scratch_bytes(f, r, ctypes.byref(p), int(M), int(N), int(D), int(E))
+
+
+def output_shape(formula, reduction, M, D, E, K=0):
+    f, r = _codes(formula, reduction)
+    if r == REDUCTIONS["argkmin"]:
+        return (M, K)
+    if f == FORMULAS["gauss_gradx"]:
+        return (M, 1 + D)
+    if r == REDUCTIONS["lse"]:
+        return (M, 1)
+    return (M, E)
+
+
+class Context:
+    """A kred context on one GPU (owns the library's scratch memory)."""
+
+    def __init__(self, device=0):
+        import torch
+        if not torch.cuda.is_available():
+            raise RuntimeError("kred needs a GPU: torch.cuda.is_available() is False")
+        self.device = int(device)
+        h = ctypes.c_void_p()
+        st = load().kred_create(ctypes.byref(h), self.device)
+        if st != 0:
+            raise KredError(st, "kred_create")
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            load().kred_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    @staticmethod
+    def _dev_ptr(t, name, dtype):
+        import torch
+        if t is None:
+            return None
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            raise TypeError("%s must be a GPU torch tensor" % name)
+        if t.dtype != dtype or not t.is_contiguous():
+            raise TypeError("%s must be a contiguous %s tensor" % (name, dtype))
+        return t.data_ptr() if t.numel() else None
+
+    def run(self, formula, reduction, x, y, b=None, out=None, sigma=1.0, eps=1.0, K=0,
+            col_blocks=0, flags=0, stream=None):
+        """Evaluate the reduction; returns `out` (allocated when None).
+
+        x: (M, D) float32, y: (N, D) float32, b: (N, E) float32 or None (arg-K-min),
+        all contiguous on the context's GPU.  The call is asynchronous on `stream`
+        (a torch.cuda.Stream; default the current stream).
+        """
+        import torch
+        f, r = _codes(formula, reduction)
+        M, D = x.shape
+        N = y.shape[0]
+        if y.dim() != 2 or y.shape[1] != D:
+            raise ValueError("y must be (N, D) with the same D as x")
+        E = 0 if b is None else (b.shape[1] if b.dim() == 2 else 1)
+        if b is not None and b.shape[0] != N:
+            raise ValueError("b must have N rows")
+        shape = output_shape(f, r, M, D, E, K)
+        odt = torch.int32 if r == REDUCTIONS["argkmin"] else torch.float32
+        if out is None:
+            out = torch.empty(shape, dtype=odt, device=x.device)
+        elif tuple(out.shape) != shape:
+            raise ValueError("out must have shape %s" % (shape,))
+        p = make_params(sigma, eps, K, col_blocks, flags)
+        s = (stream if stream is not None else torch.cuda.current_stream(x.device)).cuda_stream
+        st = load().kred_run(self._h, f, r, ctypes.byref(p), M, N, D, E,
+                             self._dev_ptr(x, "x", torch.float32),
+                             self._dev_ptr(y, "y", torch.float32),
+                             self._dev_ptr(b, "b", torch.float32),
+                             self._dev_ptr(out, "out", odt), s)
+        if st != 0:
+            raise KredError(st, "kred_run(%s, %s, M=%d, N=%d, D=%d, E=%d)" % (formula, reduction,
+                                                                             M, N, D, E))
+        return out
+
+    def profile_collect(self):
+        """(count, total_ms, kernel) of main kernels timed since the last collect."""
+        n = ctypes.c_int32()
+        ms = ctypes.c_double()
+        name = ctypes.c_char_p()
+        st = load().kred_profile_collect(self._h, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(name))
+        if st != 0:
+            raise KredError(st, "kred_profile_collect")
+        return n.value, ms.value, name.value.decode() if name.value else ""

@@ -1,0 +1,122 @@
+"""The C ABI on the host (no GPU needed): the library loads, exports every symbol
+include/kred.h declares, and rejects bad arguments before touching a device."""
+import ctypes
+
+import pytest
+
+from paper_2004_11127_amd import kred
+
+OK, INVALID, UNSUPPORTED, NO_DEVICE = 0, 1, 2, 5
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return kred.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = kred.header_symbols()
+    assert set(names) >= {"kred_create", "kred_destroy", "kred_run", "kred_validate",
+                          "kred_scratch_bytes", "kred_profile_collect", "kred_strerror",
+                          "kred_version"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_strerror(lib):
+    assert kred.version() == 1
+    for code in range(6):
+        assert kred.strerror(code)
+    assert kred.strerror(0) == "success"
+    assert kred.strerror(999) == "unknown status"
+
+
+def test_create_rejects_bad_device(lib):
+    h = ctypes.c_void_p()
+    assert lib.kred_create(ctypes.byref(h), 4096) == NO_DEVICE
+    assert lib.kred_create(None, 0) == INVALID
+    assert lib.kred_destroy(None) == OK
+
+
+def test_run_rejects_null_context(lib):
+    p = kred.make_params(sigma=1.0)
+    assert lib.kred_run(None, 0, 0, ctypes.byref(p), 4, 4, 3, 1, 16, 16, 16, 16, None) == INVALID
+
+
+V = kred.validate
+
+
+@pytest.mark.parametrize("formula,reduction,E,kw", [
+    ("gauss", "sum", 1, dict(sigma=0.1)), ("gauss", "sum", 64, dict(sigma=2.0)),
+    ("laplace", "sum", 3, dict(sigma=1.0)), ("sqdist", "sum", 7, {}),
+    ("gauss_gradx", "sum", 1, dict(sigma=0.05)), ("sinkhorn", "lse", 1, dict(eps=0.01)),
+])
+def test_valid_pairs(lib, formula, reduction, E, kw):
+    assert V(formula, reduction, 100, 200, 3, E, **kw) == OK
+
+
+def test_valid_argkmin(lib):
+    assert V("sqdist", "argkmin", 100, 200, 3, 0, b=None, K=10) == OK
+    assert V("sqdist", "argkmin", 100, 64, 16, 0, b=None, K=64) == OK
+
+
+@pytest.mark.parametrize("formula,reduction", [
+    ("gauss", "lse"), ("gauss", "argkmin"), ("laplace", "argkmin"), ("sinkhorn", "sum"),
+    ("gauss_gradx", "lse"), ("sqdist", "lse")])
+def test_unsupported_pairs(lib, formula, reduction):
+    b = None if reduction == "argkmin" else 1
+    assert V(formula, reduction, 10, 10, 3, 1, b=b, K=1, sigma=1.0, eps=1.0) == UNSUPPORTED
+
+
+def test_invalid_arguments(lib):
+    g = dict(sigma=1.0)
+    assert V("gauss", "sum", -1, 10, 3, 1, **g) == INVALID          # M < 0
+    assert V("gauss", "sum", 10, -1, 3, 1, **g) == INVALID          # N < 0
+    assert V("gauss", "sum", 2**31, 10, 3, 1, **g) == INVALID       # M too large
+    assert V("gauss", "sum", 10, 10, 0, 1, **g) == INVALID          # D < 1
+    assert V("gauss", "sum", 10, 10, 257, 1, **g) == INVALID        # D > 256
+    assert V("gauss", "sum", 10, 10, 3, 0, **g) == INVALID          # E < 1
+    assert V("gauss", "sum", 10, 10, 3, 65, **g) == INVALID         # E > 64
+    assert V("gauss", "sum", 10, 10, 3, 1, sigma=0.0) == INVALID    # sigma <= 0
+    assert V("gauss", "sum", 10, 10, 3, 1, sigma=float("nan")) == INVALID
+    assert V("laplace", "sum", 10, 10, 3, 1, sigma=-1.0) == INVALID
+    assert V("gauss_gradx", "sum", 10, 10, 3, 2, **g) == INVALID    # gradient needs E = 1
+    assert V("sinkhorn", "lse", 10, 10, 3, 1, eps=0.0) == INVALID
+    assert V("sinkhorn", "lse", 10, 10, 3, 1, eps=float("inf")) == INVALID
+    assert V("sinkhorn", "lse", 10, 10, 3, 2, eps=1.0) == INVALID
+    assert V("sqdist", "argkmin", 10, 10, 3, 0, b=None, K=0) == INVALID
+    assert V("sqdist", "argkmin", 10, 10, 3, 0, b=None, K=11) == INVALID   # K > N
+    assert V("sqdist", "argkmin", 10, 100, 3, 0, b=None, K=65) == INVALID  # K > 64
+    assert V("sqdist", "argkmin", 10, 10, 3, 0, b=16, K=3) == INVALID      # b must be NULL
+    assert V("gauss", "sum", 10, 10, 3, 1, col_blocks=-1, **g) == INVALID
+    assert V("gauss", "sum", 10, 10, 3, 1, col_blocks=257, **g) == INVALID
+    assert V(7, "sum", 10, 10, 3, 1, **g) == INVALID                       # unknown formula
+    assert V("gauss", 9, 10, 10, 3, 1, **g) == INVALID                     # unknown reduction
+
+
+def test_pointer_rules(lib):
+    g = dict(sigma=1.0)
+    assert V("gauss", "sum", 10, 10, 3, 1, x=None, **g) == INVALID
+    assert V("gauss", "sum", 10, 10, 3, 1, out=None, **g) == INVALID
+    assert V("gauss", "sum", 10, 10, 3, 1, y=None, **g) == INVALID
+    assert V("gauss", "sum", 10, 10, 3, 1, b=None, **g) == INVALID
+    assert V("gauss", "sum", 10, 10, 3, 1, x=18, **g) == INVALID             # misaligned
+    assert V("gauss", "sum", 10, 0, 3, 1, y=None, b=None, **g) == OK         # N = 0 needs no y, b
+    assert V("gauss", "sum", 0, 10, 3, 1, x=None, y=None, b=None, out=None, **g) == OK  # M = 0
+
+
+def test_unsupported_sizes_are_reported(lib):
+    # pairs the library has no kernel for at this D report UNSUPPORTED, not a crash
+    st = V("gauss_gradx", "sum", 10, 10, 200, 1, sigma=1.0)
+    assert st in (OK, UNSUPPORTED)
+
+
+def test_scratch_is_linear_not_quadratic(lib):
+    # No M x N buffer: scratch grows linearly in M and N (Sec. 2 linear memory footprint).
+    s1 = kred.scratch_bytes("gauss", "sum", 100_000, 100_000, 3, 1, sigma=0.1)
+    s2 = kred.scratch_bytes("gauss", "sum", 1_000_000, 1_000_000, 3, 1, sigma=0.1)
+    assert 0 < s1 and 0 < s2
+    assert s2 < 40 * s1                       # 10x the points, far less than 100x the bytes
+    assert s2 < 1_000_000 * 1_000_000 * 4 / 1000
+    assert kred.scratch_bytes("gauss", "sum", 10, 10, 3, 0, sigma=0.1) == -1
+    assert kred.scratch_bytes("gauss", "sum", 0, 10, 3, 1, sigma=0.1) == 0

@@ -1,0 +1,232 @@
+"""GPU parity: libkred against the fp64 oracle, element by element, through the C ABI.
+
+Small ragged shapes that span several row blocks, column tiles and a ragged
+tail, every (formula, reduction) pair, forced column splits (second pass),
+edge cases (M = 0, N = 0, single rows and columns), determinism and stream use.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import LSE_TOL, SUM_TOL, dev, host, lse_err, norm_err, true_dists
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    import torch
+    from paper_2004_11127_amd import kred
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    with kred.Context(0) as c:
+        yield c
+
+
+def _pts(rng, n, D, scale=1.0):
+    return (rng.uniform(0.0, 1.0, (n, D)) * scale).astype(np.float32)
+
+
+SUM_CASES = [
+    # formula, M, N, D, E, sigma, col_blocks
+    ("gauss", 1, 1, 3, 1, 0.3, 0),
+    ("gauss", 7, 63, 3, 1, 0.3, 0),
+    ("gauss", 65, 257, 3, 1, 0.2, 1),
+    ("gauss", 1000, 4099, 3, 1, 0.1, 0),
+    ("gauss", 4099, 1000, 3, 1, 0.1, 7),
+    ("gauss", 2049, 1031, 1, 1, 0.05, 2),
+    ("gauss", 513, 777, 2, 3, 0.1, 64),
+    ("gauss", 300, 1500, 4, 16, 0.2, 0),
+    ("gauss", 300, 1500, 5, 17, 0.3, 3),
+    ("gauss", 129, 999, 8, 40, 0.4, 1),
+    ("gauss", 257, 700, 16, 2, 0.6, 0),
+    ("gauss", 100, 333, 9, 64, 0.5, 5),
+    ("laplace", 1000, 4099, 3, 1, 0.1, 0),
+    ("laplace", 77, 500, 7, 4, 0.3, 7),
+    ("laplace", 3000, 200, 16, 1, 0.5, 1),
+    ("sqdist", 1000, 4099, 3, 1, 1.0, 0),
+    ("sqdist", 333, 1234, 12, 5, 1.0, 2),
+    ("sqdist", 65, 64, 1, 16, 1.0, 64),
+]
+
+
+@pytest.mark.parametrize("formula,M,N,D,E,sigma,C", SUM_CASES)
+def test_sum_parity(ctx, formula, M, N, D, E, sigma, C):
+    rng = np.random.default_rng(M * 7 + N * 3 + D + E)
+    x = _pts(rng, M, D); y = _pts(rng, N, D)
+    b = rng.standard_normal((N, E)).astype(np.float32)
+    out = host(ctx.run(formula, "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C))
+    ref, norm = oracle.kernel_sum(formula, x, y, b, sigma=sigma)
+    assert out.shape == (M, E)
+    assert norm_err(out, ref, norm) <= SUM_TOL
+
+
+GRADX_CASES = [
+    (1, 1, 3, 0.3, 0), (7, 63, 3, 0.2, 0), (1000, 4099, 3, 0.1, 0), (4099, 1000, 3, 0.05, 7),
+    (2049, 517, 1, 0.05, 2), (300, 999, 2, 0.1, 64), (257, 1200, 5, 0.3, 1), (129, 700, 16, 0.6, 3),
+]
+
+
+@pytest.mark.parametrize("M,N,D,sigma,C", GRADX_CASES)
+def test_gradx_parity(ctx, M, N, D, sigma, C):
+    rng = np.random.default_rng(M + 11 * N + D)
+    x = _pts(rng, M, D); y = _pts(rng, N, D)
+    b = rng.standard_normal((N, 1)).astype(np.float32)
+    out = host(ctx.run("gauss_gradx", "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C))
+    ref, norm = oracle.gauss_gradx(x, y, b, sigma)
+    assert out.shape == (M, 1 + D)
+    assert norm_err(out, ref, norm) <= SUM_TOL
+
+
+LSE_CASES = [
+    (1, 1, 3, 0.1, 0), (7, 63, 3, 0.05, 0), (1000, 4099, 3, 0.01, 0), (4099, 1000, 3, 0.01, 7),
+    (2049, 777, 1, 0.001, 2), (300, 1500, 2, 0.02, 64), (257, 999, 6, 0.1, 1), (65, 640, 16, 0.5, 3),
+]
+
+
+@pytest.mark.parametrize("M,N,D,eps,C", LSE_CASES)
+def test_lse_parity(ctx, M, N, D, eps, C):
+    rng = np.random.default_rng(M + 5 * N + D)
+    x = _pts(rng, M, D); y = _pts(rng, N, D)
+    y[:, 0] += 0.3
+    g = rng.standard_normal((N, 1)).astype(np.float32)
+    out = host(ctx.run("sinkhorn", "lse", dev(x), dev(y), dev(g), eps=eps, col_blocks=C))
+    ref, m = oracle.sinkhorn_lse(x, y, g, eps)
+    assert out.shape == (M, 1)
+    assert lse_err(out[:, 0], ref, m) <= LSE_TOL
+
+
+def test_lse_far_rows_and_large_offsets(ctx):
+    # rows far from every column (all terms tiny) and a large shift of g: the
+    # running maximum must keep every row finite and accurate
+    rng = np.random.default_rng(3)
+    x = _pts(rng, 500, 3, 4.0); y = _pts(rng, 2000, 3)
+    g = (rng.standard_normal((2000, 1)) - 40.0).astype(np.float32)
+    out = host(ctx.run("sinkhorn", "lse", dev(x), dev(y), dev(g), eps=0.05))
+    ref, m = oracle.sinkhorn_lse(x, y, g, 0.05)
+    assert np.all(np.isfinite(out))
+    assert lse_err(out[:, 0], ref, m) <= LSE_TOL
+
+
+def _int_pts(rng, n, D, lo=-3, hi=3):
+    return rng.integers(lo, hi + 1, (n, D)).astype(np.float32)
+
+
+KNN_CASES = [
+    # M, N, D, K, col_blocks
+    (1, 1, 3, 1, 0), (7, 63, 3, 4, 0), (1000, 4099, 3, 10, 0), (4099, 1000, 2, 16, 7),
+    (513, 2000, 8, 1, 2), (300, 999, 5, 32, 64), (129, 700, 16, 64, 3), (65, 64, 4, 64, 1),
+    (2000, 3000, 3, 3, 0),
+]
+
+
+@pytest.mark.parametrize("M,N,D,K,C", KNN_CASES)
+def test_argkmin_integer_bit_exact(ctx, M, N, D, K, C):
+    # integer coordinates in a small box: many equal distances, exact in fp32
+    rng = np.random.default_rng(M + 3 * N + D + K)
+    x = _int_pts(rng, M, D); y = _int_pts(rng, N, D)
+    out = host(ctx.run("sqdist", "argkmin", dev(x), dev(y), None, K=K, col_blocks=C))
+    ref, _ = oracle.argkmin(x, y, K)
+    assert out.dtype == np.int32 and out.shape == (M, K)
+    np.testing.assert_array_equal(out, ref)
+
+
+def test_argkmin_float_coordinates(ctx):
+    # non-integer data: fp32 rounding may reorder near-ties, so compare the
+    # selected distances (fp64) with the oracle's and check validity
+    rng = np.random.default_rng(17)
+    x = _pts(rng, 700, 3); y = _pts(rng, 3001, 3)
+    K = 10
+    out = host(ctx.run("sqdist", "argkmin", dev(x), dev(y), None, K=K))
+    ref_idx, ref_d = oracle.argkmin(x, y, K)
+    got_d = true_dists(x, y, np.arange(700), out)
+    np.testing.assert_allclose(got_d, ref_d, rtol=1e-5, atol=1e-9)
+    assert np.all((out >= 0) & (out < 3001))
+    assert all(len(set(r)) == K for r in out.tolist())
+    assert (out == ref_idx).mean() > 0.99
+
+
+# ----------------------------------------------------------------- edge cases
+
+def test_empty_m_is_noop(ctx):
+    import torch
+    x = torch.empty((0, 3), device="cuda"); y = dev(np.ones((5, 3), np.float32))
+    b = dev(np.ones((5, 1), np.float32))
+    out = ctx.run("gauss", "sum", x, y, b, sigma=1.0)
+    assert out.shape == (0, 1)
+
+
+def test_empty_n_gives_identity_of_the_reduction(ctx):
+    import torch
+    x = dev(np.ones((9, 3), np.float32)); y = torch.empty((0, 3), device="cuda")
+    b = torch.empty((0, 2), device="cuda")
+    out = host(ctx.run("gauss", "sum", x, y, b, sigma=1.0))
+    assert out.shape == (9, 2) and not out.any()
+    g = host(ctx.run("gauss_gradx", "sum", x, y, torch.empty((0, 1), device="cuda"), sigma=1.0))
+    assert g.shape == (9, 4) and not g.any()
+    l = host(ctx.run("sinkhorn", "lse", x, y, torch.empty((0, 1), device="cuda"), eps=1.0))
+    assert np.all(np.isneginf(l))
+
+
+def test_errors_raise_and_leave_output(ctx):
+    import torch
+    from paper_2004_11127_amd import kred
+    x = dev(np.ones((4, 3), np.float32)); y = dev(np.ones((4, 3), np.float32))
+    out = torch.full((4, 5), 7.0, device="cuda")
+    with pytest.raises(kred.KredError):
+        ctx.run("sqdist", "argkmin", x, y, None, K=5, out=torch.zeros((4, 5), dtype=torch.int32,
+                                                                         device="cuda"))
+    with pytest.raises(kred.KredError):
+        ctx.run("gauss", "sum", x, y, dev(np.ones((4, 5), np.float32)), out=out, sigma=-1.0)
+    assert torch.all(out == 7.0)
+
+
+def test_deterministic_and_split_invariant(ctx):
+    rng = np.random.default_rng(21)
+    x = _pts(rng, 3000, 3); y = _pts(rng, 5000, 3)
+    b = rng.standard_normal((5000, 1)).astype(np.float32)
+    xd, yd, bd = dev(x), dev(y), dev(b)
+    a1 = host(ctx.run("gauss", "sum", xd, yd, bd, sigma=0.1))
+    a2 = host(ctx.run("gauss", "sum", xd, yd, bd, sigma=0.1))
+    np.testing.assert_array_equal(a1, a2)
+    ref, norm = oracle.kernel_sum("gauss", x, y, b, sigma=0.1)
+    for C in (1, 3, 16, 200):
+        aC = host(ctx.run("gauss", "sum", xd, yd, bd, sigma=0.1, col_blocks=C))
+        assert norm_err(aC, ref, norm) <= SUM_TOL
+
+
+def test_joint_permutation_of_columns(ctx):
+    rng = np.random.default_rng(22)
+    x = _pts(rng, 500, 3); y = _pts(rng, 2000, 3)
+    b = rng.standard_normal((2000, 2)).astype(np.float32)
+    p = rng.permutation(2000)
+    a = host(ctx.run("gauss", "sum", dev(x), dev(y), dev(b), sigma=0.2))
+    ap = host(ctx.run("gauss", "sum", dev(x), dev(y[p]), dev(b[p]), sigma=0.2))
+    _, norm = oracle.kernel_sum("gauss", x, y, b, sigma=0.2)
+    assert norm_err(ap, a.astype(np.float64), norm) <= 2 * SUM_TOL
+
+
+def test_runs_on_a_side_stream(ctx):
+    import torch
+    rng = np.random.default_rng(23)
+    x = _pts(rng, 1000, 3); y = _pts(rng, 1000, 3)
+    b = rng.standard_normal((1000, 1)).astype(np.float32)
+    xd, yd, bd = dev(x), dev(y), dev(b)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        out = ctx.run("gauss", "sum", xd, yd, bd, sigma=0.1, stream=s)
+    s.synchronize()
+    ref, norm = oracle.kernel_sum("gauss", x, y, b, sigma=0.1)
+    assert norm_err(host(out), ref, norm) <= SUM_TOL
+
+
+def test_profile_collect_counts_launches(ctx):
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(24)
+    x = dev(_pts(rng, 2000, 3)); y = dev(_pts(rng, 2000, 3))
+    b = dev(rng.standard_normal((2000, 1)).astype(np.float32))
+    ctx.profile_collect()
+    for _ in range(3):
+        ctx.run("gauss", "sum", x, y, b, sigma=0.1, flags=kred.FLAG_PROFILE)
+    n, ms, name = ctx.profile_collect()
+    assert n == 3 and ms > 0 and name == "sum_kernel"
