@@ -65,11 +65,17 @@ def _load():
             lib.oracle_argkmin.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                            ctypes.c_int, _dp, _dp, _i64p, ctypes.c_int64,
                                            _i64p, _dp]
+            lib.oracle_num_threads.restype = ctypes.c_int
             for f in (lib.oracle_kernel_sum, lib.oracle_gauss_gradx, lib.oracle_sinkhorn_lse,
                       lib.oracle_argkmin):
                 f.restype = ctypes.c_int
             _lib = lib
     return _lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle routines run on."""
+    return int(_load().oracle_num_threads())
 
 
 def _f64(a, ncols=None):

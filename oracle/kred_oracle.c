@@ -35,6 +35,7 @@
 #include <math.h>
 #include <stdint.h>
 #include <stddef.h>
+#include <omp.h>
 
 #define ORACLE_GAUSS 0
 #define ORACLE_LAPLACE 1
@@ -202,4 +203,15 @@ int oracle_argkmin(int64_t M, int64_t N, int D, int K,
   }
   (void)M;
   return 0;
+}
+
+/* Number of OpenMP threads the routines above use. */
+int oracle_num_threads(void) {
+  int n = 1;
+#pragma omp parallel
+  {
+#pragma omp single
+    n = omp_get_num_threads();
+  }
+  return n;
 }

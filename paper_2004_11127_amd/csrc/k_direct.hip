@@ -1,16 +1,20 @@
 // Direct-form reduction kernels for small D (D <= 16) on gfx950.
 //
-// The reduction of Eq. (2) (Sec. 2) over a symbolic M x N matrix: each lane
-// owns R rows x_i held in VGPRs and streams every y_j of its column block.
-// y_j is the same for every lane of the wave, so it is read with scalar loads
-// into SGPRs (no LDS, no barriers): each VALU instruction of the pair loop
-// takes y_j as its scalar operand.  The pair term is evaluated in the direct
-// form |x - y|^2 = sum_k (x_k - y_k)^2, which keeps full fp32 accuracy when
-// x is close to y (where the Gaussian is large); coordinates arrive
-// prescaled so that the kernel value is one v_exp_f32 (2^-d) with no extra
-// multiply.  Sums are two-level (a tile partial folded into the running
-// total every kTileJ columns) to keep fp32 rounding growth at
-// O(u (sqrt(T) + sqrt(N/T))) instead of O(u N).
+// The reduction of Eq. (2) (Sec. 2) over a symbolic M x N matrix that is
+// never stored.  Each lane owns R rows x_i held in VGPRs.  The workgroup
+// streams its column block of packed (y_j, b_j) rows through a double-
+// buffered LDS tile: coalesced global loads of tile t+1 are in flight while
+// the pair loop runs on tile t, and every lane reads y_j with one broadcast
+// LDS load into VGPRs.  Keeping every pair-loop operand in VGPRs matters on
+// gfx950: an FP32 VALU instruction whose sources are all VGPRs issues in about
+// half the cycles of one that takes a scalar (SGPR) operand.
+//
+// The pair term uses the direct form |x - y|^2 = sum_k (x_k - y_k)^2, which
+// keeps full fp32 accuracy where x is close to y (where the Gaussian is
+// large).  Coordinates arrive prescaled so that the kernel value is a single
+// v_exp_f32 (2^-d) with no extra multiply.  Sums are two-level (a per-tile
+// partial folded into the running total once per tile), which keeps fp32
+// rounding growth near u (sqrt(T) + sqrt(N / T)) instead of u N.
 #include "kred_internal.h"
 
 #include <cfloat>
@@ -19,8 +23,7 @@
 namespace kred {
 namespace {
 
-constexpr int kTileJ = 256;
-constexpr float kRescale = 32.0f;   // log-sum-exp: rescale when a term exceeds 2^32 x reference
+constexpr float kRescale = 32.0f;   // log-sum-exp: rescale once a term exceeds 2^32 x reference
 
 __device__ __forceinline__ float fast_exp2(float v) { return __builtin_amdgcn_exp2f(v); }
 __device__ __forceinline__ float fast_sqrt(float v) { return __builtin_amdgcn_sqrtf(v); }
@@ -51,6 +54,94 @@ __global__ __launch_bounds__(256) void fill_kernel(float* out, int64_t count, fl
     out[t] = value;
 }
 
+// ------------------------------------------------------ LDS tile streaming
+// Packed rows have S floats; in LDS each row is padded to SP (a multiple of
+// 4) so that one row is read with SP/4 aligned 16-byte broadcast loads.
+template <int S>
+struct Tile {
+  static constexpr int SP = (S + 3) / 4 * 4;
+  static constexpr int TJ = SP <= 4 ? 256 : (SP <= 8 ? 128 : 64);   // rows per tile
+  static constexpr int LOADS = (TJ * S + kThreads - 1) / kThreads;   // floats per thread per tile
+  static constexpr int U = SP <= 8 ? 4 : 2;                          // j unroll
+};
+
+// Walk columns [j0, j1) of ypk through LDS; call pair(yv, j) for each column
+// (yv: the SP floats of row j, in VGPRs), skipping the first `skip` columns,
+// and tile_end() after each tile.  All threads of the block must call this.
+template <int S, typename PairFn, typename TileEndFn>
+__device__ __forceinline__ void stream_columns(const float* __restrict__ ypk, int64_t j0,
+                                               int64_t j1, int skip, float4* lds, PairFn&& pair,
+                                               TileEndFn&& tile_end) {
+  using T = Tile<S>;
+  constexpr int SP = T::SP, TJ = T::TJ, U = T::U;
+  constexpr int ROW4 = SP / 4;
+  const int tid = threadIdx.x;
+  float* ldsf = reinterpret_cast<float*>(lds);
+  const int64_t ntiles = (j1 - j0 + TJ - 1) / TJ;
+  float stage[T::LOADS];
+
+  auto fetch = [&](int64_t t) {
+    const int64_t jt = j0 + t * TJ;
+    const int nf = (int)(min((int64_t)TJ, j1 - jt)) * S;
+    const float* src = ypk + jt * S;
+#pragma unroll
+    for (int q = 0; q < T::LOADS; ++q) {
+      const int i = tid + q * kThreads;
+      stage[q] = (i < nf) ? src[i] : 0.0f;
+    }
+  };
+  auto put = [&](int64_t t) {
+    float* dst = ldsf + (t & 1) * (TJ * SP);
+#pragma unroll
+    for (int q = 0; q < T::LOADS; ++q) {
+      const int i = tid + q * kThreads;
+      if (i < TJ * S) dst[(i / S) * SP + (i % S)] = stage[q];
+    }
+  };
+
+  if (ntiles <= 0) return;
+  fetch(0);
+  put(0);
+  __syncthreads();
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int64_t jt = j0 + t * TJ;
+    const int n = (int)min((int64_t)TJ, j1 - jt);
+    if (t + 1 < ntiles) fetch(t + 1);
+    const float4* buf = lds + (t & 1) * (TJ * ROW4);
+    int jj = (t == 0) ? skip : 0;
+    for (; jj + U <= n; jj += U) {
+      float yv[U][SP];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int q = 0; q < ROW4; ++q) {
+          const float4 v = buf[(jj + u) * ROW4 + q];
+          yv[u][4 * q + 0] = v.x;
+          yv[u][4 * q + 1] = v.y;
+          yv[u][4 * q + 2] = v.z;
+          yv[u][4 * q + 3] = v.w;
+        }
+#pragma unroll
+      for (int u = 0; u < U; ++u) pair(yv[u], jt + jj + u);
+    }
+    for (; jj < n; ++jj) {
+      float yv[SP];
+#pragma unroll
+      for (int q = 0; q < ROW4; ++q) {
+        const float4 v = buf[jj * ROW4 + q];
+        yv[4 * q + 0] = v.x;
+        yv[4 * q + 1] = v.y;
+        yv[4 * q + 2] = v.z;
+        yv[4 * q + 3] = v.w;
+      }
+      pair(yv, jt + jj);
+    }
+    tile_end();
+    if (t + 1 < ntiles) put(t + 1);
+    __syncthreads();
+  }
+}
+
 // -------------------------------------------------------- common row set-up
 template <int DP, int R>
 __device__ __forceinline__ void load_rows(const DirectArgs& a, int64_t rb, float (&xr)[R][DP],
@@ -77,6 +168,22 @@ __device__ __forceinline__ float sq_dist(const float (&xr)[DP], const float* yv)
   return d;
 }
 
+// Work item of a block: row block rb and column block c (consecutive blocks
+// take consecutive column blocks, so with C a multiple of 8 each XCD streams
+// its own share of the columns through its L2).
+struct Item {
+  int c;
+  int64_t rb, j0, j1;
+};
+__device__ __forceinline__ Item item_of(const DirectArgs& a) {
+  Item it;
+  it.c = blockIdx.x % a.C;
+  it.rb = blockIdx.x / a.C;
+  it.j0 = (int64_t)it.c * a.jpb;
+  it.j1 = min(a.N, it.j0 + a.jpb);
+  return it;
+}
+
 // ------------------------------------------------------- sum-type formulas
 // F = k(d) b_j with k = 2^-d (Gauss, prescaled), 2^-sqrt(d) (Laplace,
 // prescaled) or d (squared distance).
@@ -90,62 +197,36 @@ __device__ __forceinline__ float kernel_of(float d) {
 template <int F, int DP, int EP, int R>
 __global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
   constexpr int S = DP + EP;
-  constexpr int U = S <= 4 ? 4 : (S <= 8 ? 2 : 1);
-  const int c = blockIdx.x % a.C;
-  const int64_t rb = blockIdx.x / a.C;
-  const int64_t j0 = c * a.jpb;
-  const int64_t j1 = min(a.N, j0 + a.jpb);
-
+  __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  const Item it = item_of(a);
   float xr[R][DP];
   int64_t row[R];
-  load_rows<DP, R>(a, rb, xr, row);
-  float tot[R][EP];
+  load_rows<DP, R>(a, it.rb, xr, row);
+  float tot[R][EP], part[R][EP];
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
-    for (int e = 0; e < EP; ++e) tot[r][e] = 0.0f;
+    for (int e = 0; e < EP; ++e) tot[r][e] = part[r][e] = 0.0f;
 
-  for (int64_t jt = j0; jt < j1; jt += kTileJ) {
-    const int64_t je = min(j1, jt + kTileJ);
-    float part[R][EP];
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-      for (int e = 0; e < EP; ++e) part[r][e] = 0.0f;
-    int64_t j = jt;
-    for (; j + U <= je; j += U) {
-      const float* __restrict__ yp = a.ypk + j * S;
-      float yv[U][S];
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int s = 0; s < S; ++s) yv[u][s] = yp[u * S + s];
-#pragma unroll
-      for (int u = 0; u < U; ++u)
+  stream_columns<S>(
+      a.ypk, it.j0, it.j1, 0, lds,
+      [&](const float* yv, int64_t) {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-          const float k = kernel_of<F>(sq_dist<DP>(xr[r], yv[u]));
+          const float k = kernel_of<F>(sq_dist<DP>(xr[r], yv));
 #pragma unroll
-          for (int e = 0; e < EP; ++e) part[r][e] = __builtin_fmaf(k, yv[u][DP + e], part[r][e]);
+          for (int e = 0; e < EP; ++e) part[r][e] = __builtin_fmaf(k, yv[DP + e], part[r][e]);
         }
-    }
-    for (; j < je; ++j) {
-      const float* __restrict__ yp = a.ypk + j * S;
-      float yv[S];
+      },
+      [&]() {
 #pragma unroll
-      for (int s = 0; s < S; ++s) yv[s] = yp[s];
+        for (int r = 0; r < R; ++r)
 #pragma unroll
-      for (int r = 0; r < R; ++r) {
-        const float k = kernel_of<F>(sq_dist<DP>(xr[r], yv));
-#pragma unroll
-        for (int e = 0; e < EP; ++e) part[r][e] = __builtin_fmaf(k, yv[DP + e], part[r][e]);
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-      for (int e = 0; e < EP; ++e) tot[r][e] += part[r][e];
-  }
+          for (int e = 0; e < EP; ++e) {
+            tot[r][e] += part[r][e];
+            part[r][e] = 0.0f;
+          }
+      });
 
   const int Ec = min(EP, a.E - a.e0);
 #pragma unroll
@@ -157,7 +238,7 @@ __global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
       for (int e = 0; e < EP; ++e)
         if (e < Ec) o[e] = tot[r][e];
     } else {
-      float* p = a.part + ((int64_t)c * a.M + row[r]) * EP;
+      float* p = a.part + ((int64_t)it.c * a.M + row[r]) * EP;
 #pragma unroll
       for (int e = 0; e < EP; ++e) p[e] = tot[r][e];
     }
@@ -170,68 +251,44 @@ template <int DP, int R>
 __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   constexpr int W = DP + 1;
-  constexpr int U = S <= 4 ? 4 : (S <= 8 ? 2 : 1);
-  const int c = blockIdx.x % a.C;
-  const int64_t rb = blockIdx.x / a.C;
-  const int64_t j0 = c * a.jpb;
-  const int64_t j1 = min(a.N, j0 + a.jpb);
-
+  __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  const Item it = item_of(a);
   float xr[R][DP];
   int64_t row[R];
-  load_rows<DP, R>(a, rb, xr, row);
-  float tot[R][W];
+  load_rows<DP, R>(a, it.rb, xr, row);
+  float tot[R][W], part[R][W];
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
-    for (int w = 0; w < W; ++w) tot[r][w] = 0.0f;
+    for (int w = 0; w < W; ++w) tot[r][w] = part[r][w] = 0.0f;
 
-  auto pair = [&](float (&part)[R][W], const float* yv) {
+  stream_columns<S>(
+      a.ypk, it.j0, it.j1, 0, lds,
+      [&](const float* yv, int64_t) {
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      float t[DP];
-      float d = 0.0f;
+        for (int r = 0; r < R; ++r) {
+          float t[DP];
+          float d = 0.0f;
 #pragma unroll
-      for (int k = 0; k < DP; ++k) {
-        t[k] = xr[r][k] - yv[k];
-        d = (k == 0) ? t[0] * t[0] : __builtin_fmaf(t[k], t[k], d);
-      }
-      const float w = fast_exp2(-d) * yv[DP];
-      part[r][0] += w;
+          for (int k = 0; k < DP; ++k) {
+            t[k] = xr[r][k] - yv[k];
+            d = (k == 0) ? t[0] * t[0] : __builtin_fmaf(t[k], t[k], d);
+          }
+          const float w = fast_exp2(-d) * yv[DP];
+          part[r][0] += w;
 #pragma unroll
-      for (int k = 0; k < DP; ++k) part[r][1 + k] = __builtin_fmaf(w, t[k], part[r][1 + k]);
-    }
-  };
-
-  for (int64_t jt = j0; jt < j1; jt += kTileJ) {
-    const int64_t je = min(j1, jt + kTileJ);
-    float part[R][W];
+          for (int k = 0; k < DP; ++k) part[r][1 + k] = __builtin_fmaf(w, t[k], part[r][1 + k]);
+        }
+      },
+      [&]() {
 #pragma unroll
-    for (int r = 0; r < R; ++r)
+        for (int r = 0; r < R; ++r)
 #pragma unroll
-      for (int w = 0; w < W; ++w) part[r][w] = 0.0f;
-    int64_t j = jt;
-    for (; j + U <= je; j += U) {
-      const float* __restrict__ yp = a.ypk + j * S;
-      float yv[U][S];
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int s = 0; s < S; ++s) yv[u][s] = yp[u * S + s];
-#pragma unroll
-      for (int u = 0; u < U; ++u) pair(part, yv[u]);
-    }
-    for (; j < je; ++j) {
-      const float* __restrict__ yp = a.ypk + j * S;
-      float yv[S];
-#pragma unroll
-      for (int s = 0; s < S; ++s) yv[s] = yp[s];
-      pair(part, yv);
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-      for (int w = 0; w < W; ++w) tot[r][w] += part[r][w];
-  }
+          for (int w = 0; w < W; ++w) {
+            tot[r][w] += part[r][w];
+            part[r][w] = 0.0f;
+          }
+      });
 
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -243,7 +300,7 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
       for (int k = 0; k < DP; ++k)
         if (k < a.D) o[1 + k] = -tot[r][1 + k] * a.gscale;
     } else {
-      float* p = a.part + ((int64_t)c * a.M + row[r]) * W;
+      float* p = a.part + ((int64_t)it.c * a.M + row[r]) * W;
 #pragma unroll
       for (int w = 0; w < W; ++w) p[w] = tot[r][w];
     }
@@ -257,22 +314,18 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
 template <int DP, int R>
 __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
-  constexpr int U = S <= 4 ? 4 : (S <= 8 ? 2 : 1);
-  const int c = blockIdx.x % a.C;
-  const int64_t rb = blockIdx.x / a.C;
-  const int64_t j0 = c * a.jpb;
-  const int64_t j1 = min(a.N, j0 + a.jpb);
-
+  __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  const Item it = item_of(a);
   float xr[R][DP];
   int64_t row[R];
-  load_rows<DP, R>(a, rb, xr, row);
+  load_rows<DP, R>(a, it.rb, xr, row);
   float m[R], tot[R], part[R];
   {
-    // first column of the block sets the reference: term 2^0 = 1
-    const float* __restrict__ yp = a.ypk + j0 * S;
+    // the block's first column sets the reference: its term is 2^0 = 1
+    const float* y0 = a.ypk + it.j0 * S;
     float yv[S];
 #pragma unroll
-    for (int s = 0; s < S; ++s) yv[s] = yp[s];
+    for (int s = 0; s < S; ++s) yv[s] = y0[s];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       m[r] = yv[DP] - sq_dist<DP>(xr[r], yv);
@@ -281,61 +334,43 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
     }
   }
 
-  auto pair = [&](const float* yv) {
-    float uu[R];
-    bool big = false;
+  stream_columns<S>(
+      a.ypk, it.j0, it.j1, 1, lds,
+      [&](const float* yv, int64_t) {
+        float uu[R];
+        bool big = false;
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      float u = yv[DP] - m[r];
+        for (int r = 0; r < R; ++r) {
+          float u = yv[DP] - m[r];
 #pragma unroll
-      for (int k = 0; k < DP; ++k) {
-        const float t = xr[r][k] - yv[k];
-        u = __builtin_fmaf(-t, t, u);
-      }
-      uu[r] = u;
-      big |= (u > kRescale);
-    }
-    if (__builtin_expect(big, 0)) {
-#pragma unroll
-      for (int r = 0; r < R; ++r)
-        if (uu[r] > kRescale) {
-          const float f = fast_exp2(-uu[r]);
-          part[r] *= f;
-          tot[r] *= f;
-          m[r] += uu[r];
-          uu[r] = 0.0f;
+          for (int k = 0; k < DP; ++k) {
+            const float t = xr[r][k] - yv[k];
+            u = __builtin_fmaf(-t, t, u);
+          }
+          uu[r] = u;
+          big |= (u > kRescale);
         }
-    }
+        if (__builtin_expect(big, 0)) {
 #pragma unroll
-    for (int r = 0; r < R; ++r) part[r] += fast_exp2(uu[r]);
-  };
-
-  for (int64_t jt = j0 + 1; jt < j1; jt += kTileJ) {
-    const int64_t je = min(j1, jt + kTileJ);
-    int64_t j = jt;
-    for (; j + U <= je; j += U) {
-      const float* __restrict__ yp = a.ypk + j * S;
-      float yv[U][S];
+          for (int r = 0; r < R; ++r)
+            if (uu[r] > kRescale) {
+              const float f = fast_exp2(-uu[r]);
+              part[r] *= f;
+              tot[r] *= f;
+              m[r] += uu[r];
+              uu[r] = 0.0f;
+            }
+        }
 #pragma unroll
-      for (int u = 0; u < U; ++u)
+        for (int r = 0; r < R; ++r) part[r] += fast_exp2(uu[r]);
+      },
+      [&]() {
 #pragma unroll
-        for (int s = 0; s < S; ++s) yv[u][s] = yp[u * S + s];
-#pragma unroll
-      for (int u = 0; u < U; ++u) pair(yv[u]);
-    }
-    for (; j < je; ++j) {
-      const float* __restrict__ yp = a.ypk + j * S;
-      float yv[S];
-#pragma unroll
-      for (int s = 0; s < S; ++s) yv[s] = yp[s];
-      pair(yv);
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      tot[r] += part[r];
-      part[r] = 0.0f;
-    }
-  }
+        for (int r = 0; r < R; ++r) {
+          tot[r] += part[r];
+          part[r] = 0.0f;
+        }
+      });
 #pragma unroll
   for (int r = 0; r < R; ++r) tot[r] += part[r];
 
@@ -345,7 +380,7 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
     if (a.C == 1) {
       static_cast<float*>(a.out)[row[r]] = (m[r] + fast_log2(tot[r])) * kLn2;
     } else {
-      float* p = a.part + ((int64_t)c * a.M + row[r]) * 2;
+      float* p = a.part + ((int64_t)it.c * a.M + row[r]) * 2;
       p[0] = m[r];
       p[1] = tot[r];
     }
@@ -374,15 +409,11 @@ __device__ __forceinline__ void knn_insert(float (&dk)[KP], int (&jk)[KP], float
 template <int DP, int KP, int R>
 __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
   constexpr int S = DP + 1;   // the prologue pads one zero signal column
-  constexpr int U = S <= 4 ? 4 : (S <= 8 ? 2 : 1);
-  const int c = blockIdx.x % a.C;
-  const int64_t rb = blockIdx.x / a.C;
-  const int64_t j0 = c * a.jpb;
-  const int64_t j1 = min(a.N, j0 + a.jpb);
-
+  __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  const Item it = item_of(a);
   float xr[R][DP];
   int64_t row[R];
-  load_rows<DP, R>(a, rb, xr, row);
+  load_rows<DP, R>(a, it.rb, xr, row);
   float dk[R][KP];
   int jk[R][KP];
 #pragma unroll
@@ -393,39 +424,23 @@ __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
       jk[r][p] = INT_MAX;
     }
 
-  auto pair = [&](const float* yv, int j) {
-    float d[R];
-    bool any = false;
+  stream_columns<S>(
+      a.ypk, it.j0, it.j1, 0, lds,
+      [&](const float* yv, int64_t j) {
+        float d[R];
+        bool any = false;
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      d[r] = sq_dist<DP>(xr[r], yv);
-      any |= d[r] < dk[r][KP - 1];
-    }
-    if (__builtin_expect(any, 0)) {
+        for (int r = 0; r < R; ++r) {
+          d[r] = sq_dist<DP>(xr[r], yv);
+          any |= d[r] < dk[r][KP - 1];
+        }
+        if (__builtin_expect(any, 0)) {
 #pragma unroll
-      for (int r = 0; r < R; ++r)
-        if (d[r] < dk[r][KP - 1]) knn_insert<KP>(dk[r], jk[r], d[r], j);
-    }
-  };
-
-  int64_t j = j0;
-  for (; j + U <= j1; j += U) {
-    const float* __restrict__ yp = a.ypk + j * S;
-    float yv[U][S];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int s = 0; s < S; ++s) yv[u][s] = yp[u * S + s];
-#pragma unroll
-    for (int u = 0; u < U; ++u) pair(yv[u], (int)(j + u));
-  }
-  for (; j < j1; ++j) {
-    const float* __restrict__ yp = a.ypk + j * S;
-    float yv[S];
-#pragma unroll
-    for (int s = 0; s < S; ++s) yv[s] = yp[s];
-    pair(yv, (int)j);
-  }
+          for (int r = 0; r < R; ++r)
+            if (d[r] < dk[r][KP - 1]) knn_insert<KP>(dk[r], jk[r], d[r], (int)j);
+        }
+      },
+      [&]() {});
 
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -436,7 +451,7 @@ __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
       for (int p = 0; p < KP; ++p)
         if (p < a.K) o[p] = jk[r][p];
     } else {
-      float* q = a.part + ((int64_t)c * a.M + row[r]) * (2 * KP);
+      float* q = a.part + ((int64_t)it.c * a.M + row[r]) * (2 * KP);
 #pragma unroll
       for (int p = 0; p < KP; ++p) {
         q[2 * p] = dk[r][p];
