@@ -1,0 +1,370 @@
+// Large-D reductions (16 < D <= 256) on the fp32 matrix cores of gfx950.
+//
+// For large D the pair term is dominated by the inner product <x_i, y_j>, a
+// genuine dense contraction.  Each wave owns RB blocks of 16 rows x_i and
+// streams the workgroup's column block through double-buffered LDS tiles.
+// Per 16 x 16 (column, row) block it computes, with v_mfma_f32_16x16x4_f32,
+//
+//     T[j][i] = sum_d Yop[j][d] X[i][d] + (ny_j + nx_i)
+//
+// where the prologue has packed Yop = 2 y' and ny = -|y'|^2 (sums) or
+// Yop = -2 y and ny = |y|^2 (arg-K-min), so that T = -|x' - y'|^2 in the
+// expanded form |x|^2 + |y|^2 - 2 <x, y> (prescaled coordinates, log2 units).
+//   * sums:  p = 2^T (Gauss), 2^-sqrt(-T) (Laplace) or -T (squared distance);
+//     the 16 x 16 tile p is already laid out as the A operand of the next
+//     v_mfma_f32_16x16x4_f32, so a = P . B accumulates on the matrix cores
+//     with no data movement;
+//   * arg-K-min: T = |y|^2 - 2 <x, y> ranks columns exactly like |x - y|^2
+//     for a fixed row; each lane keeps a sorted K-list over the columns it
+//     sees, and the second pass merges the lists.
+//
+// MFMA 16x16x4 f32 operand layout (lane l = 16 g + li, g = l / 16):
+//   A (16 x 4):  lane l supplies A[li][g];   B (4 x 16): lane l supplies B[g][li];
+//   D (16 x 16): lane l holds D[4 g + r][li] in register r = 0..3.
+// With A = Y rows (m = column j) and B = X rows (n = row i), the result lane
+// l holds T[j = 4 g + r][i = li], i.e. P[i = li][j = 4 g + r]: exactly the A
+// operand of the P . B product when its k index is j = 4 g + r.
+// The contraction index d is split by lane group: chunk q of lane group g
+// covers d = g Q + q, so each lane reads Q contiguous floats of a row.
+#include "kred_internal.h"
+
+#include <climits>
+
+namespace kred {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// ------------------------------------------------------------------ prologue
+__global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  // y operand and norms: one thread per column j (norm accumulated in fp32)
+  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < a.N16; j += stride) {
+    float nrm = 0.0f;
+    const bool ok = j < a.N;
+    for (int d = 0; d < a.DP; ++d) {
+      const float v = (ok && d < a.D) ? a.y[j * a.D + d] : 0.0f;
+      const float s = v * a.coord_scale;
+      nrm = __builtin_fmaf(s, s, nrm);
+      a.yop[j * a.DP + d] = v * a.yop_scale;
+    }
+    a.ny[j] = ok ? a.nrm_sign * nrm : a.pad_norm;
+  }
+  // signal tiles: b[j][e0 + e] stored at (j/16)*16W + ((j%16)/4)*4W + e*4 + j%4, W = 16*EB
+  if (a.bpk != nullptr) {
+    const int W = 16 * a.EB;
+    const int64_t total = a.N16 * W;
+    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total; t += stride) {
+      const int64_t j = t / W;
+      const int e = (int)(t - j * W);
+      const float v = (j < a.N && e < a.Ec) ? a.b[j * a.E + a.e0 + e] : 0.0f;
+      const int64_t blk = j / 16;
+      const int jr = (int)(j % 16);
+      a.bpk[blk * 16 * W + (jr / 4) * 4 * W + e * 4 + (jr % 4)] = v;
+    }
+  }
+}
+
+constexpr int tile_cols(int DP) {
+  // LDS budget per buffer: about 4608 floats of y rows (padded stride DP + 4)
+  return (4608 / (DP + 4)) >= 64 ? 64 : ((4608 / (DP + 4)) >= 32 ? 32 : 16);
+}
+
+template <int KP>
+__device__ __forceinline__ void list_insert(float (&dk)[KP], int (&jk)[KP], float d, int j) {
+#pragma unroll
+  for (int p = KP - 1; p > 0; --p) {
+    const bool shift = d < dk[p - 1];
+    const bool here = !shift && d < dk[p];
+    dk[p] = shift ? dk[p - 1] : (here ? d : dk[p]);
+    jk[p] = shift ? jk[p - 1] : (here ? j : jk[p]);
+  }
+  if (d < dk[0]) {
+    dk[0] = d;
+    jk[0] = j;
+  }
+}
+
+// EPI: 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min.
+template <int Q, int RB, int EPI, int EB, int KP>
+__global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
+  constexpr int DP = 4 * Q;
+  constexpr int LDY = DP + 4;
+  constexpr int TJ = tile_cols(DP);
+  constexpr bool SUM = EPI != 3;
+  constexpr int W = 16 * EB;                       // signal columns per row in a tile
+  constexpr int YF4 = TJ * DP / 4;                 // float4s of y per tile
+  constexpr int YL = (YF4 + 255) / 256;            // per thread
+  constexpr int BF4 = SUM ? TJ * W / 4 : 0;        // float4s of b per tile
+  constexpr int BL = SUM ? (BF4 + 255) / 256 : 0;
+  constexpr int KL = SUM ? 1 : KP;
+
+  __shared__ float4 ys[2][TJ * LDY / 4];
+  __shared__ float4 ns[2][TJ / 4];
+  __shared__ float4 bs[2][SUM ? TJ * W / 4 : 1];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int li = lane & 15, g = lane >> 4;
+  const int c = blockIdx.x % a.C;
+  const int64_t rbk = blockIdx.x / a.C;
+  const int64_t j0 = (int64_t)c * a.jpb;
+  const int64_t j1 = min(a.N16, j0 + a.jpb);
+  const int64_t i0 = rbk * (64 * RB) + wave * (16 * RB);
+
+  // rows: lane supplies X[i = li][d = g Q + q] of each of its RB row blocks
+  float xr[RB][Q];
+  float nx[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int64_t row = i0 + 16 * rb + li;
+    const bool ok = row < a.M;
+    float part = 0.0f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int d = g * Q + q;
+      const float v = (ok && d < a.D) ? a.x[row * a.D + d] * a.xscale : 0.0f;
+      xr[rb][q] = v;
+      part = __builtin_fmaf(v, v, part);
+    }
+    part += __shfl_xor(part, 16);
+    part += __shfl_xor(part, 32);
+    nx[rb] = SUM ? -part : 0.0f;
+  }
+
+  f4 oacc[RB][EB], tot[RB][EB];
+  float dk[RB][KL];
+  int jk[RB][KL];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int eb = 0; eb < EB; ++eb) oacc[rb][eb] = tot[rb][eb] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < KL; ++p) {
+      dk[rb][p] = __builtin_inff();
+      jk[rb][p] = INT_MAX;
+    }
+  }
+
+  float4 ystage[YL];
+  float4 bstage[BL > 0 ? BL : 1];
+  float4 nstage;
+  auto fetch = [&](int64_t jt) {
+    const int ncol = (int)min((int64_t)TJ, j1 - jt);
+    const float4* ysrc = reinterpret_cast<const float4*>(a.yop + jt * DP);
+#pragma unroll
+    for (int k = 0; k < YL; ++k) {
+      const int f = tid + k * 256;
+      ystage[k] = (f < YF4 && f < ncol * (DP / 4)) ? ysrc[f] : float4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (tid < TJ / 4)
+      nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
+                                : float4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (SUM) {
+      const float4* bsrc = reinterpret_cast<const float4*>(a.bpk + jt * W);
+#pragma unroll
+      for (int k = 0; k < BL; ++k) {
+        const int f = tid + k * 256;
+        bstage[k] = (f < BF4 && f < ncol * W / 4) ? bsrc[f] : float4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < YL; ++k) {
+      const int f = tid + k * 256;
+      if (f < YF4) {
+        const int row = f / (DP / 4), cq = f % (DP / 4);
+        ys[buf][row * (LDY / 4) + cq] = ystage[k];
+      }
+    }
+    if (tid < TJ / 4) ns[buf][tid] = nstage;
+    if constexpr (SUM) {
+#pragma unroll
+      for (int k = 0; k < BL; ++k) {
+        const int f = tid + k * 256;
+        if (f < BF4) bs[buf][f] = bstage[k];
+      }
+    }
+  };
+
+  const int64_t ntiles = (j1 - j0 + TJ - 1) / TJ;
+  if (ntiles > 0) {
+    fetch(j0);
+    put(0);
+  }
+  __syncthreads();
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int64_t jt = j0 + t * TJ;
+    const int buf = (int)(t & 1);
+    const int nblk = (int)(min((int64_t)TJ, j1 - jt) / 16);
+    if (t + 1 < ntiles) fetch(jt + TJ);
+    for (int blk = 0; blk < nblk; ++blk) {
+      float yo[Q];
+      const float4* yrow = &ys[buf][(blk * 16 + li) * (LDY / 4) + g * (Q / 4)];
+#pragma unroll
+      for (int qq = 0; qq < Q / 4; ++qq) {
+        const float4 v = yrow[qq];
+        yo[4 * qq + 0] = v.x;
+        yo[4 * qq + 1] = v.y;
+        yo[4 * qq + 2] = v.z;
+        yo[4 * qq + 3] = v.w;
+      }
+      const float4 nyv = ns[buf][blk * 4 + g];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        f4 acc = f4{nx[rb] + nyv.x, nx[rb] + nyv.y, nx[rb] + nyv.z, nx[rb] + nyv.w};
+#pragma unroll
+        for (int q = 0; q < Q; ++q) acc = mfma4(yo[q], xr[rb][q], acc);
+        if constexpr (SUM) {
+          f4 p;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if constexpr (EPI == 0) p[r] = __builtin_amdgcn_exp2f(acc[r]);
+            else if constexpr (EPI == 1) p[r] = __builtin_amdgcn_exp2f(-__builtin_amdgcn_sqrtf(fmaxf(-acc[r], 0.0f)));
+            else p[r] = fmaxf(-acc[r], 0.0f);
+          }
+#pragma unroll
+          for (int eb = 0; eb < EB; ++eb) {
+            // lane needs b[j = blk*16 + 4g + r][e = 16 eb + li] for r = 0..3
+            const float* bl = reinterpret_cast<const float*>(&bs[buf][0]) +
+                              blk * 16 * W + g * 4 * W + (16 * eb + li) * 4;
+            const float4 bv = *reinterpret_cast<const float4*>(bl);
+            oacc[rb][eb] = mfma4(p[0], bv.x, oacc[rb][eb]);
+            oacc[rb][eb] = mfma4(p[1], bv.y, oacc[rb][eb]);
+            oacc[rb][eb] = mfma4(p[2], bv.z, oacc[rb][eb]);
+            oacc[rb][eb] = mfma4(p[3], bv.w, oacc[rb][eb]);
+          }
+        } else {
+          const float kth = dk[rb][KL - 1];
+          const bool any = acc[0] < kth || acc[1] < kth || acc[2] < kth || acc[3] < kth;
+          if (__builtin_expect(any, 0)) {
+            const int jb = (int)(jt + blk * 16 + 4 * g);
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (acc[r] < dk[rb][KL - 1]) list_insert<KL>(dk[rb], jk[rb], acc[r], jb + r);
+          }
+        }
+      }
+    }
+    if constexpr (SUM) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int eb = 0; eb < EB; ++eb) {
+          tot[rb][eb] += oacc[rb][eb];
+          oacc[rb][eb] = f4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+    // buffer (t+1)&1 was last read in iteration t-1, which ended with a barrier
+    if (t + 1 < ntiles) put((int)((t + 1) & 1));
+    __syncthreads();
+  }
+
+  if constexpr (SUM) {
+    // D layout of the P . B product: lane holds out[i = 4 g + r][e = 16 eb + li]
+    const int Ec = min(W, a.E - a.e0);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int eb = 0; eb < EB; ++eb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t row = i0 + 16 * rb + 4 * g + r;
+          const int e = 16 * eb + li;
+          if (row >= a.M) continue;
+          if (a.C == 1) {
+            if (e < Ec) static_cast<float*>(a.out)[row * a.E + a.e0 + e] = tot[rb][eb][r];
+          } else {
+            a.part[((int64_t)c * a.M + row) * W + e] = tot[rb][eb][r];
+          }
+        }
+  } else {
+    // one partial list per (column block, lane group); the second pass merges them
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int64_t row = i0 + 16 * rb + li;
+      if (row >= a.M) continue;
+      float* q = a.part + (((int64_t)c * 4 + g) * a.M + row) * (2 * KL);
+#pragma unroll
+      for (int p = 0; p < KL; ++p) {
+        q[2 * p] = dk[rb][p];
+        q[2 * p + 1] = __int_as_float(jk[rb][p]);
+      }
+    }
+  }
+}
+
+template <int Q>
+constexpr int rows_blocks() { return Q >= 64 ? 1 : 2; }
+
+template <int Q, int EPI>
+hipError_t launch_sum_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
+  constexpr int RB = rows_blocks<Q>();
+  switch (a.EB) {
+    case 1: hipLaunchKernelGGL((mfma_kernel<Q, RB, EPI, 1, 1>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((mfma_kernel<Q, RB, EPI, 2, 1>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((mfma_kernel<Q, RB, EPI, 4, 1>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int Q>
+hipError_t launch_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
+  constexpr int RB = rows_blocks<Q>();
+  switch (a.epi) {
+    case 0: return launch_sum_q<Q, 0>(a, grid, s);
+    case 1: return launch_sum_q<Q, 1>(a, grid, s);
+    case 2: return launch_sum_q<Q, 2>(a, grid, s);
+    case 3:
+      switch (a.KP) {
+        case 1: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 1>), grid, dim3(256), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 4>), grid, dim3(256), 0, s, a); break;
+        case 16: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 16>), grid, dim3(256), 0, s, a); break;
+        case 64: hipLaunchKernelGGL((mfma_kernel<Q, 1, 3, 1, 64>), grid, dim3(256), 0, s, a); break;
+        default: return hipErrorInvalidValue;
+      }
+      return hipGetLastError();
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+int mfma_pad_d(int D) { return D <= 32 ? 32 : (D <= 64 ? 64 : (D <= 128 ? 128 : (D <= 256 ? 256 : 0))); }
+
+int mfma_tile_cols(int DP) { return tile_cols(DP); }
+
+int mfma_rows_per_block(int DP, int KP) {
+  const int Q = DP / 4;
+  return 64 * ((Q >= 64 || KP == 64) ? 1 : 2);
+}
+
+hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s) {
+  if (a.N16 == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((a.N16 * 16 * a.EB + 255) / 256, 8192);
+  hipLaunchKernelGGL(mfma_pack_kernel, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(256), 0,
+                     s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s) {
+  const int rows = mfma_rows_per_block(a.DP, a.KP);
+  const int64_t rb = (a.M + rows - 1) / rows;
+  const dim3 grid((unsigned)(rb * a.C));
+  switch (a.DP) {
+    case 32: return launch_q<8>(a, grid, s);
+    case 64: return launch_q<16>(a, grid, s);
+    case 128: return launch_q<32>(a, grid, s);
+    case 256: return launch_q<64>(a, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace kred

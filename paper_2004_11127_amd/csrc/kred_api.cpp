@@ -117,6 +117,75 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
   return true;
 }
 
+// Large-D (matrix-core) plan.
+struct MPlan {
+  int epi, DP, TJ, EB, W, KP, K;
+  int64_t N16;
+  int C;
+  int64_t jpb;
+  int64_t yop_bytes, ny_bytes, b_bytes, part_bytes;
+  float xscale, yop_scale, coord_scale, nrm_sign, pad_norm;
+};
+
+bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M, int64_t N,
+                int32_t D, int32_t E, int num_cus, MPlan* pl) {
+  MPlan q{};
+  q.DP = mfma_pad_d(D);
+  if (q.DP == 0) return false;
+  q.TJ = mfma_tile_cols(q.DP);
+  q.KP = 0;
+  q.K = 0;
+  const double log2e = 1.4426950408889634;
+  if (r == KRED_R_ARGKMIN) {
+    q.epi = 3;
+    q.K = p->K;
+    q.KP = knn_pad_k(p->K);
+    q.EB = 1;
+    q.xscale = 1.0f;
+    q.yop_scale = -2.0f;
+    q.coord_scale = 1.0f;
+    q.nrm_sign = 1.0f;
+    q.pad_norm = INFINITY;
+  } else {
+    q.EB = E <= 16 ? 1 : (E <= 32 ? 2 : 4);
+    double sc = 1.0;
+    if (f == KRED_F_GAUSS) {
+      q.epi = 0;
+      sc = std::sqrt(log2e / (2.0 * (double)p->sigma * (double)p->sigma));
+      q.pad_norm = -INFINITY;
+    } else if (f == KRED_F_LAPLACE) {
+      q.epi = 1;
+      sc = log2e / (double)p->sigma;
+      q.pad_norm = -INFINITY;
+    } else {
+      q.epi = 2;
+      q.pad_norm = 0.0f;
+    }
+    q.xscale = (float)sc;
+    q.coord_scale = (float)sc;
+    q.yop_scale = (float)(2.0 * sc);
+    q.nrm_sign = -1.0f;
+  }
+  q.W = 16 * q.EB;
+  q.N16 = (N + 15) / 16 * 16;
+  const int rows = mfma_rows_per_block(q.DP, q.KP);
+  const int64_t row_blocks = std::max<int64_t>(1, (M + rows - 1) / rows);
+  int C = choose_col_blocks(row_blocks, q.N16, num_cus, p->col_blocks);
+  int64_t jpb = (q.N16 + C - 1) / C;
+  jpb = (jpb + q.TJ - 1) / q.TJ * q.TJ;
+  q.jpb = jpb;
+  q.C = (int)((q.N16 + jpb - 1) / jpb);
+  q.yop_bytes = align_up(q.N16 * q.DP * (int64_t)sizeof(float));
+  q.ny_bytes = align_up(q.N16 * (int64_t)sizeof(float));
+  q.b_bytes = (r == KRED_R_ARGKMIN) ? 0 : align_up(q.N16 * q.W * (int64_t)sizeof(float));
+  if (r == KRED_R_ARGKMIN)
+    q.part_bytes = align_up((int64_t)4 * q.C * M * 2 * q.KP * (int64_t)sizeof(float));
+  else
+    q.part_bytes = q.C > 1 ? align_up((int64_t)q.C * M * q.W * (int64_t)sizeof(float)) : 0;
+  *pl = q;
+  return true;
+}
+
 kred_status grow_scratch(kred_ctx* ctx, size_t bytes) {
   if (bytes <= ctx->scratch_bytes) return KRED_OK;
   const size_t want = std::max(bytes, ctx->scratch_bytes * 5 / 4);
@@ -155,6 +224,95 @@ hipEvent_t next_event(kred_ctx* ctx) {
     ctx->ev.push_back(e);
   }
   return ctx->ev[ctx->ev_used++];
+}
+
+kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
+                     int64_t M, int64_t N, int32_t D, int32_t E, const float* x, const float* y,
+                     const float* b, void* out, hipStream_t s) {
+  MPlan pl;
+  if (!make_mplan(f, r, p, M, N, D, E, ctx->num_cus, &pl)) return KRED_ERR_UNSUPPORTED;
+  const kred_status gs =
+      grow_scratch(ctx, (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes));
+  if (gs != KRED_OK) return gs;
+  char* base = static_cast<char*>(ctx->scratch);
+  float* yop = reinterpret_cast<float*>(base);
+  float* ny = reinterpret_cast<float*>(base + pl.yop_bytes);
+  float* bpk = pl.b_bytes ? reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes) : nullptr;
+  float* part = pl.part_bytes
+                    ? reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes + pl.b_bytes)
+                    : nullptr;
+  const bool knn = (r == KRED_R_ARGKMIN);
+
+  MfmaPackArgs pa{};
+  pa.y = y;
+  pa.b = knn ? nullptr : b;
+  pa.N = N;
+  pa.N16 = pl.N16;
+  pa.D = D;
+  pa.DP = pl.DP;
+  pa.E = E;
+  pa.e0 = 0;
+  pa.Ec = knn ? 0 : E;
+  pa.EB = pl.EB;
+  pa.yop_scale = pl.yop_scale;
+  pa.coord_scale = pl.coord_scale;
+  pa.nrm_sign = pl.nrm_sign;
+  pa.pad_norm = pl.pad_norm;
+  pa.yop = yop;
+  pa.ny = ny;
+  pa.bpk = bpk;
+  if (launch_mfma_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
+
+  MfmaArgs ma{};
+  ma.epi = pl.epi;
+  ma.D = D;
+  ma.DP = pl.DP;
+  ma.E = E;
+  ma.e0 = 0;
+  ma.EB = pl.EB;
+  ma.M = M;
+  ma.N16 = pl.N16;
+  ma.C = pl.C;
+  ma.jpb = pl.jpb;
+  ma.x = x;
+  ma.xscale = pl.xscale;
+  ma.yop = yop;
+  ma.ny = ny;
+  ma.bpk = bpk;
+  ma.out = out;
+  ma.part = part;
+  ma.KP = pl.KP;
+  ma.K = pl.K;
+  const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (prof) {
+    e0 = next_event(ctx);
+    e1 = next_event(ctx);
+    if (!e0 || !e1 || hipEventRecord(e0, s) != hipSuccess) return KRED_ERR_HIP;
+  }
+  if (launch_mfma(ma, s) != hipSuccess) return KRED_ERR_HIP;
+  if (prof) {
+    if (hipEventRecord(e1, s) != hipSuccess) return KRED_ERR_HIP;
+    ctx->last_kernel = "mfma_kernel";
+  }
+  if (knn || pl.C > 1) {
+    CombineArgs ca{};
+    ca.formula = knn ? (int)KRED_F_SQDIST : (int)f;
+    ca.D = D;
+    ca.DP = pl.DP;
+    ca.E = E;
+    ca.EP = pl.W;
+    ca.e0 = 0;
+    ca.M = M;
+    ca.C = knn ? 4 * pl.C : pl.C;
+    ca.part = part;
+    ca.out = out;
+    ca.gscale = 0.0f;
+    ca.KP = knn ? pl.KP : 0;
+    ca.K = pl.K;
+    if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
+  }
+  return KRED_OK;
 }
 
 }  // namespace
@@ -201,8 +359,10 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
   } else {
     return KRED_ERR_UNSUPPORTED;
   }
-  // Paths: the direct-form kernels cover D <= 16 for every pair.
-  if (D > kMaxDirectD) return KRED_ERR_UNSUPPORTED;
+  // Paths: the direct-form kernels cover D <= 16 for every pair; the
+  // matrix-core kernels cover 16 < D <= 256 for the sums and arg-K-min.
+  if (D > kMaxDirectD && (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN))
+    return KRED_ERR_UNSUPPORTED;
   if (M == 0) return KRED_OK;
   if (x == nullptr || out == nullptr) return KRED_ERR_INVALID_ARG;
   if (N > 0 && (y == nullptr || (needs_b && b == nullptr))) return KRED_ERR_INVALID_ARG;
@@ -217,6 +377,11 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
   const void* bp = (r == KRED_R_ARGKMIN) ? nullptr : &dummy;
   if (kred_validate(f, r, p, M, N, D, E, &dummy, &dummy, bp, &dummy) != KRED_OK) return -1;
   if (M == 0 || N == 0) return 0;
+  if (D > kMaxDirectD) {
+    MPlan mp;
+    if (!make_mplan(f, r, p, M, N, D, E, 256, &mp)) return -1;
+    return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes;
+  }
   Plan pl;
   if (!make_plan(f, r, p, M, N, D, E, 256, &pl)) return -1;
   return pl.pack_bytes + pl.part_bytes;
@@ -274,6 +439,8 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     return launch_fill(static_cast<float*>(out), count, value, s) == hipSuccess ? KRED_OK
                                                                                 : KRED_ERR_HIP;
   }
+
+  if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s);
 
   Plan pl;
   if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &pl)) return KRED_ERR_UNSUPPORTED;

@@ -64,6 +64,42 @@ struct CombineArgs {
 };
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 
+// Large-D path (matrix cores).  Prologue: Yop[j][d] = y[j][d] * yop_scale
+// (zero for d >= D), ny[j] = nrm_sign * |y_j * coord_scale|^2 (pad_norm for
+// the padding columns N <= j < N16), and the signal tiles bpk (16 * EB
+// values of b per column, laid out as the B operand of the P . B product).
+struct MfmaPackArgs {
+  const float* y;
+  const float* b;
+  int64_t N, N16;
+  int D, DP, E, e0, Ec, EB;
+  float yop_scale, coord_scale, nrm_sign, pad_norm;
+  float* yop;
+  float* ny;
+  float* bpk;     // null for arg-K-min
+};
+hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
+
+struct MfmaArgs {
+  int epi;        // 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min
+  int D, DP, E, e0, EB;
+  int64_t M, N16;
+  int C;          // column blocks
+  int64_t jpb;    // columns per block (multiple of the tile width)
+  const float* x;
+  float xscale;
+  const float* yop;
+  const float* ny;
+  const float* bpk;
+  void* out;      // final output (sums with C == 1)
+  float* part;    // sums: C x M x 16 EB; arg-K-min: 4 C x M x 2 KP
+  int KP, K;
+};
+hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
+int mfma_pad_d(int D);               // DP for D > 16 (0 if D > 256)
+int mfma_tile_cols(int DP);          // columns per LDS tile
+int mfma_rows_per_block(int DP, int KP);
+
 // Fill out with a constant (N = 0 cases); a kernel, not a memset, so that
 // callers may capture it in a graph.
 hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s);

@@ -230,3 +230,62 @@ def test_profile_collect_counts_launches(ctx):
         ctx.run("gauss", "sum", x, y, b, sigma=0.1, flags=kred.FLAG_PROFILE)
     n, ms, name = ctx.profile_collect()
     assert n == 3 and ms > 0 and name == "sum_kernel"
+
+
+# ------------------------------------------------------- large D (matrix cores)
+
+LARGE_SUM_CASES = [
+    # formula, M, N, D, E, sigma, col_blocks
+    ("gauss", 1, 1, 17, 1, 1.0, 0),
+    ("gauss", 33, 47, 32, 16, 1.0, 0),
+    ("gauss", 300, 1000, 128, 16, 1.0, 0),
+    ("gauss", 1000, 777, 128, 16, 1.0, 3),
+    ("gauss", 257, 1500, 64, 5, 0.7, 0),
+    ("gauss", 129, 2001, 100, 17, 1.2, 2),
+    ("gauss", 200, 900, 33, 40, 0.8, 1),
+    ("gauss", 150, 640, 256, 64, 1.0, 5),
+    ("gauss", 517, 333, 200, 1, 1.0, 64),
+    ("laplace", 300, 1200, 64, 16, 1.0, 0),
+    ("laplace", 77, 500, 128, 3, 2.0, 7),
+    ("sqdist", 300, 1200, 64, 16, 1.0, 0),
+    ("sqdist", 91, 450, 48, 2, 1.0, 3),
+]
+
+
+@pytest.mark.parametrize("formula,M,N,D,E,sigma,C", LARGE_SUM_CASES)
+def test_large_d_sum_parity(ctx, formula, M, N, D, E, sigma, C):
+    rng = np.random.default_rng(M * 3 + N + D * 7 + E)
+    x = (rng.standard_normal((M, D)) / np.sqrt(D)).astype(np.float32)
+    y = (rng.standard_normal((N, D)) / np.sqrt(D)).astype(np.float32)
+    b = rng.standard_normal((N, E)).astype(np.float32)
+    out = host(ctx.run(formula, "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C))
+    ref, norm = oracle.kernel_sum(formula, x, y, b, sigma=sigma)
+    assert out.shape == (M, E)
+    assert norm_err(out, ref, norm) <= SUM_TOL
+
+
+LARGE_KNN_CASES = [
+    # M, N, D, K, col_blocks
+    (1, 1, 17, 1, 0), (65, 300, 32, 10, 0), (300, 2000, 64, 10, 0), (1000, 1500, 64, 10, 5),
+    (129, 777, 128, 16, 0), (100, 900, 200, 4, 2), (70, 640, 64, 64, 1), (513, 1001, 40, 1, 3),
+    (64, 64, 64, 64, 0),
+]
+
+
+@pytest.mark.parametrize("M,N,D,K,C", LARGE_KNN_CASES)
+def test_large_d_argkmin_integer_bit_exact(ctx, M, N, D, K, C):
+    rng = np.random.default_rng(M + 3 * N + D + K)
+    x = _int_pts(rng, M, D, -8, 8); y = _int_pts(rng, N, D, -8, 8)
+    # duplicate some columns to force exact ties
+    y[N // 2:N // 2 + N // 8] = y[:N // 8]
+    out = host(ctx.run("sqdist", "argkmin", dev(x), dev(y), None, K=K, col_blocks=C))
+    ref, _ = oracle.argkmin(x, y, K)
+    np.testing.assert_array_equal(out, ref)
+
+
+def test_large_d_unsupported_pairs_raise(ctx):
+    from paper_2004_11127_amd import kred
+    x = dev(np.ones((4, 32), np.float32)); y = dev(np.ones((4, 32), np.float32))
+    with pytest.raises(kred.KredError) as e:
+        ctx.run("gauss_gradx", "sum", x, y, dev(np.ones((4, 1), np.float32)), sigma=1.0)
+    assert e.value.status == 2
