@@ -1,19 +1,21 @@
-"""kred benchmark: Gaussian kernel sum of Eq. (1) with its x-gradient, fused,
-at M = N = 1e6, D = 3, E = 1 (one MI355X).
+"""kred benchmark on one MI355X.
 
-A step is one kred_run over the whole hot path: the packing prologue of y and
-b (prescale), the direct-form pair loop with its fused sum and gradient
-reduction, and the column-block second pass.  Inputs are seeded synthetic
-points (a mixture of 8 isotropic Gaussians, std 0.05, centres in [0,1]^3;
-b ~ N(0,1); sigma = 0.05) already resident in HBM when timing starts.
+Default workload: the Gaussian kernel sum of Eq. (1) with its x-gradient,
+fused, at M = N = 1e6, D = 3, E = 1.  A step is one kred_run over the whole
+hot path: the packing prologue of y and b (prescale), the pair loop with its
+fused sum and gradient reduction, and the column-block second pass.  Inputs
+are seeded synthetic points (a mixture of 8 isotropic Gaussians, std 0.05,
+centres in [0,1]^3; b ~ N(0,1); sigma = 0.05) already resident in HBM when
+timing starts.  `--workload` selects the other workloads.
 
 Prints one JSON line.  `value` is pair evaluations per second (Gpairs/s) of
 the whole step; `roofline` prices the main kernel's algorithmic flops
-(17 per pair) against the FP32 vector peak, timed with HIP events the
+against the FP32 vector (or FP32 matrix) peak, timed with HIP events the
 library records around that kernel on the launch stream; `cpu_baseline`
 times the fp64 oracle on the host over a bounded sample of rows.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -22,9 +24,27 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-FLOPS_PER_PAIR = {"gauss_gradx": 17, "gauss": 11}
 PEAK_FP32_VECTOR_TFLOPS = 157.3     # MI355X published FP32 vector peak
-HBM_PEAK_GBS = 8000.0
+PEAK_FP32_MATRIX_TFLOPS = 157.3     # MI355X published FP32 matrix (MFMA) peak
+
+# name: (generator kwargs, formula, reduction, flops per pair, bound, description)
+WORKLOADS = {
+    "c2": ("mixture_gauss", dict(M=1_000_000, N=1_000_000, D=3, sigma=0.05), "gauss_gradx", "sum",
+           17, "alu", "gaussian kernel sum + x-gradient (fused), mixture of 8 Gaussians, 1e6 x 1e6, D=3"),
+    "headline": ("mixture_gauss", dict(M=1_000_000, N=1_000_000, D=3, sigma=0.05), "gauss", "sum",
+                 11, "alu", "gaussian kernel sum (value only), mixture of 8 Gaussians, 1e6 x 1e6, D=3"),
+    "c1": ("uniform_gauss", dict(M=10_000, N=10_000, D=3, E=1, sigma=0.1), "gauss", "sum",
+           11, "alu", "gaussian kernel sum, uniform [0,1]^3, 1e4 x 1e4, D=3"),
+    "c3": ("sinkhorn_lse", dict(M=1_000_000, N=1_000_000, D=3, eps=0.01), "sinkhorn", "lse",
+           14, "alu", "sinkhorn log-sum-exp, uniform / shifted uniform, 1e6 x 1e6, D=3"),
+    "c4": ("highdim_gauss", dict(M=200_000, N=200_000, D=128, E=16, sigma=1.0), "gauss", "sum",
+           291, "mfma", "gaussian kernel sum, N(0, I/128), 2e5 x 2e5, D=128, E=16"),
+    "c5": ("integer_knn", dict(M=100_000, N=1_000_000, D=64, K=10), "sqdist", "argkmin",
+           131, "mfma", "arg-K-min K=10, integer mixture, 1e5 queries x 1e6 points, D=64"),
+}
+KERNEL_SOURCES = {"sum_kernel": "k_direct.hip", "gradx_kernel": "k_direct.hip",
+                  "lse_kernel": "k_direct.hip", "knn_kernel": "k_direct.hip",
+                  "mfma_kernel": "k_mfma.hip"}
 
 
 def parse():
@@ -32,24 +52,48 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--M", type=int, default=1_000_000)
-    ap.add_argument("--N", type=int, default=1_000_000)
+    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-value-only", action="store_true",
-                    help="skip the value-only Gaussian sum timed alongside")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run one 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
-                    help="HBM bytes per launch measured with rocprofv3 --pmc (JSON)")
+                    help="HBM bytes per launch measured with rocprofv3 --pmc")
     return ap.parse_args()
 
 
-def time_steps(ctx, formula, x, y, b, sigma, steps, warmup):
+def source_sha(kernel):
+    path = os.path.join(ROOT, "paper_2004_11127_amd", "csrc", KERNEL_SOURCES.get(kernel, ""))
+    try:
+        with open(path, "rb") as f:
+            return hashlib.sha1(f.read()).hexdigest()[:12]
+    except OSError:
+        return None
+
+
+def traffic_for(path, workload, kernel):
+    """Bytes per launch from the committed counter summary, if it matches the current source."""
+    try:
+        with open(path) as f:
+            tj = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = tj.get(workload)
+    if not ent or ent.get("kernel") != kernel or ent.get("source_sha") != source_sha(kernel):
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+def time_steps(ctx, w, formula, reduction, steps, warmup):
     import torch
     from paper_2004_11127_amd import kred
+    x, y = torch.from_numpy(w.x).cuda(), torch.from_numpy(w.y).cuda()
+    b = torch.from_numpy(w.b).cuda() if w.b is not None else None
+    kw = dict(sigma=w.sigma, eps=w.eps, K=w.K)
     stream = torch.cuda.current_stream()
     for _ in range(warmup):
-        ctx.run(formula, "sum", x, y, b, sigma=sigma, stream=stream)
+        ctx.run(formula, reduction, x, y, b, stream=stream, **kw)
     torch.cuda.synchronize()
     ctx.profile_collect()
     ev0 = torch.cuda.Event(enable_timing=True)
@@ -58,16 +102,16 @@ def time_steps(ctx, formula, x, y, b, sigma, steps, warmup):
     t0 = time.perf_counter()
     ev0.record(stream)
     for _ in range(steps):
-        out = ctx.run(formula, "sum", x, y, b, sigma=sigma, flags=kred.FLAG_PROFILE, stream=stream)
+        out = ctx.run(formula, reduction, x, y, b, flags=kred.FLAG_PROFILE, stream=stream, **kw)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     n, kern_ms, kname = ctx.profile_collect()
     return dict(wall_s=wall, event_ms=ev0.elapsed_time(ev1), kernel_ms=kern_ms / max(n, 1),
-                launches=n, kernel=kname, out=out)
+                launches=n, kernel=kname, out=out.cpu().numpy())
 
 
-def cpu_baseline(w, out_gpu, seconds):
+def cpu_baseline(w, formula, reduction, out_gpu, seconds):
     """Time the fp64 oracle on a bounded sample of rows (all N columns)."""
     import numpy as np
 
@@ -75,20 +119,37 @@ def cpu_baseline(w, out_gpu, seconds):
     from paper_2004_11127_amd import inputs
 
     oracle.build()
-    probe = inputs.sample_rows(w.M, 32, seed=777)
+
+    def run(rows):
+        if formula == "gauss_gradx":
+            return oracle.gauss_gradx(w.x, w.y, w.b, w.sigma, rows=rows)
+        if reduction == "lse":
+            return oracle.sinkhorn_lse(w.x, w.y, w.b, w.eps, rows=rows)
+        if reduction == "argkmin":
+            return oracle.argkmin(w.x, w.y, w.K, rows=rows)
+        return oracle.kernel_sum(formula, w.x, w.y, w.b, sigma=w.sigma, rows=rows)
+
+    probe = inputs.sample_rows(w.M, min(w.M, 32), seed=777)
     t0 = time.perf_counter()
-    oracle.gauss_gradx(w.x, w.y, w.b, w.sigma, rows=probe)
+    run(probe)
     t_probe = time.perf_counter() - t0
-    S = int(min(4096, max(64, 32 * seconds / max(t_probe, 1e-3))))
+    S = int(min(w.M, 65536, max(64, len(probe) * seconds / max(t_probe, 1e-3))))
     rows = inputs.sample_rows(w.M, S, seed=12345)
     t0 = time.perf_counter()
-    ref, norm = oracle.gauss_gradx(w.x, w.y, w.b, w.sigma, rows=rows)
+    ref, aux = run(rows)
     t = time.perf_counter() - t0
-    got = out_gpu[rows].astype(np.float64)
-    err = float(np.max(np.abs(got - ref) / np.maximum(norm, 1e-30)))
-    return dict(value=S * w.N / t / 1e9, unit="Gpairs/s", cores=oracle.num_threads(),
-                kind="oracle", sample="%d seeded rows x all %d columns (%.1f s)" % (S, w.N, t),
-                seconds=t, max_norm_err_on_sample=err)
+    got = out_gpu[rows]
+    if reduction == "argkmin":
+        check = {"index_mismatches_on_sample": int((got != ref).sum())}
+    elif reduction == "lse":
+        check = {"max_abs_err_on_sample": float(np.max(np.abs(got[:, 0] - ref)))}
+    else:
+        check = {"max_norm_err_on_sample": float(np.max(np.abs(got - ref) / np.maximum(aux, 1e-30)))}
+    res = dict(value=S * w.N / t / 1e9, unit="Gpairs/s", cores=oracle.num_threads(),
+               kind="oracle", sample="%d seeded rows x all %d columns (%.1f s)" % (S, w.N, t),
+               seconds=t)
+    res.update(check)
+    return res
 
 
 def main():
@@ -97,38 +158,24 @@ def main():
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         sys.exit(2)
-    import numpy as np
     import torch
 
     from paper_2004_11127_amd import inputs, kred
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    w = inputs.mixture_gauss(M=args.M, N=args.N, D=3, sigma=0.05, seed=0)
-    x, y, b = (torch.from_numpy(a).cuda() for a in (w.x, w.y, w.b))
+    gen, gkw, formula, reduction, fpp, bound, desc = WORKLOADS[args.workload]
+    w = getattr(inputs, gen)(seed=0, **gkw)
     pairs = float(w.M) * float(w.N)
     with kred.Context(0) as ctx:
-        r = time_steps(ctx, "gauss_gradx", x, y, b, w.sigma, args.steps, args.warmup)
-        out_gpu = r["out"].cpu().numpy()
-        extra = {}
-        if not args.no_value_only:
-            v = time_steps(ctx, "gauss", x, y, b, w.sigma, args.steps, args.warmup)
-            v_ms = v["event_ms"] / args.steps
-            extra["gauss_sum_value_only"] = dict(
-                gpairs_per_s=pairs / (v_ms / 1e3) / 1e9, ms_per_step=v_ms,
-                kernel_ms=v["kernel_ms"],
-                tflops=FLOPS_PER_PAIR["gauss"] * pairs / (v["kernel_ms"] / 1e3) / 1e12,
-                frac_fp32_vector_peak=FLOPS_PER_PAIR["gauss"] * pairs / (v["kernel_ms"] / 1e3)
-                / 1e12 / PEAK_FP32_VECTOR_TFLOPS,
-                paper_context="KeOps++ 1.38 s at M=N=1e6, D=3 on an RTX 2080 Ti (Sec. 3 table)")
+        r = time_steps(ctx, w, formula, reduction, args.steps, args.warmup)
+    if args.copy_probe:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
     ms_per_step = r["wall_s"] * 1e3 / args.steps
-    achieved = FLOPS_PER_PAIR["gauss_gradx"] * pairs / (r["kernel_ms"] / 1e3) / 1e12
-    traffic = None
-    try:
-        with open(args.traffic) as f:
-            tj = json.load(f)
-        traffic = tj.get("gradx_kernel", {}).get("bytes_per_launch")
-    except (OSError, ValueError):
-        pass
+    achieved = fpp * pairs / (r["kernel_ms"] / 1e3) / 1e12
+    peak = PEAK_FP32_VECTOR_TFLOPS if bound == "alu" else PEAK_FP32_MATRIX_TFLOPS
     line = {
         "metric": "kernel pair-evaluations/sec (Gpairs/s) at M=N=1e6 D=3; % of FP32 VALU peak",
         "value": pairs / (ms_per_step / 1e3) / 1e9,
@@ -142,18 +189,20 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "gaussian kernel sum + x-gradient (fused), mixture of 8 Gaussians",
-                   "M": w.M, "N": w.N, "D": 3, "E": 1, "sigma": w.sigma,
-                   "flops_per_pair": FLOPS_PER_PAIR["gauss_gradx"]},
-        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP32_VECTOR_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_VECTOR_TFLOPS,
-                     "traffic": traffic, "kernel": r["kernel"],
-                     "kernel_ms": r["kernel_ms"], "launches_timed": r["launches"]},
+        "config": {"workload": desc, "M": w.M, "N": w.N, "D": w.D, "E": w.E, "K": w.K,
+                   "sigma": w.sigma, "eps": w.eps, "flops_per_pair": fpp},
+        "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak,
+                     "traffic": traffic_for(args.traffic, args.workload, r["kernel"]),
+                     "kernel": r["kernel"], "kernel_ms": r["kernel_ms"],
+                     "launches_timed": r["launches"]},
         "event_ms_per_step": r["event_ms"] / args.steps,
     }
-    line.update(extra)
+    if args.workload in ("c1", "headline"):
+        line["paper_context"] = ("KeOps++ on an RTX 2080 Ti (Sec. 3 table): 0.4 ms at 1e4 and "
+                                 "1.38 s at 1e6 points, D=3, fp32")
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, out_gpu, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(w, formula, reduction, r["out"], args.cpu_seconds)
     print(json.dumps(line), flush=True)
 
 

@@ -109,20 +109,23 @@ __device__ __forceinline__ void stream_columns(const float* __restrict__ ypk, in
     if (t + 1 < ntiles) fetch(t + 1);
     const float4* buf = lds + (t & 1) * (TJ * ROW4);
     int jj = (t == 0) ? skip : 0;
+    // One y row in registers at a time: the scheduler then keeps the R
+    // independent pair chains of that row in flight instead of holding
+    // several rows and serialising each chain under the VGPR cap.
     for (; jj + U <= n; jj += U) {
-      float yv[U][SP];
 #pragma unroll
-      for (int u = 0; u < U; ++u)
+      for (int u = 0; u < U; ++u) {
+        float yv[SP];
 #pragma unroll
         for (int q = 0; q < ROW4; ++q) {
           const float4 v = buf[(jj + u) * ROW4 + q];
-          yv[u][4 * q + 0] = v.x;
-          yv[u][4 * q + 1] = v.y;
-          yv[u][4 * q + 2] = v.z;
-          yv[u][4 * q + 3] = v.w;
+          yv[4 * q + 0] = v.x;
+          yv[4 * q + 1] = v.y;
+          yv[4 * q + 2] = v.z;
+          yv[4 * q + 3] = v.w;
         }
-#pragma unroll
-      for (int u = 0; u < U; ++u) pair(yv[u], jt + jj + u);
+        pair(yv, jt + jj + u);
+      }
     }
     for (; jj < n; ++jj) {
       float yv[SP];
@@ -143,16 +146,33 @@ __device__ __forceinline__ void stream_columns(const float* __restrict__ ypk, in
 }
 
 // -------------------------------------------------------- common row set-up
+// Row r of a lane is rb * 256 R + r * 256 + threadIdx.x (rows of one r are
+// contiguous across the block, so loads and stores coalesce).  Indices are
+// recomputed where needed instead of being held in registers: the pair loop
+// runs at its best issue rate only with enough waves resident per SIMD.
+template <int R>
+__device__ __forceinline__ int64_t row_of(int64_t rb, int r, int lane_id) {
+  return rb * (int64_t)(kThreads * R) + r * kThreads + lane_id;
+}
+
+// threadIdx.x behind an empty asm: the compiler cannot prove it equal to the
+// value used before the pair loop, so it recomputes row indices after the
+// loop instead of keeping R 64-bit row values alive (and spilled) across it.
+__device__ __forceinline__ int opaque_tid() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
 template <int DP, int R>
-__device__ __forceinline__ void load_rows(const DirectArgs& a, int64_t rb, float (&xr)[R][DP],
-                                          int64_t (&row)[R]) {
+__device__ __forceinline__ void load_rows(const DirectArgs& a, int64_t rb, float (&xr)[R][DP]) {
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    row[r] = rb * (int64_t)(kThreads * R) + r * kThreads + threadIdx.x;
-    const bool ok = row[r] < a.M;
+    const int64_t row = row_of<R>(rb, r, threadIdx.x);
+    const bool ok = row < a.M;
 #pragma unroll
     for (int k = 0; k < DP; ++k)
-      xr[r][k] = (ok && k < a.D) ? a.x[row[r] * a.D + k] * a.xscale : 0.0f;
+      xr[r][k] = (ok && k < a.D) ? a.x[row * a.D + k] * a.xscale : 0.0f;
   }
 }
 
@@ -195,13 +215,12 @@ __device__ __forceinline__ float kernel_of(float d) {
 }
 
 template <int F, int DP, int EP, int R>
-__global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
+__global__ __launch_bounds__(kThreads, 8) void sum_kernel(DirectArgs a) {
   constexpr int S = DP + EP;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
   const Item it = item_of(a);
   float xr[R][DP];
-  int64_t row[R];
-  load_rows<DP, R>(a, it.rb, xr, row);
+  load_rows<DP, R>(a, it.rb, xr);
   float tot[R][EP], part[R][EP];
 #pragma unroll
   for (int r = 0; r < R; ++r)
@@ -211,12 +230,21 @@ __global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
   stream_columns<S>(
       a.ypk, it.j0, it.j1, 0, lds,
       [&](const float* yv, int64_t) {
+        // distances of all R rows first (R independent chains interleave),
+        // then the kernel values and accumulations
+        float d[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) d[r] = sq_dist<DP>(xr[r], yv);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-          const float k = kernel_of<F>(sq_dist<DP>(xr[r], yv));
+          const float k = kernel_of<F>(d[r]);
 #pragma unroll
           for (int e = 0; e < EP; ++e) part[r][e] = __builtin_fmaf(k, yv[DP + e], part[r][e]);
         }
+        // keep each column's LDS read next to its own pair work: hoisting all
+        // the unrolled reads first costs the registers the R chains need
+        __builtin_amdgcn_sched_barrier(0);
       },
       [&]() {
 #pragma unroll
@@ -229,16 +257,18 @@ __global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
       });
 
   const int Ec = min(EP, a.E - a.e0);
+  const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    if (row[r] >= a.M) continue;
+    const int64_t row = row_of<R>(it.rb, r, tid_out);
+    if (row >= a.M) continue;
     if (a.C == 1) {
-      float* o = static_cast<float*>(a.out) + row[r] * a.E + a.e0;
+      float* o = static_cast<float*>(a.out) + row * a.E + a.e0;
 #pragma unroll
       for (int e = 0; e < EP; ++e)
         if (e < Ec) o[e] = tot[r][e];
     } else {
-      float* p = a.part + ((int64_t)it.c * a.M + row[r]) * EP;
+      float* p = a.part + ((int64_t)it.c * a.M + row) * EP;
 #pragma unroll
       for (int e = 0; e < EP; ++e) p[e] = tot[r][e];
     }
@@ -248,14 +278,13 @@ __global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
 // ------------------------------------------- Gaussian sum + x-gradient
 // w = 2^-d' b_j,  a += w,  G_k += w (x'_k - y'_k);  gradient = -G * gscale.
 template <int DP, int R>
-__global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
+__global__ __launch_bounds__(kThreads, 8) void gradx_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   constexpr int W = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
   const Item it = item_of(a);
   float xr[R][DP];
-  int64_t row[R];
-  load_rows<DP, R>(a, it.rb, xr, row);
+  load_rows<DP, R>(a, it.rb, xr);
   float tot[R][W], part[R][W];
 #pragma unroll
   for (int r = 0; r < R; ++r)
@@ -290,17 +319,19 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
           }
       });
 
+  const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    if (row[r] >= a.M) continue;
+    const int64_t row = row_of<R>(it.rb, r, tid_out);
+    if (row >= a.M) continue;
     if (a.C == 1) {
-      float* o = static_cast<float*>(a.out) + row[r] * (1 + a.D);
+      float* o = static_cast<float*>(a.out) + row * (1 + a.D);
       o[0] = tot[r][0];
 #pragma unroll
       for (int k = 0; k < DP; ++k)
         if (k < a.D) o[1 + k] = -tot[r][1 + k] * a.gscale;
     } else {
-      float* p = a.part + ((int64_t)it.c * a.M + row[r]) * W;
+      float* p = a.part + ((int64_t)it.c * a.M + row) * W;
 #pragma unroll
       for (int w = 0; w < W; ++w) p[w] = tot[r][w];
     }
@@ -312,13 +343,12 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
 // Running reference m_i (<= max_j s_ij + kRescale): terms are 2^(s - m);
 // when a term would exceed 2^kRescale the sums are rescaled and m moves up.
 template <int DP, int R>
-__global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
+__global__ __launch_bounds__(kThreads, 8) void lse_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
   const Item it = item_of(a);
   float xr[R][DP];
-  int64_t row[R];
-  load_rows<DP, R>(a, it.rb, xr, row);
+  load_rows<DP, R>(a, it.rb, xr);
   float m[R], tot[R], part[R];
   {
     // the block's first column sets the reference: its term is 2^0 = 1
@@ -350,6 +380,7 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
           uu[r] = u;
           big |= (u > kRescale);
         }
+        __builtin_amdgcn_sched_barrier(0);
         if (__builtin_expect(big, 0)) {
 #pragma unroll
           for (int r = 0; r < R; ++r)
@@ -374,13 +405,15 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
 #pragma unroll
   for (int r = 0; r < R; ++r) tot[r] += part[r];
 
+  const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    if (row[r] >= a.M) continue;
+    const int64_t row = row_of<R>(it.rb, r, tid_out);
+    if (row >= a.M) continue;
     if (a.C == 1) {
-      static_cast<float*>(a.out)[row[r]] = (m[r] + fast_log2(tot[r])) * kLn2;
+      static_cast<float*>(a.out)[row] = (m[r] + fast_log2(tot[r])) * kLn2;
     } else {
-      float* p = a.part + ((int64_t)it.c * a.M + row[r]) * 2;
+      float* p = a.part + ((int64_t)it.c * a.M + row) * 2;
       p[0] = m[r];
       p[1] = tot[r];
     }
@@ -412,8 +445,7 @@ __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
   const Item it = item_of(a);
   float xr[R][DP];
-  int64_t row[R];
-  load_rows<DP, R>(a, it.rb, xr, row);
+  load_rows<DP, R>(a, it.rb, xr);
   float dk[R][KP];
   int jk[R][KP];
 #pragma unroll
@@ -442,16 +474,18 @@ __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
       },
       [&]() {});
 
+  const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    if (row[r] >= a.M) continue;
+    const int64_t row = row_of<R>(it.rb, r, tid_out);
+    if (row >= a.M) continue;
     if (a.C == 1) {
-      int* o = static_cast<int*>(a.out) + row[r] * a.K;
+      int* o = static_cast<int*>(a.out) + row * a.K;
 #pragma unroll
       for (int p = 0; p < KP; ++p)
         if (p < a.K) o[p] = jk[r][p];
     } else {
-      float* q = a.part + ((int64_t)it.c * a.M + row[r]) * (2 * KP);
+      float* q = a.part + ((int64_t)it.c * a.M + row) * (2 * KP);
 #pragma unroll
       for (int p = 0; p < KP; ++p) {
         q[2 * p] = dk[r][p];
