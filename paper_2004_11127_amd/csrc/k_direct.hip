@@ -278,7 +278,7 @@ __global__ __launch_bounds__(kThreads, 8) void sum_kernel(DirectArgs a) {
 // ------------------------------------------- Gaussian sum + x-gradient
 // w = 2^-d' b_j,  a += w,  G_k += w (x'_k - y'_k);  gradient = -G * gscale.
 template <int DP, int R>
-__global__ __launch_bounds__(kThreads, 8) void gradx_kernel(DirectArgs a) {
+__global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   constexpr int W = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
