@@ -66,6 +66,7 @@ typedef enum kred_status {
 
 /* flags */
 #define KRED_FLAG_PROFILE 1u  /* time the main kernel of each call with HIP events (kred_profile_collect) */
+#define KRED_FLAG_DIRECT 2u   /* D <= 3: always use the direct-form kernels, never the matrix-core exponent */
 
 /* Per-call parameters (the "parameters p" of Eq. (2)). */
 typedef struct kred_params {

@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libkred.so")
 
-SOURCES = ["kred_api.cpp", "k_direct.hip", "k_combine.hip", "k_mfma.hip"]
+SOURCES = ["kred_api.cpp", "k_direct.hip", "k_combine.hip", "k_mfma.hip", "k_small_mfma.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -9,10 +9,13 @@
 // gfx950: an FP32 VALU instruction whose sources are all VGPRs issues in about
 // half the cycles of one that takes a scalar (SGPR) operand.
 //
-// The pair term uses the direct form |x - y|^2 = sum_k (x_k - y_k)^2, which
-// keeps full fp32 accuracy where x is close to y (where the Gaussian is
-// large).  Coordinates arrive prescaled so that the kernel value is a single
-// v_exp_f32 (2^-d) with no extra multiply.  Sums are two-level (a per-tile
+// The pair term uses the direct form |x - y|^2 = sum_k (x_k - y_k)^2 in the
+// input coordinates, which keeps full fp32 accuracy where x is close to y
+// (where the Gaussian is large) whatever the scale of the data; the kernel
+// value is then one multiply and one v_exp_f32, 2^(-kscale d) with kscale =
+// log2(e) / (2 sigma^2).  (Prescaling the coordinates by sqrt(kscale) would
+// save the multiply but loses absolute precision in x - y when |x| sqrt(kscale)
+// is large.)  Sums are two-level (a per-tile
 // partial folded into the running total once per tile), which keeps fp32
 // rounding growth near u (sqrt(T) + sqrt(N / T)) instead of u N.
 #include "kred_internal.h"
@@ -31,6 +34,7 @@ __device__ __forceinline__ float fast_log2(float v) { return __builtin_amdgcn_lo
 
 // ------------------------------------------------------------------ prologue
 __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
   const int S = a.DP + a.EP;
   const int64_t total = a.N * S;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
@@ -205,12 +209,12 @@ __device__ __forceinline__ Item item_of(const DirectArgs& a) {
 }
 
 // ------------------------------------------------------- sum-type formulas
-// F = k(d) b_j with k = 2^-d (Gauss, prescaled), 2^-sqrt(d) (Laplace,
-// prescaled) or d (squared distance).
+// F = k(d) b_j with k = 2^(-ks d) (Gauss), 2^(-ks sqrt(d)) (Laplace) or d
+// (squared distance).
 template <int F>
-__device__ __forceinline__ float kernel_of(float d) {
-  if constexpr (F == F_GAUSS) return fast_exp2(-d);
-  else if constexpr (F == F_LAPLACE) return fast_exp2(-fast_sqrt(d));
+__device__ __forceinline__ float kernel_of(float d, float ks) {
+  if constexpr (F == F_GAUSS) return fast_exp2(-(ks * d));
+  else if constexpr (F == F_LAPLACE) return fast_exp2(-(ks * fast_sqrt(d)));
   else return d;
 }
 
@@ -218,6 +222,7 @@ template <int F, int DP, int EP, int R>
 __global__ __launch_bounds__(kThreads, 8) void sum_kernel(DirectArgs a) {
   constexpr int S = DP + EP;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
   const Item it = item_of(a);
   float xr[R][DP];
   load_rows<DP, R>(a, it.rb, xr);
@@ -226,6 +231,7 @@ __global__ __launch_bounds__(kThreads, 8) void sum_kernel(DirectArgs a) {
   for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int e = 0; e < EP; ++e) tot[r][e] = part[r][e] = 0.0f;
+  const float ks = a.kscale;
 
   stream_columns<S>(
       a.ypk, it.j0, it.j1, 0, lds,
@@ -238,7 +244,7 @@ __global__ __launch_bounds__(kThreads, 8) void sum_kernel(DirectArgs a) {
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-          const float k = kernel_of<F>(d[r]);
+          const float k = kernel_of<F>(d[r], ks);
 #pragma unroll
           for (int e = 0; e < EP; ++e) part[r][e] = __builtin_fmaf(k, yv[DP + e], part[r][e]);
         }
@@ -276,12 +282,13 @@ __global__ __launch_bounds__(kThreads, 8) void sum_kernel(DirectArgs a) {
 }
 
 // ------------------------------------------- Gaussian sum + x-gradient
-// w = 2^-d' b_j,  a += w,  G_k += w (x'_k - y'_k);  gradient = -G * gscale.
+// w = 2^(-ks d) b_j,  a += w,  G_k += w (x_k - y_k);  gradient = -G * gscale.
 template <int DP, int R>
 __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   constexpr int W = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
   const Item it = item_of(a);
   float xr[R][DP];
   load_rows<DP, R>(a, it.rb, xr);
@@ -303,7 +310,7 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
             t[k] = xr[r][k] - yv[k];
             d = (k == 0) ? t[0] * t[0] : __builtin_fmaf(t[k], t[k], d);
           }
-          const float w = fast_exp2(-d) * yv[DP];
+          const float w = fast_exp2(-(a.kscale * d)) * yv[DP];
           part[r][0] += w;
 #pragma unroll
           for (int k = 0; k < DP; ++k) part[r][1 + k] = __builtin_fmaf(w, t[k], part[r][1 + k]);
@@ -339,13 +346,14 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
 }
 
 // ------------------------------------------------ Sinkhorn log-sum-exp
-// In log2 units: s_ij = g'_j - d'_ij with g' = g log2(e), d' = |x' - y'|^2.
+// In log2 units: s_ij = g'_j - ks d_ij with g' = g log2(e), ks = log2(e) / eps.
 // Running reference m_i (<= max_j s_ij + kRescale): terms are 2^(s - m);
 // when a term would exceed 2^kRescale the sums are rescaled and m moves up.
 template <int DP, int R>
 __global__ __launch_bounds__(kThreads, 8) void lse_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
   const Item it = item_of(a);
   float xr[R][DP];
   load_rows<DP, R>(a, it.rb, xr);
@@ -358,7 +366,7 @@ __global__ __launch_bounds__(kThreads, 8) void lse_kernel(DirectArgs a) {
     for (int s = 0; s < S; ++s) yv[s] = y0[s];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      m[r] = yv[DP] - sq_dist<DP>(xr[r], yv);
+      m[r] = __builtin_fmaf(-a.kscale, sq_dist<DP>(xr[r], yv), yv[DP]);
       tot[r] = 0.0f;
       part[r] = 1.0f;
     }
@@ -371,12 +379,7 @@ __global__ __launch_bounds__(kThreads, 8) void lse_kernel(DirectArgs a) {
         bool big = false;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-          float u = yv[DP] - m[r];
-#pragma unroll
-          for (int k = 0; k < DP; ++k) {
-            const float t = xr[r][k] - yv[k];
-            u = __builtin_fmaf(-t, t, u);
-          }
+          const float u = __builtin_fmaf(-a.kscale, sq_dist<DP>(xr[r], yv), yv[DP] - m[r]);
           uu[r] = u;
           big |= (u > kRescale);
         }

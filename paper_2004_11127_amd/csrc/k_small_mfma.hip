@@ -1,0 +1,397 @@
+// Small-D (D <= 3) reductions with the exponent on the bf16 matrix cores.
+//
+// The direct form of the pair term costs about 6 VALU instructions per pair
+// before the exp.  Here the whole exponent T_ij = -c |x_i - y_j|^2 (log2
+// units) comes from one v_mfma_f32_16x16x32_bf16 per 16 x 16 block of
+// (column j, row i) pairs, which runs alongside the VALU/exp work, so the VALU
+// is left with the exp and the reduction itself.
+//
+// Accuracy.  With u = sqrt(c) (x - m) and v = sqrt(c) (y - m) for a centre m,
+//     T = 2 <u, v> - |u|^2 - |v|^2.
+// Every fp32 operand is split into three bf16 parts (h + m + l carries 24+
+// bits); the products hh, hm, mh, hl, lh, mm of each coordinate, and the
+// three parts of -|u|^2 and -|v|^2, fill 24 of the 32 K slots, so each
+// product term is exact and only terms below 2^-26 |u||v| are dropped.  The
+// large cancelling terms sit in the first 8-slot group of K, which the matrix
+// core sums with more than fp32 precision.  The remaining error grows with
+// c R^2, R the half-diagonal of the joint bounding box of x and y around its
+// centre m; the prologue computes it on the device and the kernels fall back
+// to the direct form when c R^2 > kFastLimit (no host synchronisation).
+//
+// K slots (A: column side, B: row side), for coordinate d = 0..2:
+//   6d + 0..5:  A = (Vh, Vm, Vh, Vl, Vh, Vm) of V = 2 v_d,
+//               B = (uh, uh, um, uh, ul, um) of u_d
+//   18..20:     A = parts of -|v|^2, B = 1
+//   21..23:     A = 1,               B = parts of -|u|^2
+//   24..26:     log-sum-exp only: A = parts of g' = g log2(e), B = 1
+//   27..31:     0
+// Lane layout of v_mfma_f32_16x16x32_bf16 (lane l = 16 g + li): A: lane
+// supplies A[li][8g .. 8g+7]; B: lane supplies B[8g .. 8g+7][li]; D: lane holds
+// D[4g + r][li].  With A = columns and B = rows, lane l gets T for row li and
+// columns 4g + r of the block.
+#include "kred_internal.h"
+
+#include <climits>
+
+namespace kred {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int TJF = 256;             // columns per LDS tile
+constexpr float kRescaleF = 32.0f;   // log-sum-exp rescale threshold (log2 units)
+
+__device__ __forceinline__ void split3(float v, __bf16& h, __bf16& m, __bf16& l) {
+  h = (__bf16)v;
+  float r = v - (float)h;
+  m = (__bf16)r;
+  r -= (float)m;
+  l = (__bf16)r;
+}
+
+__global__ void guard_init_kernel(FastGuard* g) {
+  const int t = threadIdx.x;
+  if (t < 4) {
+    g->lo[t] = fenc(__builtin_inff());
+    g->hi[t] = fenc(-__builtin_inff());
+  }
+}
+
+// Joint bounding box of x (M x D) and y (N x D).
+__global__ __launch_bounds__(256) void bounds_kernel(const float* __restrict__ x, int64_t M,
+                                                     const float* __restrict__ y, int64_t N, int D,
+                                                     FastGuard* g) {
+  float lo[3] = {__builtin_inff(), __builtin_inff(), __builtin_inff()};
+  float hi[3] = {-__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < M + N; t += stride) {
+    const float* p = t < M ? x + t * D : y + (t - M) * D;
+    for (int d = 0; d < D; ++d) {
+      lo[d] = fminf(lo[d], p[d]);
+      hi[d] = fmaxf(hi[d], p[d]);
+    }
+  }
+  for (int d = 0; d < D; ++d) {
+    float a = lo[d], b = hi[d];
+    for (int o = 32; o > 0; o >>= 1) {
+      a = fminf(a, __shfl_xor(a, o));
+      b = fmaxf(b, __shfl_xor(b, o));
+    }
+    if ((threadIdx.x & 63) == 0) {
+      atomicMin(&g->lo[d], fenc(a));
+      atomicMax(&g->hi[d], fenc(b));
+    }
+  }
+}
+
+// Column-side packing: A row (32 bf16) and per-column extras.
+//   sum:   ex = (b, -, -, -)        gradx: ex = (b, b v0, b v1, b v2)
+//   lse:   g' = g log2(e) in A slots 24..26
+// Padding columns (N <= j < N16) get zero A rows and zero extras.
+__global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
+  const FastFrame fr = fast_frame(a.guard, a.D, a.scale);
+  if (!fr.ok) return;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < a.N16; j += stride) {
+    __bf16 s[32];
+#pragma unroll
+    for (int k = 0; k < 32; ++k) s[k] = (__bf16)0.0f;
+    float4 ex = {0.f, 0.f, 0.f, 0.f};
+    if (j < a.N) {
+      float v[3] = {0.f, 0.f, 0.f};
+      float nv = 0.0f;
+#pragma unroll
+      for (int d = 0; d < 3; ++d)
+        if (d < a.D) {
+          v[d] = (a.y[j * a.D + d] - fr.m[d]) * a.scale;
+          nv = __builtin_fmaf(v[d], v[d], nv);
+          __bf16 h, m, l;
+          split3(2.0f * v[d], h, m, l);
+          s[6 * d + 0] = h;
+          s[6 * d + 1] = m;
+          s[6 * d + 2] = h;
+          s[6 * d + 3] = l;
+          s[6 * d + 4] = h;
+          s[6 * d + 5] = m;
+        }
+      split3(-nv, s[18], s[19], s[20]);
+      s[21] = s[22] = s[23] = (__bf16)1.0f;
+      const float bj = a.b[j];
+      if (a.epi == FAST_LSE) {
+        split3(bj * kLog2e, s[24], s[25], s[26]);
+      } else if (a.epi == FAST_GRADX) {
+        ex = float4{bj, bj * v[0], bj * v[1], bj * v[2]};
+      } else {
+        ex.x = bj;
+      }
+    }
+    uint4 w[4];
+    __builtin_memcpy(w, s, 64);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a.apk[j * 4 + q] = w[q];
+    if (a.epi == FAST_GRADX) a.ex[j] = ex;
+    else if (a.epi == FAST_SUM) a.eb[j] = ex.x;
+  }
+}
+
+// Row-side B operand: this lane's 8 K slots (8g .. 8g+7) for its row.
+__device__ __forceinline__ bf16x8 row_operand(const float (&u)[3], int D, int g, bool lse) {
+  __bf16 s[32];
+#pragma unroll
+  for (int k = 0; k < 32; ++k) s[k] = (__bf16)0.0f;
+  float nu = 0.0f;
+#pragma unroll
+  for (int d = 0; d < 3; ++d)
+    if (d < D) {
+      __bf16 h, m, l;
+      split3(u[d], h, m, l);
+      s[6 * d + 0] = h;
+      s[6 * d + 1] = h;
+      s[6 * d + 2] = m;
+      s[6 * d + 3] = h;
+      s[6 * d + 4] = l;
+      s[6 * d + 5] = m;
+      nu = __builtin_fmaf(u[d], u[d], nu);
+    }
+  s[18] = s[19] = s[20] = (__bf16)1.0f;
+  split3(-nu, s[21], s[22], s[23]);
+  if (lse) s[24] = s[25] = s[26] = (__bf16)1.0f;
+  bf16x8 o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = s[8 * g + e];
+  return o;
+}
+
+// EPI: FAST_SUM (Gauss, E = 1), FAST_GRADX, FAST_LSE.
+template <int EPI, int RB>
+__global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
+  __shared__ uint4 As[2][TJF * 4];
+  __shared__ float4 Xs[2][EPI == FAST_GRADX ? TJF : 1];    // (b, b v) per column
+  __shared__ float4 Bq[2][EPI == FAST_SUM ? TJF / 4 : 1];  // b per column, 4 to a float4
+
+  const FastFrame fr = fast_frame(a.guard, a.D, a.scale);
+  if (!fr.ok) return;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, li = lane & 15, g = lane >> 4;
+  const int c = blockIdx.x % a.C;
+  const int64_t rbk = blockIdx.x / a.C;
+  const int64_t j0 = (int64_t)c * a.jpb;
+  const int64_t j1 = min(a.N16, j0 + a.jpb);
+  const int64_t i0 = rbk * (64 * RB) + wave * (16 * RB);
+
+  bf16x8 xb[RB];
+  float ur[RB][3];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int64_t row = i0 + 16 * rb + li;
+#pragma unroll
+    for (int d = 0; d < 3; ++d)
+      ur[rb][d] = (row < a.M && d < a.D) ? (a.x[row * a.D + d] - fr.m[d]) * a.scale : 0.0f;
+    xb[rb] = row_operand(ur[rb], a.D, g, EPI == FAST_LSE);
+  }
+  // per lane: sums over its columns (4 g + r of every block) for row li
+  float acc[RB][4], tot[RB][4], mref[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[rb][q] = tot[rb][q] = 0.0f;
+    mref[rb] = -__builtin_inff();
+  }
+
+  uint4 sa[4];
+  float4 sx;
+  float sb;
+  auto fetch = [&](int64_t jt) {
+    const int ncol = (int)min((int64_t)TJF, j1 - jt);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int f = tid + q * 256;
+      sa[q] = (f / 4 < ncol) ? a.apk[jt * 4 + f] : uint4{0u, 0u, 0u, 0u};
+    }
+    if constexpr (EPI == FAST_GRADX) sx = (tid < ncol) ? a.ex[jt + tid] : float4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (EPI == FAST_SUM) sb = (tid < ncol) ? a.eb[jt + tid] : 0.0f;
+  };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) As[buf][tid + q * 256] = sa[q];
+    if constexpr (EPI == FAST_GRADX) Xs[buf][tid] = sx;
+    if constexpr (EPI == FAST_SUM) reinterpret_cast<float*>(&Bq[buf][0])[tid] = sb;
+  };
+
+  const int64_t ntiles = (j1 - j0 + TJF - 1) / TJF;
+  if (ntiles > 0) {
+    fetch(j0);
+    put(0);
+  }
+  __syncthreads();
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int64_t jt = j0 + t * TJF;
+    const int buf = (int)(t & 1);
+    const int nblk = (int)(min((int64_t)TJF, j1 - jt) / 16);
+    if (t + 1 < ntiles) fetch(jt + TJF);
+    for (int blk = 0; blk < nblk; ++blk) {
+      const uint4 av = As[buf][(blk * 16 + li) * 4 + g];
+      bf16x8 am;
+      __builtin_memcpy(&am, &av, 16);
+      float4 xv[4];
+      float4 bq;
+      if constexpr (EPI == FAST_SUM) {
+        bq = Bq[buf][blk * 4 + g];   // b of columns 4g .. 4g+3 of the block
+      } else if constexpr (EPI == FAST_GRADX) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) xv[r] = Xs[buf][blk * 16 + 4 * g + r];
+      }
+      // last (ragged) block of the column range: mask padding columns
+      const int64_t jb = jt + blk * 16 + 4 * g;
+      const bool ragged = (jt + blk * 16 + 16 > a.N);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0,
+                                                             0, 0);
+        if constexpr (EPI == FAST_SUM) {
+          acc[rb][0] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[0]), bq.x, acc[rb][0]);
+          acc[rb][1] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[1]), bq.y, acc[rb][1]);
+          acc[rb][2] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[2]), bq.z, acc[rb][2]);
+          acc[rb][3] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[3]), bq.w, acc[rb][3]);
+        } else if constexpr (EPI == FAST_GRADX) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float k = __builtin_amdgcn_exp2f(T[r]);
+            acc[rb][0] = __builtin_fmaf(k, xv[r].x, acc[rb][0]);
+            acc[rb][1] = __builtin_fmaf(k, xv[r].y, acc[rb][1]);
+            acc[rb][2] = __builtin_fmaf(k, xv[r].z, acc[rb][2]);
+            acc[rb][3] = __builtin_fmaf(k, xv[r].w, acc[rb][3]);
+          }
+        } else {
+          float u[4];
+          bool big = false;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            u[r] = T[r] - mref[rb];
+            big |= u[r] > kRescaleF;
+          }
+          if (__builtin_expect(big || ragged, 0)) {
+            // rare: a new running maximum, or padding columns in the last block
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              if (jb + r >= a.N) continue;
+              float ur = T[r] - mref[rb];
+              if (ur > kRescaleF) {
+                const float f = __builtin_amdgcn_exp2f(-ur);
+                acc[rb][0] *= f;
+                tot[rb][0] *= f;
+                mref[rb] = T[r];
+                ur = 0.0f;
+              }
+              acc[rb][0] += __builtin_amdgcn_exp2f(ur);
+            }
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[rb][0] += __builtin_amdgcn_exp2f(u[r]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        tot[rb][q] += acc[rb][q];
+        acc[rb][q] = 0.0f;
+      }
+    if (t + 1 < ntiles) put((int)((t + 1) & 1));
+    __syncthreads();
+  }
+
+  // merge the four lane groups of each row (lanes li, li+16, li+32, li+48)
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int64_t row = i0 + 16 * rb + li;
+    if constexpr (EPI == FAST_LSE) {
+      float m = mref[rb], s = tot[rb][0];
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        const float m2 = __shfl_xor(m, o), s2 = __shfl_xor(s, o);
+        const float mx = fmaxf(m, m2);
+        s = (m == -__builtin_inff() ? 0.0f : s * __builtin_amdgcn_exp2f(m - mx)) +
+            (m2 == -__builtin_inff() ? 0.0f : s2 * __builtin_amdgcn_exp2f(m2 - mx));
+        m = mx;
+      }
+      if (g == 0 && row < a.M) {
+        if (a.C == 1) {
+          static_cast<float*>(a.out)[row] = (m + __builtin_amdgcn_logf(s)) * kLn2;
+        } else {
+          float* p = a.part + ((int64_t)c * a.M + row) * 2;
+          p[0] = m;
+          p[1] = s;
+        }
+      }
+    } else {
+      float v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[q] = tot[rb][q];
+        v[q] += __shfl_xor(v[q], 16);
+        v[q] += __shfl_xor(v[q], 32);
+      }
+      if (g == 0 && row < a.M) {
+        if constexpr (EPI == FAST_SUM) {
+          const float sum = (v[0] + v[1]) + (v[2] + v[3]);
+          if (a.C == 1) static_cast<float*>(a.out)[row] = sum;
+          else a.part[(int64_t)c * a.M + row] = sum;
+        } else {
+          // G_d = sum_j k b (u_d - v_jd) = u_d a - H_d in prescaled units; divided
+          // by the prescale it is sum_j k b (x_d - y_jd), as the direct kernel sums
+          const float inv = 1.0f / a.scale;
+          const float G[3] = {(ur[rb][0] * v[0] - v[1]) * inv, (ur[rb][1] * v[0] - v[2]) * inv,
+                              (ur[rb][2] * v[0] - v[3]) * inv};
+          if (a.C == 1) {
+            float* o = static_cast<float*>(a.out) + row * (1 + a.D);
+            o[0] = v[0];
+#pragma unroll
+            for (int d = 0; d < 3; ++d)
+              if (d < a.D) o[1 + d] = -G[d] * a.gscale;
+          } else {
+            float* p = a.part + ((int64_t)c * a.M + row) * (1 + a.DP);
+            p[0] = v[0];
+#pragma unroll
+            for (int d = 0; d < 3; ++d)
+              if (d < a.DP) p[1 + d] = G[d];
+          }
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+int fast_rows_per_block(int epi) { return 64 * (epi == FAST_GRADX ? 2 : 4); }
+
+hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M, hipStream_t s) {
+  FastGuard* g = const_cast<FastGuard*>(a.guard);   // the prologue fills the guard
+  hipLaunchKernelGGL(guard_init_kernel, dim3(1), dim3(64), 0, s, g);
+  const int64_t items = M + a.N;
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 2048));
+  hipLaunchKernelGGL(bounds_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, M, a.y, a.N, a.D, g);
+  if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+  const int64_t pb = std::max<int64_t>(1, std::min<int64_t>((a.N16 + 255) / 256, 8192));
+  hipLaunchKernelGGL(fast_pack_kernel, dim3((unsigned)pb), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fast(const FastArgs& a, hipStream_t s) {
+  const int rows = fast_rows_per_block(a.epi);
+  const int64_t rb = (a.M + rows - 1) / rows;
+  const dim3 grid((unsigned)(rb * a.C));
+  switch (a.epi) {
+    case FAST_SUM: hipLaunchKernelGGL((fast_kernel<FAST_SUM, 4>), grid, dim3(256), 0, s, a); break;
+    case FAST_GRADX: hipLaunchKernelGGL((fast_kernel<FAST_GRADX, 2>), grid, dim3(256), 0, s, a); break;
+    case FAST_LSE: hipLaunchKernelGGL((fast_kernel<FAST_LSE, 4>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace kred

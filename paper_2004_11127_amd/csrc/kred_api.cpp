@@ -47,6 +47,8 @@ struct Plan {
   int W_max;      // widest partial row
   int64_t pack_bytes, part_bytes;
   float xscale, bscale, gscale;
+  float kscale;   // direct kernels: pair scale (input coordinates)
+  float fscale;   // fast path: coordinate prescale sqrt(c)
 };
 
 // Column split: enough (row block, column block) work items to keep every
@@ -62,7 +64,8 @@ int choose_col_blocks(int64_t row_blocks, int64_t N, int num_cus, int requested)
 }
 
 bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M, int64_t N,
-               int32_t D, int32_t E, int num_cus, Plan* pl) {
+               int32_t D, int32_t E, int num_cus, Plan* pl, int rows_override = 0,
+               int jpb_align = 1) {
   Plan q{};
   q.formula = (int)f;
   q.reduction = (int)r;
@@ -84,37 +87,69 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
   q.S_max = q.DP + EP_first;
   q.W_max = partial_width(q.formula, q.DP, EP_first, q.KP);
   const int R = direct_rows_per_thread(q.formula, q.DP, EP_first, q.KP);
-  const int64_t row_blocks = (M + (int64_t)kThreads * R - 1) / ((int64_t)kThreads * R);
+  const int64_t rows = rows_override > 0 ? rows_override : (int64_t)kThreads * R;
+  const int64_t row_blocks = (M + rows - 1) / rows;
   q.C = choose_col_blocks(std::max<int64_t>(1, row_blocks), N, num_cus, p->col_blocks);
   q.jpb = N > 0 ? (N + q.C - 1) / q.C : 0;
+  q.jpb = (q.jpb + jpb_align - 1) / jpb_align * jpb_align;
   if (N > 0) q.C = (int)((N + q.jpb - 1) / q.jpb);   // no empty column block
   q.pack_bytes = align_up(N * q.S_max * (int64_t)sizeof(float));
   q.part_bytes = q.C > 1 ? align_up((int64_t)q.C * M * q.W_max * (int64_t)sizeof(float)) : 0;
-  // prescales: the kernels evaluate 2^(-|x' - y'|^2) etc. with x' = x * xscale
+  // Direct kernels work in input coordinates (xscale = 1) and scale the pair:
+  // Gauss 2^(-c d), c = log2(e) / (2 sigma^2); Laplace 2^(-c sqrt d), c =
+  // log2(e) / sigma; Sinkhorn g log2(e) - c d, c = log2(e) / eps.  The small-D
+  // fast path prescales coordinates by fscale = sqrt(c) (Gauss, Sinkhorn).
   const double log2e = 1.4426950408889634;
+  q.xscale = 1.0f;
   q.bscale = 1.0f;
   q.gscale = 0.0f;
+  q.kscale = 1.0f;
+  q.fscale = 1.0f;
   switch (f) {
     case KRED_F_GAUSS:
     case KRED_F_GAUSS_GRADX: {
       const double s = (double)p->sigma;
       const double c = log2e / (2.0 * s * s);
-      q.xscale = (float)std::sqrt(c);
-      q.gscale = (float)(1.0 / (s * s * std::sqrt(c)));
+      q.kscale = (float)c;
+      q.fscale = (float)std::sqrt(c);
+      q.gscale = (float)(1.0 / (s * s));
       break;
     }
     case KRED_F_LAPLACE:
-      q.xscale = (float)(log2e / (double)p->sigma);
+      q.kscale = (float)(log2e / (double)p->sigma);
       break;
     case KRED_F_SINKHORN:
-      q.xscale = (float)std::sqrt(log2e / (double)p->eps);
+      q.kscale = (float)(log2e / (double)p->eps);
+      q.fscale = (float)std::sqrt(log2e / (double)p->eps);
       q.bscale = (float)log2e;
       break;
     default:
-      q.xscale = 1.0f;
+      break;
   }
   *pl = q;
   return true;
+}
+
+// Small-D fast path (exponent on the bf16 matrix cores), when the pair allows it.
+int fast_epi(kred_formula f, kred_reduction r, int32_t D, int32_t E, uint32_t flags) {
+  if (D > 3 || (flags & KRED_FLAG_DIRECT)) return -1;
+  if (f == KRED_F_GAUSS && r == KRED_R_SUM && E == 1) return FAST_SUM;
+  if (f == KRED_F_GAUSS_GRADX && r == KRED_R_SUM) return FAST_GRADX;
+  if (f == KRED_F_SINKHORN && r == KRED_R_LSE) return FAST_LSE;
+  return -1;
+}
+
+struct FastScratch {
+  int64_t guard_bytes, apk_bytes, ex_bytes;
+};
+FastScratch fast_scratch(int epi, int64_t N) {
+  FastScratch fs{};
+  if (epi < 0) return fs;
+  const int64_t N16 = (N + 15) / 16 * 16;
+  fs.guard_bytes = align_up(sizeof(FastGuard));
+  fs.apk_bytes = align_up(N16 * 64);
+  fs.ex_bytes = epi == FAST_GRADX ? align_up(N16 * 16) : (epi == FAST_SUM ? align_up(N16 * 4) : 0);
+  return fs;
 }
 
 // Large-D (matrix-core) plan.
@@ -382,9 +417,13 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
     if (!make_mplan(f, r, p, M, N, D, E, 256, &mp)) return -1;
     return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes;
   }
+  const int epi = fast_epi(f, r, D, E, p->flags);
   Plan pl;
-  if (!make_plan(f, r, p, M, N, D, E, 256, &pl)) return -1;
-  return pl.pack_bytes + pl.part_bytes;
+  if (!make_plan(f, r, p, M, N, D, E, 256, &pl, epi >= 0 ? fast_rows_per_block(epi) : 0,
+                 epi >= 0 ? 256 : 1))
+    return -1;
+  const FastScratch fs = fast_scratch(epi, N);
+  return pl.pack_bytes + pl.part_bytes + fs.guard_bytes + fs.apk_bytes + fs.ex_bytes;
 }
 
 kred_status kred_create(kred_ctx** ctx, int device) {
@@ -427,8 +466,8 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   if (v != KRED_OK) return v;
   if (M == 0) return KRED_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  DeviceGuard guard(ctx->device);
-  if (!guard.ok) return KRED_ERR_HIP;
+  DeviceGuard devg(ctx->device);
+  if (!devg.ok) return KRED_ERR_HIP;
 
   if (N == 0) {
     int64_t count = M;
@@ -442,16 +481,57 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
 
   if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s);
 
+  const int epi = fast_epi(f, r, D, E, p->flags);
   Plan pl;
-  if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &pl)) return KRED_ERR_UNSUPPORTED;
-  const kred_status gs = grow_scratch(ctx, (size_t)(pl.pack_bytes + pl.part_bytes));
+  if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &pl,
+                 epi >= 0 ? fast_rows_per_block(epi) : 0, epi >= 0 ? 256 : 1))
+    return KRED_ERR_UNSUPPORTED;
+  const FastScratch fs = fast_scratch(epi, N);
+  const kred_status gs = grow_scratch(
+      ctx, (size_t)(pl.pack_bytes + pl.part_bytes + fs.guard_bytes + fs.apk_bytes + fs.ex_bytes));
   if (gs != KRED_OK) return gs;
-  float* ypk = static_cast<float*>(ctx->scratch);
-  float* part = pl.part_bytes ? reinterpret_cast<float*>(static_cast<char*>(ctx->scratch) +
-                                                         pl.pack_bytes)
-                              : nullptr;
+  char* sbase = static_cast<char*>(ctx->scratch);
+  float* ypk = reinterpret_cast<float*>(sbase);
+  float* part = pl.part_bytes ? reinterpret_cast<float*>(sbase + pl.pack_bytes) : nullptr;
+  char* fbase = sbase + pl.pack_bytes + pl.part_bytes;
+  FastGuard* guard = epi >= 0 ? reinterpret_cast<FastGuard*>(fbase) : nullptr;
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
 
+  FastArgs fa{};
+  if (epi >= 0) {
+    FastPackArgs fp{};
+    fp.epi = epi;
+    fp.D = D;
+    fp.N = N;
+    fp.N16 = (N + 15) / 16 * 16;
+    fp.y = y;
+    fp.b = b;
+    fp.scale = pl.fscale;
+    fp.guard = guard;
+    fp.apk = reinterpret_cast<uint4*>(fbase + fs.guard_bytes);
+    fp.ex = epi == FAST_GRADX ? reinterpret_cast<float4*>(fbase + fs.guard_bytes + fs.apk_bytes)
+                              : nullptr;
+    fp.eb = epi == FAST_SUM ? reinterpret_cast<float*>(fbase + fs.guard_bytes + fs.apk_bytes)
+                            : nullptr;
+    if (launch_fast_prologue(fp, x, M, s) != hipSuccess) return KRED_ERR_HIP;
+    fa.epi = epi;
+    fa.D = D;
+    fa.DP = pl.DP;
+    fa.M = M;
+    fa.N = N;
+    fa.N16 = fp.N16;
+    fa.C = pl.C;
+    fa.jpb = pl.jpb;
+    fa.x = x;
+    fa.scale = pl.fscale;
+    fa.gscale = pl.gscale;
+    fa.guard = guard;
+    fa.apk = fp.apk;
+    fa.ex = fp.ex;
+    fa.eb = fp.eb;
+    fa.out = out;
+    fa.part = part;
+  }
   const int n_slices = (r == KRED_R_ARGKMIN) ? 1 : (pl.E + 15) / 16;
   for (int sl = 0; sl < n_slices; ++sl) {
     const int e0 = sl * 16;
@@ -468,6 +548,8 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     pa.e0 = e0;
     pa.yscale = pl.xscale;
     pa.bscale = pl.bscale;
+    pa.guard = guard;
+    pa.fscale = pl.fscale;
     if (launch_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
 
     DirectArgs da{};
@@ -484,21 +566,27 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     da.x = x;
     da.ypk = ypk;
     da.xscale = pl.xscale;
+    da.kscale = pl.kscale;
     da.gscale = pl.gscale;
+    da.fscale = pl.fscale;
     da.out = out;
     da.part = part;
     da.KP = pl.KP;
     da.K = pl.K;
+    da.guard = guard;
     hipEvent_t e_start = nullptr, e_stop = nullptr;
     if (prof) {
       e_start = next_event(ctx);
       e_stop = next_event(ctx);
       if (!e_start || !e_stop || hipEventRecord(e_start, s) != hipSuccess) return KRED_ERR_HIP;
     }
+    // with the fast path eligible, both launch and exactly one does the work
+    if (epi >= 0 && launch_fast(fa, s) != hipSuccess) return KRED_ERR_HIP;
     if (launch_direct(da, s) != hipSuccess) return KRED_ERR_HIP;
     if (prof) {
       if (hipEventRecord(e_stop, s) != hipSuccess) return KRED_ERR_HIP;
-      ctx->last_kernel = (r == KRED_R_ARGKMIN)       ? "knn_kernel"
+      ctx->last_kernel = (epi >= 0)                  ? "fast_kernel"
+                         : (r == KRED_R_ARGKMIN)     ? "knn_kernel"
                          : (f == KRED_F_GAUSS_GRADX) ? "gradx_kernel"
                          : (f == KRED_F_SINKHORN)    ? "lse_kernel"
                                                      : "sum_kernel";

@@ -13,6 +13,46 @@ constexpr int kThreads = 256;          // threads per workgroup for the direct-f
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
+// Small-D fast path (D <= 3): exponent on the bf16 matrix cores.  The
+// prologue computes the joint bounding box of x and y on the device; the
+// fast kernels run only when c R^2 <= kFastLimit (R the half-diagonal of the
+// box in prescaled units), otherwise the direct-form kernels do the work.
+// Both are launched; each returns at once when the other one is selected.
+enum : int { FAST_SUM = 0, FAST_GRADX = 1, FAST_LSE = 2 };
+constexpr float kFastLimit = 2048.0f;
+
+struct FastGuard {
+  int lo[4];   // order-preserving int encodings of the box corners
+  int hi[4];
+};
+
+__device__ __forceinline__ int fenc(float f) {
+  const int i = __float_as_int(f);
+  return i >= 0 ? i : i ^ 0x7fffffff;
+}
+__device__ __forceinline__ float fdec(int i) { return __int_as_float(i >= 0 ? i : i ^ 0x7fffffff); }
+
+struct FastFrame {
+  float m[3];   // centre of the box
+  bool ok;      // the expanded form meets the accuracy bound
+};
+__device__ __forceinline__ FastFrame fast_frame(const FastGuard* g, int D, float scale) {
+  FastFrame f;
+  float r2 = 0.0f;
+  for (int d = 0; d < 3; ++d) {
+    if (d < D) {
+      const float lo = fdec(g->lo[d]), hi = fdec(g->hi[d]);
+      f.m[d] = 0.5f * (lo + hi);
+      const float h = 0.5f * (hi - lo) * scale;
+      r2 += h * h;
+    } else {
+      f.m[d] = 0.0f;
+    }
+  }
+  f.ok = r2 <= kFastLimit;   // false for NaN
+  return f;
+}
+
 // Prologue: copy y (and one E-slice of b) into a padded, prescaled,
 // interleaved array ypk[j * S + s], S = DP + EP:
 //   s <  D        : y[j, s] * yscale
@@ -26,6 +66,8 @@ struct PackArgs {
   int64_t N;
   int D, DP, E, EP, e0;
   float yscale, bscale;
+  const FastGuard* guard;   // non-null: skip when the fast path is selected
+  float fscale;             // prescale of the fast path (for its guard test)
 };
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 
@@ -38,11 +80,14 @@ struct DirectArgs {
   int64_t jpb;            // j per column block
   const float* x;         // M x D
   const float* ypk;       // N x (DP + EP), from the prologue
-  float xscale;           // same scale as yscale of the prologue
+  float xscale;           // coordinate scale (1: the direct kernels work in input units)
+  float kscale;           // pair scale: Gauss 2^(-kscale d), Laplace 2^(-kscale sqrt d), LSE g' - kscale d
   float gscale;           // gradient: out = -G * gscale; unused otherwise
+  float fscale;           // prescale of the small-D fast path (for its guard test)
   void* out;              // final output (C == 1)
   float* part;            // partials (C > 1), C x M x W
   int KP, K;              // arg-K-min list length (power of two) and K
+  const FastGuard* guard; // non-null: skip when the fast path is selected
 };
 hipError_t launch_direct(const DirectArgs& a, hipStream_t s);
 int direct_rows_per_thread(int formula, int DP, int EP, int KP);
@@ -99,6 +144,36 @@ hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
 int mfma_pad_d(int D);               // DP for D > 16 (0 if D > 256)
 int mfma_tile_cols(int DP);          // columns per LDS tile
 int mfma_rows_per_block(int DP, int KP);
+
+struct FastPackArgs {
+  int epi, D;
+  int64_t N, N16;
+  const float* y;
+  const float* b;     // b (sums, gradient) or g (log-sum-exp)
+  float scale;        // prescale sqrt(c)
+  const FastGuard* guard;
+  uint4* apk;         // N16 x 4 uint4: 32 bf16 A-operand slots per column
+  float4* ex;         // gradient: (b, b v0, b v1, b v2) per column
+  float* eb;          // sum: b per column
+};
+hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M, hipStream_t s);
+
+struct FastArgs {
+  int epi, D, DP;
+  int64_t M, N, N16;
+  int C;
+  int64_t jpb;        // multiple of 256
+  const float* x;
+  float scale, gscale;
+  const FastGuard* guard;
+  const uint4* apk;
+  const float4* ex;
+  const float* eb;
+  void* out;
+  float* part;
+};
+hipError_t launch_fast(const FastArgs& a, hipStream_t s);
+int fast_rows_per_block(int epi);
 
 // Fill out with a constant (N = 0 cases); a kernel, not a memset, so that
 // callers may capture it in a graph.

@@ -21,6 +21,7 @@ REDUCTIONS = {"sum": 0, "lse": 1, "argkmin": 2}
 STATUS = {0: "KRED_OK", 1: "KRED_ERR_INVALID_ARG", 2: "KRED_ERR_UNSUPPORTED", 3: "KRED_ERR_NOMEM",
           4: "KRED_ERR_HIP", 5: "KRED_ERR_NO_DEVICE"}
 FLAG_PROFILE = 1
+FLAG_DIRECT = 2
 MAX_D, MAX_E, MAX_K, MAX_COL_BLOCKS = 256, 64, 64, 256
 
 

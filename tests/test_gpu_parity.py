@@ -229,7 +229,11 @@ def test_profile_collect_counts_launches(ctx):
     for _ in range(3):
         ctx.run("gauss", "sum", x, y, b, sigma=0.1, flags=kred.FLAG_PROFILE)
     n, ms, name = ctx.profile_collect()
-    assert n == 3 and ms > 0 and name == "sum_kernel"
+    assert n == 3 and ms > 0 and name == "fast_kernel"
+    for _ in range(2):
+        ctx.run("gauss", "sum", x, y, b, sigma=0.1, flags=kred.FLAG_PROFILE | kred.FLAG_DIRECT)
+    n, ms, name = ctx.profile_collect()
+    assert n == 2 and ms > 0 and name == "sum_kernel"
 
 
 # ------------------------------------------------------- large D (matrix cores)
@@ -289,3 +293,80 @@ def test_large_d_unsupported_pairs_raise(ctx):
     with pytest.raises(kred.KredError) as e:
         ctx.run("gauss_gradx", "sum", x, y, dev(np.ones((4, 1), np.float32)), sigma=1.0)
     assert e.value.status == 2
+
+
+# ------------------------------------------- small-D matrix-core exponent path
+
+FAST_CASES = [
+    # formula, reduction, M, N, D, param, col_blocks
+    ("gauss", "sum", 1, 1, 3, 0.3, 0),
+    ("gauss", "sum", 7, 5, 3, 0.3, 0),
+    ("gauss", "sum", 300, 17, 2, 0.2, 0),
+    ("gauss", "sum", 1000, 4099, 3, 0.05, 0),
+    ("gauss", "sum", 4099, 1000, 1, 0.02, 3),
+    ("gauss", "sum", 2000, 3001, 3, 0.1, 16),
+    ("gauss_gradx", "sum", 1, 1, 3, 0.3, 0),
+    ("gauss_gradx", "sum", 1000, 4099, 3, 0.05, 0),
+    ("gauss_gradx", "sum", 2049, 517, 2, 0.05, 2),
+    ("gauss_gradx", "sum", 333, 2050, 1, 0.1, 7),
+    ("sinkhorn", "lse", 1, 1, 3, 0.1, 0),
+    ("sinkhorn", "lse", 9, 5, 3, 0.05, 0),
+    ("sinkhorn", "lse", 1000, 4099, 3, 0.01, 0),
+    ("sinkhorn", "lse", 4099, 1000, 2, 0.002, 3),
+    ("sinkhorn", "lse", 700, 2001, 1, 0.01, 16),
+]
+
+
+def _fast_case(ctx, formula, reduction, M, N, D, param, C, flags, scale=1.0):
+    rng = np.random.default_rng(M + 17 * N + D)
+    x = _pts(rng, M, D, scale); y = _pts(rng, N, D, scale)
+    b = rng.standard_normal((N, 1)).astype(np.float32)
+    kw = dict(sigma=param) if reduction == "sum" else dict(eps=param)
+    out = host(ctx.run(formula, reduction, dev(x), dev(y), dev(b), col_blocks=C, flags=flags, **kw))
+    if formula == "gauss":
+        ref, norm = oracle.kernel_sum("gauss", x, y, b, sigma=param)
+        err = norm_err(out, ref, norm)
+        return err <= SUM_TOL, err
+    if formula == "gauss_gradx":
+        ref, norm = oracle.gauss_gradx(x, y, b, param)
+        err = norm_err(out, ref, norm)
+        return err <= SUM_TOL, err
+    ref, m = oracle.sinkhorn_lse(x, y, b, param)
+    err = lse_err(out[:, 0], ref, m)
+    return err <= LSE_TOL, err
+
+
+@pytest.mark.parametrize("formula,reduction,M,N,D,param,C", FAST_CASES)
+def test_fast_path_parity(ctx, formula, reduction, M, N, D, param, C):
+    ok, err = _fast_case(ctx, formula, reduction, M, N, D, param, C, flags=0)
+    assert ok, err
+
+
+@pytest.mark.parametrize("formula,reduction,M,N,D,param,C", FAST_CASES[3:6] + FAST_CASES[7:9] + FAST_CASES[12:14])
+def test_direct_flag_parity(ctx, formula, reduction, M, N, D, param, C):
+    from paper_2004_11127_amd import kred
+    ok, err = _fast_case(ctx, formula, reduction, M, N, D, param, C, flags=kred.FLAG_DIRECT)
+    assert ok, err
+
+
+@pytest.mark.parametrize("formula,reduction,param", [("gauss", "sum", 0.01), ("gauss_gradx", "sum", 0.01),
+                                                     ("sinkhorn", "lse", 0.1)])
+def test_fast_path_falls_back_on_wide_data(ctx, formula, reduction, param):
+    # points spread over [0, 20]^3 with a narrow kernel: c R^2 is above the fast
+    # path's limit (4300 for the log-sum-exp case, far more for the Gaussians),
+    # so the direct-form kernels must produce the result
+    ok, err = _fast_case(ctx, formula, reduction, 500, 3000, 3, param, 0, flags=0, scale=20.0)
+    assert ok, err
+
+
+def test_fast_path_deterministic(ctx):
+    rng = np.random.default_rng(31)
+    x = dev(_pts(rng, 3000, 3)); y = dev(_pts(rng, 5000, 3))
+    b = dev(rng.standard_normal((5000, 1)).astype(np.float32))
+    for f in ("gauss", "gauss_gradx"):
+        a1 = host(ctx.run(f, "sum", x, y, b, sigma=0.05))
+        a2 = host(ctx.run(f, "sum", x, y, b, sigma=0.05))
+        np.testing.assert_array_equal(a1, a2)
+    l1 = host(ctx.run("sinkhorn", "lse", x, y, b, eps=0.01))
+    l2 = host(ctx.run("sinkhorn", "lse", x, y, b, eps=0.01))
+    np.testing.assert_array_equal(l1, l2)
