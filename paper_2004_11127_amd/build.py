@@ -26,6 +26,9 @@ ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-ffp-contract=fast", "-Wall", "-Wno-unused-function",
+         # MFMA results in VGPRs: the epilogues read them at once, and the
+         # AGPR form would add a v_accvgpr_read (a VALU slot) per element
+         "-mllvm", "-amdgpu-mfma-vgpr-form",
          "-I", INCLUDE, "-I", CSRC]
 
 
