@@ -66,7 +66,11 @@ typedef enum kred_status {
 
 /* flags */
 #define KRED_FLAG_PROFILE 1u  /* time the main kernel of each call with HIP events (kred_profile_collect) */
-#define KRED_FLAG_DIRECT 2u   /* D <= 3: always use the direct-form kernels, never the matrix-core exponent */
+#define KRED_FLAG_DIRECT 2u   /* D <= 3: always use the direct-form kernels, never the matrix-core exponent
+                                 (used otherwise only below 2^28 pairs, or when the data's extent makes
+                                 the matrix-core form less accurate) */
+#define KRED_FLAG_FAST 4u     /* D <= 3: use the matrix-core exponent whatever the problem size (the
+                                 accuracy guard still falls back to the direct form); DIRECT wins */
 
 /* Per-call parameters (the "parameters p" of Eq. (2)). */
 typedef struct kred_params {

@@ -40,25 +40,21 @@ __device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
 }
 
 // ------------------------------------------------------------------ prologue
+// Coalesced: consecutive threads handle consecutive d of one column.
 __global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  // y operand and norms: one thread per column j (norm accumulated in fp32)
-  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < a.N16; j += stride) {
-    float nrm = 0.0f;
-    const bool ok = j < a.N;
-    for (int d = 0; d < a.DP; ++d) {
-      const float v = (ok && d < a.D) ? a.y[j * a.D + d] : 0.0f;
-      const float s = v * a.coord_scale;
-      nrm = __builtin_fmaf(s, s, nrm);
-      a.yop[j * a.DP + d] = v * a.yop_scale;
-    }
-    a.ny[j] = ok ? a.nrm_sign * nrm : a.pad_norm;
+  const int64_t total = a.N16 * a.DP;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total; t += stride) {
+    const int64_t j = t / a.DP;
+    const int d = (int)(t - j * a.DP);
+    const float v = (j < a.N && d < a.D) ? a.y[j * a.D + d] : 0.0f;
+    a.yop[t] = v * a.yop_scale;
   }
   // signal tiles: b[j][e0 + e] stored at (j/16)*16W + ((j%16)/4)*4W + e*4 + j%4, W = 16*EB
   if (a.bpk != nullptr) {
     const int W = 16 * a.EB;
-    const int64_t total = a.N16 * W;
-    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total; t += stride) {
+    const int64_t total_b = a.N16 * W;
+    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total_b; t += stride) {
       const int64_t j = t / W;
       const int e = (int)(t - j * W);
       const float v = (j < a.N && e < a.Ec) ? a.b[j * a.E + a.e0 + e] : 0.0f;
@@ -66,6 +62,24 @@ __global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
       const int jr = (int)(j % 16);
       a.bpk[blk * 16 * W + (jr / 4) * 4 * W + e * 4 + (jr % 4)] = v;
     }
+  }
+}
+
+// Column norms: one wave per column at a time, lanes stride over d (coalesced),
+// fp32 sum of the prescaled squares, reduced across the wave.
+__global__ __launch_bounds__(256) void mfma_norm_kernel(MfmaPackArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t j = wave; j < a.N16; j += waves) {
+    float s = 0.0f;
+    if (j < a.N)
+      for (int d = lane; d < a.D; d += 64) {
+        const float v = a.y[j * a.D + d] * a.coord_scale;
+        s = __builtin_fmaf(v, v, s);
+      }
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if (lane == 0) a.ny[j] = j < a.N ? a.nrm_sign * s : a.pad_norm;
   }
 }
 
@@ -348,9 +362,12 @@ int mfma_rows_per_block(int DP, int KP) {
 
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s) {
   if (a.N16 == 0) return hipSuccess;
-  const int64_t blocks = std::min<int64_t>((a.N16 * 16 * a.EB + 255) / 256, 8192);
-  hipLaunchKernelGGL(mfma_pack_kernel, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(256), 0,
-                     s, a);
+  const int64_t items = a.N16 * std::max(a.DP, 16 * a.EB);
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 8192));
+  hipLaunchKernelGGL(mfma_pack_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+  const int64_t nb = std::max<int64_t>(1, std::min<int64_t>((a.N16 + 3) / 4, 4096));
+  hipLaunchKernelGGL(mfma_norm_kernel, dim3((unsigned)nb), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -58,10 +58,12 @@ __global__ void guard_init_kernel(FastGuard* g) {
   }
 }
 
-// Joint bounding box of x (M x D) and y (N x D).
+// Joint bounding box of x (M x D) and y (N x D): per-block reduction (wave
+// shuffles, then LDS), then one atomic per block and coordinate.
 __global__ __launch_bounds__(256) void bounds_kernel(const float* __restrict__ x, int64_t M,
                                                      const float* __restrict__ y, int64_t N, int D,
                                                      FastGuard* g) {
+  __shared__ float red[2][3][4];
   float lo[3] = {__builtin_inff(), __builtin_inff(), __builtin_inff()};
   float hi[3] = {-__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -72,16 +74,25 @@ __global__ __launch_bounds__(256) void bounds_kernel(const float* __restrict__ x
       hi[d] = fmaxf(hi[d], p[d]);
     }
   }
-  for (int d = 0; d < D; ++d) {
+  const int wave = threadIdx.x >> 6;
+  for (int d = 0; d < 3; ++d) {
     float a = lo[d], b = hi[d];
     for (int o = 32; o > 0; o >>= 1) {
       a = fminf(a, __shfl_xor(a, o));
       b = fmaxf(b, __shfl_xor(b, o));
     }
     if ((threadIdx.x & 63) == 0) {
-      atomicMin(&g->lo[d], fenc(a));
-      atomicMax(&g->hi[d], fenc(b));
+      red[0][d][wave] = a;
+      red[1][d][wave] = b;
     }
+  }
+  __syncthreads();
+  if (threadIdx.x < D) {
+    const int d = threadIdx.x;
+    const float a = fminf(fminf(red[0][d][0], red[0][d][1]), fminf(red[0][d][2], red[0][d][3]));
+    const float b = fmaxf(fmaxf(red[1][d][0], red[1][d][1]), fmaxf(red[1][d][2], red[1][d][3]));
+    atomicMin(&g->lo[d], fenc(a));
+    atomicMax(&g->hi[d], fenc(b));
   }
 }
 
@@ -373,7 +384,7 @@ hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M
   FastGuard* g = const_cast<FastGuard*>(a.guard);   // the prologue fills the guard
   hipLaunchKernelGGL(guard_init_kernel, dim3(1), dim3(64), 0, s, g);
   const int64_t items = M + a.N;
-  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 2048));
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 512));
   hipLaunchKernelGGL(bounds_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, M, a.y, a.N, a.D, g);
   if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
   const int64_t pb = std::max<int64_t>(1, std::min<int64_t>((a.N16 + 255) / 256, 8192));

@@ -130,9 +130,15 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
   return true;
 }
 
-// Small-D fast path (exponent on the bf16 matrix cores), when the pair allows it.
-int fast_epi(kred_formula f, kred_reduction r, int32_t D, int32_t E, uint32_t flags) {
+// Small-D fast path (exponent on the bf16 matrix cores), when the pair allows
+// it and the problem is large enough for its extra prologue launches (guard,
+// bounds, packing) to pay off; below that the direct kernels are faster.
+constexpr double kFastMinPairs = 268435456.0;   // 2^28 pairs
+
+int fast_epi(kred_formula f, kred_reduction r, int64_t M, int64_t N, int32_t D, int32_t E,
+             uint32_t flags) {
   if (D > 3 || (flags & KRED_FLAG_DIRECT)) return -1;
+  if (!(flags & KRED_FLAG_FAST) && (double)M * (double)N < kFastMinPairs) return -1;
   if (f == KRED_F_GAUSS && r == KRED_R_SUM && E == 1) return FAST_SUM;
   if (f == KRED_F_GAUSS_GRADX && r == KRED_R_SUM) return FAST_GRADX;
   if (f == KRED_F_SINKHORN && r == KRED_R_LSE) return FAST_LSE;
@@ -417,7 +423,7 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
     if (!make_mplan(f, r, p, M, N, D, E, 256, &mp)) return -1;
     return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes;
   }
-  const int epi = fast_epi(f, r, D, E, p->flags);
+  const int epi = fast_epi(f, r, M, N, D, E, p->flags);
   Plan pl;
   if (!make_plan(f, r, p, M, N, D, E, 256, &pl, epi >= 0 ? fast_rows_per_block(epi) : 0,
                  epi >= 0 ? 256 : 1))
@@ -481,7 +487,7 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
 
   if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s);
 
-  const int epi = fast_epi(f, r, D, E, p->flags);
+  const int epi = fast_epi(f, r, M, N, D, E, p->flags);
   Plan pl;
   if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &pl,
                  epi >= 0 ? fast_rows_per_block(epi) : 0, epi >= 0 ? 256 : 1))

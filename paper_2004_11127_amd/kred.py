@@ -22,6 +22,7 @@ STATUS = {0: "KRED_OK", 1: "KRED_ERR_INVALID_ARG", 2: "KRED_ERR_UNSUPPORTED", 3:
           4: "KRED_ERR_HIP", 5: "KRED_ERR_NO_DEVICE"}
 FLAG_PROFILE = 1
 FLAG_DIRECT = 2
+FLAG_FAST = 4
 MAX_D, MAX_E, MAX_K, MAX_COL_BLOCKS = 256, 64, 64, 256
 
 

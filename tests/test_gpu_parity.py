@@ -223,8 +223,9 @@ def test_runs_on_a_side_stream(ctx):
 def test_profile_collect_counts_launches(ctx):
     from paper_2004_11127_amd import kred
     rng = np.random.default_rng(24)
-    x = dev(_pts(rng, 2000, 3)); y = dev(_pts(rng, 2000, 3))
-    b = dev(rng.standard_normal((2000, 1)).astype(np.float32))
+    # 2^28+ pairs take the matrix-core exponent path; small problems the direct one
+    x = dev(_pts(rng, 20000, 3)); y = dev(_pts(rng, 16384, 3))
+    b = dev(rng.standard_normal((16384, 1)).astype(np.float32))
     ctx.profile_collect()
     for _ in range(3):
         ctx.run("gauss", "sum", x, y, b, sigma=0.1, flags=kred.FLAG_PROFILE)
@@ -234,6 +235,10 @@ def test_profile_collect_counts_launches(ctx):
         ctx.run("gauss", "sum", x, y, b, sigma=0.1, flags=kred.FLAG_PROFILE | kred.FLAG_DIRECT)
     n, ms, name = ctx.profile_collect()
     assert n == 2 and ms > 0 and name == "sum_kernel"
+    xs = dev(_pts(rng, 1000, 3))
+    ctx.run("gauss", "sum", xs, y, b, sigma=0.1, flags=kred.FLAG_PROFILE)
+    n, ms, name = ctx.profile_collect()
+    assert n == 1 and name == "sum_kernel"
 
 
 # ------------------------------------------------------- large D (matrix cores)
@@ -338,7 +343,8 @@ def _fast_case(ctx, formula, reduction, M, N, D, param, C, flags, scale=1.0):
 
 @pytest.mark.parametrize("formula,reduction,M,N,D,param,C", FAST_CASES)
 def test_fast_path_parity(ctx, formula, reduction, M, N, D, param, C):
-    ok, err = _fast_case(ctx, formula, reduction, M, N, D, param, C, flags=0)
+    from paper_2004_11127_amd import kred
+    ok, err = _fast_case(ctx, formula, reduction, M, N, D, param, C, flags=kred.FLAG_FAST)
     assert ok, err
 
 
@@ -355,18 +361,22 @@ def test_fast_path_falls_back_on_wide_data(ctx, formula, reduction, param):
     # points spread over [0, 20]^3 with a narrow kernel: c R^2 is above the fast
     # path's limit (4300 for the log-sum-exp case, far more for the Gaussians),
     # so the direct-form kernels must produce the result
-    ok, err = _fast_case(ctx, formula, reduction, 500, 3000, 3, param, 0, flags=0, scale=20.0)
+    from paper_2004_11127_amd import kred
+    ok, err = _fast_case(ctx, formula, reduction, 500, 3000, 3, param, 0, flags=kred.FLAG_FAST,
+                         scale=20.0)
     assert ok, err
 
 
 def test_fast_path_deterministic(ctx):
+    from paper_2004_11127_amd import kred
+    F = kred.FLAG_FAST
     rng = np.random.default_rng(31)
     x = dev(_pts(rng, 3000, 3)); y = dev(_pts(rng, 5000, 3))
     b = dev(rng.standard_normal((5000, 1)).astype(np.float32))
     for f in ("gauss", "gauss_gradx"):
-        a1 = host(ctx.run(f, "sum", x, y, b, sigma=0.05))
-        a2 = host(ctx.run(f, "sum", x, y, b, sigma=0.05))
+        a1 = host(ctx.run(f, "sum", x, y, b, sigma=0.05, flags=F))
+        a2 = host(ctx.run(f, "sum", x, y, b, sigma=0.05, flags=F))
         np.testing.assert_array_equal(a1, a2)
-    l1 = host(ctx.run("sinkhorn", "lse", x, y, b, eps=0.01))
-    l2 = host(ctx.run("sinkhorn", "lse", x, y, b, eps=0.01))
+    l1 = host(ctx.run("sinkhorn", "lse", x, y, b, eps=0.01, flags=F))
+    l2 = host(ctx.run("sinkhorn", "lse", x, y, b, eps=0.01, flags=F))
     np.testing.assert_array_equal(l1, l2)
