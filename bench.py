@@ -44,7 +44,7 @@ WORKLOADS = {
 }
 KERNEL_SOURCES = {"sum_kernel": "k_direct.hip", "gradx_kernel": "k_direct.hip",
                   "lse_kernel": "k_direct.hip", "knn_kernel": "k_direct.hip",
-                  "mfma_kernel": "k_mfma.hip"}
+                  "mfma_kernel": "k_mfma.hip", "fast_kernel": "k_small_mfma.hip"}
 
 
 def parse():
@@ -53,7 +53,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="c2", choices=sorted(WORKLOADS))
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+    ap.add_argument("--cpu-seconds", type=float, default=25.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
