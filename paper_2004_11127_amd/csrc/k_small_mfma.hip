@@ -175,10 +175,12 @@ __device__ __forceinline__ bf16x8 row_operand(const float (&u)[3], int D, int g,
 }
 
 // EPI: FAST_SUM (Gauss, E = 1), FAST_GRADX, FAST_LSE.
+
 template <int EPI, int RB>
 __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
+  constexpr bool kLse = EPI == FAST_LSE;
   __shared__ uint4 As[2][TJF * 4];
-  __shared__ float4 Xs[2][EPI == FAST_GRADX ? TJF : 1];    // (b, b v) per column
+  __shared__ float4 Xs[2][EPI == FAST_GRADX ? TJF : 1];   // (b, b v) per column
   __shared__ float4 Bq[2][EPI == FAST_SUM ? TJF / 4 : 1];  // b per column, 4 to a float4
 
   const FastFrame fr = fast_frame(a.guard, a.D, a.scale);
@@ -199,7 +201,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
 #pragma unroll
     for (int d = 0; d < 3; ++d)
       ur[rb][d] = (row < a.M && d < a.D) ? (a.x[row * a.D + d] - fr.m[d]) * a.scale : 0.0f;
-    xb[rb] = row_operand(ur[rb], a.D, g, EPI == FAST_LSE);
+    xb[rb] = row_operand(ur[rb], a.D, g, kLse);
   }
   // per lane: sums over its columns (4 g + r of every block) for row li
   float acc[RB][4], tot[RB][4], mref[RB];
@@ -229,7 +231,12 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
     if constexpr (EPI == FAST_GRADX) Xs[buf][tid] = sx;
     if constexpr (EPI == FAST_SUM) reinterpret_cast<float*>(&Bq[buf][0])[tid] = sb;
   };
-
+  auto a_operand = [&](int buf, int blk) {
+    const uint4 av = As[buf][(blk * 16 + li) * 4 + g];
+    bf16x8 am;
+    __builtin_memcpy(&am, &av, 16);
+    return am;
+  };
   const int64_t ntiles = (j1 - j0 + TJF - 1) / TJF;
   if (ntiles > 0) {
     fetch(j0);
@@ -241,65 +248,99 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
     const int buf = (int)(t & 1);
     const int nblk = (int)(min((int64_t)TJF, j1 - jt) / 16);
     if (t + 1 < ntiles) fetch(jt + TJF);
-    for (int blk = 0; blk < nblk; ++blk) {
-      const uint4 av = As[buf][(blk * 16 + li) * 4 + g];
-      bf16x8 am;
-      __builtin_memcpy(&am, &av, 16);
-      float4 xv[4];
-      float4 bq;
-      if constexpr (EPI == FAST_SUM) {
-        bq = Bq[buf][blk * 4 + g];   // b of columns 4g .. 4g+3 of the block
-      } else if constexpr (EPI == FAST_GRADX) {
+    if constexpr (!kLse) {
+      // Padding columns have zero extras, so they add nothing: no masking.
+      for (int blk = 0; blk < nblk; ++blk) {
+        const bf16x8 am = a_operand(buf, blk);
+        float4 xv[4];
+        float4 bq;
+        if constexpr (EPI == FAST_SUM) {
+          bq = Bq[buf][blk * 4 + g];   // b of columns 4g .. 4g+3 of the block
+        } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) xv[r] = Xs[buf][blk * 16 + 4 * g + r];
+          for (int r = 0; r < 4; ++r) xv[r] = Xs[buf][blk * 16 + 4 * g + r];
+        }
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+          if constexpr (EPI == FAST_SUM) {
+            acc[rb][0] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[0]), bq.x, acc[rb][0]);
+            acc[rb][1] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[1]), bq.y, acc[rb][1]);
+            acc[rb][2] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[2]), bq.z, acc[rb][2]);
+            acc[rb][3] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[3]), bq.w, acc[rb][3]);
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float k = __builtin_amdgcn_exp2f(T[r]);
+              acc[rb][0] = __builtin_fmaf(k, xv[r].x, acc[rb][0]);
+              acc[rb][1] = __builtin_fmaf(k, xv[r].y, acc[rb][1]);
+              acc[rb][2] = __builtin_fmaf(k, xv[r].z, acc[rb][2]);
+              acc[rb][3] = __builtin_fmaf(k, xv[r].w, acc[rb][3]);
+            }
+          }
+        }
       }
-      // last (ragged) block of the column range: mask padding columns
-      const int64_t jb = jt + blk * 16 + 4 * g;
-      const bool ragged = (jt + blk * 16 + 16 > a.N);
+    } else {
+      // Fast path: the running reference enters the matrix product as its C
+      // operand, so the MFMA returns u = T - m directly; a running maximum of u
+      // over the tile tells afterwards whether any term needed a rescale.
+      const bool ragged = jt + 16 * nblk > a.N;   // padding columns must be masked
+      // The maximum is taken over the bit patterns as signed integers: that
+      // orders non-negative floats correctly and puts every negative one
+      // below them, which is all the test against the threshold needs (and
+      // it avoids the NaN quieting a float max would add per operand).
+      int run[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) run[rb] = INT_MIN;
+      if (!ragged) {
+        f4 negm[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) negm[rb] = f4{-mref[rb], -mref[rb], -mref[rb], -mref[rb]};
+        for (int blk = 0; blk < nblk; ++blk) {
+          const bf16x8 am = a_operand(buf, blk);
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            const f4 u = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], negm[rb], 0, 0, 0);
+            run[rb] = max(max(run[rb], __float_as_int(u[0])), __float_as_int(u[1]));
+            run[rb] = max(max(run[rb], __float_as_int(u[2])), __float_as_int(u[3]));
+            acc[rb][0] += (__builtin_amdgcn_exp2f(u[0]) + __builtin_amdgcn_exp2f(u[1])) +
+                          (__builtin_amdgcn_exp2f(u[2]) + __builtin_amdgcn_exp2f(u[3]));
+          }
+        }
+      }
+      bool need[RB], redo = false;
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0,
-                                                             0, 0);
-        if constexpr (EPI == FAST_SUM) {
-          acc[rb][0] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[0]), bq.x, acc[rb][0]);
-          acc[rb][1] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[1]), bq.y, acc[rb][1]);
-          acc[rb][2] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[2]), bq.z, acc[rb][2]);
-          acc[rb][3] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[3]), bq.w, acc[rb][3]);
-        } else if constexpr (EPI == FAST_GRADX) {
+        need[rb] = ragged || run[rb] > __float_as_int(kRescaleF);
+        redo |= need[rb];
+      }
+      if (__any(redo)) {
+        // Rare (a new running maximum, the first tile, or padding columns): the
+        // whole wave recomputes the tile; lanes that need it redo their sums
+        // term by term with rescaling and masking.
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float k = __builtin_amdgcn_exp2f(T[r]);
-            acc[rb][0] = __builtin_fmaf(k, xv[r].x, acc[rb][0]);
-            acc[rb][1] = __builtin_fmaf(k, xv[r].y, acc[rb][1]);
-            acc[rb][2] = __builtin_fmaf(k, xv[r].z, acc[rb][2]);
-            acc[rb][3] = __builtin_fmaf(k, xv[r].w, acc[rb][3]);
-          }
-        } else {
-          float u[4];
-          bool big = false;
+        for (int rb = 0; rb < RB; ++rb)
+          if (need[rb]) acc[rb][0] = 0.0f;
+        for (int blk = 0; blk < nblk; ++blk) {
+          const bf16x8 am = a_operand(buf, blk);
+          const int64_t jb = jt + blk * 16 + 4 * g;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            u[r] = T[r] - mref[rb];
-            big |= u[r] > kRescaleF;
-          }
-          if (__builtin_expect(big || ragged, 0)) {
-            // rare: a new running maximum, or padding columns in the last block
+          for (int rb = 0; rb < RB; ++rb) {
+            const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            if (!need[rb]) continue;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               if (jb + r >= a.N) continue;
-              float ur = T[r] - mref[rb];
-              if (ur > kRescaleF) {
-                const float f = __builtin_amdgcn_exp2f(-ur);
+              float d = T[r] - mref[rb];
+              if (d > kRescaleF) {
+                const float f = __builtin_amdgcn_exp2f(-d);
                 acc[rb][0] *= f;
                 tot[rb][0] *= f;
                 mref[rb] = T[r];
-                ur = 0.0f;
+                d = 0.0f;
               }
-              acc[rb][0] += __builtin_amdgcn_exp2f(ur);
+              acc[rb][0] += __builtin_amdgcn_exp2f(d);
             }
-          } else {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) acc[rb][0] += __builtin_amdgcn_exp2f(u[r]);
           }
         }
       }
@@ -378,7 +419,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
 
 }  // namespace
 
-int fast_rows_per_block(int epi) { return 64 * (epi == FAST_GRADX ? 2 : 4); }
+int fast_rows_per_block(int epi) { return 64 * 4; }
 
 hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M, hipStream_t s) {
   FastGuard* g = const_cast<FastGuard*>(a.guard);   // the prologue fills the guard
@@ -398,7 +439,7 @@ hipError_t launch_fast(const FastArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)(rb * a.C));
   switch (a.epi) {
     case FAST_SUM: hipLaunchKernelGGL((fast_kernel<FAST_SUM, 4>), grid, dim3(256), 0, s, a); break;
-    case FAST_GRADX: hipLaunchKernelGGL((fast_kernel<FAST_GRADX, 2>), grid, dim3(256), 0, s, a); break;
+    case FAST_GRADX: hipLaunchKernelGGL((fast_kernel<FAST_GRADX, 4>), grid, dim3(256), 0, s, a); break;
     case FAST_LSE: hipLaunchKernelGGL((fast_kernel<FAST_LSE, 4>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }

@@ -367,6 +367,30 @@ def test_fast_path_falls_back_on_wide_data(ctx, formula, reduction, param):
     assert ok, err
 
 
+@pytest.mark.parametrize("path", ["fast", "direct"])
+@pytest.mark.parametrize("profile", ["rising", "falling", "spread"])
+def test_lse_running_maximum(ctx, path, profile):
+    # g_j chosen so the row maximum of s_ij = g_j - |x_i - y_j|^2 / eps moves by
+    # far more than the rescale threshold inside a column range: "rising" puts
+    # a new maximum in almost every tile (and inside tiles), "falling" puts it
+    # in the first tile, "spread" scatters large values at random
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(5)
+    M, N, eps = 777, 5000, 0.05
+    x = _pts(rng, M, 3); y = _pts(rng, N, 3)
+    ramp = np.linspace(0.0, 600.0, N)
+    g = {"rising": ramp, "falling": ramp[::-1].copy(),
+         "spread": 80.0 * rng.standard_normal(N)}[profile]
+    g = g.astype(np.float32).reshape(N, 1)
+    flags = kred.FLAG_FAST if path == "fast" else kred.FLAG_DIRECT
+    for C in (0, 3):
+        out = host(ctx.run("sinkhorn", "lse", dev(x), dev(y), dev(g), eps=eps, col_blocks=C,
+                           flags=flags))
+        ref, m = oracle.sinkhorn_lse(x, y, g, eps)
+        err = lse_err(out[:, 0], ref, m)
+        assert err <= LSE_TOL, (C, err)
+
+
 def test_fast_path_deterministic(ctx):
     from paper_2004_11127_amd import kred
     F = kred.FLAG_FAST
