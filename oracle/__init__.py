@@ -11,7 +11,7 @@ marshals arguments.  What each routine computes follows Charlier et al.,
 "Kernel Operations on the GPU, with Autodiff, without Memory Overflows"
 (arXiv:2004.11127): Eq. (1) (Gaussian kernel sum), Eq. (2) with the
 reductions of Sec. 2 (sum, log-sum-exp, arg-K-min), and the x-gradient of
-Eq. (1) (Sec. 2, "Backpropagation").  The C file's header lists the readings
+Eq. (1) and its vector-Jacobian products (Sec. 2, "Backpropagation").  The C file's header lists the readings
 taken where the paper is silent.
 """
 from __future__ import annotations
@@ -59,6 +59,9 @@ def _load():
             lib.oracle_gauss_gradx.argtypes = [ctypes.c_double, ctypes.c_int64, ctypes.c_int64,
                                                ctypes.c_int, _dp, _dp, _dp, _i64p,
                                                ctypes.c_int64, _dp, _dp]
+            lib.oracle_gauss_vjp.argtypes = [ctypes.c_double, ctypes.c_int64, ctypes.c_int64,
+                                             ctypes.c_int, ctypes.c_int, _dp, _dp, _dp, _dp,
+                                             _i64p, ctypes.c_int64, _dp, _dp]
             lib.oracle_sinkhorn_lse.argtypes = [ctypes.c_double, ctypes.c_int64, ctypes.c_int64,
                                                 ctypes.c_int, _dp, _dp, _dp, _i64p,
                                                 ctypes.c_int64, _dp, _dp]
@@ -66,8 +69,8 @@ def _load():
                                            ctypes.c_int, _dp, _dp, _i64p, ctypes.c_int64,
                                            _i64p, _dp]
             lib.oracle_num_threads.restype = ctypes.c_int
-            for f in (lib.oracle_kernel_sum, lib.oracle_gauss_gradx, lib.oracle_sinkhorn_lse,
-                      lib.oracle_argkmin):
+            for f in (lib.oracle_kernel_sum, lib.oracle_gauss_gradx, lib.oracle_gauss_vjp,
+                      lib.oracle_sinkhorn_lse, lib.oracle_argkmin):
                 f.restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -136,6 +139,29 @@ def gauss_gradx(x, y, b, sigma, rows=None):
     out = np.empty((nr, 1 + D)); norm = np.empty((nr, 1 + D))
     _check(_load().oracle_gauss_gradx(float(sigma), M, N, D, _ptr(x), _ptr(y), _ptr(b),
                                       _ptr(r, _i64p), nr, _ptr(out), _ptr(norm)))
+    return out, norm
+
+
+def gauss_vjp(x, y, b, e, sigma, rows=None):
+    """Vector-Jacobian product of the Gaussian sum a = K b (E columns) in x.
+
+    For a cotangent e (M x E) of a: g_i = sum_j k_ij <e_i, b_j> (y_j - x_i) / sigma^2,
+    the gradient of L = sum_i <e_i, a_i> in x_i.  The y-gradient is
+    gauss_vjp(y, x, e, b, sigma); the b-gradient is kernel_sum("gauss", y, x, e).
+    Returns (g, norm), each (nrows, D); norm sums the absolute summands.
+    """
+    x = _f64(x); y = _f64(y)
+    M, D = x.shape
+    N = y.shape[0]
+    b = np.asarray(b, dtype=np.float64)
+    E = b.shape[1] if b.ndim == 2 else 1
+    b = _f64(b, E); e = _f64(e, E)
+    if e.shape[0] != M or b.shape[0] != N:
+        raise ValueError("e must be M x E and b N x E")
+    r, nr = _rows(rows, M)
+    out = np.empty((nr, D)); norm = np.empty((nr, D))
+    _check(_load().oracle_gauss_vjp(float(sigma), M, N, D, E, _ptr(x), _ptr(y), _ptr(b),
+                                    _ptr(e), _ptr(r, _i64p), nr, _ptr(out), _ptr(norm)))
     return out, norm
 
 

@@ -12,7 +12,8 @@
  *   - Eq. (2), Sec. 2: a_i = Reduction_{j=1..N} F(p, x_i, y_j) for a formula F
  *     and a reduction among those Sec. 2 lists (sum, log-sum-exp, arg-K-min);
  *   - Sec. 2 "Backpropagation": the gradient of a reduction is again a
- *     reduction of the same form; here d a_i / d x_i of Eq. (1).
+ *     reduction of the same form; here d a_i / d x_i of Eq. (1), and the
+ *     vector-Jacobian product of Eq. (1) in x for a cotangent of its output.
  *
  * Every routine is the definition written out: a double loop over (i, j) in
  * fp64 with a sequential j loop, libm exp/log/sqrt, no blocking and no
@@ -121,6 +122,46 @@ int oracle_gauss_gradx(double sigma, int64_t M, int64_t N, int D,
         const double term = w * (yj[k] - xi[k]) / s2;
         out[r * W + 1 + k] += term;
         norm[r * W + 1 + k] += fabs(term);
+      }
+    }
+  }
+  (void)M;
+  return 0;
+}
+
+/*
+ * Vector-Jacobian product of the Gaussian kernel sum in x (Sec. 2,
+ * "Backpropagation": the gradient of a reduction is again a reduction of the
+ * form of Eq. (2)).  For the output a_i = sum_j k_ij b_j of Eq. (1) with E
+ * signal columns, k_ij = exp(-|x_i - y_j|^2 / (2 sigma^2)), and a cotangent
+ * e (M x E), the scalar L = sum_i <e_i, a_i> has
+ *   dL/dx_ik = sum_j k_ij <e_i, b_j> (y_jk - x_ik) / sigma^2.
+ * The y-gradient is this same reduction with the roles of (x, e) and (y, b)
+ * exchanged; dL/db_j = sum_i k_ij e_i is the Gaussian sum with x and y
+ * exchanged.  norm holds the sums of absolute values of the summands.
+ * out and norm: nrows x D.
+ */
+int oracle_gauss_vjp(double sigma, int64_t M, int64_t N, int D, int E,
+                     const double* x, const double* y, const double* b, const double* e,
+                     const int64_t* rows, int64_t nrows, double* out, double* norm) {
+  if (D < 1 || E < 1 || nrows < 0 || !(sigma > 0.0)) return -1;
+  const double s2 = sigma * sigma;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int64_t r = 0; r < nrows; ++r) {
+    const int64_t i = row_of(rows, r);
+    const double* xi = x + i * D;
+    const double* ei = e + i * E;
+    for (int k = 0; k < D; ++k) { out[r * D + k] = 0.0; norm[r * D + k] = 0.0; }
+    for (int64_t j = 0; j < N; ++j) {
+      const double* yj = y + j * D;
+      const double* bj = b + j * E;
+      double dot = 0.0;
+      for (int c = 0; c < E; ++c) dot += ei[c] * bj[c];
+      const double w = exp(-sq_dist(xi, yj, D) / (2.0 * s2)) * dot;
+      for (int k = 0; k < D; ++k) {
+        const double term = w * (yj[k] - xi[k]) / s2;
+        out[r * D + k] += term;
+        norm[r * D + k] += fabs(term);
       }
     }
   }

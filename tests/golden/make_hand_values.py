@@ -34,6 +34,11 @@ VALUES = {
         "b": [[2]], "sigma": 2.0,
         "closed_form": "a = 2 exp(-5/8); g = a (y - x) / sigma^2 = a (1, 2, 0) / 4",
         "value": [2 * E(-5 / 8), 2 * E(-5 / 8) / 4, 2 * E(-5 / 8) * 2 / 4, 0.0]},
+    "vjp_two_point": {
+        "cite": "Sec. 2 (Backpropagation): d/dx_i of L = sum_i <e_i, a_i>, a_i from Eq. (1) with E = 2",
+        "x": [[0, 0]], "y": [[1, 0], [0, 2]], "b": [[1, 2], [-1, 0]], "e": [[3, 1]], "sigma": 1.0,
+        "closed_form": "<e, b_0> = 5, <e, b_1> = -3; g = 5 exp(-1/2) (1, 0) - 3 exp(-2) (0, 2)",
+        "value": [5 * E(-0.5), -6 * E(-2.0)]},
     "lse_two_point": {
         "cite": "Eq. (2) with the log-sum-exp reduction of Sec. 2, F = g_j - |x-y|^2/eps",
         "x": [[0, 0]], "y": [[0, 0], [1, 1]], "g": [[0], [2]], "eps": 1.0,

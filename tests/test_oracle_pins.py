@@ -37,6 +37,8 @@ def test_golden_file_matches_its_closed_forms(hv):
     assert hv["gauss_two_point_scaled"]["value"] == pytest.approx(3 - math.exp(-2), rel=1e-15)
     assert hv["laplace_two_point"]["value"] == pytest.approx(1 + 2 * math.exp(-1), rel=1e-15)
     assert hv["lse_two_point"]["value"] == pytest.approx(math.log(2), rel=1e-15)
+    assert hv["vjp_two_point"]["value"] == pytest.approx([5 * math.exp(-0.5), -6 * math.exp(-2)],
+                                                         rel=1e-15)
 
 
 @pytest.mark.parametrize("key,formula", [("gauss_two_point", "gauss"),
@@ -194,6 +196,73 @@ def test_gradx_matches_finite_differences(oracle_mod, sigma, D):
         am, _ = oracle_mod.kernel_sum("gauss", xm, y, b, sigma=sigma)
         fd = (ap[:, 0] - am[:, 0]) / (2 * h)
         np.testing.assert_allclose(out[:, 1 + k], fd, rtol=1e-6, atol=1e-7 * norm[:, 1 + k].max())
+
+
+def test_vjp_hand_value(oracle_mod, hv):
+    c = hv["vjp_two_point"]
+    g, norm = oracle_mod.gauss_vjp(_a(c["x"]), _a(c["y"]), _a(c["b"]), _a(c["e"]), c["sigma"])
+    np.testing.assert_allclose(g[0], c["value"], rtol=1e-14, atol=1e-15)
+
+
+def _loss(oracle_mod, x, y, b, e, sigma):
+    # L = sum_i <e_i, a_i> with a from the oracle's Gaussian sum
+    a, _ = oracle_mod.kernel_sum("gauss", x, y, b, sigma=sigma)
+    return float((a * e).sum())
+
+
+@pytest.mark.parametrize("sigma,D,E", [(0.3, 3, 1), (0.2, 2, 4), (1.1, 5, 3)])
+def test_vjp_matches_finite_differences(oracle_mod, sigma, D, E):
+    # x-gradient, y-gradient (the same routine with the roles exchanged) and
+    # b-gradient (the Gaussian sum with x and y exchanged) of L = sum_i <e_i, a_i>,
+    # against central differences of L in fp64.
+    rng = np.random.default_rng(9 + D + E)
+    M, N = 5, 23
+    x = rng.uniform(0, 1, (M, D)) * (4 * sigma); y = rng.uniform(0, 1, (N, D)) * (4 * sigma)
+    b = rng.normal(size=(N, E)); e = rng.normal(size=(M, E))
+    gx, nx = oracle_mod.gauss_vjp(x, y, b, e, sigma)
+    gy, ny = oracle_mod.gauss_vjp(y, x, e, b, sigma)
+    gb, _ = oracle_mod.kernel_sum("gauss", y, x, e, sigma=sigma)
+    h = 1e-5 * sigma
+    for (var, grad, scale) in (("x", gx, nx.max()), ("y", gy, ny.max())):
+        base = x if var == "x" else y
+        for i in range(base.shape[0]):
+            for k in range(D):
+                p = base.copy(); p[i, k] += h
+                m = base.copy(); m[i, k] -= h
+                if var == "x":
+                    fd = (_loss(oracle_mod, p, y, b, e, sigma) - _loss(oracle_mod, m, y, b, e, sigma)) / (2 * h)
+                else:
+                    fd = (_loss(oracle_mod, x, p, b, e, sigma) - _loss(oracle_mod, x, m, b, e, sigma)) / (2 * h)
+                assert grad[i, k] == pytest.approx(fd, rel=1e-6, abs=1e-7 * scale)
+    for j in range(N):
+        for c in range(E):
+            p = b.copy(); p[j, c] += 1.0
+            fd = _loss(oracle_mod, x, y, p, e, sigma) - _loss(oracle_mod, x, y, b, e, sigma)   # linear in b
+            assert gb[j, c] == pytest.approx(fd, rel=1e-10, abs=1e-12)
+
+
+def test_vjp_unit_cotangent_is_gradx(oracle_mod):
+    # E = 1 and e = 1: the product is the x-gradient the fused routine returns
+    rng = np.random.default_rng(10)
+    x = rng.uniform(0, 1, (9, 3)); y = rng.uniform(0, 1, (31, 3)); b = rng.normal(size=(31, 1))
+    g, n = oracle_mod.gauss_vjp(x, y, b, np.ones((9, 1)), 0.25)
+    out, norm = oracle_mod.gauss_gradx(x, y, b, 0.25)
+    np.testing.assert_allclose(g, out[:, 1:], rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(n, norm[:, 1:], rtol=1e-13)
+
+
+def test_vjp_linear_in_cotangent_and_signal(oracle_mod):
+    rng = np.random.default_rng(11)
+    x = rng.uniform(0, 1, (7, 2)); y = rng.uniform(0, 1, (19, 2))
+    b = rng.normal(size=(19, 3)); e1 = rng.normal(size=(7, 3)); e2 = rng.normal(size=(7, 3))
+    g1, _ = oracle_mod.gauss_vjp(x, y, b, e1, 0.4)
+    g2, _ = oracle_mod.gauss_vjp(x, y, b, e2, 0.4)
+    g12, _ = oracle_mod.gauss_vjp(x, y, b, e1 - 2 * e2, 0.4)
+    np.testing.assert_allclose(g12, g1 - 2 * g2, rtol=1e-12, atol=1e-14)
+    # <e_i, b_j> is symmetric in the two operands' roles only through the dot product:
+    # swapping the columns of both e and b together leaves g unchanged
+    gp, _ = oracle_mod.gauss_vjp(x, y, b[:, ::-1], e1[:, ::-1], 0.4)
+    np.testing.assert_allclose(gp, g1, rtol=1e-13, atol=1e-15)
 
 
 # ---------------------------------------------------------------------- log-sum-exp
