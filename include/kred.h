@@ -153,6 +153,42 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
                            int64_t M, int64_t N, int32_t D, int32_t E);
 
 /*
+ * Gradients of the Gaussian kernel sum (Sec. 2 "Backpropagation": the
+ * derivative of a reduction of the form of Eq. (2) is again such a
+ * reduction).  For a = K b with a_i = sum_j k_ij b_j, k_ij = exp(-|x_i - y_j|^2
+ * / (2 sigma^2)), b N x E (Eq. (1) with E signal columns), and a cotangent e
+ * (M x E, the gradient of a scalar loss with respect to a), this computes the
+ * gradients of L = sum_i <e_i, a_i>:
+ *   gx (M x D):  gx[i] = sum_j k_ij <e_i, b_j> (y_j - x_i) / sigma^2
+ *   gy (N x D):  gy[j] = sum_i k_ij <e_i, b_j> (x_i - y_j) / sigma^2
+ *   gb (N x E):  gb[j] = sum_i k_ij e_i
+ * Each output pointer may be NULL, and that gradient is not computed.  gy is
+ * the gx reduction with the roles of (x, e) and (y, b) exchanged, and gb the
+ * Gaussian sum with x and y exchanged; all three run on the same kernels as
+ * kred_run, one after the other on `stream`.  Outputs are fp32, dense,
+ * row-major device arrays owned by the caller.
+ *
+ * Parameters: p->sigma (> 0, finite), p->col_blocks and p->flags as for
+ * kred_run (KRED_FLAG_DIRECT / KRED_FLAG_FAST steer the path of every
+ * reduction in the call; KRED_FLAG_PROFILE times each main kernel); p->eps
+ * and p->K are ignored.  Ranges: 0 <= M, N <= 2^31 - 1, 1 <= D <= 16 (larger
+ * D returns KRED_ERR_UNSUPPORTED), 1 <= E <= KRED_MAX_E.  With M = 0 or N = 0
+ * the requested outputs are filled with zeros.  x, y and e are required, and
+ * b too for gx or gy, whenever M, N > 0 and an output is requested.  Same
+ * error and asynchrony rules as kred_run: on any argument error nothing runs.
+ */
+kred_status kred_gauss_backward(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N,
+                                int32_t D, int32_t E, const float* x, const float* y,
+                                const float* b, const float* e, float* gx, float* gy, float* gb,
+                                void* stream);
+
+/* Host-only argument check of kred_gauss_backward (no device, no dereference). */
+kred_status kred_validate_backward(const kred_params* p, int64_t M, int64_t N, int32_t D,
+                                   int32_t E, const void* x, const void* y, const void* b,
+                                   const void* e, const void* gx, const void* gy,
+                                   const void* gb);
+
+/*
  * With KRED_FLAG_PROFILE set on calls, the context records a HIP event pair
  * around the main reduction kernel of each call.  This waits for those
  * events, returns the number of timed launches in *count and their summed

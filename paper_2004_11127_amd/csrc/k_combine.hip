@@ -3,7 +3,8 @@
 // reduction of Eq. (2) over one block of columns; this pass applies the same
 // reduction across blocks, in increasing block order (fixed, so results are
 // reproducible run to run):
-//   sum:          a = sum_c a_c
+//   sum:          a = sum_c a_c  (also the x-gradient sums of the Gaussian
+//                 vector-Jacobian product, scaled by -1/sigma^2)
 //   log-sum-exp:  (m, s) = (max_c m_c, sum_c s_c 2^(m_c - m)),  a = (m + log2 s) ln 2
 //   arg-K-min:    merge the C sorted (distance, index) lists, keep the K first.
 // The second pass reads C x M x W floats once; it is HBM-bound.
@@ -37,6 +38,21 @@ __global__ __launch_bounds__(256) void combine_gradx_kernel(CombineArgs a) {
     float s = 0.0f;
     for (int c = 0; c < a.C; ++c) s += a.part[((int64_t)c * a.M + row) * W + w];
     static_cast<float*>(a.out)[t] = (w == 0) ? s : -s * a.gscale;
+  }
+}
+
+// vector-Jacobian product in x: partials are the DP sums G_k; out = -G * gscale
+__global__ __launch_bounds__(256) void combine_vjp_kernel(CombineArgs a) {
+  const int64_t total = a.M * a.D;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = t / a.D;
+    const int k = (int)(t - row * a.D);
+    float s = 0.0f;
+    for (int c = 0; c < a.C; ++c) s += a.part[((int64_t)c * a.M + row) * a.DP + k];
+    float* o = static_cast<float*>(a.out) + t;
+    const float v = -s * a.gscale;
+    *o = a.accumulate ? *o + v : v;
   }
 }
 
@@ -122,6 +138,9 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
       break;
     case F_SINKHORN:
       hipLaunchKernelGGL(combine_lse_kernel, dim3(grid_for(a.M)), dim3(256), 0, s, a);
+      break;
+    case F_VJP:
+      hipLaunchKernelGGL(combine_vjp_kernel, dim3(grid_for(a.M * a.D)), dim3(256), 0, s, a);
       break;
     default:
       hipLaunchKernelGGL(combine_sum_kernel, dim3(grid_for(a.M * a.EP)), dim3(256), 0, s, a);

@@ -345,6 +345,98 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
   }
 }
 
+// ------------------------- Gaussian sum: vector-Jacobian product in x
+// For a cotangent e_i of a_i = sum_j k_ij b_j (E signal columns):
+// w = 2^(-ks d) <e_i, b_j>,  G_k += w (x_k - y_k);  the x-gradient of
+// L = sum_i <e_i, a_i> is -G * gscale.  Rows hold x_i and this E-slice of
+// e_i; columns hold (y_j, the same E-slice of b_j), packed as for the sums.
+// The product is linear in <e_i, b_j>, so E-slices after the first add to
+// the output.
+template <int DP, int EP, int R>
+__global__ __launch_bounds__(kThreads) void vjp_kernel(DirectArgs a) {
+  constexpr int S = DP + EP;
+  __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  const Item it = item_of(a);
+  float xr[R][DP];
+  load_rows<DP, R>(a, it.rb, xr);
+  float er[R][EP];
+  const int Ec = min(EP, a.E - a.e0);
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t row = row_of<R>(it.rb, r, threadIdx.x);
+    const bool ok = row < a.M;
+#pragma unroll
+    for (int e = 0; e < EP; ++e) er[r][e] = (ok && e < Ec) ? a.xe[row * a.E + a.e0 + e] : 0.0f;
+  }
+  float tot[R][DP], part[R][DP];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int k = 0; k < DP; ++k) tot[r][k] = part[r][k] = 0.0f;
+
+  stream_columns<S>(
+      a.ypk, it.j0, it.j1, 0, lds,
+      [&](const float* yv, int64_t) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          float t[DP];
+          float d = 0.0f;
+#pragma unroll
+          for (int k = 0; k < DP; ++k) {
+            t[k] = xr[r][k] - yv[k];
+            d = (k == 0) ? t[0] * t[0] : __builtin_fmaf(t[k], t[k], d);
+          }
+          float dot = er[r][0] * yv[DP];
+#pragma unroll
+          for (int e = 1; e < EP; ++e) dot = __builtin_fmaf(er[r][e], yv[DP + e], dot);
+          const float w = fast_exp2(-(a.kscale * d)) * dot;
+#pragma unroll
+          for (int k = 0; k < DP; ++k) part[r][k] = __builtin_fmaf(w, t[k], part[r][k]);
+        }
+      },
+      [&]() {
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+          for (int k = 0; k < DP; ++k) {
+            tot[r][k] += part[r][k];
+            part[r][k] = 0.0f;
+          }
+      });
+
+  const int tid_out = opaque_tid();
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t row = row_of<R>(it.rb, r, tid_out);
+    if (row >= a.M) continue;
+    if (a.C == 1) {
+      float* o = static_cast<float*>(a.out) + row * a.D;
+#pragma unroll
+      for (int k = 0; k < DP; ++k)
+        if (k < a.D) {
+          const float v = -tot[r][k] * a.gscale;
+          o[k] = a.accumulate ? o[k] + v : v;
+        }
+    } else {
+      float* p = a.part + ((int64_t)it.c * a.M + row) * DP;
+#pragma unroll
+      for (int k = 0; k < DP; ++k) p[k] = tot[r][k];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void scale_rows_kernel(const float* __restrict__ src, int64_t M,
+                                                         int D, const float* __restrict__ e,
+                                                         float* __restrict__ dst) {
+  const int64_t total = M * D;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = t / D;
+    const int k = (int)(t - i * D);
+    dst[t] = e[i] * src[i * (1 + D) + 1 + k];
+  }
+}
+
 // ------------------------------------------------ Sinkhorn log-sum-exp
 // In log2 units: s_ij = g'_j - ks d_ij with g' = g log2(e), ks = log2(e) / eps.
 // Running reference m_i (<= max_j s_ij + kRescale): terms are 2^(s - m);
@@ -505,6 +597,7 @@ constexpr int pow2_floor(int v) { return v >= 8 ? 8 : v >= 4 ? 4 : v >= 2 ? 2 : 
 
 constexpr int rows_for(int formula, int DP, int EP, int KP) {
   const int state = formula == F_GRADX      ? DP + 2 * (DP + 1)
+                    : formula == F_VJP      ? DP + EP + 2 * DP
                     : formula == F_SINKHORN ? DP + 3
                     : KP > 0                ? DP + 2 * KP
                                             : DP + 2 * EP;
@@ -556,6 +649,18 @@ hipError_t launch_dp(const DirectArgs& a, dim3 grid, hipStream_t s) {
       hipLaunchKernelGGL((lse_kernel<DP, rows_for(F_SINKHORN, DP, 1, 0)>), grid, dim3(kThreads),
                          0, s, a);
       return hipGetLastError();
+    case F_VJP:
+      switch (a.EP) {
+#define KRED_VJP(EPV)                                                                           \
+  case EPV:                                                                                    \
+    hipLaunchKernelGGL((vjp_kernel<DP, EPV, rows_for(F_VJP, DP, EPV, 0)>), grid, dim3(kThreads), \
+                       0, s, a);                                                               \
+    return hipGetLastError();
+        KRED_VJP(1) KRED_VJP(4) KRED_VJP(16)
+#undef KRED_VJP
+        default:
+          return hipErrorInvalidValue;
+      }
     default:
       switch (a.EP) {
         case 1: return launch_sum_e<DP, 1>(a, grid, s);
@@ -586,6 +691,7 @@ int direct_rows_per_thread(int formula, int DP, int EP, int KP) {
 int partial_width(int formula, int DP, int EP, int KP) {
   if (KP > 0) return 2 * KP;
   if (formula == F_GRADX) return DP + 1;
+  if (formula == F_VJP) return DP;
   if (formula == F_SINKHORN) return 2;
   return EP;
 }
@@ -595,6 +701,15 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
   if (total == 0) return hipSuccess;
   const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
   hipLaunchKernelGGL(pack_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_scale_rows(const float* src, int64_t M, int D, const float* e, float* dst,
+                             hipStream_t s) {
+  const int64_t total = M * D;
+  if (total == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(scale_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, s, src, M, D, e, dst);
   return hipGetLastError();
 }
 

@@ -19,6 +19,8 @@ struct kred_ctx {
   int num_cus = 256;
   void* scratch = nullptr;
   size_t scratch_bytes = 0;
+  void* aux = nullptr;       // backward: the fused value + gradient of the scalar-cotangent route
+  size_t aux_bytes = 0;
   // KRED_FLAG_PROFILE: event pairs around main kernels, reused across collects
   std::vector<hipEvent_t> ev;
   size_t ev_used = 0;
@@ -105,9 +107,10 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
   q.gscale = 0.0f;
   q.kscale = 1.0f;
   q.fscale = 1.0f;
-  switch (f) {
+  switch ((int)f) {
     case KRED_F_GAUSS:
-    case KRED_F_GAUSS_GRADX: {
+    case KRED_F_GAUSS_GRADX:
+    case F_VJP: {
       const double s = (double)p->sigma;
       const double c = log2e / (2.0 * s * s);
       q.kscale = (float)c;
@@ -227,22 +230,28 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   return true;
 }
 
-kred_status grow_scratch(kred_ctx* ctx, size_t bytes) {
-  if (bytes <= ctx->scratch_bytes) return KRED_OK;
-  const size_t want = std::max(bytes, ctx->scratch_bytes * 5 / 4);
-  if (ctx->scratch) {
+// Grow a context buffer; the old one may still be in use by queued kernels,
+// so the device is synchronised before it is freed.
+kred_status grow_buffer(void** buf, size_t* have, size_t bytes) {
+  if (bytes <= *have) return KRED_OK;
+  const size_t want = std::max(bytes, *have * 5 / 4);
+  if (*buf) {
     if (hipDeviceSynchronize() != hipSuccess) return KRED_ERR_HIP;
-    (void)hipFree(ctx->scratch);
-    ctx->scratch = nullptr;
-    ctx->scratch_bytes = 0;
+    (void)hipFree(*buf);
+    *buf = nullptr;
+    *have = 0;
   }
-  if (hipMalloc(&ctx->scratch, want) != hipSuccess) {
+  if (hipMalloc(buf, want) != hipSuccess) {
     (void)hipGetLastError();
-    ctx->scratch = nullptr;
+    *buf = nullptr;
     return KRED_ERR_NOMEM;
   }
-  ctx->scratch_bytes = want;
+  *have = want;
   return KRED_OK;
+}
+
+kred_status grow_scratch(kred_ctx* ctx, size_t bytes) {
+  return grow_buffer(&ctx->scratch, &ctx->scratch_bytes, bytes);
 }
 
 struct DeviceGuard {
@@ -356,125 +365,10 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   return KRED_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char* kred_strerror(kred_status s) {
-  switch (s) {
-    case KRED_OK: return "success";
-    case KRED_ERR_INVALID_ARG: return "invalid argument";
-    case KRED_ERR_UNSUPPORTED: return "unsupported formula/reduction/size combination";
-    case KRED_ERR_NOMEM: return "out of device memory for scratch";
-    case KRED_ERR_HIP: return "HIP runtime error";
-    case KRED_ERR_NO_DEVICE: return "no usable gfx950 device";
-  }
-  return "unknown status";
-}
-
-int32_t kred_version(void) { return KRED_VERSION; }
-
-kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p, int64_t M,
-                          int64_t N, int32_t D, int32_t E, const void* x, const void* y,
-                          const void* b, const void* out) {
-  if (p == nullptr) return KRED_ERR_INVALID_ARG;
-  if ((int)f < KRED_F_GAUSS || (int)f > KRED_F_SINKHORN) return KRED_ERR_INVALID_ARG;
-  if ((int)r < KRED_R_SUM || (int)r > KRED_R_ARGKMIN) return KRED_ERR_INVALID_ARG;
-  if (M < 0 || N < 0 || M > INT32_MAX || N > INT32_MAX) return KRED_ERR_INVALID_ARG;
-  if (D < 1 || D > KRED_MAX_D) return KRED_ERR_INVALID_ARG;
-  if (p->col_blocks < 0 || p->col_blocks > KRED_MAX_COL_BLOCKS) return KRED_ERR_INVALID_ARG;
-  bool needs_b = true;
-  if (r == KRED_R_SUM && (f == KRED_F_GAUSS || f == KRED_F_LAPLACE || f == KRED_F_SQDIST)) {
-    if (E < 1 || E > KRED_MAX_E) return KRED_ERR_INVALID_ARG;
-    if (f != KRED_F_SQDIST && !finite_pos(p->sigma)) return KRED_ERR_INVALID_ARG;
-  } else if (r == KRED_R_SUM && f == KRED_F_GAUSS_GRADX) {
-    if (E != 1) return KRED_ERR_INVALID_ARG;
-    if (!finite_pos(p->sigma)) return KRED_ERR_INVALID_ARG;
-  } else if (r == KRED_R_LSE && f == KRED_F_SINKHORN) {
-    if (E != 1) return KRED_ERR_INVALID_ARG;
-    if (!finite_pos(p->eps)) return KRED_ERR_INVALID_ARG;
-  } else if (r == KRED_R_ARGKMIN && f == KRED_F_SQDIST) {
-    if (b != nullptr) return KRED_ERR_INVALID_ARG;
-    if (p->K < 1 || p->K > KRED_MAX_K || p->K > N) return KRED_ERR_INVALID_ARG;
-    needs_b = false;
-  } else {
-    return KRED_ERR_UNSUPPORTED;
-  }
-  // Paths: the direct-form kernels cover D <= 16 for every pair; the
-  // matrix-core kernels cover 16 < D <= 256 for the sums and arg-K-min.
-  if (D > kMaxDirectD && (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN))
-    return KRED_ERR_UNSUPPORTED;
-  if (M == 0) return KRED_OK;
-  if (x == nullptr || out == nullptr) return KRED_ERR_INVALID_ARG;
-  if (N > 0 && (y == nullptr || (needs_b && b == nullptr))) return KRED_ERR_INVALID_ARG;
-  if (misaligned(x) || misaligned(y) || misaligned(b) || misaligned(out))
-    return KRED_ERR_INVALID_ARG;
-  return KRED_OK;
-}
-
-int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* p, int64_t M,
-                           int64_t N, int32_t D, int32_t E) {
-  const float dummy = 0.0f;
-  const void* bp = (r == KRED_R_ARGKMIN) ? nullptr : &dummy;
-  if (kred_validate(f, r, p, M, N, D, E, &dummy, &dummy, bp, &dummy) != KRED_OK) return -1;
-  if (M == 0 || N == 0) return 0;
-  if (D > kMaxDirectD) {
-    MPlan mp;
-    if (!make_mplan(f, r, p, M, N, D, E, 256, &mp)) return -1;
-    return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes;
-  }
-  const int epi = fast_epi(f, r, M, N, D, E, p->flags);
-  Plan pl;
-  if (!make_plan(f, r, p, M, N, D, E, 256, &pl, epi >= 0 ? fast_rows_per_block(epi) : 0,
-                 epi >= 0 ? 256 : 1))
-    return -1;
-  const FastScratch fs = fast_scratch(epi, N);
-  return pl.pack_bytes + pl.part_bytes + fs.guard_bytes + fs.apk_bytes + fs.ex_bytes;
-}
-
-kred_status kred_create(kred_ctx** ctx, int device) {
-  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
-  *ctx = nullptr;
-  int n = 0;
-  if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n) {
-    (void)hipGetLastError();
-    return KRED_ERR_NO_DEVICE;
-  }
-  hipDeviceProp_t prop;
-  if (hipGetDeviceProperties(&prop, device) != hipSuccess) return KRED_ERR_NO_DEVICE;
-  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) return KRED_ERR_NO_DEVICE;
-  kred_ctx* c = new (std::nothrow) kred_ctx();
-  if (c == nullptr) return KRED_ERR_NOMEM;
-  c->device = device;
-  c->num_cus = prop.multiProcessorCount;
-  *ctx = c;
-  return KRED_OK;
-}
-
-kred_status kred_destroy(kred_ctx* ctx) {
-  if (ctx == nullptr) return KRED_OK;
-  kred_status st = KRED_OK;
-  {
-    DeviceGuard g(ctx->device);
-    if (hipDeviceSynchronize() != hipSuccess) st = KRED_ERR_HIP;
-    if (ctx->scratch) (void)hipFree(ctx->scratch);
-    for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
-  }
-  delete ctx;
-  return st;
-}
-
-kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
-                     int64_t M, int64_t N, int32_t D, int32_t E, const float* x, const float* y,
-                     const float* b, void* out, void* stream) {
-  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
-  const kred_status v = kred_validate(f, r, p, M, N, D, E, x, y, b, out);
-  if (v != KRED_OK) return v;
-  if (M == 0) return KRED_OK;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  DeviceGuard devg(ctx->device);
-  if (!devg.ok) return KRED_ERR_HIP;
-
+// One reduction on validated arguments, M > 0, on the current device.
+kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
+                          int64_t M, int64_t N, int32_t D, int32_t E, const float* x,
+                          const float* y, const float* b, void* out, hipStream_t s) {
   if (N == 0) {
     int64_t count = M;
     float value = 0.0f;
@@ -614,6 +508,275 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
       ca.K = pl.K;
       if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
     }
+  }
+  return KRED_OK;
+}
+
+// x-gradient of L = sum_i <e_i, a_i> for the Gaussian sum a = K b (D <= 16),
+// on validated arguments with M, N > 0.  With one signal column and the
+// matrix-core path eligible, the fused value + gradient reduction runs and its
+// gradient is scaled by the scalar cotangent; otherwise the direct-form
+// vector-Jacobian kernel runs once per E-slice of 16.
+kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, int32_t D,
+                    int32_t E, const float* x, const float* y, const float* b, const float* e,
+                    float* g, hipStream_t s) {
+  if (E == 1 && fast_epi(KRED_F_GAUSS_GRADX, KRED_R_SUM, M, N, D, 1, p->flags) >= 0) {
+    const kred_status ga =
+        grow_buffer(&ctx->aux, &ctx->aux_bytes, (size_t)(M * (1 + D) * (int64_t)sizeof(float)));
+    if (ga != KRED_OK) return ga;
+    float* fused = static_cast<float*>(ctx->aux);
+    const kred_status st =
+        run_reduction(ctx, KRED_F_GAUSS_GRADX, KRED_R_SUM, p, M, N, D, 1, x, y, b, fused, s);
+    if (st != KRED_OK) return st;
+    return launch_scale_rows(fused, M, D, e, g, s) == hipSuccess ? KRED_OK : KRED_ERR_HIP;
+  }
+  Plan pl;
+  if (!make_plan((kred_formula)F_VJP, KRED_R_SUM, p, M, N, D, E, ctx->num_cus, &pl))
+    return KRED_ERR_UNSUPPORTED;
+  const kred_status gs = grow_scratch(ctx, (size_t)(pl.pack_bytes + pl.part_bytes));
+  if (gs != KRED_OK) return gs;
+  char* sbase = static_cast<char*>(ctx->scratch);
+  float* ypk = reinterpret_cast<float*>(sbase);
+  float* part = pl.part_bytes ? reinterpret_cast<float*>(sbase + pl.pack_bytes) : nullptr;
+  const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
+  const int n_slices = (E + 15) / 16;
+  for (int sl = 0; sl < n_slices; ++sl) {
+    const int e0 = sl * 16;
+    const int EP = direct_pad_e(std::min(16, E - e0));
+    PackArgs pa{};
+    pa.y = y;
+    pa.b = b;
+    pa.ypk = ypk;
+    pa.N = N;
+    pa.D = D;
+    pa.DP = pl.DP;
+    pa.E = E;
+    pa.EP = EP;
+    pa.e0 = e0;
+    pa.yscale = 1.0f;
+    pa.bscale = 1.0f;
+    if (launch_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
+
+    DirectArgs da{};
+    da.formula = F_VJP;
+    da.D = D;
+    da.DP = pl.DP;
+    da.E = E;
+    da.EP = EP;
+    da.e0 = e0;
+    da.M = M;
+    da.N = N;
+    da.C = pl.C;
+    da.jpb = pl.jpb;
+    da.x = x;
+    da.ypk = ypk;
+    da.xscale = 1.0f;
+    da.kscale = pl.kscale;
+    da.gscale = pl.gscale;
+    da.out = g;
+    da.part = part;
+    da.xe = e;
+    da.accumulate = sl > 0;
+    hipEvent_t e_start = nullptr, e_stop = nullptr;
+    if (prof) {
+      e_start = next_event(ctx);
+      e_stop = next_event(ctx);
+      if (!e_start || !e_stop || hipEventRecord(e_start, s) != hipSuccess) return KRED_ERR_HIP;
+    }
+    if (launch_direct(da, s) != hipSuccess) return KRED_ERR_HIP;
+    if (prof) {
+      if (hipEventRecord(e_stop, s) != hipSuccess) return KRED_ERR_HIP;
+      ctx->last_kernel = "vjp_kernel";
+    }
+    if (pl.C > 1) {
+      CombineArgs ca{};
+      ca.formula = F_VJP;
+      ca.D = D;
+      ca.DP = pl.DP;
+      ca.E = E;
+      ca.EP = EP;
+      ca.e0 = e0;
+      ca.M = M;
+      ca.C = pl.C;
+      ca.part = part;
+      ca.out = g;
+      ca.gscale = pl.gscale;
+      ca.accumulate = sl > 0;
+      if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
+    }
+  }
+  return KRED_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* kred_strerror(kred_status s) {
+  switch (s) {
+    case KRED_OK: return "success";
+    case KRED_ERR_INVALID_ARG: return "invalid argument";
+    case KRED_ERR_UNSUPPORTED: return "unsupported formula/reduction/size combination";
+    case KRED_ERR_NOMEM: return "out of device memory for scratch";
+    case KRED_ERR_HIP: return "HIP runtime error";
+    case KRED_ERR_NO_DEVICE: return "no usable gfx950 device";
+  }
+  return "unknown status";
+}
+
+int32_t kred_version(void) { return KRED_VERSION; }
+
+kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p, int64_t M,
+                          int64_t N, int32_t D, int32_t E, const void* x, const void* y,
+                          const void* b, const void* out) {
+  if (p == nullptr) return KRED_ERR_INVALID_ARG;
+  if ((int)f < KRED_F_GAUSS || (int)f > KRED_F_SINKHORN) return KRED_ERR_INVALID_ARG;
+  if ((int)r < KRED_R_SUM || (int)r > KRED_R_ARGKMIN) return KRED_ERR_INVALID_ARG;
+  if (M < 0 || N < 0 || M > INT32_MAX || N > INT32_MAX) return KRED_ERR_INVALID_ARG;
+  if (D < 1 || D > KRED_MAX_D) return KRED_ERR_INVALID_ARG;
+  if (p->col_blocks < 0 || p->col_blocks > KRED_MAX_COL_BLOCKS) return KRED_ERR_INVALID_ARG;
+  bool needs_b = true;
+  if (r == KRED_R_SUM && (f == KRED_F_GAUSS || f == KRED_F_LAPLACE || f == KRED_F_SQDIST)) {
+    if (E < 1 || E > KRED_MAX_E) return KRED_ERR_INVALID_ARG;
+    if (f != KRED_F_SQDIST && !finite_pos(p->sigma)) return KRED_ERR_INVALID_ARG;
+  } else if (r == KRED_R_SUM && f == KRED_F_GAUSS_GRADX) {
+    if (E != 1) return KRED_ERR_INVALID_ARG;
+    if (!finite_pos(p->sigma)) return KRED_ERR_INVALID_ARG;
+  } else if (r == KRED_R_LSE && f == KRED_F_SINKHORN) {
+    if (E != 1) return KRED_ERR_INVALID_ARG;
+    if (!finite_pos(p->eps)) return KRED_ERR_INVALID_ARG;
+  } else if (r == KRED_R_ARGKMIN && f == KRED_F_SQDIST) {
+    if (b != nullptr) return KRED_ERR_INVALID_ARG;
+    if (p->K < 1 || p->K > KRED_MAX_K || p->K > N) return KRED_ERR_INVALID_ARG;
+    needs_b = false;
+  } else {
+    return KRED_ERR_UNSUPPORTED;
+  }
+  // Paths: the direct-form kernels cover D <= 16 for every pair; the
+  // matrix-core kernels cover 16 < D <= 256 for the sums and arg-K-min.
+  if (D > kMaxDirectD && (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN))
+    return KRED_ERR_UNSUPPORTED;
+  if (M == 0) return KRED_OK;
+  if (x == nullptr || out == nullptr) return KRED_ERR_INVALID_ARG;
+  if (N > 0 && (y == nullptr || (needs_b && b == nullptr))) return KRED_ERR_INVALID_ARG;
+  if (misaligned(x) || misaligned(y) || misaligned(b) || misaligned(out))
+    return KRED_ERR_INVALID_ARG;
+  return KRED_OK;
+}
+
+int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* p, int64_t M,
+                           int64_t N, int32_t D, int32_t E) {
+  const float dummy = 0.0f;
+  const void* bp = (r == KRED_R_ARGKMIN) ? nullptr : &dummy;
+  if (kred_validate(f, r, p, M, N, D, E, &dummy, &dummy, bp, &dummy) != KRED_OK) return -1;
+  if (M == 0 || N == 0) return 0;
+  if (D > kMaxDirectD) {
+    MPlan mp;
+    if (!make_mplan(f, r, p, M, N, D, E, 256, &mp)) return -1;
+    return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes;
+  }
+  const int epi = fast_epi(f, r, M, N, D, E, p->flags);
+  Plan pl;
+  if (!make_plan(f, r, p, M, N, D, E, 256, &pl, epi >= 0 ? fast_rows_per_block(epi) : 0,
+                 epi >= 0 ? 256 : 1))
+    return -1;
+  const FastScratch fs = fast_scratch(epi, N);
+  return pl.pack_bytes + pl.part_bytes + fs.guard_bytes + fs.apk_bytes + fs.ex_bytes;
+}
+
+kred_status kred_create(kred_ctx** ctx, int device) {
+  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
+  *ctx = nullptr;
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n) {
+    (void)hipGetLastError();
+    return KRED_ERR_NO_DEVICE;
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, device) != hipSuccess) return KRED_ERR_NO_DEVICE;
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) return KRED_ERR_NO_DEVICE;
+  kred_ctx* c = new (std::nothrow) kred_ctx();
+  if (c == nullptr) return KRED_ERR_NOMEM;
+  c->device = device;
+  c->num_cus = prop.multiProcessorCount;
+  *ctx = c;
+  return KRED_OK;
+}
+
+kred_status kred_destroy(kred_ctx* ctx) {
+  if (ctx == nullptr) return KRED_OK;
+  kred_status st = KRED_OK;
+  {
+    DeviceGuard g(ctx->device);
+    if (hipDeviceSynchronize() != hipSuccess) st = KRED_ERR_HIP;
+    if (ctx->scratch) (void)hipFree(ctx->scratch);
+    if (ctx->aux) (void)hipFree(ctx->aux);
+    for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
+  }
+  delete ctx;
+  return st;
+}
+
+kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
+                     int64_t M, int64_t N, int32_t D, int32_t E, const float* x, const float* y,
+                     const float* b, void* out, void* stream) {
+  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
+  const kred_status v = kred_validate(f, r, p, M, N, D, E, x, y, b, out);
+  if (v != KRED_OK) return v;
+  if (M == 0) return KRED_OK;
+  DeviceGuard devg(ctx->device);
+  if (!devg.ok) return KRED_ERR_HIP;
+  return run_reduction(ctx, f, r, p, M, N, D, E, x, y, b, out, static_cast<hipStream_t>(stream));
+}
+
+kred_status kred_validate_backward(const kred_params* p, int64_t M, int64_t N, int32_t D,
+                                   int32_t E, const void* x, const void* y, const void* b,
+                                   const void* e, const void* gx, const void* gy,
+                                   const void* gb) {
+  if (p == nullptr || !finite_pos(p->sigma)) return KRED_ERR_INVALID_ARG;
+  if (p->col_blocks < 0 || p->col_blocks > KRED_MAX_COL_BLOCKS) return KRED_ERR_INVALID_ARG;
+  if (M < 0 || N < 0 || M > INT32_MAX || N > INT32_MAX) return KRED_ERR_INVALID_ARG;
+  if (D < 1 || D > KRED_MAX_D || E < 1 || E > KRED_MAX_E) return KRED_ERR_INVALID_ARG;
+  if (D > kMaxDirectD) return KRED_ERR_UNSUPPORTED;
+  // Inputs the requested outputs read.  With M = 0 or N = 0 every reduction
+  // is empty and the outputs are filled with zeros without reading any input.
+  if (M > 0 && N > 0 && (gx || gy || gb)) {
+    if (x == nullptr || y == nullptr || e == nullptr) return KRED_ERR_INVALID_ARG;
+    if ((gx || gy) && b == nullptr) return KRED_ERR_INVALID_ARG;
+  }
+  for (const void* q : {x, y, b, e, gx, gy, gb})
+    if (misaligned(q)) return KRED_ERR_INVALID_ARG;
+  return KRED_OK;
+}
+
+kred_status kred_gauss_backward(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N,
+                                int32_t D, int32_t E, const float* x, const float* y,
+                                const float* b, const float* e, float* gx, float* gy, float* gb,
+                                void* stream) {
+  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
+  const kred_status v = kred_validate_backward(p, M, N, D, E, x, y, b, e, gx, gy, gb);
+  if (v != KRED_OK) return v;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  DeviceGuard devg(ctx->device);
+  if (!devg.ok) return KRED_ERR_HIP;
+  kred_status st = KRED_OK;
+  // dL/dx_i: sum over j of k_ij <e_i, b_j> (y_j - x_i) / sigma^2
+  if (gx && M > 0) {
+    st = N == 0 ? (launch_fill(gx, M * D, 0.0f, s) == hipSuccess ? KRED_OK : KRED_ERR_HIP)
+                : run_vjp(ctx, p, M, N, D, E, x, y, b, e, gx, s);
+    if (st != KRED_OK) return st;
+  }
+  // dL/dy_j: the same reduction with the roles of (x, e) and (y, b) exchanged
+  if (gy && N > 0) {
+    st = M == 0 ? (launch_fill(gy, N * D, 0.0f, s) == hipSuccess ? KRED_OK : KRED_ERR_HIP)
+                : run_vjp(ctx, p, N, M, D, E, y, x, e, b, gy, s);
+    if (st != KRED_OK) return st;
+  }
+  // dL/db_j = sum_i k_ij e_i: the Gaussian sum with x and y exchanged
+  if (gb && N > 0) {
+    st = M == 0 ? (launch_fill(gb, N * E, 0.0f, s) == hipSuccess ? KRED_OK : KRED_ERR_HIP)
+                : run_reduction(ctx, KRED_F_GAUSS, KRED_R_SUM, p, N, M, D, E, y, x, e, gb, s);
+    if (st != KRED_OK) return st;
   }
   return KRED_OK;
 }

@@ -6,8 +6,9 @@
 
 namespace kred {
 
-// Formula codes used inside the kernels (same values as the public enum).
-enum : int { F_GAUSS = 0, F_LAPLACE = 1, F_SQDIST = 2, F_GRADX = 3, F_SINKHORN = 4 };
+// Formula codes used inside the kernels (same values as the public enum;
+// F_VJP, the vector-Jacobian product of the Gaussian sum in x, is internal).
+enum : int { F_GAUSS = 0, F_LAPLACE = 1, F_SQDIST = 2, F_GRADX = 3, F_SINKHORN = 4, F_VJP = 5 };
 
 constexpr int kThreads = 256;          // threads per workgroup for the direct-form kernels
 constexpr float kLog2e = 1.4426950408889634f;
@@ -88,6 +89,8 @@ struct DirectArgs {
   float* part;            // partials (C > 1), C x M x W
   int KP, K;              // arg-K-min list length (power of two) and K
   const FastGuard* guard; // non-null: skip when the fast path is selected
+  const float* xe;        // F_VJP: row cotangent e, M x E (this call reads its E-slice)
+  int accumulate;         // F_VJP with C == 1: add to out instead of storing (E-slices after the first)
 };
 hipError_t launch_direct(const DirectArgs& a, hipStream_t s);
 int direct_rows_per_thread(int formula, int DP, int EP, int KP);
@@ -106,8 +109,14 @@ struct CombineArgs {
   void* out;
   float gscale;
   int KP, K;
+  int accumulate;   // F_VJP: add to out instead of storing
 };
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+
+// dst[i, k] = e[i] * src[i, 1 + k] for i < M, k < D (src is M x (1 + D)):
+// the x-gradient of the fused value + gradient reduction times a scalar cotangent.
+hipError_t launch_scale_rows(const float* src, int64_t M, int D, const float* e, float* dst,
+                             hipStream_t s);
 
 // Large-D path (matrix cores).  Prologue: Yop[j][d] = y[j][d] * yop_scale
 // (zero for d >= D), ny[j] = nrm_sign * |y_j * coord_scale|^2 (pad_norm for

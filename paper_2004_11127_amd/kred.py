@@ -60,11 +60,14 @@ def load():
         lib.kred_scratch_bytes.restype = i64
         lib.kred_profile_collect.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double),
                                              ctypes.POINTER(ctypes.c_char_p)]
+        lib.kred_gauss_backward.argtypes = [vp, pp, i64, i64, i32, i32, vp, vp, vp, vp,
+                                            vp, vp, vp, vp]
+        lib.kred_validate_backward.argtypes = [pp, i64, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp]
         lib.kred_strerror.argtypes = [ctypes.c_int]
         lib.kred_strerror.restype = ctypes.c_char_p
         lib.kred_version.restype = i32
         for f in (lib.kred_create, lib.kred_destroy, lib.kred_run, lib.kred_validate,
-                  lib.kred_profile_collect):
+                  lib.kred_gauss_backward, lib.kred_validate_backward, lib.kred_profile_collect):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -105,6 +108,13 @@ def validate(formula, reduction, M, N, D, E, x=16, y=16, b=16, out=16, **params)
     p = make_params(**params)
     return load().kred_validate(f, r, ctypes.byref(p), int(M), int(N), int(D), int(E),
                                 x, y, b, out)
+
+
+def validate_backward(M, N, D, E, x=16, y=16, b=16, e=16, gx=16, gy=16, gb=16, **params):
+    """Host-only argument check of the Gaussian backward (pointers as plain integers)."""
+    p = make_params(**params)
+    return load().kred_validate_backward(ctypes.byref(p), int(M), int(N), int(D), int(E),
+                                         x, y, b, e, gx, gy, gb)
 
 
 def scratch_bytes(formula, reduction, M, N, D, E, **params):
@@ -200,6 +210,47 @@ class Context:
             raise KredError(st, "kred_run(%s, %s, M=%d, N=%d, D=%d, E=%d)" % (formula, reduction,
                                                                              M, N, D, E))
         return out
+
+    def gauss_backward(self, x, y, b, e, sigma=1.0, gx=True, gy=True, gb=True, col_blocks=0,
+                       flags=0, stream=None):
+        """Gradients of L = sum_i <e_i, a_i> for the Gaussian sum a = K b.
+
+        x (M, D), y (N, D), b (N, E), e (M, E): contiguous float32 on the context's
+        GPU.  gx, gy, gb: True (allocate), a preallocated tensor, or False/None
+        (not computed).  Returns the tuple (gx, gy, gb), None where not computed.
+        """
+        import torch
+        M, D = x.shape
+        N = y.shape[0]
+        if y.dim() != 2 or y.shape[1] != D:
+            raise ValueError("y must be (N, D) with the same D as x")
+        b2 = b if b.dim() == 2 else b.reshape(-1, 1)
+        e2 = e if e.dim() == 2 else e.reshape(-1, 1)
+        E = b2.shape[1]
+        if b2.shape[0] != N or tuple(e2.shape) != (M, E):
+            raise ValueError("b must be (N, E) and e (M, E)")
+
+        def want(v, shape):
+            if v is True:
+                return torch.empty(shape, dtype=torch.float32, device=x.device)
+            if v is None or v is False:
+                return None
+            if tuple(v.shape) != shape:
+                raise ValueError("gradient output must have shape %s" % (shape,))
+            return v
+
+        ox, oy, ob = want(gx, (M, D)), want(gy, (N, D)), want(gb, (N, E))
+        p = make_params(sigma, 1.0, 0, col_blocks, flags)
+        s = (stream if stream is not None else torch.cuda.current_stream(x.device)).cuda_stream
+        f32 = torch.float32
+        st = load().kred_gauss_backward(self._h, ctypes.byref(p), M, N, D, E,
+                                        self._dev_ptr(x, "x", f32), self._dev_ptr(y, "y", f32),
+                                        self._dev_ptr(b2, "b", f32), self._dev_ptr(e2, "e", f32),
+                                        self._dev_ptr(ox, "gx", f32), self._dev_ptr(oy, "gy", f32),
+                                        self._dev_ptr(ob, "gb", f32), s)
+        if st != 0:
+            raise KredError(st, "kred_gauss_backward(M=%d, N=%d, D=%d, E=%d)" % (M, N, D, E))
+        return ox, oy, ob
 
     def profile_collect(self):
         """(count, total_ms, kernel) of main kernels timed since the last collect."""

@@ -120,3 +120,49 @@ def test_scratch_is_linear_not_quadratic(lib):
     assert s2 < 1_000_000 * 1_000_000 * 4 / 1000
     assert kred.scratch_bytes("gauss", "sum", 10, 10, 3, 0, sigma=0.1) == -1
     assert kred.scratch_bytes("gauss", "sum", 0, 10, 3, 1, sigma=0.1) == 0
+
+
+# ------------------------------------------------------- Gaussian backward
+
+VB = kred.validate_backward
+
+
+def test_backward_declared_and_null_context(lib):
+    assert {"kred_gauss_backward", "kred_validate_backward"} <= set(kred.header_symbols())
+    p = kred.make_params(sigma=1.0)
+    assert lib.kred_gauss_backward(None, ctypes.byref(p), 4, 4, 3, 1, 16, 16, 16, 16,
+                                   16, 16, 16, None) == INVALID
+
+
+def test_backward_valid_arguments(lib):
+    assert VB(100, 200, 3, 1, sigma=0.1) == OK
+    assert VB(100, 200, 16, 64, sigma=2.0) == OK
+    assert VB(100, 200, 3, 5, gy=None, gb=None, sigma=0.1) == OK     # gx only
+    assert VB(100, 200, 3, 5, gx=None, gy=None, b=None, sigma=0.1) == OK   # gb reads no b
+    assert VB(100, 200, 3, 5, gx=None, gy=None, gb=None, x=None, y=None, b=None, e=None,
+              sigma=0.1) == OK   # nothing requested
+    # empty reductions read no input: the outputs are zero-filled
+    assert VB(0, 200, 3, 2, x=None, y=None, b=None, e=None, sigma=0.1) == OK
+    assert VB(100, 0, 3, 2, x=None, y=None, b=None, e=None, sigma=0.1) == OK
+
+
+def test_backward_invalid_arguments(lib):
+    assert VB(100, 200, 3, 1, sigma=0.0) == INVALID
+    assert VB(100, 200, 3, 1, sigma=float("inf")) == INVALID
+    assert VB(100, 200, 0, 1, sigma=1.0) == INVALID
+    assert VB(100, 200, 3, 0, sigma=1.0) == INVALID
+    assert VB(100, 200, 3, 65, sigma=1.0) == INVALID
+    assert VB(-1, 200, 3, 1, sigma=1.0) == INVALID
+    assert VB(100, 2 ** 31, 3, 1, sigma=1.0) == INVALID
+    assert VB(100, 200, 3, 1, sigma=1.0, col_blocks=257) == INVALID
+    assert VB(100, 200, 3, 1, b=None, sigma=1.0) == INVALID          # gx, gy need b
+    assert VB(100, 200, 3, 1, e=None, sigma=1.0) == INVALID
+    assert VB(100, 200, 3, 1, x=None, gx=None, gy=None, sigma=1.0) == INVALID   # gb needs x
+    assert VB(100, 200, 3, 1, gx=18, sigma=1.0) == INVALID           # misaligned output
+    assert VB(100, 200, 3, 1, e=2, sigma=1.0) == INVALID             # misaligned input
+
+
+def test_backward_large_d_unsupported(lib):
+    assert VB(100, 200, 17, 1, sigma=1.0) == UNSUPPORTED
+    assert VB(100, 200, 256, 1, sigma=1.0) == UNSUPPORTED
+    assert VB(100, 200, 257, 1, sigma=1.0) == INVALID
