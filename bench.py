@@ -6,13 +6,16 @@ hot path: the packing prologue of y and b (prescale), the pair loop with its
 fused sum and gradient reduction, and the column-block second pass.  Inputs
 are seeded synthetic points (a mixture of 8 isotropic Gaussians, std 0.05,
 centres in [0,1]^3; b ~ N(0,1); sigma = 0.05) already resident in HBM when
-timing starts.  `--workload` selects the other workloads.
+timing starts.  `--workload` selects the other workloads, among them the
+Gaussian backward (the x, y and b gradients for a cotangent e, three
+reductions per step).
 
 Prints one JSON line.  `value` is pair evaluations per second (Gpairs/s) of
-the whole step; `roofline` prices the main kernel's algorithmic flops
-against the FP32 vector (or FP32 matrix) peak, timed with HIP events the
-library records around that kernel on the launch stream; `cpu_baseline`
-times the fp64 oracle on the host over a bounded sample of rows.
+the whole step (each reduction of a step counts its M x N pairs); `roofline`
+prices the main kernels' algorithmic flops against the FP32 vector (or FP32
+matrix) peak, timed with HIP events the library records around each main
+kernel on the launch stream; `cpu_baseline` times the fp64 oracle on the
+host over a bounded sample of rows.
 """
 import argparse
 import hashlib
@@ -41,9 +44,22 @@ WORKLOADS = {
            291, "mfma", "gaussian kernel sum, N(0, I/128), 2e5 x 2e5, D=128, E=16"),
     "c5": ("integer_knn", dict(M=100_000, N=1_000_000, D=64, K=10), "sqdist", "argkmin",
            131, "mfma", "arg-K-min K=10, integer mixture, 1e5 queries x 1e6 points, D=64"),
+    # Gaussian backward: the x, y and b gradients of L = sum_i <e_i, a_i>, three
+    # reductions over the M x N pairs per step (flops per pair summed over them)
+    "backward": ("mixture_gauss", dict(M=1_000_000, N=1_000_000, D=3, sigma=0.05), "backward",
+                 None, 17 + 17 + 11, "alu",
+                 "gaussian backward (x, y, b gradients), scalar cotangent, mixture of 8 "
+                 "Gaussians, 1e6 x 1e6, D=3"),
+    "backward_e16": ("uniform_gauss", dict(M=200_000, N=200_000, D=3, E=16, sigma=0.1), "backward",
+                     None, 48 + 48 + 42, "alu",
+                     "gaussian backward (x, y, b gradients), E=16 cotangent, uniform [0,1]^3, "
+                     "2e5 x 2e5, D=3"),
 }
+# the three reductions of a backward step: (rows, columns) = (M, N), (N, M), (N, M)
+REDUCTIONS_PER_STEP = {"backward": 3, "backward_e16": 3}
 KERNEL_SOURCES = {"sum_kernel": "k_direct.hip", "gradx_kernel": "k_direct.hip",
                   "lse_kernel": "k_direct.hip", "knn_kernel": "k_direct.hip",
+                  "vjp_kernel": "k_direct.hip",
                   "mfma_kernel": "k_mfma.hip", "fast_kernel": "k_small_mfma.hip"}
 
 
@@ -85,15 +101,31 @@ def traffic_for(path, workload, kernel):
     return ent.get("hbm_bytes_per_launch")
 
 
+def cotangent(w):
+    """Seeded N(0, 1) cotangent e (M x E) of the Gaussian sum, for the backward workloads."""
+    import numpy as np
+    return np.random.default_rng(1).standard_normal((w.M, w.E)).astype(np.float32)
+
+
 def time_steps(ctx, w, formula, reduction, steps, warmup):
+    """Time `steps` calls; kernel_ms is the main kernels' time per step (HIP events)."""
     import torch
     from paper_2004_11127_amd import kred
     x, y = torch.from_numpy(w.x).cuda(), torch.from_numpy(w.y).cuda()
     b = torch.from_numpy(w.b).cuda() if w.b is not None else None
-    kw = dict(sigma=w.sigma, eps=w.eps, K=w.K)
     stream = torch.cuda.current_stream()
+    if formula == "backward":
+        e = torch.from_numpy(cotangent(w)).cuda()
+
+        def call(flags):
+            return ctx.gauss_backward(x, y, b, e, sigma=w.sigma, flags=flags, stream=stream)
+    else:
+        kw = dict(sigma=w.sigma, eps=w.eps, K=w.K)
+
+        def call(flags):
+            return ctx.run(formula, reduction, x, y, b, flags=flags, stream=stream, **kw)
     for _ in range(warmup):
-        ctx.run(formula, reduction, x, y, b, stream=stream, **kw)
+        call(0)
     torch.cuda.synchronize()
     ctx.profile_collect()
     ev0 = torch.cuda.Event(enable_timing=True)
@@ -102,12 +134,14 @@ def time_steps(ctx, w, formula, reduction, steps, warmup):
     t0 = time.perf_counter()
     ev0.record(stream)
     for _ in range(steps):
-        out = ctx.run(formula, reduction, x, y, b, flags=kred.FLAG_PROFILE, stream=stream, **kw)
+        out = call(kred.FLAG_PROFILE)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     n, kern_ms, kname = ctx.profile_collect()
-    return dict(wall_s=wall, event_ms=ev0.elapsed_time(ev1), kernel_ms=kern_ms / max(n, 1),
+    if formula == "backward":
+        out = out[0]   # the x-gradient, for the CPU baseline's check
+    return dict(wall_s=wall, event_ms=ev0.elapsed_time(ev1), kernel_ms=kern_ms / steps,
                 launches=n, kernel=kname, out=out.cpu().numpy())
 
 
@@ -121,6 +155,13 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds):
     oracle.build()
 
     def run(rows):
+        if formula == "backward":
+            # the three reductions of a step on the same sampled row indices
+            e = cotangent(w)
+            gx, nx = oracle.gauss_vjp(w.x, w.y, w.b, e, w.sigma, rows=rows)
+            oracle.gauss_vjp(w.y, w.x, e, w.b, w.sigma, rows=rows)
+            oracle.kernel_sum("gauss", w.y, w.x, e, sigma=w.sigma, rows=rows)
+            return gx, nx
         if formula == "gauss_gradx":
             return oracle.gauss_gradx(w.x, w.y, w.b, w.sigma, rows=rows)
         if reduction == "lse":
@@ -145,8 +186,11 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds):
         check = {"max_abs_err_on_sample": float(np.max(np.abs(got[:, 0] - ref)))}
     else:
         check = {"max_norm_err_on_sample": float(np.max(np.abs(got - ref) / np.maximum(aux, 1e-30)))}
-    res = dict(value=S * w.N / t / 1e9, unit="Gpairs/s", cores=oracle.num_threads(),
-               kind="oracle", sample="%d seeded rows x all %d columns (%.1f s)" % (S, w.N, t),
+    red = 3 if formula == "backward" else 1
+    res = dict(value=red * S * w.N / t / 1e9, unit="Gpairs/s", cores=oracle.num_threads(),
+               kind="oracle",
+               sample="%d seeded rows x all %d columns%s (%.1f s)"
+                      % (S, w.N, " for each of the 3 gradients" if red > 1 else "", t),
                seconds=t)
     res.update(check)
     return res
@@ -165,7 +209,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     gen, gkw, formula, reduction, fpp, bound, desc = WORKLOADS[args.workload]
     w = getattr(inputs, gen)(seed=0, **gkw)
-    pairs = float(w.M) * float(w.N)
+    pairs = float(w.M) * float(w.N) * REDUCTIONS_PER_STEP.get(args.workload, 1)
     with kred.Context(0) as ctx:
         r = time_steps(ctx, w, formula, reduction, args.steps, args.warmup)
     if args.copy_probe:
@@ -174,7 +218,8 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
     ms_per_step = r["wall_s"] * 1e3 / args.steps
-    achieved = fpp * pairs / (r["kernel_ms"] / 1e3) / 1e12
+    # fpp counts the flops of one (i, j) over all reductions of a step
+    achieved = fpp * float(w.M) * float(w.N) / (r["kernel_ms"] / 1e3) / 1e12
     peak = PEAK_FP32_VECTOR_TFLOPS if bound == "alu" else PEAK_FP32_MATRIX_TFLOPS
     line = {
         "metric": "kernel pair-evaluations/sec (Gpairs/s) at M=N=1e6 D=3; % of FP32 VALU peak",
@@ -194,8 +239,9 @@ def main():
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": traffic_for(args.traffic, args.workload, r["kernel"]),
-                     "kernel": r["kernel"], "kernel_ms": r["kernel_ms"],
-                     "launches_timed": r["launches"]},
+                     "kernel": r["kernel"], "kernel_ms_per_step": r["kernel_ms"],
+                     "launches_timed": r["launches"],
+                     "launches_per_step": r["launches"] / args.steps},
         "event_ms_per_step": r["event_ms"] / args.steps,
     }
     if args.workload in ("c1", "headline"):
