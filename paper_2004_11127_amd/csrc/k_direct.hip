@@ -219,7 +219,7 @@ __device__ __forceinline__ float kernel_of(float d, float ks) {
 }
 
 template <int F, int DP, int EP, int R>
-__global__ __launch_bounds__(kThreads, 8) void sum_kernel(DirectArgs a) {
+__global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
   constexpr int S = DP + EP;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
   if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
@@ -442,7 +442,7 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const float* __restrict
 // Running reference m_i (<= max_j s_ij + kRescale): terms are 2^(s - m);
 // when a term would exceed 2^kRescale the sums are rescaled and m moves up.
 template <int DP, int R>
-__global__ __launch_bounds__(kThreads, 8) void lse_kernel(DirectArgs a) {
+__global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
   if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
@@ -591,7 +591,11 @@ __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
 }
 
 // ------------------------------------------------------------- dispatch
-constexpr int kStateBudget = 48;   // VGPRs of per-row state a lane may hold
+// Rows per lane: as many as fit a budget of VGPRs of per-row state.  Wide
+// signals (16 columns) get a larger budget: each column's LDS read then
+// serves at least two rows, which outweighs the lower occupancy.
+constexpr int kStateBudget = 48;
+constexpr int kWideStateBudget = 96;
 
 constexpr int pow2_floor(int v) { return v >= 8 ? 8 : v >= 4 ? 4 : v >= 2 ? 2 : 1; }
 
@@ -601,7 +605,8 @@ constexpr int rows_for(int formula, int DP, int EP, int KP) {
                     : formula == F_SINKHORN ? DP + 3
                     : KP > 0                ? DP + 2 * KP
                                             : DP + 2 * EP;
-  return pow2_floor(kStateBudget / state > 0 ? kStateBudget / state : 1);
+  const int budget = (EP >= 16 && KP == 0) ? kWideStateBudget : kStateBudget;
+  return pow2_floor(budget / state > 0 ? budget / state : 1);
 }
 
 template <int DP, int EP>
