@@ -29,7 +29,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 _lock = threading.Lock()
 _lib = None
 
-GAUSS, LAPLACE, SQDIST = 0, 1, 2
+GAUSS, LAPLACE, SQDIST, SINKHORN = 0, 1, 2, 4
 _FORMULAS = {"gauss": GAUSS, "laplace": LAPLACE, "sqdist": SQDIST}
 
 _dp = ctypes.POINTER(ctypes.c_double)
@@ -62,6 +62,10 @@ def _load():
             lib.oracle_gauss_vjp.argtypes = [ctypes.c_double, ctypes.c_int64, ctypes.c_int64,
                                              ctypes.c_int, ctypes.c_int, _dp, _dp, _dp, _dp,
                                              _i64p, ctypes.c_int64, _dp, _dp]
+            lib.oracle_extreme.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                           ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                           ctypes.c_int, _dp, _dp, _dp, _i64p, ctypes.c_int64,
+                                           _dp, _i64p, _dp]
             lib.oracle_sinkhorn_lse.argtypes = [ctypes.c_double, ctypes.c_int64, ctypes.c_int64,
                                                 ctypes.c_int, _dp, _dp, _dp, _i64p,
                                                 ctypes.c_int64, _dp, _dp]
@@ -70,7 +74,7 @@ def _load():
                                            _i64p, _dp]
             lib.oracle_num_threads.restype = ctypes.c_int
             for f in (lib.oracle_kernel_sum, lib.oracle_gauss_gradx, lib.oracle_gauss_vjp,
-                      lib.oracle_sinkhorn_lse, lib.oracle_argkmin):
+                      lib.oracle_extreme, lib.oracle_sinkhorn_lse, lib.oracle_argkmin):
                 f.restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -163,6 +167,32 @@ def gauss_vjp(x, y, b, e, sigma, rows=None):
     _check(_load().oracle_gauss_vjp(float(sigma), M, N, D, E, _ptr(x), _ptr(y), _ptr(b),
                                     _ptr(e), _ptr(r, _i64p), nr, _ptr(out), _ptr(norm)))
     return out, norm
+
+
+def extreme(formula, op, x, y, b=None, param=1.0, rows=None):
+    """Min or max reduction (op "min" / "max") with the lowest arg index on ties.
+
+    formula "gauss" / "laplace" / "sqdist": F_ije = kernel(|x_i - y_j|^2) b_je
+    ("sqdist" with b None: F_ij = |x_i - y_j|^2); "sinkhorn": F_ij = g_j -
+    |x_i - y_j|^2 / eps with b = g.  param: sigma, or eps for "sinkhorn".
+    Returns (val, idx int64, scale), each (nrows, E); scale = max_j |F_ije|.
+    """
+    fcode = SINKHORN if formula == "sinkhorn" else _FORMULAS[formula]
+    x = _f64(x); y = _f64(y)
+    M, D = x.shape
+    N = y.shape[0]
+    if b is None:
+        E = 1
+    else:
+        b = np.asarray(b, dtype=np.float64)
+        E = b.shape[1] if b.ndim == 2 else 1
+        b = _f64(b, E)
+    r, nr = _rows(rows, M)
+    val = np.empty((nr, E)); idx = np.empty((nr, E), dtype=np.int64); scale = np.empty((nr, E))
+    _check(_load().oracle_extreme(fcode, {"min": 0, "max": 1}[op], float(param), M, N, D, E,
+                                  _ptr(x), _ptr(y), _ptr(b), _ptr(r, _i64p), nr, _ptr(val),
+                                  _ptr(idx, _i64p), _ptr(scale)))
+    return val, idx, scale
 
 
 def sinkhorn_lse(x, y, g, eps, rows=None):

@@ -10,7 +10,8 @@
  * (arXiv:2004.11127):
  *   - Eq. (1): a_i = sum_j exp(-|x_i - y_j|^2 / (2 sigma^2)) b_j, i = 1..M;
  *   - Eq. (2), Sec. 2: a_i = Reduction_{j=1..N} F(p, x_i, y_j) for a formula F
- *     and a reduction among those Sec. 2 lists (sum, log-sum-exp, arg-K-min);
+ *     and a reduction among those Sec. 2 lists (sum, log-sum-exp, min, max,
+ *     arg-min, arg-K-min; arg-max by symmetry with arg-min);
  *   - Sec. 2 "Backpropagation": the gradient of a reduction is again a
  *     reduction of the same form; here d a_i / d x_i of Eq. (1), and the
  *     vector-Jacobian product of Eq. (1) in x for a cotangent of its output.
@@ -196,6 +197,56 @@ int oracle_sinkhorn_lse(double eps, int64_t M, int64_t N, int D,
     }
     out[r] = (N > 0) ? m + log(acc) : -INFINITY;
     if (maxv) maxv[r] = m;
+  }
+  (void)M;
+  return 0;
+}
+
+/*
+ * Min, max, arg-min and arg-max reductions of Eq. (2) (Sec. 2 lists .min(),
+ * .max() and .argmin() beside the sum): for each selected row i and each
+ * component e of the formula, the extreme value over j of F_ije and the
+ * lowest index j where it is reached.  Formulas:
+ *   formula 0..2 (Gauss, Laplace, squared distance) with b: F_ije = kernel(d_ij) b_je;
+ *   formula 2 with b == NULL:                               F_ij  = d_ij (E = 1);
+ *   formula 4 (log-sum-exp formula):                         F_ij  = b_j - d_ij / param (E = 1).
+ * param is sigma (Gauss, Laplace) or eps (formula 4).  op: 0 = min, 1 = max.
+ * val, idx (idx may be NULL) and scale: nrows x E; scale holds max_j |F_ije|,
+ * the size of the row's values.  With N = 0: val = +inf (min) or -inf (max),
+ * idx = -1, scale = 0.
+ */
+int oracle_extreme(int formula, int op, double param, int64_t M, int64_t N, int D, int E,
+                   const double* x, const double* y, const double* b,
+                   const int64_t* rows, int64_t nrows, double* val, int64_t* idx, double* scale) {
+  if (D < 1 || E < 1 || nrows < 0 || (op != 0 && op != 1)) return -1;
+  if (formula == 3 || formula < 0 || formula > 4) return -1;
+  if (formula != ORACLE_SQDIST && !(param > 0.0)) return -1;
+  if ((formula == 4 || b == NULL) && E != 1) return -1;
+  if (b == NULL && formula != ORACLE_SQDIST) return -1;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int64_t r = 0; r < nrows; ++r) {
+    const int64_t i = row_of(rows, r);
+    const double* xi = x + i * D;
+    for (int e = 0; e < E; ++e) {
+      val[r * E + e] = op == 0 ? INFINITY : -INFINITY;
+      if (idx) idx[r * E + e] = -1;
+      scale[r * E + e] = 0.0;
+    }
+    for (int64_t j = 0; j < N; ++j) {
+      const double d = sq_dist(xi, y + j * D, D);
+      for (int e = 0; e < E; ++e) {
+        double f;
+        if (formula == 4) f = b[j] - d / param;
+        else if (b == NULL) f = d;
+        else f = kernel_value(formula, d, param) * b[j * E + e];
+        const int better = op == 0 ? f < val[r * E + e] : f > val[r * E + e];
+        if (better) {   /* strict: the first (lowest) j keeps a tie */
+          val[r * E + e] = f;
+          if (idx) idx[r * E + e] = j;
+        }
+        if (fabs(f) > scale[r * E + e]) scale[r * E + e] = fabs(f);
+      }
+    }
   }
   (void)M;
   return 0;

@@ -39,6 +39,15 @@ VALUES = {
         "x": [[0, 0]], "y": [[1, 0], [0, 2]], "b": [[1, 2], [-1, 0]], "e": [[3, 1]], "sigma": 1.0,
         "closed_form": "<e, b_0> = 5, <e, b_1> = -3; g = 5 exp(-1/2) (1, 0) - 3 exp(-2) (0, 2)",
         "value": [5 * E(-0.5), -6 * E(-2.0)]},
+    "extreme_small": {
+        "cite": "Sec. 2 (.min(), .max(), .argmin()): extreme entries of a row of F and their lowest index",
+        "x": [[0, 0]], "y": [[2, 0], [1, 0], [0, 1], [0, 0], [-1, 0], [3, 3]],
+        "b": [[1], [2], [-2], [0.5], [2], [7]], "sigma": 1.0,
+        "closed_form": "squared distances (4, 1, 1, 0, 1, 18): min 0 at j=3, max 18 at j=5; Gaussian "
+                       "F = exp(-d/2) b = (e^-2, 2e^-1/2, -2e^-1/2, 1/2, 2e^-1/2, 7e^-9): max 2e^-1/2 "
+                       "at j=1 (tie with j=4 keeps the lower index), min -2e^-1/2 at j=2",
+        "value": {"sqdist_min": [0.0, 3], "sqdist_max": [18.0, 5],
+                  "gauss_max": [2 * E(-0.5), 1], "gauss_min": [-2 * E(-0.5), 2]}},
     "lse_two_point": {
         "cite": "Eq. (2) with the log-sum-exp reduction of Sec. 2, F = g_j - |x-y|^2/eps",
         "x": [[0, 0]], "y": [[0, 0], [1, 1]], "g": [[0], [2]], "eps": 1.0,

@@ -265,6 +265,80 @@ def test_vjp_linear_in_cotangent_and_signal(oracle_mod):
     np.testing.assert_allclose(gp, g1, rtol=1e-13, atol=1e-15)
 
 
+# ------------------------------------------------------------ min / max / arg-min
+
+def test_extreme_hand_values(oracle_mod, hv):
+    c = hv["extreme_small"]
+    x, y, b = _a(c["x"]), _a(c["y"]), _a(c["b"])
+    for key, formula, op, bb in (("sqdist_min", "sqdist", "min", None), ("sqdist_max", "sqdist", "max", None),
+                                 ("gauss_max", "gauss", "max", b), ("gauss_min", "gauss", "min", b)):
+        v, i, _ = oracle_mod.extreme(formula, op, x, y, bb, param=c["sigma"])
+        assert v[0, 0] == pytest.approx(c["value"][key][0], rel=1e-14, abs=1e-15), key
+        assert i[0, 0] == c["value"][key][1], key
+
+
+def test_extreme_min_is_argkmin_k1(oracle_mod):
+    # squared-distance min / arg-min against the brute-force-pinned arg-K-min
+    # with K = 1, on integer coordinates full of exact ties
+    rng = np.random.default_rng(12)
+    x = rng.integers(-2, 3, (40, 3)).astype(np.float64); y = rng.integers(-2, 3, (60, 3)).astype(np.float64)
+    v, i, _ = oracle_mod.extreme("sqdist", "min", x, y)
+    idx, dist = oracle_mod.argkmin(x, y, 1)
+    np.testing.assert_array_equal(i[:, 0], idx[:, 0])
+    np.testing.assert_array_equal(v[:, 0], dist[:, 0])
+
+
+def test_extreme_lse_formula_max_is_lse_row_max(oracle_mod):
+    # the log-sum-exp routine's two-pass maximum m_i = max_j s_ij
+    rng = np.random.default_rng(13)
+    x = rng.uniform(0, 1, (9, 3)); y = rng.uniform(0, 1, (40, 3)); g = rng.normal(size=(40, 1))
+    v, i, _ = oracle_mod.extreme("sinkhorn", "max", x, y, g, param=0.05)
+    a, m = oracle_mod.sinkhorn_lse(x, y, g, 0.05)
+    np.testing.assert_allclose(v[:, 0], m, rtol=1e-15)
+
+
+@pytest.mark.parametrize("formula", ["gauss", "laplace", "sqdist"])
+def test_extreme_sign_symmetry_and_ties(oracle_mod, formula):
+    # min of F b = -(max of F (-b)), same (lowest) index; duplicated columns tie
+    rng = np.random.default_rng(14)
+    x = rng.uniform(0, 1, (11, 2)); y = rng.uniform(0, 1, (30, 2))
+    y = np.concatenate([y, y[::-1]])   # every column appears twice
+    b = rng.normal(size=(30, 3)); b = np.concatenate([b, b[::-1]])
+    vmin, imin, s1 = oracle_mod.extreme(formula, "min", x, y, b, param=0.3)
+    vmax, imax, s2 = oracle_mod.extreme(formula, "max", x, y, -b, param=0.3)
+    np.testing.assert_array_equal(vmin, -vmax)
+    np.testing.assert_array_equal(imin, imax)
+    assert (imin < 30).all()   # the first copy of a tied column wins
+    np.testing.assert_array_equal(s1, s2)
+
+
+@pytest.mark.parametrize("op", ["min", "max"])
+def test_extreme_components_are_independent(oracle_mod, op):
+    # component e of an E-column call equals the one-column call on b[:, e]
+    rng = np.random.default_rng(16)
+    x = rng.uniform(0, 1, (10, 3)); y = rng.uniform(0, 1, (35, 3)); b = rng.normal(size=(35, 4))
+    v, i, s = oracle_mod.extreme("gauss", op, x, y, b, param=0.25)
+    for e in range(4):
+        ve, ie, se = oracle_mod.extreme("gauss", op, x, y, b[:, [e]], param=0.25)
+        np.testing.assert_array_equal(v[:, e], ve[:, 0])
+        np.testing.assert_array_equal(i[:, e], ie[:, 0])
+
+
+def test_extreme_gauss_max_is_nearest_point(oracle_mod):
+    # with b = 1 the Gaussian is largest at the nearest point: exp(-d_min / 2 sigma^2)
+    rng = np.random.default_rng(15)
+    x = rng.uniform(0, 1, (12, 3)); y = rng.uniform(0, 1, (50, 3))
+    v, i, _ = oracle_mod.extreme("gauss", "max", x, y, np.ones((50, 1)), param=0.2)
+    idx, dist = oracle_mod.argkmin(x, y, 1)
+    np.testing.assert_array_equal(i[:, 0], idx[:, 0])
+    np.testing.assert_allclose(v[:, 0], np.exp(-dist[:, 0] / (2 * 0.2 ** 2)), rtol=1e-14)
+
+
+def test_extreme_empty(oracle_mod):
+    v, i, s = oracle_mod.extreme("sqdist", "min", np.zeros((2, 3)), np.zeros((0, 3)))
+    assert np.isinf(v).all() and (v > 0).all() and (i == -1).all() and (s == 0).all()
+
+
 # ---------------------------------------------------------------------- log-sum-exp
 
 def test_lse_single_point(oracle_mod):
