@@ -48,11 +48,17 @@ typedef enum kred_formula {
   KRED_F_SINKHORN = 4     /* s = g_j - |x - y|^2 / eps, with g_j passed in b          */
 } kred_formula;
 
-/* Reductions over j (Sec. 2: .sum(), .logsumexp(), .argKmin(K)). */
+/* Reductions over j (Sec. 2: .sum(), .logsumexp(), .min(), .max(), .argmin(),
+ * .argKmin(K); arg-max and the K smallest values complete the set). */
 typedef enum kred_reduction {
   KRED_R_SUM = 0,
   KRED_R_LSE = 1,
-  KRED_R_ARGKMIN = 2
+  KRED_R_ARGKMIN = 2,
+  KRED_R_MIN = 3,
+  KRED_R_MAX = 4,
+  KRED_R_ARGMIN = 5,
+  KRED_R_ARGMAX = 6,
+  KRED_R_KMIN = 7
 } kred_reduction;
 
 typedef enum kred_status {
@@ -116,13 +122,27 @@ kred_status kred_destroy(kred_ctx* ctx);
  *   (SQDIST, ARGKMIN):  b must be NULL and E is ignored (pass 0), out is int32
  *        M x K: the indices j of the K smallest |x_i - y_j|^2, ascending by
  *        (distance, index): equal distances keep the lower index first.
+ *   (SQDIST, KMIN):  as ARGKMIN, but out is fp32 M x K: the K smallest
+ *        squared distances themselves, in the same order.
+ *   (GAUSS | LAPLACE | SQDIST, MIN | MAX | ARGMIN | ARGMAX) with b (N x E):
+ *        per component e of F_ije = k(|x_i - y_j|^2) b_je (k as for SUM; k = d
+ *        for SQDIST), the smallest / largest value over j (out fp32 M x E) or
+ *        the lowest index j where it is reached (out int32 M x E).
+ *   (SQDIST, MIN | MAX | ARGMIN | ARGMAX) with b = NULL:  F_ij = |x_i - y_j|^2,
+ *        E ignored, out M x 1 (nearest / farthest distance or index).
+ *   (SINKHORN, MIN | MAX | ARGMIN | ARGMAX), E = 1:  F_ij = g_j - |x_i - y_j|^2
+ *        / eps with g in b, out M x 1 (the max is the hard limit of LSE).
  * Any other pair returns KRED_ERR_UNSUPPORTED.
  *
  * Ranges: 0 <= M, N <= 2^31 - 1; 1 <= D <= KRED_MAX_D; 1 <= E <= KRED_MAX_E
- * for SUM; p->col_blocks in [0, KRED_MAX_COL_BLOCKS].  Inputs must be finite
- * (NaN or Inf in x, y or b gives an undefined result).
+ * where b has E columns; p->col_blocks in [0, KRED_MAX_COL_BLOCKS].  D > 16
+ * is supported by the sums, ARGKMIN, KMIN, and MIN / ARGMIN of SQDIST without
+ * b; the other pairs return KRED_ERR_UNSUPPORTED there.  Inputs must be
+ * finite (NaN or Inf in x, y or b gives an undefined result).
  * Edge cases: M = 0 returns KRED_OK and touches nothing.  N = 0 writes zeros
- * (SUM) or -infinity (LSE); ARGKMIN with N = 0 fails since it needs K <= N.
+ * (SUM), -infinity (LSE, MAX), +infinity (MIN) or -1 (ARGMIN, ARGMAX) and
+ * reads no input (b may then be NULL; for SQDIST, a NULL b means one output
+ * column); ARGKMIN and KMIN with N = 0 fail since they need K <= N.
  *
  * `stream` is a hipStream_t (NULL = the null stream of the context's device).
  * The call is asynchronous: it returns once the kernels are enqueued.
@@ -147,7 +167,8 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
 
 /*
  * Scratch bytes kred_run will need for this call (0 when none), or -1 when
- * the arguments are invalid.  Host-only.
+ * the arguments are invalid.  Host-only.  For the MIN / MAX / ARGMIN / ARGMAX
+ * reductions of SQDIST, E = 0 stands for a call without b.
  */
 int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* p,
                            int64_t M, int64_t N, int32_t D, int32_t E);

@@ -105,10 +105,43 @@ __global__ __launch_bounds__(256) void combine_knn_kernel(CombineArgs a) {
         }
       }
     }
-    int* o = static_cast<int*>(a.out) + row * a.K;
+    if (a.kvalues) {
+      // the expanded form can round a zero distance to a tiny negative value
+      float* o = static_cast<float*>(a.out) + row * a.K;
 #pragma unroll
-    for (int p = 0; p < KP; ++p)
-      if (p < a.K) o[p] = jk[p];
+      for (int p = 0; p < KP; ++p)
+        if (p < a.K) o[p] = fmaxf(dk[p], 0.0f);
+    } else {
+      int* o = static_cast<int*>(a.out) + row * a.K;
+#pragma unroll
+      for (int p = 0; p < KP; ++p)
+        if (p < a.K) o[p] = jk[p];
+    }
+  }
+}
+
+// min / max: partials are (sign * value, index) pairs; keep the smallest in
+// (value, index) order, so equal values keep the lowest index.
+__global__ __launch_bounds__(256) void combine_extreme_kernel(CombineArgs a) {
+  const int Ec = min(a.EP, a.E - a.e0);
+  const int64_t total = a.M * Ec;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = t / Ec;
+    const int e = (int)(t - row * Ec);
+    float v = __builtin_inff();
+    int j = -1;
+    for (int c = 0; c < a.C; ++c) {
+      const float* p = a.part + ((int64_t)c * a.M + row) * (2 * a.EP) + 2 * e;
+      const int pj = __float_as_int(p[1]);
+      if (pj >= 0 && (j < 0 || p[0] < v || (p[0] == v && pj < j))) {
+        v = p[0];
+        j = pj;
+      }
+    }
+    const int64_t o = row * a.E + a.e0 + e;
+    if (a.arg) static_cast<int*>(a.out)[o] = j;
+    else static_cast<float*>(a.out)[o] = a.ext_sign * v;
   }
 }
 
@@ -121,6 +154,10 @@ unsigned grid_for(int64_t items) {
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   if (a.M == 0) return hipSuccess;
+  if (a.ext) {
+    hipLaunchKernelGGL(combine_extreme_kernel, dim3(grid_for(a.M * a.EP)), dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.KP > 0) {
     const dim3 g(grid_for(a.M));
     switch (a.KP) {

@@ -47,6 +47,7 @@ __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
     } else if (s >= a.DP) {
       const int e = a.e0 + s - a.DP;
       if (a.b != nullptr && e < a.E) v = a.b[j * a.E + e] * a.bscale;
+      else if (a.unit_b && s == a.DP) v = a.bscale;
     }
     a.ypk[t] = v;
   }
@@ -515,6 +516,84 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
   }
 }
 
+// ------------------------------------------------- min / max / arg-min / arg-max
+// Minimum over j of f = sign * F_ije with the lowest index on ties (the max
+// of F is the min of -F; the sign is folded into the packed b and kscale):
+//   Gauss / Laplace / squared distance: f = kernel(d) * (sign b_je)
+//   log-sum-exp formula:                f = (sign g_j) - (sign / eps) d
+// Columns are visited in increasing j and the compare is strict, so a later
+// equal value never replaces an earlier one.  Partials are (f, j) pairs.
+template <int F, int DP, int EP, int R>
+__global__ __launch_bounds__(kThreads) void extreme_kernel(DirectArgs a) {
+  constexpr int S = DP + EP;
+  __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  const Item it = item_of(a);
+  float xr[R][DP];
+  load_rows<DP, R>(a, it.rb, xr);
+  float best[R][EP];
+  int bj[R][EP];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+      best[r][e] = __builtin_inff();
+      bj[r][e] = -1;
+    }
+  const float ks = a.kscale;
+
+  stream_columns<S>(
+      a.ypk, it.j0, it.j1, 0, lds,
+      [&](const float* yv, int64_t j) {
+        float d[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) d[r] = sq_dist<DP>(xr[r], yv);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if constexpr (F == F_SINKHORN) {
+            const float f = __builtin_fmaf(-ks, d[r], yv[DP]);
+            if (f < best[r][0]) {
+              best[r][0] = f;
+              bj[r][0] = (int)j;
+            }
+          } else {
+            const float k = kernel_of<F>(d[r], ks);
+#pragma unroll
+            for (int e = 0; e < EP; ++e) {
+              const float f = k * yv[DP + e];
+              if (f < best[r][e]) {
+                best[r][e] = f;
+                bj[r][e] = (int)j;
+              }
+            }
+          }
+        }
+      },
+      [&]() {});
+
+  const int Ec = min(EP, a.E - a.e0);
+  const int tid_out = opaque_tid();
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t row = row_of<R>(it.rb, r, tid_out);
+    if (row >= a.M) continue;
+    if (a.C == 1) {
+#pragma unroll
+      for (int e = 0; e < EP; ++e)
+        if (e < Ec) {
+          if (a.arg) static_cast<int*>(a.out)[row * a.E + a.e0 + e] = bj[r][e];
+          else static_cast<float*>(a.out)[row * a.E + a.e0 + e] = a.ext_sign * best[r][e];
+        }
+    } else {
+      float* p = a.part + ((int64_t)it.c * a.M + row) * (2 * EP);
+#pragma unroll
+      for (int e = 0; e < EP; ++e) {
+        p[2 * e] = best[r][e];
+        p[2 * e + 1] = __int_as_float(bj[r][e]);
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------ arg-K-min
 // Per row a sorted register list of the KP smallest (d, j) seen; columns are
 // visited in increasing j, so a later equal distance never displaces an
@@ -575,10 +654,17 @@ __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
     const int64_t row = row_of<R>(it.rb, r, tid_out);
     if (row >= a.M) continue;
     if (a.C == 1) {
-      int* o = static_cast<int*>(a.out) + row * a.K;
+      if (a.kvalues) {
+        float* o = static_cast<float*>(a.out) + row * a.K;
 #pragma unroll
-      for (int p = 0; p < KP; ++p)
-        if (p < a.K) o[p] = jk[r][p];
+        for (int p = 0; p < KP; ++p)
+          if (p < a.K) o[p] = dk[r][p];
+      } else {
+        int* o = static_cast<int*>(a.out) + row * a.K;
+#pragma unroll
+        for (int p = 0; p < KP; ++p)
+          if (p < a.K) o[p] = jk[r][p];
+      }
     } else {
       float* q = a.part + ((int64_t)it.c * a.M + row) * (2 * KP);
 #pragma unroll
@@ -630,8 +716,41 @@ hipError_t launch_sum_e(const DirectArgs& a, dim3 grid, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int DP, int EP>
+hipError_t launch_ext_e(const DirectArgs& a, dim3 grid, hipStream_t s) {
+  constexpr int R = rows_for(F_SQDIST, DP, EP, 0);   // same per-row state as the sums
+  switch (a.formula) {
+    case F_GAUSS:
+      hipLaunchKernelGGL((extreme_kernel<F_GAUSS, DP, EP, R>), grid, dim3(kThreads), 0, s, a);
+      break;
+    case F_LAPLACE:
+      hipLaunchKernelGGL((extreme_kernel<F_LAPLACE, DP, EP, R>), grid, dim3(kThreads), 0, s, a);
+      break;
+    case F_SQDIST:
+      hipLaunchKernelGGL((extreme_kernel<F_SQDIST, DP, EP, R>), grid, dim3(kThreads), 0, s, a);
+      break;
+    case F_SINKHORN:
+      if constexpr (EP == 1) {
+        hipLaunchKernelGGL((extreme_kernel<F_SINKHORN, DP, 1, R>), grid, dim3(kThreads), 0, s, a);
+        break;
+      }
+      return hipErrorInvalidValue;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <int DP>
 hipError_t launch_dp(const DirectArgs& a, dim3 grid, hipStream_t s) {
+  if (a.ext) {
+    switch (a.EP) {
+      case 1: return launch_ext_e<DP, 1>(a, grid, s);
+      case 4: return launch_ext_e<DP, 4>(a, grid, s);
+      case 16: return launch_ext_e<DP, 16>(a, grid, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
   if (a.KP > 0) {
     switch (a.KP) {
 #define KRED_KNN(KPV)                                                                           \
@@ -693,8 +812,9 @@ int direct_rows_per_thread(int formula, int DP, int EP, int KP) {
   return rows_for(formula, DP, EP, KP);
 }
 
-int partial_width(int formula, int DP, int EP, int KP) {
+int partial_width(int formula, int DP, int EP, int KP, int ext) {
   if (KP > 0) return 2 * KP;
+  if (ext) return 2 * EP;
   if (formula == F_GRADX) return DP + 1;
   if (formula == F_VJP) return DP;
   if (formula == F_SINKHORN) return 2;
@@ -726,7 +846,8 @@ hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s) {
 }
 
 hipError_t launch_direct(const DirectArgs& a, hipStream_t s) {
-  const int R = direct_rows_per_thread(a.formula, a.DP, a.EP, a.KP);
+  const int R = a.ext ? direct_rows_per_thread(F_SQDIST, a.DP, a.EP, 0)
+                      : direct_rows_per_thread(a.formula, a.DP, a.EP, a.KP);
   const int64_t rb = (a.M + (int64_t)kThreads * R - 1) / ((int64_t)kThreads * R);
   const dim3 grid((unsigned)(rb * a.C));
   switch (a.DP) {

@@ -14,9 +14,10 @@
 //     the 16 x 16 tile p is already laid out as the A operand of the next
 //     v_mfma_f32_16x16x4_f32, so a = P . B accumulates on the matrix cores
 //     with no data movement;
-//   * arg-K-min: T = |y|^2 - 2 <x, y> ranks columns exactly like |x - y|^2
-//     for a fixed row; each lane keeps a sorted K-list over the columns it
-//     sees, and the second pass merges the lists.
+//   * arg-K-min: T = |x|^2 + |y|^2 - 2 <x, y>, the squared distance in the
+//     expanded form (the row norm enters the accumulator's initial value, so
+//     it is free); each lane keeps a sorted K-list over the columns it sees,
+//     and the second pass merges the lists (and can return the distances).
 //
 // MFMA 16x16x4 f32 operand layout (lane l = 16 g + li, g = l / 16):
 //   A (16 x 4):  lane l supplies A[li][g];   B (4 x 16): lane l supplies B[g][li];
@@ -147,7 +148,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
     }
     part += __shfl_xor(part, 16);
     part += __shfl_xor(part, 32);
-    nx[rb] = SUM ? -part : 0.0f;
+    nx[rb] = SUM ? -part : part;
   }
 
   f4 oacc[RB][EB], tot[RB][EB];

@@ -34,6 +34,13 @@ constexpr int64_t kAlign = 256;
 
 inline int64_t align_up(int64_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
+// min / max / arg-min / arg-max
+inline bool is_extreme(kred_reduction r) {
+  return r == KRED_R_MIN || r == KRED_R_MAX || r == KRED_R_ARGMIN || r == KRED_R_ARGMAX;
+}
+inline bool is_max(kred_reduction r) { return r == KRED_R_MAX || r == KRED_R_ARGMAX; }
+inline bool is_arg(kred_reduction r) { return r == KRED_R_ARGMIN || r == KRED_R_ARGMAX; }
+
 bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
 
 bool misaligned(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 3u); }
@@ -85,10 +92,12 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
     q.E = 0;
   }
   if (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN) q.E = 1;
+  const int ext = is_extreme(r) ? 1 : 0;
   const int EP_first = (r == KRED_R_ARGKMIN) ? 1 : direct_pad_e(std::min(q.E, 16));
   q.S_max = q.DP + EP_first;
-  q.W_max = partial_width(q.formula, q.DP, EP_first, q.KP);
-  const int R = direct_rows_per_thread(q.formula, q.DP, EP_first, q.KP);
+  q.W_max = partial_width(q.formula, q.DP, EP_first, q.KP, ext);
+  const int R = ext ? direct_rows_per_thread(F_SQDIST, q.DP, EP_first, 0)
+                    : direct_rows_per_thread(q.formula, q.DP, EP_first, q.KP);
   const int64_t rows = rows_override > 0 ? rows_override : (int64_t)kThreads * R;
   const int64_t row_blocks = (M + rows - 1) / rows;
   q.C = choose_col_blocks(std::max<int64_t>(1, row_blocks), N, num_cus, p->col_blocks);
@@ -128,6 +137,13 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
       break;
     default:
       break;
+  }
+  if (ext) {
+    // min of sign * F in natural units: the sign rides on the packed b (and
+    // on kscale for the log-sum-exp formula, f = sign g - (sign / eps) d)
+    const float sign = is_max(r) ? -1.0f : 1.0f;
+    q.bscale = sign;
+    if (f == KRED_F_SINKHORN) q.kscale = (float)((double)sign / (double)p->eps);
   }
   *pl = q;
   return true;
@@ -278,7 +294,7 @@ hipEvent_t next_event(kred_ctx* ctx) {
 
 kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                      int64_t M, int64_t N, int32_t D, int32_t E, const float* x, const float* y,
-                     const float* b, void* out, hipStream_t s) {
+                     const float* b, void* out, hipStream_t s, int kvalues) {
   MPlan pl;
   if (!make_mplan(f, r, p, M, N, D, E, ctx->num_cus, &pl)) return KRED_ERR_UNSUPPORTED;
   const kred_status gs =
@@ -360,6 +376,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     ca.gscale = 0.0f;
     ca.KP = knn ? pl.KP : 0;
     ca.K = pl.K;
+    ca.kvalues = kvalues;
     if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
   }
   return KRED_OK;
@@ -372,14 +389,36 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   if (N == 0) {
     int64_t count = M;
     float value = 0.0f;
+    const int64_t e_out = (f == KRED_F_SINKHORN || (f == KRED_F_SQDIST && b == nullptr)) ? 1 : E;
     if (f == KRED_F_GAUSS_GRADX) count = M * (1 + D);
     else if (r == KRED_R_SUM) count = M * E;
     else if (r == KRED_R_LSE) value = -INFINITY;
+    else if (is_extreme(r)) {
+      count = M * e_out;
+      // an empty min is +inf, an empty max -inf, an empty arg -1 (int32 bits)
+      value = is_arg(r) ? __builtin_bit_cast(float, (int32_t)-1)
+                        : (is_max(r) ? -INFINITY : INFINITY);
+    }
     return launch_fill(static_cast<float*>(out), count, value, s) == hipSuccess ? KRED_OK
                                                                                 : KRED_ERR_HIP;
   }
 
-  if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s);
+  // The squared distance's min and arg-min (without b) and its K smallest
+  // values are read off the arg-K-min lists (K = 1 for min and arg-min).
+  int kvalues = 0;
+  kred_params pk;
+  if (f == KRED_F_SQDIST && b == nullptr &&
+      (r == KRED_R_MIN || r == KRED_R_ARGMIN || r == KRED_R_KMIN)) {
+    kvalues = r != KRED_R_ARGMIN;
+    pk = *p;
+    if (r != KRED_R_KMIN) pk.K = 1;
+    p = &pk;
+    r = KRED_R_ARGKMIN;
+  }
+  const bool ext = is_extreme(r);
+  if (ext && (b == nullptr || f == KRED_F_SINKHORN)) E = 1;   // one output column
+
+  if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s, kvalues);
 
   const int epi = fast_epi(f, r, M, N, D, E, p->flags);
   Plan pl;
@@ -450,6 +489,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     pa.bscale = pl.bscale;
     pa.guard = guard;
     pa.fscale = pl.fscale;
+    pa.unit_b = ext && b == nullptr;   // squared-distance max without b: F = d * 1
     if (launch_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
 
     DirectArgs da{};
@@ -474,6 +514,10 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     da.KP = pl.KP;
     da.K = pl.K;
     da.guard = guard;
+    da.ext = ext;
+    da.ext_sign = is_max(r) ? -1.0f : 1.0f;
+    da.arg = is_arg(r);
+    da.kvalues = kvalues;
     hipEvent_t e_start = nullptr, e_stop = nullptr;
     if (prof) {
       e_start = next_event(ctx);
@@ -486,6 +530,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     if (prof) {
       if (hipEventRecord(e_stop, s) != hipSuccess) return KRED_ERR_HIP;
       ctx->last_kernel = (epi >= 0)                  ? "fast_kernel"
+                         : ext                       ? "extreme_kernel"
                          : (r == KRED_R_ARGKMIN)     ? "knn_kernel"
                          : (f == KRED_F_GAUSS_GRADX) ? "gradx_kernel"
                          : (f == KRED_F_SINKHORN)    ? "lse_kernel"
@@ -506,6 +551,10 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
       ca.gscale = pl.gscale;
       ca.KP = pl.KP;
       ca.K = pl.K;
+      ca.ext = ext;
+      ca.ext_sign = da.ext_sign;
+      ca.arg = da.arg;
+      ca.kvalues = kvalues;
       if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
     }
   }
@@ -631,7 +680,7 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
                           const void* b, const void* out) {
   if (p == nullptr) return KRED_ERR_INVALID_ARG;
   if ((int)f < KRED_F_GAUSS || (int)f > KRED_F_SINKHORN) return KRED_ERR_INVALID_ARG;
-  if ((int)r < KRED_R_SUM || (int)r > KRED_R_ARGKMIN) return KRED_ERR_INVALID_ARG;
+  if ((int)r < KRED_R_SUM || (int)r > KRED_R_KMIN) return KRED_ERR_INVALID_ARG;
   if (M < 0 || N < 0 || M > INT32_MAX || N > INT32_MAX) return KRED_ERR_INVALID_ARG;
   if (D < 1 || D > KRED_MAX_D) return KRED_ERR_INVALID_ARG;
   if (p->col_blocks < 0 || p->col_blocks > KRED_MAX_COL_BLOCKS) return KRED_ERR_INVALID_ARG;
@@ -645,16 +694,30 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
   } else if (r == KRED_R_LSE && f == KRED_F_SINKHORN) {
     if (E != 1) return KRED_ERR_INVALID_ARG;
     if (!finite_pos(p->eps)) return KRED_ERR_INVALID_ARG;
-  } else if (r == KRED_R_ARGKMIN && f == KRED_F_SQDIST) {
+  } else if ((r == KRED_R_ARGKMIN || r == KRED_R_KMIN) && f == KRED_F_SQDIST) {
     if (b != nullptr) return KRED_ERR_INVALID_ARG;
     if (p->K < 1 || p->K > KRED_MAX_K || p->K > N) return KRED_ERR_INVALID_ARG;
     needs_b = false;
+  } else if (is_extreme(r) && f != KRED_F_GAUSS_GRADX) {
+    if (f == KRED_F_SINKHORN) {
+      if (E != 1 || !finite_pos(p->eps)) return KRED_ERR_INVALID_ARG;
+    } else if (f == KRED_F_SQDIST && b == nullptr) {
+      needs_b = false;   // F = d; E is ignored
+    } else {
+      if (E < 1 || E > KRED_MAX_E) return KRED_ERR_INVALID_ARG;
+      if (f != KRED_F_SQDIST && !finite_pos(p->sigma)) return KRED_ERR_INVALID_ARG;
+    }
   } else {
     return KRED_ERR_UNSUPPORTED;
   }
   // Paths: the direct-form kernels cover D <= 16 for every pair; the
-  // matrix-core kernels cover 16 < D <= 256 for the sums and arg-K-min.
-  if (D > kMaxDirectD && (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN))
+  // matrix-core kernels cover 16 < D <= 256 for the sums and the arg-K-min
+  // lists (arg-K-min, K-min, and min / arg-min of the squared distance).
+  const bool lists = f == KRED_F_SQDIST && b == nullptr &&
+                     (r == KRED_R_ARGKMIN || r == KRED_R_KMIN || r == KRED_R_MIN ||
+                      r == KRED_R_ARGMIN);
+  if (D > kMaxDirectD && (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN ||
+                          (is_extreme(r) && !lists)))
     return KRED_ERR_UNSUPPORTED;
   if (M == 0) return KRED_OK;
   if (x == nullptr || out == nullptr) return KRED_ERR_INVALID_ARG;
@@ -667,9 +730,19 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
 int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* p, int64_t M,
                            int64_t N, int32_t D, int32_t E) {
   const float dummy = 0.0f;
-  const void* bp = (r == KRED_R_ARGKMIN) ? nullptr : &dummy;
+  // E = 0 with the squared distance's min / max reductions means "without b"
+  const bool nob = r == KRED_R_ARGKMIN || r == KRED_R_KMIN ||
+                   (f == KRED_F_SQDIST && is_extreme(r) && E == 0);
+  const void* bp = nob ? nullptr : &dummy;
   if (kred_validate(f, r, p, M, N, D, E, &dummy, &dummy, bp, &dummy) != KRED_OK) return -1;
   if (M == 0 || N == 0) return 0;
+  kred_params pk = *p;
+  if (nob && (r == KRED_R_KMIN || r == KRED_R_MIN || r == KRED_R_ARGMIN)) {
+    if (r != KRED_R_KMIN) pk.K = 1;
+    r = KRED_R_ARGKMIN;
+    p = &pk;
+  }
+  if (is_extreme(r) && (nob || f == KRED_F_SINKHORN)) E = 1;
   if (D > kMaxDirectD) {
     MPlan mp;
     if (!make_mplan(f, r, p, M, N, D, E, 256, &mp)) return -1;

@@ -69,6 +69,7 @@ struct PackArgs {
   float yscale, bscale;
   const FastGuard* guard;   // non-null: skip when the fast path is selected
   float fscale;             // prescale of the fast path (for its guard test)
+  int unit_b;               // b == null: the signal column is bscale (a constant 1 * sign)
 };
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 
@@ -91,13 +92,17 @@ struct DirectArgs {
   const FastGuard* guard; // non-null: skip when the fast path is selected
   const float* xe;        // F_VJP: row cotangent e, M x E (this call reads its E-slice)
   int accumulate;         // F_VJP with C == 1: add to out instead of storing (E-slices after the first)
+  int ext;                // min / max reductions: the kernel takes the min over j of sign * F
+  float ext_sign;         // +1 (min) or -1 (max); folded into kscale and the packed b
+  int arg;                // min / max: write the index (int32) instead of the value
+  int kvalues;            // arg-K-min lists: write the distances (fp32) instead of the indices
 };
 hipError_t launch_direct(const DirectArgs& a, hipStream_t s);
 int direct_rows_per_thread(int formula, int DP, int EP, int KP);
 int direct_pad_d(int D);      // DP for a given D, 0 if the direct path has none
 int direct_pad_e(int E);      // EP for one E-slice
 int knn_pad_k(int K);         // KP for a given K
-int partial_width(int formula, int DP, int EP, int KP);  // W (floats per row per column block)
+int partial_width(int formula, int DP, int EP, int KP, int ext);  // W (floats per row per column block)
 
 // Second pass: combine C column-block partials into the final output.
 struct CombineArgs {
@@ -110,6 +115,10 @@ struct CombineArgs {
   float gscale;
   int KP, K;
   int accumulate;   // F_VJP: add to out instead of storing
+  int ext;          // min / max partials: (sign * value, index) pairs
+  float ext_sign;
+  int arg;
+  int kvalues;      // arg-K-min: write the distances instead of the indices
 };
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 

@@ -17,7 +17,9 @@ LIB_PATH = os.path.join(PKG, "libkred.so")
 HEADER = os.path.join(os.path.dirname(PKG), "include", "kred.h")
 
 FORMULAS = {"gauss": 0, "laplace": 1, "sqdist": 2, "gauss_gradx": 3, "sinkhorn": 4}
-REDUCTIONS = {"sum": 0, "lse": 1, "argkmin": 2}
+REDUCTIONS = {"sum": 0, "lse": 1, "argkmin": 2, "min": 3, "max": 4, "argmin": 5, "argmax": 6,
+              "kmin": 7}
+INDEX_REDUCTIONS = (2, 5, 6)     # int32 outputs
 STATUS = {0: "KRED_OK", 1: "KRED_ERR_INVALID_ARG", 2: "KRED_ERR_UNSUPPORTED", 3: "KRED_ERR_NOMEM",
           4: "KRED_ERR_HIP", 5: "KRED_ERR_NO_DEVICE"}
 FLAG_PROFILE = 1
@@ -124,9 +126,12 @@ def scratch_bytes(formula, reduction, M, N, D, E, **params):
 
 
 def output_shape(formula, reduction, M, D, E, K=0):
+    """Shape of the output; E = 0 stands for a call without b."""
     f, r = _codes(formula, reduction)
-    if r == REDUCTIONS["argkmin"]:
+    if r in (REDUCTIONS["argkmin"], REDUCTIONS["kmin"]):
         return (M, K)
+    if r in (REDUCTIONS["min"], REDUCTIONS["max"], REDUCTIONS["argmin"], REDUCTIONS["argmax"]):
+        return (M, 1 if (E == 0 or f == FORMULAS["sinkhorn"]) else E)
     if f == FORMULAS["gauss_gradx"]:
         return (M, 1 + D)
     if r == REDUCTIONS["lse"]:
@@ -180,9 +185,11 @@ class Context:
             col_blocks=0, flags=0, stream=None):
         """Evaluate the reduction; returns `out` (allocated when None).
 
-        x: (M, D) float32, y: (N, D) float32, b: (N, E) float32 or None (arg-K-min),
-        all contiguous on the context's GPU.  The call is asynchronous on `stream`
-        (a torch.cuda.Stream; default the current stream).
+        x: (M, D) float32, y: (N, D) float32, b: (N, E) float32 or None (arg-K-min,
+        K-min, and the squared distance's min / max reductions), all contiguous on
+        the context's GPU.  Index outputs (arg-K-min, arg-min, arg-max) are int32.
+        The call is asynchronous on `stream` (a torch.cuda.Stream; default the
+        current stream).
         """
         import torch
         f, r = _codes(formula, reduction)
@@ -194,17 +201,20 @@ class Context:
         if b is not None and b.shape[0] != N:
             raise ValueError("b must have N rows")
         shape = output_shape(f, r, M, D, E, K)
-        odt = torch.int32 if r == REDUCTIONS["argkmin"] else torch.float32
+        odt = torch.int32 if r in INDEX_REDUCTIONS else torch.float32
         if out is None:
             out = torch.empty(shape, dtype=odt, device=x.device)
         elif tuple(out.shape) != shape:
             raise ValueError("out must have shape %s" % (shape,))
         p = make_params(sigma, eps, K, col_blocks, flags)
         s = (stream if stream is not None else torch.cuda.current_stream(x.device)).cuda_stream
+        bptr = self._dev_ptr(b, "b", torch.float32)
+        if b is not None and bptr is None:
+            # an empty b (N = 0) is never read, but its presence sets the output width
+            bptr = 16
         st = load().kred_run(self._h, f, r, ctypes.byref(p), M, N, D, E,
                              self._dev_ptr(x, "x", torch.float32),
-                             self._dev_ptr(y, "y", torch.float32),
-                             self._dev_ptr(b, "b", torch.float32),
+                             self._dev_ptr(y, "y", torch.float32), bptr,
                              self._dev_ptr(out, "out", odt), s)
         if st != 0:
             raise KredError(st, "kred_run(%s, %s, M=%d, N=%d, D=%d, E=%d)" % (formula, reduction,

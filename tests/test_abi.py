@@ -166,3 +166,42 @@ def test_backward_large_d_unsupported(lib):
     assert VB(100, 200, 17, 1, sigma=1.0) == UNSUPPORTED
     assert VB(100, 200, 256, 1, sigma=1.0) == UNSUPPORTED
     assert VB(100, 200, 257, 1, sigma=1.0) == INVALID
+
+
+# ------------------------------------------------ min / max / arg-min / K-min
+
+@pytest.mark.parametrize("red", ["min", "max", "argmin", "argmax"])
+def test_extreme_pairs(lib, red):
+    assert V("gauss", red, 100, 200, 3, 4, sigma=0.3) == OK
+    assert V("laplace", red, 100, 200, 16, 64, sigma=0.3) == OK
+    assert V("sqdist", red, 100, 200, 3, 2) == OK                  # with b
+    assert V("sqdist", red, 100, 200, 3, 0, b=None) == OK          # F = d, E ignored
+    assert V("sinkhorn", red, 100, 200, 3, 1, eps=0.1) == OK
+    assert V("sinkhorn", red, 100, 200, 3, 2, eps=0.1) == INVALID  # one column
+    assert V("gauss", red, 100, 200, 3, 4, b=None, sigma=0.3) == INVALID
+    assert V("gauss", red, 100, 200, 3, 0, sigma=0.3) == INVALID
+    assert V("gauss", red, 100, 200, 3, 1, sigma=0.0) == INVALID
+    assert V("gauss_gradx", red, 100, 200, 3, 1, sigma=0.3) == UNSUPPORTED
+    # D > 16: only the squared distance's min / arg-min without b
+    assert V("gauss", red, 100, 200, 17, 1, sigma=0.3) == UNSUPPORTED
+    expect = OK if red in ("min", "argmin") else UNSUPPORTED
+    assert V("sqdist", red, 100, 200, 64, 0, b=None) == expect
+
+
+def test_kmin_pairs(lib):
+    assert V("sqdist", "kmin", 100, 200, 3, 0, b=None, K=10) == OK
+    assert V("sqdist", "kmin", 100, 200, 128, 0, b=None, K=64) == OK
+    assert V("sqdist", "kmin", 100, 200, 3, 0, K=10) == INVALID          # b must be NULL
+    assert V("sqdist", "kmin", 100, 5, 3, 0, b=None, K=10) == INVALID    # K > N
+    assert V("sqdist", "kmin", 100, 0, 3, 0, b=None, K=1) == INVALID     # N = 0
+    assert V("gauss", "kmin", 100, 200, 3, 0, b=None, K=10, sigma=1.0) == UNSUPPORTED
+    assert V("sqdist", 8, 100, 200, 3, 0, b=None, K=10) == INVALID       # unknown reduction
+
+
+def test_extreme_output_shapes(lib):
+    assert kred.output_shape("gauss", "max", 10, 3, 4) == (10, 4)
+    assert kred.output_shape("sqdist", "argmin", 10, 3, 0) == (10, 1)
+    assert kred.output_shape("sinkhorn", "max", 10, 3, 1) == (10, 1)
+    assert kred.output_shape("sqdist", "kmin", 10, 3, 0, K=7) == (10, 7)
+    assert kred.scratch_bytes("sqdist", "min", 1000, 2000, 64, 0) > 0
+    assert kred.scratch_bytes("sqdist", "argmax", 1000, 2000, 64, 0) == -1
