@@ -66,6 +66,9 @@ def _load():
                                            ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                            ctypes.c_int, _dp, _dp, _dp, _i64p, ctypes.c_int64,
                                            _dp, _i64p, _dp]
+            lib.oracle_kernel_lse.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_int64,
+                                              ctypes.c_int64, ctypes.c_int, _dp, _dp, _dp, _i64p,
+                                              ctypes.c_int64, _dp, _dp]
             lib.oracle_sinkhorn_lse.argtypes = [ctypes.c_double, ctypes.c_int64, ctypes.c_int64,
                                                 ctypes.c_int, _dp, _dp, _dp, _i64p,
                                                 ctypes.c_int64, _dp, _dp]
@@ -74,7 +77,8 @@ def _load():
                                            _i64p, _dp]
             lib.oracle_num_threads.restype = ctypes.c_int
             for f in (lib.oracle_kernel_sum, lib.oracle_gauss_gradx, lib.oracle_gauss_vjp,
-                      lib.oracle_extreme, lib.oracle_sinkhorn_lse, lib.oracle_argkmin):
+                      lib.oracle_extreme, lib.oracle_kernel_lse, lib.oracle_sinkhorn_lse,
+                      lib.oracle_argkmin):
                 f.restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -208,6 +212,23 @@ def sinkhorn_lse(x, y, g, eps, rows=None):
     out = np.empty(nr); mx = np.empty(nr)
     _check(_load().oracle_sinkhorn_lse(float(eps), M, N, D, _ptr(x), _ptr(y), _ptr(g),
                                        _ptr(r, _i64p), nr, _ptr(out), _ptr(mx)))
+    return out, mx
+
+
+def kernel_lse(formula, x, y, g, sigma, rows=None):
+    """Log-domain kernel sum a_i = log sum_j k_ij exp(g_j) for "gauss" or "laplace".
+
+    Returns (a, m): a (nrows,) and the row maxima m_i = max_j (g_j + log k_ij).
+    """
+    fcode = _FORMULAS[formula]
+    x = _f64(x); y = _f64(y)
+    M, D = x.shape
+    N = y.shape[0]
+    g = _f64(g).reshape(N)
+    r, nr = _rows(rows, M)
+    out = np.empty(nr); mx = np.empty(nr)
+    _check(_load().oracle_kernel_lse(fcode, float(sigma), M, N, D, _ptr(x), _ptr(y), _ptr(g),
+                                     _ptr(r, _i64p), nr, _ptr(out), _ptr(mx)))
     return out, mx
 
 

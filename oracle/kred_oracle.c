@@ -203,6 +203,43 @@ int oracle_sinkhorn_lse(double eps, int64_t M, int64_t N, int D,
 }
 
 /*
+ * Log-sum-exp reduction of Eq. (2) for the log-domain kernel sums: with
+ * weights g_j in the log domain,
+ *   a_i = log sum_j k_ij exp(g_j) = log sum_j exp(s_ij),  s_ij = g_j + log k_ij,
+ * for the Gaussian (log k = -d / (2 sigma^2), formula 0) and the Laplacian
+ * (log k = -sqrt(d) / sigma, formula 1) kernels, d = |x_i - y_j|^2.  Two
+ * passes as in the Sinkhorn-form routine above: the row maximum m_i, then
+ * m_i + log sum_j exp(s_ij - m_i).  out, maxv (may be NULL): nrows.
+ */
+int oracle_kernel_lse(int formula, double sigma, int64_t M, int64_t N, int D,
+                      const double* x, const double* y, const double* g,
+                      const int64_t* rows, int64_t nrows, double* out, double* maxv) {
+  if (D < 1 || nrows < 0 || !(sigma > 0.0)) return -1;
+  if (formula != ORACLE_GAUSS && formula != ORACLE_LAPLACE) return -1;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int64_t r = 0; r < nrows; ++r) {
+    const int64_t i = row_of(rows, r);
+    const double* xi = x + i * D;
+    double m = -INFINITY;
+    for (int64_t j = 0; j < N; ++j) {
+      const double d = sq_dist(xi, y + j * D, D);
+      const double s = g[j] + (formula == ORACLE_GAUSS ? -d / (2.0 * sigma * sigma) : -sqrt(d) / sigma);
+      if (s > m) m = s;
+    }
+    double acc = 0.0;
+    for (int64_t j = 0; j < N; ++j) {
+      const double d = sq_dist(xi, y + j * D, D);
+      const double s = g[j] + (formula == ORACLE_GAUSS ? -d / (2.0 * sigma * sigma) : -sqrt(d) / sigma);
+      acc += exp(s - m);
+    }
+    out[r] = (N > 0) ? m + log(acc) : -INFINITY;
+    if (maxv) maxv[r] = m;
+  }
+  (void)M;
+  return 0;
+}
+
+/*
  * Min, max, arg-min and arg-max reductions of Eq. (2) (Sec. 2 lists .min(),
  * .max() and .argmin() beside the sum): for each selected row i and each
  * component e of the formula, the extreme value over j of F_ije and the

@@ -265,6 +265,35 @@ def test_vjp_linear_in_cotangent_and_signal(oracle_mod):
     np.testing.assert_allclose(gp, g1, rtol=1e-13, atol=1e-15)
 
 
+@pytest.mark.parametrize("formula", ["gauss", "laplace"])
+def test_kernel_lse_is_log_of_kernel_sum(oracle_mod, formula):
+    # log sum_j k_ij exp(g_j) against the (pinned) kernel sum with b = exp(g)
+    rng = np.random.default_rng(17)
+    x = rng.uniform(0, 1, (10, 3)); y = rng.uniform(0, 1, (45, 3)); g = rng.normal(size=(45, 1))
+    a, m = oracle_mod.kernel_lse(formula, x, y, g, 0.2)
+    s, _ = oracle_mod.kernel_sum(formula, x, y, np.exp(g), sigma=0.2)
+    np.testing.assert_allclose(a, np.log(s[:, 0]), rtol=1e-13)
+
+
+def test_kernel_lse_gauss_is_sinkhorn_form(oracle_mod):
+    # g_j - d / (2 sigma^2) is the Sinkhorn-form formula with eps = 2 sigma^2,
+    # also far outside exp's range (g shifted by 1e4)
+    rng = np.random.default_rng(18)
+    x = rng.uniform(0, 1, (8, 2)); y = rng.uniform(0, 1, (30, 2)); g = rng.normal(size=(30, 1)) + 1e4
+    a, m = oracle_mod.kernel_lse("gauss", x, y, g, 0.1)
+    a2, m2 = oracle_mod.sinkhorn_lse(x, y, g, 2 * 0.1 ** 2)
+    np.testing.assert_allclose(a, a2, rtol=1e-15)
+    np.testing.assert_allclose(m, m2, rtol=1e-15)
+
+
+def test_kernel_lse_laplace_two_points(oracle_mod):
+    # closed form: log(exp(0 - 0) + exp(1 - 5/5)) = log 2 with |y_1 - x| = 5
+    x = np.zeros((1, 2)); y = np.array([[0.0, 0.0], [3.0, 4.0]]); g = np.array([[0.0], [1.0]])
+    a, m = oracle_mod.kernel_lse("laplace", x, y, g, 5.0)
+    assert a[0] == pytest.approx(math.log(2.0), rel=1e-15)
+    assert m[0] == 0.0
+
+
 # ------------------------------------------------------------ min / max / arg-min
 
 def test_extreme_hand_values(oracle_mod, hv):
