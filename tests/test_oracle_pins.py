@@ -273,6 +273,9 @@ def test_kernel_lse_is_log_of_kernel_sum(oracle_mod, formula):
     a, m = oracle_mod.kernel_lse(formula, x, y, g, 0.2)
     s, _ = oracle_mod.kernel_sum(formula, x, y, np.exp(g), sigma=0.2)
     np.testing.assert_allclose(a, np.log(s[:, 0]), rtol=1e-13)
+    # and the row maximum is the log of the largest term k_ij exp(g_j)
+    v, _, _ = oracle_mod.extreme(formula, "max", x, y, np.exp(g), param=0.2)
+    np.testing.assert_allclose(m, np.log(v[:, 0]), rtol=1e-12, atol=1e-14)
 
 
 def test_kernel_lse_gauss_is_sinkhorn_form(oracle_mod):
