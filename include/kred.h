@@ -119,6 +119,9 @@ kred_status kred_destroy(kred_ctx* ctx);
  *        out[i, 1 + k] = sum_j k_ij b_j (y_jk - x_ik) / sigma^2 = d a_i / d x_ik.
  *   (SINKHORN, LSE), E = 1:  b holds g (N x 1), out is fp32 M x 1:
  *        out[i] = log sum_j exp(g_j - |x_i - y_j|^2 / eps)   (natural log).
+ *   (GAUSS | LAPLACE, LSE), E = 1:  the log-domain kernel sum with weights g
+ *        in b: out[i] = log sum_j k_ij exp(g_j), i.e. log sum_j exp(g_j -
+ *        |x_i - y_j|^2 / (2 sigma^2)) or log sum_j exp(g_j - |x_i - y_j| / sigma).
  *   (SQDIST, ARGKMIN):  b must be NULL and E is ignored (pass 0), out is int32
  *        M x K: the indices j of the K smallest |x_i - y_j|^2, ascending by
  *        (distance, index): equal distances keep the lower index first.
@@ -137,7 +140,8 @@ kred_status kred_destroy(kred_ctx* ctx);
  * Ranges: 0 <= M, N <= 2^31 - 1; 1 <= D <= KRED_MAX_D; 1 <= E <= KRED_MAX_E
  * where b has E columns; p->col_blocks in [0, KRED_MAX_COL_BLOCKS].  D > 16
  * is supported by the sums, ARGKMIN, KMIN, and MIN / ARGMIN of SQDIST without
- * b; the other pairs return KRED_ERR_UNSUPPORTED there.  Inputs must be
+ * b; the other pairs (GAUSS_GRADX and every LSE among them) return
+ * KRED_ERR_UNSUPPORTED there.  Inputs must be
  * finite (NaN or Inf in x, y or b gives an undefined result).
  * Edge cases: M = 0 returns KRED_OK and touches nothing.  N = 0 writes zeros
  * (SUM), -infinity (LSE, MAX), +infinity (MIN) or -1 (ARGMIN, ARGMAX) and

@@ -174,6 +174,7 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(combine_gradx_kernel, dim3(grid_for(a.M * (1 + a.D))), dim3(256), 0, s, a);
       break;
     case F_SINKHORN:
+    case F_LAPLACE_LSE:
       hipLaunchKernelGGL(combine_lse_kernel, dim3(grid_for(a.M)), dim3(256), 0, s, a);
       break;
     case F_VJP:

@@ -439,10 +439,18 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const float* __restrict
 }
 
 // ------------------------------------------------ Sinkhorn log-sum-exp
-// In log2 units: s_ij = g'_j - ks d_ij with g' = g log2(e), ks = log2(e) / eps.
+// In log2 units: s_ij = g'_j - ks d_ij with g' = g log2(e), ks = log2(e) / eps
+// (LAP: s_ij = g'_j - ks sqrt(d_ij), ks = log2(e) / sigma).
 // Running reference m_i (<= max_j s_ij + kRescale): terms are 2^(s - m);
 // when a term would exceed 2^kRescale the sums are rescaled and m moves up.
-template <int DP, int R>
+template <int DP, bool LAP>
+__device__ __forceinline__ float lse_dist(const float (&xr)[DP], const float* yv) {
+  const float d = sq_dist<DP>(xr, yv);
+  if constexpr (LAP) return fast_sqrt(d);
+  else return d;
+}
+
+template <int DP, int R, bool LAP>
 __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
@@ -459,7 +467,7 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
     for (int s = 0; s < S; ++s) yv[s] = y0[s];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      m[r] = __builtin_fmaf(-a.kscale, sq_dist<DP>(xr[r], yv), yv[DP]);
+      m[r] = __builtin_fmaf(-a.kscale, lse_dist<DP, LAP>(xr[r], yv), yv[DP]);
       tot[r] = 0.0f;
       part[r] = 1.0f;
     }
@@ -472,7 +480,7 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
         bool big = false;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-          const float u = __builtin_fmaf(-a.kscale, sq_dist<DP>(xr[r], yv), yv[DP] - m[r]);
+          const float u = __builtin_fmaf(-a.kscale, lse_dist<DP, LAP>(xr[r], yv), yv[DP] - m[r]);
           uu[r] = u;
           big |= (u > kRescale);
         }
@@ -688,7 +696,7 @@ constexpr int pow2_floor(int v) { return v >= 8 ? 8 : v >= 4 ? 4 : v >= 2 ? 2 : 
 constexpr int rows_for(int formula, int DP, int EP, int KP) {
   const int state = formula == F_GRADX      ? DP + 2 * (DP + 1)
                     : formula == F_VJP      ? DP + EP + 2 * DP
-                    : formula == F_SINKHORN ? DP + 3
+                    : (formula == F_SINKHORN || formula == F_LAPLACE_LSE) ? DP + 3
                     : KP > 0                ? DP + 2 * KP
                                             : DP + 2 * EP;
   const int budget = (EP >= 16 && KP == 0) ? kWideStateBudget : kStateBudget;
@@ -770,8 +778,12 @@ hipError_t launch_dp(const DirectArgs& a, dim3 grid, hipStream_t s) {
                          0, s, a);
       return hipGetLastError();
     case F_SINKHORN:
-      hipLaunchKernelGGL((lse_kernel<DP, rows_for(F_SINKHORN, DP, 1, 0)>), grid, dim3(kThreads),
-                         0, s, a);
+      hipLaunchKernelGGL((lse_kernel<DP, rows_for(F_SINKHORN, DP, 1, 0), false>), grid,
+                         dim3(kThreads), 0, s, a);
+      return hipGetLastError();
+    case F_LAPLACE_LSE:
+      hipLaunchKernelGGL((lse_kernel<DP, rows_for(F_LAPLACE_LSE, DP, 1, 0), true>), grid,
+                         dim3(kThreads), 0, s, a);
       return hipGetLastError();
     case F_VJP:
       switch (a.EP) {
@@ -817,7 +829,7 @@ int partial_width(int formula, int DP, int EP, int KP, int ext) {
   if (ext) return 2 * EP;
   if (formula == F_GRADX) return DP + 1;
   if (formula == F_VJP) return DP;
-  if (formula == F_SINKHORN) return 2;
+  if (formula == F_SINKHORN || formula == F_LAPLACE_LSE) return 2;
   return EP;
 }
 

@@ -91,13 +91,15 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
     q.KP = knn_pad_k(p->K);
     q.E = 0;
   }
-  if (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN) q.E = 1;
+  if (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN || r == KRED_R_LSE) q.E = 1;
   const int ext = is_extreme(r) ? 1 : 0;
+  // kernel-side formula: log-sum-exps run on the Sinkhorn-form kernels
+  const int kf = (r == KRED_R_LSE) ? (f == KRED_F_LAPLACE ? F_LAPLACE_LSE : F_SINKHORN) : (int)f;
   const int EP_first = (r == KRED_R_ARGKMIN) ? 1 : direct_pad_e(std::min(q.E, 16));
   q.S_max = q.DP + EP_first;
-  q.W_max = partial_width(q.formula, q.DP, EP_first, q.KP, ext);
+  q.W_max = partial_width(kf, q.DP, EP_first, q.KP, ext);
   const int R = ext ? direct_rows_per_thread(F_SQDIST, q.DP, EP_first, 0)
-                    : direct_rows_per_thread(q.formula, q.DP, EP_first, q.KP);
+                    : direct_rows_per_thread(kf, q.DP, EP_first, q.KP);
   const int64_t rows = rows_override > 0 ? rows_override : (int64_t)kThreads * R;
   const int64_t row_blocks = (M + rows - 1) / rows;
   q.C = choose_col_blocks(std::max<int64_t>(1, row_blocks), N, num_cus, p->col_blocks);
@@ -138,6 +140,7 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
     default:
       break;
   }
+  if (r == KRED_R_LSE) q.bscale = (float)log2e;   // log-domain weights g' = g log2(e)
   if (ext) {
     // min of sign * F in natural units: the sign rides on the packed b (and
     // on kscale for the log-sum-exp formula, f = sign g - (sign / eps) d)
@@ -160,7 +163,7 @@ int fast_epi(kred_formula f, kred_reduction r, int64_t M, int64_t N, int32_t D, 
   if (!(flags & KRED_FLAG_FAST) && (double)M * (double)N < kFastMinPairs) return -1;
   if (f == KRED_F_GAUSS && r == KRED_R_SUM && E == 1) return FAST_SUM;
   if (f == KRED_F_GAUSS_GRADX && r == KRED_R_SUM) return FAST_GRADX;
-  if (f == KRED_F_SINKHORN && r == KRED_R_LSE) return FAST_LSE;
+  if ((f == KRED_F_SINKHORN || f == KRED_F_GAUSS) && r == KRED_R_LSE) return FAST_LSE;
   return -1;
 }
 
@@ -417,6 +420,8 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   }
   const bool ext = is_extreme(r);
   if (ext && (b == nullptr || f == KRED_F_SINKHORN)) E = 1;   // one output column
+  // kernel-side formula: log-sum-exps run on the Sinkhorn-form kernels
+  const int kf = (r == KRED_R_LSE) ? (f == KRED_F_LAPLACE ? F_LAPLACE_LSE : F_SINKHORN) : (int)f;
 
   if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s, kvalues);
 
@@ -493,7 +498,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     if (launch_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
 
     DirectArgs da{};
-    da.formula = (int)f;
+    da.formula = kf;
     da.D = D;
     da.DP = pl.DP;
     da.E = pl.E;
@@ -533,12 +538,12 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
                          : ext                       ? "extreme_kernel"
                          : (r == KRED_R_ARGKMIN)     ? "knn_kernel"
                          : (f == KRED_F_GAUSS_GRADX) ? "gradx_kernel"
-                         : (f == KRED_F_SINKHORN)    ? "lse_kernel"
+                         : (r == KRED_R_LSE)         ? "lse_kernel"
                                                      : "sum_kernel";
     }
     if (pl.C > 1) {
       CombineArgs ca{};
-      ca.formula = (int)f;
+      ca.formula = kf;
       ca.D = D;
       ca.DP = pl.DP;
       ca.E = pl.E;
@@ -691,9 +696,10 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
   } else if (r == KRED_R_SUM && f == KRED_F_GAUSS_GRADX) {
     if (E != 1) return KRED_ERR_INVALID_ARG;
     if (!finite_pos(p->sigma)) return KRED_ERR_INVALID_ARG;
-  } else if (r == KRED_R_LSE && f == KRED_F_SINKHORN) {
+  } else if (r == KRED_R_LSE &&
+             (f == KRED_F_SINKHORN || f == KRED_F_GAUSS || f == KRED_F_LAPLACE)) {
     if (E != 1) return KRED_ERR_INVALID_ARG;
-    if (!finite_pos(p->eps)) return KRED_ERR_INVALID_ARG;
+    if (!finite_pos(f == KRED_F_SINKHORN ? p->eps : p->sigma)) return KRED_ERR_INVALID_ARG;
   } else if ((r == KRED_R_ARGKMIN || r == KRED_R_KMIN) && f == KRED_F_SQDIST) {
     if (b != nullptr) return KRED_ERR_INVALID_ARG;
     if (p->K < 1 || p->K > KRED_MAX_K || p->K > N) return KRED_ERR_INVALID_ARG;
@@ -716,7 +722,7 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
   const bool lists = f == KRED_F_SQDIST && b == nullptr &&
                      (r == KRED_R_ARGKMIN || r == KRED_R_KMIN || r == KRED_R_MIN ||
                       r == KRED_R_ARGMIN);
-  if (D > kMaxDirectD && (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN ||
+  if (D > kMaxDirectD && (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN || r == KRED_R_LSE ||
                           (is_extreme(r) && !lists)))
     return KRED_ERR_UNSUPPORTED;
   if (M == 0) return KRED_OK;

@@ -6,9 +6,14 @@
 
 namespace kred {
 
-// Formula codes used inside the kernels (same values as the public enum;
-// F_VJP, the vector-Jacobian product of the Gaussian sum in x, is internal).
-enum : int { F_GAUSS = 0, F_LAPLACE = 1, F_SQDIST = 2, F_GRADX = 3, F_SINKHORN = 4, F_VJP = 5 };
+// Formula codes used inside the kernels (same values as the public enum).
+// Internal ones: F_VJP, the vector-Jacobian product of the Gaussian sum in x;
+// F_LAPLACE_LSE, the log-sum-exp of g_j - |x_i - y_j| / sigma (the Gaussian's
+// log-sum-exp, g_j - |x_i - y_j|^2 / (2 sigma^2), runs as F_SINKHORN).
+enum : int {
+  F_GAUSS = 0, F_LAPLACE = 1, F_SQDIST = 2, F_GRADX = 3, F_SINKHORN = 4, F_VJP = 5,
+  F_LAPLACE_LSE = 6
+};
 
 constexpr int kThreads = 256;          // threads per workgroup for the direct-form kernels
 constexpr float kLog2e = 1.4426950408889634f;

@@ -61,10 +61,10 @@ def test_valid_argkmin(lib):
 
 
 @pytest.mark.parametrize("formula,reduction", [
-    ("gauss", "lse"), ("gauss", "argkmin"), ("laplace", "argkmin"), ("sinkhorn", "sum"),
+    ("gauss", "kmin"), ("gauss", "argkmin"), ("laplace", "argkmin"), ("sinkhorn", "sum"),
     ("gauss_gradx", "lse"), ("sqdist", "lse")])
 def test_unsupported_pairs(lib, formula, reduction):
-    b = None if reduction == "argkmin" else 1
+    b = None if reduction in ("argkmin", "kmin") else 16
     assert V(formula, reduction, 10, 10, 3, 1, b=b, K=1, sigma=1.0, eps=1.0) == UNSUPPORTED
 
 
@@ -205,3 +205,13 @@ def test_extreme_output_shapes(lib):
     assert kred.output_shape("sqdist", "kmin", 10, 3, 0, K=7) == (10, 7)
     assert kred.scratch_bytes("sqdist", "min", 1000, 2000, 64, 0) > 0
     assert kred.scratch_bytes("sqdist", "argmax", 1000, 2000, 64, 0) == -1
+
+
+def test_kernel_lse_pairs(lib):
+    assert V("gauss", "lse", 100, 200, 3, 1, sigma=0.1) == OK
+    assert V("laplace", "lse", 100, 200, 16, 1, sigma=0.1) == OK
+    assert V("gauss", "lse", 100, 200, 3, 2, sigma=0.1) == INVALID
+    assert V("laplace", "lse", 100, 200, 3, 1, sigma=0.0) == INVALID
+    assert V("gauss", "lse", 100, 200, 3, 1, sigma=0.1, b=None) == INVALID
+    assert V("sqdist", "lse", 100, 200, 3, 1) == UNSUPPORTED
+    assert V("gauss", "lse", 100, 200, 17, 1, sigma=0.1) == UNSUPPORTED
