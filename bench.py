@@ -54,9 +54,14 @@ WORKLOADS = {
                      None, 48 + 48 + 42, "alu",
                      "gaussian backward (x, y, b gradients), E=16 cotangent, uniform [0,1]^3, "
                      "2e5 x 2e5, D=3"),
+    # one direction of a Chamfer distance: each query's nearest squared distance
+    "chamfer": ("mixture_gauss", dict(M=1_000_000, N=1_000_000, D=3, sigma=0.05), "sqdist", "min",
+                9, "alu", "nearest-neighbour squared distance (min reduction, no b), mixture of 8 "
+                          "Gaussians, 1e6 x 1e6, D=3"),
 }
 # the three reductions of a backward step: (rows, columns) = (M, N), (N, M), (N, M)
 REDUCTIONS_PER_STEP = {"backward": 3, "backward_e16": 3}
+NO_SIGNAL = {"chamfer"}   # reductions of the bare squared distance (b = NULL)
 KERNEL_SOURCES = {"sum_kernel": "k_direct.hip", "gradx_kernel": "k_direct.hip",
                   "lse_kernel": "k_direct.hip", "knn_kernel": "k_direct.hip",
                   "vjp_kernel": "k_direct.hip",
@@ -113,6 +118,8 @@ def time_steps(ctx, w, formula, reduction, steps, warmup):
     from paper_2004_11127_amd import kred
     x, y = torch.from_numpy(w.x).cuda(), torch.from_numpy(w.y).cuda()
     b = torch.from_numpy(w.b).cuda() if w.b is not None else None
+    if reduction == "min" and formula == "sqdist":
+        b = None
     stream = torch.cuda.current_stream()
     if formula == "backward":
         e = torch.from_numpy(cotangent(w)).cuda()
@@ -168,6 +175,9 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds):
             return oracle.sinkhorn_lse(w.x, w.y, w.b, w.eps, rows=rows)
         if reduction == "argkmin":
             return oracle.argkmin(w.x, w.y, w.K, rows=rows)
+        if reduction == "min":
+            val, _, scale = oracle.extreme("sqdist", "min", w.x, w.y, rows=rows)
+            return val, scale
         return oracle.kernel_sum(formula, w.x, w.y, w.b, sigma=w.sigma, rows=rows)
 
     probe = inputs.sample_rows(w.M, min(w.M, 32), seed=777)
@@ -182,6 +192,8 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds):
     got = out_gpu[rows]
     if reduction == "argkmin":
         check = {"index_mismatches_on_sample": int((got != ref).sum())}
+    elif reduction == "min":
+        check = {"max_rel_err_on_sample": float(np.max(np.abs(got - ref) / np.maximum(aux, 1e-30)))}
     elif reduction == "lse":
         check = {"max_abs_err_on_sample": float(np.max(np.abs(got[:, 0] - ref)))}
     else:
