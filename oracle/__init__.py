@@ -7,7 +7,9 @@ this package shares no code with it.
 
 The arithmetic lives in ``kred_oracle.c`` (plain C, fp64, OpenMP over rows);
 this module builds it with gcc on first use, converts fp32 inputs to fp64 and
-marshals arguments.  What each routine computes follows Charlier et al.,
+marshals arguments.  The block-sparse (cluster-wise) reductions of Sec. 3 are
+composed here from those routines: each row cluster is reduced over its
+gathered columns.  What each routine computes follows Charlier et al.,
 "Kernel Operations on the GPU, with Autodiff, without Memory Overflows"
 (arXiv:2004.11127): Eq. (1) (Gaussian kernel sum), Eq. (2) with the
 reductions of Sec. 2 (sum, log-sum-exp, arg-K-min), and the x-gradient of
@@ -247,3 +249,83 @@ def argkmin(x, y, K, rows=None):
     _check(_load().oracle_argkmin(M, N, D, int(K), _ptr(x), _ptr(y), _ptr(r, _i64p), nr,
                                   _ptr(idx, _i64p), _ptr(dist)))
     return idx, dist
+
+
+def _cluster_columns(col_ptr, col_ranges, I, N):
+    """Column indices of row cluster I: its ranges, clamped to [0, N), in list order."""
+    cols = []
+    for q in range(int(col_ptr[I]), int(col_ptr[I + 1])):
+        js = min(max(int(col_ranges[q][0]), 0), N)
+        je = min(max(int(col_ranges[q][1]), js), N)
+        cols.extend(range(js, je))
+    return np.asarray(cols, dtype=np.int64)
+
+
+def ranges_reduce(kind, x, y, b, row_ranges, col_ptr, col_ranges, **kw):
+    """Block-sparse (cluster-wise) reduction.
+
+    Row cluster I is rows [row_ranges[I][0], row_ranges[I][1]); its rows reduce
+    over the columns of its ranges col_ranges[col_ptr[I] : col_ptr[I + 1]] only
+    (the paper's cluster-wise block-sparsity, Sec. 3).  Each cluster is handed
+    to the dense routine above on its gathered columns; rows outside every
+    cluster get the empty reduction.  kind:
+      "sum" (formula=, sigma=), "gradx" (sigma=), "lse" (eps=; or formula= and
+      sigma= for the log-domain kernel sums), "argkmin" / "kmin" (K=),
+      "min" / "max" (formula=, param=).
+    Returns (out, aux): out as the library writes it; aux the normaliser (sums,
+    gradient), the row maximum (log-sum-exp) or the index array (min / max).
+    """
+    x = np.asarray(x); y = np.asarray(y)
+    M, D = x.shape
+    N = y.shape[0]
+    R = len(row_ranges)
+    formula = kw.get("formula")
+    if kind == "sum":
+        E = b.shape[1]
+        out = np.zeros((M, E)); aux = np.zeros((M, E))
+    elif kind == "gradx":
+        out = np.zeros((M, 1 + D)); aux = np.zeros((M, 1 + D))
+    elif kind == "lse":
+        out = np.full(M, -np.inf); aux = np.full(M, -np.inf)
+    elif kind in ("argkmin", "kmin"):
+        K = kw["K"]
+        out = np.full((M, K), -1 if kind == "argkmin" else np.inf)
+        aux = None
+    else:
+        E = 1 if b is None or formula == "sinkhorn" else b.shape[1]
+        out = np.full((M, E), np.inf if kind == "min" else -np.inf)
+        aux = np.full((M, E), -1, dtype=np.int64)
+    for I in range(R):
+        r0 = min(max(int(row_ranges[I][0]), 0), M)
+        r1 = min(max(int(row_ranges[I][1]), r0), M)
+        if r1 <= r0:
+            continue
+        cols = _cluster_columns(col_ptr, col_ranges, I, N)
+        xs = x[r0:r1]
+        if cols.size == 0:
+            continue
+        ys = y[cols]
+        bs = None if b is None else np.asarray(b)[cols]
+        if kind == "sum":
+            o, n = kernel_sum(formula, xs, ys, bs, sigma=kw.get("sigma", 1.0))
+            out[r0:r1] = o; aux[r0:r1] = n
+        elif kind == "gradx":
+            o, n = gauss_gradx(xs, ys, bs, kw["sigma"])
+            out[r0:r1] = o; aux[r0:r1] = n
+        elif kind == "lse":
+            if formula in ("gauss", "laplace"):
+                o, m = kernel_lse(formula, xs, ys, bs, kw["sigma"])
+            else:
+                o, m = sinkhorn_lse(xs, ys, bs, kw["eps"])
+            out[r0:r1] = o; aux[r0:r1] = m
+        elif kind in ("argkmin", "kmin"):
+            K = min(kw["K"], cols.size)
+            idx, dist = argkmin(xs, ys, K)
+            if kind == "argkmin":
+                out[r0:r1, :K] = cols[idx]
+            else:
+                out[r0:r1, :K] = dist
+        else:
+            v, i, _ = extreme(formula, kind, xs, ys, bs, param=kw.get("param", 1.0))
+            out[r0:r1] = v; aux[r0:r1] = cols[i]
+    return out, aux

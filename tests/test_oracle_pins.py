@@ -459,3 +459,83 @@ def test_argkmin_rejects_bad_k(oracle_mod):
         oracle_mod.argkmin(x, y, 4)
     with pytest.raises(ValueError):
         oracle_mod.argkmin(x, y, 0)
+
+
+# ---------------------------------------------------------- block-sparse ranges
+
+def _random_ranges(rng, M, N, n_rc, n_cc):
+    """Row clusters covering part of [0, M) and, per cluster, sorted disjoint column ranges."""
+    rcuts = np.sort(rng.choice(np.arange(1, M), n_rc * 2 - 1, replace=False))
+    rcuts = np.concatenate([[0], rcuts, [M]])
+    rows = [(int(rcuts[2 * i]), int(rcuts[2 * i + 1])) for i in range(n_rc)]   # gaps between clusters
+    ccuts = np.concatenate([[0], np.sort(rng.choice(np.arange(1, N), n_cc - 1, replace=False)), [N]])
+    cblocks = [(int(ccuts[k]), int(ccuts[k + 1])) for k in range(n_cc)]
+    ptr, cr = [0], []
+    for i in range(n_rc):
+        keep = sorted(rng.choice(n_cc, rng.integers(0, n_cc + 1), replace=False))
+        cr.extend(cblocks[k] for k in keep)
+        ptr.append(len(cr))
+    return np.array(rows), np.array(ptr), np.array(cr).reshape(-1, 2)
+
+
+def _row_mask(rows, ptr, cr, M, N):
+    mask = np.zeros((M, N), dtype=bool)
+    covered = np.zeros(M, dtype=bool)
+    for I, (r0, r1) in enumerate(rows):
+        covered[r0:r1] = True
+        for q in range(ptr[I], ptr[I + 1]):
+            mask[r0:r1, cr[q][0]:cr[q][1]] = True
+    return mask, covered
+
+
+def test_ranges_full_cover_is_dense(oracle_mod):
+    rng = np.random.default_rng(20)
+    x = rng.uniform(0, 1, (30, 3)); y = rng.uniform(0, 1, (50, 3)); b = rng.normal(size=(50, 2))
+    rows, ptr, cr = np.array([[0, 30]]), np.array([0, 1]), np.array([[0, 50]])
+    a, n = oracle_mod.ranges_reduce("sum", x, y, b, rows, ptr, cr, formula="gauss", sigma=0.3)
+    a2, n2 = oracle_mod.kernel_sum("gauss", x, y, b, sigma=0.3)
+    np.testing.assert_array_equal(a, a2)
+    idx, _ = oracle_mod.ranges_reduce("argkmin", x, y, None, rows, ptr, cr, K=4)
+    idx2, _ = oracle_mod.argkmin(x, y, 4)
+    np.testing.assert_array_equal(idx, idx2)
+
+
+def test_ranges_sum_equals_masked_dense_rows(oracle_mod):
+    # a_i over the allowed columns = the dense sum of row i with b zeroed
+    # outside them; rows outside every cluster are 0
+    rng = np.random.default_rng(21)
+    M, N = 40, 60
+    x = rng.uniform(0, 1, (M, 2)); y = rng.uniform(0, 1, (N, 2)); b = rng.normal(size=(N, 3))
+    rows, ptr, cr = _random_ranges(rng, M, N, 4, 5)
+    mask, covered = _row_mask(rows, ptr, cr, M, N)
+    a, _ = oracle_mod.ranges_reduce("sum", x, y, b, rows, ptr, cr, formula="laplace", sigma=0.4)
+    for i in range(M):
+        ref, _ = oracle_mod.kernel_sum("laplace", x[i:i + 1], y, b * mask[i][:, None], sigma=0.4)
+        np.testing.assert_allclose(a[i], ref[0], rtol=1e-13, atol=1e-15)
+    assert (a[~covered] == 0).all()
+
+
+def test_ranges_lse_equals_masked_log_weights(oracle_mod):
+    # columns outside the pattern get log-weight -inf (their terms vanish)
+    rng = np.random.default_rng(22)
+    M, N = 35, 50
+    x = rng.uniform(0, 1, (M, 3)); y = rng.uniform(0, 1, (N, 3)); g = rng.normal(size=(N, 1))
+    rows, ptr, cr = _random_ranges(rng, M, N, 3, 4)
+    mask, covered = _row_mask(rows, ptr, cr, M, N)
+    a, _ = oracle_mod.ranges_reduce("lse", x, y, g, rows, ptr, cr, eps=0.05)
+    for i in range(M):
+        if not mask[i].any():
+            assert a[i] == -np.inf
+            continue
+        gi = np.where(mask[i][:, None], g, -np.inf)
+        keep = mask[i]
+        ref, _ = oracle_mod.sinkhorn_lse(x[i:i + 1], y[keep], gi[keep], 0.05)
+        assert a[i] == pytest.approx(ref[0], rel=1e-14)
+
+
+def test_ranges_argkmin_maps_back_to_global_indices(oracle_mod):
+    # indices are global column indices; a cluster with fewer than K columns pads with -1
+    x = np.array([[0.0], [10.0]]); y = np.arange(12, dtype=np.float64).reshape(12, 1)
+    rows, ptr, cr = np.array([[0, 1], [1, 2]]), np.array([0, 2, 3]), np.array([[8, 10], [2, 4], [11, 12]])
+    idx, _ = oracle_mod.ranges_reduce("argkmin", x, y, None, rows, ptr, cr, K=3)
+    np.testing.assert_array_equal(idx, [[2, 3, 8], [11, -1, -1]])
