@@ -160,6 +160,43 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
                      void* stream);
 
 /*
+ * Block-sparse reduction (the cluster-wise block-sparsity patterns and the
+ * block-sparse truncation rule of Sec. 3): kred_run restricted to a pattern
+ * of (row cluster, column range) blocks.  Row cluster I = 0..nr-1 is the rows
+ * [row_ranges[2I], row_ranges[2I+1]); its rows reduce over the columns of the
+ * ranges [col_ranges[2q], col_ranges[2q+1]) for q in [col_ptr[I],
+ * col_ptr[I+1]) only, as if F_ij were absent elsewhere.  Typical use: sort the
+ * points by cluster, and list for each cluster of x the clusters of y whose
+ * centroids are near enough (a truncation rule for a fast-decaying kernel).
+ *
+ * The three index arrays are int32 in device memory (row_ranges nr x 2,
+ * col_ptr nr + 1, col_ranges col_ptr[nr] x 2), read by the kernels; the host
+ * never dereferences them.  Row clusters must be disjoint; the column ranges
+ * of a cluster should be sorted and disjoint for the arg-reductions' lowest-
+ * index tie rule (otherwise ties resolve in list order).  Ranges are clamped
+ * to [0, M) and [0, N); overlapping row clusters give an undefined result.
+ * Rows in no cluster, and clusters without columns, hold the empty reduction
+ * (as for N = 0; arg-K-min / K-min pad short lists with -1 / +infinity).
+ *
+ * Every pair kred_run accepts with D <= 16 (larger D: KRED_ERR_UNSUPPORTED);
+ * the direct-form kernels run, without column split.  Arguments, layouts,
+ * errors and asynchrony otherwise as kred_run; nr = 0 leaves every row empty.
+ */
+kred_status kred_run_ranges(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
+                            int64_t M, int64_t N, int32_t D, int32_t E,
+                            const float* x, const float* y, const float* b, void* out,
+                            int32_t nr, const int32_t* row_ranges, const int32_t* col_ptr,
+                            const int32_t* col_ranges, void* stream);
+
+/* Host-only argument check of kred_run_ranges (the index arrays are only
+ * checked for null and alignment). */
+kred_status kred_validate_ranges(kred_formula f, kred_reduction r, const kred_params* p,
+                                 int64_t M, int64_t N, int32_t D, int32_t E,
+                                 const void* x, const void* y, const void* b, const void* out,
+                                 int32_t nr, const void* row_ranges, const void* col_ptr,
+                                 const void* col_ranges);
+
+/*
  * Host-only argument check with the same rules kred_run applies (kred_run
  * calls it first).  Touches no device and dereferences no array pointer, so
  * it runs on machines without a GPU.  Returns KRED_OK or the error kred_run

@@ -151,13 +151,66 @@ __device__ __forceinline__ void stream_columns(const float* __restrict__ ypk, in
 }
 
 // -------------------------------------------------------- common row set-up
-// Row r of a lane is rb * 256 R + r * 256 + threadIdx.x (rows of one r are
-// contiguous across the block, so loads and stores coalesce).  Indices are
-// recomputed where needed instead of being held in registers: the pair loop
-// runs at its best issue rate only with enough waves resident per SIMD.
+// Work item of a block.
+//   Dense: row block rb and column block c (consecutive blocks take
+//   consecutive column blocks, so with C a multiple of 8 each XCD streams its
+//   own share of the columns through its L2).
+//   Block-sparse: one row block inside row cluster I; its reduction runs over
+//   I's list of column ranges (ranges are clamped to [0, N), rows to [0, M)).
+// Row r of a lane is row0 + r * 256 + threadIdx.x (rows of one r are
+// contiguous across the block, so loads and stores coalesce), valid below
+// row_end.  Indices are recomputed where needed instead of being held in
+// registers: the pair loop runs at its best issue rate only with enough
+// waves resident per SIMD.
+struct Item {
+  int c;                    // column block (dense; 0 when block-sparse)
+  int64_t row0, row_end;
+  int64_t j0, j1;           // dense column block
+  int nrange;               // block-sparse: number of column ranges (0: dense)
+  const int* cr;            // block-sparse: this cluster's column ranges
+  bool live;                // false: a spare workgroup of a block-sparse grid
+};
+
 template <int R>
-__device__ __forceinline__ int64_t row_of(int64_t rb, int r, int lane_id) {
-  return rb * (int64_t)(kThreads * R) + r * kThreads + lane_id;
+__device__ __forceinline__ Item item_of(const DirectArgs& a) {
+  Item it;
+  it.nrange = 0;
+  it.cr = nullptr;
+  it.live = true;
+  if (a.nr == 0) {
+    it.c = blockIdx.x % a.C;
+    const int64_t rb = blockIdx.x / a.C;
+    it.row0 = rb * (int64_t)(kThreads * R);
+    it.row_end = a.M;
+    it.j0 = (int64_t)it.c * a.jpb;
+    it.j1 = min(a.N, it.j0 + a.jpb);
+    return it;
+  }
+  it.c = 0;
+  it.j0 = it.j1 = 0;
+  const int blk = (int)blockIdx.x;
+  if (blk >= a.bstart[a.nr]) {
+    it.live = false;
+    it.row0 = it.row_end = 0;
+    return it;
+  }
+  int lo = 0, hi = a.nr - 1;   // last cluster I with bstart[I] <= blk
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.bstart[mid] <= blk) lo = mid;
+    else hi = mid - 1;
+  }
+  const int64_t r0 = min(max((int64_t)a.rr[2 * lo], (int64_t)0), a.M);
+  const int64_t r1 = min(max((int64_t)a.rr[2 * lo + 1], r0), a.M);
+  it.row0 = r0 + (int64_t)(blk - a.bstart[lo]) * (kThreads * R);
+  it.row_end = r1;
+  it.cr = a.cr + 2 * (int64_t)a.cp[lo];
+  it.nrange = a.cp[lo + 1] - a.cp[lo];
+  return it;
+}
+
+__device__ __forceinline__ int64_t row_at(const Item& it, int r, int lane_id) {
+  return it.row0 + (int64_t)r * kThreads + lane_id;
 }
 
 // threadIdx.x behind an empty asm: the compiler cannot prove it equal to the
@@ -170,11 +223,12 @@ __device__ __forceinline__ int opaque_tid() {
 }
 
 template <int DP, int R>
-__device__ __forceinline__ void load_rows(const DirectArgs& a, int64_t rb, float (&xr)[R][DP]) {
+__device__ __forceinline__ void load_rows(const DirectArgs& a, const Item& it,
+                                          float (&xr)[R][DP]) {
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int64_t row = row_of<R>(rb, r, threadIdx.x);
-    const bool ok = row < a.M;
+    const int64_t row = row_at(it, r, threadIdx.x);
+    const bool ok = row < it.row_end;
 #pragma unroll
     for (int k = 0; k < DP; ++k)
       xr[r][k] = (ok && k < a.D) ? a.x[row * a.D + k] * a.xscale : 0.0f;
@@ -193,20 +247,41 @@ __device__ __forceinline__ float sq_dist(const float (&xr)[DP], const float* yv)
   return d;
 }
 
-// Work item of a block: row block rb and column block c (consecutive blocks
-// take consecutive column blocks, so with C a multiple of 8 each XCD streams
-// its own share of the columns through its L2).
-struct Item {
-  int c;
-  int64_t rb, j0, j1;
-};
-__device__ __forceinline__ Item item_of(const DirectArgs& a) {
-  Item it;
-  it.c = blockIdx.x % a.C;
-  it.rb = blockIdx.x / a.C;
-  it.j0 = (int64_t)it.c * a.jpb;
-  it.j1 = min(a.N, it.j0 + a.jpb);
-  return it;
+// Column range q of a block-sparse item, clamped to [0, N).
+__device__ __forceinline__ void col_range(const DirectArgs& a, const Item& it, int q,
+                                          int64_t& js, int64_t& je) {
+  js = min(max((int64_t)it.cr[2 * q], (int64_t)0), a.N);
+  je = min(max((int64_t)it.cr[2 * q + 1], js), a.N);
+}
+
+// The item's columns through stream_columns: the column block, or each
+// non-empty column range in list order (`skip` applies to the first column
+// streamed).  Block-uniform, as stream_columns requires.
+template <int S, typename PairFn, typename TileEndFn>
+__device__ __forceinline__ void stream_item(const DirectArgs& a, const Item& it, int skip,
+                                            float4* lds, PairFn&& pair, TileEndFn&& tile_end) {
+  if (it.nrange == 0) {
+    stream_columns<S>(a.ypk, it.j0, it.j1, skip, lds, pair, tile_end);
+    return;
+  }
+  for (int q = 0; q < it.nrange; ++q) {
+    int64_t js, je;
+    col_range(a, it, q, js, je);
+    if (je <= js) continue;
+    stream_columns<S>(a.ypk, js, je, skip, lds, pair, tile_end);
+    skip = 0;
+  }
+}
+
+// First column of the item (-1 when it has none).
+__device__ __forceinline__ int64_t first_column(const DirectArgs& a, const Item& it) {
+  if (it.nrange == 0) return it.j0 < it.j1 ? it.j0 : -1;
+  for (int q = 0; q < it.nrange; ++q) {
+    int64_t js, je;
+    col_range(a, it, q, js, je);
+    if (je > js) return js;
+  }
+  return -1;
 }
 
 // ------------------------------------------------------- sum-type formulas
@@ -224,9 +299,10 @@ __global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
   constexpr int S = DP + EP;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
   if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
-  const Item it = item_of(a);
+  const Item it = item_of<R>(a);
+  if (!it.live) return;
   float xr[R][DP];
-  load_rows<DP, R>(a, it.rb, xr);
+  load_rows<DP, R>(a, it, xr);
   float tot[R][EP], part[R][EP];
 #pragma unroll
   for (int r = 0; r < R; ++r)
@@ -234,8 +310,8 @@ __global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
     for (int e = 0; e < EP; ++e) tot[r][e] = part[r][e] = 0.0f;
   const float ks = a.kscale;
 
-  stream_columns<S>(
-      a.ypk, it.j0, it.j1, 0, lds,
+  stream_item<S>(
+      a, it, 0, lds,
       [&](const float* yv, int64_t) {
         // distances of all R rows first (R independent chains interleave),
         // then the kernel values and accumulations
@@ -267,8 +343,8 @@ __global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
   const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int64_t row = row_of<R>(it.rb, r, tid_out);
-    if (row >= a.M) continue;
+    const int64_t row = row_at(it, r, tid_out);
+    if (row >= it.row_end) continue;
     if (a.C == 1) {
       float* o = static_cast<float*>(a.out) + row * a.E + a.e0;
 #pragma unroll
@@ -290,17 +366,18 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
   constexpr int W = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
   if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
-  const Item it = item_of(a);
+  const Item it = item_of<R>(a);
+  if (!it.live) return;
   float xr[R][DP];
-  load_rows<DP, R>(a, it.rb, xr);
+  load_rows<DP, R>(a, it, xr);
   float tot[R][W], part[R][W];
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int w = 0; w < W; ++w) tot[r][w] = part[r][w] = 0.0f;
 
-  stream_columns<S>(
-      a.ypk, it.j0, it.j1, 0, lds,
+  stream_item<S>(
+      a, it, 0, lds,
       [&](const float* yv, int64_t) {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -330,8 +407,8 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
   const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int64_t row = row_of<R>(it.rb, r, tid_out);
-    if (row >= a.M) continue;
+    const int64_t row = row_at(it, r, tid_out);
+    if (row >= it.row_end) continue;
     if (a.C == 1) {
       float* o = static_cast<float*>(a.out) + row * (1 + a.D);
       o[0] = tot[r][0];
@@ -357,15 +434,16 @@ template <int DP, int EP, int R>
 __global__ __launch_bounds__(kThreads) void vjp_kernel(DirectArgs a) {
   constexpr int S = DP + EP;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
-  const Item it = item_of(a);
+  const Item it = item_of<R>(a);
+  if (!it.live) return;
   float xr[R][DP];
-  load_rows<DP, R>(a, it.rb, xr);
+  load_rows<DP, R>(a, it, xr);
   float er[R][EP];
   const int Ec = min(EP, a.E - a.e0);
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int64_t row = row_of<R>(it.rb, r, threadIdx.x);
-    const bool ok = row < a.M;
+    const int64_t row = row_at(it, r, threadIdx.x);
+    const bool ok = row < it.row_end;
 #pragma unroll
     for (int e = 0; e < EP; ++e) er[r][e] = (ok && e < Ec) ? a.xe[row * a.E + a.e0 + e] : 0.0f;
   }
@@ -375,8 +453,8 @@ __global__ __launch_bounds__(kThreads) void vjp_kernel(DirectArgs a) {
 #pragma unroll
     for (int k = 0; k < DP; ++k) tot[r][k] = part[r][k] = 0.0f;
 
-  stream_columns<S>(
-      a.ypk, it.j0, it.j1, 0, lds,
+  stream_item<S>(
+      a, it, 0, lds,
       [&](const float* yv, int64_t) {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -408,8 +486,8 @@ __global__ __launch_bounds__(kThreads) void vjp_kernel(DirectArgs a) {
   const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int64_t row = row_of<R>(it.rb, r, tid_out);
-    if (row >= a.M) continue;
+    const int64_t row = row_at(it, r, tid_out);
+    if (row >= it.row_end) continue;
     if (a.C == 1) {
       float* o = static_cast<float*>(a.out) + row * a.D;
 #pragma unroll
@@ -455,13 +533,15 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
   if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
-  const Item it = item_of(a);
+  const Item it = item_of<R>(a);
+  if (!it.live) return;
   float xr[R][DP];
-  load_rows<DP, R>(a, it.rb, xr);
+  load_rows<DP, R>(a, it, xr);
   float m[R], tot[R], part[R];
-  {
-    // the block's first column sets the reference: its term is 2^0 = 1
-    const float* y0 = a.ypk + it.j0 * S;
+  const int64_t jf = first_column(a, it);
+  if (jf >= 0) {
+    // the item's first column sets the reference: its term is 2^0 = 1
+    const float* y0 = a.ypk + jf * S;
     float yv[S];
 #pragma unroll
     for (int s = 0; s < S; ++s) yv[s] = y0[s];
@@ -471,10 +551,17 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
       tot[r] = 0.0f;
       part[r] = 1.0f;
     }
+  } else {
+    // no columns: the empty sum, log 0 = -infinity
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      m[r] = -__builtin_inff();
+      tot[r] = part[r] = 0.0f;
+    }
   }
 
-  stream_columns<S>(
-      a.ypk, it.j0, it.j1, 1, lds,
+  stream_item<S>(
+      a, it, 1, lds,
       [&](const float* yv, int64_t) {
         float uu[R];
         bool big = false;
@@ -512,8 +599,8 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
   const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int64_t row = row_of<R>(it.rb, r, tid_out);
-    if (row >= a.M) continue;
+    const int64_t row = row_at(it, r, tid_out);
+    if (row >= it.row_end) continue;
     if (a.C == 1) {
       static_cast<float*>(a.out)[row] = (m[r] + fast_log2(tot[r])) * kLn2;
     } else {
@@ -535,9 +622,10 @@ template <int F, int DP, int EP, int R>
 __global__ __launch_bounds__(kThreads) void extreme_kernel(DirectArgs a) {
   constexpr int S = DP + EP;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
-  const Item it = item_of(a);
+  const Item it = item_of<R>(a);
+  if (!it.live) return;
   float xr[R][DP];
-  load_rows<DP, R>(a, it.rb, xr);
+  load_rows<DP, R>(a, it, xr);
   float best[R][EP];
   int bj[R][EP];
 #pragma unroll
@@ -549,8 +637,8 @@ __global__ __launch_bounds__(kThreads) void extreme_kernel(DirectArgs a) {
     }
   const float ks = a.kscale;
 
-  stream_columns<S>(
-      a.ypk, it.j0, it.j1, 0, lds,
+  stream_item<S>(
+      a, it, 0, lds,
       [&](const float* yv, int64_t j) {
         float d[R];
 #pragma unroll
@@ -582,8 +670,8 @@ __global__ __launch_bounds__(kThreads) void extreme_kernel(DirectArgs a) {
   const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int64_t row = row_of<R>(it.rb, r, tid_out);
-    if (row >= a.M) continue;
+    const int64_t row = row_at(it, r, tid_out);
+    if (row >= it.row_end) continue;
     if (a.C == 1) {
 #pragma unroll
       for (int e = 0; e < EP; ++e)
@@ -625,9 +713,10 @@ template <int DP, int KP, int R>
 __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
   constexpr int S = DP + 1;   // the prologue pads one zero signal column
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
-  const Item it = item_of(a);
+  const Item it = item_of<R>(a);
+  if (!it.live) return;
   float xr[R][DP];
-  load_rows<DP, R>(a, it.rb, xr);
+  load_rows<DP, R>(a, it, xr);
   float dk[R][KP];
   int jk[R][KP];
 #pragma unroll
@@ -638,8 +727,8 @@ __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
       jk[r][p] = INT_MAX;
     }
 
-  stream_columns<S>(
-      a.ypk, it.j0, it.j1, 0, lds,
+  stream_item<S>(
+      a, it, 0, lds,
       [&](const float* yv, int64_t j) {
         float d[R];
         bool any = false;
@@ -659,8 +748,8 @@ __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
   const int tid_out = opaque_tid();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int64_t row = row_of<R>(it.rb, r, tid_out);
-    if (row >= a.M) continue;
+    const int64_t row = row_at(it, r, tid_out);
+    if (row >= it.row_end) continue;
     if (a.C == 1) {
       if (a.kvalues) {
         float* o = static_cast<float*>(a.out) + row * a.K;
@@ -671,7 +760,7 @@ __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
         int* o = static_cast<int*>(a.out) + row * a.K;
 #pragma unroll
         for (int p = 0; p < KP; ++p)
-          if (p < a.K) o[p] = jk[r][p];
+          if (p < a.K) o[p] = jk[r][p] == INT_MAX ? -1 : jk[r][p];
       }
     } else {
       float* q = a.part + ((int64_t)it.c * a.M + row) * (2 * KP);
@@ -850,6 +939,49 @@ hipError_t launch_scale_rows(const float* src, int64_t M, int D, const float* e,
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void range_blocks_kernel(const int* __restrict__ rr, int nr,
+                                                           int64_t M, int rpb,
+                                                           int* __restrict__ bstart) {
+  // one workgroup: each thread counts a contiguous chunk of clusters, the 256
+  // chunk totals are scanned in LDS, then each thread writes its prefixes
+  __shared__ int tot[256];
+  const int t = threadIdx.x;
+  const int chunk = (nr + 255) / 256;
+  const int c0 = min(nr, t * chunk), c1 = min(nr, c0 + chunk);
+  auto blocks = [&](int I) {
+    const int64_t r0 = min(max((int64_t)rr[2 * I], (int64_t)0), M);
+    const int64_t r1 = min(max((int64_t)rr[2 * I + 1], r0), M);
+    return (int)((r1 - r0 + rpb - 1) / rpb);
+  };
+  int sum = 0;
+  for (int I = c0; I < c1; ++I) sum += blocks(I);
+  tot[t] = sum;
+  __syncthreads();
+  for (int o = 1; o < 256; o <<= 1) {
+    const int v = t >= o ? tot[t - o] : 0;
+    __syncthreads();
+    tot[t] += v;
+    __syncthreads();
+  }
+  int run = t > 0 ? tot[t - 1] : 0;
+  for (int I = c0; I < c1; ++I) {
+    bstart[I] = run;
+    run += blocks(I);
+  }
+  if (t == 255) bstart[nr] = tot[255];
+}
+
+hipError_t launch_range_blocks(const int* rr, int nr, int64_t M, int rows_per_block, int* bstart,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(range_blocks_kernel, dim3(1), dim3(256), 0, s, rr, nr, M, rows_per_block,
+                     bstart);
+  return hipGetLastError();
+}
+
+int64_t range_grid_bound(int nr, int64_t M, int rows_per_block) {
+  return (int64_t)nr + (M + rows_per_block - 1) / rows_per_block;
+}
+
 hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s) {
   if (count == 0) return hipSuccess;
   const int64_t blocks = std::min<int64_t>((count + 255) / 256, 8192);
@@ -857,11 +989,15 @@ hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s) {
   return hipGetLastError();
 }
 
+int direct_rows_for(const DirectArgs& a) {
+  return a.ext ? direct_rows_per_thread(F_SQDIST, a.DP, a.EP, 0)
+               : direct_rows_per_thread(a.formula, a.DP, a.EP, a.KP);
+}
+
 hipError_t launch_direct(const DirectArgs& a, hipStream_t s) {
-  const int R = a.ext ? direct_rows_per_thread(F_SQDIST, a.DP, a.EP, 0)
-                      : direct_rows_per_thread(a.formula, a.DP, a.EP, a.KP);
+  const int R = direct_rows_for(a);
   const int64_t rb = (a.M + (int64_t)kThreads * R - 1) / ((int64_t)kThreads * R);
-  const dim3 grid((unsigned)(rb * a.C));
+  const dim3 grid((unsigned)(a.nr > 0 ? range_grid_bound(a.nr, a.M, kThreads * R) : rb * a.C));
   switch (a.DP) {
     case 1: return launch_dp<1>(a, grid, s);
     case 2: return launch_dp<2>(a, grid, s);

@@ -385,23 +385,43 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   return KRED_OK;
 }
 
-// One reduction on validated arguments, M > 0, on the current device.
+// Block-sparse pattern of a call (nr row clusters; see DirectArgs).
+struct Ranges {
+  int nr;
+  const int* rr;
+  const int* cp;
+  const int* cr;
+};
+
+// Value an empty reduction writes (and the output's element count) for r.
+void empty_fill(kred_formula f, kred_reduction r, const kred_params* p, int64_t M, int32_t D,
+                int32_t E, const float* b, int64_t* count, float* value) {
+  const int64_t e_out = (f == KRED_F_SINKHORN || (f == KRED_F_SQDIST && b == nullptr)) ? 1 : E;
+  *count = M;
+  *value = 0.0f;
+  if (f == KRED_F_GAUSS_GRADX) *count = M * (1 + D);
+  else if (r == KRED_R_SUM) *count = M * E;
+  else if (r == KRED_R_LSE) *value = -INFINITY;
+  else if (r == KRED_R_ARGKMIN || r == KRED_R_KMIN) {
+    *count = M * p->K;
+    *value = r == KRED_R_KMIN ? INFINITY : __builtin_bit_cast(float, (int32_t)-1);
+  } else if (is_extreme(r)) {
+    *count = M * e_out;
+    // an empty min is +inf, an empty max -inf, an empty arg -1 (int32 bits)
+    *value = is_arg(r) ? __builtin_bit_cast(float, (int32_t)-1) : (is_max(r) ? -INFINITY : INFINITY);
+  }
+}
+
+// One reduction on validated arguments, M > 0, on the current device;
+// block-sparse when rg is given (direct kernels, no column split).
 kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                           int64_t M, int64_t N, int32_t D, int32_t E, const float* x,
-                          const float* y, const float* b, void* out, hipStream_t s) {
+                          const float* y, const float* b, void* out, hipStream_t s,
+                          const Ranges* rg = nullptr) {
   if (N == 0) {
-    int64_t count = M;
-    float value = 0.0f;
-    const int64_t e_out = (f == KRED_F_SINKHORN || (f == KRED_F_SQDIST && b == nullptr)) ? 1 : E;
-    if (f == KRED_F_GAUSS_GRADX) count = M * (1 + D);
-    else if (r == KRED_R_SUM) count = M * E;
-    else if (r == KRED_R_LSE) value = -INFINITY;
-    else if (is_extreme(r)) {
-      count = M * e_out;
-      // an empty min is +inf, an empty max -inf, an empty arg -1 (int32 bits)
-      value = is_arg(r) ? __builtin_bit_cast(float, (int32_t)-1)
-                        : (is_max(r) ? -INFINITY : INFINITY);
-    }
+    int64_t count;
+    float value;
+    empty_fill(f, r, p, M, D, E, b, &count, &value);
     return launch_fill(static_cast<float*>(out), count, value, s) == hipSuccess ? KRED_OK
                                                                                 : KRED_ERR_HIP;
   }
@@ -425,19 +445,29 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
 
   if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s, kvalues);
 
-  const int epi = fast_epi(f, r, M, N, D, E, p->flags);
+  kred_params pr;
+  if (rg) {
+    pr = *p;
+    pr.col_blocks = 1;   // a block-sparse item reduces its whole column list
+    p = &pr;
+  }
+  const int epi = rg ? -1 : fast_epi(f, r, M, N, D, E, p->flags);
   Plan pl;
   if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &pl,
                  epi >= 0 ? fast_rows_per_block(epi) : 0, epi >= 0 ? 256 : 1))
     return KRED_ERR_UNSUPPORTED;
   const FastScratch fs = fast_scratch(epi, N);
-  const kred_status gs = grow_scratch(
-      ctx, (size_t)(pl.pack_bytes + pl.part_bytes + fs.guard_bytes + fs.apk_bytes + fs.ex_bytes));
+  const int64_t bstart_bytes = rg ? align_up((int64_t)(rg->nr + 1) * (int64_t)sizeof(int)) : 0;
+  const kred_status gs =
+      grow_scratch(ctx, (size_t)(pl.pack_bytes + pl.part_bytes + fs.guard_bytes + fs.apk_bytes +
+                                 fs.ex_bytes + bstart_bytes));
   if (gs != KRED_OK) return gs;
   char* sbase = static_cast<char*>(ctx->scratch);
   float* ypk = reinterpret_cast<float*>(sbase);
   float* part = pl.part_bytes ? reinterpret_cast<float*>(sbase + pl.pack_bytes) : nullptr;
   char* fbase = sbase + pl.pack_bytes + pl.part_bytes;
+  int* bstart = rg ? reinterpret_cast<int*>(fbase + fs.guard_bytes + fs.apk_bytes + fs.ex_bytes)
+                   : nullptr;
   FastGuard* guard = epi >= 0 ? reinterpret_cast<FastGuard*>(fbase) : nullptr;
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
 
@@ -523,6 +553,16 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     da.ext_sign = is_max(r) ? -1.0f : 1.0f;
     da.arg = is_arg(r);
     da.kvalues = kvalues;
+    if (rg) {
+      da.nr = rg->nr;
+      da.rr = rg->rr;
+      da.cp = rg->cp;
+      da.cr = rg->cr;
+      da.bstart = bstart;
+      if (launch_range_blocks(rg->rr, rg->nr, M, kThreads * direct_rows_for(da), bstart, s) !=
+          hipSuccess)
+        return KRED_ERR_HIP;
+    }
     hipEvent_t e_start = nullptr, e_stop = nullptr;
     if (prof) {
       e_start = next_event(ctx);
@@ -806,6 +846,45 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   DeviceGuard devg(ctx->device);
   if (!devg.ok) return KRED_ERR_HIP;
   return run_reduction(ctx, f, r, p, M, N, D, E, x, y, b, out, static_cast<hipStream_t>(stream));
+}
+
+kred_status kred_validate_ranges(kred_formula f, kred_reduction r, const kred_params* p,
+                                 int64_t M, int64_t N, int32_t D, int32_t E, const void* x,
+                                 const void* y, const void* b, const void* out, int32_t nr,
+                                 const void* row_ranges, const void* col_ptr,
+                                 const void* col_ranges) {
+  const kred_status v = kred_validate(f, r, p, M, N, D, E, x, y, b, out);
+  if (v != KRED_OK) return v;
+  if (nr < 0) return KRED_ERR_INVALID_ARG;
+  if (D > kMaxDirectD) return KRED_ERR_UNSUPPORTED;
+  if (nr > 0 && (row_ranges == nullptr || col_ptr == nullptr || col_ranges == nullptr))
+    return KRED_ERR_INVALID_ARG;
+  if (misaligned(row_ranges) || misaligned(col_ptr) || misaligned(col_ranges))
+    return KRED_ERR_INVALID_ARG;
+  return KRED_OK;
+}
+
+kred_status kred_run_ranges(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
+                            int64_t M, int64_t N, int32_t D, int32_t E, const float* x,
+                            const float* y, const float* b, void* out, int32_t nr,
+                            const int32_t* row_ranges, const int32_t* col_ptr,
+                            const int32_t* col_ranges, void* stream) {
+  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
+  const kred_status v = kred_validate_ranges(f, r, p, M, N, D, E, x, y, b, out, nr, row_ranges,
+                                             col_ptr, col_ranges);
+  if (v != KRED_OK) return v;
+  if (M == 0) return KRED_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  DeviceGuard devg(ctx->device);
+  if (!devg.ok) return KRED_ERR_HIP;
+  // rows outside every cluster (and clusters without columns) hold the empty reduction
+  int64_t count;
+  float value;
+  empty_fill(f, r, p, M, D, E, b, &count, &value);
+  if (launch_fill(static_cast<float*>(out), count, value, s) != hipSuccess) return KRED_ERR_HIP;
+  if (nr == 0 || N == 0) return KRED_OK;
+  const Ranges rg{nr, row_ranges, col_ptr, col_ranges};
+  return run_reduction(ctx, f, r, p, M, N, D, E, x, y, b, out, s, &rg);
 }
 
 kred_status kred_validate_backward(const kred_params* p, int64_t M, int64_t N, int32_t D,

@@ -101,9 +101,24 @@ struct DirectArgs {
   float ext_sign;         // +1 (min) or -1 (max); folded into kscale and the packed b
   int arg;                // min / max: write the index (int32) instead of the value
   int kvalues;            // arg-K-min lists: write the distances (fp32) instead of the indices
+  // Block-sparse reductions (nr > 0): row cluster I is rows [rr[2I], rr[2I+1]);
+  // its reduction runs over the column ranges cr[2q], cr[2q+1]) for q in
+  // [cp[I], cp[I+1]).  bstart[I] is the first workgroup of cluster I (a
+  // prefix over clusters of their row-block counts, made on the device).
+  int nr;
+  const int* rr;
+  const int* cp;
+  const int* cr;
+  const int* bstart;
 };
 hipError_t launch_direct(const DirectArgs& a, hipStream_t s);
+// bstart[0..nr]: prefix sums of ceil(cluster rows / rows_per_block) (one workgroup).
+hipError_t launch_range_blocks(const int* rr, int nr, int64_t M, int rows_per_block, int* bstart,
+                               hipStream_t s);
+// Workgroups a block-sparse launch needs at most (disjoint row ranges).
+int64_t range_grid_bound(int nr, int64_t M, int rows_per_block);
 int direct_rows_per_thread(int formula, int DP, int EP, int KP);
+int direct_rows_for(const DirectArgs& a);   // rows per lane launch_direct uses for these args
 int direct_pad_d(int D);      // DP for a given D, 0 if the direct path has none
 int direct_pad_e(int E);      // EP for one E-slice
 int knn_pad_k(int K);         // KP for a given K

@@ -65,11 +65,16 @@ def load():
         lib.kred_gauss_backward.argtypes = [vp, pp, i64, i64, i32, i32, vp, vp, vp, vp,
                                             vp, vp, vp, vp]
         lib.kred_validate_backward.argtypes = [pp, i64, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+        lib.kred_run_ranges.argtypes = [vp, ctypes.c_int, ctypes.c_int, pp, i64, i64, i32, i32,
+                                        vp, vp, vp, vp, i32, vp, vp, vp, vp]
+        lib.kred_validate_ranges.argtypes = [ctypes.c_int, ctypes.c_int, pp, i64, i64, i32, i32,
+                                             vp, vp, vp, vp, i32, vp, vp, vp]
         lib.kred_strerror.argtypes = [ctypes.c_int]
         lib.kred_strerror.restype = ctypes.c_char_p
         lib.kred_version.restype = i32
         for f in (lib.kred_create, lib.kred_destroy, lib.kred_run, lib.kred_validate,
-                  lib.kred_gauss_backward, lib.kred_validate_backward, lib.kred_profile_collect):
+                  lib.kred_gauss_backward, lib.kred_validate_backward, lib.kred_run_ranges,
+                  lib.kred_validate_ranges, lib.kred_profile_collect):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -117,6 +122,15 @@ def validate_backward(M, N, D, E, x=16, y=16, b=16, e=16, gx=16, gy=16, gb=16, *
     p = make_params(**params)
     return load().kred_validate_backward(ctypes.byref(p), int(M), int(N), int(D), int(E),
                                          x, y, b, e, gx, gy, gb)
+
+
+def validate_ranges(formula, reduction, M, N, D, E, nr, x=16, y=16, b=16, out=16, rr=16, cp=16,
+                    cr=16, **params):
+    """Host-only argument check of a block-sparse call (pointers as plain integers)."""
+    f, r = _codes(formula, reduction)
+    p = make_params(**params)
+    return load().kred_validate_ranges(f, r, ctypes.byref(p), int(M), int(N), int(D), int(E),
+                                       x, y, b, out, int(nr), rr, cp, cr)
 
 
 def scratch_bytes(formula, reduction, M, N, D, E, **params):
@@ -181,8 +195,18 @@ class Context:
             raise TypeError("%s must be a contiguous %s tensor" % (name, dtype))
         return t.data_ptr() if t.numel() else None
 
+    def run_ranges(self, formula, reduction, x, y, b, row_ranges, col_ptr, col_ranges, out=None,
+                   sigma=1.0, eps=1.0, K=0, flags=0, stream=None):
+        """Block-sparse reduction (kred_run_ranges): row cluster I = rows
+        row_ranges[I, 0] .. row_ranges[I, 1] - 1 reduces over the column ranges
+        col_ranges[col_ptr[I] : col_ptr[I + 1]] only.  The index arrays are int32
+        GPU tensors (nr x 2, nr + 1, nnz x 2); otherwise as run()."""
+        return self.run(formula, reduction, x, y, b, out=out, sigma=sigma, eps=eps, K=K,
+                        flags=flags, stream=stream,
+                        _ranges=(row_ranges, col_ptr, col_ranges))
+
     def run(self, formula, reduction, x, y, b=None, out=None, sigma=1.0, eps=1.0, K=0,
-            col_blocks=0, flags=0, stream=None):
+            col_blocks=0, flags=0, stream=None, _ranges=None):
         """Evaluate the reduction; returns `out` (allocated when None).
 
         x: (M, D) float32, y: (N, D) float32, b: (N, E) float32 or None (arg-K-min,
@@ -212,10 +236,19 @@ class Context:
         if b is not None and bptr is None:
             # an empty b (N = 0) is never read, but its presence sets the output width
             bptr = 16
-        st = load().kred_run(self._h, f, r, ctypes.byref(p), M, N, D, E,
-                             self._dev_ptr(x, "x", torch.float32),
-                             self._dev_ptr(y, "y", torch.float32), bptr,
-                             self._dev_ptr(out, "out", odt), s)
+        args = (self._h, f, r, ctypes.byref(p), M, N, D, E, self._dev_ptr(x, "x", torch.float32),
+                self._dev_ptr(y, "y", torch.float32), bptr, self._dev_ptr(out, "out", odt))
+        if _ranges is None:
+            st = load().kred_run(*args, s)
+        else:
+            rr, cp, cr = _ranges
+            nr = rr.shape[0]
+            if tuple(cp.shape) != (nr + 1,) or rr.dim() != 2 or rr.shape[1] != 2:
+                raise ValueError("row_ranges must be (nr, 2) and col_ptr (nr + 1,)")
+            i32 = torch.int32
+            st = load().kred_run_ranges(*args, nr, self._dev_ptr(rr, "row_ranges", i32),
+                                        self._dev_ptr(cp, "col_ptr", i32),
+                                        self._dev_ptr(cr, "col_ranges", i32), s)
         if st != 0:
             raise KredError(st, "kred_run(%s, %s, M=%d, N=%d, D=%d, E=%d)" % (formula, reduction,
                                                                              M, N, D, E))

@@ -215,3 +215,16 @@ def test_kernel_lse_pairs(lib):
     assert V("gauss", "lse", 100, 200, 3, 1, sigma=0.1, b=None) == INVALID
     assert V("sqdist", "lse", 100, 200, 3, 1) == UNSUPPORTED
     assert V("gauss", "lse", 100, 200, 17, 1, sigma=0.1) == UNSUPPORTED
+
+
+def test_ranges_validation(lib):
+    VR = kred.validate_ranges
+    assert "kred_run_ranges" in kred.header_symbols()
+    assert VR("gauss", "sum", 100, 200, 3, 1, 5, sigma=1.0) == OK
+    assert VR("sqdist", "argkmin", 100, 200, 3, 0, 5, b=None, K=4) == OK
+    assert VR("gauss", "sum", 100, 200, 3, 1, 0, rr=None, cp=None, cr=None, sigma=1.0) == OK
+    assert VR("gauss", "sum", 100, 200, 3, 1, 5, cr=None, sigma=1.0) == INVALID
+    assert VR("gauss", "sum", 100, 200, 3, 1, -1, sigma=1.0) == INVALID
+    assert VR("gauss", "sum", 100, 200, 3, 1, 5, rr=2, sigma=1.0) == INVALID   # misaligned
+    assert VR("gauss", "sum", 100, 200, 17, 1, 5, sigma=1.0) == UNSUPPORTED
+    assert VR("gauss", "sum", 100, 200, 3, 1, 5, sigma=0.0) == INVALID         # as kred_run

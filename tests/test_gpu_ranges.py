@@ -1,0 +1,162 @@
+"""GPU parity of block-sparse (cluster-wise) reductions, kred_run_ranges, against the oracle.
+
+Row cluster I reduces over its own list of column ranges only; rows in no
+cluster, and clusters without columns, hold the empty reduction.  Patterns are
+random (gaps between row clusters, clusters with no column ranges, clusters
+spanning several workgroups, hundreds of clusters for the device-side block
+map) plus ranges that need clamping to [0, M) x [0, N).  Same bars as the
+dense tests: normalised 1e-4 for sums, 1e-4 in the log domain for
+log-sum-exp, bit-exact values and indices on integer data for the
+arg-K-min / K-min / min / max families.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import LSE_TOL, SUM_TOL, dev, host, lse_err, norm_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    import torch
+    from paper_2004_11127_amd import kred
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    with kred.Context(0) as c:
+        yield c
+
+
+def random_pattern(rng, M, N, n_rc, n_cc, p_keep=0.4):
+    """Row clusters (with gaps) over [0, M), and per cluster sorted disjoint column ranges."""
+    rc = np.sort(rng.choice(np.arange(1, M), 2 * n_rc - 1, replace=False))
+    rc = np.concatenate([[0], rc, [M]])
+    rows = np.array([[rc[2 * i], rc[2 * i + 1]] for i in range(n_rc)], dtype=np.int32)
+    cc = np.concatenate([[0], np.sort(rng.choice(np.arange(1, N), n_cc - 1, replace=False)), [N]])
+    ptr, cr = [0], []
+    for i in range(n_rc):
+        keep = np.nonzero(rng.uniform(size=n_cc) < p_keep)[0]
+        cr.extend([cc[k], cc[k + 1]] for k in keep)
+        ptr.append(len(cr))
+    cr = np.array(cr, dtype=np.int32).reshape(-1, 2)
+    return rows, np.array(ptr, dtype=np.int32), cr
+
+
+def call(ctx, formula, reduction, x, y, b, pat, **kw):
+    import torch
+    rows, ptr, cr = pat
+    crt = dev(cr) if cr.size else torch.zeros((0, 2), dtype=torch.int32, device="cuda")
+    return host(ctx.run_ranges(formula, reduction, dev(x), dev(y), None if b is None else dev(b),
+                               dev(rows), dev(ptr), crt, **kw))
+
+
+SUMS = [
+    # formula, M, N, D, E, sigma, clusters (rows, cols)
+    ("gauss", 3000, 4000, 3, 1, 0.1, (6, 10)),
+    ("gauss", 5000, 3000, 2, 3, 0.2, (300, 40)),
+    ("gauss", 800, 2500, 8, 20, 0.4, (5, 7)),
+    ("laplace", 2000, 2000, 3, 4, 0.2, (9, 9)),
+    ("sqdist", 1500, 1200, 16, 2, 1.0, (4, 6)),
+]
+
+
+@pytest.mark.parametrize("formula,M,N,D,E,sigma,cl", SUMS)
+def test_ranges_sum(ctx, formula, M, N, D, E, sigma, cl):
+    rng = np.random.default_rng(M + N + E)
+    x = rng.uniform(0, 1, (M, D)).astype(np.float32)
+    y = rng.uniform(0, 1, (N, D)).astype(np.float32)
+    b = rng.standard_normal((N, E)).astype(np.float32)
+    pat = random_pattern(rng, M, N, *cl)
+    out = call(ctx, formula, "sum", x, y, b, pat, sigma=sigma)
+    ref, norm = oracle.ranges_reduce("sum", x, y, b, *pat, formula=formula, sigma=sigma)
+    assert norm_err(out, ref, norm) <= SUM_TOL
+    covered = np.zeros(M, bool)
+    for r0, r1 in pat[0]:
+        covered[r0:r1] = True
+    assert (out[~covered] == 0).all()
+
+
+def test_ranges_gradx(ctx):
+    rng = np.random.default_rng(1)
+    M, N = 4000, 3000
+    x = rng.uniform(0, 1, (M, 3)).astype(np.float32); y = rng.uniform(0, 1, (N, 3)).astype(np.float32)
+    b = rng.standard_normal((N, 1)).astype(np.float32)
+    pat = random_pattern(rng, M, N, 12, 15)
+    out = call(ctx, "gauss_gradx", "sum", x, y, b, pat, sigma=0.1)
+    ref, norm = oracle.ranges_reduce("gradx", x, y, b, *pat, sigma=0.1)
+    assert norm_err(out, ref, norm) <= SUM_TOL
+
+
+@pytest.mark.parametrize("formula,param", [("sinkhorn", 0.01), ("gauss", 0.1), ("laplace", 0.05)])
+def test_ranges_lse(ctx, formula, param):
+    rng = np.random.default_rng(2)
+    M, N = 3000, 2500
+    x = rng.uniform(0, 1, (M, 3)).astype(np.float32); y = rng.uniform(0, 1, (N, 3)).astype(np.float32)
+    g = (2.0 * rng.standard_normal((N, 1))).astype(np.float32)
+    pat = random_pattern(rng, M, N, 10, 12)
+    kw = dict(eps=param) if formula == "sinkhorn" else dict(sigma=param)
+    out = call(ctx, formula, "lse", x, y, g, pat, **kw)
+    okw = dict(eps=param) if formula == "sinkhorn" else dict(formula=formula, sigma=param)
+    ref, m = oracle.ranges_reduce("lse", x, y, g, *pat, **okw)
+    empty = np.isneginf(ref)
+    assert (np.isneginf(out[empty, 0])).all()
+    assert lse_err(out[~empty, 0], ref[~empty], m[~empty]) <= LSE_TOL
+
+
+@pytest.mark.parametrize("red,K", [("argkmin", 5), ("kmin", 5), ("argkmin", 1)])
+def test_ranges_knn_exact(ctx, red, K):
+    rng = np.random.default_rng(3 + K)
+    M, N, D = 2000, 3000, 4
+    x = rng.integers(-3, 4, (M, D)).astype(np.float32); y = rng.integers(-3, 4, (N, D)).astype(np.float32)
+    pat = random_pattern(rng, M, N, 8, 20, p_keep=0.15)   # some clusters get fewer than K columns
+    out = call(ctx, "sqdist", red, x, y, None, pat, K=K)
+    ref, _ = oracle.ranges_reduce(red, x, y, None, *pat, K=K)
+    np.testing.assert_array_equal(out, ref.astype(out.dtype))
+
+
+@pytest.mark.parametrize("red", ["min", "max", "argmin", "argmax"])
+def test_ranges_extreme_exact(ctx, red):
+    rng = np.random.default_rng(4)
+    M, N = 1500, 2000
+    x = rng.integers(-3, 4, (M, 3)).astype(np.float32); y = rng.integers(-3, 4, (N, 3)).astype(np.float32)
+    b = rng.integers(-3, 4, (N, 2)).astype(np.float32)
+    pat = random_pattern(rng, M, N, 7, 9)
+    op = "max" if "max" in red else "min"
+    for bb in (None, b):
+        out = call(ctx, "sqdist", red, x, y, bb, pat)
+        val, idx = oracle.ranges_reduce(op, x, y, bb, *pat, formula="sqdist")
+        ref = idx.astype(np.int32) if red.startswith("arg") else val.astype(np.float32)
+        np.testing.assert_array_equal(out, ref)
+
+
+def test_ranges_clamped_and_empty_patterns(ctx):
+    rng = np.random.default_rng(5)
+    M, N = 600, 900
+    x = rng.uniform(0, 1, (M, 3)).astype(np.float32); y = rng.uniform(0, 1, (N, 3)).astype(np.float32)
+    b = rng.standard_normal((N, 1)).astype(np.float32)
+    # ranges reaching outside [0, M) x [0, N) are clamped; an inverted range is empty
+    rows = np.array([[-50, 200], [400, 10 ** 6], [300, 250]], np.int32)
+    ptr = np.array([0, 2, 3, 4], np.int32)
+    cr = np.array([[-10, 100], [850, 5000], [100, 400], [0, 900]], np.int32)
+    out = call(ctx, "gauss", "sum", x, y, b, (rows, ptr, cr), sigma=0.2)
+    ref, norm = oracle.ranges_reduce("sum", x, y, b, rows, ptr, cr, formula="gauss", sigma=0.2)
+    assert norm_err(out, ref, norm) <= SUM_TOL
+    assert (out[200:400] == 0).all()
+    # no clusters at all: every row holds the empty reduction
+    empty = (np.zeros((0, 2), np.int32), np.zeros(1, np.int32), np.zeros((0, 2), np.int32))
+    out = call(ctx, "gauss", "sum", x, y, b, empty, sigma=0.2)
+    assert (out == 0).all()
+    out = call(ctx, "sinkhorn", "lse", x, y, b, empty, eps=0.1)
+    assert np.isneginf(out).all()
+
+
+def test_ranges_full_pattern_matches_dense(ctx):
+    # one cluster over everything reproduces kred_run (same kernels, no split)
+    rng = np.random.default_rng(6)
+    M, N = 2500, 3500
+    x = rng.uniform(0, 1, (M, 3)).astype(np.float32); y = rng.uniform(0, 1, (N, 3)).astype(np.float32)
+    b = rng.standard_normal((N, 2)).astype(np.float32)
+    pat = (np.array([[0, M]], np.int32), np.array([0, 1], np.int32), np.array([[0, N]], np.int32))
+    out = call(ctx, "gauss", "sum", x, y, b, pat, sigma=0.1)
+    dense = host(ctx.run("gauss", "sum", dev(x), dev(y), dev(b), sigma=0.1, col_blocks=1))
+    np.testing.assert_array_equal(out, dense)
