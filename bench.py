@@ -58,7 +58,13 @@ WORKLOADS = {
     "chamfer": ("mixture_gauss", dict(M=1_000_000, N=1_000_000, D=3, sigma=0.05), "sqdist", "min",
                 9, "alu", "nearest-neighbour squared distance (min reduction, no b), mixture of 8 "
                           "Gaussians, 1e6 x 1e6, D=3"),
+    # block-sparse Gaussian sum: grid clusters of side 2 sigma, cluster pairs kept
+    # within 6 sigma (+ the cell diagonal); pairs and flops count the kept pairs
+    "sparse": ("mixture_gauss", dict(M=1_000_000, N=1_000_000, D=3, sigma=0.05), "gauss", "sum",
+               11, "alu", "block-sparse gaussian kernel sum (grid clusters of side 2 sigma, "
+                          "truncation at 6 sigma), mixture of 8 Gaussians, 1e6 x 1e6, D=3"),
 }
+SPARSE_CELL, SPARSE_CUTOFF = 2.0, 6.0   # in units of sigma
 # the three reductions of a backward step: (rows, columns) = (M, N), (N, M), (N, M)
 REDUCTIONS_PER_STEP = {"backward": 3, "backward_e16": 3}
 NO_SIGNAL = {"chamfer"}   # reductions of the bare squared distance (b = NULL)
@@ -112,7 +118,16 @@ def cotangent(w):
     return np.random.default_rng(1).standard_normal((w.M, w.E)).astype(np.float32)
 
 
-def time_steps(ctx, w, formula, reduction, steps, warmup):
+def sparse_pattern(w):
+    """Sorted copy of the workload and its block-sparse pattern (host setup, not timed)."""
+    from paper_2004_11127_amd import clusters
+    pat = clusters.truncation_pattern(w.x, w.y, SPARSE_CELL * w.sigma, SPARSE_CUTOFF * w.sigma)
+    w.x = w.x[pat["order_x"]].copy(); w.y = w.y[pat["order_y"]].copy()
+    w.b = w.b[pat["order_y"]].copy()
+    return pat
+
+
+def time_steps(ctx, w, formula, reduction, steps, warmup, pattern=None):
     """Time `steps` calls; kernel_ms is the main kernels' time per step (HIP events)."""
     import torch
     from paper_2004_11127_amd import kred
@@ -121,7 +136,15 @@ def time_steps(ctx, w, formula, reduction, steps, warmup):
     if reduction == "min" and formula == "sqdist":
         b = None
     stream = torch.cuda.current_stream()
-    if formula == "backward":
+    if pattern is not None:
+        rr, cp, cr = (torch.from_numpy(pattern[k]).cuda() for k in ("row_ranges", "col_ptr",
+                                                                     "col_ranges"))
+        kw = dict(sigma=w.sigma, eps=w.eps, K=w.K)
+
+        def call(flags):
+            return ctx.run_ranges(formula, reduction, x, y, b, rr, cp, cr, flags=flags,
+                                  stream=stream, **kw)
+    elif formula == "backward":
         e = torch.from_numpy(cotangent(w)).cuda()
 
         def call(flags):
@@ -152,8 +175,9 @@ def time_steps(ctx, w, formula, reduction, steps, warmup):
                 launches=n, kernel=kname, out=out.cpu().numpy())
 
 
-def cpu_baseline(w, formula, reduction, out_gpu, seconds):
-    """Time the fp64 oracle on a bounded sample of rows (all N columns)."""
+def cpu_baseline(w, formula, reduction, out_gpu, seconds, pattern=None):
+    """Time the fp64 oracle on a bounded sample of rows (all N columns, or the
+    pattern's columns of the sampled rows' clusters)."""
     import numpy as np
 
     import oracle
@@ -162,6 +186,19 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds):
     oracle.build()
 
     def run(rows):
+        if pattern is not None:
+            # the sampled rows' clusters, each reduced over its pattern columns
+            rr = pattern["row_ranges"]
+            cl = np.searchsorted(rr[:, 1], rows, side="right")
+            val = np.zeros((len(rows), 1)); nrm = np.zeros((len(rows), 1))
+            for I in np.unique(cl):
+                sel = cl == I
+                cols = oracle._cluster_columns(pattern["col_ptr"], pattern["col_ranges"], I, w.N)
+                if cols.size:
+                    v, n = oracle.kernel_sum("gauss", w.x[rows[sel]], w.y[cols], w.b[cols],
+                                             sigma=w.sigma)
+                    val[sel] = v; nrm[sel] = n
+            return val, nrm
         if formula == "backward":
             # the three reductions of a step on the same sampled row indices
             e = cotangent(w)
@@ -199,12 +236,20 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds):
     else:
         check = {"max_norm_err_on_sample": float(np.max(np.abs(got - ref) / np.maximum(aux, 1e-30)))}
     red = 3 if formula == "backward" else 1
-    res = dict(value=red * S * w.N / t / 1e9, unit="Gpairs/s", cores=oracle.num_threads(),
+    cols = w.N if pattern is None else pattern["pairs"] / w.M   # columns per row (mean)
+    res = dict(value=red * S * cols / t / 1e9, unit="Gpairs/s", cores=oracle.num_threads(),
                kind="oracle",
-               sample="%d seeded rows x all %d columns%s (%.1f s)"
-                      % (S, w.N, " for each of the 3 gradients" if red > 1 else "", t),
+               sample="%d seeded rows x %s%s (%.1f s)"
+                      % (S, "all %d columns" % w.N if pattern is None else "their pattern columns",
+                         " for each of the 3 gradients" if red > 1 else "", t),
                seconds=t)
     res.update(check)
+    if pattern is not None:
+        # what the truncation drops: the block-sparse result against the dense sum
+        few = rows[:: max(1, len(rows) // 64)]
+        dense, dn = oracle.kernel_sum("gauss", w.x[few], w.y, w.b, sigma=w.sigma)
+        res["truncation_err_vs_dense"] = float(np.max(np.abs(out_gpu[few] - dense) /
+                                                      np.maximum(dn, 1e-30)))
     return res
 
 
@@ -221,9 +266,11 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     gen, gkw, formula, reduction, fpp, bound, desc = WORKLOADS[args.workload]
     w = getattr(inputs, gen)(seed=0, **gkw)
-    pairs = float(w.M) * float(w.N) * REDUCTIONS_PER_STEP.get(args.workload, 1)
+    pattern = sparse_pattern(w) if args.workload == "sparse" else None
+    pairs = (float(pattern["pairs"]) if pattern is not None else float(w.M) * float(w.N)) \
+        * REDUCTIONS_PER_STEP.get(args.workload, 1)
     with kred.Context(0) as ctx:
-        r = time_steps(ctx, w, formula, reduction, args.steps, args.warmup)
+        r = time_steps(ctx, w, formula, reduction, args.steps, args.warmup, pattern)
     if args.copy_probe:
         src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -231,7 +278,8 @@ def main():
         torch.cuda.synchronize()
     ms_per_step = r["wall_s"] * 1e3 / args.steps
     # fpp counts the flops of one (i, j) over all reductions of a step
-    achieved = fpp * float(w.M) * float(w.N) / (r["kernel_ms"] / 1e3) / 1e12
+    step_pairs = pairs / REDUCTIONS_PER_STEP.get(args.workload, 1)   # pairs of one reduction
+    achieved = fpp * step_pairs / (r["kernel_ms"] / 1e3) / 1e12
     peak = PEAK_FP32_VECTOR_TFLOPS if bound == "alu" else PEAK_FP32_MATRIX_TFLOPS
     line = {
         "metric": "kernel pair-evaluations/sec (Gpairs/s) at M=N=1e6 D=3; % of FP32 VALU peak",
@@ -259,8 +307,12 @@ def main():
     if args.workload in ("c1", "headline"):
         line["paper_context"] = ("KeOps++ on an RTX 2080 Ti (Sec. 3 table): 0.4 ms at 1e4 and "
                                  "1.38 s at 1e6 points, D=3, fp32")
+    if pattern is not None:
+        line["config"]["pattern_pairs_fraction"] = pattern["pairs"] / (float(w.M) * w.N)
+        line["config"]["clusters"] = int(len(pattern["row_ranges"]))
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, formula, reduction, r["out"], args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(w, formula, reduction, r["out"], args.cpu_seconds,
+                                            pattern)
     print(json.dumps(line), flush=True)
 
 

@@ -64,6 +64,7 @@ __global__ __launch_bounds__(256) void combine_lse_kernel(CombineArgs a) {
     float s = 0.0f;
     for (int c = 0; c < a.C; ++c) {
       const float* p = a.part + ((int64_t)c * a.M + row) * 2;
+      if (p[0] == -__builtin_inff()) continue;   // an empty block (its sum is 0)
       s += p[1] * __builtin_amdgcn_exp2f(p[0] - m);
     }
     static_cast<float*>(a.out)[row] = (m + __builtin_amdgcn_logf(s)) * kLn2;
@@ -115,7 +116,7 @@ __global__ __launch_bounds__(256) void combine_knn_kernel(CombineArgs a) {
       int* o = static_cast<int*>(a.out) + row * a.K;
 #pragma unroll
       for (int p = 0; p < KP; ++p)
-        if (p < a.K) o[p] = jk[p];
+        if (p < a.K) o[p] = jk[p] == INT_MAX ? -1 : jk[p];   // short (block-sparse) lists
     }
   }
 }

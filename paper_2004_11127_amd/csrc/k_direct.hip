@@ -53,6 +53,14 @@ __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
   }
 }
 
+// Alternating two-value fill: (v0, v1, v0, v1, ...), the empty value of
+// (value, index) or (max, sum) partials.
+__global__ __launch_bounds__(256) void fill2_kernel(float* out, int64_t count, float v0, float v1) {
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < count;
+       t += (int64_t)gridDim.x * blockDim.x)
+    out[t] = (t & 1) ? v1 : v0;
+}
+
 __global__ __launch_bounds__(256) void fill_kernel(float* out, int64_t count, float value) {
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < count;
        t += (int64_t)gridDim.x * blockDim.x)
@@ -163,13 +171,20 @@ __device__ __forceinline__ void stream_columns(const float* __restrict__ ypk, in
 // registers: the pair loop runs at its best issue rate only with enough
 // waves resident per SIMD.
 struct Item {
-  int c;                    // column block (dense; 0 when block-sparse)
+  int c;                    // column block (dense) or column chunk (block-sparse)
   int64_t row0, row_end;
-  int64_t j0, j1;           // dense column block
+  int64_t j0, j1;           // dense: the column block; block-sparse: the chunk's window
   int nrange;               // block-sparse: number of column ranges (0: dense)
   const int* cr;            // block-sparse: this cluster's column ranges
   bool live;                // false: a spare workgroup of a block-sparse grid
 };
+
+// Column range q of a block-sparse cluster, clamped to [0, N).
+__device__ __forceinline__ void col_range(const DirectArgs& a, const int* cr, int q, int64_t& js,
+                                          int64_t& je) {
+  js = min(max((int64_t)cr[2 * q], (int64_t)0), a.N);
+  je = min(max((int64_t)cr[2 * q + 1], js), a.N);
+}
 
 template <int R>
 __device__ __forceinline__ Item item_of(const DirectArgs& a) {
@@ -177,8 +192,8 @@ __device__ __forceinline__ Item item_of(const DirectArgs& a) {
   it.nrange = 0;
   it.cr = nullptr;
   it.live = true;
+  it.c = blockIdx.x % a.C;
   if (a.nr == 0) {
-    it.c = blockIdx.x % a.C;
     const int64_t rb = blockIdx.x / a.C;
     it.row0 = rb * (int64_t)(kThreads * R);
     it.row_end = a.M;
@@ -186,12 +201,11 @@ __device__ __forceinline__ Item item_of(const DirectArgs& a) {
     it.j1 = min(a.N, it.j0 + a.jpb);
     return it;
   }
-  it.c = 0;
-  it.j0 = it.j1 = 0;
-  const int blk = (int)blockIdx.x;
+  const int blk = (int)(blockIdx.x / a.C);
   if (blk >= a.bstart[a.nr]) {
     it.live = false;
     it.row0 = it.row_end = 0;
+    it.j0 = it.j1 = 0;
     return it;
   }
   int lo = 0, hi = a.nr - 1;   // last cluster I with bstart[I] <= blk
@@ -206,6 +220,16 @@ __device__ __forceinline__ Item item_of(const DirectArgs& a) {
   it.row_end = r1;
   it.cr = a.cr + 2 * (int64_t)a.cp[lo];
   it.nrange = a.cp[lo + 1] - a.cp[lo];
+  // chunk c of C takes an equal share of the cluster's columns, counted in
+  // the concatenated order of its ranges
+  int64_t L = 0;
+  for (int q = 0; q < it.nrange; ++q) {
+    int64_t js, je;
+    col_range(a, it.cr, q, js, je);
+    L += je - js;
+  }
+  it.j0 = L * it.c / a.C;
+  it.j1 = L * (it.c + 1) / a.C;
   return it;
 }
 
@@ -247,16 +271,10 @@ __device__ __forceinline__ float sq_dist(const float (&xr)[DP], const float* yv)
   return d;
 }
 
-// Column range q of a block-sparse item, clamped to [0, N).
-__device__ __forceinline__ void col_range(const DirectArgs& a, const Item& it, int q,
-                                          int64_t& js, int64_t& je) {
-  js = min(max((int64_t)it.cr[2 * q], (int64_t)0), a.N);
-  je = min(max((int64_t)it.cr[2 * q + 1], js), a.N);
-}
-
-// The item's columns through stream_columns: the column block, or each
-// non-empty column range in list order (`skip` applies to the first column
-// streamed).  Block-uniform, as stream_columns requires.
+// The item's columns through stream_columns: the column block, or, in list
+// order, the parts of the column ranges that fall in the chunk's window
+// (`skip` applies to the first column streamed).  Block-uniform, as
+// stream_columns requires.
 template <int S, typename PairFn, typename TileEndFn>
 __device__ __forceinline__ void stream_item(const DirectArgs& a, const Item& it, int skip,
                                             float4* lds, PairFn&& pair, TileEndFn&& tile_end) {
@@ -264,11 +282,15 @@ __device__ __forceinline__ void stream_item(const DirectArgs& a, const Item& it,
     stream_columns<S>(a.ypk, it.j0, it.j1, skip, lds, pair, tile_end);
     return;
   }
-  for (int q = 0; q < it.nrange; ++q) {
+  int64_t off = 0;   // window coordinate of the range's first column
+  for (int q = 0; q < it.nrange && off < it.j1; ++q) {
     int64_t js, je;
-    col_range(a, it, q, js, je);
-    if (je <= js) continue;
-    stream_columns<S>(a.ypk, js, je, skip, lds, pair, tile_end);
+    col_range(a, it.cr, q, js, je);
+    const int64_t len = je - js;
+    const int64_t a0 = max(it.j0 - off, (int64_t)0), a1 = min(it.j1 - off, len);
+    off += len;
+    if (a1 <= a0) continue;
+    stream_columns<S>(a.ypk, js + a0, js + a1, skip, lds, pair, tile_end);
     skip = 0;
   }
 }
@@ -276,10 +298,14 @@ __device__ __forceinline__ void stream_item(const DirectArgs& a, const Item& it,
 // First column of the item (-1 when it has none).
 __device__ __forceinline__ int64_t first_column(const DirectArgs& a, const Item& it) {
   if (it.nrange == 0) return it.j0 < it.j1 ? it.j0 : -1;
-  for (int q = 0; q < it.nrange; ++q) {
+  int64_t off = 0;
+  for (int q = 0; q < it.nrange && off < it.j1; ++q) {
     int64_t js, je;
-    col_range(a, it, q, js, je);
-    if (je > js) return js;
+    col_range(a, it.cr, q, js, je);
+    const int64_t len = je - js;
+    const int64_t a0 = max(it.j0 - off, (int64_t)0), a1 = min(it.j1 - off, len);
+    off += len;
+    if (a1 > a0) return js + a0;
   }
   return -1;
 }
@@ -982,6 +1008,13 @@ int64_t range_grid_bound(int nr, int64_t M, int rows_per_block) {
   return (int64_t)nr + (M + rows_per_block - 1) / rows_per_block;
 }
 
+hipError_t launch_fill2(float* out, int64_t count, float v0, float v1, hipStream_t s) {
+  if (count == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((count + 255) / 256, 8192);
+  hipLaunchKernelGGL(fill2_kernel, dim3((unsigned)blocks), dim3(256), 0, s, out, count, v0, v1);
+  return hipGetLastError();
+}
+
 hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s) {
   if (count == 0) return hipSuccess;
   const int64_t blocks = std::min<int64_t>((count + 255) / 256, 8192);
@@ -997,7 +1030,7 @@ int direct_rows_for(const DirectArgs& a) {
 hipError_t launch_direct(const DirectArgs& a, hipStream_t s) {
   const int R = direct_rows_for(a);
   const int64_t rb = (a.M + (int64_t)kThreads * R - 1) / ((int64_t)kThreads * R);
-  const dim3 grid((unsigned)(a.nr > 0 ? range_grid_bound(a.nr, a.M, kThreads * R) : rb * a.C));
+  const dim3 grid((unsigned)((a.nr > 0 ? range_grid_bound(a.nr, a.M, kThreads * R) : rb) * a.C));
   switch (a.DP) {
     case 1: return launch_dp<1>(a, grid, s);
     case 2: return launch_dp<2>(a, grid, s);

@@ -189,9 +189,36 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, li = lane & 15, g = lane >> 4;
   const int c = blockIdx.x % a.C;
   const int64_t rbk = blockIdx.x / a.C;
-  const int64_t j0 = (int64_t)c * a.jpb;
-  const int64_t j1 = min(a.N16, j0 + a.jpb);
-  const int64_t i0 = rbk * (64 * RB) + wave * (16 * RB);
+  // Dense: row block rbk and column block c.  Block-sparse: a row block of
+  // row cluster I and chunk c of its column ranges (the chunk's window
+  // [w0, w1) counts columns in the ranges' concatenated order).
+  int64_t row0 = rbk * (64 * RB), row_end = a.M;
+  int64_t w0 = (int64_t)c * a.jpb, w1 = min(a.N16, w0 + a.jpb);
+  const int* cr = nullptr;
+  int nrange = 0;
+  if (a.nr > 0) {
+    const int blk = (int)rbk;
+    if (blk >= a.bstart[a.nr]) return;   // a spare workgroup of the grid bound
+    int lo = 0, hi = a.nr - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.bstart[mid] <= blk) lo = mid;
+      else hi = mid - 1;
+    }
+    const int64_t r0 = min(max((int64_t)a.rr[2 * lo], (int64_t)0), a.M);
+    row_end = min(max((int64_t)a.rr[2 * lo + 1], r0), a.M);
+    row0 = r0 + (int64_t)(blk - a.bstart[lo]) * (64 * RB);
+    cr = a.cr + 2 * (int64_t)a.cp[lo];
+    nrange = a.cp[lo + 1] - a.cp[lo];
+    int64_t L = 0;
+    for (int q = 0; q < nrange; ++q) {
+      const int64_t js = min(max((int64_t)cr[2 * q], (int64_t)0), a.N);
+      L += min(max((int64_t)cr[2 * q + 1], js), a.N) - js;
+    }
+    w0 = L * c / a.C;
+    w1 = L * (c + 1) / a.C;
+  }
+  const int64_t i0 = row0 + wave * (16 * RB);
 
   bf16x8 xb[RB];
   float ur[RB][3];
@@ -200,7 +227,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
     const int64_t row = i0 + 16 * rb + li;
 #pragma unroll
     for (int d = 0; d < 3; ++d)
-      ur[rb][d] = (row < a.M && d < a.D) ? (a.x[row * a.D + d] - fr.m[d]) * a.scale : 0.0f;
+      ur[rb][d] = (row < row_end && d < a.D) ? (a.x[row * a.D + d] - fr.m[d]) * a.scale : 0.0f;
     xb[rb] = row_operand(ur[rb], a.D, g, kLse);
   }
   // per lane: sums over its columns (4 g + r of every block) for row li
@@ -215,6 +242,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   uint4 sa[4];
   float4 sx;
   float sb;
+  int64_t j1 = 0;   // end of the column range being streamed (columns beyond it read as zero)
   auto fetch = [&](int64_t jt) {
     const int ncol = (int)min((int64_t)TJF, j1 - jt);
 #pragma unroll
@@ -237,129 +265,148 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
     __builtin_memcpy(&am, &av, 16);
     return am;
   };
-  const int64_t ntiles = (j1 - j0 + TJF - 1) / TJF;
-  if (ntiles > 0) {
-    fetch(j0);
-    put(0);
-  }
-  __syncthreads();
-  for (int64_t t = 0; t < ntiles; ++t) {
-    const int64_t jt = j0 + t * TJF;
-    const int buf = (int)(t & 1);
-    const int nblk = (int)(min((int64_t)TJF, j1 - jt) / 16);
-    if (t + 1 < ntiles) fetch(jt + TJF);
-    if constexpr (!kLse) {
-      // Padding columns have zero extras, so they add nothing: no masking.
-      for (int blk = 0; blk < nblk; ++blk) {
-        const bf16x8 am = a_operand(buf, blk);
-        float4 xv[4];
-        float4 bq;
-        if constexpr (EPI == FAST_SUM) {
-          bq = Bq[buf][blk * 4 + g];   // b of columns 4g .. 4g+3 of the block
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) xv[r] = Xs[buf][blk * 16 + 4 * g + r];
-        }
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+  // Stream the columns [j0, j1) in tiles.  Columns past j1 load as zero rows,
+  // which add nothing to the sums; the log-sum-exp masks them explicitly.
+  auto run_columns = [&](int64_t j0, int64_t jend) {
+    j1 = jend;
+    const int64_t jlim = min(j1, a.N);
+    const int64_t ntiles = (j1 - j0 + TJF - 1) / TJF;
+    if (ntiles > 0) {
+      fetch(j0);
+      put(0);
+    }
+    __syncthreads();
+    for (int64_t t = 0; t < ntiles; ++t) {
+      const int64_t jt = j0 + t * TJF;
+      const int buf = (int)(t & 1);
+      const int nblk = (int)((min((int64_t)TJF, j1 - jt) + 15) / 16);
+      if (t + 1 < ntiles) fetch(jt + TJF);
+      if constexpr (!kLse) {
+        // Padding columns have zero extras, so they add nothing: no masking.
+        for (int blk = 0; blk < nblk; ++blk) {
+          const bf16x8 am = a_operand(buf, blk);
+          float4 xv[4];
+          float4 bq;
           if constexpr (EPI == FAST_SUM) {
-            acc[rb][0] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[0]), bq.x, acc[rb][0]);
-            acc[rb][1] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[1]), bq.y, acc[rb][1]);
-            acc[rb][2] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[2]), bq.z, acc[rb][2]);
-            acc[rb][3] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[3]), bq.w, acc[rb][3]);
+            bq = Bq[buf][blk * 4 + g];   // b of columns 4g .. 4g+3 of the block
           } else {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float k = __builtin_amdgcn_exp2f(T[r]);
-              acc[rb][0] = __builtin_fmaf(k, xv[r].x, acc[rb][0]);
-              acc[rb][1] = __builtin_fmaf(k, xv[r].y, acc[rb][1]);
-              acc[rb][2] = __builtin_fmaf(k, xv[r].z, acc[rb][2]);
-              acc[rb][3] = __builtin_fmaf(k, xv[r].w, acc[rb][3]);
-            }
+            for (int r = 0; r < 4; ++r) xv[r] = Xs[buf][blk * 16 + 4 * g + r];
           }
-        }
-      }
-    } else {
-      // Fast path: the running reference enters the matrix product as its C
-      // operand, so the MFMA returns u = T - m directly; a running maximum of u
-      // over the tile tells afterwards whether any term needed a rescale.
-      const bool ragged = jt + 16 * nblk > a.N;   // padding columns must be masked
-      // The maximum is taken over the bit patterns as signed integers: that
-      // orders non-negative floats correctly and puts every negative one
-      // below them, which is all the test against the threshold needs (and
-      // it avoids the NaN quieting a float max would add per operand).
-      int run[RB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) run[rb] = INT_MIN;
-      if (!ragged) {
-        f4 negm[RB];
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) negm[rb] = f4{-mref[rb], -mref[rb], -mref[rb], -mref[rb]};
-        for (int blk = 0; blk < nblk; ++blk) {
-          const bf16x8 am = a_operand(buf, blk);
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) {
-            const f4 u = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], negm[rb], 0, 0, 0);
-            run[rb] = max(max(run[rb], __float_as_int(u[0])), __float_as_int(u[1]));
-            run[rb] = max(max(run[rb], __float_as_int(u[2])), __float_as_int(u[3]));
-            acc[rb][0] += (__builtin_amdgcn_exp2f(u[0]) + __builtin_amdgcn_exp2f(u[1])) +
-                          (__builtin_amdgcn_exp2f(u[2]) + __builtin_amdgcn_exp2f(u[3]));
-          }
-        }
-      }
-      bool need[RB], redo = false;
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        need[rb] = ragged || run[rb] > __float_as_int(kRescaleF);
-        redo |= need[rb];
-      }
-      if (__any(redo)) {
-        // Rare (a new running maximum, the first tile, or padding columns): the
-        // whole wave recomputes the tile; lanes that need it redo their sums
-        // term by term with rescaling and masking.
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          if (need[rb]) acc[rb][0] = 0.0f;
-        for (int blk = 0; blk < nblk; ++blk) {
-          const bf16x8 am = a_operand(buf, blk);
-          const int64_t jb = jt + blk * 16 + 4 * g;
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) {
             const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-            if (!need[rb]) continue;
+            if constexpr (EPI == FAST_SUM) {
+              acc[rb][0] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[0]), bq.x, acc[rb][0]);
+              acc[rb][1] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[1]), bq.y, acc[rb][1]);
+              acc[rb][2] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[2]), bq.z, acc[rb][2]);
+              acc[rb][3] = __builtin_fmaf(__builtin_amdgcn_exp2f(T[3]), bq.w, acc[rb][3]);
+            } else {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              if (jb + r >= a.N) continue;
-              float d = T[r] - mref[rb];
-              if (d > kRescaleF) {
-                const float f = __builtin_amdgcn_exp2f(-d);
-                acc[rb][0] *= f;
-                tot[rb][0] *= f;
-                mref[rb] = T[r];
-                d = 0.0f;
+              for (int r = 0; r < 4; ++r) {
+                const float k = __builtin_amdgcn_exp2f(T[r]);
+                acc[rb][0] = __builtin_fmaf(k, xv[r].x, acc[rb][0]);
+                acc[rb][1] = __builtin_fmaf(k, xv[r].y, acc[rb][1]);
+                acc[rb][2] = __builtin_fmaf(k, xv[r].z, acc[rb][2]);
+                acc[rb][3] = __builtin_fmaf(k, xv[r].w, acc[rb][3]);
               }
-              acc[rb][0] += __builtin_amdgcn_exp2f(d);
+            }
+          }
+        }
+      } else {
+        // Fast path: the running reference enters the matrix product as its C
+        // operand, so the MFMA returns u = T - m directly; a running maximum of u
+        // over the tile tells afterwards whether any term needed a rescale.
+        const bool ragged = jt + 16 * nblk > jlim;   // columns past the range must be masked
+        // The maximum is taken over the bit patterns as signed integers: that
+        // orders non-negative floats correctly and puts every negative one
+        // below them, which is all the test against the threshold needs (and
+        // it avoids the NaN quieting a float max would add per operand).
+        int run[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) run[rb] = INT_MIN;
+        if (!ragged) {
+          f4 negm[RB];
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) negm[rb] = f4{-mref[rb], -mref[rb], -mref[rb], -mref[rb]};
+          for (int blk = 0; blk < nblk; ++blk) {
+            const bf16x8 am = a_operand(buf, blk);
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+              const f4 u = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], negm[rb], 0, 0, 0);
+              run[rb] = max(max(run[rb], __float_as_int(u[0])), __float_as_int(u[1]));
+              run[rb] = max(max(run[rb], __float_as_int(u[2])), __float_as_int(u[3]));
+              acc[rb][0] += (__builtin_amdgcn_exp2f(u[0]) + __builtin_amdgcn_exp2f(u[1])) +
+                            (__builtin_amdgcn_exp2f(u[2]) + __builtin_amdgcn_exp2f(u[3]));
+            }
+          }
+        }
+        bool need[RB], redo = false;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          need[rb] = ragged || run[rb] > __float_as_int(kRescaleF);
+          redo |= need[rb];
+        }
+        if (__any(redo)) {
+          // Rare (a new running maximum, the first tile, or padding columns): the
+          // whole wave recomputes the tile; lanes that need it redo their sums
+          // term by term with rescaling and masking.
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            if (need[rb]) acc[rb][0] = 0.0f;
+          for (int blk = 0; blk < nblk; ++blk) {
+            const bf16x8 am = a_operand(buf, blk);
+            const int64_t jb = jt + blk * 16 + 4 * g;
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+              const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+              if (!need[rb]) continue;
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                if (jb + r >= jlim) continue;
+                float d = T[r] - mref[rb];
+                if (d > kRescaleF) {
+                  const float f = __builtin_amdgcn_exp2f(-d);
+                  acc[rb][0] *= f;
+                  tot[rb][0] *= f;
+                  mref[rb] = T[r];
+                  d = 0.0f;
+                }
+                acc[rb][0] += __builtin_amdgcn_exp2f(d);
+              }
             }
           }
         }
       }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          tot[rb][q] += acc[rb][q];
+          acc[rb][q] = 0.0f;
+        }
+      if (t + 1 < ntiles) put((int)((t + 1) & 1));
+      __syncthreads();
     }
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        tot[rb][q] += acc[rb][q];
-        acc[rb][q] = 0.0f;
-      }
-    if (t + 1 < ntiles) put((int)((t + 1) & 1));
-    __syncthreads();
+  };
+  if (nrange == 0) {
+    if (a.nr == 0) run_columns(w0, w1);
+  } else {
+    int64_t off = 0;
+    for (int q = 0; q < nrange && off < w1; ++q) {
+      const int64_t js = min(max((int64_t)cr[2 * q], (int64_t)0), a.N);
+      const int64_t len = min(max((int64_t)cr[2 * q + 1], js), a.N) - js;
+      const int64_t a0 = max(w0 - off, (int64_t)0), a1 = min(w1 - off, len);
+      off += len;
+      if (a1 > a0) run_columns(js + a0, js + a1);
+    }
   }
 
   // merge the four lane groups of each row (lanes li, li+16, li+32, li+48)
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int64_t row = i0 + 16 * rb + li;
+    const bool live_row = row < row_end;
     if constexpr (EPI == FAST_LSE) {
       float m = mref[rb], s = tot[rb][0];
 #pragma unroll
@@ -370,7 +417,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
             (m2 == -__builtin_inff() ? 0.0f : s2 * __builtin_amdgcn_exp2f(m2 - mx));
         m = mx;
       }
-      if (g == 0 && row < a.M) {
+      if (g == 0 && live_row) {
         if (a.C == 1) {
           static_cast<float*>(a.out)[row] = (m + __builtin_amdgcn_logf(s)) * kLn2;
         } else {
@@ -387,7 +434,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
         v[q] += __shfl_xor(v[q], 16);
         v[q] += __shfl_xor(v[q], 32);
       }
-      if (g == 0 && row < a.M) {
+      if (g == 0 && live_row) {
         if constexpr (EPI == FAST_SUM) {
           const float sum = (v[0] + v[1]) + (v[2] + v[3]);
           if (a.C == 1) static_cast<float*>(a.out)[row] = sum;
@@ -435,7 +482,7 @@ hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M
 
 hipError_t launch_fast(const FastArgs& a, hipStream_t s) {
   const int rows = fast_rows_per_block(a.epi);
-  const int64_t rb = (a.M + rows - 1) / rows;
+  const int64_t rb = a.nr > 0 ? range_grid_bound(a.nr, a.M, rows) : (a.M + rows - 1) / rows;
   const dim3 grid((unsigned)(rb * a.C));
   switch (a.epi) {
     case FAST_SUM: hipLaunchKernelGGL((fast_kernel<FAST_SUM, 4>), grid, dim3(256), 0, s, a); break;

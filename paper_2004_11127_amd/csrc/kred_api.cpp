@@ -447,17 +447,32 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
 
   kred_params pr;
   if (rg) {
+    // Column chunks of each cluster's list: enough workgroups for every CU.
+    // The pattern lives on the device, so the row-block count is estimated
+    // as max(clusters, M / rows per workgroup) with the kernel's rows per lane.
     pr = *p;
-    pr.col_blocks = 1;   // a block-sparse item reduces its whole column list
+    if (pr.col_blocks == 0) {
+      Plan probe;
+      if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &probe)) return KRED_ERR_UNSUPPORTED;
+      const int EP0 = (r == KRED_R_ARGKMIN) ? 1 : direct_pad_e(std::min(16, probe.E));
+      const int R0 = ext ? direct_rows_per_thread(F_SQDIST, probe.DP, EP0, 0)
+                         : direct_rows_per_thread(kf, probe.DP, EP0, probe.KP);
+      const int epi0 = fast_epi(f, r, M, N, D, E, p->flags);
+      const int64_t rpb = epi0 >= 0 ? fast_rows_per_block(epi0) : (int64_t)kThreads * R0;
+      const int64_t est = std::max<int64_t>({1, (int64_t)rg->nr, (M + rpb - 1) / rpb});
+      pr.col_blocks = (int)std::min<int64_t>(64, ((int64_t)ctx->num_cus * 16 + est - 1) / est);
+    }
     p = &pr;
   }
-  const int epi = rg ? -1 : fast_epi(f, r, M, N, D, E, p->flags);
+  const int epi = fast_epi(f, r, M, N, D, E, p->flags);
   Plan pl;
   if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &pl,
                  epi >= 0 ? fast_rows_per_block(epi) : 0, epi >= 0 ? 256 : 1))
     return KRED_ERR_UNSUPPORTED;
   const FastScratch fs = fast_scratch(epi, N);
-  const int64_t bstart_bytes = rg ? align_up((int64_t)(rg->nr + 1) * (int64_t)sizeof(int)) : 0;
+  // block-sparse: workgroup maps for the direct kernels and for the fast kernel
+  const int64_t bstart_bytes =
+      rg ? 2 * align_up((int64_t)(rg->nr + 1) * (int64_t)sizeof(int)) : 0;
   const kred_status gs =
       grow_scratch(ctx, (size_t)(pl.pack_bytes + pl.part_bytes + fs.guard_bytes + fs.apk_bytes +
                                  fs.ex_bytes + bstart_bytes));
@@ -468,6 +483,8 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   char* fbase = sbase + pl.pack_bytes + pl.part_bytes;
   int* bstart = rg ? reinterpret_cast<int*>(fbase + fs.guard_bytes + fs.apk_bytes + fs.ex_bytes)
                    : nullptr;
+  int* fbstart = rg ? reinterpret_cast<int*>(reinterpret_cast<char*>(bstart) + bstart_bytes / 2)
+                    : nullptr;
   FastGuard* guard = epi >= 0 ? reinterpret_cast<FastGuard*>(fbase) : nullptr;
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
 
@@ -505,6 +522,16 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     fa.eb = fp.eb;
     fa.out = out;
     fa.part = part;
+    if (rg) {
+      fa.nr = rg->nr;
+      fa.rr = rg->rr;
+      fa.cp = rg->cp;
+      fa.cr = rg->cr;
+      fa.bstart = fbstart;
+      if (launch_range_blocks(rg->rr, rg->nr, M, fast_rows_per_block(epi), fbstart, s) !=
+          hipSuccess)
+        return KRED_ERR_HIP;
+    }
   }
   const int n_slices = (r == KRED_R_ARGKMIN) ? 1 : (pl.E + 15) / 16;
   for (int sl = 0; sl < n_slices; ++sl) {
@@ -562,6 +589,23 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
       if (launch_range_blocks(rg->rr, rg->nr, M, kThreads * direct_rows_for(da), bstart, s) !=
           hipSuccess)
         return KRED_ERR_HIP;
+      if (pl.C > 1) {
+        // rows outside every cluster get no partials from the kernels: start
+        // every partial at the empty value, so the combine yields the empty
+        // reduction for them
+        const int W = partial_width(kf, pl.DP, EP, pl.KP, ext);
+        float v0 = 0.0f, v1 = 0.0f;
+        if (kf == F_SINKHORN || kf == F_LAPLACE_LSE) v0 = -INFINITY;   // (m, s) = (-inf, 0)
+        if (pl.KP > 0) {
+          v0 = INFINITY;
+          v1 = __builtin_bit_cast(float, (int32_t)INT32_MAX);   // (distance, index)
+        }
+        if (ext) {
+          v0 = INFINITY;
+          v1 = __builtin_bit_cast(float, (int32_t)-1);          // (sign * value, index)
+        }
+        if (launch_fill2(part, (int64_t)pl.C * M * W, v0, v1, s) != hipSuccess) return KRED_ERR_HIP;
+      }
     }
     hipEvent_t e_start = nullptr, e_stop = nullptr;
     if (prof) {

@@ -83,7 +83,7 @@ struct DirectArgs {
   int formula;            // F_*
   int D, DP, E, EP, e0;   // E-slice [e0, e0 + min(EP, E - e0)) of b / out
   int64_t M, N;
-  int C;                  // column blocks; C == 1 writes the final output
+  int C;                  // column blocks (block-sparse: column chunks); C == 1 writes the final output
   int64_t jpb;            // j per column block
   const float* x;         // M x D
   const float* ypk;       // N x (DP + EP), from the prologue
@@ -209,6 +209,13 @@ struct FastArgs {
   const float* eb;
   void* out;
   float* part;
+  // block-sparse pattern (nr > 0), as in DirectArgs; bstart counts row
+  // blocks of fast_rows_per_block rows
+  int nr;
+  const int* rr;
+  const int* cp;
+  const int* cr;
+  const int* bstart;
 };
 hipError_t launch_fast(const FastArgs& a, hipStream_t s);
 int fast_rows_per_block(int epi);
@@ -216,5 +223,6 @@ int fast_rows_per_block(int epi);
 // Fill out with a constant (N = 0 cases); a kernel, not a memset, so that
 // callers may capture it in a graph.
 hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s);
+hipError_t launch_fill2(float* out, int64_t count, float v0, float v1, hipStream_t s);
 
 }  // namespace kred

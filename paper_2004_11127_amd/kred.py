@@ -196,13 +196,14 @@ class Context:
         return t.data_ptr() if t.numel() else None
 
     def run_ranges(self, formula, reduction, x, y, b, row_ranges, col_ptr, col_ranges, out=None,
-                   sigma=1.0, eps=1.0, K=0, flags=0, stream=None):
+                   sigma=1.0, eps=1.0, K=0, col_blocks=0, flags=0, stream=None):
         """Block-sparse reduction (kred_run_ranges): row cluster I = rows
         row_ranges[I, 0] .. row_ranges[I, 1] - 1 reduces over the column ranges
         col_ranges[col_ptr[I] : col_ptr[I + 1]] only.  The index arrays are int32
-        GPU tensors (nr x 2, nr + 1, nnz x 2); otherwise as run()."""
+        GPU tensors (nr x 2, nr + 1, nnz x 2); col_blocks splits each cluster's
+        columns into that many chunks (0 = automatic); otherwise as run()."""
         return self.run(formula, reduction, x, y, b, out=out, sigma=sigma, eps=eps, K=K,
-                        flags=flags, stream=stream,
+                        col_blocks=col_blocks, flags=flags, stream=stream,
                         _ranges=(row_ranges, col_ptr, col_ranges))
 
     def run(self, formula, reduction, x, y, b=None, out=None, sigma=1.0, eps=1.0, K=0,

@@ -43,11 +43,15 @@ def random_pattern(rng, M, N, n_rc, n_cc, p_keep=0.4):
 
 
 def call(ctx, formula, reduction, x, y, b, pat, **kw):
+    """kred_run_ranges (automatic column chunks unless col_blocks is given)."""
     import torch
     rows, ptr, cr = pat
     crt = dev(cr) if cr.size else torch.zeros((0, 2), dtype=torch.int32, device="cuda")
     return host(ctx.run_ranges(formula, reduction, dev(x), dev(y), None if b is None else dev(b),
                                dev(rows), dev(ptr), crt, **kw))
+
+
+CHUNKS = [0, 1, 5]   # automatic, none, five column chunks per cluster
 
 
 SUMS = [
@@ -60,14 +64,15 @@ SUMS = [
 ]
 
 
+@pytest.mark.parametrize("C", CHUNKS)
 @pytest.mark.parametrize("formula,M,N,D,E,sigma,cl", SUMS)
-def test_ranges_sum(ctx, formula, M, N, D, E, sigma, cl):
+def test_ranges_sum(ctx, formula, M, N, D, E, sigma, cl, C):
     rng = np.random.default_rng(M + N + E)
     x = rng.uniform(0, 1, (M, D)).astype(np.float32)
     y = rng.uniform(0, 1, (N, D)).astype(np.float32)
     b = rng.standard_normal((N, E)).astype(np.float32)
     pat = random_pattern(rng, M, N, *cl)
-    out = call(ctx, formula, "sum", x, y, b, pat, sigma=sigma)
+    out = call(ctx, formula, "sum", x, y, b, pat, sigma=sigma, col_blocks=C)
     ref, norm = oracle.ranges_reduce("sum", x, y, b, *pat, formula=formula, sigma=sigma)
     assert norm_err(out, ref, norm) <= SUM_TOL
     covered = np.zeros(M, bool)
@@ -82,20 +87,24 @@ def test_ranges_gradx(ctx):
     x = rng.uniform(0, 1, (M, 3)).astype(np.float32); y = rng.uniform(0, 1, (N, 3)).astype(np.float32)
     b = rng.standard_normal((N, 1)).astype(np.float32)
     pat = random_pattern(rng, M, N, 12, 15)
-    out = call(ctx, "gauss_gradx", "sum", x, y, b, pat, sigma=0.1)
+    for C in CHUNKS:
+        out = call(ctx, "gauss_gradx", "sum", x, y, b, pat, sigma=0.1, col_blocks=C)
+        ref, norm = oracle.ranges_reduce("gradx", x, y, b, *pat, sigma=0.1)
+        assert norm_err(out, ref, norm) <= SUM_TOL
     ref, norm = oracle.ranges_reduce("gradx", x, y, b, *pat, sigma=0.1)
     assert norm_err(out, ref, norm) <= SUM_TOL
 
 
+@pytest.mark.parametrize("C", CHUNKS)
 @pytest.mark.parametrize("formula,param", [("sinkhorn", 0.01), ("gauss", 0.1), ("laplace", 0.05)])
-def test_ranges_lse(ctx, formula, param):
+def test_ranges_lse(ctx, formula, param, C):
     rng = np.random.default_rng(2)
     M, N = 3000, 2500
     x = rng.uniform(0, 1, (M, 3)).astype(np.float32); y = rng.uniform(0, 1, (N, 3)).astype(np.float32)
     g = (2.0 * rng.standard_normal((N, 1))).astype(np.float32)
     pat = random_pattern(rng, M, N, 10, 12)
     kw = dict(eps=param) if formula == "sinkhorn" else dict(sigma=param)
-    out = call(ctx, formula, "lse", x, y, g, pat, **kw)
+    out = call(ctx, formula, "lse", x, y, g, pat, col_blocks=C, **kw)
     okw = dict(eps=param) if formula == "sinkhorn" else dict(formula=formula, sigma=param)
     ref, m = oracle.ranges_reduce("lse", x, y, g, *pat, **okw)
     empty = np.isneginf(ref)
@@ -103,19 +112,21 @@ def test_ranges_lse(ctx, formula, param):
     assert lse_err(out[~empty, 0], ref[~empty], m[~empty]) <= LSE_TOL
 
 
+@pytest.mark.parametrize("C", CHUNKS)
 @pytest.mark.parametrize("red,K", [("argkmin", 5), ("kmin", 5), ("argkmin", 1)])
-def test_ranges_knn_exact(ctx, red, K):
+def test_ranges_knn_exact(ctx, red, K, C):
     rng = np.random.default_rng(3 + K)
     M, N, D = 2000, 3000, 4
     x = rng.integers(-3, 4, (M, D)).astype(np.float32); y = rng.integers(-3, 4, (N, D)).astype(np.float32)
     pat = random_pattern(rng, M, N, 8, 20, p_keep=0.15)   # some clusters get fewer than K columns
-    out = call(ctx, "sqdist", red, x, y, None, pat, K=K)
+    out = call(ctx, "sqdist", red, x, y, None, pat, K=K, col_blocks=C)
     ref, _ = oracle.ranges_reduce(red, x, y, None, *pat, K=K)
     np.testing.assert_array_equal(out, ref.astype(out.dtype))
 
 
+@pytest.mark.parametrize("C", CHUNKS)
 @pytest.mark.parametrize("red", ["min", "max", "argmin", "argmax"])
-def test_ranges_extreme_exact(ctx, red):
+def test_ranges_extreme_exact(ctx, red, C):
     rng = np.random.default_rng(4)
     M, N = 1500, 2000
     x = rng.integers(-3, 4, (M, 3)).astype(np.float32); y = rng.integers(-3, 4, (N, 3)).astype(np.float32)
@@ -123,7 +134,7 @@ def test_ranges_extreme_exact(ctx, red):
     pat = random_pattern(rng, M, N, 7, 9)
     op = "max" if "max" in red else "min"
     for bb in (None, b):
-        out = call(ctx, "sqdist", red, x, y, bb, pat)
+        out = call(ctx, "sqdist", red, x, y, bb, pat, col_blocks=C)
         val, idx = oracle.ranges_reduce(op, x, y, bb, *pat, formula="sqdist")
         ref = idx.astype(np.int32) if red.startswith("arg") else val.astype(np.float32)
         np.testing.assert_array_equal(out, ref)
@@ -144,10 +155,11 @@ def test_ranges_clamped_and_empty_patterns(ctx):
     assert (out[200:400] == 0).all()
     # no clusters at all: every row holds the empty reduction
     empty = (np.zeros((0, 2), np.int32), np.zeros(1, np.int32), np.zeros((0, 2), np.int32))
-    out = call(ctx, "gauss", "sum", x, y, b, empty, sigma=0.2)
-    assert (out == 0).all()
-    out = call(ctx, "sinkhorn", "lse", x, y, b, empty, eps=0.1)
-    assert np.isneginf(out).all()
+    for C in CHUNKS:
+        out = call(ctx, "gauss", "sum", x, y, b, empty, sigma=0.2, col_blocks=C)
+        assert (out == 0).all()
+        out = call(ctx, "sinkhorn", "lse", x, y, b, empty, eps=0.1, col_blocks=C)
+        assert np.isneginf(out).all()
 
 
 def test_ranges_full_pattern_matches_dense(ctx):
@@ -157,6 +169,52 @@ def test_ranges_full_pattern_matches_dense(ctx):
     x = rng.uniform(0, 1, (M, 3)).astype(np.float32); y = rng.uniform(0, 1, (N, 3)).astype(np.float32)
     b = rng.standard_normal((N, 2)).astype(np.float32)
     pat = (np.array([[0, M]], np.int32), np.array([0, 1], np.int32), np.array([[0, N]], np.int32))
-    out = call(ctx, "gauss", "sum", x, y, b, pat, sigma=0.1)
+    out = call(ctx, "gauss", "sum", x, y, b, pat, sigma=0.1, col_blocks=1)
     dense = host(ctx.run("gauss", "sum", dev(x), dev(y), dev(b), sigma=0.1, col_blocks=1))
     np.testing.assert_array_equal(out, dense)
+
+
+FAST = [
+    # formula, reduction, D, param, chunks
+    ("gauss", "sum", 3, 0.05, 0), ("gauss", "sum", 2, 0.1, 1), ("gauss", "sum", 3, 0.05, 5),
+    ("gauss_gradx", "sum", 3, 0.05, 0), ("gauss_gradx", "sum", 1, 0.1, 3),
+    ("sinkhorn", "lse", 3, 0.01, 0), ("sinkhorn", "lse", 3, 0.01, 4), ("gauss", "lse", 2, 0.1, 0),
+]
+
+
+@pytest.mark.parametrize("formula,reduction,D,param,C", FAST)
+def test_ranges_fast_path(ctx, formula, reduction, D, param, C):
+    # D <= 3 with KRED_FLAG_FAST: the matrix-core exponent kernel walks the
+    # same pattern (ranges start and end anywhere, not on 16-column blocks)
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(D * 10 + C)
+    M, N = 5000, 4000
+    x = rng.uniform(0, 1, (M, D)).astype(np.float32); y = rng.uniform(0, 1, (N, D)).astype(np.float32)
+    b = rng.standard_normal((N, 1)).astype(np.float32)
+    pat = random_pattern(rng, M, N, 20, 30)
+    kw = dict(eps=param) if formula == "sinkhorn" else dict(sigma=param)
+    out = call(ctx, formula, reduction, x, y, b, pat, col_blocks=C, flags=kred.FLAG_FAST, **kw)
+    if reduction == "lse":
+        okw = dict(eps=param) if formula == "sinkhorn" else dict(formula=formula, sigma=param)
+        ref, m = oracle.ranges_reduce("lse", x, y, b, *pat, **okw)
+        empty = np.isneginf(ref)
+        assert np.isneginf(out[empty, 0]).all()
+        assert lse_err(out[~empty, 0], ref[~empty], m[~empty]) <= LSE_TOL
+    elif formula == "gauss_gradx":
+        ref, norm = oracle.ranges_reduce("gradx", x, y, b, *pat, sigma=param)
+        assert norm_err(out, ref, norm) <= SUM_TOL
+    else:
+        ref, norm = oracle.ranges_reduce("sum", x, y, b, *pat, formula="gauss", sigma=param)
+        assert norm_err(out, ref, norm) <= SUM_TOL
+
+
+def test_ranges_fast_kernel_is_used(ctx):
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(11)
+    x = rng.uniform(0, 1, (3000, 3)).astype(np.float32); y = rng.uniform(0, 1, (3000, 3)).astype(np.float32)
+    b = rng.standard_normal((3000, 1)).astype(np.float32)
+    pat = random_pattern(rng, 3000, 3000, 6, 8)
+    ctx.profile_collect()
+    call(ctx, "gauss", "sum", x, y, b, pat, sigma=0.1, flags=kred.FLAG_FAST | kred.FLAG_PROFILE)
+    n, ms, name = ctx.profile_collect()
+    assert name == "fast_kernel"
