@@ -739,6 +739,7 @@ template <int DP, int KP, int R>
 __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
   constexpr int S = DP + 1;   // the prologue pads one zero signal column
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;   // K = 1 on the fast path
   const Item it = item_of<R>(a);
   if (!it.live) return;
   float xr[R][DP];

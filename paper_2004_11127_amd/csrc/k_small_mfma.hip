@@ -18,6 +18,10 @@
 // centre m; the prologue computes it on the device and the kernels fall back
 // to the direct form when c R^2 > kFastLimit (no host synchronisation).
 //
+// The nearest-neighbour variant (FAST_MIN) flips every sign, so that the
+// matrix core returns the squared distance |u - v|^2 itself (c = 1, centred
+// coordinates): minimum and arg-minimum then need no exp at all.
+//
 // K slots (A: column side, B: row side), for coordinate d = 0..2:
 //   6d + 0..5:  A = (Vh, Vm, Vh, Vl, Vh, Vm) of V = 2 v_d,
 //               B = (uh, uh, um, uh, ul, um) of u_d
@@ -112,13 +116,14 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
     if (j < a.N) {
       float v[3] = {0.f, 0.f, 0.f};
       float nv = 0.0f;
+      const float sg = a.epi == FAST_MIN ? -1.0f : 1.0f;   // MIN: T = +|u - v|^2
 #pragma unroll
       for (int d = 0; d < 3; ++d)
         if (d < a.D) {
           v[d] = (a.y[j * a.D + d] - fr.m[d]) * a.scale;
           nv = __builtin_fmaf(v[d], v[d], nv);
           __bf16 h, m, l;
-          split3(2.0f * v[d], h, m, l);
+          split3(sg * 2.0f * v[d], h, m, l);
           s[6 * d + 0] = h;
           s[6 * d + 1] = m;
           s[6 * d + 2] = h;
@@ -126,14 +131,14 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
           s[6 * d + 4] = h;
           s[6 * d + 5] = m;
         }
-      split3(-nv, s[18], s[19], s[20]);
+      split3(-sg * nv, s[18], s[19], s[20]);
       s[21] = s[22] = s[23] = (__bf16)1.0f;
-      const float bj = a.b[j];
+      const float bj = a.epi == FAST_MIN ? 0.0f : a.b[j];   // MIN reads no b
       if (a.epi == FAST_LSE) {
         split3(bj * kLog2e, s[24], s[25], s[26]);
       } else if (a.epi == FAST_GRADX) {
         ex = float4{bj, bj * v[0], bj * v[1], bj * v[2]};
-      } else {
+      } else if (a.epi == FAST_SUM) {
         ex.x = bj;
       }
     }
@@ -147,7 +152,8 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
 }
 
 // Row-side B operand: this lane's 8 K slots (8g .. 8g+7) for its row.
-__device__ __forceinline__ bf16x8 row_operand(const float (&u)[3], int D, int g, bool lse) {
+__device__ __forceinline__ bf16x8 row_operand(const float (&u)[3], int D, int g, bool lse,
+                                               bool neg) {
   __bf16 s[32];
 #pragma unroll
   for (int k = 0; k < 32; ++k) s[k] = (__bf16)0.0f;
@@ -166,7 +172,7 @@ __device__ __forceinline__ bf16x8 row_operand(const float (&u)[3], int D, int g,
       nu = __builtin_fmaf(u[d], u[d], nu);
     }
   s[18] = s[19] = s[20] = (__bf16)1.0f;
-  split3(-nu, s[21], s[22], s[23]);
+  split3(neg ? nu : -nu, s[21], s[22], s[23]);
   if (lse) s[24] = s[25] = s[26] = (__bf16)1.0f;
   bf16x8 o;
 #pragma unroll
@@ -176,9 +182,11 @@ __device__ __forceinline__ bf16x8 row_operand(const float (&u)[3], int D, int g,
 
 // EPI: FAST_SUM (Gauss, E = 1), FAST_GRADX, FAST_LSE.
 
-template <int EPI, int RB>
+// KV (FAST_MIN): write the distance (else the index).
+template <int EPI, int RB, bool KV = false>
 __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   constexpr bool kLse = EPI == FAST_LSE;
+  constexpr bool kMin = EPI == FAST_MIN;
   __shared__ uint4 As[2][TJF * 4];
   __shared__ float4 Xs[2][EPI == FAST_GRADX ? TJF : 1];   // (b, b v) per column
   __shared__ float4 Bq[2][EPI == FAST_SUM ? TJF / 4 : 1];  // b per column, 4 to a float4
@@ -228,9 +236,16 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
 #pragma unroll
     for (int d = 0; d < 3; ++d)
       ur[rb][d] = (row < row_end && d < a.D) ? (a.x[row * a.D + d] - fr.m[d]) * a.scale : 0.0f;
-    xb[rb] = row_operand(ur[rb], a.D, g, kLse);
+    xb[rb] = row_operand(ur[rb], a.D, g, kLse, kMin);
   }
-  // per lane: sums over its columns (4 g + r of every block) for row li
+  // per lane: sums over its columns (4 g + r of every block) for row li;
+  // MIN: the smallest distance (as its int bits, exact order for d >= 0) and its column
+  int best[RB], bidx[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    best[rb] = INT_MAX;
+    bidx[rb] = INT_MAX;
+  }
   float acc[RB][4], tot[RB][4], mref[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
@@ -281,7 +296,50 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
       const int buf = (int)(t & 1);
       const int nblk = (int)((min((int64_t)TJF, j1 - jt) + 15) / 16);
       if (t + 1 < ntiles) fetch(jt + TJF);
-      if constexpr (!kLse) {
+      if constexpr (kMin) {
+        // d for the lane's columns 4g + r of each block.  Full blocks first,
+        // then the range's last block if columns past its end (zero A rows,
+        // d = 0) must be masked; each MFMA is followed by straight-line
+        // reads of its result, with no branch in between.
+        const bool ragged = jt + 16 * nblk > jlim;
+        const int nfull = ragged ? nblk - 1 : nblk;
+        auto take = [&](int rb, int64_t jb, const int (&d)[4]) {
+          const int m4 = min(min(min(d[0], d[1]), d[2]), d[3]);
+          if constexpr (KV) {
+            best[rb] = min(best[rb], m4);
+          } else if (__builtin_expect(m4 < best[rb], 0)) {
+            // strictly smaller: the lowest r reaching it (columns come in increasing j)
+            const int r = d[0] == m4 ? 0 : (d[1] == m4 ? 1 : (d[2] == m4 ? 2 : 3));
+            best[rb] = m4;
+            bidx[rb] = (int)(jb + r);
+          }
+        };
+        for (int blk = 0; blk < nfull; ++blk) {
+          const bf16x8 am = a_operand(buf, blk);
+          const int64_t jb = jt + blk * 16 + 4 * g;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            const int d[4] = {__float_as_int(T[0]), __float_as_int(T[1]), __float_as_int(T[2]),
+                              __float_as_int(T[3])};
+            take(rb, jb, d);
+          }
+        }
+        if (ragged) {
+          const int blk = nblk - 1;
+          const bf16x8 am = a_operand(buf, blk);
+          const int64_t jb = jt + blk * 16 + 4 * g;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            const int d[4] = {jb + 0 < jlim ? __float_as_int(T[0]) : INT_MAX,
+                              jb + 1 < jlim ? __float_as_int(T[1]) : INT_MAX,
+                              jb + 2 < jlim ? __float_as_int(T[2]) : INT_MAX,
+                              jb + 3 < jlim ? __float_as_int(T[3]) : INT_MAX};
+            take(rb, jb, d);
+          }
+        }
+      } else if constexpr (!kLse) {
         // Padding columns have zero extras, so they add nothing: no masking.
         for (int blk = 0; blk < nblk; ++blk) {
           const bf16x8 am = a_operand(buf, blk);
@@ -407,7 +465,30 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   for (int rb = 0; rb < RB; ++rb) {
     const int64_t row = i0 + 16 * rb + li;
     const bool live_row = row < row_end;
-    if constexpr (EPI == FAST_LSE) {
+    if constexpr (kMin) {
+      // smallest (distance, index) over the four lane groups; ties keep the lower index
+      int v = best[rb], j = bidx[rb];
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        const int v2 = __shfl_xor(v, o), j2 = __shfl_xor(j, o);
+        if (v2 < v || (v2 == v && j2 < j)) {
+          v = v2;
+          j = j2;
+        }
+      }
+      if (g == 0 && live_row) {
+        // a tiny negative distance from rounding reads as 0
+        const float dv = v == INT_MAX ? __builtin_inff() : fmaxf(__int_as_float(v), 0.0f);
+        if (a.C == 1) {
+          if constexpr (KV) static_cast<float*>(a.out)[row] = dv;
+          else static_cast<int*>(a.out)[row] = j == INT_MAX ? -1 : j;
+        } else {
+          float* p = a.part + ((int64_t)c * a.M + row) * 2;   // one (distance, index) list entry
+          p[0] = dv;
+          p[1] = __int_as_float(j);
+        }
+      }
+    } else if constexpr (EPI == FAST_LSE) {
       float m = mref[rb], s = tot[rb][0];
 #pragma unroll
       for (int o = 16; o <= 32; o <<= 1) {
@@ -488,6 +569,10 @@ hipError_t launch_fast(const FastArgs& a, hipStream_t s) {
     case FAST_SUM: hipLaunchKernelGGL((fast_kernel<FAST_SUM, 4>), grid, dim3(256), 0, s, a); break;
     case FAST_GRADX: hipLaunchKernelGGL((fast_kernel<FAST_GRADX, 4>), grid, dim3(256), 0, s, a); break;
     case FAST_LSE: hipLaunchKernelGGL((fast_kernel<FAST_LSE, 4>), grid, dim3(256), 0, s, a); break;
+    case FAST_MIN:
+      if (a.kvalues) hipLaunchKernelGGL((fast_kernel<FAST_MIN, 4, true>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((fast_kernel<FAST_MIN, 4, false>), grid, dim3(256), 0, s, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

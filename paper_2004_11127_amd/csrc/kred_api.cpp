@@ -158,12 +158,14 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
 constexpr double kFastMinPairs = 268435456.0;   // 2^28 pairs
 
 int fast_epi(kred_formula f, kred_reduction r, int64_t M, int64_t N, int32_t D, int32_t E,
-             uint32_t flags) {
+             uint32_t flags, int K = 0) {
   if (D > 3 || (flags & KRED_FLAG_DIRECT)) return -1;
   if (!(flags & KRED_FLAG_FAST) && (double)M * (double)N < kFastMinPairs) return -1;
   if (f == KRED_F_GAUSS && r == KRED_R_SUM && E == 1) return FAST_SUM;
   if (f == KRED_F_GAUSS_GRADX && r == KRED_R_SUM) return FAST_GRADX;
   if ((f == KRED_F_SINKHORN || f == KRED_F_GAUSS) && r == KRED_R_LSE) return FAST_LSE;
+  // nearest neighbour: arg-K-min with K = 1, and the distance's min / arg-min
+  if (f == KRED_F_SQDIST && r == KRED_R_ARGKMIN && K == 1) return FAST_MIN;
   return -1;
 }
 
@@ -457,14 +459,14 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
       const int EP0 = (r == KRED_R_ARGKMIN) ? 1 : direct_pad_e(std::min(16, probe.E));
       const int R0 = ext ? direct_rows_per_thread(F_SQDIST, probe.DP, EP0, 0)
                          : direct_rows_per_thread(kf, probe.DP, EP0, probe.KP);
-      const int epi0 = fast_epi(f, r, M, N, D, E, p->flags);
+      const int epi0 = fast_epi(f, r, M, N, D, E, p->flags, p->K);
       const int64_t rpb = epi0 >= 0 ? fast_rows_per_block(epi0) : (int64_t)kThreads * R0;
       const int64_t est = std::max<int64_t>({1, (int64_t)rg->nr, (M + rpb - 1) / rpb});
       pr.col_blocks = (int)std::min<int64_t>(64, ((int64_t)ctx->num_cus * 16 + est - 1) / est);
     }
     p = &pr;
   }
-  const int epi = fast_epi(f, r, M, N, D, E, p->flags);
+  const int epi = fast_epi(f, r, M, N, D, E, p->flags, p->K);
   Plan pl;
   if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &pl,
                  epi >= 0 ? fast_rows_per_block(epi) : 0, epi >= 0 ? 256 : 1))
@@ -522,6 +524,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     fa.eb = fp.eb;
     fa.out = out;
     fa.part = part;
+    fa.kvalues = kvalues;
     if (rg) {
       fa.nr = rg->nr;
       fa.rr = rg->rr;
@@ -838,7 +841,7 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
     if (!make_mplan(f, r, p, M, N, D, E, 256, &mp)) return -1;
     return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes;
   }
-  const int epi = fast_epi(f, r, M, N, D, E, p->flags);
+  const int epi = fast_epi(f, r, M, N, D, E, p->flags, p->K);
   Plan pl;
   if (!make_plan(f, r, p, M, N, D, E, 256, &pl, epi >= 0 ? fast_rows_per_block(epi) : 0,
                  epi >= 0 ? 256 : 1))

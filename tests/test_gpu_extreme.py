@@ -165,3 +165,57 @@ def test_extreme_deterministic_and_profiled(ctx):
     assert n == 1 and name == "extreme_kernel"
     r2 = host(ctx.run("gauss", "argmax", x, y, b, sigma=0.05))
     np.testing.assert_array_equal(r1, r2)
+
+
+FAST_NN = [
+    # M, N, D, C
+    (1, 1, 3, 0), (700, 2049, 3, 3), (3000, 5000, 2, 0), (1500, 999, 1, 16),
+]
+
+
+@pytest.mark.parametrize("M,N,D,C", FAST_NN)
+@pytest.mark.parametrize("red", ["min", "argmin", "argkmin1"])
+def test_nearest_fast_path_exact(ctx, M, N, D, C, red):
+    # D <= 3 with KRED_FLAG_FAST: the distance comes from the matrix cores (exact
+    # on integer coordinates); min / arg-min / arg-K-min with K = 1 must match
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(M + N + D + C)
+    x, y = _ints(rng, M, D, -20, 21), _ints(rng, N, D, -20, 21)
+    if red == "argkmin1":
+        out = host(ctx.run("sqdist", "argkmin", dev(x), dev(y), None, K=1, col_blocks=C,
+                           flags=kred.FLAG_FAST))
+    else:
+        out = host(ctx.run("sqdist", red, dev(x), dev(y), None, col_blocks=C, flags=kred.FLAG_FAST))
+    val, idx, _ = oracle.extreme("sqdist", "min", x, y)
+    if red == "min":
+        np.testing.assert_array_equal(out, val.astype(np.float32))
+    else:
+        np.testing.assert_array_equal(out, idx.astype(np.int32))
+
+
+def test_nearest_fast_path_real_data(ctx):
+    # real-valued mixture data: the distance and a valid nearest index
+    from paper_2004_11127_amd import inputs, kred
+    w = inputs.mixture_gauss(M=20000, N=30000, D=3, sigma=0.05, seed=3)
+    d = host(ctx.run("sqdist", "min", dev(w.x), dev(w.y), None, flags=kred.FLAG_FAST))
+    j = host(ctx.run("sqdist", "argmin", dev(w.x), dev(w.y), None, flags=kred.FLAG_FAST))
+    val, idx, scale = oracle.extreme("sqdist", "min", w.x, w.y)
+    allow = TOL * scale
+    assert (np.abs(d.astype(np.float64) - val) <= allow).all()
+    f = _f_at("sqdist", w.x, w.y, None, j.astype(np.int64), 1.0)
+    assert (np.abs(f - val) <= allow).all()
+    assert (j == idx).mean() > 0.999
+
+
+def test_nearest_fast_kernel_is_used_and_falls_back(ctx):
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(12)
+    x = rng.uniform(0, 1, (3000, 3)).astype(np.float32); y = rng.uniform(0, 1, (3000, 3)).astype(np.float32)
+    ctx.profile_collect()
+    ctx.run("sqdist", "min", dev(x), dev(y), None, flags=kred.FLAG_FAST | kred.FLAG_PROFILE)
+    assert ctx.profile_collect()[2] == "fast_kernel"
+    # data far outside the accuracy guard (half-diagonal 86): the direct kernel answers
+    xs, ys = x * 100.0, y * 100.0
+    d = host(ctx.run("sqdist", "min", dev(xs), dev(ys), None, flags=kred.FLAG_FAST))
+    val, _, scale = oracle.extreme("sqdist", "min", xs, ys)
+    assert (np.abs(d.astype(np.float64) - val) <= TOL * scale).all()

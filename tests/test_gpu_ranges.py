@@ -218,3 +218,17 @@ def test_ranges_fast_kernel_is_used(ctx):
     call(ctx, "gauss", "sum", x, y, b, pat, sigma=0.1, flags=kred.FLAG_FAST | kred.FLAG_PROFILE)
     n, ms, name = ctx.profile_collect()
     assert name == "fast_kernel"
+
+
+@pytest.mark.parametrize("red", ["min", "argmin"])
+def test_ranges_nearest_fast_path(ctx, red):
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(13)
+    M, N = 4000, 5000
+    x = rng.integers(-20, 21, (M, 3)).astype(np.float32); y = rng.integers(-20, 21, (N, 3)).astype(np.float32)
+    pat = random_pattern(rng, M, N, 15, 25)
+    for C in CHUNKS:
+        out = call(ctx, "sqdist", red, x, y, None, pat, col_blocks=C, flags=kred.FLAG_FAST)
+        val, idx = oracle.ranges_reduce("min", x, y, None, *pat, formula="sqdist")
+        ref = idx.astype(np.int32) if red == "argmin" else val.astype(np.float32)
+        np.testing.assert_array_equal(out, ref)
