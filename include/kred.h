@@ -74,9 +74,16 @@ typedef enum kred_status {
 #define KRED_FLAG_PROFILE 1u  /* time the main kernel of each call with HIP events (kred_profile_collect) */
 #define KRED_FLAG_DIRECT 2u   /* D <= 3: always use the direct-form kernels, never the matrix-core exponent
                                  (used otherwise only below 2^28 pairs, or when the data's extent makes
-                                 the matrix-core form less accurate) */
+                                 the matrix-core form less accurate).  D > 16 arg-K-min (and K-min,
+                                 min / arg-min without b): always the fp32 matrix-core kernel, never
+                                 the exact bf16 one */
 #define KRED_FLAG_FAST 4u     /* D <= 3: use the matrix-core exponent whatever the problem size (the
-                                 accuracy guard still falls back to the direct form); DIRECT wins */
+                                 accuracy guard still falls back to the direct form).  D > 16
+                                 arg-K-min: consider the exact bf16 kernel whatever the size (it
+                                 runs only when every coordinate is an integer with |v| <= 256 and
+                                 D max|v|^2 <= 2^22, where bf16 products and fp32 sums are exact;
+                                 otherwise the fp32 kernel runs; by default it is considered from
+                                 2^28 pairs).  DIRECT wins */
 
 /* Per-call parameters (the "parameters p" of Eq. (2)). */
 typedef struct kred_params {

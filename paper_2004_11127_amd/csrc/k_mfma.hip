@@ -46,13 +46,15 @@ __device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
 // ------------------------------------------------------------------ prologue
 // Coalesced: consecutive threads handle consecutive d of one column.
 __global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
+  const bool ex = exact_ok(a.exact, a.D);   // arg-K-min on the exact bf16 path
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const int64_t total = a.N16 * a.DP;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total; t += stride) {
     const int64_t j = t / a.DP;
     const int d = (int)(t - j * a.DP);
     const float v = (j < a.N && d < a.D) ? a.y[j * a.D + d] : 0.0f;
-    a.yop[t] = v * a.yop_scale;
+    if (ex) a.ybf[t] = __builtin_bit_cast(unsigned short, (__bf16)(v * a.yop_scale));
+    else a.yop[t] = v * a.yop_scale;
   }
   // signal tiles: b[j][e0 + e] stored at (j/16)*16W + ((j%16)/4)*4W + e*4 + j%4, W = 16*EB
   if (a.bpk != nullptr) {
@@ -125,6 +127,9 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
   __shared__ float4 ns[2][TJ / 4];
   __shared__ float4 bs[2][SUM ? TJ * W / 4 : 1];
 
+  if constexpr (!SUM) {
+    if (exact_ok(a.exact, a.D)) return;   // the bf16 kernel does the work
+  }
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int li = lane & 15, g = lane >> 4;
@@ -324,6 +329,191 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
   }
 }
 
+// ------------------------------------------------------- exact bf16 arg-K-min
+// Guard: the largest |v| and whether every v is an integer, over x and y.
+__global__ void exact_init_kernel(ExactGuard* g) {
+  if (threadIdx.x == 0) {
+    g->maxabs = 0u;
+    g->nonint = 0u;
+  }
+}
+
+__global__ __launch_bounds__(256) void exact_check_kernel(const float* __restrict__ x, int64_t nx,
+                                                          const float* __restrict__ y, int64_t ny,
+                                                          ExactGuard* g) {
+  unsigned int m = 0u, bad = 0u;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < nx + ny; t += stride) {
+    const float v = t < nx ? x[t] : y[t - nx];
+    m = max(m, __float_as_uint(fabsf(v)));   // NaN and inf exceed every limit
+    bad |= (v != rintf(v)) ? 1u : 0u;        // true for NaN
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    m = max(m, (unsigned int)__shfl_xor((int)m, o));
+    bad |= (unsigned int)__shfl_xor((int)bad, o);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    if (m != 0u) atomicMax(&g->maxabs, m);
+    if (bad != 0u) atomicOr(&g->nonint, 1u);
+  }
+}
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int bf16_tile_cols(int DP) { return DP <= 128 ? 64 : 32; }
+
+// Arg-K-min on the bf16 matrix cores, for data the guard has shown to be
+// exact there: T[j][i] = ny_j + sum_d (-2 y_jd) x_id with one
+// v_mfma_f32_16x16x32_bf16 per 32 coordinates of a 16 x 16 block.  The
+// ranking, ties, lists and partial layout are those of the fp32 kernel.
+// bf16 16x16x32 operand layout (lane l = 16 g + li): A (16 x 32): lane l
+// supplies A[li][8 g .. 8 g + 7]; B (32 x 16): lane l supplies
+// B[8 g .. 8 g + 7][li]; D as for the fp32 product, lane l holds
+// D[4 g + r][li].  With A = Y rows and B = X rows, lane l ranks column
+// j = 4 g + r for row i = li.  Coordinates d = 32 ch + 8 g + t.
+template <int NCH, int RB, int KP>
+__global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
+  if (!exact_ok(a.exact, a.D)) return;   // the fp32 kernel does the work
+  constexpr int DP = 32 * NCH;
+  constexpr int TJ = bf16_tile_cols(DP);
+  constexpr int RU = DP / 8 + 1;           // uint4 per LDS row: DP bf16 and 8 of padding
+  constexpr int TU = TJ * (DP / 8);        // uint4 of y per tile
+  constexpr int YL = (TU + 255) / 256;     // per thread
+
+  __shared__ uint4 ys[2][TJ * RU];
+  __shared__ float4 ns[2][TJ / 4];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int li = lane & 15, g = lane >> 4;
+  const int c = blockIdx.x % a.C;
+  const int64_t rbk = blockIdx.x / a.C;
+  const int64_t j0 = (int64_t)c * a.jpb;
+  const int64_t j1 = min(a.N16, j0 + a.jpb);
+  const int64_t i0 = rbk * (64 * RB) + wave * (16 * RB);
+
+  bf16x8 xb[RB][NCH];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int64_t row = i0 + 16 * rb + li;
+    const bool ok = row < a.M;
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int d = 32 * ch + 8 * g + t;
+        xb[rb][ch][t] = (__bf16)((ok && d < a.D) ? a.x[row * a.D + d] : 0.0f);
+      }
+  }
+
+  float dk[RB][KP];
+  int jk[RB][KP];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      dk[rb][p] = __builtin_inff();
+      jk[rb][p] = INT_MAX;
+    }
+
+  uint4 ystage[YL];
+  float4 nstage;
+  auto fetch = [&](int64_t jt) {
+    const int ncol = (int)min((int64_t)TJ, j1 - jt);
+    const uint4* ysrc = reinterpret_cast<const uint4*>(a.ybf + jt * DP);
+#pragma unroll
+    for (int k = 0; k < YL; ++k) {
+      const int f = tid + k * 256;
+      ystage[k] = (f < TU && f < ncol * (DP / 8)) ? ysrc[f] : uint4{0u, 0u, 0u, 0u};
+    }
+    if (tid < TJ / 4)
+      nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
+                                : float4{0.f, 0.f, 0.f, 0.f};
+  };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < YL; ++k) {
+      const int f = tid + k * 256;
+      if (f < TU) ys[buf][(f / (DP / 8)) * RU + f % (DP / 8)] = ystage[k];
+    }
+    if (tid < TJ / 4) ns[buf][tid] = nstage;
+  };
+
+  const int64_t ntiles = (j1 - j0 + TJ - 1) / TJ;
+  if (ntiles > 0) {
+    fetch(j0);
+    put(0);
+  }
+  __syncthreads();
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int64_t jt = j0 + t * TJ;
+    const int buf = (int)(t & 1);
+    const int nblk = (int)(min((int64_t)TJ, j1 - jt) / 16);
+    if (t + 1 < ntiles) fetch(jt + TJ);
+    for (int blk = 0; blk < nblk; ++blk) {
+      bf16x8 ya[NCH];
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch)
+        ya[ch] = __builtin_bit_cast(bf16x8, ys[buf][(blk * 16 + li) * RU + 4 * ch + g]);
+      const float4 nyv = ns[buf][blk * 4 + g];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        f4 acc = f4{nyv.x, nyv.y, nyv.z, nyv.w};
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch)
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ya[ch], xb[rb][ch], acc, 0, 0, 0);
+        const float kth = dk[rb][KP - 1];
+        const bool any = acc[0] < kth || acc[1] < kth || acc[2] < kth || acc[3] < kth;
+        if (__builtin_expect(any, 0)) {
+          const int jb = (int)(jt + blk * 16 + 4 * g);
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (acc[r] < dk[rb][KP - 1]) list_insert<KP>(dk[rb], jk[rb], acc[r], jb + r);
+        }
+      }
+    }
+    // buffer (t+1)&1 was last read in iteration t-1, which ended with a barrier
+    if (t + 1 < ntiles) put((int)((t + 1) & 1));
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    float part = 0.0f;   // the row norm (exact: integers below 2^24)
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float v = (float)xb[rb][ch][t];
+        part = __builtin_fmaf(v, v, part);
+      }
+    part += __shfl_xor(part, 16);
+    part += __shfl_xor(part, 32);
+    const int64_t row = i0 + 16 * rb + li;
+    if (row >= a.M) continue;
+    float* q = a.part + (((int64_t)c * 4 + g) * a.M + row) * (2 * KP);
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      q[2 * p] = dk[rb][p] + part;
+      q[2 * p + 1] = __int_as_float(jk[rb][p]);
+    }
+  }
+}
+
+constexpr int bf16_rows_blocks(int KP) { return KP >= 64 ? 1 : 2; }
+
+template <int NCH>
+hipError_t launch_knn_bf16_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
+  switch (a.KP) {
+    case 1: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(1), 1>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(4), 4>), grid, dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(16), 16>), grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(64), 64>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <int Q>
 constexpr int rows_blocks() { return Q >= 64 ? 1 : 2; }
 
@@ -380,6 +570,30 @@ hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s) {
   const int64_t nb = std::max<int64_t>(1, std::min<int64_t>((a.N16 + 3) / 4, 4096));
   hipLaunchKernelGGL(mfma_norm_kernel, dim3((unsigned)nb), dim3(256), 0, s, a);
   return hipGetLastError();
+}
+
+hipError_t launch_exact_check(const float* x, int64_t M, const float* y, int64_t N, int D,
+                              ExactGuard* g, hipStream_t s) {
+  hipLaunchKernelGGL(exact_init_kernel, dim3(1), dim3(64), 0, s, g);
+  if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+  const int64_t total = (M + N) * (int64_t)D;
+  if (total == 0) return hipSuccess;
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((total + 255) / 256, 4096));
+  hipLaunchKernelGGL(exact_check_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, M * D, y,
+                     N * D, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_knn_bf16(const MfmaArgs& a, hipStream_t s) {
+  const int rows = 64 * bf16_rows_blocks(a.KP);
+  const dim3 grid((unsigned)((a.M + rows - 1) / rows * a.C));
+  switch (a.DP) {
+    case 32: return launch_knn_bf16_n<1>(a, grid, s);
+    case 64: return launch_knn_bf16_n<2>(a, grid, s);
+    case 128: return launch_knn_bf16_n<4>(a, grid, s);
+    case 256: return launch_knn_bf16_n<8>(a, grid, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s) {

@@ -25,6 +25,10 @@ struct kred_ctx {
   std::vector<hipEvent_t> ev;
   size_t ev_used = 0;
   const char* last_kernel = "none";
+  // exact bf16 arg-K-min: the device-side guard (its own allocation, so it
+  // outlives scratch growth), and whether the last profiled call used it
+  ExactGuard* exact_guard = nullptr;
+  int last_exact_D = 0;
 };
 
 namespace {
@@ -169,6 +173,15 @@ int fast_epi(kred_formula f, kred_reduction r, int64_t M, int64_t N, int32_t D, 
   return -1;
 }
 
+// Large-D arg-K-min: the exact bf16 kernel is launched beside the fp32 one
+// (the device-side guard picks one) for problems large enough that the guard's
+// pass over x and y pays off, or always with KRED_FLAG_FAST; never with
+// KRED_FLAG_DIRECT.
+bool exact_eligible(uint32_t flags, int64_t M, int64_t N) {
+  if (flags & KRED_FLAG_DIRECT) return false;
+  return (flags & KRED_FLAG_FAST) || (double)M * (double)N >= kFastMinPairs;
+}
+
 struct FastScratch {
   int64_t guard_bytes, apk_bytes, ex_bytes;
 };
@@ -302,9 +315,18 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
                      const float* b, void* out, hipStream_t s, int kvalues) {
   MPlan pl;
   if (!make_mplan(f, r, p, M, N, D, E, ctx->num_cus, &pl)) return KRED_ERR_UNSUPPORTED;
-  const kred_status gs =
-      grow_scratch(ctx, (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes));
+  const bool knn = (r == KRED_R_ARGKMIN);
+  // arg-K-min: the exact bf16 kernel is a candidate (the device decides)
+  const bool exact = knn && exact_eligible(p->flags, M, N);
+  const int64_t ybf_bytes = exact ? align_up(pl.N16 * pl.DP * (int64_t)sizeof(uint16_t)) : 0;
+  const kred_status gs = grow_scratch(
+      ctx, (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes + ybf_bytes));
   if (gs != KRED_OK) return gs;
+  if (exact && ctx->exact_guard == nullptr &&
+      hipMalloc(reinterpret_cast<void**>(&ctx->exact_guard), sizeof(ExactGuard)) != hipSuccess) {
+    ctx->exact_guard = nullptr;
+    return KRED_ERR_NOMEM;
+  }
   char* base = static_cast<char*>(ctx->scratch);
   float* yop = reinterpret_cast<float*>(base);
   float* ny = reinterpret_cast<float*>(base + pl.yop_bytes);
@@ -312,7 +334,11 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   float* part = pl.part_bytes
                     ? reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes + pl.b_bytes)
                     : nullptr;
-  const bool knn = (r == KRED_R_ARGKMIN);
+  uint16_t* ybf = exact ? reinterpret_cast<uint16_t*>(base + pl.yop_bytes + pl.ny_bytes +
+                                                        pl.b_bytes + pl.part_bytes)
+                        : nullptr;
+  ExactGuard* eg = exact ? ctx->exact_guard : nullptr;
+  if (exact && launch_exact_check(x, M, y, N, D, eg, s) != hipSuccess) return KRED_ERR_HIP;
 
   MfmaPackArgs pa{};
   pa.y = y;
@@ -332,6 +358,8 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   pa.yop = yop;
   pa.ny = ny;
   pa.bpk = bpk;
+  pa.exact = eg;
+  pa.ybf = ybf;
   if (launch_mfma_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
 
   MfmaArgs ma{};
@@ -354,6 +382,8 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   ma.part = part;
   ma.KP = pl.KP;
   ma.K = pl.K;
+  ma.exact = eg;
+  ma.ybf = ybf;
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (prof) {
@@ -361,10 +391,13 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     e1 = next_event(ctx);
     if (!e0 || !e1 || hipEventRecord(e0, s) != hipSuccess) return KRED_ERR_HIP;
   }
+  // with the exact kernel a candidate, both launch and exactly one does the work
   if (launch_mfma(ma, s) != hipSuccess) return KRED_ERR_HIP;
+  if (exact && launch_knn_bf16(ma, s) != hipSuccess) return KRED_ERR_HIP;
   if (prof) {
     if (hipEventRecord(e1, s) != hipSuccess) return KRED_ERR_HIP;
     ctx->last_kernel = "mfma_kernel";
+    ctx->last_exact_D = exact ? D : 0;   // resolved from the guard at collect time
   }
   if (knn || pl.C > 1) {
     CombineArgs ca{};
@@ -621,6 +654,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     if (launch_direct(da, s) != hipSuccess) return KRED_ERR_HIP;
     if (prof) {
       if (hipEventRecord(e_stop, s) != hipSuccess) return KRED_ERR_HIP;
+      ctx->last_exact_D = 0;
       ctx->last_kernel = (epi >= 0)                  ? "fast_kernel"
                          : ext                       ? "extreme_kernel"
                          : (r == KRED_R_ARGKMIN)     ? "knn_kernel"
@@ -727,6 +761,7 @@ kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, i
     if (launch_direct(da, s) != hipSuccess) return KRED_ERR_HIP;
     if (prof) {
       if (hipEventRecord(e_stop, s) != hipSuccess) return KRED_ERR_HIP;
+      ctx->last_exact_D = 0;
       ctx->last_kernel = "vjp_kernel";
     }
     if (pl.C > 1) {
@@ -877,6 +912,7 @@ kred_status kred_destroy(kred_ctx* ctx) {
     if (hipDeviceSynchronize() != hipSuccess) st = KRED_ERR_HIP;
     if (ctx->scratch) (void)hipFree(ctx->scratch);
     if (ctx->aux) (void)hipFree(ctx->aux);
+    if (ctx->exact_guard) (void)hipFree(ctx->exact_guard);
     for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
   }
   delete ctx;
@@ -999,6 +1035,16 @@ kred_status kred_profile_collect(kred_ctx* ctx, int32_t* count, double* total_ms
   }
   *count = (int32_t)(ctx->ev_used / 2);
   *total_ms = sum;
+  if (ctx->last_exact_D > 0 && ctx->exact_guard != nullptr) {
+    // which arg-K-min kernel the device chose in the last profiled call
+    ExactGuard h{};
+    if (hipMemcpy(&h, ctx->exact_guard, sizeof(h), hipMemcpyDeviceToHost) != hipSuccess)
+      return KRED_ERR_HIP;
+    const float m = __builtin_bit_cast(float, h.maxabs);
+    const bool ok = h.nonint == 0u && m <= kExactMaxAbs &&
+                    (float)ctx->last_exact_D * m * m <= kExactMaxSum;
+    ctx->last_kernel = ok ? "knn_bf16_kernel" : "mfma_kernel";
+  }
   if (kernel) *kernel = ctx->last_kernel;
   ctx->ev_used = 0;
   return KRED_OK;

@@ -151,6 +151,26 @@ hipError_t launch_scale_rows(const float* src, int64_t M, int D, const float* e,
 // (zero for d >= D), ny[j] = nrm_sign * |y_j * coord_scale|^2 (pad_norm for
 // the padding columns N <= j < N16), and the signal tiles bpk (16 * EB
 // values of b per column, laid out as the B operand of the P . B product).
+// Exactness guard of the bf16 arg-K-min kernel.  When every coordinate of x
+// and y is an integer with |v| <= kExactMaxAbs and D max|v|^2 <= kExactMaxSum,
+// every operand (v and -2 v) is exact in bf16 and every product, partial sum
+// and norm is an integer below 2^24, exact in fp32: the bf16 matrix cores then
+// give the same squared distances, and so the same ranking and ties, as exact
+// arithmetic.  The prologue fills the guard on the device; the fp32 and bf16
+// kernels are both launched and each returns at once unless it is selected.
+struct ExactGuard {
+  unsigned int maxabs;   // bit pattern of max |v| (non-negative floats order as unsigned ints)
+  unsigned int nonint;   // non-zero once some coordinate is not an integer (NaN, inf included)
+};
+constexpr float kExactMaxAbs = 256.0f;
+constexpr float kExactMaxSum = 4194304.0f;   // 2^22
+
+__device__ __forceinline__ bool exact_ok(const ExactGuard* g, int D) {
+  if (g == nullptr || g->nonint != 0u) return false;
+  const float m = __uint_as_float(g->maxabs);
+  return m <= kExactMaxAbs && (float)D * m * m <= kExactMaxSum;
+}
+
 struct MfmaPackArgs {
   const float* y;
   const float* b;
@@ -160,6 +180,8 @@ struct MfmaPackArgs {
   float* yop;
   float* ny;
   float* bpk;     // null for arg-K-min
+  const ExactGuard* exact;   // arg-K-min with the exact path enabled, else null
+  unsigned short* ybf;       // bf16 copy of yop (N16 x DP), written instead of yop when exact
 };
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
 
@@ -177,8 +199,16 @@ struct MfmaArgs {
   void* out;      // final output (sums with C == 1)
   float* part;    // sums: C x M x 16 EB; arg-K-min: 4 C x M x 2 KP
   int KP, K;
+  const ExactGuard* exact;     // arg-K-min: exact-path guard, or null (fp32 kernel only)
+  const unsigned short* ybf;   // arg-K-min: bf16 column operand when exact
 };
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
+// Exact-path prologue: reset the guard, then fold every coordinate of x and y into it.
+hipError_t launch_exact_check(const float* x, int64_t M, const float* y, int64_t N, int D,
+                              ExactGuard* g, hipStream_t s);
+// The bf16 arg-K-min kernel (runs only when the guard allows it); same partial layout as the
+// fp32 kernel for the same C and jpb.
+hipError_t launch_knn_bf16(const MfmaArgs& a, hipStream_t s);
 int mfma_pad_d(int D);               // DP for D > 16 (0 if D > 256)
 int mfma_tile_cols(int DP);          // columns per LDS tile
 int mfma_rows_per_block(int DP, int KP);
