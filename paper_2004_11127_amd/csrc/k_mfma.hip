@@ -416,6 +416,15 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
       jk[rb][p] = INT_MAX;
     }
 
+  // Filter shared by the 4 lanes of a row (each lists its own quarter of the
+  // columns): the smallest of their K-th values.  The lane holding it has K
+  // candidates at or below it, so a column above it cannot be among the row's
+  // K nearest in this column block; ties pass (<=) for the lowest-index rule.
+  // It is refreshed once per tile; a stale value is only looser.
+  float thr[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) thr[rb] = __builtin_inff();
+
   uint4 ystage[YL];
   float4 nstage;
   auto fetch = [&](int64_t jt) {
@@ -450,6 +459,12 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
     const int buf = (int)(t & 1);
     const int nblk = (int)(min((int64_t)TJ, j1 - jt) / 16);
     if (t + 1 < ntiles) fetch(jt + TJ);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      float v = dk[rb][KP - 1];
+      v = fminf(v, __shfl_xor(v, 16));
+      thr[rb] = fminf(v, __shfl_xor(v, 32));
+    }
     for (int blk = 0; blk < nblk; ++blk) {
       bf16x8 ya[NCH];
 #pragma unroll
@@ -462,8 +477,8 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
 #pragma unroll
         for (int ch = 0; ch < NCH; ++ch)
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ya[ch], xb[rb][ch], acc, 0, 0, 0);
-        const float kth = dk[rb][KP - 1];
-        const bool any = acc[0] < kth || acc[1] < kth || acc[2] < kth || acc[3] < kth;
+        const float th = thr[rb];
+        const bool any = acc[0] <= th || acc[1] <= th || acc[2] <= th || acc[3] <= th;
         if (__builtin_expect(any, 0)) {
           const int jb = (int)(jt + blk * 16 + 4 * g);
 #pragma unroll
@@ -507,6 +522,8 @@ hipError_t launch_knn_bf16_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   switch (a.KP) {
     case 1: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(1), 1>), grid, dim3(256), 0, s, a); break;
     case 4: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(4), 4>), grid, dim3(256), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(8), 8>), grid, dim3(256), 0, s, a); break;
+    case 12: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(12), 12>), grid, dim3(256), 0, s, a); break;
     case 16: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(16), 16>), grid, dim3(256), 0, s, a); break;
     case 64: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(64), 64>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
@@ -540,6 +557,8 @@ hipError_t launch_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
       switch (a.KP) {
         case 1: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 1>), grid, dim3(256), 0, s, a); break;
         case 4: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 4>), grid, dim3(256), 0, s, a); break;
+        case 8: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 8>), grid, dim3(256), 0, s, a); break;
+        case 12: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 12>), grid, dim3(256), 0, s, a); break;
         case 16: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 16>), grid, dim3(256), 0, s, a); break;
         case 64: hipLaunchKernelGGL((mfma_kernel<Q, 1, 3, 1, 64>), grid, dim3(256), 0, s, a); break;
         default: return hipErrorInvalidValue;
@@ -555,6 +574,10 @@ hipError_t launch_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
 int mfma_pad_d(int D) { return D <= 32 ? 32 : (D <= 64 ? 64 : (D <= 128 ? 128 : (D <= 256 ? 256 : 0))); }
 
 int mfma_tile_cols(int DP) { return tile_cols(DP); }
+
+int mfma_knn_pad_k(int K) {
+  return K <= 1 ? 1 : (K <= 4 ? 4 : (K <= 8 ? 8 : (K <= 12 ? 12 : (K <= 16 ? 16 : 64))));
+}
 
 int mfma_rows_per_block(int DP, int KP) {
   const int Q = DP / 4;

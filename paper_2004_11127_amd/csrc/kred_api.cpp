@@ -217,7 +217,7 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   if (r == KRED_R_ARGKMIN) {
     q.epi = 3;
     q.K = p->K;
-    q.KP = knn_pad_k(p->K);
+    q.KP = mfma_knn_pad_k(p->K);
     q.EB = 1;
     q.xscale = 1.0f;
     q.yop_scale = -2.0f;

@@ -211,6 +211,7 @@ hipError_t launch_exact_check(const float* x, int64_t M, const float* y, int64_t
 hipError_t launch_knn_bf16(const MfmaArgs& a, hipStream_t s);
 int mfma_pad_d(int D);               // DP for D > 16 (0 if D > 256)
 int mfma_tile_cols(int DP);          // columns per LDS tile
+int mfma_knn_pad_k(int K);           // list length of the matrix-core arg-K-min kernels
 int mfma_rows_per_block(int DP, int KP);
 
 struct FastPackArgs {
