@@ -165,6 +165,7 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
       case 1: hipLaunchKernelGGL(combine_knn_kernel<1>, g, dim3(256), 0, s, a); break;
       case 4: hipLaunchKernelGGL(combine_knn_kernel<4>, g, dim3(256), 0, s, a); break;
       case 8: hipLaunchKernelGGL(combine_knn_kernel<8>, g, dim3(256), 0, s, a); break;
+      case 10: hipLaunchKernelGGL(combine_knn_kernel<10>, g, dim3(256), 0, s, a); break;
       case 12: hipLaunchKernelGGL(combine_knn_kernel<12>, g, dim3(256), 0, s, a); break;
       case 16: hipLaunchKernelGGL(combine_knn_kernel<16>, g, dim3(256), 0, s, a); break;
       case 64: hipLaunchKernelGGL(combine_knn_kernel<64>, g, dim3(256), 0, s, a); break;

@@ -417,10 +417,12 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
     }
 
   // Filter shared by the 4 lanes of a row (each lists its own quarter of the
-  // columns): the smallest of their K-th values.  The lane holding it has K
-  // candidates at or below it, so a column above it cannot be among the row's
-  // K nearest in this column block; ties pass (<=) for the lowest-index rule.
-  // It is refreshed once per tile; a stale value is only looser.
+  // columns): any value with at least KP of the row's candidates at or below
+  // it bounds the row's K-th nearest in this column block, so a column above
+  // it cannot be among them; ties pass (<=) for the lowest-index rule.  Two
+  // such bounds: the smallest of the 4 lanes' KP-th values, and the largest
+  // of their ceil(KP/4)-th values (4 ceil(KP/4) >= KP candidates).  It is
+  // refreshed once per tile; a stale value is only looser.
   float thr[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) thr[rb] = __builtin_inff();
@@ -463,7 +465,11 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
     for (int rb = 0; rb < RB; ++rb) {
       float v = dk[rb][KP - 1];
       v = fminf(v, __shfl_xor(v, 16));
-      thr[rb] = fminf(v, __shfl_xor(v, 32));
+      v = fminf(v, __shfl_xor(v, 32));
+      float u = dk[rb][(KP + 3) / 4 - 1];
+      u = fmaxf(u, __shfl_xor(u, 16));
+      u = fmaxf(u, __shfl_xor(u, 32));
+      thr[rb] = fminf(v, u);
     }
     for (int blk = 0; blk < nblk; ++blk) {
       bf16x8 ya[NCH];
@@ -471,19 +477,30 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
       for (int ch = 0; ch < NCH; ++ch)
         ya[ch] = __builtin_bit_cast(bf16x8, ys[buf][(blk * 16 + li) * RU + 4 * ch + g]);
       const float4 nyv = ns[buf][blk * 4 + g];
+      // all row blocks' products first (independent chains overlap), then
+      // every filter test, and only then the branches: no branch sits between
+      // an MFMA and the first read of its result
+      f4 acc[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        f4 acc = f4{nyv.x, nyv.y, nyv.z, nyv.w};
+        acc[rb] = f4{nyv.x, nyv.y, nyv.z, nyv.w};
 #pragma unroll
         for (int ch = 0; ch < NCH; ++ch)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ya[ch], xb[rb][ch], acc, 0, 0, 0);
+          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ya[ch], xb[rb][ch], acc[rb], 0, 0, 0);
+      }
+      bool any[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
         const float th = thr[rb];
-        const bool any = acc[0] <= th || acc[1] <= th || acc[2] <= th || acc[3] <= th;
-        if (__builtin_expect(any, 0)) {
+        any[rb] = fminf(fminf(acc[rb][0], acc[rb][1]), fminf(acc[rb][2], acc[rb][3])) <= th;
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        if (__builtin_expect(any[rb], 0)) {
           const int jb = (int)(jt + blk * 16 + 4 * g);
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            if (acc[r] < dk[rb][KP - 1]) list_insert<KP>(dk[rb], jk[rb], acc[r], jb + r);
+            if (acc[rb][r] < dk[rb][KP - 1]) list_insert<KP>(dk[rb], jk[rb], acc[rb][r], jb + r);
         }
       }
     }
@@ -523,6 +540,7 @@ hipError_t launch_knn_bf16_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
     case 1: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(1), 1>), grid, dim3(256), 0, s, a); break;
     case 4: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(4), 4>), grid, dim3(256), 0, s, a); break;
     case 8: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(8), 8>), grid, dim3(256), 0, s, a); break;
+    case 10: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(10), 10>), grid, dim3(256), 0, s, a); break;
     case 12: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(12), 12>), grid, dim3(256), 0, s, a); break;
     case 16: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(16), 16>), grid, dim3(256), 0, s, a); break;
     case 64: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(64), 64>), grid, dim3(256), 0, s, a); break;
@@ -558,6 +576,7 @@ hipError_t launch_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
         case 1: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 1>), grid, dim3(256), 0, s, a); break;
         case 4: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 4>), grid, dim3(256), 0, s, a); break;
         case 8: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 8>), grid, dim3(256), 0, s, a); break;
+        case 10: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 10>), grid, dim3(256), 0, s, a); break;
         case 12: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 12>), grid, dim3(256), 0, s, a); break;
         case 16: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 16>), grid, dim3(256), 0, s, a); break;
         case 64: hipLaunchKernelGGL((mfma_kernel<Q, 1, 3, 1, 64>), grid, dim3(256), 0, s, a); break;
@@ -576,7 +595,7 @@ int mfma_pad_d(int D) { return D <= 32 ? 32 : (D <= 64 ? 64 : (D <= 128 ? 128 : 
 int mfma_tile_cols(int DP) { return tile_cols(DP); }
 
 int mfma_knn_pad_k(int K) {
-  return K <= 1 ? 1 : (K <= 4 ? 4 : (K <= 8 ? 8 : (K <= 12 ? 12 : (K <= 16 ? 16 : 64))));
+  return K <= 1 ? 1 : K <= 4 ? 4 : K <= 8 ? 8 : K <= 10 ? 10 : K <= 12 ? 12 : K <= 16 ? 16 : 64;
 }
 
 int mfma_rows_per_block(int DP, int KP) {

@@ -51,6 +51,9 @@ CASES = [
     (64, 64, 64, 64, 0, 0, 1),
     (200, 3000, 256, 10, 0, -2, 2),
     (257, 999, 33, 16, 7, -256, 256),   # |v| = 256 allowed while 33 * 256^2 <= 2^22
+    (300, 1200, 64, 12, 0, -8, 8),
+    (200, 900, 96, 7, 3, -8, 8),
+    (4000, 3000, 64, 9, 0, -4, 4),      # many row blocks, dense ties
 ]
 
 
@@ -113,13 +116,14 @@ def test_guard_falls_back_to_fp32(ctx, why, make):
         np.testing.assert_array_equal(out, ref)
 
 
-def test_direct_flag_keeps_fp32_kernel(ctx):
+@pytest.mark.parametrize("K", [7, 10, 12])
+def test_direct_flag_keeps_fp32_kernel(ctx, K):
     from paper_2004_11127_amd import kred
-    rng = np.random.default_rng(3)
+    rng = np.random.default_rng(3 + K)
     x = _ints(rng, 200, 64, -8, 8); y = _ints(rng, 1000, 64, -8, 8)
-    out, name = _run(ctx, "argkmin", x, y, K=10, flags=kred.FLAG_DIRECT)
+    out, name = _run(ctx, "argkmin", x, y, K=K, flags=kred.FLAG_DIRECT)
     assert name == "mfma_kernel"
-    np.testing.assert_array_equal(out, oracle.argkmin(x, y, 10)[0])
+    np.testing.assert_array_equal(out, oracle.argkmin(x, y, K)[0])
 
 
 def test_exact_path_matches_fp32_path_and_repeats(ctx):
