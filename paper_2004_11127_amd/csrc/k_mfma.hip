@@ -43,6 +43,16 @@ __device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// v = h + m + l exactly, each part a bf16 (round to nearest): h keeps the top
+// 8 significant bits, the remainder v - h is exact in fp32 with at most 16,
+// m keeps 8 of those and l the last 8.
+__device__ __forceinline__ void split3(float v, __bf16& h, __bf16& m, __bf16& l) {
+  h = (__bf16)v;
+  const float r = v - (float)h;
+  m = (__bf16)r;
+  l = (__bf16)(r - (float)m);
+}
+
 // ------------------------------------------------------------------ prologue
 // Coalesced: consecutive threads handle consecutive d of one column.
 __global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
@@ -53,8 +63,18 @@ __global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
     const int64_t j = t / a.DP;
     const int d = (int)(t - j * a.DP);
     const float v = (j < a.N && d < a.D) ? a.y[j * a.D + d] : 0.0f;
-    if (ex) a.ybf[t] = __builtin_bit_cast(unsigned short, (__bf16)(v * a.yop_scale));
-    else a.yop[t] = v * a.yop_scale;
+    if (ex) {
+      a.ybf[t] = __builtin_bit_cast(unsigned short, (__bf16)(v * a.yop_scale));
+    } else if (a.ysp != nullptr) {
+      __bf16 h, m, l;
+      split3(v * a.yop_scale, h, m, l);
+      unsigned short* q = a.ysp + j * 3 * a.DP + d;   // planes h, m, l of column j
+      q[0] = __builtin_bit_cast(unsigned short, h);
+      q[a.DP] = __builtin_bit_cast(unsigned short, m);
+      q[2 * a.DP] = __builtin_bit_cast(unsigned short, l);
+    } else {
+      a.yop[t] = v * a.yop_scale;
+    }
   }
   // signal tiles: b[j][e0 + e] stored at (j/16)*16W + ((j%16)/4)*4W + e*4 + j%4, W = 16*EB
   if (a.bpk != nullptr) {
@@ -549,6 +569,221 @@ hipError_t launch_knn_bf16_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------ sums, split bf16 products
+// The same reduction as mfma_kernel's sums, with the inner product on the
+// bf16 matrix cores: every coordinate is split exactly into three bf16 parts
+// (v = h + m + l, 24 significant bits), and per 32 coordinates six
+// v_mfma_f32_16x16x32_bf16 accumulate the partial products hh, hm, mh, hl,
+// lh and mm, each exact in fp32.  The dropped ml, lm and ll terms are below
+// 2^-24 |x||y|, so the result carries fp32 accuracy at six bf16 products per
+// coordinate instead of one fp32 product (a sixth of the matrix-core time per
+// flop for the fp32 form, at 16x the rate).  The P . B product and the
+// epilogue are those of the fp32 kernel.  Column operand: three bf16 planes
+// per column (prologue); row operand: the planes of x in registers.
+constexpr int split_tile_cols(int DP) { return DP <= 64 ? 64 : (DP <= 128 ? 32 : 16); }
+
+template <int NCH, int RB, int EPI, int EB>
+__global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
+  constexpr int DP = 32 * NCH;
+  constexpr int TJ = split_tile_cols(DP);
+  constexpr int PU = DP / 8;                  // uint4 per plane of a column
+  constexpr int RU = 3 * PU + 1;              // uint4 per LDS column row (16 B of padding)
+  constexpr int TU = TJ * 3 * PU;             // uint4 of y planes per tile
+  constexpr int YL = (TU + 255) / 256;
+  constexpr int W = 16 * EB;
+  constexpr int BF4 = TJ * W / 4;
+  constexpr int BL = (BF4 + 255) / 256;
+
+  __shared__ uint4 ys[2][TJ * RU];
+  __shared__ float4 ns[2][TJ / 4];
+  __shared__ float4 bs[2][TJ * W / 4];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int li = lane & 15, g = lane >> 4;
+  const int c = blockIdx.x % a.C;
+  const int64_t rbk = blockIdx.x / a.C;
+  const int64_t j0 = (int64_t)c * a.jpb;
+  const int64_t j1 = min(a.N16, j0 + a.jpb);
+  const int64_t i0 = rbk * (64 * RB) + wave * (16 * RB);
+
+  // rows: lane supplies B[k = 8 g .. 8 g + 7][n = li] of chunk ch, i.e. the
+  // planes of x[i = li][32 ch + 8 g + t]
+  bf16x8 xh[RB][NCH], xm[RB][NCH], xl[RB][NCH];
+  float nx[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int64_t row = i0 + 16 * rb + li;
+    const bool ok = row < a.M;
+    float part = 0.0f;
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int d = 32 * ch + 8 * g + t;
+        const float v = (ok && d < a.D) ? a.x[row * a.D + d] * a.xscale : 0.0f;
+        __bf16 h, m, l;
+        split3(v, h, m, l);
+        xh[rb][ch][t] = h;
+        xm[rb][ch][t] = m;
+        xl[rb][ch][t] = l;
+        part = __builtin_fmaf(v, v, part);
+      }
+    part += __shfl_xor(part, 16);
+    part += __shfl_xor(part, 32);
+    nx[rb] = -part;
+  }
+
+  f4 oacc[RB][EB], tot[RB][EB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int eb = 0; eb < EB; ++eb) oacc[rb][eb] = tot[rb][eb] = f4{0.f, 0.f, 0.f, 0.f};
+
+  uint4 ystage[YL];
+  float4 bstage[BL];
+  float4 nstage;
+  auto fetch = [&](int64_t jt) {
+    const int ncol = (int)min((int64_t)TJ, j1 - jt);
+    const uint4* ysrc = reinterpret_cast<const uint4*>(a.ysp + jt * 3 * DP);
+#pragma unroll
+    for (int k = 0; k < YL; ++k) {
+      const int f = tid + k * 256;
+      ystage[k] = (f < TU && f < ncol * 3 * PU) ? ysrc[f] : uint4{0u, 0u, 0u, 0u};
+    }
+    if (tid < TJ / 4)
+      nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
+                                : float4{0.f, 0.f, 0.f, 0.f};
+    const float4* bsrc = reinterpret_cast<const float4*>(a.bpk + jt * W);
+#pragma unroll
+    for (int k = 0; k < BL; ++k) {
+      const int f = tid + k * 256;
+      bstage[k] = (f < BF4 && f < ncol * W / 4) ? bsrc[f] : float4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < YL; ++k) {
+      const int f = tid + k * 256;
+      if (f < TU) ys[buf][(f / (3 * PU)) * RU + f % (3 * PU)] = ystage[k];
+    }
+    if (tid < TJ / 4) ns[buf][tid] = nstage;
+#pragma unroll
+    for (int k = 0; k < BL; ++k) {
+      const int f = tid + k * 256;
+      if (f < BF4) bs[buf][f] = bstage[k];
+    }
+  };
+
+  const int64_t ntiles = (j1 - j0 + TJ - 1) / TJ;
+  if (ntiles > 0) {
+    fetch(j0);
+    put(0);
+  }
+  __syncthreads();
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int64_t jt = j0 + t * TJ;
+    const int buf = (int)(t & 1);
+    const int nblk = (int)(min((int64_t)TJ, j1 - jt) / 16);
+    if (t + 1 < ntiles) fetch(jt + TJ);
+    for (int blk = 0; blk < nblk; ++blk) {
+      const float4 nyv = ns[buf][blk * 4 + g];
+      f4 acc[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        acc[rb] = f4{nx[rb] + nyv.x, nx[rb] + nyv.y, nx[rb] + nyv.z, nx[rb] + nyv.w};
+      const uint4* col = &ys[buf][(blk * 16 + li) * RU + g];
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        const bf16x8 yh = __builtin_bit_cast(bf16x8, col[4 * ch]);
+        const bf16x8 ym = __builtin_bit_cast(bf16x8, col[PU + 4 * ch]);
+        const bf16x8 yl = __builtin_bit_cast(bf16x8, col[2 * PU + 4 * ch]);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          // smallest partial products first
+          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xm[rb][ch], acc[rb], 0, 0, 0);
+          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yl, xh[rb][ch], acc[rb], 0, 0, 0);
+          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xl[rb][ch], acc[rb], 0, 0, 0);
+          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xh[rb][ch], acc[rb], 0, 0, 0);
+          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xm[rb][ch], acc[rb], 0, 0, 0);
+          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xh[rb][ch], acc[rb], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        f4 p;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if constexpr (EPI == 0) p[r] = __builtin_amdgcn_exp2f(acc[rb][r]);
+          else if constexpr (EPI == 1) p[r] = __builtin_amdgcn_exp2f(-__builtin_amdgcn_sqrtf(fmaxf(-acc[rb][r], 0.0f)));
+          else p[r] = fmaxf(-acc[rb][r], 0.0f);
+        }
+#pragma unroll
+        for (int eb = 0; eb < EB; ++eb) {
+          // lane needs b[j = blk*16 + 4g + r][e = 16 eb + li] for r = 0..3
+          const float* bl = reinterpret_cast<const float*>(&bs[buf][0]) +
+                            blk * 16 * W + g * 4 * W + (16 * eb + li) * 4;
+          const float4 bv = *reinterpret_cast<const float4*>(bl);
+          oacc[rb][eb] = mfma4(p[0], bv.x, oacc[rb][eb]);
+          oacc[rb][eb] = mfma4(p[1], bv.y, oacc[rb][eb]);
+          oacc[rb][eb] = mfma4(p[2], bv.z, oacc[rb][eb]);
+          oacc[rb][eb] = mfma4(p[3], bv.w, oacc[rb][eb]);
+        }
+      }
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int eb = 0; eb < EB; ++eb) {
+        tot[rb][eb] += oacc[rb][eb];
+        oacc[rb][eb] = f4{0.f, 0.f, 0.f, 0.f};
+      }
+    // buffer (t+1)&1 was last read in iteration t-1, which ended with a barrier
+    if (t + 1 < ntiles) put((int)((t + 1) & 1));
+    __syncthreads();
+  }
+
+  // D layout of the P . B product: lane holds out[i = 4 g + r][e = 16 eb + li]
+  const int Ec = min(W, a.E - a.e0);
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int eb = 0; eb < EB; ++eb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = i0 + 16 * rb + 4 * g + r;
+        const int e = 16 * eb + li;
+        if (row >= a.M) continue;
+        if (a.C == 1) {
+          if (e < Ec) static_cast<float*>(a.out)[row * a.E + a.e0 + e] = tot[rb][eb][r];
+        } else {
+          a.part[((int64_t)c * a.M + row) * W + e] = tot[rb][eb][r];
+        }
+      }
+}
+
+template <int NCH, int RB, int EPI>
+hipError_t launch_split_e(const MfmaArgs& a, dim3 grid, hipStream_t s) {
+  switch (a.EB) {
+    case 1: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 1>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 2>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 4>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int NCH>
+hipError_t launch_split_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
+  constexpr int RB = NCH >= 8 ? 1 : 2;   // the row count of the fp32 kernel's grid
+  switch (a.epi) {
+    case 0: return launch_split_e<NCH, RB, 0>(a, grid, s);
+    case 1: return launch_split_e<NCH, RB, 1>(a, grid, s);
+    case 2: return launch_split_e<NCH, RB, 2>(a, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int Q>
 constexpr int rows_blocks() { return Q >= 64 ? 1 : 2; }
 
@@ -634,6 +869,18 @@ hipError_t launch_knn_bf16(const MfmaArgs& a, hipStream_t s) {
     case 64: return launch_knn_bf16_n<2>(a, grid, s);
     case 128: return launch_knn_bf16_n<4>(a, grid, s);
     case 256: return launch_knn_bf16_n<8>(a, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_mfma_split(const MfmaArgs& a, hipStream_t s) {
+  const int rows = mfma_rows_per_block(a.DP, 0);
+  const dim3 grid((unsigned)((a.M + rows - 1) / rows * a.C));
+  switch (a.DP) {
+    case 32: return launch_split_n<1>(a, grid, s);
+    case 64: return launch_split_n<2>(a, grid, s);
+    case 128: return launch_split_n<4>(a, grid, s);
+    case 256: return launch_split_n<8>(a, grid, s);
     default: return hipErrorInvalidValue;
   }
 }

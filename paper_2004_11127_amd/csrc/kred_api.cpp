@@ -173,10 +173,10 @@ int fast_epi(kred_formula f, kred_reduction r, int64_t M, int64_t N, int32_t D, 
   return -1;
 }
 
-// Large-D arg-K-min: the exact bf16 kernel is launched beside the fp32 one
-// (the device-side guard picks one) for problems large enough that the guard's
-// pass over x and y pays off, or always with KRED_FLAG_FAST; never with
-// KRED_FLAG_DIRECT.
+// Large D: the bf16 matrix-core kernels (arg-K-min: the exact kernel,
+// launched beside the fp32 one, the device-side guard picking one; sums: the
+// split-product kernel) serve problems large enough that their prologue work
+// pays off, or any size with KRED_FLAG_FAST; never with KRED_FLAG_DIRECT.
 bool exact_eligible(uint32_t flags, int64_t M, int64_t N) {
   if (flags & KRED_FLAG_DIRECT) return false;
   return (flags & KRED_FLAG_FAST) || (double)M * (double)N >= kFastMinPairs;
@@ -316,9 +316,13 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   MPlan pl;
   if (!make_mplan(f, r, p, M, N, D, E, ctx->num_cus, &pl)) return KRED_ERR_UNSUPPORTED;
   const bool knn = (r == KRED_R_ARGKMIN);
-  // arg-K-min: the exact bf16 kernel is a candidate (the device decides)
+  // arg-K-min: the exact bf16 kernel is a candidate (the device decides);
+  // sums: the split bf16 kernel replaces the fp32 one
   const bool exact = knn && exact_eligible(p->flags, M, N);
-  const int64_t ybf_bytes = exact ? align_up(pl.N16 * pl.DP * (int64_t)sizeof(uint16_t)) : 0;
+  const bool split = !knn && exact_eligible(p->flags, M, N);
+  const int64_t ybf_bytes = exact ? align_up(pl.N16 * pl.DP * (int64_t)sizeof(uint16_t))
+                            : split ? align_up(pl.N16 * 3 * pl.DP * (int64_t)sizeof(uint16_t))
+                                    : 0;
   const kred_status gs = grow_scratch(
       ctx, (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes + ybf_bytes));
   if (gs != KRED_OK) return gs;
@@ -334,9 +338,9 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   float* part = pl.part_bytes
                     ? reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes + pl.b_bytes)
                     : nullptr;
-  uint16_t* ybf = exact ? reinterpret_cast<uint16_t*>(base + pl.yop_bytes + pl.ny_bytes +
-                                                        pl.b_bytes + pl.part_bytes)
-                        : nullptr;
+  uint16_t* ybf = (exact || split) ? reinterpret_cast<uint16_t*>(base + pl.yop_bytes + pl.ny_bytes +
+                                                                  pl.b_bytes + pl.part_bytes)
+                                    : nullptr;
   ExactGuard* eg = exact ? ctx->exact_guard : nullptr;
   if (exact && launch_exact_check(x, M, y, N, D, eg, s) != hipSuccess) return KRED_ERR_HIP;
 
@@ -359,7 +363,8 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   pa.ny = ny;
   pa.bpk = bpk;
   pa.exact = eg;
-  pa.ybf = ybf;
+  pa.ybf = exact ? ybf : nullptr;
+  pa.ysp = split ? ybf : nullptr;
   if (launch_mfma_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
 
   MfmaArgs ma{};
@@ -383,7 +388,8 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   ma.KP = pl.KP;
   ma.K = pl.K;
   ma.exact = eg;
-  ma.ybf = ybf;
+  ma.ybf = exact ? ybf : nullptr;
+  ma.ysp = split ? ybf : nullptr;
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (prof) {
@@ -392,11 +398,15 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     if (!e0 || !e1 || hipEventRecord(e0, s) != hipSuccess) return KRED_ERR_HIP;
   }
   // with the exact kernel a candidate, both launch and exactly one does the work
-  if (launch_mfma(ma, s) != hipSuccess) return KRED_ERR_HIP;
+  if (split) {
+    if (launch_mfma_split(ma, s) != hipSuccess) return KRED_ERR_HIP;
+  } else if (launch_mfma(ma, s) != hipSuccess) {
+    return KRED_ERR_HIP;
+  }
   if (exact && launch_knn_bf16(ma, s) != hipSuccess) return KRED_ERR_HIP;
   if (prof) {
     if (hipEventRecord(e1, s) != hipSuccess) return KRED_ERR_HIP;
-    ctx->last_kernel = "mfma_kernel";
+    ctx->last_kernel = split ? "mfma_split_kernel" : "mfma_kernel";
     ctx->last_exact_D = exact ? D : 0;   // resolved from the guard at collect time
   }
   if (knn || pl.C > 1) {

@@ -182,6 +182,8 @@ struct MfmaPackArgs {
   float* bpk;     // null for arg-K-min
   const ExactGuard* exact;   // arg-K-min with the exact path enabled, else null
   unsigned short* ybf;       // bf16 copy of yop (N16 x DP), written instead of yop when exact
+  unsigned short* ysp;       // sums on the split path: yop as 3 bf16 planes (N16 x 3 x DP), written
+                             // instead of yop
 };
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
 
@@ -201,6 +203,7 @@ struct MfmaArgs {
   int KP, K;
   const ExactGuard* exact;     // arg-K-min: exact-path guard, or null (fp32 kernel only)
   const unsigned short* ybf;   // arg-K-min: bf16 column operand when exact
+  const unsigned short* ysp;   // sums: the split column operand (split kernel), else null
 };
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
 // Exact-path prologue: reset the guard, then fold every coordinate of x and y into it.
@@ -209,6 +212,8 @@ hipError_t launch_exact_check(const float* x, int64_t M, const float* y, int64_t
 // The bf16 arg-K-min kernel (runs only when the guard allows it); same partial layout as the
 // fp32 kernel for the same C and jpb.
 hipError_t launch_knn_bf16(const MfmaArgs& a, hipStream_t s);
+// Sums with the contraction on the bf16 matrix cores, fp32-accurate (3-way split, 6 products).
+hipError_t launch_mfma_split(const MfmaArgs& a, hipStream_t s);
 int mfma_pad_d(int D);               // DP for D > 16 (0 if D > 256)
 int mfma_tile_cols(int DP);          // columns per LDS tile
 int mfma_knn_pad_k(int K);           // list length of the matrix-core arg-K-min kernels

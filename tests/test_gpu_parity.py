@@ -273,6 +273,29 @@ def test_large_d_sum_parity(ctx, formula, M, N, D, E, sigma, C):
     assert norm_err(out, ref, norm) <= SUM_TOL
 
 
+@pytest.mark.parametrize("formula,M,N,D,E,sigma,C", LARGE_SUM_CASES)
+def test_large_d_sum_split_parity(ctx, formula, M, N, D, E, sigma, C):
+    # KRED_FLAG_FAST: the contraction on the bf16 matrix cores with split
+    # operands (6 partial products); fp32-level accuracy is expected, so the
+    # error must stay within a few times the fp32 kernel's as well as the bar
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(M * 3 + N + D * 7 + E)
+    x = (rng.standard_normal((M, D)) / np.sqrt(D)).astype(np.float32)
+    y = (rng.standard_normal((N, D)) / np.sqrt(D)).astype(np.float32)
+    b = rng.standard_normal((N, E)).astype(np.float32)
+    ctx.profile_collect()
+    out = host(ctx.run(formula, "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C,
+                       flags=kred.FLAG_FAST | kred.FLAG_PROFILE))
+    assert ctx.profile_collect()[2] == "mfma_split_kernel"
+    f32 = host(ctx.run(formula, "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C,
+                       flags=kred.FLAG_DIRECT))
+    ref, norm = oracle.kernel_sum(formula, x, y, b, sigma=sigma)
+    e_split, e_f32 = norm_err(out, ref, norm), norm_err(f32, ref, norm)
+    print("split %.3g  fp32 %.3g" % (e_split, e_f32))
+    assert e_split <= SUM_TOL
+    assert e_split <= max(4 * e_f32, 2e-6)
+
+
 LARGE_KNN_CASES = [
     # M, N, D, K, col_blocks
     (1, 1, 17, 1, 0), (65, 300, 32, 10, 0), (300, 2000, 64, 10, 0), (1000, 1500, 64, 10, 5),
