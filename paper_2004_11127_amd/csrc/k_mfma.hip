@@ -688,10 +688,14 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
     if (t + 1 < ntiles) fetch(jt + TJ);
     for (int blk = 0; blk < nblk; ++blk) {
       const float4 nyv = ns[buf][blk * 4 + g];
-      f4 acc[RB];
+      // two accumulators per row block (even and odd chunks): four independent
+      // matrix-core chains per wave
+      f4 acc[RB], acc2[RB];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
+      for (int rb = 0; rb < RB; ++rb) {
         acc[rb] = f4{nx[rb] + nyv.x, nx[rb] + nyv.y, nx[rb] + nyv.z, nx[rb] + nyv.w};
+        acc2[rb] = f4{0.f, 0.f, 0.f, 0.f};
+      }
       const uint4* col = &ys[buf][(blk * 16 + li) * RU + g];
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
@@ -700,15 +704,18 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
         const bf16x8 yl = __builtin_bit_cast(bf16x8, col[2 * PU + 4 * ch]);
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
+          f4& A = (ch & 1) ? acc2[rb] : acc[rb];
           // smallest partial products first
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xm[rb][ch], acc[rb], 0, 0, 0);
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yl, xh[rb][ch], acc[rb], 0, 0, 0);
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xl[rb][ch], acc[rb], 0, 0, 0);
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xh[rb][ch], acc[rb], 0, 0, 0);
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xm[rb][ch], acc[rb], 0, 0, 0);
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xh[rb][ch], acc[rb], 0, 0, 0);
+          A = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xm[rb][ch], A, 0, 0, 0);
+          A = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yl, xh[rb][ch], A, 0, 0, 0);
+          A = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xl[rb][ch], A, 0, 0, 0);
+          A = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xh[rb][ch], A, 0, 0, 0);
+          A = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xm[rb][ch], A, 0, 0, 0);
+          A = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xh[rb][ch], A, 0, 0, 0);
         }
       }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[rb] += acc2[rb];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         f4 p;
