@@ -185,9 +185,12 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
  * Rows in no cluster, and clusters without columns, hold the empty reduction
  * (as for N = 0; arg-K-min / K-min pad short lists with -1 / +infinity).
  *
- * Every pair kred_run accepts with D <= 16 (larger D: KRED_ERR_UNSUPPORTED);
- * the direct-form kernels run, without column split.  Arguments, layouts,
- * errors and asynchrony otherwise as kred_run; nr = 0 leaves every row empty.
+ * Every pair kred_run accepts, on the same paths (direct form, the D <= 3
+ * matrix-core exponent, and for 16 < D <= 256 the matrix-core kernels, which
+ * start their column tiles 16-aligned and mask the columns outside a range).
+ * col_blocks (0: automatic) splits each cluster's columns into that many
+ * chunks, reduced by the second pass.  Arguments, layouts, errors and
+ * asynchrony otherwise as kred_run; nr = 0 leaves every row empty.
  */
 kred_status kred_run_ranges(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                             int64_t M, int64_t N, int32_t D, int32_t E,

@@ -129,8 +129,125 @@ __device__ __forceinline__ void list_insert(float (&dk)[KP], int (&jk)[KP], floa
   }
 }
 
+// ------------------------------------------------------------ work items
+// A workgroup's work: dense, a (row block, column block) pair; block-sparse,
+// a row block inside row cluster I and chunk c of I's columns, the chunk
+// being an equal share of the columns of I's ranges in their concatenated
+// order (clamped to [0, N)).  Both are walked as segments [a0, a1) of
+// consecutive columns, in tiles that start 16-aligned (a0 rounded down); the
+// tile's columns outside the segment get b = 0 and the padding norm, which
+// remove them (sums: the norm -infinity gives 2^-inf = 0, and the squared
+// distance's finite value meets b = 0; arg-K-min: +infinity never enters a
+// list).
+struct MItem {
+  int c;                    // column block (dense) or chunk (block-sparse)
+  int64_t row0, row_end;    // the workgroup's first row and the end of its rows
+  int64_t w0, w1;           // dense: the columns; block-sparse: the chunk's window
+  const int* cr;            // block-sparse: the cluster's ranges
+  int nrange;               // 0: dense
+  bool live;                // false: a spare workgroup of a block-sparse grid
+};
+
+__device__ __forceinline__ void mcol_range(const MfmaArgs& a, const int* cr, int q, int64_t& js,
+                                           int64_t& je) {
+  js = min(max((int64_t)cr[2 * q], (int64_t)0), a.N);
+  je = min(max((int64_t)cr[2 * q + 1], js), a.N);
+}
+
+template <bool SP>
+__device__ __forceinline__ MItem mitem(const MfmaArgs& a, int rows) {
+  MItem it;
+  it.cr = nullptr;
+  it.nrange = 0;
+  it.live = true;
+  it.c = blockIdx.x % a.C;
+  if (!SP) {
+    it.row0 = (int64_t)(blockIdx.x / a.C) * rows;
+    it.row_end = a.M;
+    it.w0 = (int64_t)it.c * a.jpb;
+    it.w1 = min(a.N16, it.w0 + a.jpb);
+    return it;
+  }
+  const int blk = (int)(blockIdx.x / a.C);
+  if (blk >= a.bstart[a.nr]) {
+    it.live = false;
+    it.row0 = it.row_end = it.w0 = it.w1 = 0;
+    return it;
+  }
+  int lo = 0, hi = a.nr - 1;   // last cluster I with bstart[I] <= blk
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.bstart[mid] <= blk) lo = mid;
+    else hi = mid - 1;
+  }
+  const int64_t r0 = min(max((int64_t)a.rr[2 * lo], (int64_t)0), a.M);
+  const int64_t r1 = min(max((int64_t)a.rr[2 * lo + 1], r0), a.M);
+  it.row0 = r0 + (int64_t)(blk - a.bstart[lo]) * rows;
+  it.row_end = r1;
+  it.cr = a.cr + 2 * (int64_t)a.cp[lo];
+  it.nrange = a.cp[lo + 1] - a.cp[lo];
+  int64_t L = 0;
+  for (int q = 0; q < it.nrange; ++q) {
+    int64_t js, je;
+    mcol_range(a, it.cr, q, js, je);
+    L += je - js;
+  }
+  it.w0 = L * it.c / a.C;
+  it.w1 = L * (it.c + 1) / a.C;
+  return it;
+}
+
+// Calls seg(a0, a1) for each segment of the item's columns (workgroup-uniform).
+template <class Seg>
+__device__ __forceinline__ void for_segments(const MfmaArgs& a, const MItem& it, Seg&& seg) {
+  if (it.nrange == 0) {
+    if (it.w0 < it.w1) seg(it.w0, it.w1);
+    return;
+  }
+  int64_t off = 0;
+  for (int q = 0; q < it.nrange && off < it.w1; ++q) {
+    int64_t js, je;
+    mcol_range(a, it.cr, q, js, je);
+    const int64_t s0 = max(js, js + (it.w0 - off)), s1 = min(je, js + (it.w1 - off));
+    if (s0 < s1) seg(s0, s1);
+    off += je - js;
+  }
+}
+
+// ny of the 4 columns col .. col + 3 (16-byte aligned), those outside [lo, hi)
+// replaced by the padding norm pad (a value, so that the compiler selects
+// values, not the addresses of two loads).
+__device__ __forceinline__ float4 masked_ny(const float* __restrict__ ny, float pad, int64_t col,
+                                            int64_t lo, int64_t hi) {
+  if (col >= lo && col + 4 <= hi) return *reinterpret_cast<const float4*>(ny + col);
+  float v[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    v[u] = pad;
+    if (col + u >= lo && col + u < hi) v[u] = ny[col + u];
+  }
+  return float4{v[0], v[1], v[2], v[3]};
+}
+
+// A float4 of packed b holding columns col .. col + 3 (one signal column),
+// those outside [lo, hi) zeroed; p is its address.
+__device__ __forceinline__ float4 masked_b(const float4* p, int64_t col, int64_t lo, int64_t hi) {
+  if (col >= lo && col + 4 <= hi) return *p;
+  if (col + 4 <= lo || col >= hi) return float4{0.f, 0.f, 0.f, 0.f};
+  const float4 v = *p;
+  return float4{(col >= lo && col < hi) ? v.x : 0.f, (col + 1 >= lo && col + 1 < hi) ? v.y : 0.f,
+                (col + 2 >= lo && col + 2 < hi) ? v.z : 0.f, (col + 3 >= lo && col + 3 < hi) ? v.w : 0.f};
+}
+
+// Column of the first of the 4 packed-b floats at float offset t4 of a tile
+// starting at column jt (layout: 16-column blocks, 4-column groups, W signal columns).
+__device__ __forceinline__ int64_t bpk_col(int64_t jt, int t4, int W) {
+  return jt + (int64_t)(t4 / (16 * W)) * 16 + ((t4 % (16 * W)) / (4 * W)) * 4;
+}
+
 // EPI: 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min.
-template <int Q, int RB, int EPI, int EB, int KP>
+// SP: block-sparse (a pattern of row clusters and column ranges) or dense.
+template <int Q, int RB, int EPI, int EB, int KP, bool SP>
 __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
   constexpr int DP = 4 * Q;
   constexpr int LDY = DP + 4;
@@ -150,14 +267,15 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
   if constexpr (!SUM) {
     if (exact_ok(a.exact, a.D)) return;   // the bf16 kernel does the work
   }
+  const MItem it = mitem<SP>(a, 64 * RB);
+  if (!it.live) return;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int li = lane & 15, g = lane >> 4;
-  const int c = blockIdx.x % a.C;
-  const int64_t rbk = blockIdx.x / a.C;
-  const int64_t j0 = (int64_t)c * a.jpb;
-  const int64_t j1 = min(a.N16, j0 + a.jpb);
-  const int64_t i0 = rbk * (64 * RB) + wave * (16 * RB);
+  const int c = it.c;
+  const int64_t rend = it.row_end;
+  const float pad_ny = a.pad_ny;
+  const int64_t i0 = it.row0 + wave * (16 * RB);
 
   // rows: lane supplies X[i = li][d = g Q + q] of each of its RB row blocks
   float xr[RB][Q];
@@ -165,7 +283,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int64_t row = i0 + 16 * rb + li;
-    const bool ok = row < a.M;
+    const bool ok = row < rend;
     float part = 0.0f;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
@@ -196,23 +314,32 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
   float4 ystage[YL];
   float4 bstage[BL > 0 ? BL : 1];
   float4 nstage;
-  auto fetch = [&](int64_t jt) {
-    const int ncol = (int)min((int64_t)TJ, j1 - jt);
+  // the tile at column jt (16-aligned), its columns outside [lo, hi) masked
+  auto fetch = [&](int64_t jt, int64_t lo, int64_t hi) {
+    // y of masked columns is loaded as is (inside the padded array): their
+    // padding norm and zero b already remove them
+    const int ncol = (int)min((int64_t)TJ, ((hi + 15) & ~(int64_t)15) - jt);
     const float4* ysrc = reinterpret_cast<const float4*>(a.yop + jt * DP);
 #pragma unroll
     for (int k = 0; k < YL; ++k) {
       const int f = tid + k * 256;
       ystage[k] = (f < YF4 && f < ncol * (DP / 4)) ? ysrc[f] : float4{0.f, 0.f, 0.f, 0.f};
     }
-    if (tid < TJ / 4)
-      nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
-                                : float4{0.f, 0.f, 0.f, 0.f};
+    if (tid < TJ / 4) {
+      if constexpr (SP) nstage = masked_ny(a.ny, pad_ny, jt + 4 * tid, lo, hi);
+      else nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
+                                     : float4{0.f, 0.f, 0.f, 0.f};
+    }
     if constexpr (SUM) {
       const float4* bsrc = reinterpret_cast<const float4*>(a.bpk + jt * W);
 #pragma unroll
       for (int k = 0; k < BL; ++k) {
         const int f = tid + k * 256;
-        bstage[k] = (f < BF4 && f < ncol * W / 4) ? bsrc[f] : float4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (SP)
+          bstage[k] = f < BF4 ? masked_b(bsrc + f, bpk_col(jt, 4 * f, W), lo, hi)
+                              : float4{0.f, 0.f, 0.f, 0.f};
+        else
+          bstage[k] = (f < BF4 && f < ncol * W / 4) ? bsrc[f] : float4{0.f, 0.f, 0.f, 0.f};
       }
     }
   };
@@ -235,17 +362,17 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
     }
   };
 
-  const int64_t ntiles = (j1 - j0 + TJ - 1) / TJ;
-  if (ntiles > 0) {
-    fetch(j0);
-    put(0);
-  }
+  auto segment = [&](int64_t a0, int64_t a1) {
+  const int64_t base = a0 & ~(int64_t)15;
+  const int64_t ntiles = (a1 - base + TJ - 1) / TJ;
+  fetch(base, a0, a1);
+  put(0);
   __syncthreads();
   for (int64_t t = 0; t < ntiles; ++t) {
-    const int64_t jt = j0 + t * TJ;
+    const int64_t jt = base + t * TJ;
     const int buf = (int)(t & 1);
-    const int nblk = (int)(min((int64_t)TJ, j1 - jt) / 16);
-    if (t + 1 < ntiles) fetch(jt + TJ);
+    const int nblk = (int)((min((int64_t)TJ, a1 - jt) + 15) / 16);
+    if (t + 1 < ntiles) fetch(jt + TJ, a0, a1);
     for (int blk = 0; blk < nblk; ++blk) {
       float yo[Q];
       const float4* yrow = &ys[buf][(blk * 16 + li) * (LDY / 4) + g * (Q / 4)];
@@ -308,6 +435,9 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
     if (t + 1 < ntiles) put((int)((t + 1) & 1));
     __syncthreads();
   }
+  };
+  if constexpr (SP) for_segments(a, it, segment);
+  else if (it.w0 < it.w1) segment(it.w0, it.w1);
 
   if constexpr (SUM) {
     // D layout of the P . B product: lane holds out[i = 4 g + r][e = 16 eb + li]
@@ -320,7 +450,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
         for (int r = 0; r < 4; ++r) {
           const int64_t row = i0 + 16 * rb + 4 * g + r;
           const int e = 16 * eb + li;
-          if (row >= a.M) continue;
+          if (row >= rend) continue;
           if (a.C == 1) {
             if (e < Ec) static_cast<float*>(a.out)[row * a.E + a.e0 + e] = tot[rb][eb][r];
           } else {
@@ -338,7 +468,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
       part += __shfl_xor(part, 16);
       part += __shfl_xor(part, 32);
       const int64_t row = i0 + 16 * rb + li;
-      if (row >= a.M) continue;
+      if (row >= rend) continue;
       float* q = a.part + (((int64_t)c * 4 + g) * a.M + row) * (2 * KL);
 #pragma unroll
       for (int p = 0; p < KL; ++p) {
@@ -391,7 +521,7 @@ constexpr int bf16_tile_cols(int DP) { return DP <= 128 ? 64 : 32; }
 // B[8 g .. 8 g + 7][li]; D as for the fp32 product, lane l holds
 // D[4 g + r][li].  With A = Y rows and B = X rows, lane l ranks column
 // j = 4 g + r for row i = li.  Coordinates d = 32 ch + 8 g + t.
-template <int NCH, int RB, int KP>
+template <int NCH, int RB, int KP, bool SP>
 __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
   if (!exact_ok(a.exact, a.D)) return;   // the fp32 kernel does the work
   constexpr int DP = 32 * NCH;
@@ -403,20 +533,21 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
   __shared__ uint4 ys[2][TJ * RU];
   __shared__ float4 ns[2][TJ / 4];
 
+  const MItem it = mitem<SP>(a, 64 * RB);
+  if (!it.live) return;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int li = lane & 15, g = lane >> 4;
-  const int c = blockIdx.x % a.C;
-  const int64_t rbk = blockIdx.x / a.C;
-  const int64_t j0 = (int64_t)c * a.jpb;
-  const int64_t j1 = min(a.N16, j0 + a.jpb);
-  const int64_t i0 = rbk * (64 * RB) + wave * (16 * RB);
+  const int c = it.c;
+  const int64_t rend = it.row_end;
+  const float pad_ny = a.pad_ny;
+  const int64_t i0 = it.row0 + wave * (16 * RB);
 
   bf16x8 xb[RB][NCH];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int64_t row = i0 + 16 * rb + li;
-    const bool ok = row < a.M;
+    const bool ok = row < rend;
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch)
 #pragma unroll
@@ -449,17 +580,22 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
 
   uint4 ystage[YL];
   float4 nstage;
-  auto fetch = [&](int64_t jt) {
-    const int ncol = (int)min((int64_t)TJ, j1 - jt);
+  // the tile at column jt (16-aligned), its columns outside [lo, hi) masked
+  auto fetch = [&](int64_t jt, int64_t lo, int64_t hi) {
+    // y of masked columns is loaded as is (inside the padded array): their
+    // padding norm (+infinity) keeps them out of every list
+    const int ncol = (int)min((int64_t)TJ, ((hi + 15) & ~(int64_t)15) - jt);
     const uint4* ysrc = reinterpret_cast<const uint4*>(a.ybf + jt * DP);
 #pragma unroll
     for (int k = 0; k < YL; ++k) {
       const int f = tid + k * 256;
       ystage[k] = (f < TU && f < ncol * (DP / 8)) ? ysrc[f] : uint4{0u, 0u, 0u, 0u};
     }
-    if (tid < TJ / 4)
-      nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
-                                : float4{0.f, 0.f, 0.f, 0.f};
+    if (tid < TJ / 4) {
+      if constexpr (SP) nstage = masked_ny(a.ny, pad_ny, jt + 4 * tid, lo, hi);
+      else nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
+                                     : float4{0.f, 0.f, 0.f, 0.f};
+    }
   };
   auto put = [&](int buf) {
 #pragma unroll
@@ -470,17 +606,17 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
     if (tid < TJ / 4) ns[buf][tid] = nstage;
   };
 
-  const int64_t ntiles = (j1 - j0 + TJ - 1) / TJ;
-  if (ntiles > 0) {
-    fetch(j0);
-    put(0);
-  }
+  auto segment = [&](int64_t a0, int64_t a1) {
+  const int64_t base = a0 & ~(int64_t)15;
+  const int64_t ntiles = (a1 - base + TJ - 1) / TJ;
+  fetch(base, a0, a1);
+  put(0);
   __syncthreads();
   for (int64_t t = 0; t < ntiles; ++t) {
-    const int64_t jt = j0 + t * TJ;
+    const int64_t jt = base + t * TJ;
     const int buf = (int)(t & 1);
-    const int nblk = (int)(min((int64_t)TJ, j1 - jt) / 16);
-    if (t + 1 < ntiles) fetch(jt + TJ);
+    const int nblk = (int)((min((int64_t)TJ, a1 - jt) + 15) / 16);
+    if (t + 1 < ntiles) fetch(jt + TJ, a0, a1);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       float v = dk[rb][KP - 1];
@@ -528,6 +664,9 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
     if (t + 1 < ntiles) put((int)((t + 1) & 1));
     __syncthreads();
   }
+  };
+  if constexpr (SP) for_segments(a, it, segment);
+  else if (it.w0 < it.w1) segment(it.w0, it.w1);
 
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
@@ -542,7 +681,7 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
     part += __shfl_xor(part, 16);
     part += __shfl_xor(part, 32);
     const int64_t row = i0 + 16 * rb + li;
-    if (row >= a.M) continue;
+    if (row >= rend) continue;
     float* q = a.part + (((int64_t)c * 4 + g) * a.M + row) * (2 * KP);
 #pragma unroll
     for (int p = 0; p < KP; ++p) {
@@ -552,18 +691,21 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
   }
 }
 
-constexpr int bf16_rows_blocks(int KP) { return KP >= 64 ? 1 : 2; }
+// rows per workgroup as in the fp32 kernel, so both share one grid and one
+// block-sparse workgroup map
+constexpr int bf16_rows_blocks(int NCH, int KP) { return (NCH >= 8 || KP >= 64) ? 1 : 2; }
 
-template <int NCH>
+template <int NCH, bool SP>
 hipError_t launch_knn_bf16_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   switch (a.KP) {
-    case 1: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(1), 1>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(4), 4>), grid, dim3(256), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(8), 8>), grid, dim3(256), 0, s, a); break;
-    case 10: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(10), 10>), grid, dim3(256), 0, s, a); break;
-    case 12: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(12), 12>), grid, dim3(256), 0, s, a); break;
-    case 16: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(16), 16>), grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(64), 64>), grid, dim3(256), 0, s, a); break;
+#define KRED_KNN_BF16(KPV)                                                                     \
+  case KPV:                                                                                     \
+    hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(NCH, KPV), KPV, SP>), grid, dim3(256), \
+                       0, s, a);                                                                \
+    break;
+    KRED_KNN_BF16(1) KRED_KNN_BF16(4) KRED_KNN_BF16(8) KRED_KNN_BF16(10) KRED_KNN_BF16(12)
+    KRED_KNN_BF16(16) KRED_KNN_BF16(64)
+#undef KRED_KNN_BF16
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -582,7 +724,7 @@ hipError_t launch_knn_bf16_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
 // per column (prologue); row operand: the planes of x in registers.
 constexpr int split_tile_cols(int DP) { return DP <= 64 ? 64 : (DP <= 128 ? 32 : 16); }
 
-template <int NCH, int RB, int EPI, int EB>
+template <int NCH, int RB, int EPI, int EB, bool SP>
 __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
   constexpr int DP = 32 * NCH;
   constexpr int TJ = split_tile_cols(DP);
@@ -598,14 +740,15 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
   __shared__ float4 ns[2][TJ / 4];
   __shared__ float4 bs[2][TJ * W / 4];
 
+  const MItem it = mitem<SP>(a, 64 * RB);
+  if (!it.live) return;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int li = lane & 15, g = lane >> 4;
-  const int c = blockIdx.x % a.C;
-  const int64_t rbk = blockIdx.x / a.C;
-  const int64_t j0 = (int64_t)c * a.jpb;
-  const int64_t j1 = min(a.N16, j0 + a.jpb);
-  const int64_t i0 = rbk * (64 * RB) + wave * (16 * RB);
+  const int c = it.c;
+  const int64_t rend = it.row_end;
+  const float pad_ny = a.pad_ny;
+  const int64_t i0 = it.row0 + wave * (16 * RB);
 
   // rows: lane supplies B[k = 8 g .. 8 g + 7][n = li] of chunk ch, i.e. the
   // planes of x[i = li][32 ch + 8 g + t]
@@ -614,7 +757,7 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int64_t row = i0 + 16 * rb + li;
-    const bool ok = row < a.M;
+    const bool ok = row < rend;
     float part = 0.0f;
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch)
@@ -643,22 +786,31 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
   uint4 ystage[YL];
   float4 bstage[BL];
   float4 nstage;
-  auto fetch = [&](int64_t jt) {
-    const int ncol = (int)min((int64_t)TJ, j1 - jt);
+  // the tile at column jt (16-aligned), its columns outside [lo, hi) masked
+  auto fetch = [&](int64_t jt, int64_t lo, int64_t hi) {
+    // y of masked columns is loaded as is (inside the padded array): their
+    // padding norm and zero b already remove them
+    const int ncol = (int)min((int64_t)TJ, ((hi + 15) & ~(int64_t)15) - jt);
     const uint4* ysrc = reinterpret_cast<const uint4*>(a.ysp + jt * 3 * DP);
 #pragma unroll
     for (int k = 0; k < YL; ++k) {
       const int f = tid + k * 256;
       ystage[k] = (f < TU && f < ncol * 3 * PU) ? ysrc[f] : uint4{0u, 0u, 0u, 0u};
     }
-    if (tid < TJ / 4)
-      nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
-                                : float4{0.f, 0.f, 0.f, 0.f};
+    if (tid < TJ / 4) {
+      if constexpr (SP) nstage = masked_ny(a.ny, pad_ny, jt + 4 * tid, lo, hi);
+      else nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
+                                     : float4{0.f, 0.f, 0.f, 0.f};
+    }
     const float4* bsrc = reinterpret_cast<const float4*>(a.bpk + jt * W);
 #pragma unroll
     for (int k = 0; k < BL; ++k) {
       const int f = tid + k * 256;
-      bstage[k] = (f < BF4 && f < ncol * W / 4) ? bsrc[f] : float4{0.f, 0.f, 0.f, 0.f};
+      if constexpr (SP)
+        bstage[k] = f < BF4 ? masked_b(bsrc + f, bpk_col(jt, 4 * f, W), lo, hi)
+                            : float4{0.f, 0.f, 0.f, 0.f};
+      else
+        bstage[k] = (f < BF4 && f < ncol * W / 4) ? bsrc[f] : float4{0.f, 0.f, 0.f, 0.f};
     }
   };
   auto put = [&](int buf) {
@@ -675,17 +827,17 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
     }
   };
 
-  const int64_t ntiles = (j1 - j0 + TJ - 1) / TJ;
-  if (ntiles > 0) {
-    fetch(j0);
-    put(0);
-  }
+  auto segment = [&](int64_t a0, int64_t a1) {
+  const int64_t base = a0 & ~(int64_t)15;
+  const int64_t ntiles = (a1 - base + TJ - 1) / TJ;
+  fetch(base, a0, a1);
+  put(0);
   __syncthreads();
   for (int64_t t = 0; t < ntiles; ++t) {
-    const int64_t jt = j0 + t * TJ;
+    const int64_t jt = base + t * TJ;
     const int buf = (int)(t & 1);
-    const int nblk = (int)(min((int64_t)TJ, j1 - jt) / 16);
-    if (t + 1 < ntiles) fetch(jt + TJ);
+    const int nblk = (int)((min((int64_t)TJ, a1 - jt) + 15) / 16);
+    if (t + 1 < ntiles) fetch(jt + TJ, a0, a1);
     for (int blk = 0; blk < nblk; ++blk) {
       const float4 nyv = ns[buf][blk * 4 + g];
       // two accumulators per row block (even and odd chunks): four independent
@@ -749,6 +901,9 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
     if (t + 1 < ntiles) put((int)((t + 1) & 1));
     __syncthreads();
   }
+  };
+  if constexpr (SP) for_segments(a, it, segment);
+  else if (it.w0 < it.w1) segment(it.w0, it.w1);
 
   // D layout of the P . B product: lane holds out[i = 4 g + r][e = 16 eb + li]
   const int Ec = min(W, a.E - a.e0);
@@ -760,7 +915,7 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
       for (int r = 0; r < 4; ++r) {
         const int64_t row = i0 + 16 * rb + 4 * g + r;
         const int e = 16 * eb + li;
-        if (row >= a.M) continue;
+        if (row >= rend) continue;
         if (a.C == 1) {
           if (e < Ec) static_cast<float*>(a.out)[row * a.E + a.e0 + e] = tot[rb][eb][r];
         } else {
@@ -769,24 +924,24 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
       }
 }
 
-template <int NCH, int RB, int EPI>
+template <int NCH, int RB, int EPI, bool SP>
 hipError_t launch_split_e(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   switch (a.EB) {
-    case 1: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 1>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 2>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 4>), grid, dim3(256), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 1, SP>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 2, SP>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 4, SP>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-template <int NCH>
+template <int NCH, bool SP>
 hipError_t launch_split_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   constexpr int RB = NCH >= 8 ? 1 : 2;   // the row count of the fp32 kernel's grid
   switch (a.epi) {
-    case 0: return launch_split_e<NCH, RB, 0>(a, grid, s);
-    case 1: return launch_split_e<NCH, RB, 1>(a, grid, s);
-    case 2: return launch_split_e<NCH, RB, 2>(a, grid, s);
+    case 0: return launch_split_e<NCH, RB, 0, SP>(a, grid, s);
+    case 1: return launch_split_e<NCH, RB, 1, SP>(a, grid, s);
+    case 2: return launch_split_e<NCH, RB, 2, SP>(a, grid, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -794,34 +949,34 @@ hipError_t launch_split_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
 template <int Q>
 constexpr int rows_blocks() { return Q >= 64 ? 1 : 2; }
 
-template <int Q, int EPI>
+template <int Q, int EPI, bool SP>
 hipError_t launch_sum_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   constexpr int RB = rows_blocks<Q>();
   switch (a.EB) {
-    case 1: hipLaunchKernelGGL((mfma_kernel<Q, RB, EPI, 1, 1>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((mfma_kernel<Q, RB, EPI, 2, 1>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((mfma_kernel<Q, RB, EPI, 4, 1>), grid, dim3(256), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((mfma_kernel<Q, RB, EPI, 1, 1, SP>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((mfma_kernel<Q, RB, EPI, 2, 1, SP>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((mfma_kernel<Q, RB, EPI, 4, 1, SP>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-template <int Q>
+template <int Q, bool SP>
 hipError_t launch_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   constexpr int RB = rows_blocks<Q>();
   switch (a.epi) {
-    case 0: return launch_sum_q<Q, 0>(a, grid, s);
-    case 1: return launch_sum_q<Q, 1>(a, grid, s);
-    case 2: return launch_sum_q<Q, 2>(a, grid, s);
+    case 0: return launch_sum_q<Q, 0, SP>(a, grid, s);
+    case 1: return launch_sum_q<Q, 1, SP>(a, grid, s);
+    case 2: return launch_sum_q<Q, 2, SP>(a, grid, s);
     case 3:
       switch (a.KP) {
-        case 1: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 1>), grid, dim3(256), 0, s, a); break;
-        case 4: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 4>), grid, dim3(256), 0, s, a); break;
-        case 8: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 8>), grid, dim3(256), 0, s, a); break;
-        case 10: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 10>), grid, dim3(256), 0, s, a); break;
-        case 12: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 12>), grid, dim3(256), 0, s, a); break;
-        case 16: hipLaunchKernelGGL((mfma_kernel<Q, RB, 3, 1, 16>), grid, dim3(256), 0, s, a); break;
-        case 64: hipLaunchKernelGGL((mfma_kernel<Q, 1, 3, 1, 64>), grid, dim3(256), 0, s, a); break;
+#define KRED_KNN_F32(KPV, RBV)                                                                 \
+  case KPV:                                                                                     \
+    hipLaunchKernelGGL((mfma_kernel<Q, RBV, 3, 1, KPV, SP>), grid, dim3(256), 0, s, a);        \
+    break;
+        KRED_KNN_F32(1, RB) KRED_KNN_F32(4, RB) KRED_KNN_F32(8, RB) KRED_KNN_F32(10, RB)
+        KRED_KNN_F32(12, RB) KRED_KNN_F32(16, RB) KRED_KNN_F32(64, 1)
+#undef KRED_KNN_F32
         default: return hipErrorInvalidValue;
       }
       return hipGetLastError();
@@ -835,6 +990,10 @@ hipError_t launch_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
 int mfma_pad_d(int D) { return D <= 32 ? 32 : (D <= 64 ? 64 : (D <= 128 ? 128 : (D <= 256 ? 256 : 0))); }
 
 int mfma_tile_cols(int DP) { return tile_cols(DP); }
+
+int64_t mfma_row_groups(const MfmaArgs& a, int rows) {
+  return a.nr > 0 ? range_grid_bound(a.nr, a.M, rows) : (a.M + rows - 1) / rows;
+}
 
 int mfma_knn_pad_k(int K) {
   return K <= 1 ? 1 : K <= 4 ? 4 : K <= 8 ? 8 : K <= 10 ? 10 : K <= 12 ? 12 : K <= 16 ? 16 : 64;
@@ -869,38 +1028,37 @@ hipError_t launch_exact_check(const float* x, int64_t M, const float* y, int64_t
 }
 
 hipError_t launch_knn_bf16(const MfmaArgs& a, hipStream_t s) {
-  const int rows = 64 * bf16_rows_blocks(a.KP);
-  const dim3 grid((unsigned)((a.M + rows - 1) / rows * a.C));
+  const int rows = mfma_rows_per_block(a.DP, a.KP);
+  const dim3 grid((unsigned)(mfma_row_groups(a, rows) * a.C));
   switch (a.DP) {
-    case 32: return launch_knn_bf16_n<1>(a, grid, s);
-    case 64: return launch_knn_bf16_n<2>(a, grid, s);
-    case 128: return launch_knn_bf16_n<4>(a, grid, s);
-    case 256: return launch_knn_bf16_n<8>(a, grid, s);
+    case 32: return a.nr > 0 ? launch_knn_bf16_n<1, true>(a, grid, s) : launch_knn_bf16_n<1, false>(a, grid, s);
+    case 64: return a.nr > 0 ? launch_knn_bf16_n<2, true>(a, grid, s) : launch_knn_bf16_n<2, false>(a, grid, s);
+    case 128: return a.nr > 0 ? launch_knn_bf16_n<4, true>(a, grid, s) : launch_knn_bf16_n<4, false>(a, grid, s);
+    case 256: return a.nr > 0 ? launch_knn_bf16_n<8, true>(a, grid, s) : launch_knn_bf16_n<8, false>(a, grid, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_mfma_split(const MfmaArgs& a, hipStream_t s) {
   const int rows = mfma_rows_per_block(a.DP, 0);
-  const dim3 grid((unsigned)((a.M + rows - 1) / rows * a.C));
+  const dim3 grid((unsigned)(mfma_row_groups(a, rows) * a.C));
   switch (a.DP) {
-    case 32: return launch_split_n<1>(a, grid, s);
-    case 64: return launch_split_n<2>(a, grid, s);
-    case 128: return launch_split_n<4>(a, grid, s);
-    case 256: return launch_split_n<8>(a, grid, s);
+    case 32: return a.nr > 0 ? launch_split_n<1, true>(a, grid, s) : launch_split_n<1, false>(a, grid, s);
+    case 64: return a.nr > 0 ? launch_split_n<2, true>(a, grid, s) : launch_split_n<2, false>(a, grid, s);
+    case 128: return a.nr > 0 ? launch_split_n<4, true>(a, grid, s) : launch_split_n<4, false>(a, grid, s);
+    case 256: return a.nr > 0 ? launch_split_n<8, true>(a, grid, s) : launch_split_n<8, false>(a, grid, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s) {
   const int rows = mfma_rows_per_block(a.DP, a.KP);
-  const int64_t rb = (a.M + rows - 1) / rows;
-  const dim3 grid((unsigned)(rb * a.C));
+  const dim3 grid((unsigned)(mfma_row_groups(a, rows) * a.C));
   switch (a.DP) {
-    case 32: return launch_q<8>(a, grid, s);
-    case 64: return launch_q<16>(a, grid, s);
-    case 128: return launch_q<32>(a, grid, s);
-    case 256: return launch_q<64>(a, grid, s);
+    case 32: return a.nr > 0 ? launch_q<8, true>(a, grid, s) : launch_q<8, false>(a, grid, s);
+    case 64: return a.nr > 0 ? launch_q<16, true>(a, grid, s) : launch_q<16, false>(a, grid, s);
+    case 128: return a.nr > 0 ? launch_q<32, true>(a, grid, s) : launch_q<32, false>(a, grid, s);
+    case 256: return a.nr > 0 ? launch_q<64, true>(a, grid, s) : launch_q<64, false>(a, grid, s);
     default: return hipErrorInvalidValue;
   }
 }

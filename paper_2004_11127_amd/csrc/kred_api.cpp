@@ -310,11 +310,33 @@ hipEvent_t next_event(kred_ctx* ctx) {
   return ctx->ev[ctx->ev_used++];
 }
 
+// Block-sparse pattern of a call (nr row clusters; see DirectArgs).
+struct Ranges {
+  int nr;
+  const int* rr;
+  const int* cp;
+  const int* cr;
+};
+
 kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                      int64_t M, int64_t N, int32_t D, int32_t E, const float* x, const float* y,
-                     const float* b, void* out, hipStream_t s, int kvalues) {
+                     const float* b, void* out, hipStream_t s, int kvalues,
+                     const Ranges* rg = nullptr) {
+  kred_params pr;
+  if (rg && p->col_blocks == 0) {
+    // chunks of each cluster's columns: enough workgroups for every CU, the
+    // row-block count estimated as max(clusters, M / rows per workgroup)
+    const int DP = mfma_pad_d(D);
+    const int rows = mfma_rows_per_block(DP, r == KRED_R_ARGKMIN ? mfma_knn_pad_k(p->K) : 0);
+    const int64_t est = std::max<int64_t>({1, (int64_t)rg->nr, (M + rows - 1) / rows});
+    pr = *p;
+    pr.col_blocks = (int)std::min<int64_t>(64, ((int64_t)ctx->num_cus * 16 + est - 1) / est);
+    p = &pr;
+  }
   MPlan pl;
   if (!make_mplan(f, r, p, M, N, D, E, ctx->num_cus, &pl)) return KRED_ERR_UNSUPPORTED;
+  if (rg) pl.C = std::max(1, std::min(p->col_blocks, KRED_MAX_COL_BLOCKS));   // chunks per cluster
+  const int64_t rows_wg = mfma_rows_per_block(pl.DP, pl.KP);
   const bool knn = (r == KRED_R_ARGKMIN);
   // arg-K-min: the exact bf16 kernel is a candidate (the device decides);
   // sums: the split bf16 kernel replaces the fp32 one
@@ -323,8 +345,15 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   const int64_t ybf_bytes = exact ? align_up(pl.N16 * pl.DP * (int64_t)sizeof(uint16_t))
                             : split ? align_up(pl.N16 * 3 * pl.DP * (int64_t)sizeof(uint16_t))
                                     : 0;
+  if (rg) {   // partials of every chunk (rows outside the clusters read the empty value)
+    pl.part_bytes = knn ? align_up((int64_t)4 * pl.C * M * 2 * pl.KP * (int64_t)sizeof(float))
+                  : pl.C > 1 ? align_up((int64_t)pl.C * M * pl.W * (int64_t)sizeof(float))
+                             : 0;
+  }
+  const int64_t bstart_bytes = rg ? align_up((int64_t)(rg->nr + 1) * (int64_t)sizeof(int)) : 0;
   const kred_status gs = grow_scratch(
-      ctx, (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes + ybf_bytes));
+      ctx, (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes + ybf_bytes +
+                    bstart_bytes));
   if (gs != KRED_OK) return gs;
   if (exact && ctx->exact_guard == nullptr &&
       hipMalloc(reinterpret_cast<void**>(&ctx->exact_guard), sizeof(ExactGuard)) != hipSuccess) {
@@ -341,8 +370,21 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   uint16_t* ybf = (exact || split) ? reinterpret_cast<uint16_t*>(base + pl.yop_bytes + pl.ny_bytes +
                                                                   pl.b_bytes + pl.part_bytes)
                                     : nullptr;
+  int* bstart = rg ? reinterpret_cast<int*>(base + pl.yop_bytes + pl.ny_bytes + pl.b_bytes +
+                                            pl.part_bytes + ybf_bytes)
+                   : nullptr;
   ExactGuard* eg = exact ? ctx->exact_guard : nullptr;
   if (exact && launch_exact_check(x, M, y, N, D, eg, s) != hipSuccess) return KRED_ERR_HIP;
+  if (rg) {
+    if (launch_range_blocks(rg->rr, rg->nr, M, (int)rows_wg, bstart, s) != hipSuccess)
+      return KRED_ERR_HIP;
+    // (distance, index) pairs: 4 C lists of KP pairs per row, count in floats
+    if (knn && launch_fill2(part, (int64_t)4 * pl.C * M * 2 * pl.KP, INFINITY,
+                            __builtin_bit_cast(float, (int32_t)INT32_MAX), s) != hipSuccess)
+      return KRED_ERR_HIP;
+    if (!knn && pl.C > 1 && launch_fill(part, (int64_t)pl.C * M * pl.W, 0.0f, s) != hipSuccess)
+      return KRED_ERR_HIP;
+  }
 
   MfmaPackArgs pa{};
   pa.y = y;
@@ -390,6 +432,15 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   ma.exact = eg;
   ma.ybf = exact ? ybf : nullptr;
   ma.ysp = split ? ybf : nullptr;
+  ma.N = N;
+  ma.pad_ny = pl.pad_norm;
+  if (rg) {
+    ma.nr = rg->nr;
+    ma.rr = rg->rr;
+    ma.cp = rg->cp;
+    ma.cr = rg->cr;
+    ma.bstart = bstart;
+  }
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (prof) {
@@ -430,14 +481,6 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   return KRED_OK;
 }
 
-// Block-sparse pattern of a call (nr row clusters; see DirectArgs).
-struct Ranges {
-  int nr;
-  const int* rr;
-  const int* cp;
-  const int* cr;
-};
-
 // Value an empty reduction writes (and the output's element count) for r.
 void empty_fill(kred_formula f, kred_reduction r, const kred_params* p, int64_t M, int32_t D,
                 int32_t E, const float* b, int64_t* count, float* value) {
@@ -458,7 +501,7 @@ void empty_fill(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
 }
 
 // One reduction on validated arguments, M > 0, on the current device;
-// block-sparse when rg is given (direct kernels, no column split).
+// block-sparse when rg is given.
 kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                           int64_t M, int64_t N, int32_t D, int32_t E, const float* x,
                           const float* y, const float* b, void* out, hipStream_t s,
@@ -488,7 +531,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   // kernel-side formula: log-sum-exps run on the Sinkhorn-form kernels
   const int kf = (r == KRED_R_LSE) ? (f == KRED_F_LAPLACE ? F_LAPLACE_LSE : F_SINKHORN) : (int)f;
 
-  if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s, kvalues);
+  if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s, kvalues, rg);
 
   kred_params pr;
   if (rg) {
@@ -949,7 +992,6 @@ kred_status kred_validate_ranges(kred_formula f, kred_reduction r, const kred_pa
   const kred_status v = kred_validate(f, r, p, M, N, D, E, x, y, b, out);
   if (v != KRED_OK) return v;
   if (nr < 0) return KRED_ERR_INVALID_ARG;
-  if (D > kMaxDirectD) return KRED_ERR_UNSUPPORTED;
   if (nr > 0 && (row_ranges == nullptr || col_ptr == nullptr || col_ranges == nullptr))
     return KRED_ERR_INVALID_ARG;
   if (misaligned(row_ranges) || misaligned(col_ptr) || misaligned(col_ranges))

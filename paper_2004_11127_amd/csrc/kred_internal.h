@@ -204,6 +204,15 @@ struct MfmaArgs {
   const ExactGuard* exact;     // arg-K-min: exact-path guard, or null (fp32 kernel only)
   const unsigned short* ybf;   // arg-K-min: bf16 column operand when exact
   const unsigned short* ysp;   // sums: the split column operand (split kernel), else null
+  int64_t N;                   // columns (block-sparse ranges are clamped to it)
+  float pad_ny;                // the padding columns' norm (masked columns of a tile)
+  // block-sparse pattern (nr = 0: dense), as for the direct kernels; bstart is
+  // the workgroup map for the kernels' rows per workgroup
+  int nr;
+  const int* rr;
+  const int* cp;
+  const int* cr;
+  const int* bstart;
 };
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
 // Exact-path prologue: reset the guard, then fold every coordinate of x and y into it.
@@ -218,6 +227,7 @@ int mfma_pad_d(int D);               // DP for D > 16 (0 if D > 256)
 int mfma_tile_cols(int DP);          // columns per LDS tile
 int mfma_knn_pad_k(int K);           // list length of the matrix-core arg-K-min kernels
 int mfma_rows_per_block(int DP, int KP);
+int64_t mfma_row_groups(const MfmaArgs& a, int rows);   // row-block slots of the grid
 
 struct FastPackArgs {
   int epi, D;

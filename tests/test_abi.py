@@ -226,5 +226,9 @@ def test_ranges_validation(lib):
     assert VR("gauss", "sum", 100, 200, 3, 1, 5, cr=None, sigma=1.0) == INVALID
     assert VR("gauss", "sum", 100, 200, 3, 1, -1, sigma=1.0) == INVALID
     assert VR("gauss", "sum", 100, 200, 3, 1, 5, rr=2, sigma=1.0) == INVALID   # misaligned
-    assert VR("gauss", "sum", 100, 200, 17, 1, 5, sigma=1.0) == UNSUPPORTED
+    # the matrix-core path (16 < D <= 256) takes patterns for what kred_run accepts there
+    assert VR("gauss", "sum", 100, 200, 17, 1, 5, sigma=1.0) == OK
+    assert VR("sqdist", "argkmin", 100, 200, 64, 0, 5, b=None, K=10) == OK
+    assert VR("gauss", "lse", 100, 200, 17, 1, 5, sigma=1.0) == UNSUPPORTED
+    assert VR("gauss", "sum", 100, 200, 257, 1, 5, sigma=1.0) == INVALID        # as kred_run
     assert VR("gauss", "sum", 100, 200, 3, 1, 5, sigma=0.0) == INVALID         # as kred_run

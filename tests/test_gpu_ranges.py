@@ -232,3 +232,88 @@ def test_ranges_nearest_fast_path(ctx, red):
         val, idx = oracle.ranges_reduce("min", x, y, None, *pat, formula="sqdist")
         ref = idx.astype(np.int32) if red == "argmin" else val.astype(np.float32)
         np.testing.assert_array_equal(out, ref)
+
+
+# ---------------------------------------------------------------- 16 < D <= 256
+LARGE_SUMS = [
+    # formula, M, N, D, E, sigma, clusters (rows, cols)
+    ("gauss", 1500, 2000, 64, 16, 1.0, (6, 10)),
+    ("gauss", 700, 1300, 128, 5, 1.2, (40, 25)),
+    ("laplace", 900, 1100, 40, 3, 1.0, (5, 8)),
+    ("sqdist", 600, 800, 33, 20, 1.0, (4, 6)),
+    ("gauss", 300, 900, 256, 64, 1.0, (3, 5)),
+]
+
+
+@pytest.mark.parametrize("path", ["fp32", "split"])
+@pytest.mark.parametrize("C", CHUNKS)
+@pytest.mark.parametrize("formula,M,N,D,E,sigma,cl", LARGE_SUMS)
+def test_ranges_large_d_sum(ctx, formula, M, N, D, E, sigma, cl, C, path):
+    # the matrix-core sums: fp32 products (KRED_FLAG_DIRECT) or split bf16 products
+    # (KRED_FLAG_FAST); tiles start 16-aligned and mask the columns outside each range
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(M + N + E + D)
+    x = (rng.standard_normal((M, D)) / np.sqrt(D)).astype(np.float32)
+    y = (rng.standard_normal((N, D)) / np.sqrt(D)).astype(np.float32)
+    b = rng.standard_normal((N, E)).astype(np.float32)
+    pat = random_pattern(rng, M, N, *cl)
+    fl = kred.FLAG_DIRECT if path == "fp32" else kred.FLAG_FAST
+    ctx.profile_collect()
+    out = call(ctx, formula, "sum", x, y, b, pat, sigma=sigma, col_blocks=C,
+               flags=fl | kred.FLAG_PROFILE)
+    assert ctx.profile_collect()[2] == ("mfma_kernel" if path == "fp32" else "mfma_split_kernel")
+    ref, norm = oracle.ranges_reduce("sum", x, y, b, *pat, formula=formula, sigma=sigma)
+    assert norm_err(out, ref, norm) <= SUM_TOL
+    covered = np.zeros(M, bool)
+    for r0, r1 in pat[0]:
+        covered[r0:r1] = True
+    assert (out[~covered] == 0).all()
+
+
+@pytest.mark.parametrize("path", ["fp32", "exact"])
+@pytest.mark.parametrize("C", CHUNKS)
+@pytest.mark.parametrize("red,K,D", [("argkmin", 10, 64), ("kmin", 5, 40), ("argkmin", 1, 128),
+                                     ("argkmin", 16, 200), ("kmin", 64, 24)])
+def test_ranges_large_d_knn_exact(ctx, red, K, D, C, path):
+    # integer coordinates: the fp32 kernel and the exact bf16 kernel must both
+    # match the oracle bit for bit, ties included
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(7 + K + D)
+    M, N = 1200, 2500
+    x = rng.integers(-4, 5, (M, D)).astype(np.float32); y = rng.integers(-4, 5, (N, D)).astype(np.float32)
+    y[N // 2:N // 2 + N // 10] = y[:N // 10]
+    pat = random_pattern(rng, M, N, 7, 18, p_keep=0.3)   # some clusters get fewer than K columns
+    fl = kred.FLAG_DIRECT if path == "fp32" else kred.FLAG_FAST
+    ctx.profile_collect()
+    out = call(ctx, "sqdist", red, x, y, None, pat, K=K, col_blocks=C, flags=fl | kred.FLAG_PROFILE)
+    assert ctx.profile_collect()[2] == ("mfma_kernel" if path == "fp32" else "knn_bf16_kernel")
+    ref, _ = oracle.ranges_reduce(red, x, y, None, *pat, K=K)
+    np.testing.assert_array_equal(out, ref.astype(out.dtype))
+
+
+@pytest.mark.parametrize("red", ["min", "argmin"])
+def test_ranges_large_d_nearest(ctx, red):
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(12)
+    M, N, D = 900, 1700, 48
+    x = rng.integers(-4, 5, (M, D)).astype(np.float32); y = rng.integers(-4, 5, (N, D)).astype(np.float32)
+    pat = random_pattern(rng, M, N, 9, 12)
+    out = call(ctx, "sqdist", red, x, y, None, pat, flags=kred.FLAG_FAST)
+    val, idx = oracle.ranges_reduce("min", x, y, None, *pat, formula="sqdist")
+    ref = idx.astype(np.int32) if red == "argmin" else val.astype(np.float32)
+    np.testing.assert_array_equal(out.reshape(ref.shape), ref)
+
+
+def test_ranges_large_d_full_pattern_matches_dense(ctx):
+    # one cluster holding every row and every column: same values as kred_run
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(13)
+    M, N, D, E = 777, 1333, 96, 16
+    x = (rng.standard_normal((M, D)) / np.sqrt(D)).astype(np.float32)
+    y = (rng.standard_normal((N, D)) / np.sqrt(D)).astype(np.float32)
+    b = rng.standard_normal((N, E)).astype(np.float32)
+    pat = (np.array([[0, M]], np.int32), np.array([0, 1], np.int32), np.array([[0, N]], np.int32))
+    for fl in (kred.FLAG_DIRECT, kred.FLAG_FAST):
+        dense = host(ctx.run("gauss", "sum", dev(x), dev(y), dev(b), sigma=1.0, col_blocks=1, flags=fl))
+        sparse = call(ctx, "gauss", "sum", x, y, b, pat, sigma=1.0, col_blocks=1, flags=fl)
+        np.testing.assert_array_equal(sparse, dense)
