@@ -1,8 +1,8 @@
 // Second pass over column-block partials (when the j range was split into C
 // blocks to give a small-M problem enough workgroups).  Each partial is the
 // reduction of Eq. (2) over one block of columns; this pass applies the same
-// reduction across blocks, in increasing block order (fixed, so results are
-// reproducible run to run):
+// reduction across blocks in a fixed order (so results are reproducible run
+// to run; the sums interleave four lanes per element, see combine_sum_kernel):
 //   sum:          a = sum_c a_c  (also the x-gradient sums of the Gaussian
 //                 vector-Jacobian product, scaled by -1/sigma^2)
 //   log-sum-exp:  (m, s) = (max_c m_c, sum_c s_c 2^(m_c - m)),  a = (m + log2 s) ln 2
@@ -15,16 +15,34 @@
 namespace kred {
 namespace {
 
+// Four lanes per output element: lane q of a group sums the blocks c = q,
+// q + 4, q + 8, ... in increasing order (four loads in flight), and the group
+// then adds its four sums as (s0 + s1) + (s2 + s3).  The order is fixed, so
+// results repeat run to run; the group's lanes share t and leave the loop
+// together, so the shuffles see the whole group.
 __global__ __launch_bounds__(256) void combine_sum_kernel(CombineArgs a) {
   const int Ec = min(a.EP, a.E - a.e0);
   const int64_t total = a.M * Ec;
-  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
-       t += (int64_t)gridDim.x * blockDim.x) {
+  const int q = threadIdx.x & 3;
+  const int64_t st = a.M * a.EP;   // floats between consecutive blocks
+  for (int64_t t = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 2; t < total;
+       t += ((int64_t)gridDim.x * blockDim.x) >> 2) {
     const int64_t row = t / Ec;
     const int e = (int)(t - row * Ec);
+    const float* p = a.part + row * a.EP + e;
     float s = 0.0f;
-    for (int c = 0; c < a.C; ++c) s += a.part[((int64_t)c * a.M + row) * a.EP + e];
-    static_cast<float*>(a.out)[row * a.E + a.e0 + e] = s;
+    int c = q;
+    for (; c + 12 < a.C; c += 16) {
+      const float v0 = p[c * st], v1 = p[(c + 4) * st], v2 = p[(c + 8) * st], v3 = p[(c + 12) * st];
+      s += v0;
+      s += v1;
+      s += v2;
+      s += v3;
+    }
+    for (; c < a.C; c += 4) s += p[c * st];
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    if (q == 0) static_cast<float*>(a.out)[row * a.E + a.e0 + e] = s;
   }
 }
 
@@ -185,7 +203,7 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(combine_vjp_kernel, dim3(grid_for(a.M * a.D)), dim3(256), 0, s, a);
       break;
     default:
-      hipLaunchKernelGGL(combine_sum_kernel, dim3(grid_for(a.M * a.EP)), dim3(256), 0, s, a);
+      hipLaunchKernelGGL(combine_sum_kernel, dim3(grid_for(4 * a.M * a.EP)), dim3(256), 0, s, a);
       break;
   }
   return hipGetLastError();

@@ -18,6 +18,7 @@
 // is large.)  Sums are two-level (a per-tile
 // partial folded into the running total once per tile), which keeps fp32
 // rounding growth near u (sqrt(T) + sqrt(N / T)) instead of u N.
+#include "kred.h"
 #include "kred_internal.h"
 
 #include <cfloat>
@@ -819,20 +820,31 @@ constexpr int rows_for(int formula, int DP, int EP, int KP) {
   return pow2_floor(budget / state > 0 ? budget / state : 1);
 }
 
+// The sums come in two row counts: the default, and 2 rows per thread for
+// small M, where the default's few row blocks would leave CUs idle.
+constexpr int kSmallRows = 2;
+
+template <int F, int DP, int EP>
+void launch_sum_f(const DirectArgs& a, dim3 grid, hipStream_t s) {
+  constexpr int R = rows_for(F, DP, EP, 0);
+  if (R > kSmallRows && a.rows == kSmallRows)
+    hipLaunchKernelGGL((sum_kernel<F, DP, EP, (R > kSmallRows ? kSmallRows : R)>), grid,
+                       dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((sum_kernel<F, DP, EP, R>), grid, dim3(kThreads), 0, s, a);
+}
+
 template <int DP, int EP>
 hipError_t launch_sum_e(const DirectArgs& a, dim3 grid, hipStream_t s) {
   switch (a.formula) {
     case F_GAUSS:
-      hipLaunchKernelGGL((sum_kernel<F_GAUSS, DP, EP, rows_for(F_GAUSS, DP, EP, 0)>), grid,
-                         dim3(kThreads), 0, s, a);
+      launch_sum_f<F_GAUSS, DP, EP>(a, grid, s);
       break;
     case F_LAPLACE:
-      hipLaunchKernelGGL((sum_kernel<F_LAPLACE, DP, EP, rows_for(F_LAPLACE, DP, EP, 0)>), grid,
-                         dim3(kThreads), 0, s, a);
+      launch_sum_f<F_LAPLACE, DP, EP>(a, grid, s);
       break;
     case F_SQDIST:
-      hipLaunchKernelGGL((sum_kernel<F_SQDIST, DP, EP, rows_for(F_SQDIST, DP, EP, 0)>), grid,
-                         dim3(kThreads), 0, s, a);
+      launch_sum_f<F_SQDIST, DP, EP>(a, grid, s);
       break;
     default:
       return hipErrorInvalidValue;
@@ -940,6 +952,18 @@ int direct_rows_per_thread(int formula, int DP, int EP, int KP) {
   return rows_for(formula, DP, EP, KP);
 }
 
+int direct_sum_rows(int formula, int DP, int EP, int KP, int ext, int64_t M, int64_t N,
+                    int num_cus) {
+  const int R = ext ? rows_for(F_SQDIST, DP, EP, 0) : rows_for(formula, DP, EP, KP);
+  const bool sum = !ext && KP == 0 &&
+                   (formula == F_GAUSS || formula == F_LAPLACE || formula == F_SQDIST);
+  if (!sum || R <= kSmallRows) return R;
+  // the default grid's work items at the largest useful column split
+  const int64_t rb = (M + (int64_t)kThreads * R - 1) / ((int64_t)kThreads * R);
+  const int64_t cmax = std::max<int64_t>(1, std::min<int64_t>(KRED_MAX_COL_BLOCKS, N / 128));
+  return rb * cmax < 4 * (int64_t)num_cus ? kSmallRows : R;
+}
+
 int partial_width(int formula, int DP, int EP, int KP, int ext) {
   if (KP > 0) return 2 * KP;
   if (ext) return 2 * EP;
@@ -1024,8 +1048,9 @@ hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s) {
 }
 
 int direct_rows_for(const DirectArgs& a) {
-  return a.ext ? direct_rows_per_thread(F_SQDIST, a.DP, a.EP, 0)
-               : direct_rows_per_thread(a.formula, a.DP, a.EP, a.KP);
+  const int R = a.ext ? direct_rows_per_thread(F_SQDIST, a.DP, a.EP, 0)
+                      : direct_rows_per_thread(a.formula, a.DP, a.EP, a.KP);
+  return (a.rows == kSmallRows && R > kSmallRows) ? kSmallRows : R;
 }
 
 hipError_t launch_direct(const DirectArgs& a, hipStream_t s) {

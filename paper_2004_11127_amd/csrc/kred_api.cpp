@@ -58,6 +58,7 @@ struct Plan {
   int64_t jpb;    // j per column block
   int S_max;      // widest packed row over the E-slices
   int W_max;      // widest partial row
+  int R;          // rows per thread of the direct kernels (first E-slice)
   int64_t pack_bytes, part_bytes;
   float xscale, bscale, gscale;
   float kscale;   // direct kernels: pair scale (input coordinates)
@@ -102,8 +103,8 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
   const int EP_first = (r == KRED_R_ARGKMIN) ? 1 : direct_pad_e(std::min(q.E, 16));
   q.S_max = q.DP + EP_first;
   q.W_max = partial_width(kf, q.DP, EP_first, q.KP, ext);
-  const int R = ext ? direct_rows_per_thread(F_SQDIST, q.DP, EP_first, 0)
-                    : direct_rows_per_thread(kf, q.DP, EP_first, q.KP);
+  const int R = direct_sum_rows(kf, q.DP, EP_first, q.KP, ext, M, N, num_cus);
+  q.R = R;
   const int64_t rows = rows_override > 0 ? rows_override : (int64_t)kThreads * R;
   const int64_t row_blocks = (M + rows - 1) / rows;
   q.C = choose_col_blocks(std::max<int64_t>(1, row_blocks), N, num_cus, p->col_blocks);
@@ -542,9 +543,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     if (pr.col_blocks == 0) {
       Plan probe;
       if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &probe)) return KRED_ERR_UNSUPPORTED;
-      const int EP0 = (r == KRED_R_ARGKMIN) ? 1 : direct_pad_e(std::min(16, probe.E));
-      const int R0 = ext ? direct_rows_per_thread(F_SQDIST, probe.DP, EP0, 0)
-                         : direct_rows_per_thread(kf, probe.DP, EP0, probe.KP);
+      const int R0 = probe.R;
       const int epi0 = fast_epi(f, r, M, N, D, E, p->flags, p->K);
       const int64_t rpb = epi0 >= 0 ? fast_rows_per_block(epi0) : (int64_t)kThreads * R0;
       const int64_t est = std::max<int64_t>({1, (int64_t)rg->nr, (M + rpb - 1) / rpb});
@@ -664,6 +663,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     da.part = part;
     da.KP = pl.KP;
     da.K = pl.K;
+    da.rows = pl.R;
     da.guard = guard;
     da.ext = ext;
     da.ext_sign = is_max(r) ? -1.0f : 1.0f;

@@ -94,6 +94,7 @@ struct DirectArgs {
   void* out;              // final output (C == 1)
   float* part;            // partials (C > 1), C x M x W
   int KP, K;              // arg-K-min list length (power of two) and K
+  int rows;               // rows per thread of the sums (0: the kernel's default)
   const FastGuard* guard; // non-null: skip when the fast path is selected
   const float* xe;        // F_VJP: row cotangent e, M x E (this call reads its E-slice)
   int accumulate;         // F_VJP with C == 1: add to out instead of storing (E-slices after the first)
@@ -118,6 +119,10 @@ hipError_t launch_range_blocks(const int* rr, int nr, int64_t M, int rows_per_bl
 // Workgroups a block-sparse launch needs at most (disjoint row ranges).
 int64_t range_grid_bound(int nr, int64_t M, int rows_per_block);
 int direct_rows_per_thread(int formula, int DP, int EP, int KP);
+// Rows per thread for a direct-form call: the default, or 2 for a plain sum
+// whose default grid would leave CUs idle (small M).
+int direct_sum_rows(int formula, int DP, int EP, int KP, int ext, int64_t M, int64_t N,
+                    int num_cus);
 int direct_rows_for(const DirectArgs& a);   // rows per lane launch_direct uses for these args
 int direct_pad_d(int D);      // DP for a given D, 0 if the direct path has none
 int direct_pad_e(int E);      // EP for one E-slice

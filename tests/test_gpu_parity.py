@@ -427,3 +427,19 @@ def test_fast_path_deterministic(ctx):
     l1 = host(ctx.run("sinkhorn", "lse", x, y, b, eps=0.01, flags=F))
     l2 = host(ctx.run("sinkhorn", "lse", x, y, b, eps=0.01, flags=F))
     np.testing.assert_array_equal(l1, l2)
+
+
+@pytest.mark.parametrize("formula,E", [("gauss", 1), ("laplace", 3), ("sqdist", 16)])
+def test_direct_sum_both_row_counts(ctx, formula, E):
+    # the direct sums run 2 rows per thread when the default grid would leave
+    # CUs idle (small M) and their default row count otherwise; both must agree
+    # with the oracle (sampled rows at the larger size)
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(31 + E)
+    for M, N in ((3000, 4000), (60000, 20000)):
+        x = _pts(rng, M, 3); y = _pts(rng, N, 3)
+        b = rng.standard_normal((N, E)).astype(np.float32)
+        out = host(ctx.run(formula, "sum", dev(x), dev(y), dev(b), sigma=0.1, flags=kred.FLAG_DIRECT))
+        rows = np.sort(rng.choice(M, 300, replace=False))
+        ref, norm = oracle.kernel_sum(formula, x, y, b, sigma=0.1, rows=rows)
+        assert norm_err(out[rows], ref, norm) <= SUM_TOL
