@@ -114,19 +114,23 @@ constexpr int tile_cols(int DP) {
   return (4608 / (DP + 4)) >= 64 ? 64 : ((4608 / (DP + 4)) >= 32 ? 32 : 16);
 }
 
+// Insert (d, j) into the ascending list (dk, jk) of KP entries; equal
+// distances keep the earlier entry first (columns arrive in index order).
+// Entry p becomes dk[p-1] (d moves in above it), d (it lands here) or stays:
+// that is the median of (dk[p-1], d, dk[p]) for a sorted list, one v_med3;
+// the indices follow the same two comparisons, each made once.
 template <int KP>
 __device__ __forceinline__ void list_insert(float (&dk)[KP], int (&jk)[KP], float d, int j) {
+  bool lt[KP];
+#pragma unroll
+  for (int p = 0; p < KP; ++p) lt[p] = d < dk[p];
 #pragma unroll
   for (int p = KP - 1; p > 0; --p) {
-    const bool shift = d < dk[p - 1];
-    const bool here = !shift && d < dk[p];
-    dk[p] = shift ? dk[p - 1] : (here ? d : dk[p]);
-    jk[p] = shift ? jk[p - 1] : (here ? j : jk[p]);
+    dk[p] = __builtin_amdgcn_fmed3f(dk[p - 1], d, dk[p]);
+    jk[p] = lt[p - 1] ? jk[p - 1] : (lt[p] ? j : jk[p]);
   }
-  if (d < dk[0]) {
-    dk[0] = d;
-    jk[0] = j;
-  }
+  dk[0] = lt[0] ? d : dk[0];
+  jk[0] = lt[0] ? j : jk[0];
 }
 
 // ------------------------------------------------------------ work items
