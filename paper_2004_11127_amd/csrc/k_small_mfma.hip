@@ -116,7 +116,8 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
     if (j < a.N) {
       float v[3] = {0.f, 0.f, 0.f};
       float nv = 0.0f;
-      const float sg = a.epi == FAST_MIN ? -1.0f : 1.0f;   // MIN: T = +|u - v|^2
+      const bool nearest = a.epi == FAST_MIN || a.epi == FAST_KNN;
+      const float sg = nearest ? -1.0f : 1.0f;   // MIN, KNN: T = +|u - v|^2
 #pragma unroll
       for (int d = 0; d < 3; ++d)
         if (d < a.D) {
@@ -133,7 +134,7 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
         }
       split3(-sg * nv, s[18], s[19], s[20]);
       s[21] = s[22] = s[23] = (__bf16)1.0f;
-      const float bj = a.epi == FAST_MIN ? 0.0f : a.b[j];   // MIN reads no b
+      const float bj = nearest ? 0.0f : a.b[j];   // MIN and KNN read no b
       if (a.epi == FAST_LSE) {
         split3(bj * kLog2e, s[24], s[25], s[26]);
       } else if (a.epi == FAST_GRADX) {
@@ -180,12 +181,46 @@ __device__ __forceinline__ bf16x8 row_operand(const float (&u)[3], int D, int g,
   return o;
 }
 
+// Insert (d, j) into the ascending list (dk, jk): entries arrive in column
+// order, so equal distances keep the earlier entry first.  Entry p becomes
+// dk[p-1], d or itself: the median of (dk[p-1], d, dk[p]) for a sorted list.
+template <int KL>
+__device__ __forceinline__ void list_insert(float (&dk)[KL], int (&jk)[KL], float d, int j) {
+  bool lt[KL];
+#pragma unroll
+  for (int p = 0; p < KL; ++p) lt[p] = d < dk[p];
+#pragma unroll
+  for (int p = KL - 1; p > 0; --p) {
+    dk[p] = __builtin_amdgcn_fmed3f(dk[p - 1], d, dk[p]);
+    jk[p] = lt[p - 1] ? jk[p - 1] : (lt[p] ? j : jk[p]);
+  }
+  dk[0] = lt[0] ? d : dk[0];
+  jk[0] = lt[0] ? j : jk[0];
+}
+
+// The same, ordered by (distance, index): for merging lists of different lanes.
+template <int KL>
+__device__ __forceinline__ void list_insert_lex(float (&dk)[KL], int (&jk)[KL], float d, int j) {
+  bool lt[KL];
+#pragma unroll
+  for (int p = 0; p < KL; ++p) lt[p] = d < dk[p] || (d == dk[p] && j < jk[p]);
+#pragma unroll
+  for (int p = KL - 1; p > 0; --p) {
+    dk[p] = lt[p - 1] ? dk[p - 1] : (lt[p] ? d : dk[p]);
+    jk[p] = lt[p - 1] ? jk[p - 1] : (lt[p] ? j : jk[p]);
+  }
+  dk[0] = lt[0] ? d : dk[0];
+  jk[0] = lt[0] ? j : jk[0];
+}
+
 // EPI: FAST_SUM (Gauss, E = 1), FAST_GRADX, FAST_LSE.
 
-// KV (FAST_MIN): write the distance (else the index).
-template <int EPI, int RB, bool KV = false>
+// KV (FAST_MIN): write the distance (else the index).  KL (FAST_KNN): the
+// length of each lane's sorted list.
+template <int EPI, int RB, bool KV = false, int KL = 1>
 __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   constexpr bool kLse = EPI == FAST_LSE;
+  constexpr bool kKnn = EPI == FAST_KNN;
   constexpr bool kMin = EPI == FAST_MIN;
   __shared__ uint4 As[2][TJF * 4];
   __shared__ float4 Xs[2][EPI == FAST_GRADX ? TJF : 1];   // (b, b v) per column
@@ -236,7 +271,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
 #pragma unroll
     for (int d = 0; d < 3; ++d)
       ur[rb][d] = (row < row_end && d < a.D) ? (a.x[row * a.D + d] - fr.m[d]) * a.scale : 0.0f;
-    xb[rb] = row_operand(ur[rb], a.D, g, kLse, kMin);
+    xb[rb] = row_operand(ur[rb], a.D, g, kLse, kMin || kKnn);
   }
   // per lane: sums over its columns (4 g + r of every block) for row li;
   // MIN: the smallest distance (as its int bits, exact order for d >= 0) and its column
@@ -246,6 +281,35 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
     best[rb] = INT_MAX;
     bidx[rb] = INT_MAX;
   }
+  // KNN: per lane and row block a sorted list of (distance, column) over the
+  // lane's columns, and the row's shared filter (see refresh_filter)
+  float dk[RB][KL];
+  int jk[RB][KL];
+  float thr[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    thr[rb] = __builtin_inff();
+#pragma unroll
+    for (int p = 0; p < KL; ++p) {
+      dk[rb][p] = __builtin_inff();
+      jk[rb][p] = INT_MAX;
+    }
+  }
+  // Any value with at least KL of the row's candidates at or below it bounds
+  // the row's K-th nearest here (K <= KL): the smaller of the 4 lane groups'
+  // smallest KL-th value and their largest ceil(KL/4)-th value.  Ties pass.
+  auto refresh_filter = [&]() {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      float v = dk[rb][KL - 1];
+      v = fminf(v, __shfl_xor(v, 16));
+      v = fminf(v, __shfl_xor(v, 32));
+      float u = dk[rb][(KL + 3) / 4 - 1];
+      u = fmaxf(u, __shfl_xor(u, 16));
+      u = fmaxf(u, __shfl_xor(u, 32));
+      thr[rb] = fminf(v, u);
+    }
+  };
   float acc[RB][4], tot[RB][4], mref[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
@@ -282,7 +346,9 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   };
   // Stream the columns [j0, j1) in tiles.  Columns past j1 load as zero rows,
   // which add nothing to the sums; the log-sum-exp masks them explicitly.
-  auto run_columns = [&](int64_t j0, int64_t jend) {
+  // (always inlined: it is called from two sites, and an outlined copy would
+  // keep the per-lane lists and sums in scratch memory)
+  auto run_columns = [&](int64_t j0, int64_t jend) __attribute__((always_inline)) {
     j1 = jend;
     const int64_t jlim = min(j1, a.N);
     const int64_t ntiles = (j1 - j0 + TJF - 1) / TJF;
@@ -296,7 +362,36 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
       const int buf = (int)(t & 1);
       const int nblk = (int)((min((int64_t)TJF, j1 - jt) + 15) / 16);
       if (t + 1 < ntiles) fetch(jt + TJF);
-      if constexpr (kMin) {
+      if constexpr (kKnn) {
+        refresh_filter();
+        // the lane's 4 distances of each row block; columns past the range
+        // (the last block's zero A rows) read as +infinity.  All products and
+        // filter tests come before the first branch.
+        for (int blk = 0; blk < nblk; ++blk) {
+          const bf16x8 am = a_operand(buf, blk);
+          const int64_t jb = jt + blk * 16 + 4 * g;
+          const int64_t room = jlim - jb;   // per lane: a select, not a branch, after the MFMA
+          float dd[RB][4];
+          bool any[RB];
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dd[rb][r] = r < room ? T[r] : __builtin_inff();
+          }
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            any[rb] = fminf(fminf(dd[rb][0], dd[rb][1]), fminf(dd[rb][2], dd[rb][3])) <= thr[rb];
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            if (__builtin_expect(any[rb], 0)) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (dd[rb][r] < dk[rb][KL - 1]) list_insert<KL>(dk[rb], jk[rb], dd[rb][r], (int)(jb + r));
+            }
+          }
+        }
+      } else if constexpr (kMin) {
         // d for the lane's columns 4g + r of each block.  Full blocks first,
         // then the range's last block if columns past its end (zero A rows,
         // d = 0) must be masked; each MFMA is followed by straight-line
@@ -460,12 +555,70 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
     }
   }
 
+  // KNN: lane group 0 merges the other groups' lists into its own, by
+  // (distance, index) so that ties across groups keep the lower index; every
+  // lane takes part in the shuffles.  The lists come in by reference, so that
+  // every index is a compile-time constant (a runtime row-block index would
+  // put them in scratch memory).
+  auto knn_out = [&](const float (&dl)[KL], const int (&jl)[KL], int64_t row, bool live_row)
+      __attribute__((always_inline)) {
+    float md[16];
+    int mj[16];
+#pragma unroll
+    for (int p = 0; p < 16; ++p) {
+      md[p] = __builtin_inff();
+      mj[p] = INT_MAX;
+    }
+#pragma unroll
+    for (int p = 0; p < KL; ++p) {
+      md[p] = dl[p];
+      mj[p] = jl[p];
+    }
+#pragma unroll
+    for (int src = 16; src <= 48; src += 16) {
+#pragma unroll
+      for (int p = 0; p < KL; ++p) {
+        const float d2 = __shfl(dl[p], li + src);
+        const int j2 = __shfl(jl[p], li + src);
+        if (g == 0) list_insert_lex<16>(md, mj, d2, j2);
+      }
+    }
+    if (g == 0 && live_row) {
+      if (a.C == 1) {
+#pragma unroll
+        for (int p = 0; p < 16; ++p) {
+          if (p >= a.K) break;
+          if (a.kvalues) static_cast<float*>(a.out)[row * a.K + p] = mj[p] == INT_MAX ? __builtin_inff() : fmaxf(md[p], 0.0f);
+          else static_cast<int*>(a.out)[row * a.K + p] = mj[p] == INT_MAX ? -1 : mj[p];
+        }
+      } else {
+        float* q = a.part + ((int64_t)c * a.M + row) * (2 * a.KP);   // the direct kernel's list layout
+#pragma unroll
+        for (int p = 0; p < 16; ++p) {
+          if (p >= a.KP) break;
+          q[2 * p] = md[p];
+          q[2 * p + 1] = __int_as_float(mj[p]);
+        }
+      }
+    }
+  };
+
+  // KNN (two row blocks): the merge unrolled by hand, so that the lists are
+  // indexed by constants only
+  if constexpr (kKnn) {
+    static_assert(RB == 2, "the K-nearest epilogue runs two row blocks per wave");
+    knn_out(dk[0], jk[0], i0 + li, i0 + li < row_end);
+    knn_out(dk[1], jk[1], i0 + 16 + li, i0 + 16 + li < row_end);
+  }
+
   // merge the four lane groups of each row (lanes li, li+16, li+32, li+48)
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int64_t row = i0 + 16 * rb + li;
     const bool live_row = row < row_end;
-    if constexpr (kMin) {
+    if constexpr (kKnn) {
+      // (written out below, outside this loop)
+    } else if constexpr (kMin) {
       // smallest (distance, index) over the four lane groups; ties keep the lower index
       int v = best[rb], j = bidx[rb];
 #pragma unroll
@@ -547,7 +700,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
 
 }  // namespace
 
-int fast_rows_per_block(int epi) { return 64 * 4; }
+int fast_rows_per_block(int epi) { return epi == FAST_KNN ? 64 * 2 : 64 * 4; }
 
 hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M, hipStream_t s) {
   FastGuard* g = const_cast<FastGuard*>(a.guard);   // the prologue fills the guard
@@ -572,6 +725,15 @@ hipError_t launch_fast(const FastArgs& a, hipStream_t s) {
     case FAST_MIN:
       if (a.kvalues) hipLaunchKernelGGL((fast_kernel<FAST_MIN, 4, true>), grid, dim3(256), 0, s, a);
       else hipLaunchKernelGGL((fast_kernel<FAST_MIN, 4, false>), grid, dim3(256), 0, s, a);
+      break;
+    case FAST_KNN:
+      // two row blocks per wave: the lists hold 2 KL registers per row block
+      if (a.K <= 4) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 2, false, 4>), grid, dim3(256), 0, s, a);
+      else if (a.K <= 8) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 2, false, 8>), grid, dim3(256), 0, s, a);
+      else if (a.K <= 10) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 2, false, 10>), grid, dim3(256), 0, s, a);
+      else if (a.K <= 12) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 2, false, 12>), grid, dim3(256), 0, s, a);
+      else if (a.K <= 16) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 2, false, 16>), grid, dim3(256), 0, s, a);
+      else return hipErrorInvalidValue;
       break;
     default: return hipErrorInvalidValue;
   }

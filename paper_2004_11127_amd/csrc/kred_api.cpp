@@ -171,6 +171,7 @@ int fast_epi(kred_formula f, kred_reduction r, int64_t M, int64_t N, int32_t D, 
   if ((f == KRED_F_SINKHORN || f == KRED_F_GAUSS) && r == KRED_R_LSE) return FAST_LSE;
   // nearest neighbour: arg-K-min with K = 1, and the distance's min / arg-min
   if (f == KRED_F_SQDIST && r == KRED_R_ARGKMIN && K == 1) return FAST_MIN;
+  if (f == KRED_F_SQDIST && r == KRED_R_ARGKMIN && K > 1 && K <= 16) return FAST_KNN;
   return -1;
 }
 
@@ -610,6 +611,8 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     fa.out = out;
     fa.part = part;
     fa.kvalues = kvalues;
+    fa.K = pl.K;
+    fa.KP = pl.KP;
     if (rg) {
       fa.nr = rg->nr;
       fa.rr = rg->rr;

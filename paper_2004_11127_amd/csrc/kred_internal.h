@@ -24,7 +24,8 @@ constexpr float kLn2 = 0.6931471805599453f;
 // fast kernels run only when c R^2 <= kFastLimit (R the half-diagonal of the
 // box in prescaled units), otherwise the direct-form kernels do the work.
 // Both are launched; each returns at once when the other one is selected.
-enum : int { FAST_SUM = 0, FAST_GRADX = 1, FAST_LSE = 2, FAST_MIN = 3 };   // MIN: nearest distance / index
+// MIN: nearest distance / index; KNN: the K nearest (1 < K <= 16)
+enum : int { FAST_SUM = 0, FAST_GRADX = 1, FAST_LSE = 2, FAST_MIN = 3, FAST_KNN = 4 };
 constexpr float kFastLimit = 2048.0f;
 
 struct FastGuard {
@@ -260,7 +261,8 @@ struct FastArgs {
   const float* eb;
   void* out;
   float* part;
-  int kvalues;        // FAST_MIN: write the distance (else the index)
+  int kvalues;        // FAST_MIN, FAST_KNN: write the distances (else the indices)
+  int K, KP;          // FAST_KNN: K, and the list length of the output / partial layout
   // block-sparse pattern (nr > 0), as in DirectArgs; bstart counts row
   // blocks of fast_rows_per_block rows
   int nr;

@@ -219,3 +219,56 @@ def test_nearest_fast_kernel_is_used_and_falls_back(ctx):
     d = host(ctx.run("sqdist", "min", dev(xs), dev(ys), None, flags=kred.FLAG_FAST))
     val, _, scale = oracle.extreme("sqdist", "min", xs, ys)
     assert (np.abs(d.astype(np.float64) - val) <= TOL * scale).all()
+
+
+FAST_KNN = [
+    # M, N, D, K, C
+    (700, 2049, 3, 4, 3), (3000, 5000, 2, 10, 0), (1500, 999, 1, 16, 16), (257, 4000, 3, 7, 0),
+    (1000, 1500, 3, 12, 1), (64, 64, 3, 16, 0),
+]
+
+
+@pytest.mark.parametrize("M,N,D,K,C", FAST_KNN)
+@pytest.mark.parametrize("red", ["argkmin", "kmin"])
+def test_knn_fast_path_exact(ctx, M, N, D, K, C, red):
+    # D <= 3, 1 < K <= 16 with KRED_FLAG_FAST: distances from the matrix cores (exact on
+    # integer coordinates inside the guard), per-lane lists merged by (distance, index)
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(M + N + D + K + C)
+    x, y = _ints(rng, M, D, -20, 21), _ints(rng, N, D, -20, 21)
+    y[N // 2:N // 2 + N // 8] = y[:N // 8]   # exact ties between columns
+    ctx.profile_collect()
+    out = host(ctx.run("sqdist", red, dev(x), dev(y), None, K=K, col_blocks=C,
+                       flags=kred.FLAG_FAST | kred.FLAG_PROFILE))
+    assert ctx.profile_collect()[2] == "fast_kernel"
+    idx, dist = oracle.argkmin(x, y, K)
+    if red == "argkmin":
+        np.testing.assert_array_equal(out, idx.astype(np.int32))
+    else:
+        np.testing.assert_array_equal(out, dist.astype(np.float32))
+
+
+def test_knn_fast_path_real_data(ctx):
+    # real-valued mixture data: distances within the tolerance, valid indices
+    from paper_2004_11127_amd import inputs, kred
+    w = inputs.mixture_gauss(M=20000, N=30000, D=3, sigma=0.05, seed=4)
+    K = 10
+    idx = host(ctx.run("sqdist", "argkmin", dev(w.x), dev(w.y), None, K=K, flags=kred.FLAG_FAST))
+    kd = host(ctx.run("sqdist", "kmin", dev(w.x), dev(w.y), None, K=K, flags=kred.FLAG_FAST))
+    rows = np.sort(np.random.default_rng(1).choice(20000, 500, replace=False))
+    ridx, rdist = oracle.argkmin(w.x, w.y, K, rows=rows)
+    scale = ((w.x[rows, None, :].astype(np.float64) - w.y[None].astype(np.float64)) ** 2).sum(-1).max(1)
+    allow = TOL * scale[:, None]
+    assert (np.abs(kd[rows].astype(np.float64) - rdist) <= allow).all()
+    got = ((w.x[rows, None, :].astype(np.float64) - w.y[idx[rows]].astype(np.float64)) ** 2).sum(-1)
+    assert (np.abs(got - rdist) <= allow).all()
+    # fp32 and fp64 may order near-ties among the K-th neighbours differently
+    assert (idx[rows] == ridx).mean() > 0.99
+
+
+def test_knn_fast_path_falls_back_on_wide_data(ctx):
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(6)
+    x = _ints(rng, 800, 3, -300, 300); y = _ints(rng, 1200, 3, -300, 300)   # R^2 >> 2048
+    out = host(ctx.run("sqdist", "argkmin", dev(x), dev(y), None, K=6, flags=kred.FLAG_FAST))
+    np.testing.assert_array_equal(out, oracle.argkmin(x, y, 6)[0].astype(np.int32))

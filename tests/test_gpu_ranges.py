@@ -317,3 +317,19 @@ def test_ranges_large_d_full_pattern_matches_dense(ctx):
         dense = host(ctx.run("gauss", "sum", dev(x), dev(y), dev(b), sigma=1.0, col_blocks=1, flags=fl))
         sparse = call(ctx, "gauss", "sum", x, y, b, pat, sigma=1.0, col_blocks=1, flags=fl)
         np.testing.assert_array_equal(sparse, dense)
+
+
+@pytest.mark.parametrize("C", CHUNKS)
+@pytest.mark.parametrize("red,K", [("argkmin", 5), ("kmin", 10), ("argkmin", 16)])
+def test_ranges_knn_fast_path(ctx, red, K, C):
+    # D <= 3 with KRED_FLAG_FAST: the K-nearest lists on the matrix-core distance
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(40 + K)
+    M, N, D = 2500, 3500, 3
+    x = rng.integers(-9, 10, (M, D)).astype(np.float32); y = rng.integers(-9, 10, (N, D)).astype(np.float32)
+    pat = random_pattern(rng, M, N, 9, 22, p_keep=0.2)   # some clusters get fewer than K columns
+    ctx.profile_collect()
+    out = call(ctx, "sqdist", red, x, y, None, pat, K=K, col_blocks=C, flags=kred.FLAG_FAST | kred.FLAG_PROFILE)
+    assert ctx.profile_collect()[2] == "fast_kernel"
+    ref, _ = oracle.ranges_reduce(red, x, y, None, *pat, K=K)
+    np.testing.assert_array_equal(out, ref.astype(out.dtype))
