@@ -555,13 +555,31 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
     }
   }
 
-  // KNN: lane group 0 merges the other groups' lists into its own, by
-  // (distance, index) so that ties across groups keep the lower index; every
-  // lane takes part in the shuffles.  The lists come in by reference, so that
-  // every index is a compile-time constant (a runtime row-block index would
-  // put them in scratch memory).
+  // The expanded form's distance carries an absolute error of about 2^-24 R^2
+  // (R the box's half-diagonal), large against a close neighbour's distance;
+  // it only ranks.  The final candidates get their distance in the direct
+  // form, sum_d (x_d - y_d)^2, which is accurate relative to itself (and
+  // exact on integer coordinates), and are ranked again by it.
+  auto exact_d = [&](int64_t row, int j) __attribute__((always_inline)) {
+    float s = 0.0f;
+#pragma unroll
+    for (int d = 0; d < 3; ++d)
+      if (d < a.D) {
+        const float t = a.x[row * a.D + d] - a.y[(int64_t)j * a.D + d];
+        s = __builtin_fmaf(t, t, s);
+      }
+    return s;
+  };
+
+  // KNN: lane group 0 gathers the four groups' candidates (4 KL per row, each
+  // group's own KL nearest by the expanded form) and keeps the K nearest by
+  // the direct-form distance, ordered by (distance, index) so that ties keep
+  // the lower index; every lane takes part in the shuffles.  The lists come
+  // in by reference, so that every index is a compile-time constant (a
+  // runtime row-block index would put them in scratch memory).
   auto knn_out = [&](const float (&dl)[KL], const int (&jl)[KL], int64_t row, bool live_row)
       __attribute__((always_inline)) {
+    (void)dl;
     float md[16];
     int mj[16];
 #pragma unroll
@@ -570,17 +588,11 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
       mj[p] = INT_MAX;
     }
 #pragma unroll
-    for (int p = 0; p < KL; ++p) {
-      md[p] = dl[p];
-      mj[p] = jl[p];
-    }
-#pragma unroll
-    for (int src = 16; src <= 48; src += 16) {
+    for (int src = 0; src <= 48; src += 16) {
 #pragma unroll
       for (int p = 0; p < KL; ++p) {
-        const float d2 = __shfl(dl[p], li + src);
-        const int j2 = __shfl(jl[p], li + src);
-        if (g == 0) list_insert_lex<16>(md, mj, d2, j2);
+        const int j2 = src == 0 ? jl[p] : __shfl(jl[p], li + src);
+        if (g == 0 && live_row && j2 != INT_MAX) list_insert_lex<16>(md, mj, exact_d(row, j2), j2);
       }
     }
     if (g == 0 && live_row) {
@@ -606,9 +618,13 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   // KNN (two row blocks): the merge unrolled by hand, so that the lists are
   // indexed by constants only
   if constexpr (kKnn) {
-    static_assert(RB == 2, "the K-nearest epilogue runs two row blocks per wave");
+    static_assert(RB == 2 || RB == 4, "the K-nearest epilogue runs 2 or 4 row blocks per wave");
     knn_out(dk[0], jk[0], i0 + li, i0 + li < row_end);
     knn_out(dk[1], jk[1], i0 + 16 + li, i0 + 16 + li < row_end);
+    if constexpr (RB == 4) {
+      knn_out(dk[RB > 2 ? 2 : 0], jk[RB > 2 ? 2 : 0], i0 + 32 + li, i0 + 32 + li < row_end);
+      knn_out(dk[RB > 3 ? 3 : 0], jk[RB > 3 ? 3 : 0], i0 + 48 + li, i0 + 48 + li < row_end);
+    }
   }
 
   // merge the four lane groups of each row (lanes li, li+16, li+32, li+48)
@@ -619,8 +635,13 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
     if constexpr (kKnn) {
       // (written out below, outside this loop)
     } else if constexpr (kMin) {
-      // smallest (distance, index) over the four lane groups; ties keep the lower index
+      // smallest (distance, index) over the four lane groups; ties keep the
+      // lower index.  With indices, each group's candidate gets its
+      // direct-form distance first (see exact_d).
       int v = best[rb], j = bidx[rb];
+      if constexpr (!KV) {
+        if (live_row && j != INT_MAX) v = __float_as_int(fmaxf(exact_d(row, j), 0.0f));
+      }
 #pragma unroll
       for (int o = 16; o <= 32; o <<= 1) {
         const int v2 = __shfl_xor(v, o), j2 = __shfl_xor(j, o);
@@ -700,7 +721,10 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
 
 }  // namespace
 
-int fast_rows_per_block(int epi) { return epi == FAST_KNN ? 64 * 2 : 64 * 4; }
+// Rows per workgroup: four row blocks per wave, except the K-nearest lists
+// beyond 4 entries, which run two (measured at 1e6 x 1e6, D = 3: four row
+// blocks gain at K = 4, 123 -> 112 ms, and lose at K = 10, 132 -> 165 ms).
+int fast_rows_per_block(int epi, int K) { return (epi == FAST_KNN && K > 4) ? 64 * 2 : 64 * 4; }
 
 hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M, hipStream_t s) {
   FastGuard* g = const_cast<FastGuard*>(a.guard);   // the prologue fills the guard
@@ -715,7 +739,7 @@ hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M
 }
 
 hipError_t launch_fast(const FastArgs& a, hipStream_t s) {
-  const int rows = fast_rows_per_block(a.epi);
+  const int rows = fast_rows_per_block(a.epi, a.K);
   const int64_t rb = a.nr > 0 ? range_grid_bound(a.nr, a.M, rows) : (a.M + rows - 1) / rows;
   const dim3 grid((unsigned)(rb * a.C));
   switch (a.epi) {
@@ -727,8 +751,8 @@ hipError_t launch_fast(const FastArgs& a, hipStream_t s) {
       else hipLaunchKernelGGL((fast_kernel<FAST_MIN, 4, false>), grid, dim3(256), 0, s, a);
       break;
     case FAST_KNN:
-      // two row blocks per wave: the lists hold 2 KL registers per row block
-      if (a.K <= 4) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 2, false, 4>), grid, dim3(256), 0, s, a);
+      // row blocks per wave as fast_rows_per_block: the lists hold 2 KL registers each
+      if (a.K <= 4) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 4, false, 4>), grid, dim3(256), 0, s, a);
       else if (a.K <= 8) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 2, false, 8>), grid, dim3(256), 0, s, a);
       else if (a.K <= 10) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 2, false, 10>), grid, dim3(256), 0, s, a);
       else if (a.K <= 12) hipLaunchKernelGGL((fast_kernel<FAST_KNN, 2, false, 12>), grid, dim3(256), 0, s, a);

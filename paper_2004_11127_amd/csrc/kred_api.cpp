@@ -320,6 +320,13 @@ struct Ranges {
   const int* cr;
 };
 
+// Scratch for the bf16 column operand of the large-D kernels: the exact k-NN
+// kernel's copy (DP bf16 per column) or the split kernel's three planes.
+int64_t mfma_bf16_bytes(const MPlan& pl, bool knn, uint32_t flags, int64_t M, int64_t N) {
+  if (!exact_eligible(flags, M, N)) return 0;
+  return align_up(pl.N16 * (knn ? 1 : 3) * pl.DP * (int64_t)sizeof(uint16_t));
+}
+
 kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                      int64_t M, int64_t N, int32_t D, int32_t E, const float* x, const float* y,
                      const float* b, void* out, hipStream_t s, int kvalues,
@@ -344,9 +351,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   // sums: the split bf16 kernel replaces the fp32 one
   const bool exact = knn && exact_eligible(p->flags, M, N);
   const bool split = !knn && exact_eligible(p->flags, M, N);
-  const int64_t ybf_bytes = exact ? align_up(pl.N16 * pl.DP * (int64_t)sizeof(uint16_t))
-                            : split ? align_up(pl.N16 * 3 * pl.DP * (int64_t)sizeof(uint16_t))
-                                    : 0;
+  const int64_t ybf_bytes = mfma_bf16_bytes(pl, knn, p->flags, M, N);
   if (rg) {   // partials of every chunk (rows outside the clusters read the empty value)
     pl.part_bytes = knn ? align_up((int64_t)4 * pl.C * M * 2 * pl.KP * (int64_t)sizeof(float))
                   : pl.C > 1 ? align_up((int64_t)pl.C * M * pl.W * (int64_t)sizeof(float))
@@ -546,7 +551,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
       if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &probe)) return KRED_ERR_UNSUPPORTED;
       const int R0 = probe.R;
       const int epi0 = fast_epi(f, r, M, N, D, E, p->flags, p->K);
-      const int64_t rpb = epi0 >= 0 ? fast_rows_per_block(epi0) : (int64_t)kThreads * R0;
+      const int64_t rpb = epi0 >= 0 ? fast_rows_per_block(epi0, p->K) : (int64_t)kThreads * R0;
       const int64_t est = std::max<int64_t>({1, (int64_t)rg->nr, (M + rpb - 1) / rpb});
       pr.col_blocks = (int)std::min<int64_t>(64, ((int64_t)ctx->num_cus * 16 + est - 1) / est);
     }
@@ -555,7 +560,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   const int epi = fast_epi(f, r, M, N, D, E, p->flags, p->K);
   Plan pl;
   if (!make_plan(f, r, p, M, N, D, E, ctx->num_cus, &pl,
-                 epi >= 0 ? fast_rows_per_block(epi) : 0, epi >= 0 ? 256 : 1))
+                 epi >= 0 ? fast_rows_per_block(epi, p->K) : 0, epi >= 0 ? 256 : 1))
     return KRED_ERR_UNSUPPORTED;
   const FastScratch fs = fast_scratch(epi, N);
   // block-sparse: workgroup maps for the direct kernels and for the fast kernel
@@ -613,13 +618,14 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     fa.kvalues = kvalues;
     fa.K = pl.K;
     fa.KP = pl.KP;
+    fa.y = y;
     if (rg) {
       fa.nr = rg->nr;
       fa.rr = rg->rr;
       fa.cp = rg->cp;
       fa.cr = rg->cr;
       fa.bstart = fbstart;
-      if (launch_range_blocks(rg->rr, rg->nr, M, fast_rows_per_block(epi), fbstart, s) !=
+      if (launch_range_blocks(rg->rr, rg->nr, M, fast_rows_per_block(epi, p->K), fbstart, s) !=
           hipSuccess)
         return KRED_ERR_HIP;
     }
@@ -930,11 +936,12 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
   if (D > kMaxDirectD) {
     MPlan mp;
     if (!make_mplan(f, r, p, M, N, D, E, 256, &mp)) return -1;
-    return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes;
+    return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes +
+           mfma_bf16_bytes(mp, r == KRED_R_ARGKMIN, p->flags, M, N);
   }
   const int epi = fast_epi(f, r, M, N, D, E, p->flags, p->K);
   Plan pl;
-  if (!make_plan(f, r, p, M, N, D, E, 256, &pl, epi >= 0 ? fast_rows_per_block(epi) : 0,
+  if (!make_plan(f, r, p, M, N, D, E, 256, &pl, epi >= 0 ? fast_rows_per_block(epi, p->K) : 0,
                  epi >= 0 ? 256 : 1))
     return -1;
   const FastScratch fs = fast_scratch(epi, N);

@@ -263,6 +263,7 @@ struct FastArgs {
   float* part;
   int kvalues;        // FAST_MIN, FAST_KNN: write the distances (else the indices)
   int K, KP;          // FAST_KNN: K, and the list length of the output / partial layout
+  const float* y;     // FAST_MIN, FAST_KNN: the points (N x D), for the exact final distances
   // block-sparse pattern (nr > 0), as in DirectArgs; bstart counts row
   // blocks of fast_rows_per_block rows
   int nr;
@@ -272,7 +273,7 @@ struct FastArgs {
   const int* bstart;
 };
 hipError_t launch_fast(const FastArgs& a, hipStream_t s);
-int fast_rows_per_block(int epi);
+int fast_rows_per_block(int epi, int K);
 
 // Fill out with a constant (N = 0 cases); a kernel, not a memset, so that
 // callers may capture it in a graph.

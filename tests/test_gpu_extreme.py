@@ -204,6 +204,9 @@ def test_nearest_fast_path_real_data(ctx):
     assert (np.abs(d.astype(np.float64) - val) <= allow).all()
     f = _f_at("sqdist", w.x, w.y, None, j.astype(np.int64), 1.0)
     assert (np.abs(f - val) <= allow).all()
+    # the index comes from re-ranking the four lane groups' candidates by the
+    # direct-form distance: it is the nearest point to fp32 accuracy
+    assert (np.abs(f - val) <= 1e-5 * val + 1e-12).mean() > 0.999
     assert (j == idx).mean() > 0.999
 
 
@@ -257,13 +260,14 @@ def test_knn_fast_path_real_data(ctx):
     kd = host(ctx.run("sqdist", "kmin", dev(w.x), dev(w.y), None, K=K, flags=kred.FLAG_FAST))
     rows = np.sort(np.random.default_rng(1).choice(20000, 500, replace=False))
     ridx, rdist = oracle.argkmin(w.x, w.y, K, rows=rows)
-    scale = ((w.x[rows, None, :].astype(np.float64) - w.y[None].astype(np.float64)) ** 2).sum(-1).max(1)
-    allow = TOL * scale[:, None]
-    assert (np.abs(kd[rows].astype(np.float64) - rdist) <= allow).all()
+    # the matrix cores only rank; the returned distances are direct-form fp32,
+    # accurate relative to themselves (not only to the row's largest distance)
+    rel = 1e-5 * rdist + 1e-12
+    assert (np.abs(kd[rows].astype(np.float64) - rdist) <= rel).all()
     got = ((w.x[rows, None, :].astype(np.float64) - w.y[idx[rows]].astype(np.float64)) ** 2).sum(-1)
-    assert (np.abs(got - rdist) <= allow).all()
+    assert (np.abs(got - rdist) <= rel).all()
     # fp32 and fp64 may order near-ties among the K-th neighbours differently
-    assert (idx[rows] == ridx).mean() > 0.99
+    assert (idx[rows] == ridx).mean() > 0.999
 
 
 def test_knn_fast_path_falls_back_on_wide_data(ctx):
