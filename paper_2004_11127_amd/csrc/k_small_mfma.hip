@@ -275,11 +275,15 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   }
   // per lane: sums over its columns (4 g + r of every block) for row li;
   // MIN: the smallest distance (as its int bits, exact order for d >= 0) and its column
-  int best[RB], bidx[RB];
+  // MIN: per lane its smallest expanded-form distance (int bits) and the tile
+  // [btile, bend) where it last improved; that tile's columns of the lane get
+  // their direct-form distance at the end (see exact_d)
+  int best[RB], btile[RB], bend[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     best[rb] = INT_MAX;
-    bidx[rb] = INT_MAX;
+    btile[rb] = INT_MAX;
+    bend[rb] = 0;
   }
   // KNN: per lane and row block a sorted list of (distance, column) over the
   // lane's columns, and the row's shared filter (see refresh_filter)
@@ -398,16 +402,11 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
         // reads of its result, with no branch in between.
         const bool ragged = jt + 16 * nblk > jlim;
         const int nfull = ragged ? nblk - 1 : nblk;
+        int before[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) before[rb] = best[rb];
         auto take = [&](int rb, int64_t jb, const int (&d)[4]) {
-          const int m4 = min(min(min(d[0], d[1]), d[2]), d[3]);
-          if constexpr (KV) {
-            best[rb] = min(best[rb], m4);
-          } else if (__builtin_expect(m4 < best[rb], 0)) {
-            // strictly smaller: the lowest r reaching it (columns come in increasing j)
-            const int r = d[0] == m4 ? 0 : (d[1] == m4 ? 1 : (d[2] == m4 ? 2 : 3));
-            best[rb] = m4;
-            bidx[rb] = (int)(jb + r);
-          }
+          best[rb] = min(best[rb], min(min(min(d[0], d[1]), d[2]), d[3]));
         };
         for (int blk = 0; blk < nfull; ++blk) {
           const bf16x8 am = a_operand(buf, blk);
@@ -433,6 +432,14 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
                               jb + 3 < jlim ? __float_as_int(T[3]) : INT_MAX};
             take(rb, jb, d);
           }
+        }
+        // a strictly smaller value in this tile: remember the tile (the
+        // earliest such tile keeps ties)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const bool lt = best[rb] < before[rb];
+          btile[rb] = lt ? (int)jt : btile[rb];
+          bend[rb] = lt ? (int)min(jt + TJF, jlim) : bend[rb];
         }
       } else if constexpr (!kLse) {
         // Padding columns have zero extras, so they add nothing: no masking.
@@ -560,12 +567,16 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   // it only ranks.  The final candidates get their distance in the direct
   // form, sum_d (x_d - y_d)^2, which is accurate relative to itself (and
   // exact on integer coordinates), and are ranked again by it.
-  auto exact_d = [&](int64_t row, int j) __attribute__((always_inline)) {
+  auto load_row = [&](int64_t row, bool live_row, float (&xr)[3]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int d = 0; d < 3; ++d) xr[d] = (live_row && d < a.D) ? a.x[row * a.D + d] : 0.0f;
+  };
+  auto exact_d = [&](const float (&xr)[3], int j) __attribute__((always_inline)) {
     float s = 0.0f;
 #pragma unroll
     for (int d = 0; d < 3; ++d)
       if (d < a.D) {
-        const float t = a.x[row * a.D + d] - a.y[(int64_t)j * a.D + d];
+        const float t = xr[d] - a.y[(int64_t)j * a.D + d];
         s = __builtin_fmaf(t, t, s);
       }
     return s;
@@ -580,6 +591,8 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   auto knn_out = [&](const float (&dl)[KL], const int (&jl)[KL], int64_t row, bool live_row)
       __attribute__((always_inline)) {
     (void)dl;
+    float xr[3];
+    load_row(row, live_row, xr);
     float md[16];
     int mj[16];
 #pragma unroll
@@ -592,7 +605,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
 #pragma unroll
       for (int p = 0; p < KL; ++p) {
         const int j2 = src == 0 ? jl[p] : __shfl(jl[p], li + src);
-        if (g == 0 && live_row && j2 != INT_MAX) list_insert_lex<16>(md, mj, exact_d(row, j2), j2);
+        if (g == 0 && live_row && j2 != INT_MAX) list_insert_lex<16>(md, mj, exact_d(xr, j2), j2);
       }
     }
     if (g == 0 && live_row) {
@@ -638,9 +651,23 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
       // smallest (distance, index) over the four lane groups; ties keep the
       // lower index.  With indices, each group's candidate gets its
       // direct-form distance first (see exact_d).
-      int v = best[rb], j = bidx[rb];
-      if constexpr (!KV) {
-        if (live_row && j != INT_MAX) v = __float_as_int(fmaxf(exact_d(row, j), 0.0f));
+      int v = INT_MAX, j = INT_MAX;
+      if (live_row && btile[rb] != INT_MAX) {
+        float xr[3];
+        load_row(row, true, xr);
+        // the lane's columns 4 g + r of each block of that tile, in column order
+        for (int jb = btile[rb] + 4 * g; jb < bend[rb]; jb += 16) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int jr = jb + r;
+            if (jr >= bend[rb]) break;
+            const int vr = __float_as_int(exact_d(xr, jr));   // >= 0: int order is float order
+            if (vr < v) {
+              v = vr;
+              j = jr;
+            }
+          }
+        }
       }
 #pragma unroll
       for (int o = 16; o <= 32; o <<= 1) {

@@ -204,9 +204,10 @@ def test_nearest_fast_path_real_data(ctx):
     assert (np.abs(d.astype(np.float64) - val) <= allow).all()
     f = _f_at("sqdist", w.x, w.y, None, j.astype(np.int64), 1.0)
     assert (np.abs(f - val) <= allow).all()
-    # the index comes from re-ranking the four lane groups' candidates by the
-    # direct-form distance: it is the nearest point to fp32 accuracy
+    # values and indices come from re-ranking candidates by the direct-form
+    # distance: the nearest point and its distance to fp32 accuracy
     assert (np.abs(f - val) <= 1e-5 * val + 1e-12).mean() > 0.999
+    assert (np.abs(d.astype(np.float64) - val) <= 1e-5 * val + 1e-12).mean() > 0.999
     assert (j == idx).mean() > 0.999
 
 
