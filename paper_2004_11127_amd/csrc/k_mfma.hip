@@ -133,6 +133,23 @@ __device__ __forceinline__ void list_insert(float (&dk)[KP], int (&jk)[KP], floa
   jk[0] = lt[0] ? j : jk[0];
 }
 
+// The exact kernel's lists hold (d, j) as one fp64 key d 2^28 + j: d is an
+// integer with |d| < 2^24 and 0 <= j < 2^28, so the key is exact and orders
+// as (d, j).  Insertion runs from the top down, in place: entry p becomes
+// min(old p, max(old p-1, key)), two fp64 operations and no comparison.
+constexpr double kKeyScale = 268435456.0;   // 2^28
+constexpr double kKeyInv = 1.0 / 268435456.0;
+
+template <int KP>
+__device__ __forceinline__ void key_insert(double (&kk)[KP], double key) {
+#pragma unroll
+  for (int p = KP - 1; p > 0; --p) kk[p] = __builtin_fmin(kk[p], __builtin_fmax(kk[p - 1], key));
+  kk[0] = __builtin_fmin(kk[0], key);
+}
+
+// the distance part of a key (+infinity stays +infinity)
+__device__ __forceinline__ float key_d(double key) { return (float)__builtin_floor(key * kKeyInv); }
+
 // ------------------------------------------------------------ work items
 // A workgroup's work: dense, a (row block, column block) pair; block-sparse,
 // a row block inside row cluster I and chunk c of I's columns, the chunk
@@ -514,7 +531,7 @@ __global__ __launch_bounds__(256) void exact_check_kernel(const float* __restric
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int bf16_tile_cols(int DP) { return DP <= 128 ? 64 : 32; }
+constexpr int bf16_tile_cols(int DP) { return DP <= 64 ? 128 : (DP <= 128 ? 64 : 32); }
 
 // Arg-K-min on the bf16 matrix cores, for data the guard has shown to be
 // exact there: T[j][i] = ny_j + sum_d (-2 y_jd) x_id with one
@@ -561,15 +578,16 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
       }
   }
 
-  float dk[RB][KP];
-  int jk[RB][KP];
+  // per row block the lane's sorted keys (see key_insert) and the distance
+  // part of its last one
+  double kk[RB][KP];
+  float dlast[RB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
+  for (int rb = 0; rb < RB; ++rb) {
+    dlast[rb] = __builtin_inff();
 #pragma unroll
-    for (int p = 0; p < KP; ++p) {
-      dk[rb][p] = __builtin_inff();
-      jk[rb][p] = INT_MAX;
-    }
+    for (int p = 0; p < KP; ++p) kk[rb][p] = __builtin_inf();
+  }
 
   // Filter shared by the 4 lanes of a row (each lists its own quarter of the
   // columns): any value with at least KP of the row's candidates at or below
@@ -623,10 +641,10 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
     if (t + 1 < ntiles) fetch(jt + TJ, a0, a1);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      float v = dk[rb][KP - 1];
+      float v = dlast[rb];
       v = fminf(v, __shfl_xor(v, 16));
       v = fminf(v, __shfl_xor(v, 32));
-      float u = dk[rb][(KP + 3) / 4 - 1];
+      float u = key_d(kk[rb][(KP + 3) / 4 - 1]);
       u = fmaxf(u, __shfl_xor(u, 16));
       u = fmaxf(u, __shfl_xor(u, 32));
       thr[rb] = fminf(v, u);
@@ -658,9 +676,14 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
       for (int rb = 0; rb < RB; ++rb) {
         if (__builtin_expect(any[rb], 0)) {
           const int jb = (int)(jt + blk * 16 + 4 * g);
+          // columns arrive in index order, so a distance equal to the last
+          // entry's loses the tie
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            if (acc[rb][r] < dk[rb][KP - 1]) list_insert<KP>(dk[rb], jk[rb], acc[rb][r], jb + r);
+            if (acc[rb][r] < dlast[rb]) {
+              key_insert<KP>(kk[rb], __builtin_fma((double)acc[rb][r], kKeyScale, (double)(jb + r)));
+              dlast[rb] = key_d(kk[rb][KP - 1]);
+            }
         }
       }
     }
@@ -689,8 +712,11 @@ __global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
     float* q = a.part + (((int64_t)c * 4 + g) * a.M + row) * (2 * KP);
 #pragma unroll
     for (int p = 0; p < KP; ++p) {
-      q[2 * p] = dk[rb][p] + part;
-      q[2 * p + 1] = __int_as_float(jk[rb][p]);
+      const double key = kk[rb][p];
+      const double d = __builtin_floor(key * kKeyInv);
+      const bool empty = key == __builtin_inf();
+      q[2 * p] = empty ? __builtin_inff() : (float)d + part;
+      q[2 * p + 1] = __int_as_float(empty ? INT_MAX : (int)(key - d * kKeyScale));
     }
   }
 }

@@ -184,6 +184,11 @@ bool exact_eligible(uint32_t flags, int64_t M, int64_t N) {
   return (flags & KRED_FLAG_FAST) || (double)M * (double)N >= kFastMinPairs;
 }
 
+// the exact k-NN kernel's list keys hold column indices below 2^28
+bool exact_knn_eligible(uint32_t flags, int64_t M, int64_t N) {
+  return exact_eligible(flags, M, N) && N <= ((int64_t)1 << 28);
+}
+
 struct FastScratch {
   int64_t guard_bytes, apk_bytes, ex_bytes;
 };
@@ -323,7 +328,7 @@ struct Ranges {
 // Scratch for the bf16 column operand of the large-D kernels: the exact k-NN
 // kernel's copy (DP bf16 per column) or the split kernel's three planes.
 int64_t mfma_bf16_bytes(const MPlan& pl, bool knn, uint32_t flags, int64_t M, int64_t N) {
-  if (!exact_eligible(flags, M, N)) return 0;
+  if (!(knn ? exact_knn_eligible(flags, M, N) : exact_eligible(flags, M, N))) return 0;
   return align_up(pl.N16 * (knn ? 1 : 3) * pl.DP * (int64_t)sizeof(uint16_t));
 }
 
@@ -349,7 +354,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   const bool knn = (r == KRED_R_ARGKMIN);
   // arg-K-min: the exact bf16 kernel is a candidate (the device decides);
   // sums: the split bf16 kernel replaces the fp32 one
-  const bool exact = knn && exact_eligible(p->flags, M, N);
+  const bool exact = knn && exact_knn_eligible(p->flags, M, N);
   const bool split = !knn && exact_eligible(p->flags, M, N);
   const int64_t ybf_bytes = mfma_bf16_bytes(pl, knn, p->flags, M, N);
   if (rg) {   // partials of every chunk (rows outside the clusters read the empty value)
