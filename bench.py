@@ -76,10 +76,19 @@ WORKLOADS = {
     "sparse": ("mixture_gauss", dict(M=1_000_000, N=1_000_000, D=3, sigma=0.05), "gauss", "sum",
                11, "alu", "block-sparse gaussian kernel sum (grid clusters of side 2 sigma, "
                           "truncation at 6 sigma), mixture of 8 Gaussians, 1e6 x 1e6, D=3"),
+    # its backward: the x, y and b gradients of L = sum_i <e_i, a_i> over the kept
+    # pairs (x from the row clusters, y and b from the same blocks seen from the
+    # column clusters)
+    "sparse_backward": ("mixture_gauss", dict(M=1_000_000, N=1_000_000, D=3, sigma=0.05),
+                        "backward", None, 17 + 17 + 11, "alu",
+                        "block-sparse gaussian backward (x, y, b gradients, scalar cotangent; "
+                        "grid clusters of side 2 sigma, truncation at 6 sigma), mixture of 8 "
+                        "Gaussians, 1e6 x 1e6, D=3"),
 }
 SPARSE_CELL, SPARSE_CUTOFF = 2.0, 6.0   # in units of sigma
+SPARSE = ("sparse", "sparse_backward")
 # the three reductions of a backward step: (rows, columns) = (M, N), (N, M), (N, M)
-REDUCTIONS_PER_STEP = {"backward": 3, "backward_e16": 3}
+REDUCTIONS_PER_STEP = {"backward": 3, "backward_e16": 3, "sparse_backward": 3}
 LIST_K = {"knn3": 10}   # K of the arg-K-min workloads drawn by a generator without one
 KERNEL_SOURCES = {"sum_kernel": "k_direct.hip", "gradx_kernel": "k_direct.hip",
                   "lse_kernel": "k_direct.hip", "knn_kernel": "k_direct.hip",
@@ -159,6 +168,8 @@ def sparse_pattern(w):
     pat = clusters.truncation_pattern(w.x, w.y, SPARSE_CELL * w.sigma, SPARSE_CUTOFF * w.sigma)
     w.x = w.x[pat["order_x"]].copy(); w.y = w.y[pat["order_y"]].copy()
     w.b = w.b[pat["order_y"]].copy()
+    pat["transposed"] = clusters.transpose_pattern(pat["row_ranges"], pat["col_ptr"],
+                                                   pat["col_ranges"], w.M, w.N)
     return pat
 
 
@@ -171,7 +182,16 @@ def time_steps(ctx, w, formula, reduction, steps, warmup, pattern=None):
     if formula == "sqdist" and reduction in ("min", "argkmin"):
         b = None   # reductions of the bare squared distance
     stream = torch.cuda.current_stream()
-    if pattern is not None:
+    if pattern is not None and formula == "backward":
+        e = torch.from_numpy(cotangent(w)).cuda()
+        fwd = tuple(torch.from_numpy(pattern[k]).cuda() for k in ("row_ranges", "col_ptr",
+                                                                  "col_ranges"))
+        tr = tuple(torch.from_numpy(a).cuda() for a in pattern["transposed"])
+
+        def call(flags):
+            return ctx.gauss_backward_ranges(x, y, b, e, fwd, tr, sigma=w.sigma, flags=flags,
+                                             stream=stream)
+    elif pattern is not None:
         rr, cp, cr = (torch.from_numpy(pattern[k]).cuda() for k in ("row_ranges", "col_ptr",
                                                                      "col_ranges"))
         kw = dict(sigma=w.sigma, eps=w.eps, K=w.K)
@@ -220,20 +240,41 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds, pattern=None):
 
     oracle.build()
 
+    def clustered(rows, rr, cp, cr, ncols, reduce, width):
+        # the sampled rows' clusters, each reduced over its pattern columns;
+        # rows in no cluster hold zero
+        cl = np.searchsorted(rr[:, 1], rows, side="right")
+        inside = cl < len(rr)
+        inside[inside] &= rows[inside] >= rr[cl[inside], 0]
+        val = np.zeros((len(rows), width)); nrm = np.zeros_like(val)
+        for I in np.unique(cl[inside]):
+            sel = inside & (cl == I)
+            cols = oracle._cluster_columns(cp, cr, I, ncols)
+            if cols.size:
+                v, n = reduce(rows[sel], cols)
+                val[sel] = v; nrm[sel] = n
+        return val, nrm
+
     def run(rows):
+        if pattern is not None and formula == "backward":
+            # gx of the sampled rows over their clusters' columns; gy and gb of
+            # the same indices as columns, over their column clusters' rows
+            e = cotangent(w)
+            gx = clustered(rows, pattern["row_ranges"], pattern["col_ptr"], pattern["col_ranges"],
+                           w.N, lambda r, c: oracle.gauss_vjp(w.x[r], w.y[c], w.b[c], e[r],
+                                                              w.sigma), w.D)
+            cc, rp, rt = pattern["transposed"]
+            clustered(rows, cc, rp, rt, w.M,
+                      lambda r, c: oracle.gauss_vjp(w.y[r], w.x[c], e[c], w.b[r], w.sigma), w.D)
+            clustered(rows, cc, rp, rt, w.M,
+                      lambda r, c: oracle.kernel_sum("gauss", w.y[r], w.x[c], e[c], sigma=w.sigma),
+                      w.E)
+            return gx
         if pattern is not None:
-            # the sampled rows' clusters, each reduced over its pattern columns
-            rr = pattern["row_ranges"]
-            cl = np.searchsorted(rr[:, 1], rows, side="right")
-            val = np.zeros((len(rows), 1)); nrm = np.zeros((len(rows), 1))
-            for I in np.unique(cl):
-                sel = cl == I
-                cols = oracle._cluster_columns(pattern["col_ptr"], pattern["col_ranges"], I, w.N)
-                if cols.size:
-                    v, n = oracle.kernel_sum("gauss", w.x[rows[sel]], w.y[cols], w.b[cols],
-                                             sigma=w.sigma)
-                    val[sel] = v; nrm[sel] = n
-            return val, nrm
+            return clustered(rows, pattern["row_ranges"], pattern["col_ptr"],
+                             pattern["col_ranges"], w.N,
+                             lambda r, c: oracle.kernel_sum("gauss", w.x[r], w.y[c], w.b[c],
+                                                            sigma=w.sigma), w.E)
         if formula == "backward":
             # the three reductions of a step on the same sampled row indices
             e = cotangent(w)
@@ -285,7 +326,7 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds, pattern=None):
                          " for each of the 3 gradients" if red > 1 else "", t),
                seconds=t)
     res.update(check)
-    if pattern is not None:
+    if pattern is not None and formula != "backward":
         # what the truncation drops: the block-sparse result against the dense sum
         few = rows[:: max(1, len(rows) // 64)]
         dense, dn = oracle.kernel_sum("gauss", w.x[few], w.y, w.b, sigma=w.sigma)
@@ -309,7 +350,7 @@ def main():
     w = getattr(inputs, gen)(seed=0, **gkw)
     if args.workload in LIST_K:
         w.K = LIST_K[args.workload]
-    pattern = sparse_pattern(w) if args.workload == "sparse" else None
+    pattern = sparse_pattern(w) if args.workload in SPARSE else None
     pairs = (float(pattern["pairs"]) if pattern is not None else float(w.M) * float(w.N)) \
         * REDUCTIONS_PER_STEP.get(args.workload, 1)
     with kred.Context(0) as ctx:

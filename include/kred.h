@@ -261,6 +261,52 @@ kred_status kred_validate_backward(const kred_params* p, int64_t M, int64_t N, i
                                    const void* gb);
 
 /*
+ * Gradients of the block-sparse Gaussian sum (Sec. 2 "Backpropagation" with
+ * the cluster-wise block-sparsity of Sec. 3): a_i = sum_{j in S(i)} k_ij b_j,
+ * S(i) the column ranges of row i's cluster as in kred_run_ranges, and the
+ * gradients of L = sum_i <e_i, a_i> as in kred_gauss_backward restricted to
+ * the kept pairs:
+ *   gx[i] = sum_{j in S(i)} k_ij <e_i, b_j> (y_j - x_i) / sigma^2
+ *   gy[j] = sum_{i : j in S(i)} k_ij <e_i, b_j> (x_i - y_j) / sigma^2
+ *   gb[j] = sum_{i : j in S(i)} k_ij e_i
+ * gx reduces over rows with the row-cluster pattern (nr, row_ranges,
+ * col_ptr, col_ranges: exactly kred_run_ranges's arrays).  gy and gb reduce
+ * over columns, so they take the same block set from the columns' side:
+ * column cluster J = 0..nc-1 is the columns [col_clusters[2J],
+ * col_clusters[2J+1]), and its columns sum over the rows of the ranges
+ * [row_ranges_t[2q], row_ranges_t[2q+1]) for q in [row_ptr[J], row_ptr[J+1]).
+ * The caller keeps the two patterns consistent (the same (i, j) pairs;
+ * clusters.transpose_pattern in the Python package builds one from the
+ * other); otherwise gy and gb are the gradients of another mask.  Columns
+ * in no cluster get zero gy and gb, rows in no cluster zero gx.
+ *
+ * All index arrays are int32 device arrays with the rules of
+ * kred_run_ranges (disjoint clusters, clamping to [0, M) and [0, N)); a
+ * pattern's arrays may be NULL when its count is 0 or when the outputs it
+ * serves are not requested.  Parameters, outputs, errors and asynchrony as
+ * kred_gauss_backward (1 <= D <= 16; E-slices and col_blocks as there, the
+ * column split applying to each cluster's ranges).
+ */
+kred_status kred_gauss_backward_ranges(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N,
+                                       int32_t D, int32_t E, const float* x, const float* y,
+                                       const float* b, const float* e, float* gx, float* gy,
+                                       float* gb, int32_t nr, const int32_t* row_ranges,
+                                       const int32_t* col_ptr, const int32_t* col_ranges,
+                                       int32_t nc, const int32_t* col_clusters,
+                                       const int32_t* row_ptr, const int32_t* row_ranges_t,
+                                       void* stream);
+
+/* Host-only argument check of kred_gauss_backward_ranges (the index arrays
+ * are only checked for null and alignment). */
+kred_status kred_validate_backward_ranges(const kred_params* p, int64_t M, int64_t N, int32_t D,
+                                          int32_t E, const void* x, const void* y, const void* b,
+                                          const void* e, const void* gx, const void* gy,
+                                          const void* gb, int32_t nr, const void* row_ranges,
+                                          const void* col_ptr, const void* col_ranges, int32_t nc,
+                                          const void* col_clusters, const void* row_ptr,
+                                          const void* row_ranges_t);
+
+/*
  * With KRED_FLAG_PROFILE set on calls, the context records a HIP event pair
  * around the main reduction kernel of each call.  This waits for those
  * events, returns the number of timed launches in *count and their summed

@@ -329,3 +329,40 @@ def ranges_reduce(kind, x, y, b, row_ranges, col_ptr, col_ranges, **kw):
             v, i, _ = extreme(formula, kind, xs, ys, bs, param=kw.get("param", 1.0))
             out[r0:r1] = v; aux[r0:r1] = cols[i]
     return out, aux
+
+
+def ranges_backward(x, y, b, e, sigma, row_ranges, col_ptr, col_ranges):
+    """Gradients of L = sum_i <e_i, a_i> for the block-sparse Gaussian sum.
+
+    a_i = sum_{j in S(i)} k_ij b_j with S(i) the column ranges of row i's
+    cluster (Sec. 3's cluster-wise block-sparsity); the derivative of such a
+    reduction is again one of the same form (Sec. 2, "Backpropagation"), taken
+    over the kept pairs only.  Built from the row-cluster pattern alone: each
+    cluster's gathered block goes through the dense routines, its y- and
+    b-gradients scattered back onto its columns.  Returns
+    (gx, nx, gy, ny, gb, nb): the gradients and their normalisers (sums of
+    absolute summands); rows and columns outside the pattern get zeros.
+    """
+    x = np.asarray(x, dtype=np.float64); y = np.asarray(y, dtype=np.float64)
+    M, D = x.shape
+    N = y.shape[0]
+    b = np.asarray(b, dtype=np.float64).reshape(N, -1)
+    E = b.shape[1]
+    e = np.asarray(e, dtype=np.float64).reshape(M, E)
+    gx = np.zeros((M, D)); nx = np.zeros((M, D))
+    gy = np.zeros((N, D)); ny = np.zeros((N, D))
+    gb = np.zeros((N, E)); nb = np.zeros((N, E))
+    for I in range(len(row_ranges)):
+        r0 = min(max(int(row_ranges[I][0]), 0), M)
+        r1 = min(max(int(row_ranges[I][1]), r0), M)
+        cols = _cluster_columns(col_ptr, col_ranges, I, N)
+        if r1 <= r0 or cols.size == 0:
+            continue
+        xs, es, ys, bs = x[r0:r1], e[r0:r1], y[cols], b[cols]
+        g, n = gauss_vjp(xs, ys, bs, es, sigma)
+        gx[r0:r1] += g; nx[r0:r1] += n
+        g, n = gauss_vjp(ys, xs, es, bs, sigma)
+        np.add.at(gy, cols, g); np.add.at(ny, cols, n)
+        g, n = kernel_sum("gauss", ys, xs, es, sigma=sigma)
+        np.add.at(gb, cols, g); np.add.at(nb, cols, n)
+    return gx, nx, gy, ny, gb, nb

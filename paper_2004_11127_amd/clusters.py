@@ -10,7 +10,10 @@ such a pattern with numpy (setup work, outside the GPU hot path):
 * sort_by_labels: the permutation making each cluster contiguous, and its ranges;
 * truncation_pattern: for each cluster of x, the ranges of the clusters of y
   whose cell centres lie within a cutoff distance (plus the cell diagonal,
-  so that no pair of points closer than the cutoff is dropped).
+  so that no pair of points closer than the cutoff is dropped);
+* transpose_pattern: the same block set seen from the columns (column
+  clusters, each with its row ranges), which the gradients in y and b of a
+  block-sparse reduction sum over.
 
 For a kernel that decays like the Gaussian exp(-|x - y|^2 / (2 sigma^2)), a
 cutoff of c sigma drops only terms below exp(-c^2 / 2) of the largest.
@@ -95,3 +98,54 @@ def truncation_pattern(x, y, cell, cutoff):
     return dict(order_x=ox, order_y=oy, row_ranges=rx.astype(np.int32),
                 col_ptr=np.asarray(ptr, dtype=np.int32),
                 col_ranges=np.asarray(col, dtype=np.int32).reshape(-1, 2), pairs=pairs)
+
+
+def transpose_pattern(row_ranges, col_ptr, col_ranges, M, N):
+    """The column-side view of a row-cluster pattern (kred_run_ranges's arrays).
+
+    Returns int32 arrays (col_clusters (nc x 2), row_ptr (nc + 1), row_ranges_t
+    (nnz x 2)) for kred_gauss_backward_ranges: column cluster J is the columns
+    [col_clusters[J, 0], col_clusters[J, 1]) and its columns pair with the rows
+    of row_ranges_t[row_ptr[J] : row_ptr[J + 1]], which are exactly the row
+    clusters listing those columns.  Ranges are clamped to [0, M) x [0, N);
+    row clusters must be disjoint.  Column clusters are the pieces between all
+    range end points, merged where neighbours pair with the same rows; columns
+    no row cluster lists belong to no column cluster.
+    """
+    rows = []   # (js, je, r0, r1) of every non-empty block
+    for I in range(len(row_ranges)):
+        r0 = min(max(int(row_ranges[I][0]), 0), M)
+        r1 = min(max(int(row_ranges[I][1]), r0), M)
+        if r1 <= r0:
+            continue
+        for q in range(int(col_ptr[I]), int(col_ptr[I + 1])):
+            js = min(max(int(col_ranges[q][0]), 0), N)
+            je = min(max(int(col_ranges[q][1]), js), N)
+            if je > js:
+                rows.append((js, je, r0, r1))
+    cuts = np.unique(np.array([v for blk in rows for v in blk[:2]], dtype=np.int64))
+    lists = [[] for _ in range(max(len(cuts) - 1, 0))]
+    for js, je, r0, r1 in rows:
+        for k in range(int(np.searchsorted(cuts, js)), int(np.searchsorted(cuts, je))):
+            lists[k].append((r0, r1))
+    clusters, ptr, rr = [], [0], []
+    prev = None
+    for k, lst in enumerate(lists):
+        if not lst:
+            prev = None
+            continue
+        merged = []
+        for r0, r1 in sorted(lst):
+            if merged and merged[-1][1] == r0:
+                merged[-1][1] = r1
+            else:
+                merged.append([r0, r1])
+        if prev is not None and prev == merged and clusters[-1][1] == int(cuts[k]):
+            clusters[-1][1] = int(cuts[k + 1])   # same rows as the piece before: extend it
+            continue
+        clusters.append([int(cuts[k]), int(cuts[k + 1])])
+        rr.extend(merged)
+        ptr.append(len(rr))
+        prev = merged
+    return (np.asarray(clusters, dtype=np.int32).reshape(-1, 2),
+            np.asarray(ptr, dtype=np.int32), np.asarray(rr, dtype=np.int32).reshape(-1, 2))

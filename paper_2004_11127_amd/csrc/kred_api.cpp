@@ -758,29 +758,55 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
 // on validated arguments with M, N > 0.  With one signal column and the
 // matrix-core path eligible, the fused value + gradient reduction runs and its
 // gradient is scaled by the scalar cotangent; otherwise the direct-form
-// vector-Jacobian kernel runs once per E-slice of 16.
+// vector-Jacobian kernel runs once per E-slice of 16.  With a block-sparse
+// pattern rg the sums run over each row cluster's column ranges only, and
+// rows outside every cluster get zero.
 kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, int32_t D,
                     int32_t E, const float* x, const float* y, const float* b, const float* e,
-                    float* g, hipStream_t s) {
+                    float* g, hipStream_t s, const Ranges* rg = nullptr) {
   if (E == 1 && fast_epi(KRED_F_GAUSS_GRADX, KRED_R_SUM, M, N, D, 1, p->flags) >= 0) {
     const kred_status ga =
         grow_buffer(&ctx->aux, &ctx->aux_bytes, (size_t)(M * (1 + D) * (int64_t)sizeof(float)));
     if (ga != KRED_OK) return ga;
     float* fused = static_cast<float*>(ctx->aux);
+    if (rg && launch_fill(fused, M * (1 + D), 0.0f, s) != hipSuccess) return KRED_ERR_HIP;
     const kred_status st =
-        run_reduction(ctx, KRED_F_GAUSS_GRADX, KRED_R_SUM, p, M, N, D, 1, x, y, b, fused, s);
+        run_reduction(ctx, KRED_F_GAUSS_GRADX, KRED_R_SUM, p, M, N, D, 1, x, y, b, fused, s, rg);
     if (st != KRED_OK) return st;
     return launch_scale_rows(fused, M, D, e, g, s) == hipSuccess ? KRED_OK : KRED_ERR_HIP;
+  }
+  kred_params pr;
+  if (rg) {
+    pr = *p;
+    if (pr.col_blocks == 0) {
+      // chunks of each cluster's columns, as for the block-sparse reductions
+      Plan probe;
+      if (!make_plan((kred_formula)F_VJP, KRED_R_SUM, p, M, N, D, E, ctx->num_cus, &probe))
+        return KRED_ERR_UNSUPPORTED;
+      const int64_t rpb = (int64_t)kThreads * probe.R;
+      const int64_t est = std::max<int64_t>({1, (int64_t)rg->nr, (M + rpb - 1) / rpb});
+      pr.col_blocks = (int)std::min<int64_t>(64, ((int64_t)ctx->num_cus * 16 + est - 1) / est);
+    }
+    p = &pr;
   }
   Plan pl;
   if (!make_plan((kred_formula)F_VJP, KRED_R_SUM, p, M, N, D, E, ctx->num_cus, &pl))
     return KRED_ERR_UNSUPPORTED;
-  const kred_status gs = grow_scratch(ctx, (size_t)(pl.pack_bytes + pl.part_bytes));
+  const int64_t bstart_bytes = rg ? align_up((int64_t)(rg->nr + 1) * (int64_t)sizeof(int)) : 0;
+  const kred_status gs = grow_scratch(ctx, (size_t)(pl.pack_bytes + pl.part_bytes + bstart_bytes));
   if (gs != KRED_OK) return gs;
   char* sbase = static_cast<char*>(ctx->scratch);
   float* ypk = reinterpret_cast<float*>(sbase);
   float* part = pl.part_bytes ? reinterpret_cast<float*>(sbase + pl.pack_bytes) : nullptr;
+  int* bstart = rg ? reinterpret_cast<int*>(sbase + pl.pack_bytes + pl.part_bytes) : nullptr;
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
+  if (rg) {
+    // rows outside every cluster: zero output, and zero partials, which the
+    // kernels never write for them
+    if (launch_fill(g, M * D, 0.0f, s) != hipSuccess) return KRED_ERR_HIP;
+    if (pl.C > 1 && launch_fill2(part, (int64_t)pl.C * M * pl.DP, 0.0f, 0.0f, s) != hipSuccess)
+      return KRED_ERR_HIP;
+  }
   const int n_slices = (E + 15) / 16;
   for (int sl = 0; sl < n_slices; ++sl) {
     const int e0 = sl * 16;
@@ -819,6 +845,19 @@ kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, i
     da.part = part;
     da.xe = e;
     da.accumulate = sl > 0;
+    if (rg) {
+      da.nr = rg->nr;
+      da.rr = rg->rr;
+      da.cp = rg->cp;
+      da.cr = rg->cr;
+      da.bstart = bstart;
+      // the workgroup map depends on the rows per lane, which depend on the
+      // slice's width: rebuilt per slice (stream order keeps the previous
+      // slice's kernel ahead of the rewrite)
+      if (launch_range_blocks(rg->rr, rg->nr, M, kThreads * direct_rows_for(da), bstart, s) !=
+          hipSuccess)
+        return KRED_ERR_HIP;
+    }
     hipEvent_t e_start = nullptr, e_stop = nullptr;
     if (prof) {
       e_start = next_event(ctx);
@@ -1085,6 +1124,69 @@ kred_status kred_gauss_backward(kred_ctx* ctx, const kred_params* p, int64_t M, 
     st = M == 0 ? (launch_fill(gb, N * E, 0.0f, s) == hipSuccess ? KRED_OK : KRED_ERR_HIP)
                 : run_reduction(ctx, KRED_F_GAUSS, KRED_R_SUM, p, N, M, D, E, y, x, e, gb, s);
     if (st != KRED_OK) return st;
+  }
+  return KRED_OK;
+}
+
+kred_status kred_validate_backward_ranges(const kred_params* p, int64_t M, int64_t N, int32_t D,
+                                          int32_t E, const void* x, const void* y, const void* b,
+                                          const void* e, const void* gx, const void* gy,
+                                          const void* gb, int32_t nr, const void* row_ranges,
+                                          const void* col_ptr, const void* col_ranges, int32_t nc,
+                                          const void* col_clusters, const void* row_ptr,
+                                          const void* row_ranges_t) {
+  const kred_status v = kred_validate_backward(p, M, N, D, E, x, y, b, e, gx, gy, gb);
+  if (v != KRED_OK) return v;
+  if (nr < 0 || nc < 0) return KRED_ERR_INVALID_ARG;
+  // the row-cluster pattern serves gx, the column-cluster pattern gy and gb
+  if (gx && nr > 0 && (row_ranges == nullptr || col_ptr == nullptr || col_ranges == nullptr))
+    return KRED_ERR_INVALID_ARG;
+  if ((gy || gb) && nc > 0 &&
+      (col_clusters == nullptr || row_ptr == nullptr || row_ranges_t == nullptr))
+    return KRED_ERR_INVALID_ARG;
+  for (const void* q : {row_ranges, col_ptr, col_ranges, col_clusters, row_ptr, row_ranges_t})
+    if (misaligned(q)) return KRED_ERR_INVALID_ARG;
+  return KRED_OK;
+}
+
+kred_status kred_gauss_backward_ranges(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N,
+                                       int32_t D, int32_t E, const float* x, const float* y,
+                                       const float* b, const float* e, float* gx, float* gy,
+                                       float* gb, int32_t nr, const int32_t* row_ranges,
+                                       const int32_t* col_ptr, const int32_t* col_ranges,
+                                       int32_t nc, const int32_t* col_clusters,
+                                       const int32_t* row_ptr, const int32_t* row_ranges_t,
+                                       void* stream) {
+  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
+  const kred_status v = kred_validate_backward_ranges(
+      p, M, N, D, E, x, y, b, e, gx, gy, gb, nr, row_ranges, col_ptr, col_ranges, nc,
+      col_clusters, row_ptr, row_ranges_t);
+  if (v != KRED_OK) return v;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  DeviceGuard devg(ctx->device);
+  if (!devg.ok) return KRED_ERR_HIP;
+  kred_status st = KRED_OK;
+  const Ranges fwd{nr, row_ranges, col_ptr, col_ranges};
+  const Ranges tr{nc, col_clusters, row_ptr, row_ranges_t};
+  // dL/dx_i over row i's cluster columns
+  if (gx && M > 0) {
+    st = (N == 0 || nr == 0) ? (launch_fill(gx, M * D, 0.0f, s) == hipSuccess ? KRED_OK : KRED_ERR_HIP)
+                             : run_vjp(ctx, p, M, N, D, E, x, y, b, e, gx, s, &fwd);
+    if (st != KRED_OK) return st;
+  }
+  // dL/dy_j over the rows of column j's cluster, roles of (x, e) and (y, b) exchanged
+  if (gy && N > 0) {
+    st = (M == 0 || nc == 0) ? (launch_fill(gy, N * D, 0.0f, s) == hipSuccess ? KRED_OK : KRED_ERR_HIP)
+                             : run_vjp(ctx, p, N, M, D, E, y, x, e, b, gy, s, &tr);
+    if (st != KRED_OK) return st;
+  }
+  // dL/db_j = sum over the same rows of k_ij e_i
+  if (gb && N > 0) {
+    if (launch_fill(gb, N * E, 0.0f, s) != hipSuccess) return KRED_ERR_HIP;
+    if (M > 0 && nc > 0) {
+      st = run_reduction(ctx, KRED_F_GAUSS, KRED_R_SUM, p, N, M, D, E, y, x, e, gb, s, &tr);
+      if (st != KRED_OK) return st;
+    }
   }
   return KRED_OK;
 }

@@ -69,12 +69,18 @@ def load():
                                         vp, vp, vp, vp, i32, vp, vp, vp, vp]
         lib.kred_validate_ranges.argtypes = [ctypes.c_int, ctypes.c_int, pp, i64, i64, i32, i32,
                                              vp, vp, vp, vp, i32, vp, vp, vp]
+        lib.kred_gauss_backward_ranges.argtypes = [vp, pp, i64, i64, i32, i32, vp, vp, vp, vp,
+                                                   vp, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp,
+                                                   vp]
+        lib.kred_validate_backward_ranges.argtypes = [pp, i64, i64, i32, i32, vp, vp, vp, vp, vp,
+                                                      vp, vp, i32, vp, vp, vp, i32, vp, vp, vp]
         lib.kred_strerror.argtypes = [ctypes.c_int]
         lib.kred_strerror.restype = ctypes.c_char_p
         lib.kred_version.restype = i32
         for f in (lib.kred_create, lib.kred_destroy, lib.kred_run, lib.kred_validate,
                   lib.kred_gauss_backward, lib.kred_validate_backward, lib.kred_run_ranges,
-                  lib.kred_validate_ranges, lib.kred_profile_collect):
+                  lib.kred_validate_ranges, lib.kred_gauss_backward_ranges,
+                  lib.kred_validate_backward_ranges, lib.kred_profile_collect):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -122,6 +128,15 @@ def validate_backward(M, N, D, E, x=16, y=16, b=16, e=16, gx=16, gy=16, gb=16, *
     p = make_params(**params)
     return load().kred_validate_backward(ctypes.byref(p), int(M), int(N), int(D), int(E),
                                          x, y, b, e, gx, gy, gb)
+
+
+def validate_backward_ranges(M, N, D, E, nr, nc, x=16, y=16, b=16, e=16, gx=16, gy=16, gb=16,
+                             rr=16, cp=16, cr=16, cc=16, rp=16, rt=16, **params):
+    """Host-only argument check of the block-sparse backward (pointers as plain integers)."""
+    p = make_params(**params)
+    return load().kred_validate_backward_ranges(ctypes.byref(p), int(M), int(N), int(D), int(E),
+                                                x, y, b, e, gx, gy, gb, int(nr), rr, cp, cr,
+                                                int(nc), cc, rp, rt)
 
 
 def validate_ranges(formula, reduction, M, N, D, E, nr, x=16, y=16, b=16, out=16, rr=16, cp=16,
@@ -195,6 +210,18 @@ class Context:
             raise TypeError("%s must be a contiguous %s tensor" % (name, dtype))
         return t.data_ptr() if t.numel() else None
 
+    def _idx_ptr(self, t, name):
+        """Device pointer of an int32 index array; an empty one (a pattern with no
+        ranges) gets a small zeroed buffer of the context's device, never read, so
+        that the library sees a valid pointer."""
+        import torch
+        ptr = self._dev_ptr(t, name, torch.int32)
+        if ptr is None and t is not None:
+            if getattr(self, "_empty_idx", None) is None:
+                self._empty_idx = torch.zeros(4, dtype=torch.int32, device=t.device)
+            ptr = self._empty_idx.data_ptr()
+        return ptr
+
     def run_ranges(self, formula, reduction, x, y, b, row_ranges, col_ptr, col_ranges, out=None,
                    sigma=1.0, eps=1.0, K=0, col_blocks=0, flags=0, stream=None):
         """Block-sparse reduction (kred_run_ranges): row cluster I = rows
@@ -246,17 +273,29 @@ class Context:
             nr = rr.shape[0]
             if tuple(cp.shape) != (nr + 1,) or rr.dim() != 2 or rr.shape[1] != 2:
                 raise ValueError("row_ranges must be (nr, 2) and col_ptr (nr + 1,)")
-            i32 = torch.int32
-            st = load().kred_run_ranges(*args, nr, self._dev_ptr(rr, "row_ranges", i32),
-                                        self._dev_ptr(cp, "col_ptr", i32),
-                                        self._dev_ptr(cr, "col_ranges", i32), s)
+            st = load().kred_run_ranges(*args, nr, self._idx_ptr(rr, "row_ranges"),
+                                        self._idx_ptr(cp, "col_ptr"),
+                                        self._idx_ptr(cr, "col_ranges"), s)
         if st != 0:
             raise KredError(st, "kred_run(%s, %s, M=%d, N=%d, D=%d, E=%d)" % (formula, reduction,
                                                                              M, N, D, E))
         return out
 
+    def gauss_backward_ranges(self, x, y, b, e, pattern, transposed, sigma=1.0, gx=True,
+                              gy=True, gb=True, col_blocks=0, flags=0, stream=None):
+        """Gradients of the block-sparse Gaussian sum (kred_gauss_backward_ranges).
+
+        pattern = (row_ranges, col_ptr, col_ranges) as for run_ranges, serving gx;
+        transposed = (col_clusters, row_ptr, row_ranges_t), the same block set seen
+        from the columns (clusters.transpose_pattern builds it), serving gy and gb.
+        Index arrays are int32 GPU tensors; otherwise as gauss_backward.
+        """
+        return self.gauss_backward(x, y, b, e, sigma=sigma, gx=gx, gy=gy, gb=gb,
+                                   col_blocks=col_blocks, flags=flags, stream=stream,
+                                   _ranges=(pattern, transposed))
+
     def gauss_backward(self, x, y, b, e, sigma=1.0, gx=True, gy=True, gb=True, col_blocks=0,
-                       flags=0, stream=None):
+                       flags=0, stream=None, _ranges=None):
         """Gradients of L = sum_i <e_i, a_i> for the Gaussian sum a = K b.
 
         x (M, D), y (N, D), b (N, E), e (M, E): contiguous float32 on the context's
@@ -287,11 +326,22 @@ class Context:
         p = make_params(sigma, 1.0, 0, col_blocks, flags)
         s = (stream if stream is not None else torch.cuda.current_stream(x.device)).cuda_stream
         f32 = torch.float32
-        st = load().kred_gauss_backward(self._h, ctypes.byref(p), M, N, D, E,
-                                        self._dev_ptr(x, "x", f32), self._dev_ptr(y, "y", f32),
-                                        self._dev_ptr(b2, "b", f32), self._dev_ptr(e2, "e", f32),
-                                        self._dev_ptr(ox, "gx", f32), self._dev_ptr(oy, "gy", f32),
-                                        self._dev_ptr(ob, "gb", f32), s)
+        args = (self._h, ctypes.byref(p), M, N, D, E,
+                self._dev_ptr(x, "x", f32), self._dev_ptr(y, "y", f32),
+                self._dev_ptr(b2, "b", f32), self._dev_ptr(e2, "e", f32),
+                self._dev_ptr(ox, "gx", f32), self._dev_ptr(oy, "gy", f32),
+                self._dev_ptr(ob, "gb", f32))
+        if _ranges is None:
+            st = load().kred_gauss_backward(*args, s)
+        else:
+            pat = []
+            for (a0, a1, a2), name in zip(_ranges, ("pattern", "transposed")):
+                n = a0.shape[0]
+                if a0.dim() != 2 or a0.shape[1] != 2 or tuple(a1.shape) != (n + 1,):
+                    raise ValueError("%s: clusters must be (n, 2) and the pointer (n + 1,)" % name)
+                pat += [n, self._idx_ptr(a0, name), self._idx_ptr(a1, name),
+                        self._idx_ptr(a2, name)]
+            st = load().kred_gauss_backward_ranges(*args, *pat, s)
         if st != 0:
             raise KredError(st, "kred_gauss_backward(M=%d, N=%d, D=%d, E=%d)" % (M, N, D, E))
         return ox, oy, ob

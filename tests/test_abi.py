@@ -232,3 +232,27 @@ def test_ranges_validation(lib):
     assert VR("gauss", "lse", 100, 200, 17, 1, 5, sigma=1.0) == UNSUPPORTED
     assert VR("gauss", "sum", 100, 200, 257, 1, 5, sigma=1.0) == INVALID        # as kred_run
     assert VR("gauss", "sum", 100, 200, 3, 1, 5, sigma=0.0) == INVALID         # as kred_run
+
+
+def test_backward_ranges_validation(lib):
+    VBR = kred.validate_backward_ranges
+    assert {"kred_gauss_backward_ranges", "kred_validate_backward_ranges"} <= set(kred.header_symbols())
+    p = kred.make_params(sigma=1.0)
+    assert lib.kred_gauss_backward_ranges(None, ctypes.byref(p), 4, 4, 3, 1, 16, 16, 16, 16, 16, 16,
+                                          16, 1, 16, 16, 16, 1, 16, 16, 16, None) == INVALID
+    assert VBR(100, 200, 3, 1, 5, 7, sigma=0.1) == OK
+    assert VBR(100, 200, 16, 40, 5, 7, sigma=0.1) == OK
+    # a pattern's arrays are only needed by the outputs it serves
+    assert VBR(100, 200, 3, 1, 5, 7, cc=None, rp=None, rt=None, gy=None, gb=None, sigma=0.1) == OK
+    assert VBR(100, 200, 3, 1, 5, 7, rr=None, cp=None, cr=None, gx=None, sigma=0.1) == OK
+    assert VBR(100, 200, 3, 1, 0, 0, rr=None, cp=None, cr=None, cc=None, rp=None, rt=None,
+               sigma=0.1) == OK
+    assert VBR(100, 200, 3, 1, 5, 7, cr=None, sigma=0.1) == INVALID
+    assert VBR(100, 200, 3, 1, 5, 7, rt=None, gy=None, sigma=0.1) == INVALID    # gb needs it
+    assert VBR(100, 200, 3, 1, -1, 7, sigma=0.1) == INVALID
+    assert VBR(100, 200, 3, 1, 5, -1, sigma=0.1) == INVALID
+    assert VBR(100, 200, 3, 1, 5, 7, rp=2, sigma=0.1) == INVALID                # misaligned
+    # the dense backward's rules
+    assert VBR(100, 200, 3, 1, 5, 7, sigma=0.0) == INVALID
+    assert VBR(100, 200, 17, 1, 5, 7, sigma=1.0) == UNSUPPORTED
+    assert VBR(100, 200, 3, 1, 5, 7, b=None, sigma=1.0) == INVALID

@@ -539,3 +539,53 @@ def test_ranges_argkmin_maps_back_to_global_indices(oracle_mod):
     rows, ptr, cr = np.array([[0, 1], [1, 2]]), np.array([0, 2, 3]), np.array([[8, 10], [2, 4], [11, 12]])
     idx, _ = oracle_mod.ranges_reduce("argkmin", x, y, None, rows, ptr, cr, K=3)
     np.testing.assert_array_equal(idx, [[2, 3, 8], [11, -1, -1]])
+
+
+def _ranges_loss(oracle_mod, x, y, b, e, sigma, pat):
+    # L = sum_i <e_i, a_i> with a the oracle's block-sparse Gaussian sum
+    a, _ = oracle_mod.ranges_reduce("sum", x, y, b, *pat, formula="gauss", sigma=sigma)
+    return float((a * e).sum())
+
+
+def test_ranges_backward_matches_finite_differences(oracle_mod):
+    # gradients of the masked sum in x, y (central differences) and b (exact:
+    # L is linear in b), from the forward (row-cluster) pattern alone; rows
+    # and columns the pattern never pairs get zero
+    rng = np.random.default_rng(23)
+    M, N, D, E, sigma = 14, 19, 2, 2, 0.3
+    x = rng.uniform(0, 1, (M, D)); y = rng.uniform(0, 1, (N, D))
+    b = rng.normal(size=(N, E)); e = rng.normal(size=(M, E))
+    pat = _random_ranges(rng, M, N, 3, 4)
+    gx, nx, gy, ny, gb, nb = oracle_mod.ranges_backward(x, y, b, e, sigma, *pat)
+    mask, covered = _row_mask(*pat, M, N)
+    h = 1e-5 * sigma
+    for var, grad, scale in (("x", gx, nx.max()), ("y", gy, ny.max())):
+        base = x if var == "x" else y
+        for i in range(base.shape[0]):
+            for k in range(D):
+                p = base.copy(); p[i, k] += h
+                m = base.copy(); m[i, k] -= h
+                args_p = (p, y) if var == "x" else (x, p)
+                args_m = (m, y) if var == "x" else (x, m)
+                fd = (_ranges_loss(oracle_mod, *args_p, b, e, sigma, pat) -
+                      _ranges_loss(oracle_mod, *args_m, b, e, sigma, pat)) / (2 * h)
+                assert grad[i, k] == pytest.approx(fd, rel=1e-6, abs=1e-7 * scale)
+    for j in range(N):
+        for c in range(E):
+            p = b.copy(); p[j, c] += 1.0
+            fd = _ranges_loss(oracle_mod, x, y, p, e, sigma, pat) - _ranges_loss(oracle_mod, x, y, b, e, sigma, pat)
+            assert gb[j, c] == pytest.approx(fd, rel=1e-10, abs=1e-12)
+    assert (gx[~covered] == 0).all()
+    assert (gy[~mask.any(0)] == 0).all() and (gb[~mask.any(0)] == 0).all()
+
+
+def test_ranges_backward_full_cover_is_dense(oracle_mod):
+    rng = np.random.default_rng(24)
+    x = rng.uniform(0, 1, (25, 3)); y = rng.uniform(0, 1, (31, 3))
+    b = rng.normal(size=(31, 3)); e = rng.normal(size=(25, 3))
+    pat = (np.array([[0, 25]]), np.array([0, 2]), np.array([[0, 12], [12, 31]]))
+    gx, _, gy, _, gb, _ = oracle_mod.ranges_backward(x, y, b, e, 0.4, *pat)
+    np.testing.assert_allclose(gx, oracle_mod.gauss_vjp(x, y, b, e, 0.4)[0], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(gy, oracle_mod.gauss_vjp(y, x, e, b, 0.4)[0], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(gb, oracle_mod.kernel_sum("gauss", y, x, e, sigma=0.4)[0],
+                               rtol=1e-12, atol=1e-14)
