@@ -9,7 +9,9 @@ The arithmetic lives in ``kred_oracle.c`` (plain C, fp64, OpenMP over rows);
 this module builds it with gcc on first use, converts fp32 inputs to fp64 and
 marshals arguments.  The block-sparse (cluster-wise) reductions of Sec. 3 are
 composed here from those routines: each row cluster is reduced over its
-gathered columns.  What each routine computes follows Charlier et al.,
+gathered columns, and the gradients of the block-sparse Gaussian sum take the
+same blocks (a row or column the pattern never pairs gets zero).  What each
+routine computes follows Charlier et al.,
 "Kernel Operations on the GPU, with Autodiff, without Memory Overflows"
 (arXiv:2004.11127): Eq. (1) (Gaussian kernel sum), Eq. (2) with the
 reductions of Sec. 2 (sum, log-sum-exp, arg-K-min), and the x-gradient of
