@@ -289,10 +289,10 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   // lane's columns, and the row's shared filter (see refresh_filter)
   float dk[RB][KL];
   int jk[RB][KL];
-  float thr[RB];
+  int thi[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    thr[rb] = __builtin_inff();
+    thi[rb] = __float_as_int(__builtin_inff());
 #pragma unroll
     for (int p = 0; p < KL; ++p) {
       dk[rb][p] = __builtin_inff();
@@ -302,6 +302,11 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   // Any value with at least KL of the row's candidates at or below it bounds
   // the row's K-th nearest here (K <= KL): the smaller of the 4 lane groups'
   // smallest KL-th value and their largest ceil(KL/4)-th value.  Ties pass.
+  // The test runs on the bit patterns as signed integers: for values >= 0
+  // that is the float order, and a negative value (a tiny distance that
+  // rounding pushed below zero) reads as smaller than every non-negative one;
+  // a negative bound is raised to +0, so the test only ever passes more
+  // columns than the float test would.
   auto refresh_filter = [&]() {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -311,7 +316,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
       float u = dk[rb][(KL + 3) / 4 - 1];
       u = fmaxf(u, __shfl_xor(u, 16));
       u = fmaxf(u, __shfl_xor(u, 32));
-      thr[rb] = fminf(v, u);
+      thi[rb] = max(__float_as_int(fminf(v, u)), 0);
     }
   };
   float acc[RB][4], tot[RB][4], mref[RB];
@@ -368,24 +373,29 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
       if (t + 1 < ntiles) fetch(jt + TJF);
       if constexpr (kKnn) {
         refresh_filter();
-        // the lane's 4 distances of each row block; columns past the range
-        // (the last block's zero A rows) read as +infinity.  All products and
-        // filter tests come before the first branch.
-        for (int blk = 0; blk < nblk; ++blk) {
+        // the lane's 4 distances of each row block.  Full blocks first, then
+        // the range's last block if columns past its end (zero A rows) must
+        // read as +infinity.  All products and filter tests come before the
+        // first branch.
+        const bool ragged = jt + 16 * nblk > jlim;
+        const int nfull = ragged ? nblk - 1 : nblk;
+        auto knn_block = [&](int blk, bool masked) __attribute__((always_inline)) {
           const bf16x8 am = a_operand(buf, blk);
           const int64_t jb = jt + blk * 16 + 4 * g;
-          const int64_t room = jlim - jb;   // per lane: a select, not a branch, after the MFMA
           float dd[RB][4];
           bool any[RB];
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) {
             const f4 T = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, xb[rb], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dd[rb][r] = r < room ? T[r] : __builtin_inff();
+            for (int r = 0; r < 4; ++r) dd[rb][r] = (!masked || jb + r < jlim) ? T[r] : __builtin_inff();
           }
 #pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-            any[rb] = fminf(fminf(dd[rb][0], dd[rb][1]), fminf(dd[rb][2], dd[rb][3])) <= thr[rb];
+          for (int rb = 0; rb < RB; ++rb) {
+            const int m = min(min(__float_as_int(dd[rb][0]), __float_as_int(dd[rb][1])),
+                              min(__float_as_int(dd[rb][2]), __float_as_int(dd[rb][3])));
+            any[rb] = m <= thi[rb];
+          }
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) {
             if (__builtin_expect(any[rb], 0)) {
@@ -394,7 +404,9 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
                 if (dd[rb][r] < dk[rb][KL - 1]) list_insert<KL>(dk[rb], jk[rb], dd[rb][r], (int)(jb + r));
             }
           }
-        }
+        };
+        for (int blk = 0; blk < nfull; ++blk) knn_block(blk, false);
+        if (ragged) knn_block(nblk - 1, true);
       } else if constexpr (kMin) {
         // d for the lane's columns 4g + r of each block.  Full blocks first,
         // then the range's last block if columns past its end (zero A rows,
