@@ -46,6 +46,12 @@ WORKLOADS = {
            14, "alu", "sinkhorn log-sum-exp, uniform / shifted uniform, 1e6 x 1e6, D=3"),
     "c4": ("highdim_gauss", dict(M=200_000, N=200_000, D=128, E=16, sigma=1.0), "gauss", "sum",
            291, "mfma", "gaussian kernel sum, N(0, I/128), 2e5 x 2e5, D=128, E=16"),
+    # the fused value + x-gradient at D = 128: one Gaussian sum with D + 1 = 129
+    # signal columns [b, b (y - m)] on the matrix cores (three launches of up to
+    # 64 columns); 2D + 3 flops for the exponent and 2 (D + 1) for the sums
+    "gradx_d128": ("highdim_gauss", dict(M=200_000, N=200_000, D=128, E=1, sigma=1.0),
+                   "gauss_gradx", "sum", 2 * 128 + 3 + 2 * 129, "mfma",
+                   "gaussian kernel sum + x-gradient (fused), N(0, I/128), 2e5 x 2e5, D=128"),
     # the integer coordinates pass the library's exactness guard, so the contraction
     # runs on the bf16 matrix cores
     "c5": ("integer_knn", dict(M=100_000, N=1_000_000, D=64, K=10), "sqdist", "argkmin",
@@ -97,20 +103,25 @@ KERNEL_SOURCES = {"sum_kernel": "k_direct.hip", "gradx_kernel": "k_direct.hip",
                   "fast_kernel": "k_small_mfma.hip"}
 
 
-def matrix_flops_per_pair(kernel, w, reduction):
-    """Matrix-core flops a kernel executes per pair, by operand type.
+def matrix_flops_per_pair(kernel, w, reduction, formula=None):
+    """Matrix-core flops a kernel executes per pair (over a step's launches), by operand type.
 
     The bf16 kernels execute more matrix work than the algorithm needs (split
     operands, padded K slots); this is what their time is measured against in
     `matrix_executed`, beside the algorithmic roofline.
     """
     dp = next((p for p in (32, 64, 128, 256) if w.D <= p), 256)
-    eb = 1 if w.E <= 16 else (2 if w.E <= 32 else 4)
     sums = reduction == "sum"
+    # signal widths of the launches: the fused gradient at D > 16 runs sums of
+    # [b, b (y - m)] in chunks of up to 64 columns
+    widths = [w.E]
+    if formula == "gauss_gradx" and w.D > 16:
+        widths = [min(64, w.D + 1 - c) for c in range(0, w.D + 1, 64)]
+    ebs = [1 if e <= 16 else (2 if e <= 32 else 4) for e in widths]
     if kernel == "mfma_split_kernel":     # 6 split products per coordinate; P . B in fp32
-        return {"bf16": 12 * dp, "f32": 32 * eb}
+        return {"bf16": 12 * dp * len(ebs), "f32": sum(32 * eb for eb in ebs)}
     if kernel == "mfma_kernel":
-        return {"f32": 2 * dp + (32 * eb if sums else 0)}
+        return {"f32": sum(2 * dp + (32 * eb if sums else 0) for eb in ebs)}
     if kernel == "knn_bf16_kernel":       # one exact bf16 product per coordinate
         return {"bf16": 2 * dp}
     if kernel == "fast_kernel":           # one 16x16x32 product per 16x16 pairs (32 K slots)
@@ -364,7 +375,7 @@ def main():
     # fpp counts the flops of one (i, j) over all reductions of a step
     step_pairs = pairs / REDUCTIONS_PER_STEP.get(args.workload, 1)   # pairs of one reduction
     achieved = fpp * step_pairs / (r["kernel_ms"] / 1e3) / 1e12
-    mx = matrix_flops_per_pair(r["kernel"], w, reduction)
+    mx = matrix_flops_per_pair(r["kernel"], w, reduction, formula)
     mdtype = ("bf16" if "bf16" in mx else "f32") if bound == "mfma" else None
     peak = {None: PEAK_FP32_VECTOR_TFLOPS, "f32": PEAK_FP32_MATRIX_TFLOPS,
             "bf16": PEAK_BF16_MATRIX_TFLOPS}[mdtype]

@@ -1034,6 +1034,92 @@ int mfma_rows_per_block(int DP, int KP) {
   return 64 * ((Q >= 64 || KP == 64) ? 1 : 2);
 }
 
+// ------------------------------------------ fused value + gradient, large D
+// The Gaussian sum's x-gradient g_i = sum_j k_ij b_j (y_j - x_i) / sigma^2
+// (the derivative of Eq. (1)) is, for any point m, (A1_i - (x_i - m) A0_i) /
+// sigma^2 with A0 = K b and A1 = K [b (y - m)]: one Gaussian sum with D + 1
+// signal columns.  m is the mean of up to the first 1024 rows of y, so that
+// |y - m| stays of the order of |y - x| and the subtraction loses little.
+
+namespace {
+
+__global__ __launch_bounds__(256) void gradx_centre_kernel(const float* __restrict__ y, int64_t N,
+                                                           int D, float* __restrict__ m) {
+  const int d = threadIdx.x;
+  if (d >= D) return;
+  const int64_t n = min(N, (int64_t)1024);
+  float s = 0.0f;
+  for (int64_t j = 0; j < n; ++j) s += y[j * D + d];
+  m[d] = n > 0 ? s / (float)n : 0.0f;
+}
+
+// columns [c0, c0 + Ec) of the signal [b, b (y - m)]: N x Ec, row-major
+__global__ __launch_bounds__(256) void gradx_signal_kernel(const float* __restrict__ y,
+                                                           const float* __restrict__ b, int64_t N,
+                                                           int D, const float* __restrict__ m,
+                                                           int c0, int Ec, float* __restrict__ sig) {
+  const int64_t total = N * Ec;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t j = t / Ec;
+    const int c = c0 + (int)(t - j * Ec);
+    sig[t] = c == 0 ? b[j] : b[j] * (y[j * D + c - 1] - m[c - 1]);
+  }
+}
+
+// out[i] = (A0, (A1 - (x_i - m) A0) gscale); column c of A sits in chunk c / 64
+// (M x Ec_q at T + 64 M q)
+__global__ __launch_bounds__(256) void gradx_finish_kernel(const float* __restrict__ x, int64_t M,
+                                                           int D, const float* __restrict__ m,
+                                                           const float* __restrict__ T,
+                                                           float gscale, float* __restrict__ out) {
+  const int W = D + 1;
+  const int64_t total = M * W;
+  const int last = (W - 1) / 64;
+  const int Elast = W - 64 * last;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = t / W;
+    const int c = (int)(t - i * W);
+    const int q = c / 64;
+    const int ec = q == last ? Elast : 64;
+    const float a = T[64 * M * q + i * ec + (c - 64 * q)];
+    if (c == 0) {
+      out[t] = a;
+    } else {
+      const float a0 = T[i * (last == 0 ? Elast : 64)];
+      out[t] = (a - (x[i * D + c - 1] - m[c - 1]) * a0) * gscale;
+    }
+  }
+}
+
+int64_t grid_of(int64_t items) {
+  return std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 8192));
+}
+
+}  // namespace
+
+hipError_t launch_gradx_centre(const float* y, int64_t N, int D, float* m, hipStream_t s) {
+  hipLaunchKernelGGL(gradx_centre_kernel, dim3(1), dim3(256), 0, s, y, N, D, m);
+  return hipGetLastError();
+}
+
+hipError_t launch_gradx_signal(const float* y, const float* b, int64_t N, int D, const float* m,
+                               int c0, int Ec, float* sig, hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  hipLaunchKernelGGL(gradx_signal_kernel, dim3((unsigned)grid_of(N * Ec)), dim3(256), 0, s, y, b,
+                     N, D, m, c0, Ec, sig);
+  return hipGetLastError();
+}
+
+hipError_t launch_gradx_finish(const float* x, int64_t M, int D, const float* m, const float* T,
+                               float gscale, float* out, hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  hipLaunchKernelGGL(gradx_finish_kernel, dim3((unsigned)grid_of(M * (D + 1))), dim3(256), 0, s,
+                     x, M, D, m, T, gscale, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s) {
   if (a.N16 == 0) return hipSuccess;
   const int64_t items = a.N16 * std::max(a.DP, 16 * a.EB);

@@ -21,6 +21,8 @@ struct kred_ctx {
   size_t scratch_bytes = 0;
   void* aux = nullptr;       // backward: the fused value + gradient of the scalar-cotangent route
   size_t aux_bytes = 0;
+  void* wide = nullptr;      // fused value + gradient at large D: centre, signal and sums
+  size_t wide_bytes = 0;
   // KRED_FLAG_PROFILE: event pairs around main kernels, reused across collects
   std::vector<hipEvent_t> ev;
   size_t ev_used = 0;
@@ -514,6 +516,44 @@ void empty_fill(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
 
 // One reduction on validated arguments, M > 0, on the current device;
 // block-sparse when rg is given.
+// Bytes of the large-D fused gradient's own buffer: the centre, one signal
+// chunk (N x 64) and the sums (M x (D + 1)).
+int64_t gradx_wide_bytes(int64_t M, int64_t N, int32_t D) {
+  return align_up((int64_t)D * (int64_t)sizeof(float)) +
+         align_up(N * std::min(64, D + 1) * (int64_t)sizeof(float)) +
+         align_up(M * (D + 1) * (int64_t)sizeof(float));
+}
+
+// GAUSS_GRADX for 16 < D <= 256 (validated, M, N > 0, E = 1): the Gaussian sum
+// on the matrix cores with the D + 1 signal columns [b, b (y - m)], 64 columns
+// per call, then out = (A0, (A1 - (x - m) A0) / sigma^2).
+kred_status run_gradx_wide(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, int32_t D,
+                           const float* x, const float* y, const float* b, float* out,
+                           hipStream_t s, const Ranges* rg) {
+  const kred_status ga = grow_buffer(&ctx->wide, &ctx->wide_bytes, (size_t)gradx_wide_bytes(M, N, D));
+  if (ga != KRED_OK) return ga;
+  char* base = static_cast<char*>(ctx->wide);
+  float* m = reinterpret_cast<float*>(base);
+  float* sig = reinterpret_cast<float*>(base + align_up((int64_t)D * (int64_t)sizeof(float)));
+  float* T = reinterpret_cast<float*>(reinterpret_cast<char*>(sig) +
+                                      align_up(N * std::min(64, D + 1) * (int64_t)sizeof(float)));
+  const int W = D + 1;
+  // rows outside every cluster read zero sums (a zero value and gradient)
+  if (rg && launch_fill(T, M * W, 0.0f, s) != hipSuccess) return KRED_ERR_HIP;
+  if (launch_gradx_centre(y, N, D, m, s) != hipSuccess) return KRED_ERR_HIP;
+  for (int c0 = 0; c0 < W; c0 += 64) {
+    const int Ec = std::min(64, W - c0);
+    if (launch_gradx_signal(y, b, N, D, m, c0, Ec, sig, s) != hipSuccess) return KRED_ERR_HIP;
+    const kred_status st = run_mfma(ctx, KRED_F_GAUSS, KRED_R_SUM, p, M, N, D, Ec, x, y, sig,
+                                    T + (int64_t)c0 * M, s, 0, rg);
+    if (st != KRED_OK) return st;
+  }
+  const double sg = (double)p->sigma;
+  return launch_gradx_finish(x, M, D, m, T, (float)(1.0 / (sg * sg)), out, s) == hipSuccess
+             ? KRED_OK
+             : KRED_ERR_HIP;
+}
+
 kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                           int64_t M, int64_t N, int32_t D, int32_t E, const float* x,
                           const float* y, const float* b, void* out, hipStream_t s,
@@ -543,6 +583,8 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   // kernel-side formula: log-sum-exps run on the Sinkhorn-form kernels
   const int kf = (r == KRED_R_LSE) ? (f == KRED_F_LAPLACE ? F_LAPLACE_LSE : F_SINKHORN) : (int)f;
 
+  if (D > kMaxDirectD && f == KRED_F_GAUSS_GRADX)
+    return run_gradx_wide(ctx, p, M, N, D, x, y, b, static_cast<float*>(out), s, rg);
   if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s, kvalues, rg);
 
   kred_params pr;
@@ -764,7 +806,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
 kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, int32_t D,
                     int32_t E, const float* x, const float* y, const float* b, const float* e,
                     float* g, hipStream_t s, const Ranges* rg = nullptr) {
-  if (E == 1 && fast_epi(KRED_F_GAUSS_GRADX, KRED_R_SUM, M, N, D, 1, p->flags) >= 0) {
+  if (E == 1 && (D > kMaxDirectD || fast_epi(KRED_F_GAUSS_GRADX, KRED_R_SUM, M, N, D, 1, p->flags) >= 0)) {
     const kred_status ga =
         grow_buffer(&ctx->aux, &ctx->aux_bytes, (size_t)(M * (1 + D) * (int64_t)sizeof(float)));
     if (ga != KRED_OK) return ga;
@@ -950,8 +992,7 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
   const bool lists = f == KRED_F_SQDIST && b == nullptr &&
                      (r == KRED_R_ARGKMIN || r == KRED_R_KMIN || r == KRED_R_MIN ||
                       r == KRED_R_ARGMIN);
-  if (D > kMaxDirectD && (f == KRED_F_GAUSS_GRADX || f == KRED_F_SINKHORN || r == KRED_R_LSE ||
-                          (is_extreme(r) && !lists)))
+  if (D > kMaxDirectD && (f == KRED_F_SINKHORN || r == KRED_R_LSE || (is_extreme(r) && !lists)))
     return KRED_ERR_UNSUPPORTED;
   if (M == 0) return KRED_OK;
   if (x == nullptr || out == nullptr) return KRED_ERR_INVALID_ARG;
@@ -978,10 +1019,15 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
   }
   if (is_extreme(r) && (nob || f == KRED_F_SINKHORN)) E = 1;
   if (D > kMaxDirectD) {
+    // the fused value + gradient runs Gaussian sums of up to 64 signal columns
+    const bool wide = f == KRED_F_GAUSS_GRADX;
     MPlan mp;
-    if (!make_mplan(f, r, p, M, N, D, E, 256, &mp)) return -1;
+    if (!make_mplan(wide ? KRED_F_GAUSS : f, r, p, M, N, D, wide ? std::min(64, D + 1) : E, 256,
+                    &mp))
+      return -1;
     return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes +
-           mfma_bf16_bytes(mp, r == KRED_R_ARGKMIN, p->flags, M, N);
+           mfma_bf16_bytes(mp, r == KRED_R_ARGKMIN, p->flags, M, N) +
+           (wide ? gradx_wide_bytes(M, N, D) : 0);
   }
   const int epi = fast_epi(f, r, M, N, D, E, p->flags, p->K);
   Plan pl;
@@ -1019,6 +1065,7 @@ kred_status kred_destroy(kred_ctx* ctx) {
     if (hipDeviceSynchronize() != hipSuccess) st = KRED_ERR_HIP;
     if (ctx->scratch) (void)hipFree(ctx->scratch);
     if (ctx->aux) (void)hipFree(ctx->aux);
+    if (ctx->wide) (void)hipFree(ctx->wide);
     if (ctx->exact_guard) (void)hipFree(ctx->exact_guard);
     for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
   }
@@ -1084,7 +1131,9 @@ kred_status kred_validate_backward(const kred_params* p, int64_t M, int64_t N, i
   if (p->col_blocks < 0 || p->col_blocks > KRED_MAX_COL_BLOCKS) return KRED_ERR_INVALID_ARG;
   if (M < 0 || N < 0 || M > INT32_MAX || N > INT32_MAX) return KRED_ERR_INVALID_ARG;
   if (D < 1 || D > KRED_MAX_D || E < 1 || E > KRED_MAX_E) return KRED_ERR_INVALID_ARG;
-  if (D > kMaxDirectD) return KRED_ERR_UNSUPPORTED;
+  // 16 < D <= 256: gx and gy for a scalar cotangent (the fused value +
+  // gradient on the matrix cores), gb for any E (a Gaussian sum)
+  if (D > kMaxDirectD && E > 1 && (gx || gy)) return KRED_ERR_UNSUPPORTED;
   // Inputs the requested outputs read.  With M = 0 or N = 0 every reduction
   // is empty and the outputs are filled with zeros without reading any input.
   if (M > 0 && N > 0 && (gx || gy || gb)) {

@@ -193,6 +193,16 @@ struct MfmaPackArgs {
 };
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
 
+// Fused Gaussian value + x-gradient for 16 < D <= 256 as one Gaussian sum with
+// D + 1 signal columns [b, b (y - m)]: the centre m (D floats), the signal
+// columns [c0, c0 + Ec) (N x Ec), and the output M x (1 + D) from the sums T
+// (column c in chunk c / 64, stored M x Ec_q at T + 64 M q).
+hipError_t launch_gradx_centre(const float* y, int64_t N, int D, float* m, hipStream_t s);
+hipError_t launch_gradx_signal(const float* y, const float* b, int64_t N, int D, const float* m,
+                               int c0, int Ec, float* sig, hipStream_t s);
+hipError_t launch_gradx_finish(const float* x, int64_t M, int D, const float* m, const float* T,
+                               float gscale, float* out, hipStream_t s);
+
 struct MfmaArgs {
   int epi;        // 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min
   int D, DP, E, e0, EB;

@@ -162,10 +162,24 @@ def test_backward_invalid_arguments(lib):
     assert VB(100, 200, 3, 1, e=2, sigma=1.0) == INVALID             # misaligned input
 
 
-def test_backward_large_d_unsupported(lib):
-    assert VB(100, 200, 17, 1, sigma=1.0) == UNSUPPORTED
-    assert VB(100, 200, 256, 1, sigma=1.0) == UNSUPPORTED
+def test_backward_large_d(lib):
+    # 16 < D <= 256: scalar cotangents (the fused value + gradient on the matrix
+    # cores) and gb for any E; gx, gy with E > 1 are not served there
+    assert VB(100, 200, 17, 1, sigma=1.0) == OK
+    assert VB(100, 200, 256, 1, sigma=1.0) == OK
+    assert VB(100, 200, 64, 8, gx=None, gy=None, sigma=1.0) == OK
+    assert VB(100, 200, 64, 8, sigma=1.0) == UNSUPPORTED
+    assert VB(100, 200, 64, 8, gx=None, gb=None, sigma=1.0) == UNSUPPORTED
     assert VB(100, 200, 257, 1, sigma=1.0) == INVALID
+
+
+def test_gradx_large_d(lib):
+    V = kred.validate
+    assert V("gauss_gradx", "sum", 100, 200, 17, 1, sigma=1.0) == OK
+    assert V("gauss_gradx", "sum", 100, 200, 256, 1, sigma=1.0) == OK
+    assert V("gauss_gradx", "sum", 100, 200, 64, 2, sigma=1.0) == INVALID
+    assert kred.scratch_bytes("gauss_gradx", "sum", 1000, 2000, 128, 1, sigma=1.0) > \
+        kred.scratch_bytes("gauss", "sum", 1000, 2000, 128, 1, sigma=1.0)
 
 
 # ------------------------------------------------ min / max / arg-min / K-min
@@ -254,5 +268,5 @@ def test_backward_ranges_validation(lib):
     assert VBR(100, 200, 3, 1, 5, 7, rp=2, sigma=0.1) == INVALID                # misaligned
     # the dense backward's rules
     assert VBR(100, 200, 3, 1, 5, 7, sigma=0.0) == INVALID
-    assert VBR(100, 200, 17, 1, 5, 7, sigma=1.0) == UNSUPPORTED
+    assert VBR(100, 200, 17, 4, 5, 7, sigma=1.0) == UNSUPPORTED              # gx, gy with E > 1
     assert VBR(100, 200, 3, 1, 5, 7, b=None, sigma=1.0) == INVALID

@@ -1,0 +1,124 @@
+"""GPU parity of the fused Gaussian value + x-gradient for 16 < D <= 256.
+
+The library evaluates it as one Gaussian sum with D + 1 signal columns
+[b, b (y - m)] on the matrix cores (64 columns per launch; m a centre of y)
+and finishes g_i = (A1_i - (x_i - m) A0_i) / sigma^2.  Compared with the fp64
+oracle's gauss_gradx (the definition, any D), normalised per component by the
+sum of absolute summands as for the small-D gradient, on both matrix-core
+kernels (fp32 products, and the three-way bf16 split), with column splits,
+data far from the origin (where the centring matters), one and several
+signal chunks, block-sparse patterns, and the Gaussian backward with a scalar
+cotangent (gx, gy) and with E signal columns (gb) at these D.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import SUM_TOL, dev, host, norm_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    import torch
+    from paper_2004_11127_amd import kred
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    with kred.Context(0) as c:
+        yield c
+
+
+def _data(seed, M, N, D, offset=0.0, E=1):
+    # coordinates ~ offset + N(0, 1/D): squared distances of order 2, sigma 1
+    rng = np.random.default_rng(seed)
+    x = (offset + rng.standard_normal((M, D)) / np.sqrt(D)).astype(np.float32)
+    y = (offset + rng.standard_normal((N, D)) / np.sqrt(D)).astype(np.float32)
+    b = rng.standard_normal((N, E)).astype(np.float32)
+    return x, y, b
+
+
+CASES = [
+    # M, N, D, sigma, offset, col_blocks
+    (1, 1, 17, 1.0, 0.0, 0),
+    (300, 900, 17, 0.8, 0.0, 0),
+    (513, 1000, 64, 1.0, 3.0, 0),        # one chunk of 64 signal columns (D + 1 = 65: two)
+    (257, 777, 63, 1.0, 0.0, 3),         # D + 1 = 64: exactly one chunk
+    (400, 1200, 128, 1.2, 5.0, 1),
+    (129, 600, 200, 1.0, 0.0, 5),
+    (200, 500, 256, 1.0, 2.0, 0),        # five chunks, the last of one column
+]
+
+
+@pytest.mark.parametrize("path", ["fp32", "split"])
+@pytest.mark.parametrize("M,N,D,sigma,offset,C", CASES)
+def test_gradx_large_d_parity(ctx, M, N, D, sigma, offset, C, path):
+    from paper_2004_11127_amd import kred
+    x, y, b = _data(M + N + D, M, N, D, offset)
+    flags = kred.FLAG_DIRECT if path == "fp32" else kred.FLAG_FAST
+    out = host(ctx.run("gauss_gradx", "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C,
+                       flags=flags))
+    ref, norm = oracle.gauss_gradx(x, y, b, sigma)
+    assert out.shape == (M, 1 + D)
+    assert norm_err(out, ref, norm) <= SUM_TOL
+
+
+def test_gradx_large_d_ranges(ctx):
+    from test_gpu_ranges import random_pattern
+    rng = np.random.default_rng(4)
+    M, N, D = 1200, 1500, 48
+    x, y, b = _data(7, M, N, D, offset=1.0)
+    rows, ptr, cr = random_pattern(rng, M, N, 12, 9)
+    cr = np.concatenate([cr, [[N - 7, N + 30]]]).astype(np.int32)
+    ptr = np.concatenate([ptr, [len(cr)]]).astype(np.int32)
+    rows = np.concatenate([rows, [[M - 2, M + 9]]]).astype(np.int32)
+    for C in (0, 1, 4):
+        out = host(ctx.run_ranges("gauss_gradx", "sum", dev(x), dev(y), dev(b), dev(rows), dev(ptr),
+                                  dev(cr), sigma=1.0, col_blocks=C))
+        ref, norm = oracle.ranges_reduce("gradx", x, y, b, rows, ptr, cr, sigma=1.0)
+        assert norm_err(out, ref, norm) <= SUM_TOL, C
+        assert (out[norm.sum(1) == 0] == 0).all()
+
+
+@pytest.mark.parametrize("D,E", [(24, 1), (96, 1), (130, 1)])
+def test_backward_large_d_scalar_cotangent(ctx, D, E):
+    M, N = 600, 800
+    x, y, b = _data(D, M, N, D, offset=0.5, E=E)
+    e = np.random.default_rng(D + 1).standard_normal((M, E)).astype(np.float32)
+    gx, gy, gb = ctx.gauss_backward(dev(x), dev(y), dev(b), dev(e), sigma=1.0)
+    ref, norm = oracle.gauss_vjp(x, y, b, e, 1.0)
+    assert norm_err(host(gx), ref, norm) <= SUM_TOL
+    ref, norm = oracle.gauss_vjp(y, x, e, b, 1.0)
+    assert norm_err(host(gy), ref, norm) <= SUM_TOL
+    ref, norm = oracle.kernel_sum("gauss", y, x, e, sigma=1.0)
+    assert norm_err(host(gb), ref, norm) <= SUM_TOL
+
+
+def test_backward_large_d_signal_gradient(ctx):
+    # E > 1 at large D: gb (a Gaussian sum) is served, gx and gy are not
+    from paper_2004_11127_amd import kred
+    M, N, D, E = 500, 700, 64, 6
+    x, y, b = _data(3, M, N, D, E=E)
+    e = np.random.default_rng(2).standard_normal((M, E)).astype(np.float32)
+    _, _, gb = ctx.gauss_backward(dev(x), dev(y), dev(b), dev(e), sigma=1.0, gx=False, gy=False)
+    ref, norm = oracle.kernel_sum("gauss", y, x, e, sigma=1.0)
+    assert norm_err(host(gb), ref, norm) <= SUM_TOL
+    with pytest.raises(kred.KredError):
+        ctx.gauss_backward(dev(x), dev(y), dev(b), dev(e), sigma=1.0)
+
+
+def test_backward_ranges_large_d(ctx):
+    from paper_2004_11127_amd import clusters
+    from test_gpu_ranges import random_pattern
+    rng = np.random.default_rng(11)
+    M, N, D = 900, 1100, 40
+    x, y, b = _data(12, M, N, D, offset=0.3)
+    e = rng.standard_normal((M, 1)).astype(np.float32)
+    pat = random_pattern(rng, M, N, 8, 10)
+    tr = clusters.transpose_pattern(*pat, M, N)
+    gx, gy, gb = ctx.gauss_backward_ranges(dev(x), dev(y), dev(b), dev(e),
+                                           tuple(dev(np.asarray(a, np.int32)) for a in pat),
+                                           tuple(dev(a) for a in tr), sigma=1.0)
+    rx, nx, ry, ny, rb, nb = oracle.ranges_backward(x, y, b, e, 1.0, *pat)
+    assert norm_err(host(gx), rx, nx) <= SUM_TOL
+    assert norm_err(host(gy), ry, ny) <= SUM_TOL
+    assert norm_err(host(gb), rb, nb) <= SUM_TOL
