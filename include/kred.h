@@ -146,9 +146,11 @@ kred_status kred_destroy(kred_ctx* ctx);
  *
  * Ranges: 0 <= M, N <= 2^31 - 1; 1 <= D <= KRED_MAX_D; 1 <= E <= KRED_MAX_E
  * where b has E columns; p->col_blocks in [0, KRED_MAX_COL_BLOCKS].  D > 16
- * is supported by the sums, ARGKMIN, KMIN, and MIN / ARGMIN of SQDIST without
- * b; the other pairs (GAUSS_GRADX and every LSE among them) return
- * KRED_ERR_UNSUPPORTED there.  Inputs must be
+ * is supported by the sums, GAUSS_GRADX (as one Gaussian sum with the D + 1
+ * signal columns [b, b (y - m)] for a centre m of y, then g = (A1 - (x - m)
+ * A0) / sigma^2; scratch grows by about (M + 64 N)(D + 1) floats), ARGKMIN,
+ * KMIN, and MIN / ARGMIN of SQDIST without b; the other pairs (every LSE among
+ * them) return KRED_ERR_UNSUPPORTED there.  Inputs must be
  * finite (NaN or Inf in x, y or b gives an undefined result).
  * Edge cases: M = 0 returns KRED_OK and touches nothing.  N = 0 writes zeros
  * (SUM), -infinity (LSE, MAX), +infinity (MIN) or -1 (ARGMIN, ARGMAX) and
@@ -243,8 +245,10 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
  * Parameters: p->sigma (> 0, finite), p->col_blocks and p->flags as for
  * kred_run (KRED_FLAG_DIRECT / KRED_FLAG_FAST steer the path of every
  * reduction in the call; KRED_FLAG_PROFILE times each main kernel); p->eps
- * and p->K are ignored.  Ranges: 0 <= M, N <= 2^31 - 1, 1 <= D <= 16 (larger
- * D returns KRED_ERR_UNSUPPORTED), 1 <= E <= KRED_MAX_E.  With M = 0 or N = 0
+ * and p->K are ignored.  Ranges: 0 <= M, N <= 2^31 - 1, 1 <= D <= KRED_MAX_D,
+ * 1 <= E <= KRED_MAX_E; for D > 16, gx and gy need E = 1 (they run on the
+ * fused value + gradient; gx or gy with E > 1 there returns
+ * KRED_ERR_UNSUPPORTED) while gb takes any E.  With M = 0 or N = 0
  * the requested outputs are filled with zeros.  x, y and e are required, and
  * b too for gx or gy, whenever M, N > 0 and an output is requested.  Same
  * error and asynchrony rules as kred_run: on any argument error nothing runs.
@@ -284,7 +288,7 @@ kred_status kred_validate_backward(const kred_params* p, int64_t M, int64_t N, i
  * kred_run_ranges (disjoint clusters, clamping to [0, M) and [0, N)); a
  * pattern's arrays may be NULL when its count is 0 or when the outputs it
  * serves are not requested.  Parameters, outputs, errors and asynchrony as
- * kred_gauss_backward (1 <= D <= 16; E-slices and col_blocks as there, the
+ * kred_gauss_backward (D and E limits, E-slices and col_blocks as there, the
  * column split applying to each cluster's ranges).
  */
 kred_status kred_gauss_backward_ranges(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N,

@@ -62,7 +62,8 @@ __global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total; t += stride) {
     const int64_t j = t / a.DP;
     const int d = (int)(t - j * a.DP);
-    const float v = (j < a.N && d < a.D) ? a.y[j * a.D + d] : 0.0f;
+    const float v =
+        (j < a.N && d < a.D) ? a.y[j * a.D + d] - (a.yc != nullptr ? a.yc[d] : 0.0f) : 0.0f;
     if (ex) {
       a.ybf[t] = __builtin_bit_cast(unsigned short, (__bf16)(v * a.yop_scale));
     } else if (a.ysp != nullptr) {
@@ -101,11 +102,13 @@ __global__ __launch_bounds__(256) void mfma_norm_kernel(MfmaPackArgs a) {
     float s = 0.0f;
     if (j < a.N)
       for (int d = lane; d < a.D; d += 64) {
-        const float v = a.y[j * a.D + d] * a.coord_scale;
+        const float v = (a.y[j * a.D + d] - (a.yc != nullptr ? a.yc[d] : 0.0f)) * a.coord_scale;
         s = __builtin_fmaf(v, v, s);
       }
     for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-    if (lane == 0) a.ny[j] = j < a.N ? a.nrm_sign * s : a.pad_norm;
+    if (lane == 0)
+      a.ny[j] = j < a.N ? a.nrm_sign * s + (a.goff != nullptr ? a.goff[j] * a.goff_scale : 0.0f)
+                        : a.pad_norm;
   }
 }
 
@@ -266,26 +269,28 @@ __device__ __forceinline__ int64_t bpk_col(int64_t jt, int t4, int W) {
   return jt + (int64_t)(t4 / (16 * W)) * 16 + ((t4 % (16 * W)) / (4 * W)) * 4;
 }
 
-// EPI: 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min.
+// EPI: 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min, 4 log-sum-exp
+// of s_ij = g_j - |x_i - y_j|^2 / eps (log2 units: the column norms carry g_j).
 // SP: block-sparse (a pattern of row clusters and column ranges) or dense.
 template <int Q, int RB, int EPI, int EB, int KP, bool SP>
 __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
   constexpr int DP = 4 * Q;
   constexpr int LDY = DP + 4;
   constexpr int TJ = tile_cols(DP);
-  constexpr bool SUM = EPI != 3;
+  constexpr bool SUM = EPI < 3;
+  constexpr bool LSE = EPI == 4;
   constexpr int W = 16 * EB;                       // signal columns per row in a tile
   constexpr int YF4 = TJ * DP / 4;                 // float4s of y per tile
   constexpr int YL = (YF4 + 255) / 256;            // per thread
   constexpr int BF4 = SUM ? TJ * W / 4 : 0;        // float4s of b per tile
   constexpr int BL = SUM ? (BF4 + 255) / 256 : 0;
-  constexpr int KL = SUM ? 1 : KP;
+  constexpr int KL = EPI == 3 ? KP : 1;
 
   __shared__ float4 ys[2][TJ * LDY / 4];
   __shared__ float4 ns[2][TJ / 4];
   __shared__ float4 bs[2][SUM ? TJ * W / 4 : 1];
 
-  if constexpr (!SUM) {
+  if constexpr (EPI == 3) {
     if (exact_ok(a.exact, a.D)) return;   // the bf16 kernel does the work
   }
   const MItem it = mitem<SP>(a, 64 * RB);
@@ -309,13 +314,23 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       const int d = g * Q + q;
-      const float v = (ok && d < a.D) ? a.x[row * a.D + d] * a.xscale : 0.0f;
+      const float v =
+          (ok && d < a.D) ? (a.x[row * a.D + d] - (a.xc != nullptr ? a.xc[d] : 0.0f)) * a.xscale : 0.0f;
       xr[rb][q] = v;
       part = __builtin_fmaf(v, v, part);
     }
     part += __shfl_xor(part, 16);
     part += __shfl_xor(part, 32);
-    nx[rb] = -part;   // sums only; arg-K-min recomputes it after the loop
+    nx[rb] = -part;   // sums and log-sum-exp; arg-K-min recomputes it after the loop
+  }
+  // log-sum-exp: per lane a running reference (log2 units; a finite floor, so
+  // that differences never meet -inf - -inf), the sum of the current tile and
+  // the total, both relative to it
+  float lm[RB], lp[RB], ls[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    lm[rb] = -3.0e38f;
+    lp[rb] = ls[rb] = 0.0f;
   }
 
   f4 oacc[RB][EB], tot[RB][EB];
@@ -408,8 +423,8 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
       const float4 nyv = ns[buf][blk * 4 + g];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        f4 acc = SUM ? f4{nx[rb] + nyv.x, nx[rb] + nyv.y, nx[rb] + nyv.z, nx[rb] + nyv.w}
-                     : f4{nyv.x, nyv.y, nyv.z, nyv.w};
+        f4 acc = (SUM || LSE) ? f4{nx[rb] + nyv.x, nx[rb] + nyv.y, nx[rb] + nyv.z, nx[rb] + nyv.w}
+                              : f4{nyv.x, nyv.y, nyv.z, nyv.w};
 #pragma unroll
         for (int q = 0; q < Q; ++q) acc = mfma4(yo[q], xr[rb][q], acc);
         if constexpr (SUM) {
@@ -431,6 +446,16 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
             oacc[rb][eb] = mfma4(p[2], bv.z, oacc[rb][eb]);
             oacc[rb][eb] = mfma4(p[3], bv.w, oacc[rb][eb]);
           }
+        } else if constexpr (LSE) {
+          // s of the lane's 4 columns (padding columns: -inf); the reference
+          // moves up to the largest s seen, rescaling both sums
+          const float mb = fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3]));
+          const float nm = fmaxf(lm[rb], mb);
+          const float sc = __builtin_amdgcn_exp2f(lm[rb] - nm);
+          lp[rb] = lp[rb] * sc + ((__builtin_amdgcn_exp2f(acc[0] - nm) + __builtin_amdgcn_exp2f(acc[1] - nm)) +
+                                  (__builtin_amdgcn_exp2f(acc[2] - nm) + __builtin_amdgcn_exp2f(acc[3] - nm)));
+          ls[rb] *= sc;
+          lm[rb] = nm;
         } else {
           const float kth = dk[rb][KL - 1];
           const bool any = acc[0] < kth || acc[1] < kth || acc[2] < kth || acc[3] < kth;
@@ -451,6 +476,13 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
           tot[rb][eb] += oacc[rb][eb];
           oacc[rb][eb] = f4{0.f, 0.f, 0.f, 0.f};
         }
+    }
+    if constexpr (LSE) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        ls[rb] += lp[rb];
+        lp[rb] = 0.0f;
+      }
     }
     // buffer (t+1)&1 was last read in iteration t-1, which ended with a barrier
     if (t + 1 < ntiles) put((int)((t + 1) & 1));
@@ -478,6 +510,29 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
             a.part[((int64_t)c * a.M + row) * W + e] = tot[rb][eb][r];
           }
         }
+  } else if constexpr (LSE) {
+    // merge the row's four lane groups: (m, s) + (m', s') relative to max(m, m')
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      float m = lm[rb], t = ls[rb];
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        const float m2 = __shfl_xor(m, o), t2 = __shfl_xor(t, o);
+        const float nm = fmaxf(m, m2);
+        t = t * __builtin_amdgcn_exp2f(m - nm) + t2 * __builtin_amdgcn_exp2f(m2 - nm);
+        m = nm;
+      }
+      const int64_t row = i0 + 16 * rb + li;
+      if (g != 0 || row >= rend) continue;
+      if (a.C == 1) {
+        // an empty row (t = 0) gives -infinity
+        static_cast<float*>(a.out)[row] = (m + __builtin_amdgcn_logf(t)) * kLn2;
+      } else {
+        float* pp = a.part + ((int64_t)c * a.M + row) * 2;   // the (m, s) pair the combine merges
+        pp[0] = t > 0.0f ? m : -__builtin_inff();
+        pp[1] = t;
+      }
+    }
   } else {
     // one partial list per (column block, lane group); the second pass merges them
 #pragma unroll
@@ -794,7 +849,8 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         const int d = 32 * ch + 8 * g + t;
-        const float v = (ok && d < a.D) ? a.x[row * a.D + d] * a.xscale : 0.0f;
+        const float v =
+          (ok && d < a.D) ? (a.x[row * a.D + d] - (a.xc != nullptr ? a.xc[d] : 0.0f)) * a.xscale : 0.0f;
         __bf16 h, m, l;
         split3(v, h, m, l);
         xh[rb][ch][t] = h;
@@ -998,6 +1054,9 @@ hipError_t launch_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
     case 0: return launch_sum_q<Q, 0, SP>(a, grid, s);
     case 1: return launch_sum_q<Q, 1, SP>(a, grid, s);
     case 2: return launch_sum_q<Q, 2, SP>(a, grid, s);
+    case 4:
+      hipLaunchKernelGGL((mfma_kernel<Q, RB, 4, 1, 1, SP>), grid, dim3(256), 0, s, a);
+      return hipGetLastError();
     case 3:
       switch (a.KP) {
 #define KRED_KNN_F32(KPV, RBV)                                                                 \
@@ -1034,16 +1093,20 @@ int mfma_rows_per_block(int DP, int KP) {
   return 64 * ((Q >= 64 || KP == 64) ? 1 : 2);
 }
 
-// ------------------------------------------ fused value + gradient, large D
+// ------------------------------------------ centre; fused gradient, large D
+// Distances do not change when x and y move by the same point m; taking m
+// inside the data (the mean of up to the first 1024 rows of y) keeps the
+// expanded form's cancellation, |x|^2 + |y|^2 - 2 <x, y>, at the scale of the
+// data's spread rather than its distance from the origin.
 // The Gaussian sum's x-gradient g_i = sum_j k_ij b_j (y_j - x_i) / sigma^2
 // (the derivative of Eq. (1)) is, for any point m, (A1_i - (x_i - m) A0_i) /
 // sigma^2 with A0 = K b and A1 = K [b (y - m)]: one Gaussian sum with D + 1
-// signal columns.  m is the mean of up to the first 1024 rows of y, so that
-// |y - m| stays of the order of |y - x| and the subtraction loses little.
+// signal columns; with the same m, |y - m| stays of the order of |y - x| and
+// the subtraction loses little.
 
 namespace {
 
-__global__ __launch_bounds__(256) void gradx_centre_kernel(const float* __restrict__ y, int64_t N,
+__global__ __launch_bounds__(256) void centre_kernel(const float* __restrict__ y, int64_t N,
                                                            int D, float* __restrict__ m) {
   const int d = threadIdx.x;
   if (d >= D) return;
@@ -1099,8 +1162,8 @@ int64_t grid_of(int64_t items) {
 
 }  // namespace
 
-hipError_t launch_gradx_centre(const float* y, int64_t N, int D, float* m, hipStream_t s) {
-  hipLaunchKernelGGL(gradx_centre_kernel, dim3(1), dim3(256), 0, s, y, N, D, m);
+hipError_t launch_centre(const float* y, int64_t N, int D, float* m, hipStream_t s) {
+  hipLaunchKernelGGL(centre_kernel, dim3(1), dim3(256), 0, s, y, N, D, m);
   return hipGetLastError();
 }
 

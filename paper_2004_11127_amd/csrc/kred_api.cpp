@@ -233,6 +233,20 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
     q.coord_scale = 1.0f;
     q.nrm_sign = 1.0f;
     q.pad_norm = INFINITY;
+  } else if (r == KRED_R_LSE) {
+    // s_ij = g_j - d_ij / eps in log2 units (the Gaussian's log-domain sum is
+    // the same with eps = 2 sigma^2): x and y scaled by sqrt(log2(e) / eps),
+    // the column norms carry g_j log2(e), padding columns s = -inf
+    q.epi = 4;
+    q.EB = 1;
+    const double eps = f == KRED_F_SINKHORN ? (double)p->eps
+                                            : 2.0 * (double)p->sigma * (double)p->sigma;
+    const double sc = std::sqrt(log2e / eps);
+    q.xscale = (float)sc;
+    q.coord_scale = (float)sc;
+    q.yop_scale = (float)(2.0 * sc);
+    q.nrm_sign = -1.0f;
+    q.pad_norm = -INFINITY;
   } else {
     q.EB = E <= 16 ? 1 : (E <= 32 ? 2 : 4);
     double sc = 1.0;
@@ -264,9 +278,12 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   q.C = (int)((q.N16 + jpb - 1) / jpb);
   q.yop_bytes = align_up(q.N16 * q.DP * (int64_t)sizeof(float));
   q.ny_bytes = align_up(q.N16 * (int64_t)sizeof(float));
-  q.b_bytes = (r == KRED_R_ARGKMIN) ? 0 : align_up(q.N16 * q.W * (int64_t)sizeof(float));
+  q.b_bytes = (r == KRED_R_ARGKMIN || r == KRED_R_LSE)
+                  ? 0 : align_up(q.N16 * q.W * (int64_t)sizeof(float));
   if (r == KRED_R_ARGKMIN)
     q.part_bytes = align_up((int64_t)4 * q.C * M * 2 * q.KP * (int64_t)sizeof(float));
+  else if (r == KRED_R_LSE)
+    q.part_bytes = q.C > 1 ? align_up((int64_t)q.C * M * 2 * (int64_t)sizeof(float)) : 0;
   else
     q.part_bytes = q.C > 1 ? align_up((int64_t)q.C * M * q.W * (int64_t)sizeof(float)) : 0;
   *pl = q;
@@ -354,20 +371,25 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   if (rg) pl.C = std::max(1, std::min(p->col_blocks, KRED_MAX_COL_BLOCKS));   // chunks per cluster
   const int64_t rows_wg = mfma_rows_per_block(pl.DP, pl.KP);
   const bool knn = (r == KRED_R_ARGKMIN);
+  const bool lse = (r == KRED_R_LSE);
   // arg-K-min: the exact bf16 kernel is a candidate (the device decides);
-  // sums: the split bf16 kernel replaces the fp32 one
+  // sums: the split bf16 kernel replaces the fp32 one; log-sum-exp: fp32 only
   const bool exact = knn && exact_knn_eligible(p->flags, M, N);
-  const bool split = !knn && exact_eligible(p->flags, M, N);
+  const bool split = !knn && !lse && exact_eligible(p->flags, M, N);
   const int64_t ybf_bytes = mfma_bf16_bytes(pl, knn, p->flags, M, N);
   if (rg) {   // partials of every chunk (rows outside the clusters read the empty value)
     pl.part_bytes = knn ? align_up((int64_t)4 * pl.C * M * 2 * pl.KP * (int64_t)sizeof(float))
-                  : pl.C > 1 ? align_up((int64_t)pl.C * M * pl.W * (int64_t)sizeof(float))
+                  : pl.C > 1 ? align_up((int64_t)pl.C * M * (lse ? 2 : pl.W) * (int64_t)sizeof(float))
                              : 0;
   }
   const int64_t bstart_bytes = rg ? align_up((int64_t)(rg->nr + 1) * (int64_t)sizeof(int)) : 0;
+  // sums and log-sum-exp: x and y are centred on a point of y (distances do
+  // not change; the expanded form's cancellation then scales with the spread
+  // of the data, not with its distance from the origin)
+  const int64_t cen_bytes = knn ? 0 : align_up((int64_t)D * (int64_t)sizeof(float));
   const kred_status gs = grow_scratch(
       ctx, (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes + ybf_bytes +
-                    bstart_bytes));
+                    bstart_bytes + cen_bytes));
   if (gs != KRED_OK) return gs;
   if (exact && ctx->exact_guard == nullptr &&
       hipMalloc(reinterpret_cast<void**>(&ctx->exact_guard), sizeof(ExactGuard)) != hipSuccess) {
@@ -387,6 +409,10 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   int* bstart = rg ? reinterpret_cast<int*>(base + pl.yop_bytes + pl.ny_bytes + pl.b_bytes +
                                             pl.part_bytes + ybf_bytes)
                    : nullptr;
+  float* cen = knn ? nullptr
+                   : reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes + pl.b_bytes +
+                                              pl.part_bytes + ybf_bytes + bstart_bytes);
+  if (cen && launch_centre(y, N, D, cen, s) != hipSuccess) return KRED_ERR_HIP;
   ExactGuard* eg = exact ? ctx->exact_guard : nullptr;
   if (exact && launch_exact_check(x, M, y, N, D, eg, s) != hipSuccess) return KRED_ERR_HIP;
   if (rg) {
@@ -396,20 +422,26 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     if (knn && launch_fill2(part, (int64_t)4 * pl.C * M * 2 * pl.KP, INFINITY,
                             __builtin_bit_cast(float, (int32_t)INT32_MAX), s) != hipSuccess)
       return KRED_ERR_HIP;
-    if (!knn && pl.C > 1 && launch_fill(part, (int64_t)pl.C * M * pl.W, 0.0f, s) != hipSuccess)
+    if (lse && pl.C > 1 && launch_fill2(part, (int64_t)pl.C * M * 2, -INFINITY, 0.0f, s) != hipSuccess)
+      return KRED_ERR_HIP;
+    if (!knn && !lse && pl.C > 1 &&
+        launch_fill(part, (int64_t)pl.C * M * pl.W, 0.0f, s) != hipSuccess)
       return KRED_ERR_HIP;
   }
 
   MfmaPackArgs pa{};
   pa.y = y;
-  pa.b = knn ? nullptr : b;
+  pa.b = (knn || lse) ? nullptr : b;
   pa.N = N;
   pa.N16 = pl.N16;
   pa.D = D;
   pa.DP = pl.DP;
   pa.E = E;
   pa.e0 = 0;
-  pa.Ec = knn ? 0 : E;
+  pa.Ec = (knn || lse) ? 0 : E;
+  pa.goff = lse ? b : nullptr;
+  pa.goff_scale = 1.4426950408889634f;
+  pa.yc = cen;
   pa.EB = pl.EB;
   pa.yop_scale = pl.yop_scale;
   pa.coord_scale = pl.coord_scale;
@@ -448,6 +480,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   ma.ysp = split ? ybf : nullptr;
   ma.N = N;
   ma.pad_ny = pl.pad_norm;
+  ma.xc = cen;
   if (rg) {
     ma.nr = rg->nr;
     ma.rr = rg->rr;
@@ -476,7 +509,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   }
   if (knn || pl.C > 1) {
     CombineArgs ca{};
-    ca.formula = knn ? (int)KRED_F_SQDIST : (int)f;
+    ca.formula = knn ? (int)KRED_F_SQDIST : lse ? (int)F_SINKHORN : (int)f;
     ca.D = D;
     ca.DP = pl.DP;
     ca.E = E;
@@ -514,8 +547,6 @@ void empty_fill(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   }
 }
 
-// One reduction on validated arguments, M > 0, on the current device;
-// block-sparse when rg is given.
 // Bytes of the large-D fused gradient's own buffer: the centre, one signal
 // chunk (N x 64) and the sums (M x (D + 1)).
 int64_t gradx_wide_bytes(int64_t M, int64_t N, int32_t D) {
@@ -540,7 +571,7 @@ kred_status run_gradx_wide(kred_ctx* ctx, const kred_params* p, int64_t M, int64
   const int W = D + 1;
   // rows outside every cluster read zero sums (a zero value and gradient)
   if (rg && launch_fill(T, M * W, 0.0f, s) != hipSuccess) return KRED_ERR_HIP;
-  if (launch_gradx_centre(y, N, D, m, s) != hipSuccess) return KRED_ERR_HIP;
+  if (launch_centre(y, N, D, m, s) != hipSuccess) return KRED_ERR_HIP;
   for (int c0 = 0; c0 < W; c0 += 64) {
     const int Ec = std::min(64, W - c0);
     if (launch_gradx_signal(y, b, N, D, m, c0, Ec, sig, s) != hipSuccess) return KRED_ERR_HIP;
@@ -554,6 +585,8 @@ kred_status run_gradx_wide(kred_ctx* ctx, const kred_params* p, int64_t M, int64
              : KRED_ERR_HIP;
 }
 
+// One reduction on validated arguments, M > 0, on the current device;
+// block-sparse when rg is given.
 kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                           int64_t M, int64_t N, int32_t D, int32_t E, const float* x,
                           const float* y, const float* b, void* out, hipStream_t s,
@@ -992,7 +1025,10 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
   const bool lists = f == KRED_F_SQDIST && b == nullptr &&
                      (r == KRED_R_ARGKMIN || r == KRED_R_KMIN || r == KRED_R_MIN ||
                       r == KRED_R_ARGMIN);
-  if (D > kMaxDirectD && (f == KRED_F_SINKHORN || r == KRED_R_LSE || (is_extreme(r) && !lists)))
+  // and the log-sum-exp of the Sinkhorn form and of the Gaussian
+  const bool lse_wide = r == KRED_R_LSE && (f == KRED_F_SINKHORN || f == KRED_F_GAUSS);
+  if (D > kMaxDirectD && !lse_wide &&
+      (f == KRED_F_SINKHORN || r == KRED_R_LSE || (is_extreme(r) && !lists)))
     return KRED_ERR_UNSUPPORTED;
   if (M == 0) return KRED_OK;
   if (x == nullptr || out == nullptr) return KRED_ERR_INVALID_ARG;
@@ -1027,6 +1063,7 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
       return -1;
     return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes +
            mfma_bf16_bytes(mp, r == KRED_R_ARGKMIN, p->flags, M, N) +
+           (r == KRED_R_ARGKMIN ? 0 : align_up((int64_t)D * (int64_t)sizeof(float))) +
            (wide ? gradx_wide_bytes(M, N, D) : 0);
   }
   const int epi = fast_epi(f, r, M, N, D, E, p->flags, p->K);

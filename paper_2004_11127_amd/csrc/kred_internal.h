@@ -190,21 +190,26 @@ struct MfmaPackArgs {
   unsigned short* ybf;       // bf16 copy of yop (N16 x DP), written instead of yop when exact
   unsigned short* ysp;       // sums on the split path: yop as 3 bf16 planes (N16 x 3 x DP), written
                              // instead of yop
+  const float* goff;         // log-sum-exp: per-column offset g (N), added to ny times goff_scale
+  float goff_scale;
+  const float* yc;           // sums and log-sum-exp: a centre (D) subtracted from y, else null
 };
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
 
+// A centre of y for the large-D kernels: m = the mean of its first min(N, 1024)
+// rows (D floats; zeros when N = 0).
+hipError_t launch_centre(const float* y, int64_t N, int D, float* m, hipStream_t s);
 // Fused Gaussian value + x-gradient for 16 < D <= 256 as one Gaussian sum with
-// D + 1 signal columns [b, b (y - m)]: the centre m (D floats), the signal
-// columns [c0, c0 + Ec) (N x Ec), and the output M x (1 + D) from the sums T
-// (column c in chunk c / 64, stored M x Ec_q at T + 64 M q).
-hipError_t launch_gradx_centre(const float* y, int64_t N, int D, float* m, hipStream_t s);
+// D + 1 signal columns [b, b (y - m)]: the signal columns [c0, c0 + Ec)
+// (N x Ec), and the output M x (1 + D) from the sums T (column c in chunk
+// c / 64, stored M x Ec_q at T + 64 M q).
 hipError_t launch_gradx_signal(const float* y, const float* b, int64_t N, int D, const float* m,
                                int c0, int Ec, float* sig, hipStream_t s);
 hipError_t launch_gradx_finish(const float* x, int64_t M, int D, const float* m, const float* T,
                                float gscale, float* out, hipStream_t s);
 
 struct MfmaArgs {
-  int epi;        // 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min
+  int epi;        // 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min, 4 log-sum-exp
   int D, DP, E, e0, EB;
   int64_t M, N16;
   int C;          // column blocks
@@ -229,6 +234,7 @@ struct MfmaArgs {
   const int* cp;
   const int* cr;
   const int* bstart;
+  const float* xc;   // sums and log-sum-exp: the centre (D) subtracted from x, as from y
 };
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
 // Exact-path prologue: reset the guard, then fold every coordinate of x and y into it.
