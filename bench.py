@@ -52,6 +52,11 @@ WORKLOADS = {
     "gradx_d128": ("highdim_gauss", dict(M=200_000, N=200_000, D=128, E=1, sigma=1.0),
                    "gauss_gradx", "sum", 2 * 128 + 3 + 2 * 129, "mfma",
                    "gaussian kernel sum + x-gradient (fused), N(0, I/128), 2e5 x 2e5, D=128"),
+    # Sinkhorn log-sum-exp at D = 64 on the fp32 matrix cores (2D flops for the
+    # inner product, 3 for the norms and g, 3 for the running log-sum-exp)
+    "lse_d64": ("sinkhorn_lse", dict(M=200_000, N=200_000, D=64, eps=1.0), "sinkhorn", "lse",
+                2 * 64 + 6, "mfma", "sinkhorn log-sum-exp, uniform / shifted uniform, 2e5 x 2e5, "
+                                    "D=64, eps=1"),
     # the integer coordinates pass the library's exactness guard, so the contraction
     # runs on the bf16 matrix cores
     "c5": ("integer_knn", dict(M=100_000, N=1_000_000, D=64, K=10), "sqdist", "argkmin",
