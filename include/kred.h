@@ -249,9 +249,10 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
  * kred_run (KRED_FLAG_DIRECT / KRED_FLAG_FAST steer the path of every
  * reduction in the call; KRED_FLAG_PROFILE times each main kernel); p->eps
  * and p->K are ignored.  Ranges: 0 <= M, N <= 2^31 - 1, 1 <= D <= KRED_MAX_D,
- * 1 <= E <= KRED_MAX_E; for D > 16, gx and gy need E = 1 (they run on the
- * fused value + gradient; gx or gy with E > 1 there returns
- * KRED_ERR_UNSUPPORTED) while gb takes any E.  With M = 0 or N = 0
+ * 1 <= E <= KRED_MAX_E.  For D > 16, gx and gy run as one Gaussian sum with
+ * the E (D + 1) signal columns [b_e, b_e (y - m)] (m a centre of y), 64
+ * columns per matrix-core launch, contracted with the cotangent; scratch
+ * grows by about (M + 64 N) E (D + 1) floats.  With M = 0 or N = 0
  * the requested outputs are filled with zeros.  x, y and e are required, and
  * b too for gx or gy, whenever M, N > 0 and an output is requested.  Same
  * error and asynchrony rules as kred_run: on any argument error nothing runs.

@@ -1116,17 +1116,51 @@ __global__ __launch_bounds__(256) void centre_kernel(const float* __restrict__ y
   m[d] = n > 0 ? s / (float)n : 0.0f;
 }
 
-// columns [c0, c0 + Ec) of the signal [b, b (y - m)]: N x Ec, row-major
+// columns [c0, c0 + Ec) of the signal [b_e, b_e (y - m)] for e = 0..E-1
+// (column e (D + 1) + k): N x Ec, row-major
 __global__ __launch_bounds__(256) void gradx_signal_kernel(const float* __restrict__ y,
                                                            const float* __restrict__ b, int64_t N,
-                                                           int D, const float* __restrict__ m,
+                                                           int D, int E, const float* __restrict__ m,
                                                            int c0, int Ec, float* __restrict__ sig) {
   const int64_t total = N * Ec;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
        t += (int64_t)gridDim.x * blockDim.x) {
     const int64_t j = t / Ec;
     const int c = c0 + (int)(t - j * Ec);
-    sig[t] = c == 0 ? b[j] : b[j] * (y[j * D + c - 1] - m[c - 1]);
+    const int e = c / (D + 1), k = c - e * (D + 1);
+    const float be = b[j * E + e];
+    sig[t] = k == 0 ? be : be * (y[j * D + k - 1] - m[k - 1]);
+  }
+}
+
+// column c of the sums T (M x W in chunks of 64 columns, chunk q stored M x Ec_q
+// at T + 64 M q)
+__device__ __forceinline__ float wide_at(const float* __restrict__ T, int64_t M, int W, int64_t i,
+                                         int c) {
+  const int q = c / 64, last = (W - 1) / 64;
+  const int ec = q == last ? W - 64 * last : 64;
+  return T[64 * M * q + i * ec + (c - 64 * q)];
+}
+
+// the vector-Jacobian product: out[i, d] = gscale sum_e e_ie (A_e,1+d - (x_id - m_d) A_e,0)
+__global__ __launch_bounds__(256) void vjp_finish_kernel(const float* __restrict__ x, int64_t M,
+                                                         int D, int E, const float* __restrict__ m,
+                                                         const float* __restrict__ T,
+                                                         const float* __restrict__ e,
+                                                         float gscale, float* __restrict__ out) {
+  const int W = E * (D + 1);
+  const int64_t total = M * D;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = t / D;
+    const int d = (int)(t - i * D);
+    const float xd = x[i * D + d] - m[d];
+    float acc = 0.0f;
+    for (int f = 0; f < E; ++f) {
+      const int c = f * (D + 1);
+      acc = __builtin_fmaf(e[i * E + f], wide_at(T, M, W, i, c + 1 + d) - xd * wide_at(T, M, W, i, c), acc);
+    }
+    out[t] = acc * gscale;
   }
 }
 
@@ -1167,11 +1201,20 @@ hipError_t launch_centre(const float* y, int64_t N, int D, float* m, hipStream_t
   return hipGetLastError();
 }
 
-hipError_t launch_gradx_signal(const float* y, const float* b, int64_t N, int D, const float* m,
-                               int c0, int Ec, float* sig, hipStream_t s) {
+hipError_t launch_gradx_signal(const float* y, const float* b, int64_t N, int D, int E,
+                               const float* m, int c0, int Ec, float* sig, hipStream_t s) {
   if (N == 0) return hipSuccess;
   hipLaunchKernelGGL(gradx_signal_kernel, dim3((unsigned)grid_of(N * Ec)), dim3(256), 0, s, y, b,
-                     N, D, m, c0, Ec, sig);
+                     N, D, E, m, c0, Ec, sig);
+  return hipGetLastError();
+}
+
+hipError_t launch_vjp_finish(const float* x, int64_t M, int D, int E, const float* m,
+                             const float* T, const float* e, float gscale, float* out,
+                             hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  hipLaunchKernelGGL(vjp_finish_kernel, dim3((unsigned)grid_of(M * D)), dim3(256), 0, s, x, M, D,
+                     E, m, T, e, gscale, out);
   return hipGetLastError();
 }
 

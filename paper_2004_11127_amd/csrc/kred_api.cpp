@@ -547,42 +547,48 @@ void empty_fill(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   }
 }
 
-// Bytes of the large-D fused gradient's own buffer: the centre, one signal
-// chunk (N x 64) and the sums (M x (D + 1)).
-int64_t gradx_wide_bytes(int64_t M, int64_t N, int32_t D) {
+// Bytes of the large-D gradient's own buffer: the centre, one signal chunk
+// (N x 64) and the sums (M x E (D + 1)).
+int64_t gradx_wide_bytes(int64_t M, int64_t N, int32_t D, int32_t E = 1) {
+  const int64_t W = (int64_t)E * (D + 1);
   return align_up((int64_t)D * (int64_t)sizeof(float)) +
-         align_up(N * std::min(64, D + 1) * (int64_t)sizeof(float)) +
-         align_up(M * (D + 1) * (int64_t)sizeof(float));
+         align_up(N * std::min<int64_t>(64, W) * (int64_t)sizeof(float)) +
+         align_up(M * W * (int64_t)sizeof(float));
 }
 
-// GAUSS_GRADX for 16 < D <= 256 (validated, M, N > 0, E = 1): the Gaussian sum
-// on the matrix cores with the D + 1 signal columns [b, b (y - m)], 64 columns
-// per call, then out = (A0, (A1 - (x - m) A0) / sigma^2).
+// Gaussian x-gradients for 16 < D <= 256 (validated, M, N > 0) as one Gaussian
+// sum on the matrix cores with the E (D + 1) signal columns [b_e, b_e (y - m)],
+// 64 columns per call.  Without a cotangent (e = NULL, E = 1): GAUSS_GRADX,
+// out = (A0, (A1 - (x - m) A0) / sigma^2), M x (1 + D).  With a cotangent e
+// (M x E): the vector-Jacobian product out = sum_e e_e (A_e,1 - (x - m) A_e,0)
+// / sigma^2, M x D.
 kred_status run_gradx_wide(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, int32_t D,
-                           const float* x, const float* y, const float* b, float* out,
-                           hipStream_t s, const Ranges* rg) {
-  const kred_status ga = grow_buffer(&ctx->wide, &ctx->wide_bytes, (size_t)gradx_wide_bytes(M, N, D));
+                           int32_t E, const float* x, const float* y, const float* b,
+                           const float* e, float* out, hipStream_t s, const Ranges* rg) {
+  const kred_status ga =
+      grow_buffer(&ctx->wide, &ctx->wide_bytes, (size_t)gradx_wide_bytes(M, N, D, E));
   if (ga != KRED_OK) return ga;
+  const int W = E * (D + 1);
   char* base = static_cast<char*>(ctx->wide);
   float* m = reinterpret_cast<float*>(base);
   float* sig = reinterpret_cast<float*>(base + align_up((int64_t)D * (int64_t)sizeof(float)));
   float* T = reinterpret_cast<float*>(reinterpret_cast<char*>(sig) +
-                                      align_up(N * std::min(64, D + 1) * (int64_t)sizeof(float)));
-  const int W = D + 1;
+                                      align_up(N * std::min(64, W) * (int64_t)sizeof(float)));
   // rows outside every cluster read zero sums (a zero value and gradient)
   if (rg && launch_fill(T, M * W, 0.0f, s) != hipSuccess) return KRED_ERR_HIP;
   if (launch_centre(y, N, D, m, s) != hipSuccess) return KRED_ERR_HIP;
   for (int c0 = 0; c0 < W; c0 += 64) {
     const int Ec = std::min(64, W - c0);
-    if (launch_gradx_signal(y, b, N, D, m, c0, Ec, sig, s) != hipSuccess) return KRED_ERR_HIP;
+    if (launch_gradx_signal(y, b, N, D, E, m, c0, Ec, sig, s) != hipSuccess) return KRED_ERR_HIP;
     const kred_status st = run_mfma(ctx, KRED_F_GAUSS, KRED_R_SUM, p, M, N, D, Ec, x, y, sig,
                                     T + (int64_t)c0 * M, s, 0, rg);
     if (st != KRED_OK) return st;
   }
   const double sg = (double)p->sigma;
-  return launch_gradx_finish(x, M, D, m, T, (float)(1.0 / (sg * sg)), out, s) == hipSuccess
-             ? KRED_OK
-             : KRED_ERR_HIP;
+  const float gs = (float)(1.0 / (sg * sg));
+  const hipError_t fin = e ? launch_vjp_finish(x, M, D, E, m, T, e, gs, out, s)
+                           : launch_gradx_finish(x, M, D, m, T, gs, out, s);
+  return fin == hipSuccess ? KRED_OK : KRED_ERR_HIP;
 }
 
 // One reduction on validated arguments, M > 0, on the current device;
@@ -617,7 +623,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   const int kf = (r == KRED_R_LSE) ? (f == KRED_F_LAPLACE ? F_LAPLACE_LSE : F_SINKHORN) : (int)f;
 
   if (D > kMaxDirectD && f == KRED_F_GAUSS_GRADX)
-    return run_gradx_wide(ctx, p, M, N, D, x, y, b, static_cast<float*>(out), s, rg);
+    return run_gradx_wide(ctx, p, M, N, D, 1, x, y, b, nullptr, static_cast<float*>(out), s, rg);
   if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s, kvalues, rg);
 
   kred_params pr;
@@ -839,6 +845,9 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
 kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, int32_t D,
                     int32_t E, const float* x, const float* y, const float* b, const float* e,
                     float* g, hipStream_t s, const Ranges* rg = nullptr) {
+  // 16 < D <= 256 with several signal columns: the Gaussian sum with the
+  // E (D + 1) columns [b_e, b_e (y - m)], contracted with e
+  if (D > kMaxDirectD && E > 1) return run_gradx_wide(ctx, p, M, N, D, E, x, y, b, e, g, s, rg);
   if (E == 1 && (D > kMaxDirectD || fast_epi(KRED_F_GAUSS_GRADX, KRED_R_SUM, M, N, D, 1, p->flags) >= 0)) {
     const kred_status ga =
         grow_buffer(&ctx->aux, &ctx->aux_bytes, (size_t)(M * (1 + D) * (int64_t)sizeof(float)));
@@ -1168,9 +1177,7 @@ kred_status kred_validate_backward(const kred_params* p, int64_t M, int64_t N, i
   if (p->col_blocks < 0 || p->col_blocks > KRED_MAX_COL_BLOCKS) return KRED_ERR_INVALID_ARG;
   if (M < 0 || N < 0 || M > INT32_MAX || N > INT32_MAX) return KRED_ERR_INVALID_ARG;
   if (D < 1 || D > KRED_MAX_D || E < 1 || E > KRED_MAX_E) return KRED_ERR_INVALID_ARG;
-  // 16 < D <= 256: gx and gy for a scalar cotangent (the fused value +
-  // gradient on the matrix cores), gb for any E (a Gaussian sum)
-  if (D > kMaxDirectD && E > 1 && (gx || gy)) return KRED_ERR_UNSUPPORTED;
+
   // Inputs the requested outputs read.  With M = 0 or N = 0 every reduction
   // is empty and the outputs are filled with zeros without reading any input.
   if (M > 0 && N > 0 && (gx || gy || gb)) {

@@ -200,13 +200,17 @@ hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
 // rows (D floats; zeros when N = 0).
 hipError_t launch_centre(const float* y, int64_t N, int D, float* m, hipStream_t s);
 // Fused Gaussian value + x-gradient for 16 < D <= 256 as one Gaussian sum with
-// D + 1 signal columns [b, b (y - m)]: the signal columns [c0, c0 + Ec)
-// (N x Ec), and the output M x (1 + D) from the sums T (column c in chunk
-// c / 64, stored M x Ec_q at T + 64 M q).
-hipError_t launch_gradx_signal(const float* y, const float* b, int64_t N, int D, const float* m,
-                               int c0, int Ec, float* sig, hipStream_t s);
+// E (D + 1) signal columns [b_e, b_e (y - m)]: the signal columns [c0, c0 + Ec)
+// (N x Ec), and from the sums T (column c in chunk c / 64, stored M x Ec_q at
+// T + 64 M q) either the output M x (1 + D) (E = 1) or, for a cotangent e
+// (M x E), the vector-Jacobian product M x D.
+hipError_t launch_gradx_signal(const float* y, const float* b, int64_t N, int D, int E,
+                               const float* m, int c0, int Ec, float* sig, hipStream_t s);
 hipError_t launch_gradx_finish(const float* x, int64_t M, int D, const float* m, const float* T,
                                float gscale, float* out, hipStream_t s);
+hipError_t launch_vjp_finish(const float* x, int64_t M, int D, int E, const float* m,
+                             const float* T, const float* e, float gscale, float* out,
+                             hipStream_t s);
 
 struct MfmaArgs {
   int epi;        // 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min, 4 log-sum-exp

@@ -163,13 +163,12 @@ def test_backward_invalid_arguments(lib):
 
 
 def test_backward_large_d(lib):
-    # 16 < D <= 256: scalar cotangents (the fused value + gradient on the matrix
-    # cores) and gb for any E; gx, gy with E > 1 are not served there
+    # 16 < D <= 256 on the matrix cores, any E
     assert VB(100, 200, 17, 1, sigma=1.0) == OK
     assert VB(100, 200, 256, 1, sigma=1.0) == OK
     assert VB(100, 200, 64, 8, gx=None, gy=None, sigma=1.0) == OK
-    assert VB(100, 200, 64, 8, sigma=1.0) == UNSUPPORTED
-    assert VB(100, 200, 64, 8, gx=None, gb=None, sigma=1.0) == UNSUPPORTED
+    assert VB(100, 200, 64, 8, sigma=1.0) == OK
+    assert VB(100, 200, 256, 64, sigma=1.0) == OK
     assert VB(100, 200, 257, 1, sigma=1.0) == INVALID
 
 
@@ -273,5 +272,5 @@ def test_backward_ranges_validation(lib):
     assert VBR(100, 200, 3, 1, 5, 7, rp=2, sigma=0.1) == INVALID                # misaligned
     # the dense backward's rules
     assert VBR(100, 200, 3, 1, 5, 7, sigma=0.0) == INVALID
-    assert VBR(100, 200, 17, 4, 5, 7, sigma=1.0) == UNSUPPORTED              # gx, gy with E > 1
+    assert VBR(100, 200, 17, 4, 5, 7, sigma=1.0) == OK
     assert VBR(100, 200, 3, 1, 5, 7, b=None, sigma=1.0) == INVALID

@@ -7,8 +7,9 @@ oracle's gauss_gradx (the definition, any D), normalised per component by the
 sum of absolute summands as for the small-D gradient, on both matrix-core
 kernels (fp32 products, and the three-way bf16 split), with column splits,
 data far from the origin (where the centring matters), one and several
-signal chunks, block-sparse patterns, and the Gaussian backward with a scalar
-cotangent (gx, gy) and with E signal columns (gb) at these D.
+signal chunks, block-sparse patterns, and the Gaussian backward at these D
+with scalar cotangents (the fused value + gradient) and with E signal columns
+(one Gaussian sum with E (D + 1) columns contracted with the cotangent).
 """
 import numpy as np
 import pytest
@@ -93,26 +94,30 @@ def test_backward_large_d_scalar_cotangent(ctx, D, E):
     assert norm_err(host(gb), ref, norm) <= SUM_TOL
 
 
-def test_backward_large_d_signal_gradient(ctx):
-    # E > 1 at large D: gb (a Gaussian sum) is served, gx and gy are not
-    from paper_2004_11127_amd import kred
-    M, N, D, E = 500, 700, 64, 6
-    x, y, b = _data(3, M, N, D, E=E)
+@pytest.mark.parametrize("M,N,D,E,offset", [(500, 700, 64, 6, 0.0), (300, 450, 17, 2, 2.0),
+                                             (200, 333, 130, 3, 0.5), (150, 260, 40, 64, 0.0)])
+def test_backward_large_d_signal_gradient(ctx, M, N, D, E, offset):
+    # E > 1 at large D: gx and gy from the Gaussian sum with the E (D + 1)
+    # columns [b_e, b_e (y - m)] contracted with e, gb a Gaussian sum
+    x, y, b = _data(3 + E, M, N, D, offset=offset, E=E)
     e = np.random.default_rng(2).standard_normal((M, E)).astype(np.float32)
-    _, _, gb = ctx.gauss_backward(dev(x), dev(y), dev(b), dev(e), sigma=1.0, gx=False, gy=False)
+    gx, gy, gb = ctx.gauss_backward(dev(x), dev(y), dev(b), dev(e), sigma=1.0)
+    ref, norm = oracle.gauss_vjp(x, y, b, e, 1.0)
+    assert norm_err(host(gx), ref, norm) <= SUM_TOL
+    ref, norm = oracle.gauss_vjp(y, x, e, b, 1.0)
+    assert norm_err(host(gy), ref, norm) <= SUM_TOL
     ref, norm = oracle.kernel_sum("gauss", y, x, e, sigma=1.0)
     assert norm_err(host(gb), ref, norm) <= SUM_TOL
-    with pytest.raises(kred.KredError):
-        ctx.gauss_backward(dev(x), dev(y), dev(b), dev(e), sigma=1.0)
 
 
-def test_backward_ranges_large_d(ctx):
+@pytest.mark.parametrize("E", [1, 3])
+def test_backward_ranges_large_d(ctx, E):
     from paper_2004_11127_amd import clusters
     from test_gpu_ranges import random_pattern
     rng = np.random.default_rng(11)
     M, N, D = 900, 1100, 40
-    x, y, b = _data(12, M, N, D, offset=0.3)
-    e = rng.standard_normal((M, 1)).astype(np.float32)
+    x, y, b = _data(12, M, N, D, offset=0.3, E=E)
+    e = rng.standard_normal((M, E)).astype(np.float32)
     pat = random_pattern(rng, M, N, 8, 10)
     tr = clusters.transpose_pattern(*pat, M, N)
     gx, gy, gb = ctx.gauss_backward_ranges(dev(x), dev(y), dev(b), dev(e),
