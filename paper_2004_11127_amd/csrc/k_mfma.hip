@@ -77,6 +77,11 @@ __global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
       a.yop[t] = v * a.yop_scale;
     }
   }
+  // Laplacian log-sum-exp: g' = g log2(e) per column, -infinity for padding
+  if (a.gpk != nullptr) {
+    for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < a.N16; j += stride)
+      a.gpk[j] = j < a.N ? a.goff[j] * a.goff_scale : -__builtin_inff();
+  }
   // signal tiles: b[j][e0 + e] stored at (j/16)*16W + ((j%16)/4)*4W + e*4 + j%4, W = 16*EB
   if (a.bpk != nullptr) {
     const int W = 16 * a.EB;
@@ -107,7 +112,8 @@ __global__ __launch_bounds__(256) void mfma_norm_kernel(MfmaPackArgs a) {
       }
     for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
     if (lane == 0)
-      a.ny[j] = j < a.N ? a.nrm_sign * s + (a.goff != nullptr ? a.goff[j] * a.goff_scale : 0.0f)
+      a.ny[j] = j < a.N ? a.nrm_sign * s + ((a.goff != nullptr && a.gpk == nullptr)
+                                                ? a.goff[j] * a.goff_scale : 0.0f)
                         : a.pad_norm;
   }
 }
@@ -270,7 +276,8 @@ __device__ __forceinline__ int64_t bpk_col(int64_t jt, int t4, int W) {
 }
 
 // EPI: 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min, 4 log-sum-exp
-// of s_ij = g_j - |x_i - y_j|^2 / eps (log2 units: the column norms carry g_j).
+// of s_ij = g_j - |x_i - y_j|^2 / eps (log2 units: the column norms carry g_j),
+// 5 log-sum-exp of s_ij = g_j - |x_i - y_j| / sigma (g_j from its own array).
 // SP: block-sparse (a pattern of row clusters and column ranges) or dense.
 template <int Q, int RB, int EPI, int EB, int KP, bool SP>
 __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
@@ -278,7 +285,8 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
   constexpr int LDY = DP + 4;
   constexpr int TJ = tile_cols(DP);
   constexpr bool SUM = EPI < 3;
-  constexpr bool LSE = EPI == 4;
+  constexpr bool LSE = EPI >= 4;
+  constexpr bool LAPG = EPI == 5;   // per-column g' staged like the norms
   constexpr int W = 16 * EB;                       // signal columns per row in a tile
   constexpr int YF4 = TJ * DP / 4;                 // float4s of y per tile
   constexpr int YL = (YF4 + 255) / 256;            // per thread
@@ -289,6 +297,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
   __shared__ float4 ys[2][TJ * LDY / 4];
   __shared__ float4 ns[2][TJ / 4];
   __shared__ float4 bs[2][SUM ? TJ * W / 4 : 1];
+  __shared__ float4 gsh[2][LAPG ? TJ / 4 : 1];
 
   if constexpr (EPI == 3) {
     if (exact_ok(a.exact, a.D)) return;   // the bf16 kernel does the work
@@ -349,7 +358,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
 
   float4 ystage[YL];
   float4 bstage[BL > 0 ? BL : 1];
-  float4 nstage;
+  float4 nstage, gstage;
   // the tile at column jt (16-aligned), its columns outside [lo, hi) masked
   auto fetch = [&](int64_t jt, int64_t lo, int64_t hi) {
     // y of masked columns is loaded as is (inside the padded array): their
@@ -365,6 +374,12 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
       if constexpr (SP) nstage = masked_ny(a.ny, pad_ny, jt + 4 * tid, lo, hi);
       else nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
                                      : float4{0.f, 0.f, 0.f, 0.f};
+      if constexpr (LAPG) {
+        const float ninf = -__builtin_inff();
+        if constexpr (SP) gstage = masked_ny(a.gpk, ninf, jt + 4 * tid, lo, hi);
+        else gstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.gpk + jt)[tid]
+                                       : float4{ninf, ninf, ninf, ninf};
+      }
     }
     if constexpr (SUM) {
       const float4* bsrc = reinterpret_cast<const float4*>(a.bpk + jt * W);
@@ -389,6 +404,9 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
       }
     }
     if (tid < TJ / 4) ns[buf][tid] = nstage;
+    if constexpr (LAPG) {
+      if (tid < TJ / 4) gsh[buf][tid] = gstage;
+    }
     if constexpr (SUM) {
 #pragma unroll
       for (int k = 0; k < BL; ++k) {
@@ -449,6 +467,14 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
         } else if constexpr (LSE) {
           // s of the lane's 4 columns (padding columns: -inf); the reference
           // moves up to the largest s seen, rescaling both sums
+          if constexpr (LAPG) {
+            // acc = -(log2(e) / sigma)^2 d: s = g' - sqrt(-acc)
+            const float4 gv = gsh[buf][blk * 4 + g];
+            acc[0] = gv.x - __builtin_amdgcn_sqrtf(fmaxf(-acc[0], 0.0f));
+            acc[1] = gv.y - __builtin_amdgcn_sqrtf(fmaxf(-acc[1], 0.0f));
+            acc[2] = gv.z - __builtin_amdgcn_sqrtf(fmaxf(-acc[2], 0.0f));
+            acc[3] = gv.w - __builtin_amdgcn_sqrtf(fmaxf(-acc[3], 0.0f));
+          }
           const float mb = fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3]));
           const float nm = fmaxf(lm[rb], mb);
           const float sc = __builtin_amdgcn_exp2f(lm[rb] - nm);
@@ -1056,6 +1082,9 @@ hipError_t launch_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
     case 2: return launch_sum_q<Q, 2, SP>(a, grid, s);
     case 4:
       hipLaunchKernelGGL((mfma_kernel<Q, RB, 4, 1, 1, SP>), grid, dim3(256), 0, s, a);
+      return hipGetLastError();
+    case 5:
+      hipLaunchKernelGGL((mfma_kernel<Q, RB, 5, 1, 1, SP>), grid, dim3(256), 0, s, a);
       return hipGetLastError();
     case 3:
       switch (a.KP) {

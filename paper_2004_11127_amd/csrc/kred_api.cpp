@@ -233,6 +233,18 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
     q.coord_scale = 1.0f;
     q.nrm_sign = 1.0f;
     q.pad_norm = INFINITY;
+  } else if (r == KRED_R_LSE && f == KRED_F_LAPLACE) {
+    // s_ij = g_j - |x_i - y_j| / sigma in log2 units: x and y scaled by
+    // log2(e) / sigma, T = -(log2(e) / sigma)^2 d, s = g_j log2(e) - sqrt(-T)
+    // with g' in its own per-column array (padding columns -inf)
+    q.epi = 5;
+    q.EB = 1;
+    const double sc = log2e / (double)p->sigma;
+    q.xscale = (float)sc;
+    q.coord_scale = (float)sc;
+    q.yop_scale = (float)(2.0 * sc);
+    q.nrm_sign = -1.0f;
+    q.pad_norm = 0.0f;
   } else if (r == KRED_R_LSE) {
     // s_ij = g_j - d_ij / eps in log2 units (the Gaussian's log-domain sum is
     // the same with eps = 2 sigma^2): x and y scaled by sqrt(log2(e) / eps),
@@ -279,7 +291,8 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   q.yop_bytes = align_up(q.N16 * q.DP * (int64_t)sizeof(float));
   q.ny_bytes = align_up(q.N16 * (int64_t)sizeof(float));
   q.b_bytes = (r == KRED_R_ARGKMIN || r == KRED_R_LSE)
-                  ? 0 : align_up(q.N16 * q.W * (int64_t)sizeof(float));
+                  ? (q.epi == 5 ? align_up(q.N16 * (int64_t)sizeof(float)) : 0)
+                  : align_up(q.N16 * q.W * (int64_t)sizeof(float));
   if (r == KRED_R_ARGKMIN)
     q.part_bytes = align_up((int64_t)4 * q.C * M * 2 * q.KP * (int64_t)sizeof(float));
   else if (r == KRED_R_LSE)
@@ -400,6 +413,9 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   float* yop = reinterpret_cast<float*>(base);
   float* ny = reinterpret_cast<float*>(base + pl.yop_bytes);
   float* bpk = pl.b_bytes ? reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes) : nullptr;
+  // the Laplacian log-sum-exp keeps g' per column where the sums keep packed b
+  float* gpk = pl.epi == 5 ? bpk : nullptr;
+  if (gpk) bpk = nullptr;
   float* part = pl.part_bytes
                     ? reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes + pl.b_bytes)
                     : nullptr;
@@ -442,6 +458,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   pa.goff = lse ? b : nullptr;
   pa.goff_scale = 1.4426950408889634f;
   pa.yc = cen;
+  pa.gpk = gpk;
   pa.EB = pl.EB;
   pa.yop_scale = pl.yop_scale;
   pa.coord_scale = pl.coord_scale;
@@ -481,6 +498,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   ma.N = N;
   ma.pad_ny = pl.pad_norm;
   ma.xc = cen;
+  ma.gpk = gpk;
   if (rg) {
     ma.nr = rg->nr;
     ma.rr = rg->rr;
@@ -1035,7 +1053,7 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
                      (r == KRED_R_ARGKMIN || r == KRED_R_KMIN || r == KRED_R_MIN ||
                       r == KRED_R_ARGMIN);
   // and the log-sum-exp of the Sinkhorn form and of the Gaussian
-  const bool lse_wide = r == KRED_R_LSE && (f == KRED_F_SINKHORN || f == KRED_F_GAUSS);
+  const bool lse_wide = r == KRED_R_LSE;
   if (D > kMaxDirectD && !lse_wide &&
       (f == KRED_F_SINKHORN || r == KRED_R_LSE || (is_extreme(r) && !lists)))
     return KRED_ERR_UNSUPPORTED;

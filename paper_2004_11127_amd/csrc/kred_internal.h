@@ -193,6 +193,7 @@ struct MfmaPackArgs {
   const float* goff;         // log-sum-exp: per-column offset g (N), added to ny times goff_scale
   float goff_scale;
   const float* yc;           // sums and log-sum-exp: a centre (D) subtracted from y, else null
+  float* gpk;                // Laplacian log-sum-exp: g' = goff goff_scale per column (N16), else null
 };
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
 
@@ -214,6 +215,7 @@ hipError_t launch_vjp_finish(const float* x, int64_t M, int D, int E, const floa
 
 struct MfmaArgs {
   int epi;        // 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min, 4 log-sum-exp
+                  // (Sinkhorn form), 5 log-sum-exp of the Laplacian
   int D, DP, E, e0, EB;
   int64_t M, N16;
   int C;          // column blocks
@@ -239,6 +241,7 @@ struct MfmaArgs {
   const int* cr;
   const int* bstart;
   const float* xc;   // sums and log-sum-exp: the centre (D) subtracted from x, as from y
+  const float* gpk;  // Laplacian log-sum-exp: g' per column (N16; padding -infinity)
 };
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
 // Exact-path prologue: reset the guard, then fold every coordinate of x and y into it.

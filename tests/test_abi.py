@@ -227,11 +227,13 @@ def test_kernel_lse_pairs(lib):
     assert V("laplace", "lse", 100, 200, 3, 1, sigma=0.0) == INVALID
     assert V("gauss", "lse", 100, 200, 3, 1, sigma=0.1, b=None) == INVALID
     assert V("sqdist", "lse", 100, 200, 3, 1) == UNSUPPORTED
-    # 16 < D <= 256: the Gaussian and Sinkhorn forms on the matrix cores, not the Laplacian
+    # 16 < D <= 256: every log-sum-exp on the matrix cores; the min / max family
+    # beyond the nearest squared distance is not served there
     assert V("gauss", "lse", 100, 200, 17, 1, sigma=0.1) == OK
     assert V("sinkhorn", "lse", 100, 200, 256, 1, eps=0.1) == OK
-    assert V("laplace", "lse", 100, 200, 17, 1, sigma=0.1) == UNSUPPORTED
+    assert V("laplace", "lse", 100, 200, 17, 1, sigma=0.1) == OK
     assert V("sinkhorn", "max", 100, 200, 17, 1, eps=0.1) == UNSUPPORTED
+    assert V("gauss", "max", 100, 200, 17, 1, sigma=0.1) == UNSUPPORTED
 
 
 def test_ranges_validation(lib):
@@ -247,7 +249,8 @@ def test_ranges_validation(lib):
     assert VR("gauss", "sum", 100, 200, 17, 1, 5, sigma=1.0) == OK
     assert VR("sqdist", "argkmin", 100, 200, 64, 0, 5, b=None, K=10) == OK
     assert VR("gauss", "lse", 100, 200, 17, 1, 5, sigma=1.0) == OK
-    assert VR("laplace", "lse", 100, 200, 17, 1, 5, sigma=1.0) == UNSUPPORTED
+    assert VR("laplace", "lse", 100, 200, 17, 1, 5, sigma=1.0) == OK
+    assert VR("gauss", "min", 100, 200, 17, 1, 5, sigma=1.0) == UNSUPPORTED
     assert VR("gauss", "sum", 100, 200, 257, 1, 5, sigma=1.0) == INVALID        # as kred_run
     assert VR("gauss", "sum", 100, 200, 3, 1, 5, sigma=0.0) == INVALID         # as kred_run
 

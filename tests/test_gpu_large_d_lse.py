@@ -1,8 +1,9 @@
 """GPU parity of the log-sum-exp reductions for 16 < D <= 256 (matrix cores).
 
-a_i = log sum_j exp(g_j - |x_i - y_j|^2 / eps) (the Sinkhorn form) and the
+a_i = log sum_j exp(g_j - |x_i - y_j|^2 / eps) (the Sinkhorn form), the
 Gaussian's log-domain sum log sum_j k_ij exp(g_j) (the same with eps =
-2 sigma^2), on the fp32 matrix-core kernel: each lane keeps a running
+2 sigma^2) and the Laplacian's (s = g_j - |x_i - y_j| / sigma, the square root
+of the expanded distance), on the fp32 matrix-core kernel: each lane keeps a running
 reference and its sums in log2 units, the four lane groups and the column
 blocks are merged as (m, s) pairs.  Compared with the fp64 oracle at the
 log-sum-exp bar (1e-4 in the log domain beyond the fp32 rounding of a value
@@ -69,6 +70,16 @@ def test_gauss_lse_large_d(ctx, D, sigma, C):
     assert lse_err(out[:, 0], ref, m) <= LSE_TOL
 
 
+@pytest.mark.parametrize("D,sigma,C", [(17, 0.5, 0), (64, 0.2, 3), (200, 1.0, 0)])
+def test_laplace_lse_large_d(ctx, D, sigma, C):
+    # s = g - |x - y| / sigma: g' per column in its own array, sqrt of the expanded d
+    M, N = 300, 1000
+    x, y, g = _data(D + 5, M, N, D, offset=1.0)
+    out = host(ctx.run("laplace", "lse", dev(x), dev(y), dev(g), sigma=sigma, col_blocks=C))
+    ref, m = oracle.kernel_lse("laplace", x, y, g, sigma)
+    assert lse_err(out[:, 0], ref, m) <= LSE_TOL
+
+
 def test_lse_large_d_empty_and_ranges(ctx):
     import torch
     from test_gpu_ranges import random_pattern
@@ -84,5 +95,10 @@ def test_lse_large_d_empty_and_ranges(ctx):
                                   dev(cr), eps=0.3, col_blocks=C))[:, 0]
         ref, m = oracle.ranges_reduce("lse", x, y, g, rows, ptr, cr, eps=0.3)
         empty = np.isneginf(ref)
+        assert np.isneginf(out[empty]).all()
+        assert lse_err(out[~empty], ref[~empty], m[~empty]) <= LSE_TOL, C
+        out = host(ctx.run_ranges("laplace", "lse", dev(x), dev(y), dev(g), dev(rows), dev(ptr),
+                                  dev(cr), sigma=0.4, col_blocks=C))[:, 0]
+        ref, m = oracle.ranges_reduce("lse", x, y, g, rows, ptr, cr, formula="laplace", sigma=0.4)
         assert np.isneginf(out[empty]).all()
         assert lse_err(out[~empty], ref[~empty], m[~empty]) <= LSE_TOL, C

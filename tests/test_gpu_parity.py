@@ -319,7 +319,7 @@ def test_large_d_unsupported_pairs_raise(ctx):
     from paper_2004_11127_amd import kred
     x = dev(np.ones((4, 32), np.float32)); y = dev(np.ones((4, 32), np.float32))
     with pytest.raises(kred.KredError) as e:
-        ctx.run("laplace", "lse", x, y, dev(np.ones((4, 1), np.float32)), sigma=1.0)
+        ctx.run("gauss", "max", x, y, dev(np.ones((4, 1), np.float32)), sigma=1.0)
     assert e.value.status == 2
 
 
