@@ -1124,7 +1124,7 @@ int mfma_rows_per_block(int DP, int KP) {
 
 // ------------------------------------------ centre; fused gradient, large D
 // Distances do not change when x and y move by the same point m; taking m
-// inside the data (the mean of up to the first 1024 rows of y) keeps the
+// inside the data (the mean of up to the first 256 rows of y) keeps the
 // expanded form's cancellation, |x|^2 + |y|^2 - 2 <x, y>, at the scale of the
 // data's spread rather than its distance from the origin.
 // The Gaussian sum's x-gradient g_i = sum_j k_ij b_j (y_j - x_i) / sigma^2
@@ -1139,10 +1139,22 @@ __global__ __launch_bounds__(256) void centre_kernel(const float* __restrict__ y
                                                            int D, float* __restrict__ m) {
   const int d = threadIdx.x;
   if (d >= D) return;
-  const int64_t n = min(N, (int64_t)1024);
-  float s = 0.0f;
-  for (int64_t j = 0; j < n; ++j) s += y[j * D + d];
-  m[d] = n > 0 ? s / (float)n : 0.0f;
+  const int n = (int)min(N, (int64_t)256);
+  // 16 independent sums, so 16 loads are in flight per step
+  float s[16];
+#pragma unroll
+  for (int u = 0; u < 16; ++u) s[u] = 0.0f;
+  int j = 0;
+  for (; j + 16 <= n; j += 16) {
+#pragma unroll
+    for (int u = 0; u < 16; ++u) s[u] += y[(int64_t)(j + u) * D + d];
+  }
+  for (; j < n; ++j) s[0] += y[(int64_t)j * D + d];
+#pragma unroll
+  for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+    for (int u = 0; u < w; ++u) s[u] += s[u + w];
+  m[d] = n > 0 ? s[0] / (float)n : 0.0f;
 }
 
 // columns [c0, c0 + Ec) of the signal [b_e, b_e (y - m)] for e = 0..E-1

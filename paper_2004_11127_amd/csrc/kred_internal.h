@@ -197,7 +197,7 @@ struct MfmaPackArgs {
 };
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
 
-// A centre of y for the large-D kernels: m = the mean of its first min(N, 1024)
+// A centre of y for the large-D kernels: m = the mean of its first min(N, 256)
 // rows (D floats; zeros when N = 0).
 hipError_t launch_centre(const float* y, int64_t N, int D, float* m, hipStream_t s);
 // Fused Gaussian value + x-gradient for 16 < D <= 256 as one Gaussian sum with
