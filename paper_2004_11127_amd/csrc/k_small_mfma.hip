@@ -67,9 +67,13 @@ __global__ void guard_init_kernel(FastGuard* g) {
 __global__ __launch_bounds__(256) void bounds_kernel(const float* __restrict__ x, int64_t M,
                                                      const float* __restrict__ y, int64_t N, int D,
                                                      FastGuard* g) {
-  __shared__ float red[2][3][4];
-  float lo[3] = {__builtin_inff(), __builtin_inff(), __builtin_inff()};
-  float hi[3] = {-__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
+  __shared__ float red[2][kFastMaxD][4];
+  float lo[kFastMaxD], hi[kFastMaxD];
+#pragma unroll
+  for (int d = 0; d < kFastMaxD; ++d) {
+    lo[d] = __builtin_inff();
+    hi[d] = -__builtin_inff();
+  }
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < M + N; t += stride) {
     const float* p = t < M ? x + t * D : y + (t - M) * D;
@@ -79,7 +83,7 @@ __global__ __launch_bounds__(256) void bounds_kernel(const float* __restrict__ x
     }
   }
   const int wave = threadIdx.x >> 6;
-  for (int d = 0; d < 3; ++d) {
+  for (int d = 0; d < kFastMaxD; ++d) {
     float a = lo[d], b = hi[d];
     for (int o = 32; o > 0; o >>= 1) {
       a = fminf(a, __shfl_xor(a, o));
@@ -102,7 +106,7 @@ __global__ __launch_bounds__(256) void bounds_kernel(const float* __restrict__ x
 
 // Column-side packing: A row (32 bf16) and per-column extras.
 //   sum:   ex = (b, -, -, -)        gradx: ex = (b, b v0, b v1, b v2)
-//   lse:   g' = g log2(e) in A slots 24..26
+//   lse:   g' = g log2(e) in A slots 24..26 (D = 4: added to -|v|^2 in 24..26)
 // Padding columns (N <= j < N16) get zero A rows and zero extras.
 __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
   const FastFrame fr = fast_frame(a.guard, a.D, a.scale);
@@ -114,12 +118,12 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
     for (int k = 0; k < 32; ++k) s[k] = (__bf16)0.0f;
     float4 ex = {0.f, 0.f, 0.f, 0.f};
     if (j < a.N) {
-      float v[3] = {0.f, 0.f, 0.f};
+      float v[kFastMaxD] = {0.f, 0.f, 0.f, 0.f};
       float nv = 0.0f;
       const bool nearest = a.epi == FAST_MIN || a.epi == FAST_KNN;
       const float sg = nearest ? -1.0f : 1.0f;   // MIN, KNN: T = +|u - v|^2
 #pragma unroll
-      for (int d = 0; d < 3; ++d)
+      for (int d = 0; d < kFastMaxD; ++d)
         if (d < a.D) {
           v[d] = (a.y[j * a.D + d] - fr.m[d]) * a.scale;
           nv = __builtin_fmaf(v[d], v[d], nv);
@@ -132,12 +136,17 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
           s[6 * d + 4] = h;
           s[6 * d + 5] = m;
         }
-      split3(-sg * nv, s[18], s[19], s[20]);
-      s[21] = s[22] = s[23] = (__bf16)1.0f;
       const float bj = nearest ? 0.0f : a.b[j];   // MIN and KNN read no b
-      if (a.epi == FAST_LSE) {
-        split3(bj * kLog2e, s[24], s[25], s[26]);
-      } else if (a.epi == FAST_GRADX) {
+      if (a.D <= 3) {
+        split3(-sg * nv, s[18], s[19], s[20]);
+        s[21] = s[22] = s[23] = (__bf16)1.0f;
+        if (a.epi == FAST_LSE) split3(bj * kLog2e, s[24], s[25], s[26]);
+      } else {
+        // D = 4: the products fill slots 0..23; g' joins -|v|^2
+        split3(-sg * nv + (a.epi == FAST_LSE ? bj * kLog2e : 0.0f), s[24], s[25], s[26]);
+        s[27] = s[28] = s[29] = (__bf16)1.0f;
+      }
+      if (a.epi == FAST_GRADX) {
         ex = float4{bj, bj * v[0], bj * v[1], bj * v[2]};
       } else if (a.epi == FAST_SUM) {
         ex.x = bj;
@@ -153,14 +162,14 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
 }
 
 // Row-side B operand: this lane's 8 K slots (8g .. 8g+7) for its row.
-__device__ __forceinline__ bf16x8 row_operand(const float (&u)[3], int D, int g, bool lse,
+__device__ __forceinline__ bf16x8 row_operand(const float (&u)[kFastMaxD], int D, int g, bool lse,
                                                bool neg) {
   __bf16 s[32];
 #pragma unroll
   for (int k = 0; k < 32; ++k) s[k] = (__bf16)0.0f;
   float nu = 0.0f;
 #pragma unroll
-  for (int d = 0; d < 3; ++d)
+  for (int d = 0; d < kFastMaxD; ++d)
     if (d < D) {
       __bf16 h, m, l;
       split3(u[d], h, m, l);
@@ -172,9 +181,14 @@ __device__ __forceinline__ bf16x8 row_operand(const float (&u)[3], int D, int g,
       s[6 * d + 5] = m;
       nu = __builtin_fmaf(u[d], u[d], nu);
     }
-  s[18] = s[19] = s[20] = (__bf16)1.0f;
-  split3(neg ? nu : -nu, s[21], s[22], s[23]);
-  if (lse) s[24] = s[25] = s[26] = (__bf16)1.0f;
+  if (D <= 3) {
+    s[18] = s[19] = s[20] = (__bf16)1.0f;
+    split3(neg ? nu : -nu, s[21], s[22], s[23]);
+    if (lse) s[24] = s[25] = s[26] = (__bf16)1.0f;
+  } else {
+    s[24] = s[25] = s[26] = (__bf16)1.0f;
+    split3(neg ? nu : -nu, s[27], s[28], s[29]);
+  }
   bf16x8 o;
 #pragma unroll
   for (int e = 0; e < 8; ++e) o[e] = s[8 * g + e];
@@ -264,12 +278,12 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   const int64_t i0 = row0 + wave * (16 * RB);
 
   bf16x8 xb[RB];
-  float ur[RB][3];
+  float ur[RB][kFastMaxD];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int64_t row = i0 + 16 * rb + li;
 #pragma unroll
-    for (int d = 0; d < 3; ++d)
+    for (int d = 0; d < kFastMaxD; ++d)
       ur[rb][d] = (row < row_end && d < a.D) ? (a.x[row * a.D + d] - fr.m[d]) * a.scale : 0.0f;
     xb[rb] = row_operand(ur[rb], a.D, g, kLse, kMin || kKnn);
   }
@@ -579,14 +593,14 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   // it only ranks.  The final candidates get their distance in the direct
   // form, sum_d (x_d - y_d)^2, which is accurate relative to itself (and
   // exact on integer coordinates), and are ranked again by it.
-  auto load_row = [&](int64_t row, bool live_row, float (&xr)[3]) __attribute__((always_inline)) {
+  auto load_row = [&](int64_t row, bool live_row, float (&xr)[kFastMaxD]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int d = 0; d < 3; ++d) xr[d] = (live_row && d < a.D) ? a.x[row * a.D + d] : 0.0f;
+    for (int d = 0; d < kFastMaxD; ++d) xr[d] = (live_row && d < a.D) ? a.x[row * a.D + d] : 0.0f;
   };
-  auto exact_d = [&](const float (&xr)[3], int j) __attribute__((always_inline)) {
+  auto exact_d = [&](const float (&xr)[kFastMaxD], int j) __attribute__((always_inline)) {
     float s = 0.0f;
 #pragma unroll
-    for (int d = 0; d < 3; ++d)
+    for (int d = 0; d < kFastMaxD; ++d)
       if (d < a.D) {
         const float t = xr[d] - a.y[(int64_t)j * a.D + d];
         s = __builtin_fmaf(t, t, s);
@@ -603,7 +617,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   auto knn_out = [&](const float (&dl)[KL], const int (&jl)[KL], int64_t row, bool live_row)
       __attribute__((always_inline)) {
     (void)dl;
-    float xr[3];
+    float xr[kFastMaxD];
     load_row(row, live_row, xr);
     float md[16];
     int mj[16];
@@ -665,7 +679,7 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
       // direct-form distance first (see exact_d).
       int v = INT_MAX, j = INT_MAX;
       if (live_row && btile[rb] != INT_MAX) {
-        float xr[3];
+        float xr[kFastMaxD];
         load_row(row, true, xr);
         // the lane's columns 4 g + r of each block of that tile, in column order
         for (int jb = btile[rb] + 4 * g; jb < bend[rb]; jb += 16) {

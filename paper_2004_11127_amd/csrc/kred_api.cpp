@@ -166,10 +166,11 @@ constexpr double kFastMinPairs = 268435456.0;   // 2^28 pairs
 
 int fast_epi(kred_formula f, kred_reduction r, int64_t M, int64_t N, int32_t D, int32_t E,
              uint32_t flags, int K = 0) {
-  if (D > 3 || (flags & KRED_FLAG_DIRECT)) return -1;
+  if (D > kFastMaxD || (flags & KRED_FLAG_DIRECT)) return -1;
   if (!(flags & KRED_FLAG_FAST) && (double)M * (double)N < kFastMinPairs) return -1;
   if (f == KRED_F_GAUSS && r == KRED_R_SUM && E == 1) return FAST_SUM;
-  if (f == KRED_F_GAUSS_GRADX && r == KRED_R_SUM) return FAST_GRADX;
+  // the gradient's per-column extras (b, b v) hold three coordinates
+  if (f == KRED_F_GAUSS_GRADX && r == KRED_R_SUM) return D <= 3 ? FAST_GRADX : -1;
   if ((f == KRED_F_SINKHORN || f == KRED_F_GAUSS) && r == KRED_R_LSE) return FAST_LSE;
   // nearest neighbour: arg-K-min with K = 1, and the distance's min / arg-min
   if (f == KRED_F_SQDIST && r == KRED_R_ARGKMIN && K == 1) return FAST_MIN;

@@ -39,14 +39,16 @@ __device__ __forceinline__ int fenc(float f) {
 }
 __device__ __forceinline__ float fdec(int i) { return __int_as_float(i >= 0 ? i : i ^ 0x7fffffff); }
 
+constexpr int kFastMaxD = 4;   // coordinates the small-D matrix-core path takes
+
 struct FastFrame {
-  float m[3];   // centre of the box
-  bool ok;      // the expanded form meets the accuracy bound
+  float m[kFastMaxD];   // centre of the box
+  bool ok;              // the expanded form meets the accuracy bound
 };
 __device__ __forceinline__ FastFrame fast_frame(const FastGuard* g, int D, float scale) {
   FastFrame f;
   float r2 = 0.0f;
-  for (int d = 0; d < 3; ++d) {
+  for (int d = 0; d < kFastMaxD; ++d) {
     if (d < D) {
       const float lo = fdec(g->lo[d]), hi = fdec(g->hi[d]);
       f.m[d] = 0.5f * (lo + hi);

@@ -170,13 +170,14 @@ def test_extreme_deterministic_and_profiled(ctx):
 FAST_NN = [
     # M, N, D, C
     (1, 1, 3, 0), (700, 2049, 3, 3), (3000, 5000, 2, 0), (1500, 999, 1, 16),
+    (700, 2049, 4, 3), (3000, 5000, 4, 0),
 ]
 
 
 @pytest.mark.parametrize("M,N,D,C", FAST_NN)
 @pytest.mark.parametrize("red", ["min", "argmin", "argkmin1"])
 def test_nearest_fast_path_exact(ctx, M, N, D, C, red):
-    # D <= 3 with KRED_FLAG_FAST: the distance comes from the matrix cores (exact
+    # D <= 4 with KRED_FLAG_FAST: the distance comes from the matrix cores (exact
     # on integer coordinates); min / arg-min / arg-K-min with K = 1 must match
     from paper_2004_11127_amd import kred
     rng = np.random.default_rng(M + N + D + C)
@@ -229,13 +230,14 @@ FAST_KNN = [
     # M, N, D, K, C
     (700, 2049, 3, 4, 3), (3000, 5000, 2, 10, 0), (1500, 999, 1, 16, 16), (257, 4000, 3, 7, 0),
     (1000, 1500, 3, 12, 1), (64, 64, 3, 16, 0),
+    (700, 2049, 4, 10, 3), (1000, 1500, 4, 16, 0), (500, 800, 4, 4, 1),
 ]
 
 
 @pytest.mark.parametrize("M,N,D,K,C", FAST_KNN)
 @pytest.mark.parametrize("red", ["argkmin", "kmin"])
 def test_knn_fast_path_exact(ctx, M, N, D, K, C, red):
-    # D <= 3, 1 < K <= 16 with KRED_FLAG_FAST: distances from the matrix cores (exact on
+    # D <= 4, 1 < K <= 16 with KRED_FLAG_FAST: distances from the matrix cores (exact on
     # integer coordinates inside the guard), per-lane lists merged by (distance, index)
     from paper_2004_11127_amd import kred
     rng = np.random.default_rng(M + N + D + K + C)

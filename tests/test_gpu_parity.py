@@ -342,6 +342,12 @@ FAST_CASES = [
     ("sinkhorn", "lse", 1000, 4099, 3, 0.01, 0),
     ("sinkhorn", "lse", 4099, 1000, 2, 0.002, 3),
     ("sinkhorn", "lse", 700, 2001, 1, 0.01, 16),
+    # four coordinates: the products fill 24 K slots, the norms (with g') 6 more
+    ("gauss", "sum", 1000, 4099, 4, 0.05, 0),
+    ("gauss", "sum", 2000, 3001, 4, 0.1, 16),
+    ("sinkhorn", "lse", 1000, 4099, 4, 0.01, 0),
+    ("sinkhorn", "lse", 4099, 1000, 4, 0.002, 3),
+    ("gauss_gradx", "sum", 1000, 4099, 4, 0.05, 0),   # the direct form (no fast gradient at D = 4)
 ]
 
 
