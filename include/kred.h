@@ -72,12 +72,12 @@ typedef enum kred_status {
 
 /* flags */
 #define KRED_FLAG_PROFILE 1u  /* time the main kernel of each call with HIP events (kred_profile_collect) */
-#define KRED_FLAG_DIRECT 2u   /* D <= 3: always use the direct-form kernels, never the matrix-core exponent
+#define KRED_FLAG_DIRECT 2u   /* D <= 4: always use the direct-form kernels, never the matrix-core exponent
                                  (used otherwise only below 2^28 pairs, or when the data's extent makes
                                  the matrix-core form less accurate).  D > 16 arg-K-min (and K-min,
                                  min / arg-min without b): always the fp32 matrix-core kernel, never
                                  the exact bf16 one */
-#define KRED_FLAG_FAST 4u     /* D <= 3: use the matrix-core exponent whatever the problem size (the
+#define KRED_FLAG_FAST 4u     /* D <= 4: use the matrix-core exponent whatever the problem size (the
                                  accuracy guard still falls back to the direct form).  D > 16
                                  arg-K-min: consider the exact bf16 kernel whatever the size (it
                                  runs only when every coordinate is an integer with |v| <= 256 and
@@ -189,7 +189,7 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
  * Rows in no cluster, and clusters without columns, hold the empty reduction
  * (as for N = 0; arg-K-min / K-min pad short lists with -1 / +infinity).
  *
- * Every pair kred_run accepts, on the same paths (direct form, the D <= 3
+ * Every pair kred_run accepts, on the same paths (direct form, the D <= 4
  * matrix-core exponent, and for 16 < D <= 256 the matrix-core kernels, which
  * start their column tiles 16-aligned and mask the columns outside a range).
  * col_blocks (0: automatic) splits each cluster's columns into that many

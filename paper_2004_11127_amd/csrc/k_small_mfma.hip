@@ -1,4 +1,4 @@
-// Small-D (D <= 3) reductions with the exponent on the bf16 matrix cores.
+// Small-D (D <= 4) reductions with the exponent on the bf16 matrix cores.
 //
 // The direct form of the pair term costs about 6 VALU instructions per pair
 // before the exp.  Here the whole exponent T_ij = -c |x_i - y_j|^2 (log2
@@ -22,13 +22,17 @@
 // matrix core returns the squared distance |u - v|^2 itself (c = 1, centred
 // coordinates): minimum and arg-minimum then need no exp at all.
 //
-// K slots (A: column side, B: row side), for coordinate d = 0..2:
+// K slots (A: column side, B: row side), for coordinate d = 0..D-1, D <= 3:
 //   6d + 0..5:  A = (Vh, Vm, Vh, Vl, Vh, Vm) of V = 2 v_d,
 //               B = (uh, uh, um, uh, ul, um) of u_d
 //   18..20:     A = parts of -|v|^2, B = 1
 //   21..23:     A = 1,               B = parts of -|u|^2
 //   24..26:     log-sum-exp only: A = parts of g' = g log2(e), B = 1
 //   27..31:     0
+// D = 4: the products fill 0..23, A = parts of -|v|^2 (+ g' for the
+// log-sum-exp) with B = 1 in 24..26, A = 1 with B = parts of -|u|^2 in 27..29.
+// The fused gradient's per-column extras (b, b v) hold three coordinates, so
+// it runs here for D <= 3 only.
 // Lane layout of v_mfma_f32_16x16x32_bf16 (lane l = 16 g + li): A: lane
 // supplies A[li][8g .. 8g+7]; B: lane supplies B[8g .. 8g+7][li]; D: lane holds
 // D[4g + r][li].  With A = columns and B = rows, lane l gets T for row li and
