@@ -179,12 +179,13 @@ FAST = [
     ("gauss", "sum", 3, 0.05, 0), ("gauss", "sum", 2, 0.1, 1), ("gauss", "sum", 3, 0.05, 5),
     ("gauss_gradx", "sum", 3, 0.05, 0), ("gauss_gradx", "sum", 1, 0.1, 3),
     ("sinkhorn", "lse", 3, 0.01, 0), ("sinkhorn", "lse", 3, 0.01, 4), ("gauss", "lse", 2, 0.1, 0),
+    ("gauss", "sum", 4, 0.05, 0), ("sinkhorn", "lse", 4, 0.01, 3),
 ]
 
 
 @pytest.mark.parametrize("formula,reduction,D,param,C", FAST)
 def test_ranges_fast_path(ctx, formula, reduction, D, param, C):
-    # D <= 3 with KRED_FLAG_FAST: the matrix-core exponent kernel walks the
+    # D <= 4 with KRED_FLAG_FAST: the matrix-core exponent kernel walks the
     # same pattern (ranges start and end anywhere, not on 16-column blocks)
     from paper_2004_11127_amd import kred
     rng = np.random.default_rng(D * 10 + C)
@@ -220,12 +221,13 @@ def test_ranges_fast_kernel_is_used(ctx):
     assert name == "fast_kernel"
 
 
+@pytest.mark.parametrize("D", [3, 4])
 @pytest.mark.parametrize("red", ["min", "argmin"])
-def test_ranges_nearest_fast_path(ctx, red):
+def test_ranges_nearest_fast_path(ctx, red, D):
     from paper_2004_11127_amd import kred
-    rng = np.random.default_rng(13)
+    rng = np.random.default_rng(13 + D)
     M, N = 4000, 5000
-    x = rng.integers(-20, 21, (M, 3)).astype(np.float32); y = rng.integers(-20, 21, (N, 3)).astype(np.float32)
+    x = rng.integers(-20, 21, (M, D)).astype(np.float32); y = rng.integers(-20, 21, (N, D)).astype(np.float32)
     pat = random_pattern(rng, M, N, 15, 25)
     for C in CHUNKS:
         out = call(ctx, "sqdist", red, x, y, None, pat, col_blocks=C, flags=kred.FLAG_FAST)
