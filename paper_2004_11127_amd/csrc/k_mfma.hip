@@ -83,13 +83,14 @@ __global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
       a.gpk[j] = j < a.N ? a.goff[j] * a.goff_scale : -__builtin_inff();
   }
   // signal tiles: b[j][e0 + e] stored at (j/16)*16W + ((j%16)/4)*4W + e*4 + j%4, W = 16*EB
+  // (unit_b: ones in place of b)
   if (a.bpk != nullptr) {
     const int W = 16 * a.EB;
     const int64_t total_b = a.N16 * W;
     for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total_b; t += stride) {
       const int64_t j = t / W;
       const int e = (int)(t - j * W);
-      const float v = (j < a.N && e < a.Ec) ? a.b[j * a.E + a.e0 + e] : 0.0f;
+      const float v = (j < a.N && e < a.Ec) ? (a.unit_b ? 1.0f : a.b[j * a.E + a.e0 + e]) : 0.0f;
       const int64_t blk = j / 16;
       const int jr = (int)(j % 16);
       a.bpk[blk * 16 * W + (jr / 4) * 4 * W + e * 4 + (jr % 4)] = v;
@@ -277,7 +278,9 @@ __device__ __forceinline__ int64_t bpk_col(int64_t jt, int t4, int W) {
 
 // EPI: 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min, 4 log-sum-exp
 // of s_ij = g_j - |x_i - y_j|^2 / eps (log2 units: the column norms carry g_j),
-// 5 log-sum-exp of s_ij = g_j - |x_i - y_j| / sigma (g_j from its own array).
+// 5 log-sum-exp of s_ij = g_j - |x_i - y_j| / sigma (g_j from its own array),
+// 6..9 min / max of F_ij b_je per signal column e (F: 6 Gauss, 7 Laplace, 8
+// squared distance, 9 the Sinkhorn form s_ij, with b = 1), lowest index on ties.
 // SP: block-sparse (a pattern of row clusters and column ranges) or dense.
 template <int Q, int RB, int EPI, int EB, int KP, bool SP>
 __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
@@ -285,18 +288,20 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
   constexpr int LDY = DP + 4;
   constexpr int TJ = tile_cols(DP);
   constexpr bool SUM = EPI < 3;
-  constexpr bool LSE = EPI >= 4;
+  constexpr bool LSE = EPI == 4 || EPI == 5;
+  constexpr bool EXT = EPI >= 6;
+  constexpr bool BSIG = SUM || EXT;   // packed b tiles in LDS
   constexpr bool LAPG = EPI == 5;   // per-column g' staged like the norms
   constexpr int W = 16 * EB;                       // signal columns per row in a tile
   constexpr int YF4 = TJ * DP / 4;                 // float4s of y per tile
   constexpr int YL = (YF4 + 255) / 256;            // per thread
-  constexpr int BF4 = SUM ? TJ * W / 4 : 0;        // float4s of b per tile
-  constexpr int BL = SUM ? (BF4 + 255) / 256 : 0;
+  constexpr int BF4 = BSIG ? TJ * W / 4 : 0;       // float4s of b per tile
+  constexpr int BL = BSIG ? (BF4 + 255) / 256 : 0;
   constexpr int KL = EPI == 3 ? KP : 1;
 
   __shared__ float4 ys[2][TJ * LDY / 4];
   __shared__ float4 ns[2][TJ / 4];
-  __shared__ float4 bs[2][SUM ? TJ * W / 4 : 1];
+  __shared__ float4 bs[2][BSIG ? TJ * W / 4 : 1];
   __shared__ float4 gsh[2][LAPG ? TJ / 4 : 1];
 
   if constexpr (EPI == 3) {
@@ -341,6 +346,18 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
     lm[rb] = -3.0e38f;
     lp[rb] = ls[rb] = 0.0f;
   }
+  // extremes: per row block and signal column the smallest key sign * F b so
+  // far over the lane's columns, and its column (-1: none)
+  constexpr int XW = EXT ? W : 1;
+  float xbest[RB][XW];
+  int xidx[RB][XW];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int e = 0; e < XW; ++e) {
+      xbest[rb][e] = __builtin_inff();
+      xidx[rb][e] = -1;
+    }
 
   f4 oacc[RB][EB], tot[RB][EB];
   float dk[RB][KL];
@@ -381,7 +398,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
                                        : float4{ninf, ninf, ninf, ninf};
       }
     }
-    if constexpr (SUM) {
+    if constexpr (BSIG) {
       const float4* bsrc = reinterpret_cast<const float4*>(a.bpk + jt * W);
 #pragma unroll
       for (int k = 0; k < BL; ++k) {
@@ -407,7 +424,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
     if constexpr (LAPG) {
       if (tid < TJ / 4) gsh[buf][tid] = gstage;
     }
-    if constexpr (SUM) {
+    if constexpr (BSIG) {
 #pragma unroll
       for (int k = 0; k < BL; ++k) {
         const int f = tid + k * 256;
@@ -441,8 +458,9 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
       const float4 nyv = ns[buf][blk * 4 + g];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        f4 acc = (SUM || LSE) ? f4{nx[rb] + nyv.x, nx[rb] + nyv.y, nx[rb] + nyv.z, nx[rb] + nyv.w}
-                              : f4{nyv.x, nyv.y, nyv.z, nyv.w};
+        f4 acc = (SUM || LSE || EXT)
+                     ? f4{nx[rb] + nyv.x, nx[rb] + nyv.y, nx[rb] + nyv.z, nx[rb] + nyv.w}
+                     : f4{nyv.x, nyv.y, nyv.z, nyv.w};
 #pragma unroll
         for (int q = 0; q < Q; ++q) acc = mfma4(yo[q], xr[rb][q], acc);
         if constexpr (SUM) {
@@ -463,6 +481,36 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
             oacc[rb][eb] = mfma4(p[1], bv.y, oacc[rb][eb]);
             oacc[rb][eb] = mfma4(p[2], bv.z, oacc[rb][eb]);
             oacc[rb][eb] = mfma4(p[3], bv.w, oacc[rb][eb]);
+          }
+        } else if constexpr (EXT) {
+          // F of the lane's 4 columns, then for every signal column e the
+          // key sign * F b; columns outside [a0, min(a1, N)) never win.
+          // Columns arrive in index order, so a strict test keeps the lowest
+          // index on ties.
+          const int64_t jb = jt + blk * 16 + 4 * g;
+          const int64_t jend = min(a1, a.N);
+          float fv[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if constexpr (EPI == 6) fv[r] = __builtin_amdgcn_exp2f(acc[r]);
+            else if constexpr (EPI == 7) fv[r] = __builtin_amdgcn_exp2f(-__builtin_amdgcn_sqrtf(fmaxf(-acc[r], 0.0f)));
+            else if constexpr (EPI == 8) fv[r] = fmaxf(-acc[r], 0.0f);
+            else fv[r] = acc[r] * kLn2;
+            fv[r] = (jb + r >= a0 && jb + r < jend) ? fv[r] * a.ext_sign : __builtin_nanf("");
+          }
+#pragma unroll
+          for (int e = 0; e < W; ++e) {
+            // b of the lane's 4 columns for signal column e
+            const float4 bv = *reinterpret_cast<const float4*>(
+                reinterpret_cast<const float*>(&bs[buf][0]) + blk * 16 * W + g * 4 * W + e * 4);
+            const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float key = fv[r] * bb[r];   // NaN (an excluded column) never compares less
+              const bool lt = key < xbest[rb][e];
+              xbest[rb][e] = lt ? key : xbest[rb][e];
+              xidx[rb][e] = lt ? (int)(jb + r) : xidx[rb][e];
+            }
           }
         } else if constexpr (LSE) {
           // s of the lane's 4 columns (padding columns: -inf); the reference
@@ -536,6 +584,20 @@ __global__ __launch_bounds__(256) void mfma_kernel(MfmaArgs a) {
             a.part[((int64_t)c * a.M + row) * W + e] = tot[rb][eb][r];
           }
         }
+  } else if constexpr (EXT) {
+    // one (key, index) pair per (column block, lane group, row, signal column):
+    // the second pass merges the 4 C partials of a row
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int64_t row = i0 + 16 * rb + li;
+      if (row >= rend) continue;
+      float* q = a.part + (((int64_t)c * 4 + g) * a.M + row) * (2 * W);
+#pragma unroll
+      for (int e = 0; e < W; ++e) {
+        q[2 * e] = xbest[rb][e];
+        q[2 * e + 1] = __int_as_float(xidx[rb][e]);
+      }
+    }
   } else if constexpr (LSE) {
     // merge the row's four lane groups: (m, s) + (m', s') relative to max(m, m')
 #pragma unroll
@@ -1086,6 +1148,12 @@ hipError_t launch_q(const MfmaArgs& a, dim3 grid, hipStream_t s) {
     case 5:
       hipLaunchKernelGGL((mfma_kernel<Q, RB, 5, 1, 1, SP>), grid, dim3(256), 0, s, a);
       return hipGetLastError();
+#define KRED_EXT_F32(EPV)                                                                      \
+  case EPV:                                                                                    \
+    hipLaunchKernelGGL((mfma_kernel<Q, RB, EPV, 1, 1, SP>), grid, dim3(256), 0, s, a);        \
+    return hipGetLastError();
+    KRED_EXT_F32(6) KRED_EXT_F32(7) KRED_EXT_F32(8) KRED_EXT_F32(9)
+#undef KRED_EXT_F32
     case 3:
       switch (a.KP) {
 #define KRED_KNN_F32(KPV, RBV)                                                                 \

@@ -234,6 +234,29 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
     q.coord_scale = 1.0f;
     q.nrm_sign = 1.0f;
     q.pad_norm = INFINITY;
+  } else if (is_extreme(r)) {
+    // min / max of F b per signal column, in slices of 16 columns: F as for
+    // the sums (Gauss, Laplace, squared distance), or the Sinkhorn form's s
+    // with g in the column norms (log2 units, as for its log-sum-exp)
+    q.EB = 1;
+    double sc = 1.0;
+    q.pad_norm = 0.0f;
+    if (f == KRED_F_GAUSS) {
+      q.epi = 6;
+      sc = std::sqrt(log2e / (2.0 * (double)p->sigma * (double)p->sigma));
+    } else if (f == KRED_F_LAPLACE) {
+      q.epi = 7;
+      sc = log2e / (double)p->sigma;
+    } else if (f == KRED_F_SQDIST) {
+      q.epi = 8;
+    } else {
+      q.epi = 9;
+      sc = std::sqrt(log2e / (double)p->eps);
+    }
+    q.xscale = (float)sc;
+    q.coord_scale = (float)sc;
+    q.yop_scale = (float)(2.0 * sc);
+    q.nrm_sign = -1.0f;
   } else if (r == KRED_R_LSE && f == KRED_F_LAPLACE) {
     // s_ij = g_j - |x_i - y_j| / sigma in log2 units: x and y scaled by
     // log2(e) / sigma, T = -(log2(e) / sigma)^2 d, s = g_j log2(e) - sqrt(-T)
@@ -296,6 +319,8 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
                   : align_up(q.N16 * q.W * (int64_t)sizeof(float));
   if (r == KRED_R_ARGKMIN)
     q.part_bytes = align_up((int64_t)4 * q.C * M * 2 * q.KP * (int64_t)sizeof(float));
+  else if (is_extreme(r))
+    q.part_bytes = align_up((int64_t)4 * q.C * M * 2 * q.W * (int64_t)sizeof(float));
   else if (r == KRED_R_LSE)
     q.part_bytes = q.C > 1 ? align_up((int64_t)q.C * M * 2 * (int64_t)sizeof(float)) : 0;
   else
@@ -386,13 +411,18 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   const int64_t rows_wg = mfma_rows_per_block(pl.DP, pl.KP);
   const bool knn = (r == KRED_R_ARGKMIN);
   const bool lse = (r == KRED_R_LSE);
+  const bool ext = is_extreme(r);
+  // min / max: no b for the Sinkhorn form (g goes into the column norms) or
+  // for the bare squared distance; the signal is then a column of ones
+  const bool unit_b = ext && (f == KRED_F_SINKHORN || b == nullptr);
   // arg-K-min: the exact bf16 kernel is a candidate (the device decides);
   // sums: the split bf16 kernel replaces the fp32 one; log-sum-exp: fp32 only
   const bool exact = knn && exact_knn_eligible(p->flags, M, N);
-  const bool split = !knn && !lse && exact_eligible(p->flags, M, N);
+  const bool split = !knn && !lse && !ext && exact_eligible(p->flags, M, N);
   const int64_t ybf_bytes = mfma_bf16_bytes(pl, knn, p->flags, M, N);
   if (rg) {   // partials of every chunk (rows outside the clusters read the empty value)
     pl.part_bytes = knn ? align_up((int64_t)4 * pl.C * M * 2 * pl.KP * (int64_t)sizeof(float))
+                  : ext ? align_up((int64_t)4 * pl.C * M * 2 * pl.W * (int64_t)sizeof(float))
                   : pl.C > 1 ? align_up((int64_t)pl.C * M * (lse ? 2 : pl.W) * (int64_t)sizeof(float))
                              : 0;
   }
@@ -441,14 +471,18 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
       return KRED_ERR_HIP;
     if (lse && pl.C > 1 && launch_fill2(part, (int64_t)pl.C * M * 2, -INFINITY, 0.0f, s) != hipSuccess)
       return KRED_ERR_HIP;
-    if (!knn && !lse && pl.C > 1 &&
+    if (ext && launch_fill2(part, (int64_t)4 * pl.C * M * 2 * pl.W, INFINITY,
+                            __builtin_bit_cast(float, (int32_t)-1), s) != hipSuccess)
+      return KRED_ERR_HIP;
+    if (!knn && !lse && !ext && pl.C > 1 &&
         launch_fill(part, (int64_t)pl.C * M * pl.W, 0.0f, s) != hipSuccess)
       return KRED_ERR_HIP;
   }
 
   MfmaPackArgs pa{};
   pa.y = y;
-  pa.b = (knn || lse) ? nullptr : b;
+  pa.b = (knn || lse || unit_b) ? nullptr : b;
+  pa.unit_b = unit_b ? 1 : 0;
   pa.N = N;
   pa.N16 = pl.N16;
   pa.D = D;
@@ -456,7 +490,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   pa.E = E;
   pa.e0 = 0;
   pa.Ec = (knn || lse) ? 0 : E;
-  pa.goff = lse ? b : nullptr;
+  pa.goff = (lse || (ext && f == KRED_F_SINKHORN)) ? b : nullptr;
   pa.goff_scale = 1.4426950408889634f;
   pa.yc = cen;
   pa.gpk = gpk;
@@ -471,7 +505,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   pa.exact = eg;
   pa.ybf = exact ? ybf : nullptr;
   pa.ysp = split ? ybf : nullptr;
-  if (launch_mfma_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
+  if (!ext && launch_mfma_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
 
   MfmaArgs ma{};
   ma.epi = pl.epi;
@@ -500,6 +534,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   ma.pad_ny = pl.pad_norm;
   ma.xc = cen;
   ma.gpk = gpk;
+  ma.ext_sign = is_max(r) ? -1.0f : 1.0f;
   if (rg) {
     ma.nr = rg->nr;
     ma.rr = rg->rr;
@@ -508,6 +543,48 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     ma.bstart = bstart;
   }
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
+  if (ext) {
+    // slices of 16 signal columns: pack the slice's b, run, merge the 4 C
+    // partial (key, index) pairs of each row and column into out
+    for (int e0 = 0; e0 < E; e0 += pl.W) {
+      pa.e0 = e0;
+      pa.Ec = std::min(pl.W, E - e0);
+      if (launch_mfma_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
+      ma.e0 = e0;
+      if (rg && e0 > 0 &&
+          launch_fill2(part, (int64_t)4 * pl.C * M * 2 * pl.W, INFINITY,
+                       __builtin_bit_cast(float, (int32_t)-1), s) != hipSuccess)
+        return KRED_ERR_HIP;
+      hipEvent_t x0 = nullptr, x1 = nullptr;
+      if (prof) {
+        x0 = next_event(ctx);
+        x1 = next_event(ctx);
+        if (!x0 || !x1 || hipEventRecord(x0, s) != hipSuccess) return KRED_ERR_HIP;
+      }
+      if (launch_mfma(ma, s) != hipSuccess) return KRED_ERR_HIP;
+      if (prof) {
+        if (hipEventRecord(x1, s) != hipSuccess) return KRED_ERR_HIP;
+        ctx->last_kernel = "mfma_kernel";
+        ctx->last_exact_D = 0;
+      }
+      CombineArgs ca{};
+      ca.formula = (int)f;
+      ca.D = D;
+      ca.DP = pl.DP;
+      ca.E = E;
+      ca.EP = pl.W;
+      ca.e0 = e0;
+      ca.M = M;
+      ca.C = 4 * pl.C;
+      ca.part = part;
+      ca.out = out;
+      ca.ext = 1;
+      ca.ext_sign = ma.ext_sign;
+      ca.arg = is_arg(r) ? 1 : 0;
+      if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
+    }
+    return KRED_OK;
+  }
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (prof) {
     e0 = next_event(ctx);
@@ -1047,17 +1124,8 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
   } else {
     return KRED_ERR_UNSUPPORTED;
   }
-  // Paths: the direct-form kernels cover D <= 16 for every pair; the
-  // matrix-core kernels cover 16 < D <= 256 for the sums and the arg-K-min
-  // lists (arg-K-min, K-min, and min / arg-min of the squared distance).
-  const bool lists = f == KRED_F_SQDIST && b == nullptr &&
-                     (r == KRED_R_ARGKMIN || r == KRED_R_KMIN || r == KRED_R_MIN ||
-                      r == KRED_R_ARGMIN);
-  // and the log-sum-exp of the Sinkhorn form and of the Gaussian
-  const bool lse_wide = r == KRED_R_LSE;
-  if (D > kMaxDirectD && !lse_wide &&
-      (f == KRED_F_SINKHORN || r == KRED_R_LSE || (is_extreme(r) && !lists)))
-    return KRED_ERR_UNSUPPORTED;
+  // Paths: the direct-form kernels cover D <= 16 and the matrix-core kernels
+  // 16 < D <= 256, for every pair.
   if (M == 0) return KRED_OK;
   if (x == nullptr || out == nullptr) return KRED_ERR_INVALID_ARG;
   if (N > 0 && (y == nullptr || (needs_b && b == nullptr))) return KRED_ERR_INVALID_ARG;

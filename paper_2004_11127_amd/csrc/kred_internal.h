@@ -192,6 +192,7 @@ struct MfmaPackArgs {
   unsigned short* ybf;       // bf16 copy of yop (N16 x DP), written instead of yop when exact
   unsigned short* ysp;       // sums on the split path: yop as 3 bf16 planes (N16 x 3 x DP), written
                              // instead of yop
+  int unit_b;                // min / max without b: a signal column of ones
   const float* goff;         // log-sum-exp: per-column offset g (N), added to ny times goff_scale
   float goff_scale;
   const float* yc;           // sums and log-sum-exp: a centre (D) subtracted from y, else null
@@ -217,7 +218,8 @@ hipError_t launch_vjp_finish(const float* x, int64_t M, int D, int E, const floa
 
 struct MfmaArgs {
   int epi;        // 0 Gauss, 1 Laplace, 2 squared distance (sums), 3 arg-K-min, 4 log-sum-exp
-                  // (Sinkhorn form), 5 log-sum-exp of the Laplacian
+                  // (Sinkhorn form), 5 log-sum-exp of the Laplacian, 6..9 min / max of
+                  // F b (Gauss, Laplace, squared distance, Sinkhorn form)
   int D, DP, E, e0, EB;
   int64_t M, N16;
   int C;          // column blocks
@@ -244,6 +246,7 @@ struct MfmaArgs {
   const int* bstart;
   const float* xc;   // sums and log-sum-exp: the centre (D) subtracted from x, as from y
   const float* gpk;  // Laplacian log-sum-exp: g' per column (N16; padding -infinity)
+  float ext_sign;    // min / max (epi 6..9): +1 for min, -1 for max
 };
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
 // Exact-path prologue: reset the guard, then fold every coordinate of x and y into it.

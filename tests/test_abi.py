@@ -195,10 +195,11 @@ def test_extreme_pairs(lib, red):
     assert V("gauss", red, 100, 200, 3, 0, sigma=0.3) == INVALID
     assert V("gauss", red, 100, 200, 3, 1, sigma=0.0) == INVALID
     assert V("gauss_gradx", red, 100, 200, 3, 1, sigma=0.3) == UNSUPPORTED
-    # D > 16: only the squared distance's min / arg-min without b
-    assert V("gauss", red, 100, 200, 17, 1, sigma=0.3) == UNSUPPORTED
-    expect = OK if red in ("min", "argmin") else UNSUPPORTED
-    assert V("sqdist", red, 100, 200, 64, 0, b=None) == expect
+    # D > 16: every min / max on the matrix cores
+    assert V("gauss", red, 100, 200, 17, 1, sigma=0.3) == OK
+    assert V("sqdist", red, 100, 200, 64, 0, b=None) == OK
+    assert V("sinkhorn", red, 100, 200, 256, 1, eps=0.3) == OK
+    assert V("gauss_gradx", red, 100, 200, 64, 1, sigma=0.3) == UNSUPPORTED
 
 
 def test_kmin_pairs(lib):
@@ -232,8 +233,9 @@ def test_kernel_lse_pairs(lib):
     assert V("gauss", "lse", 100, 200, 17, 1, sigma=0.1) == OK
     assert V("sinkhorn", "lse", 100, 200, 256, 1, eps=0.1) == OK
     assert V("laplace", "lse", 100, 200, 17, 1, sigma=0.1) == OK
-    assert V("sinkhorn", "max", 100, 200, 17, 1, eps=0.1) == UNSUPPORTED
-    assert V("gauss", "max", 100, 200, 17, 1, sigma=0.1) == UNSUPPORTED
+    assert V("sinkhorn", "max", 100, 200, 17, 1, eps=0.1) == OK
+    assert V("gauss", "max", 100, 200, 17, 1, sigma=0.1) == OK
+    assert V("sqdist", "lse", 100, 200, 17, 1) == UNSUPPORTED
 
 
 def test_ranges_validation(lib):
@@ -250,7 +252,7 @@ def test_ranges_validation(lib):
     assert VR("sqdist", "argkmin", 100, 200, 64, 0, 5, b=None, K=10) == OK
     assert VR("gauss", "lse", 100, 200, 17, 1, 5, sigma=1.0) == OK
     assert VR("laplace", "lse", 100, 200, 17, 1, 5, sigma=1.0) == OK
-    assert VR("gauss", "min", 100, 200, 17, 1, 5, sigma=1.0) == UNSUPPORTED
+    assert VR("gauss", "min", 100, 200, 17, 1, 5, sigma=1.0) == OK
     assert VR("gauss", "sum", 100, 200, 257, 1, 5, sigma=1.0) == INVALID        # as kred_run
     assert VR("gauss", "sum", 100, 200, 3, 1, 5, sigma=0.0) == INVALID         # as kred_run
 

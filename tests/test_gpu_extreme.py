@@ -118,6 +118,13 @@ REAL = [
     ("sqdist", 333, 1234, 12, 2, 1.0, 0),
     ("sinkhorn", 600, 2500, 3, 1, 0.01, 0),
     ("sinkhorn", 257, 1000, 16, 1, 0.5, 5),
+    # 16 < D <= 256: the fp32 matrix-core kernel, signal columns in slices of 16
+    ("gauss", 300, 1000, 32, 1, 1.5, 0),
+    ("gauss", 200, 800, 64, 20, 2.0, 3),
+    ("laplace", 257, 900, 100, 3, 2.0, 1),
+    ("sqdist", 200, 700, 40, 2, 1.0, 0),
+    ("sinkhorn", 300, 1200, 48, 1, 4.0, 0),
+    ("sinkhorn", 129, 600, 256, 1, 20.0, 5),
 ]
 
 
@@ -140,6 +147,48 @@ def test_extreme_real_data(ctx, formula, M, N, D, E, param, C, red):
         assert (out == idx).mean() > 0.99   # near-ties aside, the same index
     else:
         assert (np.abs(out.astype(np.float64) - val) <= allow).all()
+
+
+@pytest.mark.parametrize("D,C", [(24, 0), (128, 4)])
+@pytest.mark.parametrize("red", ["max", "argmax"])
+def test_farthest_point_large_d(ctx, D, C, red):
+    # the squared distance's max without b at D > 16 (one signal column of ones)
+    rng = np.random.default_rng(D + C)
+    x = rng.uniform(0, 1, (300, D)).astype(np.float32)
+    y = rng.uniform(0, 1, (1100, D)).astype(np.float32)
+    out = host(ctx.run("sqdist", red, dev(x), dev(y), None, col_blocks=C))
+    val, idx, scale = oracle.extreme("sqdist", "max", x, y)
+    allow = TOL * scale
+    if red == "argmax":
+        f = _f_at("sqdist", x, y, None, out.astype(np.int64), 1.0)
+        assert (np.abs(f - val) <= allow).all()
+        assert (out == idx).mean() > 0.99
+    else:
+        assert (np.abs(out.astype(np.float64) - val) <= allow).all()
+
+
+def test_extreme_large_d_ranges(ctx):
+    from test_gpu_ranges import random_pattern
+    rng = np.random.default_rng(31)
+    M, N, D = 900, 1300, 48
+    x = rng.uniform(0, 1, (M, D)).astype(np.float32)
+    y = rng.uniform(0, 1, (N, D)).astype(np.float32)
+    b = rng.standard_normal((N, 2)).astype(np.float32)
+    pat = random_pattern(rng, M, N, 9, 11)
+    for red in ("max", "argmin"):
+        for C in (0, 1, 4):
+            out = host(ctx.run_ranges("gauss", red, dev(x), dev(y), dev(b), dev(pat[0]), dev(pat[1]),
+                                      dev(pat[2]), sigma=2.0, col_blocks=C))
+            ref, aux = oracle.ranges_reduce(red.replace("arg", ""), x, y, b, *pat, formula="gauss",
+                                            param=2.0)
+            empty = aux < 0
+            if red == "argmin":
+                assert (out[empty] == -1).all()
+                # a valid arg-min where the reference has one
+                assert (out[~empty] == aux[~empty]).mean() > 0.99
+            else:
+                assert np.isneginf(out[empty]).all()
+                assert np.abs(out[~empty] - ref[~empty]).max() <= 1e-4 * np.abs(b).max()
 
 
 @pytest.mark.parametrize("red,fill", [("min", np.inf), ("max", -np.inf), ("argmin", -1), ("argmax", -1)])

@@ -316,10 +316,11 @@ def test_large_d_argkmin_integer_bit_exact(ctx, M, N, D, K, C):
 
 
 def test_large_d_unsupported_pairs_raise(ctx):
+    # every valid pair is served at D > 16; a pair outside the table still fails
     from paper_2004_11127_amd import kred
     x = dev(np.ones((4, 32), np.float32)); y = dev(np.ones((4, 32), np.float32))
     with pytest.raises(kred.KredError) as e:
-        ctx.run("gauss", "max", x, y, dev(np.ones((4, 1), np.float32)), sigma=1.0)
+        ctx.run("sqdist", "lse", x, y, dev(np.ones((4, 1), np.float32)))
     assert e.value.status == 2
 
 
