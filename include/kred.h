@@ -151,8 +151,8 @@ kred_status kred_destroy(kred_ctx* ctx);
  * A0) / sigma^2; scratch grows by about (M + 64 N)(D + 1) floats), every LSE
  * (fp32 products; the expanded form's error in s is about 2^-24 (|x - m|^2 +
  * |y - m|^2) / eps, m the centre of y the matrix-core path subtracts from x and
- * y), ARGKMIN, KMIN, and MIN / ARGMIN of SQDIST without b; the other min / max
- * reductions return KRED_ERR_UNSUPPORTED there.  Inputs must be
+ * y), ARGKMIN, KMIN, and every MIN / MAX / ARGMIN / ARGMAX (fp32 products,
+ * signal columns in slices of 16).  Inputs must be
  * finite (NaN or Inf in x, y or b gives an undefined result).
  * Edge cases: M = 0 returns KRED_OK and touches nothing.  N = 0 writes zeros
  * (SUM), -infinity (LSE, MAX), +infinity (MIN) or -1 (ARGMIN, ARGMAX) and
