@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
           s[6 * d + 4] = h;
           s[6 * d + 5] = m;
         }
-      const float bj = nearest ? 0.0f : a.b[j];   // MIN and KNN read no b
+      const float bj = (nearest || a.epi == FAST_SUMV) ? 0.0f : a.b[j];   // MIN, KNN read no b
       if (a.D <= 3) {
         split3(-sg * nv, s[18], s[19], s[20]);
         s[21] = s[22] = s[23] = (__bf16)1.0f;
@@ -150,7 +150,12 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
         split3(-sg * nv + (a.epi == FAST_LSE ? bj * kLog2e : 0.0f), s[24], s[25], s[26]);
         s[27] = s[28] = s[29] = (__bf16)1.0f;
       }
-      if (a.epi == FAST_GRADX) {
+      if (a.epi == FAST_SUMV) {
+        float bv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bv[e] = e < a.E ? a.b[j * a.E + e] : 0.0f;
+        ex = float4{bv[0], bv[1], bv[2], bv[3]};
+      } else if (a.epi == FAST_GRADX) {
         ex = float4{bj, bj * v[0], bj * v[1], bj * v[2]};
       } else if (a.epi == FAST_SUM) {
         ex.x = bj;
@@ -160,7 +165,7 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
     __builtin_memcpy(w, s, 64);
 #pragma unroll
     for (int q = 0; q < 4; ++q) a.apk[j * 4 + q] = w[q];
-    if (a.epi == FAST_GRADX) a.ex[j] = ex;
+    if (a.epi == FAST_GRADX || a.epi == FAST_SUMV) a.ex[j] = ex;
     else if (a.epi == FAST_SUM) a.eb[j] = ex.x;
   }
 }
@@ -231,7 +236,8 @@ __device__ __forceinline__ void list_insert_lex(float (&dk)[KL], int (&jk)[KL], 
   jk[0] = lt[0] ? j : jk[0];
 }
 
-// EPI: FAST_SUM (Gauss, E = 1), FAST_GRADX, FAST_LSE.
+// EPI: FAST_SUM (Gauss, E = 1), FAST_GRADX, FAST_LSE, FAST_MIN, FAST_KNN, and
+// FAST_SUMV (Gauss, 2 <= E <= 4: the gradient's four accumulators on b's columns).
 
 // KV (FAST_MIN): write the distance (else the index).  KL (FAST_KNN): the
 // length of each lane's sorted list.
@@ -241,7 +247,8 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
   constexpr bool kKnn = EPI == FAST_KNN;
   constexpr bool kMin = EPI == FAST_MIN;
   __shared__ uint4 As[2][TJF * 4];
-  __shared__ float4 Xs[2][EPI == FAST_GRADX ? TJF : 1];   // (b, b v) per column
+  constexpr bool kVec = EPI == FAST_GRADX || EPI == FAST_SUMV;
+  __shared__ float4 Xs[2][kVec ? TJF : 1];   // (b, b v) or b's columns, per column
   __shared__ float4 Bq[2][EPI == FAST_SUM ? TJF / 4 : 1];  // b per column, 4 to a float4
 
   const FastFrame fr = fast_frame(a.guard, a.D, a.scale);
@@ -356,13 +363,13 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
       const int f = tid + q * 256;
       sa[q] = (f / 4 < ncol) ? a.apk[jt * 4 + f] : uint4{0u, 0u, 0u, 0u};
     }
-    if constexpr (EPI == FAST_GRADX) sx = (tid < ncol) ? a.ex[jt + tid] : float4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (kVec) sx = (tid < ncol) ? a.ex[jt + tid] : float4{0.f, 0.f, 0.f, 0.f};
     if constexpr (EPI == FAST_SUM) sb = (tid < ncol) ? a.eb[jt + tid] : 0.0f;
   };
   auto put = [&](int buf) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) As[buf][tid + q * 256] = sa[q];
-    if constexpr (EPI == FAST_GRADX) Xs[buf][tid] = sx;
+    if constexpr (kVec) Xs[buf][tid] = sx;
     if constexpr (EPI == FAST_SUM) reinterpret_cast<float*>(&Bq[buf][0])[tid] = sb;
   };
   auto a_operand = [&](int buf, int blk) {
@@ -751,6 +758,14 @@ __global__ __launch_bounds__(256) void fast_kernel(FastArgs a) {
           const float sum = (v[0] + v[1]) + (v[2] + v[3]);
           if (a.C == 1) static_cast<float*>(a.out)[row] = sum;
           else a.part[(int64_t)c * a.M + row] = sum;
+        } else if constexpr (EPI == FAST_SUMV) {
+          // the sums' layout: out M x E, partials C x M x EP
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (e >= a.E) break;
+            if (a.C == 1) static_cast<float*>(a.out)[row * a.E + e] = v[e];
+            else a.part[((int64_t)c * a.M + row) * a.EP + e] = v[e];
+          }
         } else {
           // G_d = sum_j k b (u_d - v_jd) = u_d a - H_d in prescaled units; divided
           // by the prescale it is sum_j k b (x_d - y_jd), as the direct kernel sums
@@ -802,6 +817,7 @@ hipError_t launch_fast(const FastArgs& a, hipStream_t s) {
   switch (a.epi) {
     case FAST_SUM: hipLaunchKernelGGL((fast_kernel<FAST_SUM, 4>), grid, dim3(256), 0, s, a); break;
     case FAST_GRADX: hipLaunchKernelGGL((fast_kernel<FAST_GRADX, 4>), grid, dim3(256), 0, s, a); break;
+    case FAST_SUMV: hipLaunchKernelGGL((fast_kernel<FAST_SUMV, 4>), grid, dim3(256), 0, s, a); break;
     case FAST_LSE: hipLaunchKernelGGL((fast_kernel<FAST_LSE, 4>), grid, dim3(256), 0, s, a); break;
     case FAST_MIN:
       if (a.kvalues) hipLaunchKernelGGL((fast_kernel<FAST_MIN, 4, true>), grid, dim3(256), 0, s, a);

@@ -169,6 +169,7 @@ int fast_epi(kred_formula f, kred_reduction r, int64_t M, int64_t N, int32_t D, 
   if (D > kFastMaxD || (flags & KRED_FLAG_DIRECT)) return -1;
   if (!(flags & KRED_FLAG_FAST) && (double)M * (double)N < kFastMinPairs) return -1;
   if (f == KRED_F_GAUSS && r == KRED_R_SUM && E == 1) return FAST_SUM;
+  if (f == KRED_F_GAUSS && r == KRED_R_SUM && E >= 2 && E <= 4) return FAST_SUMV;
   // the gradient's per-column extras (b, b v) hold three coordinates
   if (f == KRED_F_GAUSS_GRADX && r == KRED_R_SUM) return D <= 3 ? FAST_GRADX : -1;
   if ((f == KRED_F_SINKHORN || f == KRED_F_GAUSS) && r == KRED_R_LSE) return FAST_LSE;
@@ -201,7 +202,8 @@ FastScratch fast_scratch(int epi, int64_t N) {
   const int64_t N16 = (N + 15) / 16 * 16;
   fs.guard_bytes = align_up(sizeof(FastGuard));
   fs.apk_bytes = align_up(N16 * 64);
-  fs.ex_bytes = epi == FAST_GRADX ? align_up(N16 * 16) : (epi == FAST_SUM ? align_up(N16 * 4) : 0);
+  fs.ex_bytes = (epi == FAST_GRADX || epi == FAST_SUMV) ? align_up(N16 * 16)
+                : (epi == FAST_SUM ? align_up(N16 * 4) : 0);
   return fs;
 }
 
@@ -775,8 +777,10 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     fp.scale = pl.fscale;
     fp.guard = guard;
     fp.apk = reinterpret_cast<uint4*>(fbase + fs.guard_bytes);
-    fp.ex = epi == FAST_GRADX ? reinterpret_cast<float4*>(fbase + fs.guard_bytes + fs.apk_bytes)
-                              : nullptr;
+    fp.ex = (epi == FAST_GRADX || epi == FAST_SUMV)
+                ? reinterpret_cast<float4*>(fbase + fs.guard_bytes + fs.apk_bytes)
+                : nullptr;
+    fp.E = E;
     fp.eb = epi == FAST_SUM ? reinterpret_cast<float*>(fbase + fs.guard_bytes + fs.apk_bytes)
                             : nullptr;
     if (launch_fast_prologue(fp, x, M, s) != hipSuccess) return KRED_ERR_HIP;
@@ -801,6 +805,8 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     fa.K = pl.K;
     fa.KP = pl.KP;
     fa.y = y;
+    fa.E = E;
+    fa.EP = direct_pad_e(std::min(16, E));
     if (rg) {
       fa.nr = rg->nr;
       fa.rr = rg->rr;

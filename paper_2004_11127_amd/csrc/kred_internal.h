@@ -25,7 +25,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 // box in prescaled units), otherwise the direct-form kernels do the work.
 // Both are launched; each returns at once when the other one is selected.
 // MIN: nearest distance / index; KNN: the K nearest (1 < K <= 16)
-enum : int { FAST_SUM = 0, FAST_GRADX = 1, FAST_LSE = 2, FAST_MIN = 3, FAST_KNN = 4 };
+enum : int { FAST_SUM = 0, FAST_GRADX = 1, FAST_LSE = 2, FAST_MIN = 3, FAST_KNN = 4, FAST_SUMV = 5 };
 constexpr float kFastLimit = 2048.0f;
 
 struct FastGuard {
@@ -271,8 +271,9 @@ struct FastPackArgs {
   float scale;        // prescale sqrt(c)
   const FastGuard* guard;
   uint4* apk;         // N16 x 4 uint4: 32 bf16 A-operand slots per column
-  float4* ex;         // gradient: (b, b v0, b v1, b v2) per column
+  float4* ex;         // gradient: (b, b v0, b v1, b v2) per column; FAST_SUMV: b's E <= 4 columns
   float* eb;          // sum: b per column
+  int E;              // FAST_SUMV: signal columns of b (2..4)
 };
 hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M, hipStream_t s);
 
@@ -292,6 +293,7 @@ struct FastArgs {
   int kvalues;        // FAST_MIN, FAST_KNN: write the distances (else the indices)
   int K, KP;          // FAST_KNN: K, and the list length of the output / partial layout
   const float* y;     // FAST_MIN, FAST_KNN: the points (N x D), for the exact final distances
+  int E, EP;          // FAST_SUMV: signal columns, and the partial width of the sums' combine
   // block-sparse pattern (nr > 0), as in DirectArgs; bstart counts row
   // blocks of fast_rows_per_block rows
   int nr;

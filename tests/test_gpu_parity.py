@@ -450,3 +450,37 @@ def test_direct_sum_both_row_counts(ctx, formula, E):
         rows = np.sort(rng.choice(M, 300, replace=False))
         ref, norm = oracle.kernel_sum(formula, x, y, b, sigma=0.1, rows=rows)
         assert norm_err(out[rows], ref, norm) <= SUM_TOL
+
+
+@pytest.mark.parametrize("M,N,D,E,sigma,C", [(1000, 4099, 3, 3, 0.05, 0), (2049, 777, 2, 2, 0.1, 5),
+                                             (700, 2001, 4, 4, 0.08, 0), (1, 1, 3, 3, 0.3, 0),
+                                             (3000, 2500, 1, 4, 0.02, 16)])
+def test_fast_path_vector_signal(ctx, M, N, D, E, sigma, C):
+    # Gaussian sums with 2 <= E <= 4 signal columns on the matrix-core exponent
+    # path: the gradient's four accumulators carry b's columns
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(M + N + D + E)
+    x = _pts(rng, M, D, 1.0); y = _pts(rng, N, D, 1.0)
+    b = rng.standard_normal((N, E)).astype(np.float32)
+    ctx.profile_collect()
+    out = host(ctx.run("gauss", "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C,
+                       flags=kred.FLAG_FAST | kred.FLAG_PROFILE))
+    assert ctx.profile_collect()[2] == "fast_kernel"
+    ref, norm = oracle.kernel_sum("gauss", x, y, b, sigma=sigma)
+    assert out.shape == (M, E)
+    assert norm_err(out, ref, norm) <= SUM_TOL
+
+
+def test_fast_path_vector_signal_ranges(ctx):
+    from paper_2004_11127_amd import kred
+    from test_gpu_ranges import random_pattern
+    rng = np.random.default_rng(77)
+    M, N = 3000, 3500
+    x = _pts(rng, M, 3, 1.0); y = _pts(rng, N, 3, 1.0)
+    b = rng.standard_normal((N, 3)).astype(np.float32)
+    rows, ptr, cr = random_pattern(rng, M, N, 12, 20)
+    for C in (0, 1, 4):
+        out = host(ctx.run_ranges("gauss", "sum", dev(x), dev(y), dev(b), dev(rows), dev(ptr),
+                                  dev(cr), sigma=0.05, col_blocks=C, flags=kred.FLAG_FAST))
+        ref, norm = oracle.ranges_reduce("sum", x, y, b, rows, ptr, cr, formula="gauss", sigma=0.05)
+        assert norm_err(out, ref, norm) <= SUM_TOL, C
