@@ -685,8 +685,18 @@ constexpr int bf16_tile_cols(int DP) { return DP <= 64 ? 128 : (DP <= 128 ? 64 :
 // B[8 g .. 8 g + 7][li]; D as for the fp32 product, lane l holds
 // D[4 g + r][li].  With A = Y rows and B = X rows, lane l ranks column
 // j = 4 g + r for row i = li.  Coordinates d = 32 ch + 8 g + t.
+// Waves per SIMD the exact kernel is compiled for.  Dense, at 64 coordinates
+// and 4 <= K <= 10, its natural allocation (about 160 VGPRs) gives 3 waves;
+// held to 128 it spills 24-120 bytes per lane and the fourth wave is worth
+// more (10 nearest of 1e6 points for 1e5 queries: 21.0 -> 18.3 ms, 4 nearest
+// 17.4 -> 15.6 ms).  Elsewhere the compiler chooses.
+constexpr int knn_bf16_waves(int NCH, int KP, bool SP) {
+  return (!SP && NCH == 2 && KP >= 4 && KP <= 10) ? 4 : 1;
+}
+
 template <int NCH, int RB, int KP, bool SP>
-__global__ __launch_bounds__(256) void knn_bf16_kernel(MfmaArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(knn_bf16_waves(NCH, KP, SP))))
+void knn_bf16_kernel(MfmaArgs a) {
   if (!exact_ok(a.exact, a.D)) return;   // the fp32 kernel does the work
   constexpr int DP = 32 * NCH;
   constexpr int TJ = bf16_tile_cols(DP);
