@@ -242,13 +242,19 @@ __device__ __forceinline__ void list_insert_lex(float (&dk)[KL], int (&jk)[KL], 
 // KV (FAST_MIN): write the distance (else the index).  KL (FAST_KNN): the
 // length of each lane's sorted list.
 //
-// Waves per SIMD: the log-sum-exp form is compiled for 4 (its natural 131
-// VGPRs would give 3; held to 128 it spills 12 bytes per lane, and the fourth
-// wave pays: 1e6 x 1e6 Sinkhorn log-sum-exp 117.9 -> 113.8 ms).  For the
-// gradient the same hold spills 92 bytes and loses (154 -> 167 ms), so the
-// other forms keep the compiler's choice.
+// Waves per SIMD: the log-sum-exp form and the K-lists up to K = 12 are
+// compiled for 4.  Their natural allocations (131 to 142 VGPRs) would give 3;
+// held to 128 they spill 12 to 52 bytes per lane, and the fourth wave pays
+// (1e6 x 1e6, D = 3: Sinkhorn log-sum-exp 117.9 -> 113.8 ms, 4 nearest
+// 78.4 -> 63.6 ms, 12 nearest 117.8 -> 109.3 ms).  For the gradient the same
+// hold spills 92 bytes and loses (154 -> 167 ms), and for 16 nearest it
+// loses too (127 -> 188 ms), so the other forms keep the compiler's choice.
+constexpr int fast_waves(int EPI, int KL) {
+  return (EPI == FAST_LSE || (EPI == FAST_KNN && KL <= 12)) ? 4 : 1;
+}
+
 template <int EPI, int RB, bool KV = false, int KL = 1>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(EPI == FAST_LSE ? 4 : 1)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(fast_waves(EPI, KL))))
 void fast_kernel(FastArgs a) {
   constexpr bool kLse = EPI == FAST_LSE;
   constexpr bool kKnn = EPI == FAST_KNN;
