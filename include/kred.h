@@ -73,8 +73,17 @@ typedef enum kred_status {
 /* flags */
 #define KRED_FLAG_PROFILE 1u  /* time the main kernel of each call with HIP events (kred_profile_collect) */
 #define KRED_FLAG_DIRECT 2u   /* D <= 4: always use the direct-form kernels, never the matrix-core exponent
-                                 (used otherwise only below 2^28 pairs, or when the data's extent makes
-                                 the matrix-core form less accurate).  D > 16 arg-K-min (and K-min,
+                                 (used otherwise only below 2^28 pairs, or when the data's extent
+                                 c R^2 exceeds the matrix-core form's accuracy limit: 2048 at D <= 3,
+                                 128 at D = 4 for the sums and log-sum-exps, 2048 for the nearest
+                                 distances; R is the half-diagonal of the joint bounding box of x and
+                                 y, c = log2(e) / (2 sigma^2), log2(e) / eps, or 1).  Inside the limit
+                                 the matrix-core exponent's error stays below the direct form's parity
+                                 bar (1e-4 of sum_j |k_ij b_j|).  GAUSS_GRADX: the matrix-core path's
+                                 gradient is within 1e-4 sum_j |k_ij b_j| / sigma per component; the
+                                 direct form's within 1e-4 sum_j |k_ij b_j (y_jk - x_ik)| / sigma^2,
+                                 which resolves components that nearly cancel (e.g. x a subset of y
+                                 on data sparse against sigma).  D > 16 arg-K-min (and K-min,
                                  min / arg-min without b): always the fp32 matrix-core kernel, never
                                  the exact bf16 one */
 #define KRED_FLAG_FAST 4u     /* D <= 4: use the matrix-core exponent whatever the problem size (the
@@ -318,7 +327,11 @@ kred_status kred_validate_backward_ranges(const kred_params* p, int64_t M, int64
  * around the main reduction kernel of each call.  This waits for those
  * events, returns the number of timed launches in *count and their summed
  * duration in milliseconds in *total_ms, and forgets them.  Names the last
- * timed kernel family in *kernel (static string; may be NULL).
+ * timed kernel family in *kernel (static string; may be NULL).  Where the
+ * device picks the kernel (the small-D matrix-core path against the direct
+ * form, the exact k-NN kernel against the fp32 one), the name is what the
+ * device chose: for the small-D path over every profiled call since the last
+ * collect, "fast_kernel+direct" when the choice differed between them.
  */
 kred_status kred_profile_collect(kred_ctx* ctx, int32_t* count, double* total_ms,
                                  const char** kernel);

@@ -35,7 +35,7 @@ __device__ __forceinline__ float fast_log2(float v) { return __builtin_amdgcn_lo
 
 // ------------------------------------------------------------------ prologue
 __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
-  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale, a.flimit).ok) return;
   const int S = a.DP + a.EP;
   const int64_t total = a.N * S;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
@@ -325,7 +325,7 @@ template <int F, int DP, int EP, int R>
 __global__ __launch_bounds__(kThreads) void sum_kernel(DirectArgs a) {
   constexpr int S = DP + EP;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
-  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale, a.flimit).ok) return;
   const Item it = item_of<R>(a);
   if (!it.live) return;
   float xr[R][DP];
@@ -392,7 +392,7 @@ __global__ __launch_bounds__(kThreads) void gradx_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   constexpr int W = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
-  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale, a.flimit).ok) return;
   const Item it = item_of<R>(a);
   if (!it.live) return;
   float xr[R][DP];
@@ -559,7 +559,7 @@ template <int DP, int R, bool LAP>
 __global__ __launch_bounds__(kThreads) void lse_kernel(DirectArgs a) {
   constexpr int S = DP + 1;
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
-  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale, a.flimit).ok) return;
   const Item it = item_of<R>(a);
   if (!it.live) return;
   float xr[R][DP];
@@ -740,7 +740,7 @@ template <int DP, int KP, int R>
 __global__ __launch_bounds__(kThreads) void knn_kernel(DirectArgs a) {
   constexpr int S = DP + 1;   // the prologue pads one zero signal column
   __shared__ float4 lds[2 * Tile<S>::TJ * Tile<S>::SP / 4];
-  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale).ok) return;   // K = 1 on the fast path
+  if (a.guard != nullptr && fast_frame(a.guard, a.D, a.fscale, a.flimit).ok) return;   // K = 1 on the fast path
   const Item it = item_of<R>(a);
   if (!it.live) return;
   float xr[R][DP];

@@ -6,33 +6,59 @@
 // (column j, row i) pairs, which runs alongside the VALU/exp work, so the VALU
 // is left with the exp and the reduction itself.
 //
-// Accuracy.  With u = sqrt(c) (x - m) and v = sqrt(c) (y - m) for a centre m,
+// Operands.  With u = sqrt(c) (x - m) and v = sqrt(c) (y - m) for the centre m
+// of the joint bounding box of x and y (formed in fp64 from the fp32 inputs),
 //     T = 2 <u, v> - |u|^2 - |v|^2.
-// Every fp32 operand is split into three bf16 parts (h + m + l carries 24+
-// bits); the products hh, hm, mh, hl, lh, mm of each coordinate, and the
-// three parts of -|u|^2 and -|v|^2, fill 24 of the 32 K slots, so each
-// product term is exact and only terms below 2^-26 |u||v| are dropped.  The
-// large cancelling terms sit in the first 8-slot group of K, which the matrix
-// core sums with more than fp32 precision.  The remaining error grows with
-// c R^2, R the half-diagonal of the joint bounding box of x and y around its
-// centre m; the prologue computes it on the device and the kernels fall back
-// to the direct form when c R^2 > kFastLimit (no host synchronisation).
+// U is the largest prescaled half-width of the box, L = c R^2 its squared
+// prescaled half-diagonal, and qu the power of two with U <= 255 qu < 2 U.
+// Each coordinate is split into three bf16 parts on a common grid:
+//     u = uh + um + ul,  uh = qu k (|k| <= 256, exact in bf16),
+// um and ul the bf16 roundings of what is left (|u - (uh + um + ul)| <= 2^-19 qu);
+// V = 2 v the same way with the grid 2 qu.  Every leading product Vh uh is
+// then a multiple of q = 2 qu^2 no larger than 2^16 q.  The row norm |u~|^2 and
+// the column norm w = -|v~|^2 (+ g' = g log2(e) for the log-sum-exp) of the
+// represented coordinates are computed in fp64; their leading parts are
+// rounded to multiples of max(q, their bf16 spacing), so they too are exact
+// in bf16 and multiples of q.
 //
-// The nearest-neighbour variant (FAST_MIN) flips every sign, so that the
-// matrix core returns the squared distance |u - v|^2 itself (c = 1, centred
-// coordinates): minimum and arg-minimum then need no exp at all.
+// K slots (A: column side, B: row side).  Group 0 (slots 0..7) holds every
+// term of size O(L), all multiples of q, so their sum is exact whatever order
+// or width the matrix core adds them in (partial sums stay below 2^20 q):
+//     slot d < D: (Vh_d, uh_d);  slot 4: (w_h, 1);  slot 5: (1, -h) with h the
+//     leading part of |u~|^2 (+h, rounded up, for the nearest distances).
+// From slot 8 on, per coordinate d, the products (Vh,um), (Vm,uh), (Vh,ul),
+// (Vl,uh), (Vm,um), (Vm,ul), (Vl,um) (D <= 3: seven per coordinate, slots
+// 8 + 7d ..; D = 4: the first five, slots 8 + 5d ..), then the column norm's
+// three trailing parts with B = 1 (slots 29..31; D = 4: 28..30).  The row
+// norm's remainder r = |u~|^2 - h stays out of the product: the matrix core
+// returns T' = T~ + r, and the epilogue scales the row's sums by 2^-r (the
+// log-sum-exp subtracts r).  The nearest-neighbour forms need no correction:
+// with h rounded up, T' = |u~ - v~|^2 + (h - |u~|^2) ranks like the distance.
 //
-// K slots (A: column side, B: row side), for coordinate d = 0..D-1, D <= 3:
-//   6d + 0..5:  A = (Vh, Vm, Vh, Vl, Vh, Vm) of V = 2 v_d,
-//               B = (uh, uh, um, uh, ul, um) of u_d
-//   18..20:     A = parts of -|v|^2, B = 1
-//   21..23:     A = 1,               B = parts of -|u|^2
-//   24..26:     log-sum-exp only: A = parts of g' = g log2(e), B = 1
-//   27..31:     0
-// D = 4: the products fill 0..23, A = parts of -|v|^2 (+ g' for the
-// log-sum-exp) with B = 1 in 24..26, A = 1 with B = parts of -|u|^2 in 27..29.
-// The fused gradient's per-column extras (b, b v) hold three coordinates, so
-// it runs here for D <= 3 only.
+// Error of T' - r against -c |x - y|^2 in log2 units, for a pair with
+// t = c |x - y|^2, every rounding at its largest:
+//   representation of u and v   sqrt(D t) U 2^-24
+//   dropped products            D <= 3: (Vl, ul), below D L 2^-33;
+//                               D = 4: also (Vm, ul) and (Vl, um), below L 2^-21
+//   norms                       column: 4 parts, below 2^-35 |w|; row: exact
+//   fp32 accumulation           group 0 is exact; groups 1..3 hold terms of
+//                               total size M1 <= sqrt(D) L / 64 + L / 256, so
+//                               the 7 roundings inside group 1 are below
+//                               2^-24 M1 each, and the 3 that add the groups
+//                               below 2^-24 (t + L / 256 + 2 M1) each.
+// At D <= 3 and L = 2048 the sum is below 1.2e-4 for every t <= 126, so a
+// term's relative error (ln 2 times that) stays below 8e-5; at D = 4 and
+// L = 128 below 7.5e-5 (the dropped products dominate).  Typical errors are
+// about 40 times smaller (2e-6 at L = 2000 on uniform data).  kFastLimit3 and
+// kFastLimit4 keep inputs there: the prologue computes the box on the device
+// and the kernels fall back to the direct form beyond the limit (no host
+// synchronisation).
+//
+// The nearest-neighbour variants (FAST_MIN, FAST_KNN) flip every sign, so the
+// matrix core returns the squared distance (plus the row constant h - |u~|^2)
+// with c = 1: minimum and arg-minimum then need no exp at all.  They rank by
+// it and recompute the final candidates' distances in the direct form.
+//
 // Lane layout of v_mfma_f32_16x16x32_bf16 (lane l = 16 g + li): A: lane
 // supplies A[li][8g .. 8g+7]; B: lane supplies B[8g .. 8g+7][li]; D: lane holds
 // D[4g + r][li].  With A = columns and B = rows, lane l gets T for row li and
@@ -49,13 +75,50 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int TJF = 256;             // columns per LDS tile
 constexpr float kRescaleF = 32.0f;   // log-sum-exp rescale threshold (log2 units)
+constexpr double kLog2eD = 1.4426950408889634;
 
-__device__ __forceinline__ void split3(float v, __bf16& h, __bf16& m, __bf16& l) {
-  h = (__bf16)v;
-  float r = v - (float)h;
-  m = (__bf16)r;
-  r -= (float)m;
-  l = (__bf16)r;
+// Products beyond (h, h) per coordinate as (column part, row part), 0 = h,
+// 1 = m, 2 = l: D <= 3 takes all seven, D = 4 the first five.
+constexpr int kProdA[7] = {0, 1, 0, 2, 1, 1, 2};
+constexpr int kProdB[7] = {1, 0, 2, 0, 1, 2, 1};
+template <bool D4>
+struct Slots {
+  static constexpr int per = D4 ? 5 : 7;      // products beyond (h, h) per coordinate
+  static constexpr int tail = D4 ? 28 : 29;   // the column norm's three trailing parts
+};
+constexpr int kSlotW = 4;   // leading part of the column norm (B = 1)
+constexpr int kSlotH = 5;   // leading part of the row norm (A = 1)
+
+// The grid of the leading parts: the power of two qu with U (1 + 2^-10) <= 255 qu
+// (the margin covers the fp32 rounding of the box), so |u| / qu <= 256.
+__device__ __forceinline__ double fast_quantum(float U) {
+  int e;
+  (void)frexp((double)U * (1.0 + 1.0 / 1024.0) / 255.0, &e);
+  return ldexp(1.0, e);
+}
+
+__device__ __forceinline__ __bf16 to_bf16(double v) { return (__bf16)(float)v; }
+__device__ __forceinline__ double of_bf16(__bf16 v) { return (double)(float)v; }
+
+// v = h + m + l: h = q rint(v / q) (|v| <= 256 q, exact in bf16), m and l the
+// bf16 roundings of what is left.  Returns h + m + l (exact in fp64).
+__device__ __forceinline__ double split_fixed(double v, double q, __bf16& h, __bf16& m, __bf16& l) {
+  const double hv = q * rint(v / q);
+  h = to_bf16(hv);
+  double r = v - hv;
+  m = to_bf16(r);
+  r -= of_bf16(m);
+  l = to_bf16(r);
+  return hv + of_bf16(m) + of_bf16(l);
+}
+
+// Leading part of a norm: the nearest multiple of max(q, the bf16 spacing at
+// w) (up: the next one at or above w), exact in bf16 and a multiple of q.
+__device__ __forceinline__ double norm_head(double w, double q, bool up) {
+  int e;
+  (void)frexp(w, &e);   // |w| in [2^(e-1), 2^e)
+  const double Q = w == 0.0 ? q : fmax(q, ldexp(1.0, e - 8));
+  return Q * (up ? ceil(w / Q) : rint(w / Q));
 }
 
 __global__ void guard_init_kernel(FastGuard* g) {
@@ -108,13 +171,50 @@ __global__ __launch_bounds__(256) void bounds_kernel(const float* __restrict__ x
   }
 }
 
+// Column side of one column j < N: its 32 A slots, and the represented
+// prescaled coordinates v~ (for the gradient's extras).  g2: g' of the
+// log-sum-exp (else 0).
+template <bool D4>
+__device__ __forceinline__ void pack_column(const FastPackArgs& a, const FastFrame& fr, double qu,
+                                            int64_t j, bool nearest, double g2, __bf16 (&s)[32],
+                                            float (&vt)[kFastMaxD]) {
+  using S = Slots<D4>;
+  double nv = 0.0;
+#pragma unroll
+  for (int d = 0; d < kFastMaxD; ++d) {
+    if (D4 || d < a.D) {
+      const double v = ((double)a.y[j * a.D + d] - (double)fr.m[d]) * a.scale64;
+      __bf16 p[3];
+      // V = 2 v for the sums, -2 v for the nearest distances (T = +|u - v|^2)
+      const double V = split_fixed((nearest ? -2.0 : 2.0) * v, 2.0 * qu, p[0], p[1], p[2]);
+      nv = fma(0.5 * V, 0.5 * V, nv);
+      vt[d] = (float)(nearest ? -0.5 * V : 0.5 * V);
+      s[d] = p[0];
+#pragma unroll
+      for (int i = 0; i < S::per; ++i) s[8 + S::per * d + i] = p[kProdA[i]];
+    }
+  }
+  const double w = (nearest ? nv : -nv) + g2;
+  const double h = norm_head(w, 2.0 * qu * qu, false);
+  s[kSlotW] = to_bf16(h);
+  s[kSlotH] = (__bf16)1.0f;
+  double r = w - h;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    s[S::tail + k] = to_bf16(r);
+    r -= of_bf16(s[S::tail + k]);
+  }
+}
+
 // Column-side packing: A row (32 bf16) and per-column extras.
-//   sum:   ex = (b, -, -, -)        gradx: ex = (b, b v0, b v1, b v2)
-//   lse:   g' = g log2(e) in A slots 24..26 (D = 4: added to -|v|^2 in 24..26)
+//   sum:   eb = b                   gradx: ex = (b, b v~0, b v~1, b v~2)
+//   sumv:  ex = b's E <= 4 columns  lse:   g' = g log2(e) joins the column norm
 // Padding columns (N <= j < N16) get zero A rows and zero extras.
 __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
-  const FastFrame fr = fast_frame(a.guard, a.D, a.scale);
+  const FastFrame fr = fast_frame(a.guard, a.D, a.scale, a.limit);
   if (!fr.ok) return;
+  const double qu = fast_quantum(fr.U);
+  const bool nearest = a.epi == FAST_MIN || a.epi == FAST_KNN;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < a.N16; j += stride) {
     __bf16 s[32];
@@ -122,41 +222,18 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
     for (int k = 0; k < 32; ++k) s[k] = (__bf16)0.0f;
     float4 ex = {0.f, 0.f, 0.f, 0.f};
     if (j < a.N) {
-      float v[kFastMaxD] = {0.f, 0.f, 0.f, 0.f};
-      float nv = 0.0f;
-      const bool nearest = a.epi == FAST_MIN || a.epi == FAST_KNN;
-      const float sg = nearest ? -1.0f : 1.0f;   // MIN, KNN: T = +|u - v|^2
-#pragma unroll
-      for (int d = 0; d < kFastMaxD; ++d)
-        if (d < a.D) {
-          v[d] = (a.y[j * a.D + d] - fr.m[d]) * a.scale;
-          nv = __builtin_fmaf(v[d], v[d], nv);
-          __bf16 h, m, l;
-          split3(sg * 2.0f * v[d], h, m, l);
-          s[6 * d + 0] = h;
-          s[6 * d + 1] = m;
-          s[6 * d + 2] = h;
-          s[6 * d + 3] = l;
-          s[6 * d + 4] = h;
-          s[6 * d + 5] = m;
-        }
+      float vt[kFastMaxD] = {0.f, 0.f, 0.f, 0.f};
       const float bj = (nearest || a.epi == FAST_SUMV) ? 0.0f : a.b[j];   // MIN, KNN read no b
-      if (a.D <= 3) {
-        split3(-sg * nv, s[18], s[19], s[20]);
-        s[21] = s[22] = s[23] = (__bf16)1.0f;
-        if (a.epi == FAST_LSE) split3(bj * kLog2e, s[24], s[25], s[26]);
-      } else {
-        // D = 4: the products fill slots 0..23; g' joins -|v|^2
-        split3(-sg * nv + (a.epi == FAST_LSE ? bj * kLog2e : 0.0f), s[24], s[25], s[26]);
-        s[27] = s[28] = s[29] = (__bf16)1.0f;
-      }
+      const double g2 = a.epi == FAST_LSE ? (double)bj * kLog2eD : 0.0;
+      if (a.D == 4) pack_column<true>(a, fr, qu, j, nearest, g2, s, vt);
+      else pack_column<false>(a, fr, qu, j, nearest, g2, s, vt);
       if (a.epi == FAST_SUMV) {
         float bv[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) bv[e] = e < a.E ? a.b[j * a.E + e] : 0.0f;
         ex = float4{bv[0], bv[1], bv[2], bv[3]};
       } else if (a.epi == FAST_GRADX) {
-        ex = float4{bj, bj * v[0], bj * v[1], bj * v[2]};
+        ex = float4{bj, bj * vt[0], bj * vt[1], bj * vt[2]};
       } else if (a.epi == FAST_SUM) {
         ex.x = bj;
       }
@@ -170,34 +247,43 @@ __global__ __launch_bounds__(256) void fast_pack_kernel(FastPackArgs a) {
   }
 }
 
-// Row-side B operand: this lane's 8 K slots (8g .. 8g+7) for its row.
-__device__ __forceinline__ bf16x8 row_operand(const float (&u)[kFastMaxD], int D, int g, bool lse,
-                                               bool neg) {
-  __bf16 s[32];
+// Row side of one row: its 32 B slots from the centred, prescaled coordinates
+// u (fp64), the represented coordinates u~ (fp32, for the gradient), and the
+// row norm's remainder r = |u~|^2 - h left out of the product.
+template <bool D4>
+__device__ __forceinline__ double row_slots(const double (&u)[kFastMaxD], int D, double qu,
+                                            bool nearest, __bf16 (&s)[32], float (&ut)[kFastMaxD]) {
+  using S = Slots<D4>;
 #pragma unroll
   for (int k = 0; k < 32; ++k) s[k] = (__bf16)0.0f;
-  float nu = 0.0f;
+  double nu = 0.0;
 #pragma unroll
-  for (int d = 0; d < kFastMaxD; ++d)
-    if (d < D) {
-      __bf16 h, m, l;
-      split3(u[d], h, m, l);
-      s[6 * d + 0] = h;
-      s[6 * d + 1] = h;
-      s[6 * d + 2] = m;
-      s[6 * d + 3] = h;
-      s[6 * d + 4] = l;
-      s[6 * d + 5] = m;
-      nu = __builtin_fmaf(u[d], u[d], nu);
+  for (int d = 0; d < kFastMaxD; ++d) {
+    ut[d] = 0.0f;
+    if (D4 || d < D) {
+      __bf16 p[3];
+      const double ud = split_fixed(u[d], qu, p[0], p[1], p[2]);
+      nu = fma(ud, ud, nu);
+      ut[d] = (float)ud;
+      s[d] = p[0];
+#pragma unroll
+      for (int i = 0; i < S::per; ++i) s[8 + S::per * d + i] = p[kProdB[i]];
     }
-  if (D <= 3) {
-    s[18] = s[19] = s[20] = (__bf16)1.0f;
-    split3(neg ? nu : -nu, s[21], s[22], s[23]);
-    if (lse) s[24] = s[25] = s[26] = (__bf16)1.0f;
-  } else {
-    s[24] = s[25] = s[26] = (__bf16)1.0f;
-    split3(neg ? nu : -nu, s[27], s[28], s[29]);
   }
+  const double h = norm_head(nu, 2.0 * qu * qu, nearest);
+  s[kSlotW] = (__bf16)1.0f;
+  s[kSlotH] = to_bf16(nearest ? h : -h);
+#pragma unroll
+  for (int k = 0; k < 3; ++k) s[S::tail + k] = (__bf16)1.0f;
+  return nu - h;
+}
+
+// Row-side B operand: this lane's 8 K slots (8g .. 8g+7) for its row, and the
+// row norm's remainder (see row_slots).
+__device__ __forceinline__ bf16x8 row_operand(const double (&u)[kFastMaxD], int D, int g, double qu,
+                                               bool nearest, double* rem, float (&ut)[kFastMaxD]) {
+  __bf16 s[32];
+  *rem = D == 4 ? row_slots<true>(u, D, qu, nearest, s, ut) : row_slots<false>(u, D, qu, nearest, s, ut);
   bf16x8 o;
 #pragma unroll
   for (int e = 0; e < 8; ++e) o[e] = s[8 * g + e];
@@ -263,9 +349,15 @@ void fast_kernel(FastArgs a) {
   constexpr bool kVec = EPI == FAST_GRADX || EPI == FAST_SUMV;
   __shared__ float4 Xs[2][kVec ? TJF : 1];   // (b, b v) or b's columns, per column
   __shared__ float4 Bq[2][EPI == FAST_SUM ? TJF / 4 : 1];  // b per column, 4 to a float4
+  // per row of the workgroup: the row norm's remainder (sums, log-sum-exp)
+  // and the represented coordinates (gradient), from the set-up to the end
+  constexpr bool kRem = !kMin && !kKnn;
+  __shared__ float Rs[kRem ? 64 * RB : 1];
+  __shared__ float Us[EPI == FAST_GRADX ? 3 : 1][EPI == FAST_GRADX ? 64 * RB : 1];
 
-  const FastFrame fr = fast_frame(a.guard, a.D, a.scale);
+  const FastFrame fr = fast_frame(a.guard, a.D, a.scale, a.limit);
   if (!fr.ok) return;
+  const double qu = fast_quantum(fr.U);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, li = lane & 15, g = lane >> 4;
   const int c = blockIdx.x % a.C;
@@ -301,15 +393,34 @@ void fast_kernel(FastArgs a) {
   }
   const int64_t i0 = row0 + wave * (16 * RB);
 
-  bf16x8 xb[RB];
-  float ur[RB][kFastMaxD];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int64_t row = i0 + 16 * rb + li;
+  // The row's centred, prescaled coordinates in fp64, its B operand, and the
+  // row norm's remainder r left out of the product (row_slots); the epilogue
+  // forms them again rather than keeping them live through the column loop.
+  auto row_coords = [&](int64_t row, double (&u)[kFastMaxD]) __attribute__((always_inline)) {
 #pragma unroll
     for (int d = 0; d < kFastMaxD; ++d)
-      ur[rb][d] = (row < row_end && d < a.D) ? (a.x[row * a.D + d] - fr.m[d]) * a.scale : 0.0f;
-    xb[rb] = row_operand(ur[rb], a.D, g, kLse, kMin || kKnn);
+      u[d] = (row < row_end && d < a.D) ? ((double)a.x[row * a.D + d] - (double)fr.m[d]) * a.scale64 : 0.0;
+  };
+  bf16x8 xb[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    double u[kFastMaxD], rem;
+    float ut[kFastMaxD];
+    row_coords(i0 + 16 * rb + li, u);
+    xb[rb] = row_operand(u, a.D, g, qu, kMin || kKnn, &rem, ut);
+    const int rs = wave * (16 * RB) + 16 * rb + li;
+    if constexpr (kRem) {
+      if (g == 0) Rs[rs] = (float)rem;
+    }
+    if constexpr (EPI == FAST_GRADX) {
+      if (g == 0) {
+#pragma unroll
+        for (int d = 0; d < 3; ++d) Us[d][rs] = ut[d];
+      }
+    }
+    // one row block at a time: interleaved, the fp64 set-up of all four would
+    // set the kernel's register count
+    __builtin_amdgcn_sched_barrier(0);
   }
   // per lane: sums over its columns (4 g + r of every block) for row li;
   // MIN: the smallest distance (as its int bits, exact order for d >= 0) and its column
@@ -750,11 +861,13 @@ void fast_kernel(FastArgs a) {
         m = mx;
       }
       if (g == 0 && live_row) {
+        // the matrix core returned T + r for the row norm's remainder r
+        const float rem = Rs[wave * (16 * RB) + 16 * rb + li];
         if (a.C == 1) {
-          static_cast<float*>(a.out)[row] = (m + __builtin_amdgcn_logf(s)) * kLn2;
+          static_cast<float*>(a.out)[row] = (m + __builtin_amdgcn_logf(s) - rem) * kLn2;
         } else {
           float* p = a.part + ((int64_t)c * a.M + row) * 2;
-          p[0] = m;
+          p[0] = m - rem;
           p[1] = s;
         }
       }
@@ -767,6 +880,11 @@ void fast_kernel(FastArgs a) {
         v[q] += __shfl_xor(v[q], 32);
       }
       if (g == 0 && live_row) {
+        // the matrix core returned T + r for the row norm's remainder r
+        const int rs = wave * (16 * RB) + 16 * rb + li;
+        const float f = __builtin_amdgcn_exp2f(-Rs[rs]);   // 2^-r
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] *= f;
         if constexpr (EPI == FAST_SUM) {
           const float sum = (v[0] + v[1]) + (v[2] + v[3]);
           if (a.C == 1) static_cast<float*>(a.out)[row] = sum;
@@ -782,9 +900,9 @@ void fast_kernel(FastArgs a) {
         } else {
           // G_d = sum_j k b (u_d - v_jd) = u_d a - H_d in prescaled units; divided
           // by the prescale it is sum_j k b (x_d - y_jd), as the direct kernel sums
-          const float inv = 1.0f / a.scale;
-          const float G[3] = {(ur[rb][0] * v[0] - v[1]) * inv, (ur[rb][1] * v[0] - v[2]) * inv,
-                              (ur[rb][2] * v[0] - v[3]) * inv};
+          const float inv = (float)(1.0 / a.scale64);
+          const float G[3] = {(Us[0][rs] * v[0] - v[1]) * inv, (Us[1][rs] * v[0] - v[2]) * inv,
+                              (Us[2][rs] * v[0] - v[3]) * inv};
           if (a.C == 1) {
             float* o = static_cast<float*>(a.out) + row * (1 + a.D);
             o[0] = v[0];
@@ -820,6 +938,21 @@ hipError_t launch_fast_prologue(const FastPackArgs& a, const float* x, int64_t M
   if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
   const int64_t pb = std::max<int64_t>(1, std::min<int64_t>((a.N16 + 255) / 256, 8192));
   hipLaunchKernelGGL(fast_pack_kernel, dim3((unsigned)pb), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+namespace {
+__global__ void fast_record_kernel(const FastGuard* g, int D, float scale, float limit, int* counts) {
+  if (threadIdx.x == 0) {
+    if (fast_frame(g, D, scale, limit).ok) atomicAdd(&counts[0], 1);
+    atomicAdd(&counts[1], 1);
+  }
+}
+}  // namespace
+
+hipError_t launch_fast_record(const FastGuard* g, int D, float scale, float limit, int* counts,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(fast_record_kernel, dim3(1), dim3(64), 0, s, g, D, scale, limit, counts);
   return hipGetLastError();
 }
 

@@ -31,6 +31,12 @@ struct kred_ctx {
   // outlives scratch growth), and whether the last profiled call used it
   ExactGuard* exact_guard = nullptr;
   int last_exact_D = 0;
+  // small-D calls with the matrix-core path eligible: per profiled call, the
+  // device records whether its guard chose that path (counts[0]) out of all
+  // such calls (counts[1]); the name is resolved at collect time
+  int* fast_counts = nullptr;
+  bool last_fast = false;
+  const char* last_direct = "none";   // the direct-form kernel those calls fall back to
 };
 
 namespace {
@@ -65,6 +71,7 @@ struct Plan {
   float xscale, bscale, gscale;
   float kscale;   // direct kernels: pair scale (input coordinates)
   float fscale;   // fast path: coordinate prescale sqrt(c)
+  double fscale64;   // the same in fp64
 };
 
 // Column split: enough (row block, column block) work items to keep every
@@ -125,6 +132,7 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
   q.gscale = 0.0f;
   q.kscale = 1.0f;
   q.fscale = 1.0f;
+  q.fscale64 = 1.0;
   switch ((int)f) {
     case KRED_F_GAUSS:
     case KRED_F_GAUSS_GRADX:
@@ -133,6 +141,7 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
       const double c = log2e / (2.0 * s * s);
       q.kscale = (float)c;
       q.fscale = (float)std::sqrt(c);
+      q.fscale64 = std::sqrt(c);
       q.gscale = (float)(1.0 / (s * s));
       break;
     }
@@ -142,6 +151,7 @@ bool make_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M
     case KRED_F_SINKHORN:
       q.kscale = (float)(log2e / (double)p->eps);
       q.fscale = (float)std::sqrt(log2e / (double)p->eps);
+      q.fscale64 = std::sqrt(log2e / (double)p->eps);
       q.bscale = (float)log2e;
       break;
     default:
@@ -568,6 +578,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
         if (hipEventRecord(x1, s) != hipSuccess) return KRED_ERR_HIP;
         ctx->last_kernel = "mfma_kernel";
         ctx->last_exact_D = 0;
+        ctx->last_fast = false;
       }
       CombineArgs ca{};
       ca.formula = (int)f;
@@ -603,6 +614,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   if (prof) {
     if (hipEventRecord(e1, s) != hipSuccess) return KRED_ERR_HIP;
     ctx->last_kernel = split ? "mfma_split_kernel" : "mfma_kernel";
+    ctx->last_fast = false;
     ctx->last_exact_D = exact ? D : 0;   // resolved from the guard at collect time
   }
   if (knn || pl.C > 1) {
@@ -763,6 +775,8 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   int* fbstart = rg ? reinterpret_cast<int*>(reinterpret_cast<char*>(bstart) + bstart_bytes / 2)
                     : nullptr;
   FastGuard* guard = epi >= 0 ? reinterpret_cast<FastGuard*>(fbase) : nullptr;
+  // largest c R^2 the fast path takes: every kernel of the call tests the same
+  const float flimit = fast_limit(D, epi == FAST_MIN || epi == FAST_KNN);
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
 
   FastArgs fa{};
@@ -775,6 +789,8 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     fp.y = y;
     fp.b = b;
     fp.scale = pl.fscale;
+    fp.scale64 = pl.fscale64;
+    fp.limit = flimit;
     fp.guard = guard;
     fp.apk = reinterpret_cast<uint4*>(fbase + fs.guard_bytes);
     fp.ex = (epi == FAST_GRADX || epi == FAST_SUMV)
@@ -794,6 +810,8 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     fa.jpb = pl.jpb;
     fa.x = x;
     fa.scale = pl.fscale;
+    fa.scale64 = pl.fscale64;
+    fa.limit = flimit;
     fa.gscale = pl.gscale;
     fa.guard = guard;
     fa.apk = fp.apk;
@@ -836,6 +854,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     pa.bscale = pl.bscale;
     pa.guard = guard;
     pa.fscale = pl.fscale;
+    pa.flimit = flimit;
     pa.unit_b = ext && b == nullptr;   // squared-distance max without b: F = d * 1
     if (launch_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
 
@@ -856,6 +875,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     da.kscale = pl.kscale;
     da.gscale = pl.gscale;
     da.fscale = pl.fscale;
+    da.flimit = flimit;
     da.out = out;
     da.part = part;
     da.KP = pl.KP;
@@ -905,12 +925,27 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
     if (prof) {
       if (hipEventRecord(e_stop, s) != hipSuccess) return KRED_ERR_HIP;
       ctx->last_exact_D = 0;
-      ctx->last_kernel = (epi >= 0)                  ? "fast_kernel"
-                         : ext                       ? "extreme_kernel"
-                         : (r == KRED_R_ARGKMIN)     ? "knn_kernel"
-                         : (f == KRED_F_GAUSS_GRADX) ? "gradx_kernel"
-                         : (r == KRED_R_LSE)         ? "lse_kernel"
-                                                     : "sum_kernel";
+      const char* direct = ext                       ? "extreme_kernel"
+                           : (r == KRED_R_ARGKMIN)     ? "knn_kernel"
+                           : (f == KRED_F_GAUSS_GRADX) ? "gradx_kernel"
+                           : (r == KRED_R_LSE)         ? "lse_kernel"
+                                                       : "sum_kernel";
+      ctx->last_kernel = direct;
+      ctx->last_fast = false;
+      if (epi >= 0) {
+        // which of the two did the work is known on the device only
+        if (ctx->fast_counts == nullptr) {
+          if (hipMalloc(reinterpret_cast<void**>(&ctx->fast_counts), 2 * sizeof(int)) != hipSuccess) {
+            ctx->fast_counts = nullptr;
+            return KRED_ERR_NOMEM;
+          }
+          if (hipMemset(ctx->fast_counts, 0, 2 * sizeof(int)) != hipSuccess) return KRED_ERR_HIP;
+        }
+        if (launch_fast_record(guard, D, pl.fscale, flimit, ctx->fast_counts, s) != hipSuccess)
+          return KRED_ERR_HIP;
+        ctx->last_fast = true;
+        ctx->last_direct = direct;
+      }
     }
     if (pl.C > 1) {
       CombineArgs ca{};
@@ -1055,6 +1090,7 @@ kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, i
       if (hipEventRecord(e_stop, s) != hipSuccess) return KRED_ERR_HIP;
       ctx->last_exact_D = 0;
       ctx->last_kernel = "vjp_kernel";
+      ctx->last_fast = false;
     }
     if (pl.C > 1) {
       CombineArgs ca{};
@@ -1206,6 +1242,7 @@ kred_status kred_destroy(kred_ctx* ctx) {
     if (ctx->aux) (void)hipFree(ctx->aux);
     if (ctx->wide) (void)hipFree(ctx->wide);
     if (ctx->exact_guard) (void)hipFree(ctx->exact_guard);
+    if (ctx->fast_counts) (void)hipFree(ctx->fast_counts);
     for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
   }
   delete ctx;
@@ -1399,6 +1436,16 @@ kred_status kred_profile_collect(kred_ctx* ctx, int32_t* count, double* total_ms
     const bool ok = h.nonint == 0u && m <= kExactMaxAbs &&
                     (float)ctx->last_exact_D * m * m <= kExactMaxSum;
     ctx->last_kernel = ok ? "knn_bf16_kernel" : "mfma_kernel";
+  }
+  if (ctx->last_fast && ctx->fast_counts != nullptr) {
+    // small-D calls since the last collect: the matrix-core kernel in all of
+    // them, in none (the direct form), or in some
+    int h[2] = {0, 0};
+    if (hipMemcpy(h, ctx->fast_counts, sizeof(h), hipMemcpyDeviceToHost) != hipSuccess ||
+        hipMemset(ctx->fast_counts, 0, sizeof(h)) != hipSuccess)
+      return KRED_ERR_HIP;
+    ctx->last_kernel = h[0] == h[1] ? "fast_kernel" : h[0] == 0 ? ctx->last_direct : "fast_kernel+direct";
+    ctx->last_fast = false;
   }
   if (kernel) *kernel = ctx->last_kernel;
   ctx->ev_used = 0;

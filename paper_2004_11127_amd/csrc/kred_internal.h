@@ -19,14 +19,26 @@ constexpr int kThreads = 256;          // threads per workgroup for the direct-f
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-// Small-D fast path (D <= 3): exponent on the bf16 matrix cores.  The
+// Small-D fast path (D <= 4): exponent on the bf16 matrix cores.  The
 // prologue computes the joint bounding box of x and y on the device; the
-// fast kernels run only when c R^2 <= kFastLimit (R the half-diagonal of the
-// box in prescaled units), otherwise the direct-form kernels do the work.
+// fast kernels run only when c R^2 <= the limit for D (R the half-diagonal of
+// the box in prescaled units), otherwise the direct-form kernels do the work.
 // Both are launched; each returns at once when the other one is selected.
 // MIN: nearest distance / index; KNN: the K nearest (1 < K <= 16)
 enum : int { FAST_SUM = 0, FAST_GRADX = 1, FAST_LSE = 2, FAST_MIN = 3, FAST_KNN = 4, FAST_SUMV = 5 };
-constexpr float kFastLimit = 2048.0f;
+// Largest c R^2 the matrix-core exponent takes.  The bound on its error in
+// log2 units grows linearly with c R^2 (derived in k_small_mfma.hip): at
+// D <= 3 eight products per coordinate fit the 32 K slots and the limit is
+// 2048; at D = 4 only six fit, the two dropped ones dominate, and the limit
+// is 128.  Both keep the worst-case bound below the 1e-4 parity bar.
+// The nearest-neighbour forms use the expanded form only to rank candidates
+// (their values are recomputed in the direct form) and take 2048 at every D.
+constexpr float kFastLimit3 = 2048.0f;
+constexpr float kFastLimit4 = 128.0f;
+constexpr float kFastLimitNearest = 2048.0f;
+inline float fast_limit(int D, bool nearest) {
+  return nearest ? kFastLimitNearest : (D <= 3 ? kFastLimit3 : kFastLimit4);
+}
 
 struct FastGuard {
   int lo[4];   // order-preserving int encodings of the box corners
@@ -43,22 +55,27 @@ constexpr int kFastMaxD = 4;   // coordinates the small-D matrix-core path takes
 
 struct FastFrame {
   float m[kFastMaxD];   // centre of the box
+  float U;              // largest prescaled half-width of the box over the coordinates
   bool ok;              // the expanded form meets the accuracy bound
 };
-__device__ __forceinline__ FastFrame fast_frame(const FastGuard* g, int D, float scale) {
+// The decision (ok) is taken with this exact float arithmetic by the fast
+// kernels and by the direct-form kernels alike, so exactly one of them runs.
+__device__ __forceinline__ FastFrame fast_frame(const FastGuard* g, int D, float scale, float limit) {
   FastFrame f;
-  float r2 = 0.0f;
+  float r2 = 0.0f, U = 0.0f;
   for (int d = 0; d < kFastMaxD; ++d) {
     if (d < D) {
       const float lo = fdec(g->lo[d]), hi = fdec(g->hi[d]);
       f.m[d] = 0.5f * (lo + hi);
       const float h = 0.5f * (hi - lo) * scale;
       r2 += h * h;
+      U = fmaxf(U, h);
     } else {
       f.m[d] = 0.0f;
     }
   }
-  f.ok = r2 <= kFastLimit;   // false for NaN
+  f.U = U;
+  f.ok = r2 <= limit;   // false for NaN
   return f;
 }
 
@@ -77,6 +94,7 @@ struct PackArgs {
   float yscale, bscale;
   const FastGuard* guard;   // non-null: skip when the fast path is selected
   float fscale;             // prescale of the fast path (for its guard test)
+  float flimit;             // the fast path's limit on c R^2 (for its guard test)
   int unit_b;               // b == null: the signal column is bscale (a constant 1 * sign)
 };
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
@@ -94,6 +112,7 @@ struct DirectArgs {
   float kscale;           // pair scale: Gauss 2^(-kscale d), Laplace 2^(-kscale sqrt d), LSE g' - kscale d
   float gscale;           // gradient: out = -G * gscale; unused otherwise
   float fscale;           // prescale of the small-D fast path (for its guard test)
+  float flimit;           // the fast path's limit on c R^2 (for its guard test)
   void* out;              // final output (C == 1)
   float* part;            // partials (C > 1), C x M x W
   int KP, K;              // arg-K-min list length (power of two) and K
@@ -268,7 +287,9 @@ struct FastPackArgs {
   int64_t N, N16;
   const float* y;
   const float* b;     // b (sums, gradient) or g (log-sum-exp)
-  float scale;        // prescale sqrt(c)
+  float scale;        // prescale sqrt(c) (the guard's decision uses this float)
+  double scale64;     // the same prescale in fp64 (the operands are formed in fp64)
+  float limit;        // largest c R^2 the fast path takes for this call
   const FastGuard* guard;
   uint4* apk;         // N16 x 4 uint4: 32 bf16 A-operand slots per column
   float4* ex;         // gradient: (b, b v0, b v1, b v2) per column; FAST_SUMV: b's E <= 4 columns
@@ -284,6 +305,8 @@ struct FastArgs {
   int64_t jpb;        // multiple of 256
   const float* x;
   float scale, gscale;
+  double scale64;     // the prescale in fp64 (row operands are formed in fp64)
+  float limit;        // largest c R^2 the fast path takes for this call
   const FastGuard* guard;
   const uint4* apk;
   const float4* ex;
@@ -303,6 +326,10 @@ struct FastArgs {
   const int* bstart;
 };
 hipError_t launch_fast(const FastArgs& a, hipStream_t s);
+// counts[0] += 1 when the guard selects the fast path for (D, scale, limit),
+// counts[1] += 1 always: which kernel did the work, for the profile.
+hipError_t launch_fast_record(const FastGuard* g, int D, float scale, float limit, int* counts,
+                              hipStream_t s);
 int fast_rows_per_block(int epi, int K);
 
 // Fill out with a constant (N = 0 cases); a kernel, not a memset, so that

@@ -8,7 +8,8 @@ import numpy as np
 import pytest
 
 import oracle
-from helpers import LSE_TOL, SUM_TOL, dev, host, lse_err, norm_err, true_dists
+from helpers import (LSE_TOL, SUM_TOL, dev, fast_L, fast_limit, fast_scale, host, lse_err,
+                     norm_err, true_dists)
 
 pytestmark = pytest.mark.gpu
 
@@ -343,7 +344,10 @@ FAST_CASES = [
     ("sinkhorn", "lse", 1000, 4099, 3, 0.01, 0),
     ("sinkhorn", "lse", 4099, 1000, 2, 0.002, 3),
     ("sinkhorn", "lse", 700, 2001, 1, 0.01, 16),
-    # four coordinates: the products fill 24 K slots, the norms (with g') 6 more
+    # four coordinates: six products per coordinate; the matrix-core path takes
+    # c R^2 <= 128 (sigma = 0.1 and eps = 0.02 here), the direct form the rest
+    ("gauss", "sum", 1000, 4099, 4, 0.1, 0),
+    ("sinkhorn", "lse", 1000, 4099, 4, 0.02, 3),
     ("gauss", "sum", 1000, 4099, 4, 0.05, 0),
     ("gauss", "sum", 2000, 3001, 4, 0.1, 16),
     ("sinkhorn", "lse", 1000, 4099, 4, 0.01, 0),
@@ -352,12 +356,25 @@ FAST_CASES = [
 ]
 
 
+_DIRECT = {"gauss": "sum_kernel", "gauss_gradx": "gradx_kernel", "sinkhorn": "lse_kernel"}
+
+
 def _fast_case(ctx, formula, reduction, M, N, D, param, C, flags, scale=1.0):
+    from paper_2004_11127_amd import kred
     rng = np.random.default_rng(M + 17 * N + D)
     x = _pts(rng, M, D, scale); y = _pts(rng, N, D, scale)
     b = rng.standard_normal((N, 1)).astype(np.float32)
     kw = dict(sigma=param) if reduction == "sum" else dict(eps=param)
-    out = host(ctx.run(formula, reduction, dev(x), dev(y), dev(b), col_blocks=C, flags=flags, **kw))
+    ctx.profile_collect()
+    out = host(ctx.run(formula, reduction, dev(x), dev(y), dev(b), col_blocks=C,
+                       flags=flags | kred.FLAG_PROFILE, **kw))
+    # the kernel the device chose: the matrix-core exponent when FLAG_FAST, the
+    # pair has one (the fused gradient up to D = 3) and c R^2 is inside the guard
+    name = ctx.profile_collect()[2]
+    has_fast = D <= 3 or formula != "gauss_gradx"
+    inside = fast_L(x, y, fast_scale(formula, reduction, param)) <= fast_limit(D, False)
+    want_fast = bool(flags & kred.FLAG_FAST) and has_fast and inside
+    assert name == ("fast_kernel" if want_fast else _DIRECT[formula]), name
     if formula == "gauss":
         ref, norm = oracle.kernel_sum("gauss", x, y, b, sigma=param)
         err = norm_err(out, ref, norm)
