@@ -67,7 +67,8 @@ typedef enum kred_status {
   KRED_ERR_UNSUPPORTED = 2,  /* a (formula, reduction) pair the library does not provide */
   KRED_ERR_NOMEM = 3,        /* scratch allocation failed */
   KRED_ERR_HIP = 4,          /* a HIP runtime call or kernel launch failed */
-  KRED_ERR_NO_DEVICE = 5     /* no usable gfx950 device with that ordinal */
+  KRED_ERR_NO_DEVICE = 5,    /* no usable gfx950 device with that ordinal */
+  KRED_ERR_SCRATCH = 6       /* kred_run_noalloc: the call needs more than its fixed scratch */
 } kred_status;
 
 /* flags */
@@ -108,6 +109,8 @@ typedef struct kred_params {
 #define KRED_MAX_E 64
 #define KRED_MAX_K 64
 #define KRED_MAX_COL_BLOCKS 256
+/* Size of the fixed device scratch of kred_run_noalloc (32 MiB per GPU). */
+#define KRED_NOALLOC_SCRATCH_BYTES (32u << 20)
 
 typedef struct kred_ctx kred_ctx;
 
@@ -178,6 +181,31 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
                      int64_t M, int64_t N, int32_t D, int32_t E,
                      const float* x, const float* y, const float* b, void* out,
                      void* stream);
+
+/*
+ * kred_run for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, pairs, kernels and results as kred_run, but it calls no
+ * hipMalloc, hipFree or other allocating routine: its device scratch (packed
+ * copies of y and b, column-split partials, guards) comes from a fixed array
+ * of KRED_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs
+ * on until the process ends (its address is looked up in kred_create).
+ *
+ * Returns KRED_ERR_SCRATCH, before launching anything, when the call needs
+ * more scratch than that (kred_scratch_bytes tells how much a call needs; for
+ * example a 10^4 x 10^4 Gaussian sum needs about 3.4 MB, a 10^6-column D = 3
+ * direct-form sum about 20 MB).  KRED_FLAG_PROFILE is refused
+ * (KRED_ERR_INVALID_ARG): its events allocate.  Otherwise as kred_run.
+ *
+ * Every call on one GPU shares that GPU's array, whatever the context, and
+ * the array keeps the last call's contents (the kernels initialise what they
+ * read): calls that overlap in time on one GPU, on any streams or contexts,
+ * race and give undefined results.  Serialise them (one stream, or events).
+ */
+kred_status kred_run_noalloc(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
+                             int64_t M, int64_t N, int32_t D, int32_t E,
+                             const float* x, const float* y, const float* b, void* out,
+                             void* stream);
 
 /*
  * Block-sparse reduction (the cluster-wise block-sparsity patterns and the

@@ -9,13 +9,44 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
 using namespace kred;
 
+// Device scratch of kred_run_noalloc: a fixed array, one copy on every GPU the
+// library runs on, held until the process ends.  In host code its name is a
+// host-side stand-in, not a device address: kred_create looks the address up
+// once per device (hipGetSymbolAddress, with that device current), and host
+// code passes only that address on to kernels.
+static __device__ __align__(256) unsigned char scratch[KRED_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_fixed_mu;
+void* g_fixed[kMaxDevices] = {};   // per device: the address of `scratch` there
+}  // namespace
+
+namespace {
+// Where a call's device buffers come from.  The ordinary entry points use the
+// context's own allocations, grown with hipMalloc.  kred_run_noalloc gives the
+// call an Arena over the library's static scratch array instead: each kind of
+// buffer gets a region the first time the call asks for it (later requests of
+// the same kind reuse it), carved in order and never freed.
+enum BufKind { BUF_SCRATCH = 0, BUF_AUX = 1, BUF_WIDE = 2, BUF_GUARD = 3, BUF_KINDS = 4 };
+struct Arena {
+  char* base = nullptr;
+  size_t cap = 0, used = 0;
+  void* slot[BUF_KINDS] = {};
+  size_t size[BUF_KINDS] = {};
+};
+}  // namespace
+
 struct kred_ctx {
   int device = 0;
+  Arena* arena = nullptr;        // set only while a kred_run_noalloc call runs
+  void* fixed = nullptr;         // this device's static scratch array (device address)
   int num_cus = 256;
   void* scratch = nullptr;
   size_t scratch_bytes = 0;
@@ -361,8 +392,39 @@ kred_status grow_buffer(void** buf, size_t* have, size_t bytes) {
   return KRED_OK;
 }
 
-kred_status grow_scratch(kred_ctx* ctx, size_t bytes) {
-  return grow_buffer(&ctx->scratch, &ctx->scratch_bytes, bytes);
+// A device buffer of at least `bytes` of the given kind for this call.
+kred_status buffer(kred_ctx* ctx, BufKind k, size_t bytes, void** out) {
+  if (Arena* a = ctx->arena) {
+    if (a->slot[k] != nullptr) {
+      if (bytes > a->size[k]) return KRED_ERR_SCRATCH;
+      *out = a->slot[k];
+      return KRED_OK;
+    }
+    const size_t off = (size_t)align_up((int64_t)a->used);
+    if (off > a->cap || bytes > a->cap - off) return KRED_ERR_SCRATCH;
+    a->slot[k] = a->base + off;
+    a->size[k] = bytes;
+    a->used = off + bytes;
+    *out = a->slot[k];
+    return KRED_OK;
+  }
+  kred_status st = KRED_OK;
+  switch (k) {
+    case BUF_SCRATCH: st = grow_buffer(&ctx->scratch, &ctx->scratch_bytes, bytes); *out = ctx->scratch; break;
+    case BUF_AUX: st = grow_buffer(&ctx->aux, &ctx->aux_bytes, bytes); *out = ctx->aux; break;
+    case BUF_WIDE: st = grow_buffer(&ctx->wide, &ctx->wide_bytes, bytes); *out = ctx->wide; break;
+    case BUF_GUARD:
+      if (ctx->exact_guard == nullptr &&
+          hipMalloc(reinterpret_cast<void**>(&ctx->exact_guard), sizeof(ExactGuard)) != hipSuccess) {
+        (void)hipGetLastError();
+        ctx->exact_guard = nullptr;
+        return KRED_ERR_NOMEM;
+      }
+      *out = ctx->exact_guard;
+      break;
+    default: return KRED_ERR_INVALID_ARG;
+  }
+  return st;
 }
 
 struct DeviceGuard {
@@ -443,16 +505,17 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   // not change; the expanded form's cancellation then scales with the spread
   // of the data, not with its distance from the origin)
   const int64_t cen_bytes = knn ? 0 : align_up((int64_t)D * (int64_t)sizeof(float));
-  const kred_status gs = grow_scratch(
-      ctx, (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes + ybf_bytes +
-                    bstart_bytes + cen_bytes));
+  void* sp = nullptr;
+  const kred_status gs = buffer(ctx, BUF_SCRATCH,
+                                (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes +
+                                         ybf_bytes + bstart_bytes + cen_bytes), &sp);
   if (gs != KRED_OK) return gs;
-  if (exact && ctx->exact_guard == nullptr &&
-      hipMalloc(reinterpret_cast<void**>(&ctx->exact_guard), sizeof(ExactGuard)) != hipSuccess) {
-    ctx->exact_guard = nullptr;
-    return KRED_ERR_NOMEM;
+  void* gp = nullptr;
+  if (exact) {
+    const kred_status ge = buffer(ctx, BUF_GUARD, sizeof(ExactGuard), &gp);
+    if (ge != KRED_OK) return ge;
   }
-  char* base = static_cast<char*>(ctx->scratch);
+  char* base = static_cast<char*>(sp);
   float* yop = reinterpret_cast<float*>(base);
   float* ny = reinterpret_cast<float*>(base + pl.yop_bytes);
   float* bpk = pl.b_bytes ? reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes) : nullptr;
@@ -472,7 +535,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
                    : reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes + pl.b_bytes +
                                               pl.part_bytes + ybf_bytes + bstart_bytes);
   if (cen && launch_centre(y, N, D, cen, s) != hipSuccess) return KRED_ERR_HIP;
-  ExactGuard* eg = exact ? ctx->exact_guard : nullptr;
+  ExactGuard* eg = exact ? static_cast<ExactGuard*>(gp) : nullptr;
   if (exact && launch_exact_check(x, M, y, N, D, eg, s) != hipSuccess) return KRED_ERR_HIP;
   if (rg) {
     if (launch_range_blocks(rg->rr, rg->nr, M, (int)rows_wg, bstart, s) != hipSuccess)
@@ -675,11 +738,11 @@ int64_t gradx_wide_bytes(int64_t M, int64_t N, int32_t D, int32_t E = 1) {
 kred_status run_gradx_wide(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, int32_t D,
                            int32_t E, const float* x, const float* y, const float* b,
                            const float* e, float* out, hipStream_t s, const Ranges* rg) {
-  const kred_status ga =
-      grow_buffer(&ctx->wide, &ctx->wide_bytes, (size_t)gradx_wide_bytes(M, N, D, E));
+  void* wp = nullptr;
+  const kred_status ga = buffer(ctx, BUF_WIDE, (size_t)gradx_wide_bytes(M, N, D, E), &wp);
   if (ga != KRED_OK) return ga;
   const int W = E * (D + 1);
-  char* base = static_cast<char*>(ctx->wide);
+  char* base = static_cast<char*>(wp);
   float* m = reinterpret_cast<float*>(base);
   float* sig = reinterpret_cast<float*>(base + align_up((int64_t)D * (int64_t)sizeof(float)));
   float* T = reinterpret_cast<float*>(reinterpret_cast<char*>(sig) +
@@ -762,11 +825,12 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   // block-sparse: workgroup maps for the direct kernels and for the fast kernel
   const int64_t bstart_bytes =
       rg ? 2 * align_up((int64_t)(rg->nr + 1) * (int64_t)sizeof(int)) : 0;
+  void* sp = nullptr;
   const kred_status gs =
-      grow_scratch(ctx, (size_t)(pl.pack_bytes + pl.part_bytes + fs.guard_bytes + fs.apk_bytes +
-                                 fs.ex_bytes + bstart_bytes));
+      buffer(ctx, BUF_SCRATCH, (size_t)(pl.pack_bytes + pl.part_bytes + fs.guard_bytes +
+                                        fs.apk_bytes + fs.ex_bytes + bstart_bytes), &sp);
   if (gs != KRED_OK) return gs;
-  char* sbase = static_cast<char*>(ctx->scratch);
+  char* sbase = static_cast<char*>(sp);
   float* ypk = reinterpret_cast<float*>(sbase);
   float* part = pl.part_bytes ? reinterpret_cast<float*>(sbase + pl.pack_bytes) : nullptr;
   char* fbase = sbase + pl.pack_bytes + pl.part_bytes;
@@ -986,10 +1050,10 @@ kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, i
   // E (D + 1) columns [b_e, b_e (y - m)], contracted with e
   if (D > kMaxDirectD && E > 1) return run_gradx_wide(ctx, p, M, N, D, E, x, y, b, e, g, s, rg);
   if (E == 1 && (D > kMaxDirectD || fast_epi(KRED_F_GAUSS_GRADX, KRED_R_SUM, M, N, D, 1, p->flags) >= 0)) {
-    const kred_status ga =
-        grow_buffer(&ctx->aux, &ctx->aux_bytes, (size_t)(M * (1 + D) * (int64_t)sizeof(float)));
+    void* ap = nullptr;
+    const kred_status ga = buffer(ctx, BUF_AUX, (size_t)(M * (1 + D) * (int64_t)sizeof(float)), &ap);
     if (ga != KRED_OK) return ga;
-    float* fused = static_cast<float*>(ctx->aux);
+    float* fused = static_cast<float*>(ap);
     if (rg && launch_fill(fused, M * (1 + D), 0.0f, s) != hipSuccess) return KRED_ERR_HIP;
     const kred_status st =
         run_reduction(ctx, KRED_F_GAUSS_GRADX, KRED_R_SUM, p, M, N, D, 1, x, y, b, fused, s, rg);
@@ -1014,9 +1078,11 @@ kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, i
   if (!make_plan((kred_formula)F_VJP, KRED_R_SUM, p, M, N, D, E, ctx->num_cus, &pl))
     return KRED_ERR_UNSUPPORTED;
   const int64_t bstart_bytes = rg ? align_up((int64_t)(rg->nr + 1) * (int64_t)sizeof(int)) : 0;
-  const kred_status gs = grow_scratch(ctx, (size_t)(pl.pack_bytes + pl.part_bytes + bstart_bytes));
+  void* sp = nullptr;
+  const kred_status gs =
+      buffer(ctx, BUF_SCRATCH, (size_t)(pl.pack_bytes + pl.part_bytes + bstart_bytes), &sp);
   if (gs != KRED_OK) return gs;
-  char* sbase = static_cast<char*>(ctx->scratch);
+  char* sbase = static_cast<char*>(sp);
   float* ypk = reinterpret_cast<float*>(sbase);
   float* part = pl.part_bytes ? reinterpret_cast<float*>(sbase + pl.pack_bytes) : nullptr;
   int* bstart = rg ? reinterpret_cast<int*>(sbase + pl.pack_bytes + pl.part_bytes) : nullptr;
@@ -1124,6 +1190,7 @@ const char* kred_strerror(kred_status s) {
     case KRED_ERR_NOMEM: return "out of device memory for scratch";
     case KRED_ERR_HIP: return "HIP runtime error";
     case KRED_ERR_NO_DEVICE: return "no usable gfx950 device";
+    case KRED_ERR_SCRATCH: return "the call needs more than the no-allocation entry point's fixed scratch";
   }
   return "unknown status";
 }
@@ -1176,8 +1243,13 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
   return KRED_OK;
 }
 
-int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* p, int64_t M,
-                           int64_t N, int32_t D, int32_t E) {
+}  // extern "C"
+
+namespace {
+// Device bytes a validated kred_run call asks for, on a device with num_cus
+// compute units (the column split depends on it).
+int64_t scratch_need(kred_formula f, kred_reduction r, const kred_params* p, int64_t M, int64_t N,
+                     int32_t D, int32_t E, int num_cus) {
   const float dummy = 0.0f;
   // E = 0 with the squared distance's min / max reductions means "without b"
   const bool nob = r == KRED_R_ARGKMIN || r == KRED_R_KMIN ||
@@ -1196,8 +1268,8 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
     // the fused value + gradient runs Gaussian sums of up to 64 signal columns
     const bool wide = f == KRED_F_GAUSS_GRADX;
     MPlan mp;
-    if (!make_mplan(wide ? KRED_F_GAUSS : f, r, p, M, N, D, wide ? std::min(64, D + 1) : E, 256,
-                    &mp))
+    if (!make_mplan(wide ? KRED_F_GAUSS : f, r, p, M, N, D, wide ? std::min(64, D + 1) : E,
+                    num_cus, &mp))
       return -1;
     return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes +
            mfma_bf16_bytes(mp, r == KRED_R_ARGKMIN, p->flags, M, N) +
@@ -1206,11 +1278,19 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
   }
   const int epi = fast_epi(f, r, M, N, D, E, p->flags, p->K);
   Plan pl;
-  if (!make_plan(f, r, p, M, N, D, E, 256, &pl, epi >= 0 ? fast_rows_per_block(epi, p->K) : 0,
-                 epi >= 0 ? 256 : 1))
+  if (!make_plan(f, r, p, M, N, D, E, num_cus, &pl,
+                 epi >= 0 ? fast_rows_per_block(epi, p->K) : 0, epi >= 0 ? 256 : 1))
     return -1;
   const FastScratch fs = fast_scratch(epi, N);
   return pl.pack_bytes + pl.part_bytes + fs.guard_bytes + fs.apk_bytes + fs.ex_bytes;
+}
+}  // namespace
+
+extern "C" {
+
+int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* p, int64_t M,
+                           int64_t N, int32_t D, int32_t E) {
+  return scratch_need(f, r, p, M, N, D, E, 256);
 }
 
 kred_status kred_create(kred_ctx** ctx, int device) {
@@ -1224,10 +1304,27 @@ kred_status kred_create(kred_ctx** ctx, int device) {
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, device) != hipSuccess) return KRED_ERR_NO_DEVICE;
   if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) return KRED_ERR_NO_DEVICE;
+  void* fixed = nullptr;
+  {
+    // the no-allocation entry point's scratch: its address on this device,
+    // looked up once per device with that device current
+    std::lock_guard<std::mutex> lock(g_fixed_mu);
+    if (device < kMaxDevices && g_fixed[device] == nullptr) {
+      DeviceGuard dg(device);
+      void* ptr = nullptr;
+      if (!dg.ok || hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) {
+        (void)hipGetLastError();
+        return KRED_ERR_HIP;
+      }
+      g_fixed[device] = ptr;
+    }
+    if (device < kMaxDevices) fixed = g_fixed[device];
+  }
   kred_ctx* c = new (std::nothrow) kred_ctx();
   if (c == nullptr) return KRED_ERR_NOMEM;
   c->device = device;
   c->num_cus = prop.multiProcessorCount;
+  c->fixed = fixed;
   *ctx = c;
   return KRED_OK;
 }
@@ -1259,6 +1356,36 @@ kred_status kred_run(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   DeviceGuard devg(ctx->device);
   if (!devg.ok) return KRED_ERR_HIP;
   return run_reduction(ctx, f, r, p, M, N, D, E, x, y, b, out, static_cast<hipStream_t>(stream));
+}
+
+kred_status kred_run_noalloc(kred_ctx* ctx, kred_formula f, kred_reduction r,
+                             const kred_params* p, int64_t M, int64_t N, int32_t D, int32_t E,
+                             const float* x, const float* y, const float* b, void* out,
+                             void* stream) {
+  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
+  const kred_status v = kred_validate(f, r, p, M, N, D, E, x, y, b, out);
+  if (v != KRED_OK) return v;
+  // profiling creates events, which allocate
+  if (p->flags & KRED_FLAG_PROFILE) return KRED_ERR_INVALID_ARG;
+  if (M == 0) return KRED_OK;
+  if (ctx->fixed == nullptr) return KRED_ERR_NO_DEVICE;   // device ordinal beyond the table
+  // every region the call carves (at most four kinds, each aligned), checked
+  // before anything is launched
+  const int64_t need = N == 0 ? 0 : scratch_need(f, r, p, M, N, D, E, ctx->num_cus);
+  if (need < 0) return KRED_ERR_UNSUPPORTED;
+  if (need + (int64_t)BUF_KINDS * kAlign + align_up(sizeof(ExactGuard)) >
+      (int64_t)KRED_NOALLOC_SCRATCH_BYTES)
+    return KRED_ERR_SCRATCH;
+  DeviceGuard devg(ctx->device);
+  if (!devg.ok) return KRED_ERR_HIP;
+  Arena a;
+  a.base = static_cast<char*>(ctx->fixed);
+  a.cap = KRED_NOALLOC_SCRATCH_BYTES;
+  ctx->arena = &a;
+  const kred_status st =
+      run_reduction(ctx, f, r, p, M, N, D, E, x, y, b, out, static_cast<hipStream_t>(stream));
+  ctx->arena = nullptr;
+  return st;
 }
 
 kred_status kred_validate_ranges(kred_formula f, kred_reduction r, const kred_params* p,

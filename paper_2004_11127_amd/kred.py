@@ -21,7 +21,8 @@ REDUCTIONS = {"sum": 0, "lse": 1, "argkmin": 2, "min": 3, "max": 4, "argmin": 5,
               "kmin": 7}
 INDEX_REDUCTIONS = (2, 5, 6)     # int32 outputs
 STATUS = {0: "KRED_OK", 1: "KRED_ERR_INVALID_ARG", 2: "KRED_ERR_UNSUPPORTED", 3: "KRED_ERR_NOMEM",
-          4: "KRED_ERR_HIP", 5: "KRED_ERR_NO_DEVICE"}
+          4: "KRED_ERR_HIP", 5: "KRED_ERR_NO_DEVICE", 6: "KRED_ERR_SCRATCH"}
+NOALLOC_SCRATCH_BYTES = 32 << 20
 FLAG_PROFILE = 1
 FLAG_DIRECT = 2
 FLAG_FAST = 4
@@ -56,6 +57,7 @@ def load():
         lib.kred_destroy.argtypes = [vp]
         lib.kred_run.argtypes = [vp, ctypes.c_int, ctypes.c_int, pp, i64, i64, i32, i32,
                                  vp, vp, vp, vp, vp]
+        lib.kred_run_noalloc.argtypes = lib.kred_run.argtypes
         lib.kred_validate.argtypes = [ctypes.c_int, ctypes.c_int, pp, i64, i64, i32, i32,
                                       vp, vp, vp, vp]
         lib.kred_scratch_bytes.argtypes = [ctypes.c_int, ctypes.c_int, pp, i64, i64, i32, i32]
@@ -77,7 +79,8 @@ def load():
         lib.kred_strerror.argtypes = [ctypes.c_int]
         lib.kred_strerror.restype = ctypes.c_char_p
         lib.kred_version.restype = i32
-        for f in (lib.kred_create, lib.kred_destroy, lib.kred_run, lib.kred_validate,
+        for f in (lib.kred_create, lib.kred_destroy, lib.kred_run, lib.kred_run_noalloc,
+                  lib.kred_validate,
                   lib.kred_gauss_backward, lib.kred_validate_backward, lib.kred_run_ranges,
                   lib.kred_validate_ranges, lib.kred_gauss_backward_ranges,
                   lib.kred_validate_backward_ranges, lib.kred_profile_collect):
@@ -233,8 +236,15 @@ class Context:
                         col_blocks=col_blocks, flags=flags, stream=stream,
                         _ranges=(row_ranges, col_ptr, col_ranges))
 
+    def run_noalloc(self, formula, reduction, x, y, b=None, out=None, sigma=1.0, eps=1.0, K=0,
+                    col_blocks=0, flags=0, stream=None):
+        """As run, through kred_run_noalloc: the library's fixed per-GPU scratch, no
+        device allocation (pass `out` to allocate nothing here either)."""
+        return self.run(formula, reduction, x, y, b, out=out, sigma=sigma, eps=eps, K=K,
+                        col_blocks=col_blocks, flags=flags, stream=stream, _noalloc=True)
+
     def run(self, formula, reduction, x, y, b=None, out=None, sigma=1.0, eps=1.0, K=0,
-            col_blocks=0, flags=0, stream=None, _ranges=None):
+            col_blocks=0, flags=0, stream=None, _ranges=None, _noalloc=False):
         """Evaluate the reduction; returns `out` (allocated when None).
 
         x: (M, D) float32, y: (N, D) float32, b: (N, E) float32 or None (arg-K-min,
@@ -267,7 +277,7 @@ class Context:
         args = (self._h, f, r, ctypes.byref(p), M, N, D, E, self._dev_ptr(x, "x", torch.float32),
                 self._dev_ptr(y, "y", torch.float32), bptr, self._dev_ptr(out, "out", odt))
         if _ranges is None:
-            st = load().kred_run(*args, s)
+            st = (load().kred_run_noalloc if _noalloc else load().kred_run)(*args, s)
         else:
             rr, cp, cr = _ranges
             nr = rr.shape[0]
