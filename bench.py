@@ -1,24 +1,28 @@
 """kred benchmark on one MI355X.
 
-Default workload: the Gaussian kernel sum of Eq. (1) with its x-gradient,
-fused, at M = N = 1e6, D = 3, E = 1.  A step is one kred_run over the whole
-hot path: the packing prologue of y and b (prescale), the pair loop with its
-fused sum and gradient reduction, and the column-block second pass.  Inputs
-are seeded synthetic points (a mixture of 8 isotropic Gaussians, std 0.05,
-centres in [0,1]^3; b ~ N(0,1); sigma = 0.05) already resident in HBM when
-timing starts.  `--workload` selects the other workloads, among them the
-Gaussian backward (the x, y and b gradients for a cotangent e, three
-reductions per step).
+Default workload: the Gaussian kernel sum of Eq. (1), value only, at
+M = N = 1e6, D = 3, E = 1 (the paper's Sec. 3 benchmark problem), on seeded
+synthetic points (a mixture of 8 isotropic Gaussians, std 0.05, centres in
+[0,1]^3; b ~ N(0,1); sigma = 0.05) already resident in HBM when timing starts.
+A step is one kred_run over the whole hot path: the prologue (bounding box,
+packing of y and b), the pair loop with its reduction, and the column-block
+second pass when there is one.  The same run also times the fused sum +
+x-gradient on the same inputs (`extra.c2`), each with its own roofline and
+CPU baseline.  `--workload` selects another workload as the main line.
 
 Prints one JSON line.  `value` is pair evaluations per second (Gpairs/s) of
-the whole step (each reduction of a step counts its M x N pairs); `roofline`
-prices the main kernels' algorithmic flops against the FP32 vector peak, or
-against the matrix-core peak of the operand type the main kernel multiplies in
-(fp32 or bf16), timed with HIP events the library records around each main
-kernel on the launch stream, and for matrix-core kernels adds the matrix work
-they execute (split operands and padding included) at the published peaks
-against the same time; `cpu_baseline` times the fp64 oracle on the
-host over a bounded sample of rows.
+the whole step (each reduction of a step counts its M x N pairs);
+`ms_per_step` is wall clock over the timed steps, `step_ms` the median and
+minimum of per-step HIP events on the launch stream.  `roofline` prices the
+main kernels' algorithmic flops against the FP32 vector peak, or against the
+matrix-core peak of the operand type the main kernel multiplies in (fp32 or
+bf16), timed with HIP events the library records around each main kernel on
+the launch stream; for matrix-core kernels it adds the matrix work they
+execute (split operands and padding included) at the published peaks against
+the same time, and for vector kernels the measured sustained FMA and exp
+rates of the device (`device`, from a microbenchmark run after the timed
+steps).  `cpu_baseline` times the fp64 oracle, built for the host's CPU, on
+the host's cores over a bounded sample of rows.
 """
 import argparse
 import hashlib
@@ -134,15 +138,23 @@ def matrix_flops_per_pair(kernel, w, reduction, formula=None):
     return {}
 
 
+# workloads the default run times beside the main line (same inputs, more work per pair)
+EXTRA = {"headline": ["c2"]}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOADS))
-    ap.add_argument("--cpu-seconds", type=float, default=25.0,
-                    help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--workload", default="headline", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of each oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="time the main workload only (not the workloads in EXTRA)")
+    ap.add_argument("--no-probe", action="store_true",
+                    help="skip the sustained-rate microbenchmark of the device")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -229,21 +241,28 @@ def time_steps(ctx, w, formula, reduction, steps, warmup, pattern=None):
         call(0)
     torch.cuda.synchronize()
     ctx.profile_collect()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(steps):
+    for e0, e1 in ev:
+        e0.record(stream)
         out = call(kred.FLAG_PROFILE)
-    ev1.record(stream)
+        e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     n, kern_ms, kname = ctx.profile_collect()
     if formula == "backward":
         out = out[0]   # the x-gradient, for the CPU baseline's check
-    return dict(wall_s=wall, event_ms=ev0.elapsed_time(ev1), kernel_ms=kern_ms / steps,
+    each = sorted(e0.elapsed_time(e1) for e0, e1 in ev)
+    return dict(wall_s=wall, event_ms=ev[0][0].elapsed_time(ev[-1][1]), kernel_ms=kern_ms / steps,
+                step_ms=dict(median=each[len(each) // 2] if len(each) % 2 else
+                             0.5 * (each[len(each) // 2 - 1] + each[len(each) // 2]),
+                             min=each[0], max=each[-1]),
                 launches=n, kernel=kname, out=out.cpu().numpy())
+
+
+NATIVE_BUILD = {}
 
 
 def cpu_baseline(w, formula, reduction, out_gpu, seconds, pattern=None):
@@ -254,7 +273,8 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds, pattern=None):
     import oracle
     from paper_2004_11127_amd import inputs
 
-    oracle.build()
+    if "cmd" not in NATIVE_BUILD:
+        NATIVE_BUILD["cmd"] = oracle.use_native()   # gcc -O3 -march=native, built on this host
 
     def clustered(rows, rr, cp, cr, ncols, reduce, width):
         # the sampled rows' clusters, each reduced over its pattern columns;
@@ -336,7 +356,7 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds, pattern=None):
     red = 3 if formula == "backward" else 1
     cols = w.N if pattern is None else pattern["pairs"] / w.M   # columns per row (mean)
     res = dict(value=red * S * cols / t / 1e9, unit="Gpairs/s", cores=oracle.num_threads(),
-               kind="oracle",
+               kind="oracle", build=NATIVE_BUILD.get("cmd"),
                sample="%d seeded rows x %s%s (%.1f s)"
                       % (S, "all %d columns" % w.N if pattern is None else "their pattern columns",
                          " for each of the 3 gradients" if red > 1 else "", t),
@@ -351,34 +371,41 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds, pattern=None):
     return res
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print("bench.py measures one GPU only: the library has no multi-GPU path "
-              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
-        sys.exit(2)
-    import torch
+def probe_device():
+    """Sustained fp32 FMA and v_exp_f32 rates and the shader clock (libkred_probe.so)."""
+    import ctypes
 
-    from paper_2004_11127_amd import inputs, kred
+    class Peak(ctypes.Structure):
+        _fields_ = [("fma_tflops", ctypes.c_double), ("exp_gops", ctypes.c_double),
+                    ("sclk_mhz", ctypes.c_double), ("fma_ms", ctypes.c_double),
+                    ("exp_ms", ctypes.c_double), ("cus", ctypes.c_int)]
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    gen, gkw, formula, reduction, fpp, bound, desc = WORKLOADS[args.workload]
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2004_11127_amd", "libkred_probe.so"))
+    lib.kred_probe_peak.argtypes = [ctypes.c_int, ctypes.POINTER(Peak)]
+    lib.kred_probe_peak.restype = ctypes.c_int
+    pk = Peak()
+    rc = lib.kred_probe_peak(0, ctypes.byref(pk))
+    if rc != 0:
+        return {"error": "kred_probe_peak returned %d" % rc}
+    return {"fma_tflops": pk.fma_tflops, "exp_gops": pk.exp_gops, "sclk_mhz": pk.sclk_mhz,
+            "cus": pk.cus, "probe": "libkred_probe.so kred_probe_peak (peak_probe.hip)"}
+
+
+def measure(ctx, name, args):
+    """Time one workload; the fields of its JSON object (without the device figures)."""
+    from paper_2004_11127_amd import inputs
+
+    gen, gkw, formula, reduction, fpp, bound, desc = WORKLOADS[name]
     w = getattr(inputs, gen)(seed=0, **gkw)
-    if args.workload in LIST_K:
-        w.K = LIST_K[args.workload]
-    pattern = sparse_pattern(w) if args.workload in SPARSE else None
+    if name in LIST_K:
+        w.K = LIST_K[name]
+    pattern = sparse_pattern(w) if name in SPARSE else None
     pairs = (float(pattern["pairs"]) if pattern is not None else float(w.M) * float(w.N)) \
-        * REDUCTIONS_PER_STEP.get(args.workload, 1)
-    with kred.Context(0) as ctx:
-        r = time_steps(ctx, w, formula, reduction, args.steps, args.warmup, pattern)
-    if args.copy_probe:
-        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
+        * REDUCTIONS_PER_STEP.get(name, 1)
+    r = time_steps(ctx, w, formula, reduction, args.steps, args.warmup, pattern)
     ms_per_step = r["wall_s"] * 1e3 / args.steps
     # fpp counts the flops of one (i, j) over all reductions of a step
-    step_pairs = pairs / REDUCTIONS_PER_STEP.get(args.workload, 1)   # pairs of one reduction
+    step_pairs = pairs / REDUCTIONS_PER_STEP.get(name, 1)   # pairs of one reduction
     achieved = fpp * step_pairs / (r["kernel_ms"] / 1e3) / 1e12
     mx = matrix_flops_per_pair(r["kernel"], w, reduction, formula)
     mdtype = ("bf16" if "bf16" in mx else "f32") if bound == "mfma" else None
@@ -387,43 +414,100 @@ def main():
     # the executed matrix work at the published peaks, against the kernel time
     ms_at_peak = pairs * (mx.get("bf16", 0) / (PEAK_BF16_MATRIX_TFLOPS * 1e12) +
                           mx.get("f32", 0) / (PEAK_FP32_MATRIX_TFLOPS * 1e12)) * 1e3
-    line = {
-        "metric": "kernel pair-evaluations/sec (Gpairs/s) at M=N=1e6 D=3; % of FP32 VALU peak",
+    sub = {
         "value": pairs / (ms_per_step / 1e3) / 1e9,
         "unit": "Gpairs/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
+        "step_ms": r["step_ms"],
         "config": {"workload": desc, "M": w.M, "N": w.N, "D": w.D, "E": w.E, "K": w.K,
                    "sigma": w.sigma, "eps": w.eps, "flops_per_pair": fpp},
         "roofline": {"bound": bound, "matrix_dtype": mdtype,
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
-                     "traffic": traffic_for(args.traffic, args.workload, r["kernel"]),
+                     "traffic": traffic_for(args.traffic, name, r["kernel"]),
                      "kernel": r["kernel"], "kernel_ms_per_step": r["kernel_ms"],
                      "launches_timed": r["launches"],
                      "launches_per_step": r["launches"] / args.steps},
         "event_ms_per_step": r["event_ms"] / args.steps,
     }
     if mx:
-        line["roofline"]["matrix_executed"] = {
+        sub["roofline"]["matrix_executed"] = {
             "flops_per_pair": mx, "ms_at_peak_per_step": ms_at_peak,
             "frac": ms_at_peak / r["kernel_ms"]}
-    if args.workload in ("c1", "headline"):
-        line["paper_context"] = ("KeOps++ on an RTX 2080 Ti (Sec. 3 table): 0.4 ms at 1e4 and "
-                                 "1.38 s at 1e6 points, D=3, fp32")
+    if name in ("c1", "headline"):
+        sub["paper_context"] = ("KeOps++ on an RTX 2080 Ti (Sec. 3 table): 0.4 ms at 1e4 and "
+                                "1.38 s at 1e6 points, D=3, fp32")
     if pattern is not None:
-        line["config"]["pattern_pairs_fraction"] = pattern["pairs"] / (float(w.M) * w.N)
-        line["config"]["clusters"] = int(len(pattern["row_ranges"]))
+        sub["config"]["pattern_pairs_fraction"] = pattern["pairs"] / (float(w.M) * w.N)
+        sub["config"]["clusters"] = int(len(pattern["row_ranges"]))
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, formula, reduction, r["out"], args.cpu_seconds,
-                                            pattern)
+        sub["cpu_baseline"] = cpu_baseline(w, formula, reduction, r["out"], args.cpu_seconds,
+                                           pattern)
+    # exp-bearing vector kernels: one v_exp_f32 per pair bounds the pair rate too
+    sub["_exp_per_pair"] = 1 if (bound == "alu" and formula in ("gauss", "gauss_gradx", "sinkhorn",
+                                                                   "backward", "laplace")) else 0
+    sub["_pairs_per_s_kernel"] = step_pairs / (r["kernel_ms"] / 1e3)
+    return sub
+
+
+def with_device(sub, dev):
+    """Add the measured sustained rates to a workload's roofline."""
+    rl = sub["roofline"]
+    if "fma_tflops" in dev and rl["bound"] == "alu":
+        rl["peak_measured"] = dev["fma_tflops"]
+        rl["frac_measured"] = rl["achieved"] / dev["fma_tflops"]
+    if "exp_gops" in dev and sub["_exp_per_pair"]:
+        exp_bound = dev["exp_gops"] * 1e9 / sub["_exp_per_pair"]   # pairs/s if exp alone bound
+        rl["exp_bound_gpairs"] = exp_bound / 1e9
+        rl["frac_exp_bound"] = sub["_pairs_per_s_kernel"] / exp_bound
+    del sub["_exp_per_pair"], sub["_pairs_per_s_kernel"]
+    return sub
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2004_11127_amd import kred
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    extras = [] if args.no_extra else EXTRA.get(args.workload, [])
+    with kred.Context(0) as ctx:
+        main_sub = measure(ctx, args.workload, args)
+        extra = {name: measure(ctx, name, args) for name in extras}
+    if args.copy_probe:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+    dev = {} if args.no_probe else probe_device()
+    main_sub = with_device(main_sub, dev)
+    extra = {k: with_device(v, dev) for k, v in extra.items()}
+    line = {
+        "metric": "kernel pair-evaluations/sec (Gpairs/s) at M=N=1e6 D=3; % of FP32 VALU peak",
+        "value": main_sub["value"],
+        "unit": "Gpairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_sub["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+    }
+    for k, v in main_sub.items():
+        if k not in ("value", "unit", "ms_per_step"):
+            line[k] = v
+    if extra:
+        line["extra"] = extra
+    if dev:
+        line["device"] = dev
     print(json.dumps(line), flush=True)
 
 

@@ -51,12 +51,40 @@ def build(force: bool = False) -> str:
     return _LIB
 
 
+NATIVE_FLAGS = ["-O3", "-march=native"]
+_native_path = None
+
+
+def use_native() -> str:
+    """Load a copy of the oracle compiled for this host's CPU, for the CPU baseline's timing.
+
+    gcc -O3 -march=native, still with -fno-fast-math and -ffp-contract=off, so
+    the arithmetic (and every result) is the portable build's.  It is built in a
+    private temporary directory on the machine that runs it (a -march=native
+    binary must not travel to another CPU) and replaces the portable build for
+    the rest of the process.  Returns the compile command line.
+    """
+    import tempfile
+    global _lib, _native_path
+    with _lock:
+        d = tempfile.mkdtemp(prefix="kred_oracle_native_")
+        path = os.path.join(d, "liboracle_native.so")
+        cmd = ["gcc"] + NATIVE_FLAGS + ["-fopenmp", "-fPIC", "-shared", "-fno-fast-math",
+                                        "-ffp-contract=off", "-o", path, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        _native_path = path
+        _lib = None
+    _load()
+    return " ".join(cmd[:-4] + ["kred_oracle.c", "-lm"])
+
+
 def _load():
     global _lib
     with _lock:
         if _lib is None:
-            build()
-            lib = ctypes.CDLL(_LIB)
+            if _native_path is None:
+                build()
+            lib = ctypes.CDLL(_native_path or _LIB)
             lib.oracle_kernel_sum.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_int64,
                                               ctypes.c_int64, ctypes.c_int, ctypes.c_int,
                                               _dp, _dp, _dp, _i64p, ctypes.c_int64, _dp, _dp]

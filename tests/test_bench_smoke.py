@@ -27,6 +27,32 @@ def test_more_than_one_gpu_is_refused_before_any_gpu_work():
     assert r.stdout == ""
 
 
+def test_default_run_is_the_headline_with_the_fused_gradient_beside_it():
+    old = sys.argv
+    try:
+        sys.argv = ["bench.py"]
+        args = bench.parse()
+    finally:
+        sys.argv = old
+    assert args.workload == "headline" and args.gpus == 1
+    gen, gkw, formula, reduction, fpp, bound, desc = bench.WORKLOADS["headline"]
+    assert (formula, reduction, fpp, gkw["M"], gkw["N"], gkw["D"]) == ("gauss", "sum", 11, 10**6,
+                                                                        10**6, 3)
+    assert bench.EXTRA["headline"] == ["c2"]
+    assert bench.WORKLOADS["c2"][1] == gkw   # the same inputs
+
+
+def test_probe_library_exports_its_header():
+    import ctypes
+    import re
+    hdr = open(os.path.join(ROOT, "include", "kred_probe.h")).read()
+    names = re.findall(r"^\s*int\s+(kred_[a-z_]+)\s*\(", hdr, flags=re.M)
+    assert names == ["kred_probe_peak"]
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2004_11127_amd", "libkred_probe.so"))
+    for n in names:
+        assert hasattr(lib, n), n
+
+
 def test_workload_table_is_consistent():
     for name, (gen, gkw, formula, reduction, fpp, bound, desc) in bench.WORKLOADS.items():
         assert callable(getattr(inputs, gen)), name
@@ -111,3 +137,13 @@ def test_bench_line_fields_on_the_small_workload():
     assert cb["kind"] == "oracle" and cb["unit"] == "Gpairs/s"
     assert cb["value"] > 0 and cb["cores"] >= 1 and isinstance(cb["sample"], str)
     assert cb["max_norm_err_on_sample"] < 1e-4
+    assert "-march=native" in cb["build"]
+    # per-step events: median and minimum, neither above the slowest step
+    st = line["step_ms"]
+    assert 0 < st["min"] <= st["median"] <= st["max"]
+    # the device's measured sustained rates, and the roofline against them
+    dev = line["device"]
+    assert 10 < dev["fma_tflops"] < 400 and 100 < dev["exp_gops"] < 1e5
+    assert 500 < dev["sclk_mhz"] < 4000 and dev["cus"] > 0
+    assert rf["frac_measured"] == pytest.approx(rf["achieved"] / dev["fma_tflops"], rel=1e-9)
+    assert 0 < rf["frac_exp_bound"] < 1.0
