@@ -82,9 +82,12 @@ def _load():
     global _lib
     with _lock:
         if _lib is None:
-            if _native_path is None:
+            # KRED_ORACLE_LIBRARY may name another build of kred_oracle.c (the
+            # sanitizer test's)
+            override = os.environ.get("KRED_ORACLE_LIBRARY")
+            if _native_path is None and not override:
                 build()
-            lib = ctypes.CDLL(_native_path or _LIB)
+            lib = ctypes.CDLL(_native_path or override or _LIB)
             lib.oracle_kernel_sum.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_int64,
                                               ctypes.c_int64, ctypes.c_int, ctypes.c_int,
                                               _dp, _dp, _dp, _i64p, ctypes.c_int64, _dp, _dp]

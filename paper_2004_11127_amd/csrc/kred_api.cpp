@@ -86,6 +86,17 @@ inline bool is_arg(kred_reduction r) { return r == KRED_R_ARGMIN || r == KRED_R_
 
 bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
 
+// The integer a C caller passed for an enum argument.  Read through its bytes:
+// in C++, loading an enum object whose value lies outside the enumerators'
+// range is undefined, and a C caller may pass any int.
+template <class E>
+int code_of(const E* e) {
+  int v;
+  static_assert(sizeof(E) == sizeof(int), "the ABI's enums are int-sized");
+  std::memcpy(&v, e, sizeof v);
+  return v;
+}
+
 bool misaligned(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 3u); }
 
 // Everything a call needs, derived from validated arguments.
@@ -1183,7 +1194,7 @@ kred_status run_vjp(kred_ctx* ctx, const kred_params* p, int64_t M, int64_t N, i
 extern "C" {
 
 const char* kred_strerror(kred_status s) {
-  switch (s) {
+  switch (code_of(&s)) {
     case KRED_OK: return "success";
     case KRED_ERR_INVALID_ARG: return "invalid argument";
     case KRED_ERR_UNSUPPORTED: return "unsupported formula/reduction/size combination";
@@ -1201,8 +1212,8 @@ kred_status kred_validate(kred_formula f, kred_reduction r, const kred_params* p
                           int64_t N, int32_t D, int32_t E, const void* x, const void* y,
                           const void* b, const void* out) {
   if (p == nullptr) return KRED_ERR_INVALID_ARG;
-  if ((int)f < KRED_F_GAUSS || (int)f > KRED_F_SINKHORN) return KRED_ERR_INVALID_ARG;
-  if ((int)r < KRED_R_SUM || (int)r > KRED_R_KMIN) return KRED_ERR_INVALID_ARG;
+  if (code_of(&f) < KRED_F_GAUSS || code_of(&f) > KRED_F_SINKHORN) return KRED_ERR_INVALID_ARG;
+  if (code_of(&r) < KRED_R_SUM || code_of(&r) > KRED_R_KMIN) return KRED_ERR_INVALID_ARG;
   if (M < 0 || N < 0 || M > INT32_MAX || N > INT32_MAX) return KRED_ERR_INVALID_ARG;
   if (D < 1 || D > KRED_MAX_D) return KRED_ERR_INVALID_ARG;
   if (p->col_blocks < 0 || p->col_blocks > KRED_MAX_COL_BLOCKS) return KRED_ERR_INVALID_ARG;

@@ -13,7 +13,8 @@ import os
 import re
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libkred.so")
+# KRED_LIBRARY may name another build of the same library (the sanitizer test's)
+LIB_PATH = os.environ.get("KRED_LIBRARY") or os.path.join(PKG, "libkred.so")
 HEADER = os.path.join(os.path.dirname(PKG), "include", "kred.h")
 
 FORMULAS = {"gauss": 0, "laplace": 1, "sqdist": 2, "gauss_gradx": 3, "sinkhorn": 4}
