@@ -160,12 +160,21 @@ kred_status kred_destroy(kred_ctx* ctx);
  * where b has E columns; p->col_blocks in [0, KRED_MAX_COL_BLOCKS].  D > 16
  * is supported by the sums, GAUSS_GRADX (as one Gaussian sum with the D + 1
  * signal columns [b, b (y - m)] for a centre m of y, then g = (A1 - (x - m)
- * A0) / sigma^2; scratch grows by about (M + 64 N)(D + 1) floats), every LSE
- * (fp32 products; the expanded form's error in s is about 2^-24 (|x - m|^2 +
- * |y - m|^2) / eps, m the centre of y the matrix-core path subtracts from x and
- * y), ARGKMIN, KMIN, and every MIN / MAX / ARGMIN / ARGMAX (fp32 products,
- * signal columns in slices of 16).  Inputs must be
- * finite (NaN or Inf in x, y or b gives an undefined result).
+ * A0) / sigma^2; scratch grows by about (M + 64 N)(D + 1) floats), every LSE,
+ * ARGKMIN, KMIN, and every MIN / MAX / ARGMIN / ARGMAX (signal columns in
+ * slices of 16), on the matrix cores in the expanded form |x'|^2 + |y'|^2 -
+ * 2 <x', y'> of coordinates centred on m (the mean of y's first 256 rows) and
+ * scaled by sqrt(c), c = log2(e) / (2 sigma^2), log2(e) / eps or 1.  Accuracy
+ * guard (computed on the device, no host synchronisation): with L = c (max_i
+ * |x_i - m|^2 + max_j |y_j - m|^2), the Gaussian and Sinkhorn forms use fp32
+ * products (KRED_FLAG_DIRECT or below 2^28 pairs; error in the exponent below
+ * (D + 10) 2^-24 L) or, for the sums, split bf16 products (error below
+ * (D / 2 + 18) 2^-24 L) while that bound stays within 1.2e-4 in log2 units,
+ * and the fp64 contraction beyond it; the Laplacian forms and the squared
+ * distance's sums and extremes always use the fp64 contraction.  ARGKMIN /
+ * KMIN rank in fp32 and re-rank the merged candidates by their direct-form
+ * distance (KMIN values are the distances of the returned points).  Inputs
+ * must be finite (NaN or Inf in x, y or b gives an undefined result).
  * Edge cases: M = 0 returns KRED_OK and touches nothing.  N = 0 writes zeros
  * (SUM), -infinity (LSE, MAX), +infinity (MIN) or -1 (ARGMIN, ARGMAX) and
  * reads no input (b may then be NULL; for SQDIST, a NULL b means one output

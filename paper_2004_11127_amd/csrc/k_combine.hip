@@ -124,6 +124,30 @@ __global__ __launch_bounds__(256) void combine_knn_kernel(CombineArgs a) {
         }
       }
     }
+    if (a.rx != nullptr) {
+      // large-D lists rank by the expanded form, whose error is absolute (about
+      // 2^-24 (|x|^2 + |y|^2) per term): the merged candidates get their
+      // direct-form distance, accurate relative to itself (exact on integer
+      // data), and are ordered again by (distance, index)
+      const float* xr = a.rx + row * a.rD;
+#pragma unroll
+      for (int p = 0; p < KP; ++p) {
+        if (jk[p] == INT_MAX) continue;
+        const float* yr = a.ry + (int64_t)jk[p] * a.rD;
+        float s = 0.0f;
+        for (int d = 0; d < a.rD; ++d) {
+          const float t = xr[d] - yr[d];
+          s = __builtin_fmaf(t, t, s);
+        }
+        dk[p] = s;
+      }
+      // insertion sort by (distance, index); the unfilled entries (+inf, INT_MAX) stay last
+      for (int p = 1; p < KP; ++p)
+        for (int q = p; q > 0 && before(dk[q], jk[q], dk[q - 1], jk[q - 1]); --q) {
+          const float td = dk[q]; dk[q] = dk[q - 1]; dk[q - 1] = td;
+          const int tj = jk[q]; jk[q] = jk[q - 1]; jk[q - 1] = tj;
+        }
+    }
     if (a.kvalues) {
       // the expanded form can round a zero distance to a tiny negative value
       float* o = static_cast<float*>(a.out) + row * a.K;

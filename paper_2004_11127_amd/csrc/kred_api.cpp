@@ -62,12 +62,15 @@ struct kred_ctx {
   // outlives scratch growth), and whether the last profiled call used it
   ExactGuard* exact_guard = nullptr;
   int last_exact_D = 0;
-  // small-D calls with the matrix-core path eligible: per profiled call, the
-  // device records whether its guard chose that path (counts[0]) out of all
-  // such calls (counts[1]); the name is resolved at collect time
+  // calls where a device-side guard picks between two kernels (the small-D
+  // matrix-core path or the direct form; the fp64 or the fp32 large-D
+  // contraction): per profiled call the device counts whether it picked the
+  // first (counts[0]) out of all such calls (counts[1]); the name is resolved
+  // at collect time
   int* fast_counts = nullptr;
   bool last_fast = false;
-  const char* last_direct = "none";   // the direct-form kernel those calls fall back to
+  const char* choice_yes = "none";   // the kernel when the guard picks the first
+  const char* last_direct = "none";   // ... and when it picks the other
 };
 
 namespace {
@@ -267,6 +270,8 @@ struct MPlan {
   int64_t jpb;
   int64_t yop_bytes, ny_bytes, b_bytes, part_bytes;
   float xscale, yop_scale, coord_scale, nrm_sign, pad_norm;
+  double sc64;        // the prescale sqrt(c) in fp64 (the fp64 contraction)
+  float wide_limit;   // the accuracy guard's limit on L (< 0: always the fp64 contraction)
 };
 
 bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M, int64_t N,
@@ -308,6 +313,7 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
       sc = std::sqrt(log2e / (double)p->eps);
     }
     q.xscale = (float)sc;
+    q.sc64 = sc;
     q.coord_scale = (float)sc;
     q.yop_scale = (float)(2.0 * sc);
     q.nrm_sign = -1.0f;
@@ -319,6 +325,7 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
     q.EB = 1;
     const double sc = log2e / (double)p->sigma;
     q.xscale = (float)sc;
+    q.sc64 = sc;
     q.coord_scale = (float)sc;
     q.yop_scale = (float)(2.0 * sc);
     q.nrm_sign = -1.0f;
@@ -333,6 +340,7 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
                                             : 2.0 * (double)p->sigma * (double)p->sigma;
     const double sc = std::sqrt(log2e / eps);
     q.xscale = (float)sc;
+    q.sc64 = sc;
     q.coord_scale = (float)sc;
     q.yop_scale = (float)(2.0 * sc);
     q.nrm_sign = -1.0f;
@@ -353,12 +361,21 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
       q.pad_norm = 0.0f;
     }
     q.xscale = (float)sc;
+    q.sc64 = sc;
     q.coord_scale = (float)sc;
     q.yop_scale = (float)(2.0 * sc);
     q.nrm_sign = -1.0f;
   }
   q.W = 16 * q.EB;
   q.N16 = (N + 15) / 16 * 16;
+  // the accuracy guard (SpreadGuard): the exponential forms keep the fp32
+  // kernels up to the bound's limit; the Laplacian forms (sqrt of the
+  // distance) and the squared distance's sums and extremes always take the
+  // fp64 contraction; arg-K-min ranks in fp32 and is re-ranked exactly
+  // (sums take the split bf16 kernel where it is eligible, with its own bound)
+  const bool split_sum = q.epi <= 2 && exact_eligible(p->flags, M, N);
+  q.wide_limit = !(q.epi == 0 || q.epi == 4 || q.epi == 6 || q.epi == 9) ? -1.0f
+                 : split_sum ? wide_limit_split(D) : wide_limit_f32(D);
   const int rows = mfma_rows_per_block(q.DP, q.KP);
   const int64_t row_blocks = std::max<int64_t>(1, (M + rows - 1) / rows);
   int C = choose_col_blocks(row_blocks, q.N16, num_cus, p->col_blocks);
@@ -366,8 +383,10 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   jpb = (jpb + q.TJ - 1) / q.TJ * q.TJ;
   q.jpb = jpb;
   q.C = (int)((q.N16 + jpb - 1) / jpb);
-  q.yop_bytes = align_up(q.N16 * q.DP * (int64_t)sizeof(float));
-  q.ny_bytes = align_up(q.N16 * (int64_t)sizeof(float));
+  // (the fp64 contraction keeps yop and ny in fp64 in the same buffers)
+  const int64_t esz = r == KRED_R_ARGKMIN ? (int64_t)sizeof(float) : (int64_t)sizeof(double);
+  q.yop_bytes = align_up(q.N16 * q.DP * esz);
+  q.ny_bytes = align_up(q.N16 * esz);
   q.b_bytes = (r == KRED_R_ARGKMIN || r == KRED_R_LSE)
                   ? (q.epi == 5 ? align_up(q.N16 * (int64_t)sizeof(float)) : 0)
                   : align_up(q.N16 * q.W * (int64_t)sizeof(float));
@@ -468,6 +487,24 @@ struct Ranges {
   const int* cr;
 };
 
+// Profiled large-D call with the accuracy guard: count on the device whether
+// it picked the fp64 contraction (the name is resolved at collect time).
+kred_status record_wide(kred_ctx* ctx, const SpreadGuard* g, float c, float limit,
+                        const char* fp32_name, hipStream_t s) {
+  if (ctx->fast_counts == nullptr) {
+    if (hipMalloc(reinterpret_cast<void**>(&ctx->fast_counts), 2 * sizeof(int)) != hipSuccess) {
+      ctx->fast_counts = nullptr;
+      return KRED_ERR_NOMEM;
+    }
+    if (hipMemset(ctx->fast_counts, 0, 2 * sizeof(int)) != hipSuccess) return KRED_ERR_HIP;
+  }
+  if (launch_wide_record(g, c, limit, ctx->fast_counts, s) != hipSuccess) return KRED_ERR_HIP;
+  ctx->last_fast = true;
+  ctx->choice_yes = "mfma_f64_kernel";
+  ctx->last_direct = fp32_name;
+  return KRED_OK;
+}
+
 // Scratch for the bf16 column operand of the large-D kernels: the exact k-NN
 // kernel's copy (DP bf16 per column) or the split kernel's three planes.
 int64_t mfma_bf16_bytes(const MPlan& pl, bool knn, uint32_t flags, int64_t M, int64_t N) {
@@ -516,10 +553,15 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   // not change; the expanded form's cancellation then scales with the spread
   // of the data, not with its distance from the origin)
   const int64_t cen_bytes = knn ? 0 : align_up((int64_t)D * (int64_t)sizeof(float));
+  // the accuracy guard, and the fp64 variant's own block-sparse workgroup map
+  const int64_t sg_bytes = knn ? 0 : align_up(sizeof(SpreadGuard));
+  const int64_t rows64 = knn ? 0 : mfma64_rows_per_block(pl.DP);
+  const int64_t bstart64_bytes = (rg && !knn) ? bstart_bytes : 0;
   void* sp = nullptr;
   const kred_status gs = buffer(ctx, BUF_SCRATCH,
                                 (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes +
-                                         ybf_bytes + bstart_bytes + cen_bytes), &sp);
+                                         ybf_bytes + bstart_bytes + cen_bytes + sg_bytes +
+                                         bstart64_bytes), &sp);
   if (gs != KRED_OK) return gs;
   void* gp = nullptr;
   if (exact) {
@@ -545,11 +587,19 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   float* cen = knn ? nullptr
                    : reinterpret_cast<float*>(base + pl.yop_bytes + pl.ny_bytes + pl.b_bytes +
                                               pl.part_bytes + ybf_bytes + bstart_bytes);
+  SpreadGuard* sg = knn ? nullptr
+                        : reinterpret_cast<SpreadGuard*>(reinterpret_cast<char*>(cen) + cen_bytes);
+  int* bstart64 = bstart64_bytes ? reinterpret_cast<int*>(reinterpret_cast<char*>(sg) + sg_bytes)
+                                 : nullptr;
+  const float wide_c = (float)(pl.sc64 * pl.sc64);
   if (cen && launch_centre(y, N, D, cen, s) != hipSuccess) return KRED_ERR_HIP;
+  if (sg && launch_spread(x, M, y, N, D, cen, sg, s) != hipSuccess) return KRED_ERR_HIP;
   ExactGuard* eg = exact ? static_cast<ExactGuard*>(gp) : nullptr;
   if (exact && launch_exact_check(x, M, y, N, D, eg, s) != hipSuccess) return KRED_ERR_HIP;
   if (rg) {
     if (launch_range_blocks(rg->rr, rg->nr, M, (int)rows_wg, bstart, s) != hipSuccess)
+      return KRED_ERR_HIP;
+    if (bstart64 && launch_range_blocks(rg->rr, rg->nr, M, (int)rows64, bstart64, s) != hipSuccess)
       return KRED_ERR_HIP;
     // (distance, index) pairs: 4 C lists of KP pairs per row, count in floats
     if (knn && launch_fill2(part, (int64_t)4 * pl.C * M * 2 * pl.KP, INFINITY,
@@ -591,6 +641,11 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   pa.exact = eg;
   pa.ybf = exact ? ybf : nullptr;
   pa.ysp = split ? ybf : nullptr;
+  pa.spread = sg;
+  pa.wide_c = wide_c;
+  pa.wide_limit = pl.wide_limit;
+  pa.yop_scale64 = 2.0 * pl.sc64;
+  pa.coord_scale64 = pl.sc64;
   if (!ext && launch_mfma_pack(pa, s) != hipSuccess) return KRED_ERR_HIP;
 
   MfmaArgs ma{};
@@ -621,6 +676,10 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   ma.xc = cen;
   ma.gpk = gpk;
   ma.ext_sign = is_max(r) ? -1.0f : 1.0f;
+  ma.spread = sg;
+  ma.wide_c = wide_c;
+  ma.wide_limit = pl.wide_limit;
+  ma.xscale64 = pl.sc64;
   if (rg) {
     ma.nr = rg->nr;
     ma.rr = rg->rr;
@@ -628,6 +687,9 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     ma.cr = rg->cr;
     ma.bstart = bstart;
   }
+  // the fp64 variant: the same arguments with its own workgroup map
+  MfmaArgs ma64 = ma;
+  if (bstart64) ma64.bstart = bstart64;
   const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
   if (ext) {
     // slices of 16 signal columns: pack the slice's b, run, merge the 4 C
@@ -647,12 +709,15 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
         x1 = next_event(ctx);
         if (!x0 || !x1 || hipEventRecord(x0, s) != hipSuccess) return KRED_ERR_HIP;
       }
-      if (launch_mfma(ma, s) != hipSuccess) return KRED_ERR_HIP;
+      ma64.e0 = e0;
+      // both launch; the guard lets exactly one do the work
+      if (launch_mfma(ma, s) != hipSuccess || launch_mfma64(ma64, s) != hipSuccess)
+        return KRED_ERR_HIP;
       if (prof) {
         if (hipEventRecord(x1, s) != hipSuccess) return KRED_ERR_HIP;
-        ctx->last_kernel = "mfma_kernel";
         ctx->last_exact_D = 0;
-        ctx->last_fast = false;
+        const kred_status pr = record_wide(ctx, sg, wide_c, pl.wide_limit, "mfma_kernel", s);
+        if (pr != KRED_OK) return pr;
       }
       CombineArgs ca{};
       ca.formula = (int)f;
@@ -678,18 +743,24 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     e1 = next_event(ctx);
     if (!e0 || !e1 || hipEventRecord(e0, s) != hipSuccess) return KRED_ERR_HIP;
   }
-  // with the exact kernel a candidate, both launch and exactly one does the work
+  // with the exact kernel a candidate, both launch and exactly one does the
+  // work; likewise the fp32 (or split) kernel and the fp64 variant
   if (split) {
     if (launch_mfma_split(ma, s) != hipSuccess) return KRED_ERR_HIP;
   } else if (launch_mfma(ma, s) != hipSuccess) {
     return KRED_ERR_HIP;
   }
   if (exact && launch_knn_bf16(ma, s) != hipSuccess) return KRED_ERR_HIP;
+  if (!knn && launch_mfma64(ma64, s) != hipSuccess) return KRED_ERR_HIP;
   if (prof) {
     if (hipEventRecord(e1, s) != hipSuccess) return KRED_ERR_HIP;
     ctx->last_kernel = split ? "mfma_split_kernel" : "mfma_kernel";
     ctx->last_fast = false;
     ctx->last_exact_D = exact ? D : 0;   // resolved from the guard at collect time
+    if (!knn) {
+      const kred_status pr = record_wide(ctx, sg, wide_c, pl.wide_limit, ctx->last_kernel, s);
+      if (pr != KRED_OK) return pr;
+    }
   }
   if (knn || pl.C > 1) {
     CombineArgs ca{};
@@ -707,6 +778,12 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     ca.KP = knn ? pl.KP : 0;
     ca.K = pl.K;
     ca.kvalues = kvalues;
+    if (knn) {
+      // the merged candidates get their direct-form distances and are ranked again
+      ca.rx = x;
+      ca.ry = y;
+      ca.rD = D;
+    }
     if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
   }
   return KRED_OK;
@@ -1019,6 +1096,7 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
         if (launch_fast_record(guard, D, pl.fscale, flimit, ctx->fast_counts, s) != hipSuccess)
           return KRED_ERR_HIP;
         ctx->last_fast = true;
+        ctx->choice_yes = "fast_kernel";
         ctx->last_direct = direct;
       }
     }
@@ -1284,7 +1362,8 @@ int64_t scratch_need(kred_formula f, kred_reduction r, const kred_params* p, int
       return -1;
     return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes +
            mfma_bf16_bytes(mp, r == KRED_R_ARGKMIN, p->flags, M, N) +
-           (r == KRED_R_ARGKMIN ? 0 : align_up((int64_t)D * (int64_t)sizeof(float))) +
+           (r == KRED_R_ARGKMIN ? 0 : align_up((int64_t)D * (int64_t)sizeof(float)) +
+                                          align_up(sizeof(SpreadGuard))) +
            (wide ? gradx_wide_bytes(M, N, D) : 0);
   }
   const int epi = fast_epi(f, r, M, N, D, E, p->flags, p->K);
@@ -1582,7 +1661,8 @@ kred_status kred_profile_collect(kred_ctx* ctx, int32_t* count, double* total_ms
     if (hipMemcpy(h, ctx->fast_counts, sizeof(h), hipMemcpyDeviceToHost) != hipSuccess ||
         hipMemset(ctx->fast_counts, 0, sizeof(h)) != hipSuccess)
       return KRED_ERR_HIP;
-    ctx->last_kernel = h[0] == h[1] ? "fast_kernel" : h[0] == 0 ? ctx->last_direct : "fast_kernel+direct";
+    ctx->last_kernel = h[0] == h[1] ? ctx->choice_yes : h[0] == 0 ? ctx->last_direct
+                       : (ctx->choice_yes[0] == 'f' ? "fast_kernel+direct" : "mfma_f64_kernel+fp32");
     ctx->last_fast = false;
   }
   if (kernel) *kernel = ctx->last_kernel;

@@ -166,6 +166,12 @@ struct CombineArgs {
   float ext_sign;
   int arg;
   int kvalues;      // arg-K-min: write the distances instead of the indices
+  // arg-K-min lists of the large-D kernels: the merged candidates get their
+  // direct-form distance sum_d (x_d - y_d)^2 (x: M x rD, y: N x rD) and are
+  // ranked again by it; null for the direct kernels' lists
+  const float* rx;
+  const float* ry;
+  int rD;
 };
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 
@@ -198,6 +204,50 @@ __device__ __forceinline__ bool exact_ok(const ExactGuard* g, int D) {
   return m <= kExactMaxAbs && (float)D * m * m <= kExactMaxSum;
 }
 
+// Accuracy guard of the large-D expanded form.  With m a centre of y and s =
+// sqrt(c) in fp64, the kernels take X = fl32(s (x - m)) and Y = fl32(s (y - m))
+// (formed in fp64, one rounding each), the norms nx = -|X|^2 and ny = -|Y|^2
+// (+ g' for log-sum-exp) summed in fp64 and rounded once, and
+//     T = fl(P + fl(nx + ny)),   P = sum_d 2 Y_d X_d
+// accumulated on the matrix cores from zero.  With u = 2^-24 and L = c (max_i
+// |x_i - m|^2 + max_j |y_j - m|^2), every pair has |x'|^2 + |y'|^2 <= L and
+// sum_d |2 Y_d X_d| <= L, and the error in T = -c |x - y|^2 is at most
+//   4 u L    the rounding of the coordinates (|X - Y|^2 against |x' - y'|^2),
+//   2 u L    the two norms and their sum,
+//   2 u L    the last addition (|T| <= 2 L),
+// plus the contraction's own:
+//   fp32 (v_mfma_f32_16x16x4_f32 adds its products to the accumulator one at
+//   a time, each addition rounded; a product may round too): (D + 1) u L, in
+//   all (D + 9) u L;
+//   split bf16 (v_mfma_f32_16x16x32_bf16 adds each group of 8 products at
+//   once: they are aligned to the largest, the bits below 2^-24 of it are
+//   dropped, and the sum is rounded into the accumulator): per group at most
+//   7 u max|p| + u |acc|.  The chain of the products hh, hm and mh (3 D / 8
+//   groups, |acc| below 1.01 L) adds (3 D / 8 + 7) 1.01 u L, the chain of hl,
+//   lh and mm (below 2^-15 of the products) and the dropped ml, lm and ll
+//   below 1.1 u L, their sum u L: in all below (0.38 D + 17.2) u L.
+// Each kernel runs while its bound, (D + 10) u L and (D / 2 + 18) u L with
+// room for the higher-order terms, stays within the budget; beyond it the
+// contraction runs in fp64 (mfma_kernel<..., F64>).  The exponentials of T
+// keep their relative error ln 2 times it.  The Laplacian forms take
+// sqrt(-T), which turns an absolute error e near d = 0 into sqrt(e), and the
+// squared distance's sums have no lower bound on d against their normaliser:
+// they always run in fp64 (limit < 0).
+struct SpreadGuard {
+  unsigned int maxx;   // bit pattern of max_i |x_i - m|^2 (non-negative floats order as unsigned)
+  unsigned int maxy;   // max_j |y_j - m|^2
+};
+constexpr double kWideBudget = 1.2e-4;   // log2 units: ln 2 times it is below 1e-4
+// the largest L each kernel takes
+inline float wide_limit_f32(int D) { return (float)(kWideBudget * 16777216.0 / (D + 10.0)); }
+inline float wide_limit_split(int D) { return (float)(kWideBudget * 16777216.0 / (0.5 * D + 18.0)); }
+// true: the fp64 contraction does the work (also for a NaN spread)
+__device__ __forceinline__ bool wide64(const SpreadGuard* g, float c, float limit) {
+  if (g == nullptr) return false;
+  const float L = c * (__uint_as_float(g->maxx) + __uint_as_float(g->maxy));
+  return !(L <= limit);
+}
+
 struct MfmaPackArgs {
   const float* y;
   const float* b;
@@ -216,6 +266,11 @@ struct MfmaPackArgs {
   float goff_scale;
   const float* yc;           // sums and log-sum-exp: a centre (D) subtracted from y, else null
   float* gpk;                // Laplacian log-sum-exp: g' = goff goff_scale per column (N16), else null
+  // the fp64 contraction (when the guard selects it): yop and ny in fp64, in
+  // the same buffers (sized for it)
+  const SpreadGuard* spread;   // null: the fp32 kernels only (arg-K-min)
+  float wide_c, wide_limit;
+  double yop_scale64, coord_scale64;
 };
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
 
@@ -266,8 +321,21 @@ struct MfmaArgs {
   const float* xc;   // sums and log-sum-exp: the centre (D) subtracted from x, as from y
   const float* gpk;  // Laplacian log-sum-exp: g' per column (N16; padding -infinity)
   float ext_sign;    // min / max (epi 6..9): +1 for min, -1 for max
+  const SpreadGuard* spread;   // the guard choosing the fp32 or the fp64 contraction (null: fp32)
+  float wide_c, wide_limit;    // c of the prescale, and the limit on L
+  double xscale64;             // the row prescale in fp64 (fp64 contraction)
 };
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
+// The same reductions with the contraction in fp64 (runs only when the guard
+// selects it; launched beside the fp32 or split kernel, which then return).
+hipError_t launch_mfma64(const MfmaArgs& a, hipStream_t s);
+int mfma64_rows_per_block(int DP);   // rows per workgroup of the fp64 variant (its bstart map)
+// Zero the guard, then fold max |x_i - m|^2 and max |y_j - m|^2 into it.
+hipError_t launch_spread(const float* x, int64_t M, const float* y, int64_t N, int D,
+                         const float* m, SpreadGuard* g, hipStream_t s);
+// counts[0] += 1 when the guard selects the fp64 contraction, counts[1] += 1 (profiling)
+hipError_t launch_wide_record(const SpreadGuard* g, float c, float limit, int* counts,
+                              hipStream_t s);
 // Exact-path prologue: reset the guard, then fold every coordinate of x and y into it.
 hipError_t launch_exact_check(const float* x, int64_t M, const float* y, int64_t N, int D,
                               ExactGuard* g, hipStream_t s);

@@ -278,7 +278,8 @@ def test_large_d_sum_parity(ctx, formula, M, N, D, E, sigma, C):
 def test_large_d_sum_split_parity(ctx, formula, M, N, D, E, sigma, C):
     # KRED_FLAG_FAST: the contraction on the bf16 matrix cores with split
     # operands (6 partial products); fp32-level accuracy is expected, so the
-    # error must stay within a few times the fp32 kernel's as well as the bar
+    # error must stay within a few times the fp32 kernel's as well as the bar.
+    # The Laplacian and squared-distance sums take the fp64 contraction instead
     from paper_2004_11127_amd import kred
     rng = np.random.default_rng(M * 3 + N + D * 7 + E)
     x = (rng.standard_normal((M, D)) / np.sqrt(D)).astype(np.float32)
@@ -287,7 +288,8 @@ def test_large_d_sum_split_parity(ctx, formula, M, N, D, E, sigma, C):
     ctx.profile_collect()
     out = host(ctx.run(formula, "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C,
                        flags=kred.FLAG_FAST | kred.FLAG_PROFILE))
-    assert ctx.profile_collect()[2] == "mfma_split_kernel"
+    assert ctx.profile_collect()[2] == ("mfma_f64_kernel" if formula in ("laplace", "sqdist")
+                                        else "mfma_split_kernel")
     f32 = host(ctx.run(formula, "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C,
                        flags=kred.FLAG_DIRECT))
     ref, norm = oracle.kernel_sum(formula, x, y, b, sigma=sigma)

@@ -252,7 +252,8 @@ LARGE_SUMS = [
 @pytest.mark.parametrize("formula,M,N,D,E,sigma,cl", LARGE_SUMS)
 def test_ranges_large_d_sum(ctx, formula, M, N, D, E, sigma, cl, C, path):
     # the matrix-core sums: fp32 products (KRED_FLAG_DIRECT) or split bf16 products
-    # (KRED_FLAG_FAST); tiles start 16-aligned and mask the columns outside each range
+    # (KRED_FLAG_FAST); tiles start 16-aligned and mask the columns outside each range.
+    # The Laplacian and squared-distance sums always take the fp64 contraction
     from paper_2004_11127_amd import kred
     rng = np.random.default_rng(M + N + E + D)
     x = (rng.standard_normal((M, D)) / np.sqrt(D)).astype(np.float32)
@@ -263,7 +264,9 @@ def test_ranges_large_d_sum(ctx, formula, M, N, D, E, sigma, cl, C, path):
     ctx.profile_collect()
     out = call(ctx, formula, "sum", x, y, b, pat, sigma=sigma, col_blocks=C,
                flags=fl | kred.FLAG_PROFILE)
-    assert ctx.profile_collect()[2] == ("mfma_kernel" if path == "fp32" else "mfma_split_kernel")
+    want = ("mfma_f64_kernel" if formula in ("laplace", "sqdist")
+            else "mfma_kernel" if path == "fp32" else "mfma_split_kernel")
+    assert ctx.profile_collect()[2] == want
     ref, norm = oracle.ranges_reduce("sum", x, y, b, *pat, formula=formula, sigma=sigma)
     assert norm_err(out, ref, norm) <= SUM_TOL
     covered = np.zeros(M, bool)
