@@ -64,9 +64,30 @@ __global__ __launch_bounds__(256) void mfma_pack_kernel(MfmaPackArgs a) {
     for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < a.N16; j += stride)
       a.gpk[j] = j < a.N ? a.goff[j] * a.goff_scale : -__builtin_inff();
   }
-  // signal tiles: b[j][e0 + e] stored at (j/16)*16W + ((j%16)/4)*4W + e*4 + j%4, W = 16*EB
-  // (unit_b: ones in place of b)
-  if (a.bpk != nullptr) {
+  if (a.bpk != nullptr && a.bpair && !w64) {
+    // bf16 planes h, m, l of b per 32-column pair: plane p, signal column e
+    // and K index k at pair 96 W + p 32 W + e 32 + k, where k = 8 g + 4 h + r
+    // holds column 16 h + 4 g + r of the pair (the P . B operand's K order)
+    const int W = 16 * a.EB;
+    const int64_t total_b = (a.N + 31) / 32 * 32 * W;
+    unsigned short* bp = reinterpret_cast<unsigned short*>(a.bpk);
+    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total_b; t += stride) {
+      const int k = (int)(t & 31);
+      const int64_t pe = t >> 5;          // pair W + e
+      const int64_t pair = pe / W;
+      const int e = (int)(pe - pair * W);
+      const int64_t j = pair * 32 + 16 * ((k >> 2) & 1) + 4 * (k >> 3) + (k & 3);
+      const float v = (j < a.N && e < a.Ec) ? (a.unit_b ? 1.0f : a.b[j * a.E + a.e0 + e]) : 0.0f;
+      __bf16 h, m, l;
+      split3(v, h, m, l);
+      const int64_t o = pair * 96 * W + (int64_t)e * 32 + k;
+      bp[o] = __builtin_bit_cast(unsigned short, h);
+      bp[o + 32 * W] = __builtin_bit_cast(unsigned short, m);
+      bp[o + 64 * W] = __builtin_bit_cast(unsigned short, l);
+    }
+  } else if (a.bpk != nullptr) {
+    // signal tiles: b[j][e0 + e] stored at (j/16)*16W + ((j%16)/4)*4W + e*4 + j%4, W = 16*EB
+    // (unit_b: ones in place of b)
     const int W = 16 * a.EB;
     const int64_t total_b = a.N16 * W;
     for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total_b; t += stride) {
@@ -397,33 +418,48 @@ hipError_t launch_knn_bf16_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
 }
 
 // ------------------------------------------------ sums, split bf16 products
-// The same reduction as mfma_kernel's sums, with the inner product on the
-// bf16 matrix cores: every coordinate is split exactly into three bf16 parts
-// (v = h + m + l, 24 significant bits), and per 32 coordinates six
-// v_mfma_f32_16x16x32_bf16 accumulate the partial products hh, hm, mh, hl,
-// lh and mm, each exact in fp32.  The dropped ml, lm and ll terms are below
-// 2^-24 |x||y|, so the result carries fp32 accuracy at six bf16 products per
-// coordinate instead of one fp32 product (a sixth of the matrix-core time per
-// flop for the fp32 form, at 16x the rate).  The P . B product and the
-// epilogue are those of the fp32 kernel.  Column operand: three bf16 planes
-// per column (prologue); row operand: the planes of x in registers.
+// The Gaussian sum of mfma_kernel with the inner product on the bf16 matrix
+// cores: every coordinate is split exactly into three bf16 parts (v = h + m +
+// l, 24 significant bits), and per 32 coordinates six v_mfma_f32_16x16x32_bf16
+// accumulate the partial products hh, hm, mh, hl, lh and mm, each exact in
+// fp32.  The dropped ml, lm and ll terms are below 2^-24 |x||y|, so the result
+// carries fp32 accuracy at six bf16 products per coordinate instead of one fp32
+// product (a sixth of the matrix-core time per flop for the fp32 form, at 16x
+// the rate).  Column operand: three bf16 planes per column (prologue); row
+// operand: the planes of x in registers.
+//
+// With 32-column tiles or wider (DP <= 128) the P . B product runs on the bf16
+// matrix cores too, two 16-column blocks at a time: the lane's four p values
+// of each block (P[i = li][j = 4 g + r], the exponent's own D layout) are the 8
+// K values k = 8 g + 4 h + r of one v_mfma_f32_16x16x32_bf16, split into three
+// bf16 parts like the coordinates, and the signal is stored by the prologue as
+// three bf16 planes in the matching K order (bsplit_index), so six products
+// per 32 columns replace eight v_mfma_f32_16x16x4_f32 (48 matrix-core cycles
+// per 16 columns instead of 128).  Wider D keeps the fp32 P . B.
 constexpr int split_tile_cols(int DP) { return DP <= 64 ? 64 : (DP <= 128 ? 32 : 16); }
 
-template <int NCH, int RB, int EPI, int EB, bool SP>
+template <int NCH, int RB, int EB, bool SP>
 __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
   constexpr int DP = 32 * NCH;
   constexpr int TJ = split_tile_cols(DP);
+  constexpr bool PAIR = TJ % 32 == 0;          // P . B on the bf16 matrix cores
   constexpr int PU = DP / 8;                  // uint4 per plane of a column
-  constexpr int RU = 3 * PU + 1;              // uint4 per LDS column row (16 B of padding)
   constexpr int TU = TJ * 3 * PU;             // uint4 of y planes per tile
-  constexpr int YL = (TU + 255) / 256;
+  static_assert(TU % 256 == 0, "whole direct loads per tile");
+  constexpr int YI = TU / 256;                // direct loads per wave and tile
   constexpr int W = 16 * EB;
-  constexpr int BF4 = TJ * W / 4;
+  // signal: fp32 float4s (16-column tiles), or bf16 planes of 32-column pairs,
+  // 3 W rows of 32 values (four uint4) per pair, 5 uint4 per row in LDS
+  constexpr int BF4 = PAIR ? TJ / 32 * 12 * W : TJ * W / 4;
   constexpr int BL = (BF4 + 255) / 256;
 
-  __shared__ uint4 ys[2][TJ * RU];
+  // y planes as in HBM (3 PU uint4 per column), uint4 q of column c at
+  // position q ^ (c & (PU - 1)) within its plane: the 16 columns a wave reads
+  // at once fall on distinct bank groups
+  __shared__ uint4 ys[2][TU];
   __shared__ float4 ns[2][TJ / 4];
-  __shared__ float4 bs[2][TJ * W / 4];
+  __shared__ float4 bs[2][PAIR ? 1 : TJ * W / 4];
+  __shared__ uint4 bq[2][PAIR ? TJ / 32 * 15 * W : 1];
 
   if (wide64(a.spread, a.wide_c, a.wide_limit)) return;   // the fp64 contraction does the work
   const MItem it = mitem<SP>(a, 64 * RB);
@@ -436,8 +472,6 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
   const float pad_ny = a.pad_ny;
   const int64_t i0 = it.row0 + wave * (16 * RB);
 
-  // rows: lane supplies B[k = 8 g .. 8 g + 7][n = li] of chunk ch, i.e. the
-  // planes of x[i = li][32 ch + 8 g + t]
   // planes of x[i = li][32 ch + 8 g + t]; X = fl32(s (x - m)) formed in fp64
   // and nx = -fl32(|X|^2) summed in fp64 (the accuracy guard's arithmetic)
   bf16x8 xh[RB][NCH], xm[RB][NCH], xl[RB][NCH];
@@ -474,111 +508,193 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
 #pragma unroll
     for (int eb = 0; eb < EB; ++eb) oacc[rb][eb] = tot[rb][eb] = f4{0.f, 0.f, 0.f, 0.f};
 
-  uint4 ystage[YL];
   float4 bstage[BL];
   float4 nstage;
-  // the tile at column jt (16-aligned), its columns outside [lo, hi) masked
-  auto fetch = [&](int64_t jt, int64_t lo, int64_t hi) {
+  // the tile at column jt (16-aligned; 32-aligned with PAIR) into buffer
+  // nbuf, its columns outside [lo, hi) masked: the y planes straight into LDS
+  // (global_load_lds_dwordx4: lane l of a wave writes 16 B at the window's
+  // base + 16 l; each lane loads the uint4 that belongs at its position),
+  // norms and signal through registers (put)
+  auto fetch = [&](int nbuf, int64_t jt, int64_t lo, int64_t hi) {
     // y of masked columns is loaded as is (inside the padded array): their
-    // padding norm and zero b already remove them
+    // padding norm (-infinity) makes p exactly 0, which removes them; columns
+    // past the loaded blocks keep stale values, never used
     const int ncol = (int)min((int64_t)TJ, ((hi + 15) & ~(int64_t)15) - jt);
     const uint4* ysrc = reinterpret_cast<const uint4*>(a.ysp + jt * 3 * DP);
 #pragma unroll
-    for (int k = 0; k < YL; ++k) {
-      const int f = tid + k * 256;
-      ystage[k] = (f < TU && f < ncol * 3 * PU) ? ysrc[f] : uint4{0u, 0u, 0u, 0u};
+    for (int k = 0; k < YI; ++k) {
+      const int s0 = 64 * (4 * k + wave);   // the wave's window of the tile
+      const int sl = s0 + lane;
+      const int cc = sl / (3 * PU), qq = sl - cc * 3 * PU;
+      if (cc < ncol)
+        __builtin_amdgcn_global_load_lds(
+            static_cast<const void*>(ysrc + cc * 3 * PU + (qq ^ (cc & (PU - 1)))),
+            (__attribute__((address_space(3))) void*)(&ys[nbuf][s0]), 16, 0, 0);
     }
     if (tid < TJ / 4) {
       if constexpr (SP) nstage = masked_ny(a.ny, pad_ny, jt + 4 * tid, lo, hi);
       else nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
                                      : float4{0.f, 0.f, 0.f, 0.f};
     }
-    const float4* bsrc = reinterpret_cast<const float4*>(a.bpk + jt * W);
+    if constexpr (PAIR) {
+      // whole pairs from the prologue's array (sized for 32-column pairs)
+      const float4* bsrc = reinterpret_cast<const float4*>(a.bpk) + (jt / 32) * (12 * W);
 #pragma unroll
-    for (int k = 0; k < BL; ++k) {
-      const int f = tid + k * 256;
-      if constexpr (SP)
-        bstage[k] = f < BF4 ? masked_b(bsrc + f, bpk_col(jt, 4 * f, W), lo, hi)
-                            : float4{0.f, 0.f, 0.f, 0.f};
-      else
-        bstage[k] = (f < BF4 && f < ncol * W / 4) ? bsrc[f] : float4{0.f, 0.f, 0.f, 0.f};
+      for (int k = 0; k < BL; ++k) {
+        const int f = tid + k * 256;
+        bstage[k] = (f < BF4 && (f / (12 * W)) * 32 < ncol) ? bsrc[f] : float4{0.f, 0.f, 0.f, 0.f};
+      }
+    } else {
+      const float4* bsrc = reinterpret_cast<const float4*>(a.bpk + jt * W);
+#pragma unroll
+      for (int k = 0; k < BL; ++k) {
+        const int f = tid + k * 256;
+        if constexpr (SP)
+          bstage[k] = f < BF4 ? masked_b(bsrc + f, bpk_col(jt, 4 * f, W), lo, hi)
+                              : float4{0.f, 0.f, 0.f, 0.f};
+        else
+          bstage[k] = (f < BF4 && f < ncol * W / 4) ? bsrc[f] : float4{0.f, 0.f, 0.f, 0.f};
+      }
     }
   };
   auto put = [&](int buf) {
-#pragma unroll
-    for (int k = 0; k < YL; ++k) {
-      const int f = tid + k * 256;
-      if (f < TU) ys[buf][(f / (3 * PU)) * RU + f % (3 * PU)] = ystage[k];
-    }
     if (tid < TJ / 4) ns[buf][tid] = nstage;
 #pragma unroll
     for (int k = 0; k < BL; ++k) {
       const int f = tid + k * 256;
-      if (f < BF4) bs[buf][f] = bstage[k];
+      if (f < BF4) {
+        if constexpr (PAIR) {
+          // (pair q, row plane W + e, quarter kc) -> row q 3W + plane W + e of 5 uint4
+          const int q = f / (12 * W), rem = f - q * 12 * W;
+          bq[buf][(q * 3 * W + (rem >> 2)) * 5 + (rem & 3)] = __builtin_bit_cast(uint4, bstage[k]);
+        } else {
+          bs[buf][f] = bstage[k];
+        }
+      }
+    }
+  };
+
+  // T of block blk for every row block: two chains per row block, both from
+  // zero (four independent matrix-core chains per wave): acc the products hh,
+  // hm and mh, acc2 the small ones, mm, hl and lh (below 2^-15 of the
+  // products), so that only 3 of the 6 instructions per chunk round at the
+  // scale of the sum; then T = fl(fl(acc + acc2) + fl(nx + ny))
+  auto exponent = [&](int buf, int blk, f4 (&acc)[RB]) {
+    const float4 nyv = ns[buf][blk * 4 + g];
+    f4 acc2[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[rb] = acc2[rb] = f4{0.f, 0.f, 0.f, 0.f};
+    const int cl = blk * 16 + li;
+    const uint4* col = &ys[buf][cl * 3 * PU];
+    const int sw = cl & (PU - 1);
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      const int q = (4 * ch + g) ^ sw;
+      const bf16x8 yh = __builtin_bit_cast(bf16x8, col[q]);
+      const bf16x8 ym = __builtin_bit_cast(bf16x8, col[PU + q]);
+      const bf16x8 yl = __builtin_bit_cast(bf16x8, col[2 * PU + q]);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        acc2[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xm[rb][ch], acc2[rb], 0, 0, 0);
+        acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xh[rb][ch], acc[rb], 0, 0, 0);
+        acc2[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yl, xh[rb][ch], acc2[rb], 0, 0, 0);
+        acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xm[rb][ch], acc[rb], 0, 0, 0);
+        acc2[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xl[rb][ch], acc2[rb], 0, 0, 0);
+        acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xh[rb][ch], acc[rb], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      acc[rb] += acc2[rb];
+      acc[rb] += f4{nx[rb] + nyv.x, nx[rb] + nyv.y, nx[rb] + nyv.z, nx[rb] + nyv.w};
     }
   };
 
   auto segment = [&](int64_t a0, int64_t a1) {
-  const int64_t base = a0 & ~(int64_t)15;
+  const int64_t base = a0 & ~(int64_t)(PAIR ? 31 : 15);
   const int64_t ntiles = (a1 - base + TJ - 1) / TJ;
-  fetch(base, a0, a1);
+  // the previous segment's last tile was read before its final barrier
+  fetch(0, base, a0, a1);
   put(0);
+  __builtin_amdgcn_s_waitcnt(0);   // this wave's direct loads have landed
   __syncthreads();
   for (int64_t t = 0; t < ntiles; ++t) {
     const int64_t jt = base + t * TJ;
     const int buf = (int)(t & 1);
     const int nblk = (int)((min((int64_t)TJ, a1 - jt) + 15) / 16);
-    if (t + 1 < ntiles) fetch(jt + TJ, a0, a1);
-    for (int blk = 0; blk < nblk; ++blk) {
-      const float4 nyv = ns[buf][blk * 4 + g];
-      // two chains per row block, both from zero (four independent
-      // matrix-core chains per wave): acc the products hh, hm and mh, acc2
-      // the small ones, mm, hl and lh (below 2^-15 of the products), so that
-      // only 3 of the 6 instructions per chunk round at the scale of the sum;
-      // then T = fl(fl(acc + acc2) + fl(nx + ny))
-      f4 acc[RB], acc2[RB];
+    // buffer (t+1)&1 was last read in iteration t-1, which ended with a barrier
+    if (t + 1 < ntiles) fetch(buf ^ 1, jt + TJ, a0, a1);
+    if constexpr (PAIR) {
+      for (int bp = 0; bp < (nblk + 1) / 2; ++bp) {
+        // A planes of the pair: K values 8 g + 4 h + r = p of block 2 bp + h,
+        // column 4 g + r; a block beyond the tile's columns (odd nblk) has p = 0
+        bf16x8 ph[RB], pm[RB], pl[RB];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) acc[rb] = acc2[rb] = f4{0.f, 0.f, 0.f, 0.f};
-      const uint4* col = &ys[buf][(blk * 16 + li) * RU + g];
+        for (int h = 0; h < 2; ++h) {
+          f4 acc[RB];
+          exponent(buf, 2 * bp + h, acc);
+          const bool live = 2 * bp + h < nblk;
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        const bf16x8 yh = __builtin_bit_cast(bf16x8, col[4 * ch]);
-        const bf16x8 ym = __builtin_bit_cast(bf16x8, col[PU + 4 * ch]);
-        const bf16x8 yl = __builtin_bit_cast(bf16x8, col[2 * PU + 4 * ch]);
+          for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          acc2[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xm[rb][ch], acc2[rb], 0, 0, 0);
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ym, xh[rb][ch], acc[rb], 0, 0, 0);
-          acc2[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yl, xh[rb][ch], acc2[rb], 0, 0, 0);
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xm[rb][ch], acc[rb], 0, 0, 0);
-          acc2[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xl[rb][ch], acc2[rb], 0, 0, 0);
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(yh, xh[rb][ch], acc[rb], 0, 0, 0);
-        }
-      }
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        acc[rb] += acc2[rb];
-        acc[rb] += f4{nx[rb] + nyv.x, nx[rb] + nyv.y, nx[rb] + nyv.z, nx[rb] + nyv.w};
-      }
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        f4 p;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          if constexpr (EPI == 0) p[r] = __builtin_amdgcn_exp2f(acc[rb][r]);
-          else if constexpr (EPI == 1) p[r] = __builtin_amdgcn_exp2f(-__builtin_amdgcn_sqrtf(fmaxf(-acc[rb][r], 0.0f)));
-          else p[r] = fmaxf(-acc[rb][r], 0.0f);
+            for (int r = 0; r < 4; ++r) {
+              const float pv = live ? __builtin_amdgcn_exp2f(acc[rb][r]) : 0.0f;
+              __bf16 hh, mm, ll;
+              split3(pv, hh, mm, ll);
+              ph[rb][4 * h + r] = hh;
+              pm[rb][4 * h + r] = mm;
+              pl[rb][4 * h + r] = ll;
+            }
         }
 #pragma unroll
         for (int eb = 0; eb < EB; ++eb) {
-          // lane needs b[j = blk*16 + 4g + r][e = 16 eb + li] for r = 0..3
-          const float* bl = reinterpret_cast<const float*>(&bs[buf][0]) +
-                            blk * 16 * W + g * 4 * W + (16 * eb + li) * 4;
-          const float4 bv = *reinterpret_cast<const float4*>(bl);
-          oacc[rb][eb] = mfma4(p[0], bv.x, oacc[rb][eb]);
-          oacc[rb][eb] = mfma4(p[1], bv.y, oacc[rb][eb]);
-          oacc[rb][eb] = mfma4(p[2], bv.z, oacc[rb][eb]);
-          oacc[rb][eb] = mfma4(p[3], bv.w, oacc[rb][eb]);
+          // B planes: b[j(k)][e = 16 eb + li] for k = 8 g .. 8 g + 7
+          const uint4* brow = &bq[buf][(bp * 3 * W + 16 * eb + li) * 5 + g];
+          const bf16x8 bh = __builtin_bit_cast(bf16x8, brow[0]);
+          const bf16x8 bm = __builtin_bit_cast(bf16x8, brow[5 * W]);
+          const bf16x8 bl = __builtin_bit_cast(bf16x8, brow[10 * W]);
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            // smallest partial products first
+            f4 o = oacc[rb][eb];
+            o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pm[rb], bm, o, 0, 0, 0);
+            o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[rb], bh, o, 0, 0, 0);
+            o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[rb], bl, o, 0, 0, 0);
+            o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pm[rb], bh, o, 0, 0, 0);
+            o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[rb], bm, o, 0, 0, 0);
+            oacc[rb][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[rb], bh, o, 0, 0, 0);
+          }
+        }
+        // issue order: the first block's products alone, then the second's
+        // with the first block's exponentials and splits between them (the
+        // VALU work of one block hidden under the other's matrix-core work;
+        // 3-6% on the D = 128 sums)
+        for (int q = 0; q < 6 * NCH * RB; ++q) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        for (int q = 0; q < 6 * NCH * RB; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+        }
+      }
+    } else {
+      for (int blk = 0; blk < nblk; ++blk) {
+        f4 acc[RB];
+        exponent(buf, blk, acc);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          f4 p;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) p[r] = __builtin_amdgcn_exp2f(acc[rb][r]);
+#pragma unroll
+          for (int eb = 0; eb < EB; ++eb) {
+            // lane needs b[j = blk*16 + 4g + r][e = 16 eb + li] for r = 0..3
+            const float* bl = reinterpret_cast<const float*>(&bs[buf][0]) +
+                              blk * 16 * W + g * 4 * W + (16 * eb + li) * 4;
+            const float4 bv = *reinterpret_cast<const float4*>(bl);
+            oacc[rb][eb] = mfma4(p[0], bv.x, oacc[rb][eb]);
+            oacc[rb][eb] = mfma4(p[1], bv.y, oacc[rb][eb]);
+            oacc[rb][eb] = mfma4(p[2], bv.z, oacc[rb][eb]);
+            oacc[rb][eb] = mfma4(p[3], bv.w, oacc[rb][eb]);
+          }
         }
       }
     }
@@ -589,8 +705,8 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
         tot[rb][eb] += oacc[rb][eb];
         oacc[rb][eb] = f4{0.f, 0.f, 0.f, 0.f};
       }
-    // buffer (t+1)&1 was last read in iteration t-1, which ended with a barrier
-    if (t + 1 < ntiles) put((int)((t + 1) & 1));
+    if (t + 1 < ntiles) put(buf ^ 1);
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's direct loads have landed
     __syncthreads();
   }
   };
@@ -616,26 +732,19 @@ __global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
       }
 }
 
-template <int NCH, int RB, int EPI, bool SP>
-hipError_t launch_split_e(const MfmaArgs& a, dim3 grid, hipStream_t s) {
-  switch (a.EB) {
-    case 1: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 1, SP>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 2, SP>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, EPI, 4, SP>), grid, dim3(256), 0, s, a); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
 template <int NCH, bool SP>
 hipError_t launch_split_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   constexpr int RB = NCH >= 8 ? 1 : 2;   // the row count of the fp32 kernel's grid
-  switch (a.epi) {
-    case 0: return launch_split_e<NCH, RB, 0, SP>(a, grid, s);
-    case 1: return launch_split_e<NCH, RB, 1, SP>(a, grid, s);
-    case 2: return launch_split_e<NCH, RB, 2, SP>(a, grid, s);
+  // the Gaussian sum only: the Laplacian and squared-distance sums always take
+  // the fp64 contraction, launched beside this one
+  if (a.epi != 0) return hipSuccess;
+  switch (a.EB) {
+    case 1: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, 1, SP>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, 2, SP>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, 4, SP>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
 }
 
 template <int Q>

@@ -390,6 +390,9 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   q.b_bytes = (r == KRED_R_ARGKMIN || r == KRED_R_LSE)
                   ? (q.epi == 5 ? align_up(q.N16 * (int64_t)sizeof(float)) : 0)
                   : align_up(q.N16 * q.W * (int64_t)sizeof(float));
+  // the split kernel's bf16 planes of b per 32-column pair (in the same buffer)
+  if (split_sum && q.epi == 0 && q.DP <= 128)
+    q.b_bytes = std::max(q.b_bytes, align_up((N + 31) / 32 * 32 * q.W * 3 * (int64_t)sizeof(uint16_t)));
   if (r == KRED_R_ARGKMIN)
     q.part_bytes = align_up((int64_t)4 * q.C * M * 2 * q.KP * (int64_t)sizeof(float));
   else if (is_extreme(r))
@@ -641,6 +644,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   pa.exact = eg;
   pa.ybf = exact ? ybf : nullptr;
   pa.ysp = split ? ybf : nullptr;
+  pa.bpair = (split && pl.epi == 0 && pl.DP <= 128) ? 1 : 0;
   pa.spread = sg;
   pa.wide_c = wide_c;
   pa.wide_limit = pl.wide_limit;

@@ -271,6 +271,10 @@ struct MfmaPackArgs {
   const SpreadGuard* spread;   // null: the fp32 kernels only (arg-K-min)
   float wide_c, wide_limit;
   double yop_scale64, coord_scale64;
+  // the split kernel's Gaussian sum at DP <= 128 (unless the guard selects
+  // fp64): b as three bf16 planes per 32-column pair in the P . B operand's K
+  // order, written to bpk in place of the fp32 tiles (sized for both)
+  int bpair;
 };
 hipError_t launch_mfma_pack(const MfmaPackArgs& a, hipStream_t s);
 
