@@ -109,7 +109,7 @@ KERNEL_SOURCES = {"sum_kernel": "k_direct.hip", "gradx_kernel": "k_direct.hip",
                   "lse_kernel": "k_direct.hip", "knn_kernel": "k_direct.hip",
                   "vjp_kernel": "k_direct.hip", "mfma_kernel": "k_mfma.hip",
                   "mfma_split_kernel": "k_mfma.hip", "knn_bf16_kernel": "k_mfma.hip",
-                  "fast_kernel": "k_small_mfma.hip"}
+                  "fast_kernel": "k_small_mfma.hip", "small_kernel": "k_small.hip"}
 
 
 def matrix_flops_per_pair(kernel, w, reduction, formula=None):
@@ -127,7 +127,9 @@ def matrix_flops_per_pair(kernel, w, reduction, formula=None):
     if formula == "gauss_gradx" and w.D > 16:
         widths = [min(64, w.D + 1 - c) for c in range(0, w.D + 1, 64)]
     ebs = [1 if e <= 16 else (2 if e <= 32 else 4) for e in widths]
-    if kernel == "mfma_split_kernel":     # 6 split products per coordinate; P . B in fp32
+    if kernel == "mfma_split_kernel":     # 6 split products per coordinate
+        if dp <= 128:                     # P . B: 6 bf16 16x16x32 products per 32 x 16 pairs
+            return {"bf16": 12 * dp * len(ebs) + sum(192 * eb for eb in ebs)}
         return {"bf16": 12 * dp * len(ebs), "f32": sum(32 * eb for eb in ebs)}
     if kernel == "mfma_kernel":
         return {"f32": sum(2 * dp + (32 * eb if sums else 0) for eb in ebs)}
@@ -135,7 +137,35 @@ def matrix_flops_per_pair(kernel, w, reduction, formula=None):
         return {"bf16": 2 * dp}
     if kernel == "fast_kernel":           # one 16x16x32 product per 16x16 pairs (32 K slots)
         return {"bf16": 64}
+    if kernel == "small_kernel":          # one fp32 16x16x4 product per 16x16 pairs
+        return {"f32": 8}
     return {}
+
+
+def call_latency(ctx, w, formula, reduction, reps=200):
+    """Per-call latency: HIP events around each call, the stream drained before
+    the next one (so each call starts on an idle GPU and the span includes its
+    host-side enqueue); median and minimum over `reps` calls, in microseconds."""
+    import torch
+    x, y = torch.from_numpy(w.x).cuda(), torch.from_numpy(w.y).cuda()
+    b = torch.from_numpy(w.b).cuda()
+    out = torch.empty((w.M, w.E), device="cuda")
+    stream = torch.cuda.current_stream()
+    kw = dict(sigma=w.sigma, eps=w.eps, K=w.K)
+    for _ in range(10):
+        ctx.run(formula, reduction, x, y, b, out=out, stream=stream, **kw)
+    torch.cuda.synchronize()
+    each = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        ctx.run(formula, reduction, x, y, b, out=out, stream=stream, **kw)
+        e1.record(stream)
+        e1.synchronize()
+        each.append(e0.elapsed_time(e1) * 1e3)
+    each.sort()
+    return {"us_median": each[reps // 2], "us_min": each[0], "reps": reps,
+            "mode": "HIP events around each call, stream drained between calls"}
 
 
 # workloads the default run times beside the main line (same inputs, more work per pair)
@@ -437,6 +467,8 @@ def measure(ctx, name, args):
     if name in ("c1", "headline"):
         sub["paper_context"] = ("KeOps++ on an RTX 2080 Ti (Sec. 3 table): 0.4 ms at 1e4 and "
                                 "1.38 s at 1e6 points, D=3, fp32")
+    if name == "c1":
+        sub["latency"] = call_latency(ctx, w, formula, reduction)
     if pattern is not None:
         sub["config"]["pattern_pairs_fraction"] = pattern["pairs"] / (float(w.M) * w.N)
         sub["config"]["clusters"] = int(len(pattern["row_ranges"]))

@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "libkred.so")
 PROBE_LIB = os.path.join(PKG, "libkred_probe.so")
 
 SOURCES = ["kred_api.cpp", "k_direct.hip", "k_combine.hip", "k_mfma.hip", "k_mfma64.hip",
-           "k_small_mfma.hip"]
+           "k_small_mfma.hip", "k_small.hip"]
 PROBE_SOURCES = ["peak_probe.hip"]   # sustained-rate microbenchmarks (bench.py), not the library
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

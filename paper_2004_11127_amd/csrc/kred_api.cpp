@@ -26,6 +26,10 @@ namespace {
 constexpr int kMaxDevices = 64;
 std::mutex g_fixed_mu;
 void* g_fixed[kMaxDevices] = {};   // per device: the address of `scratch` there
+// the first bytes of `scratch` hold the one-launch Gaussian sum's row-block
+// counters (zero at load, and every call leaves them zero); the rest is the
+// calls' arena
+constexpr size_t kCounterBytes = (size_t)kSumMaxRowBlocks * sizeof(int);
 }  // namespace
 
 namespace {
@@ -69,6 +73,9 @@ struct kred_ctx {
   // at collect time
   int* fast_counts = nullptr;
   bool last_fast = false;
+  // the one-launch Gaussian sum's row-block counters (zeroed once, and every
+  // call leaves them zero)
+  int* counters = nullptr;
   const char* choice_yes = "none";   // the kernel when the guard picks the first
   const char* last_direct = "none";   // ... and when it picks the other
 };
@@ -858,6 +865,95 @@ kred_status run_gradx_wide(kred_ctx* ctx, const kred_params* p, int64_t M, int64
 
 // One reduction on validated arguments, M > 0, on the current device;
 // block-sparse when rg is given.
+// The one-launch Gaussian sum (k_small.hip): D <= 4, E <= 4, below 2^28 pairs,
+// neither KRED_FLAG_FAST nor KRED_FLAG_DIRECT.  Column blocks: enough for two
+// workgroups per CU, at most kSumCols columns each (col_blocks, when given,
+// raised to that minimum).
+struct SmallPlan {
+  int C = 1, jpb = 0;
+  int64_t nrb = 0, part_bytes = 0;
+};
+bool small_plan(kred_formula f, kred_reduction r, const kred_params* p, int64_t M, int64_t N,
+                int32_t D, int32_t E, int num_cus, SmallPlan* sp) {
+  if (f != KRED_F_GAUSS || r != KRED_R_SUM || D > 4 || E < 1 || E > 4) return false;
+  if (p->flags & (KRED_FLAG_FAST | KRED_FLAG_DIRECT)) return false;
+  if (M <= 0 || N <= 0 || (double)M * (double)N >= kFastMinPairs) return false;
+  const int64_t nrb = (M + kSumRows - 1) / kSumRows;
+  if (nrb > kSumMaxRowBlocks) return false;
+  const int64_t cmin = (N + kSumCols - 1) / kSumCols;
+  int64_t C = p->col_blocks > 0 ? (int64_t)p->col_blocks
+                                : std::max<int64_t>(1, (2 * (int64_t)num_cus + nrb - 1) / nrb);
+  C = std::min<int64_t>(std::max(C, cmin), (N + 15) / 16);
+  const int64_t jpb = std::min<int64_t>(kSumCols, ((N + C - 1) / C + 15) / 16 * 16);
+  C = (N + jpb - 1) / jpb;   // every block has at least one column
+  sp->C = (int)C;
+  sp->jpb = (int)jpb;
+  sp->nrb = nrb;
+  sp->part_bytes = C > 1 ? align_up(C * M * E * (int64_t)sizeof(float)) : 0;
+  return true;
+}
+
+kred_status run_small(kred_ctx* ctx, const kred_params* p, const SmallPlan& sp, int64_t M,
+                      int64_t N, int32_t D, int32_t E, const float* x, const float* y,
+                      const float* b, float* out, hipStream_t s) {
+  float* part = nullptr;
+  int* count = nullptr;
+  if (sp.C > 1) {
+    void* buf = nullptr;
+    const kred_status gs = buffer(ctx, BUF_SCRATCH, (size_t)sp.part_bytes, &buf);
+    if (gs != KRED_OK) return gs;
+    part = static_cast<float*>(buf);
+    if (ctx->arena) {
+      count = static_cast<int*>(ctx->fixed);
+    } else {
+      if (ctx->counters == nullptr) {
+        if (hipMalloc(reinterpret_cast<void**>(&ctx->counters), kCounterBytes) != hipSuccess) {
+          (void)hipGetLastError();
+          ctx->counters = nullptr;
+          return KRED_ERR_NOMEM;
+        }
+        if (launch_fill(reinterpret_cast<float*>(ctx->counters), kSumMaxRowBlocks, 0.0f, s) !=
+            hipSuccess)
+          return KRED_ERR_HIP;
+      }
+      count = ctx->counters;
+    }
+  }
+  SmallArgs a{};
+  a.x = x;
+  a.y = y;
+  a.b = b;
+  a.out = out;
+  a.part = part;
+  a.count = count;
+  a.M = M;
+  a.N = N;
+  a.D = D;
+  a.E = E;
+  a.C = sp.C;
+  a.jpb = sp.jpb;
+  a.c64 = 1.4426950408889634 / (2.0 * (double)p->sigma * (double)p->sigma);
+  a.s64 = std::sqrt(a.c64);
+  // the matrix-core form's bound: 15 u L with the norms in the MFMA (D <= 3,
+  // taken as 16 u L), (D + 10) u L otherwise
+  a.limit = D <= 3 ? (float)(kWideBudget * 16777216.0 / 16.0) : wide_limit_f32(D);
+  const bool prof = (p->flags & KRED_FLAG_PROFILE) != 0;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (prof) {
+    e0 = next_event(ctx);
+    e1 = next_event(ctx);
+    if (!e0 || !e1 || hipEventRecord(e0, s) != hipSuccess) return KRED_ERR_HIP;
+  }
+  if (launch_small(a, s) != hipSuccess) return KRED_ERR_HIP;
+  if (prof) {
+    if (hipEventRecord(e1, s) != hipSuccess) return KRED_ERR_HIP;
+    ctx->last_kernel = "small_kernel";
+    ctx->last_fast = false;
+    ctx->last_exact_D = 0;
+  }
+  return KRED_OK;
+}
+
 kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                           int64_t M, int64_t N, int32_t D, int32_t E, const float* x,
                           const float* y, const float* b, void* out, hipStream_t s,
@@ -887,6 +983,9 @@ kred_status run_reduction(kred_ctx* ctx, kred_formula f, kred_reduction r, const
   // kernel-side formula: log-sum-exps run on the Sinkhorn-form kernels
   const int kf = (r == KRED_R_LSE) ? (f == KRED_F_LAPLACE ? F_LAPLACE_LSE : F_SINKHORN) : (int)f;
 
+  SmallPlan spl;
+  if (!rg && small_plan(f, r, p, M, N, D, E, ctx->num_cus, &spl))
+    return run_small(ctx, p, spl, M, N, D, E, x, y, b, static_cast<float*>(out), s);
   if (D > kMaxDirectD && f == KRED_F_GAUSS_GRADX)
     return run_gradx_wide(ctx, p, M, N, D, 1, x, y, b, nullptr, static_cast<float*>(out), s, rg);
   if (D > kMaxDirectD) return run_mfma(ctx, f, r, p, M, N, D, E, x, y, b, out, s, kvalues, rg);
@@ -1357,6 +1456,8 @@ int64_t scratch_need(kred_formula f, kred_reduction r, const kred_params* p, int
     p = &pk;
   }
   if (is_extreme(r) && (nob || f == KRED_F_SINKHORN)) E = 1;
+  SmallPlan spl;
+  if (small_plan(f, r, p, M, N, D, E, num_cus, &spl)) return spl.part_bytes;
   if (D > kMaxDirectD) {
     // the fused value + gradient runs Gaussian sums of up to 64 signal columns
     const bool wide = f == KRED_F_GAUSS_GRADX;
@@ -1434,6 +1535,7 @@ kred_status kred_destroy(kred_ctx* ctx) {
     if (ctx->wide) (void)hipFree(ctx->wide);
     if (ctx->exact_guard) (void)hipFree(ctx->exact_guard);
     if (ctx->fast_counts) (void)hipFree(ctx->fast_counts);
+    if (ctx->counters) (void)hipFree(ctx->counters);
     for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
   }
   delete ctx;
@@ -1468,13 +1570,13 @@ kred_status kred_run_noalloc(kred_ctx* ctx, kred_formula f, kred_reduction r,
   const int64_t need = N == 0 ? 0 : scratch_need(f, r, p, M, N, D, E, ctx->num_cus);
   if (need < 0) return KRED_ERR_UNSUPPORTED;
   if (need + (int64_t)BUF_KINDS * kAlign + align_up(sizeof(ExactGuard)) >
-      (int64_t)KRED_NOALLOC_SCRATCH_BYTES)
+      (int64_t)(KRED_NOALLOC_SCRATCH_BYTES - kCounterBytes))
     return KRED_ERR_SCRATCH;
   DeviceGuard devg(ctx->device);
   if (!devg.ok) return KRED_ERR_HIP;
   Arena a;
-  a.base = static_cast<char*>(ctx->fixed);
-  a.cap = KRED_NOALLOC_SCRATCH_BYTES;
+  a.base = static_cast<char*>(ctx->fixed) + kCounterBytes;
+  a.cap = KRED_NOALLOC_SCRATCH_BYTES - kCounterBytes;
   ctx->arena = &a;
   const kred_status st =
       run_reduction(ctx, f, r, p, M, N, D, E, x, y, b, out, static_cast<hipStream_t>(stream));

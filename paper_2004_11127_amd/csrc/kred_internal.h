@@ -406,6 +406,28 @@ int fast_rows_per_block(int epi, int K);
 
 // Fill out with a constant (N = 0 cases); a kernel, not a memset, so that
 // callers may capture it in a graph.
+// Latency-bound Gaussian sums (D <= 4, E <= 4, below 2^28 pairs) in one
+// launch: rows in blocks of kSumRows, columns in C blocks of jpb <=
+// kSumCols read straight into LDS, the pair term on the matrix cores within
+// each workgroup's own accuracy bound (else the direct form), and the last
+// workgroup of a row block to arrive adding the C partials.
+constexpr int kSumRows = 128;
+constexpr int kSumCols = 1024;
+constexpr int kSumMaxRowBlocks = 16384;   // counters: 64 KB
+struct SmallArgs {
+  const float* x;
+  const float* y;
+  const float* b;
+  float* out;       // M x E
+  float* part;      // C > 1: C x M x E partial sums
+  int* count;       // C > 1: one counter per row block, zero between calls
+  int64_t M, N;
+  int D, E, C, jpb;
+  double c64, s64;  // c = log2(e) / (2 sigma^2) and sqrt(c)
+  float limit;      // the largest L the matrix-core form takes
+};
+hipError_t launch_small(const SmallArgs& a, hipStream_t s);
+
 hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s);
 hipError_t launch_fill2(float* out, int64_t count, float v0, float v1, hipStream_t s);
 

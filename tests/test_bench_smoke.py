@@ -82,14 +82,21 @@ def test_matrix_work_per_pair_follows_the_mfma_shapes():
     # exact bf16 k-NN at D = 64: two 32-slot products per 16 x 16 block
     assert bench.matrix_flops_per_pair("knn_bf16_kernel", _W(64), "argkmin") == {"bf16": 2 * per32}
     # split sums at D = 128, E = 16: six partial products per coordinate, and
-    # the fp32 P.B product (16x16x4 f32 per 16 columns of b: 2 * 16 flops per pair)
+    # the P.B product as six 16x16x32 bf16 products per 32 columns x 16 rows
+    # (2 * 16 * 16 * 32 * 6 / (32 * 16) = 192 flops per pair)
     mx = bench.matrix_flops_per_pair("mfma_split_kernel", _W(128, 16), "sum")
-    assert mx == {"bf16": 6 * 4 * per32, "f32": 32}
+    assert mx == {"bf16": 6 * 4 * per32 + 192}
+    # at D = 256 (16-column tiles) P.B stays on the fp32 16x16x4 product
+    # (2 * 16 flops per pair per 16 signal columns)
+    mx = bench.matrix_flops_per_pair("mfma_split_kernel", _W(256, 16), "sum")
+    assert mx == {"bf16": 6 * 8 * per32, "f32": 32}
+    # the one-launch sum: one 16x16x4 fp32 product per 16 x 16 pairs
+    assert bench.matrix_flops_per_pair("small_kernel", _W(3), "sum") == {"f32": 8}
     # fp32 log-sum-exp at D = 64: the inner product only, no signal product
     assert bench.matrix_flops_per_pair("mfma_kernel", _W(64), "lse") == {"f32": 2 * 64}
     # the fused gradient at D = 128 runs 129 signal columns in three chunks
     mx = bench.matrix_flops_per_pair("mfma_split_kernel", _W(128, 1), "sum", "gauss_gradx")
-    assert mx == {"bf16": 3 * 6 * 4 * per32, "f32": 32 * (4 + 4 + 1)}
+    assert mx == {"bf16": 3 * 6 * 4 * per32 + 192 * (4 + 4 + 1)}
     assert bench.matrix_flops_per_pair("sum_kernel", _W(3), "sum") == {}
 
 

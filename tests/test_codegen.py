@@ -21,7 +21,7 @@ import pytest
 from paper_2004_11127_amd import build
 
 MIN_SLOTS = 6
-SOURCES = ["k_small_mfma.hip", "k_mfma.hip", "k_mfma64.hip"]
+SOURCES = ["k_small_mfma.hip", "k_mfma.hip", "k_mfma64.hip", "k_small.hip"]
 
 
 def _asm(src, tmp_path):

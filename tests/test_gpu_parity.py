@@ -224,7 +224,7 @@ def test_runs_on_a_side_stream(ctx):
 def test_profile_collect_counts_launches(ctx):
     from paper_2004_11127_amd import kred
     rng = np.random.default_rng(24)
-    # 2^28+ pairs take the matrix-core exponent path; small problems the direct one
+    # 2^28+ pairs take the matrix-core exponent path; small problems the one-launch sum
     x = dev(_pts(rng, 20000, 3)); y = dev(_pts(rng, 16384, 3))
     b = dev(rng.standard_normal((16384, 1)).astype(np.float32))
     ctx.profile_collect()
@@ -239,7 +239,7 @@ def test_profile_collect_counts_launches(ctx):
     xs = dev(_pts(rng, 1000, 3))
     ctx.run("gauss", "sum", xs, y, b, sigma=0.1, flags=kred.FLAG_PROFILE)
     n, ms, name = ctx.profile_collect()
-    assert n == 1 and name == "sum_kernel"
+    assert n == 1 and name == "small_kernel"   # below 2^28 pairs: the one-launch sum
 
 
 # ------------------------------------------------------- large D (matrix cores)

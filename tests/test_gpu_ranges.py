@@ -163,14 +163,18 @@ def test_ranges_clamped_and_empty_patterns(ctx):
 
 
 def test_ranges_full_pattern_matches_dense(ctx):
-    # one cluster over everything reproduces kred_run (same kernels, no split)
+    # one cluster over everything reproduces kred_run (same kernels, no split;
+    # the direct form on both sides, since dense sums this small otherwise take
+    # the one-launch kernel)
+    from paper_2004_11127_amd import kred
     rng = np.random.default_rng(6)
     M, N = 2500, 3500
     x = rng.uniform(0, 1, (M, 3)).astype(np.float32); y = rng.uniform(0, 1, (N, 3)).astype(np.float32)
     b = rng.standard_normal((N, 2)).astype(np.float32)
     pat = (np.array([[0, M]], np.int32), np.array([0, 1], np.int32), np.array([[0, N]], np.int32))
-    out = call(ctx, "gauss", "sum", x, y, b, pat, sigma=0.1, col_blocks=1)
-    dense = host(ctx.run("gauss", "sum", dev(x), dev(y), dev(b), sigma=0.1, col_blocks=1))
+    out = call(ctx, "gauss", "sum", x, y, b, pat, sigma=0.1, col_blocks=1, flags=kred.FLAG_DIRECT)
+    dense = host(ctx.run("gauss", "sum", dev(x), dev(y), dev(b), sigma=0.1, col_blocks=1,
+                         flags=kred.FLAG_DIRECT))
     np.testing.assert_array_equal(out, dense)
 
 
