@@ -220,10 +220,41 @@ def cotangent(w):
     return np.random.default_rng(1).standard_normal((w.M, w.E)).astype(np.float32)
 
 
-def sparse_pattern(w):
-    """Sorted copy of the workload and its block-sparse pattern (host setup, not timed)."""
+def sparse_pattern(ctx, w, name):
+    """Sorted copy of the workload and its block-sparse pattern (setup, not in the steps).
+
+    The forward workload builds the pattern on the GPU (kred_cluster_pattern:
+    grid labels, stable sort, ranges and truncation) and permutes x, y and b
+    there (kred_gather_rows); only the pattern's four counts come back to the
+    host, to size the call, and `prologue_ms` times the build and the gathers
+    (HIP events).  The host copies below serve the CPU baseline only.  The
+    backward workload also needs the column-side view (transpose_pattern) and
+    builds its pattern on the host."""
+    import numpy as np
+    cell, cut = SPARSE_CELL * w.sigma, SPARSE_CUTOFF * w.sigma
+    if name == "sparse":
+        import torch
+        x, y, b = (torch.from_numpy(a).cuda() for a in (w.x, w.y, w.b))
+        t = ctx.cluster_pattern(x, y, cell, cut)          # sizing pass, then the pattern
+        cap = int(t["col_ranges"].shape[0])
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        t = ctx.cluster_pattern(x, y, cell, cut, col_cap=cap)
+        xs, ys, bs = (ctx.gather_rows(v, t[o]) for v, o in ((x, "order_x"), (y, "order_y"),
+                                                           (b, "order_y")))
+        e1.record()
+        torch.cuda.synchronize()
+        counts = t["counts"].cpu().numpy()
+        nr, nnz = int(counts[0]), int(counts[1])
+        dev = dict(x=xs, y=ys, b=bs, row_ranges=t["row_ranges"][:nr], col_ptr=t["col_ptr"][:nr + 1],
+                   col_ranges=t["col_ranges"][:nnz])
+        w.x, w.y, w.b = (v.cpu().numpy() for v in (xs, ys, bs))
+        return dict(device=dev, pairs=int(counts[2]), prologue_ms=e0.elapsed_time(e1),
+                    row_ranges=dev["row_ranges"].cpu().numpy(), col_ptr=dev["col_ptr"].cpu().numpy(),
+                    col_ranges=dev["col_ranges"].cpu().numpy())
     from paper_2004_11127_amd import clusters
-    pat = clusters.truncation_pattern(w.x, w.y, SPARSE_CELL * w.sigma, SPARSE_CUTOFF * w.sigma)
+    pat = clusters.truncation_pattern(w.x, w.y, cell, cut)
     w.x = w.x[pat["order_x"]].copy(); w.y = w.y[pat["order_y"]].copy()
     w.b = w.b[pat["order_y"]].copy()
     pat["transposed"] = clusters.transpose_pattern(pat["row_ranges"], pat["col_ptr"],
@@ -250,8 +281,13 @@ def time_steps(ctx, w, formula, reduction, steps, warmup, pattern=None):
             return ctx.gauss_backward_ranges(x, y, b, e, fwd, tr, sigma=w.sigma, flags=flags,
                                              stream=stream)
     elif pattern is not None:
-        rr, cp, cr = (torch.from_numpy(pattern[k]).cuda() for k in ("row_ranges", "col_ptr",
-                                                                     "col_ranges"))
+        if "device" in pattern:      # built and permuted on the GPU
+            d = pattern["device"]
+            x, y, b = d["x"], d["y"], d["b"]
+            rr, cp, cr = d["row_ranges"], d["col_ptr"], d["col_ranges"]
+        else:
+            rr, cp, cr = (torch.from_numpy(pattern[k]).cuda() for k in ("row_ranges", "col_ptr",
+                                                                         "col_ranges"))
         kw = dict(sigma=w.sigma, eps=w.eps, K=w.K)
 
         def call(flags):
@@ -429,7 +465,7 @@ def measure(ctx, name, args):
     w = getattr(inputs, gen)(seed=0, **gkw)
     if name in LIST_K:
         w.K = LIST_K[name]
-    pattern = sparse_pattern(w) if name in SPARSE else None
+    pattern = sparse_pattern(ctx, w, name) if name in SPARSE else None
     pairs = (float(pattern["pairs"]) if pattern is not None else float(w.M) * float(w.N)) \
         * REDUCTIONS_PER_STEP.get(name, 1)
     r = time_steps(ctx, w, formula, reduction, args.steps, args.warmup, pattern)
@@ -472,6 +508,9 @@ def measure(ctx, name, args):
     if pattern is not None:
         sub["config"]["pattern_pairs_fraction"] = pattern["pairs"] / (float(w.M) * w.N)
         sub["config"]["clusters"] = int(len(pattern["row_ranges"]))
+        if "prologue_ms" in pattern:
+            sub["config"]["pattern"] = "built on the GPU (kred_cluster_pattern)"
+            sub["prologue_ms"] = pattern["prologue_ms"]
     if not args.no_cpu_baseline:
         sub["cpu_baseline"] = cpu_baseline(w, formula, reduction, r["out"], args.cpu_seconds,
                                            pattern)

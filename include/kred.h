@@ -248,6 +248,50 @@ kred_status kred_run_ranges(kred_ctx* ctx, kred_formula f, kred_reduction r, con
                             int32_t nr, const int32_t* row_ranges, const int32_t* col_ptr,
                             const int32_t* col_ranges, void* stream);
 
+/*
+ * Block-sparse truncation pattern on the device (Sec. 3 cluster-wise
+ * block-sparsity with the block-sparse truncation rule of Sec. 4), the arrays
+ * kred_run_ranges takes, built without a pass through host memory:
+ *   - a grid of cubic cells of side `cell` over the joint bounding box of x
+ *     (M x D) and y (N x D): origin o = the coordinate-wise minimum, dims_d =
+ *     floor((max_d - o_d) / cell) + 1; each point's cell k_d = min(floor((p_d -
+ *     o_d) / cell), dims_d - 1), labelled k_0 dims_1 .. dims_{D-1} + .. + k_{D-1};
+ *   - order_x (M) / order_y (N): the stable sort of each cloud by label
+ *     (apply them to x, and to y and b, with kred_gather_rows; the result of
+ *     kred_run_ranges on the sorted points comes back in row order with the
+ *     inverse gather);
+ *   - row_ranges (M x 2): cluster I of x is rows [row_ranges[2I],
+ *     row_ranges[2I+1]) of the sorted x; entries from the cluster count up to
+ *     M are the empty range [M, M), so nr = M is always a valid count;
+ *   - col_ptr (M + 1) and col_ranges (col_cap x 2): for cluster I of x, the
+ *     clusters of y whose cell centres o + (k + 1/2) cell lie within cutoff +
+ *     cell sqrt(D) of its own centre, consecutive clusters merged into one
+ *     range of the sorted y (col_ptr[I] = col_ptr[count] for the empty ones);
+ *   - counts (4 int64): the clusters of x, the column ranges needed, the kept
+ *     (i, j) pairs, and 1 when the column ranges exceed col_cap (the ranges
+ *     past col_cap are then not written: call again with a larger col_cap).
+ * Every step repeats in fp64 the arithmetic of clusters.truncation_pattern in
+ * the Python package, so the arrays are identical to it.  1 <= M, N < 2^31 - 1,
+ * 1 <= D <= 8, cell > 0 and cutoff >= 0 finite; every array is a device array
+ * owned by the caller (col_ranges may be NULL when col_cap = 0).
+ * Asynchronous on `stream`; counts is valid once it completes.  Uses the
+ * context's scratch (about 40 bytes per point).
+ */
+kred_status kred_cluster_pattern(kred_ctx* ctx, int64_t M, int64_t N, int32_t D, const float* x,
+                                 const float* y, double cell, double cutoff, int32_t* order_x,
+                                 int32_t* order_y, int32_t* row_ranges, int32_t* col_ptr,
+                                 int32_t* col_ranges, int64_t col_cap, int64_t* counts,
+                                 void* stream);
+
+/*
+ * Row permutation of an n x width fp32 array on the device: dst[i] =
+ * src[index[i]], or with inverse = 1 dst[index[i]] = src[i] (index a
+ * permutation of 0 .. n-1, int32).  src and dst must not overlap.
+ * Asynchronous on `stream`.
+ */
+kred_status kred_gather_rows(kred_ctx* ctx, int64_t n, int32_t width, const float* src,
+                             const int32_t* index, float* dst, int32_t inverse, void* stream);
+
 /* Host-only argument check of kred_run_ranges (the index arrays are only
  * checked for null and alignment). */
 kred_status kred_validate_ranges(kred_formula f, kred_reduction r, const kred_params* p,

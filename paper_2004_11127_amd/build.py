@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "libkred.so")
 PROBE_LIB = os.path.join(PKG, "libkred_probe.so")
 
 SOURCES = ["kred_api.cpp", "k_direct.hip", "k_combine.hip", "k_mfma.hip", "k_mfma64.hip",
-           "k_small_mfma.hip", "k_small.hip"]
+           "k_small_mfma.hip", "k_small.hip", "k_cluster.hip"]
 PROBE_SOURCES = ["peak_probe.hip"]   # sustained-rate microbenchmarks (bench.py), not the library
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -35,9 +35,20 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
          "-I", INCLUDE, "-I", CSRC]
 
 
+# sources whose arithmetic must round every operation on its own (the device
+# clustering repeats a host construction bit for bit): no fused multiply-adds
+NO_CONTRACT = {"k_cluster.hip"}
+
+
+def flags_for(src: str):
+    if src in NO_CONTRACT:
+        return [f if f != "-ffp-contract=fast" else "-ffp-contract=off" for f in FLAGS]
+    return FLAGS
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC] + flags_for(src) + ["-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -1584,6 +1584,66 @@ kred_status kred_run_noalloc(kred_ctx* ctx, kred_formula f, kred_reduction r,
   return st;
 }
 
+kred_status kred_cluster_pattern(kred_ctx* ctx, int64_t M, int64_t N, int32_t D, const float* x,
+                                 const float* y, double cell, double cutoff, int32_t* order_x,
+                                 int32_t* order_y, int32_t* row_ranges, int32_t* col_ptr,
+                                 int32_t* col_ranges, int64_t col_cap, int64_t* counts,
+                                 void* stream) {
+  if (ctx == nullptr) return KRED_ERR_INVALID_ARG;
+  if (M < 1 || N < 1 || M > INT32_MAX - 1 || N > INT32_MAX - 1 || D < 1 || D > kClusterMaxD ||
+      col_cap < 0)
+    return KRED_ERR_INVALID_ARG;
+  if (!(cell > 0.0) || !std::isfinite(cell) || !(cutoff >= 0.0) || !std::isfinite(cutoff))
+    return KRED_ERR_INVALID_ARG;
+  if (!x || !y || !order_x || !order_y || !row_ranges || !col_ptr || !counts ||
+      (col_cap > 0 && !col_ranges))
+    return KRED_ERR_INVALID_ARG;
+  ClusterCall c{};
+  c.x = x;
+  c.y = y;
+  c.M = M;
+  c.N = N;
+  c.D = D;
+  c.cell = cell;
+  {
+    // the reach r = cutoff + cell sqrt(D) and r^2, rounded step by step (no
+    // fused multiply-add), as the host construction computes them
+#pragma clang fp contract(off)
+    const double t = cell * std::sqrt((double)D);
+    const double reach = cutoff + t;
+    c.reach2 = reach * reach;
+  }
+  c.order_x = order_x;
+  c.order_y = order_y;
+  c.row_ranges = row_ranges;
+  c.col_ptr = col_ptr;
+  c.col_ranges = col_ranges;
+  c.col_cap = col_cap;
+  c.counts = counts;
+  DeviceGuard devg(ctx->device);
+  if (!devg.ok) return KRED_ERR_HIP;
+  const size_t bytes = cluster_scratch_bytes(M, N);
+  void* sp = nullptr;
+  const kred_status gs = buffer(ctx, BUF_SCRATCH, bytes, &sp);
+  if (gs != KRED_OK) return gs;
+  return build_cluster_pattern(c, sp, bytes, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? KRED_OK
+             : KRED_ERR_HIP;
+}
+
+kred_status kred_gather_rows(kred_ctx* ctx, int64_t n, int32_t width, const float* src,
+                             const int32_t* index, float* dst, int32_t inverse, void* stream) {
+  if (ctx == nullptr || n < 0 || width < 1 || (inverse != 0 && inverse != 1)) return KRED_ERR_INVALID_ARG;
+  if (n == 0) return KRED_OK;
+  if (!src || !index || !dst || src == dst) return KRED_ERR_INVALID_ARG;
+  DeviceGuard devg(ctx->device);
+  if (!devg.ok) return KRED_ERR_HIP;
+  return launch_gather_rows(src, index, n, width, inverse, dst, static_cast<hipStream_t>(stream)) ==
+                 hipSuccess
+             ? KRED_OK
+             : KRED_ERR_HIP;
+}
+
 kred_status kred_validate_ranges(kred_formula f, kred_reduction r, const kred_params* p,
                                  int64_t M, int64_t N, int32_t D, int32_t E, const void* x,
                                  const void* y, const void* b, const void* out, int32_t nr,

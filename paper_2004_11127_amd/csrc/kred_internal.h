@@ -428,6 +428,51 @@ struct SmallArgs {
 };
 hipError_t launch_small(const SmallArgs& a, hipStream_t s);
 
+// Block-sparse truncation pattern on the device (k_cluster.hip): grid
+// clusters of x and y, their stable sort by label, cluster ranges, and per
+// cluster of x the runs of clusters of y within reach.
+constexpr int kClusterMaxD = 8;
+struct ClusterGrid {
+  double origin[kClusterMaxD];
+  int64_t dims[kClusterMaxD];
+};
+struct TruncArgs {
+  const uint64_t* ux;        // distinct labels of x (ascending)
+  const uint64_t* uy;        // ... of y
+  const int32_t* rx;         // cluster ranges of x (2 per cluster)
+  const int32_t* ry;         // ... of y
+  const int32_t* nx;         // cluster counts (device)
+  const int32_t* ny;
+  int64_t cap_x;             // clusters of x provided for (M)
+  int D;
+  double cell, reach2;
+  const ClusterGrid* g;
+  int32_t* runs;             // per cluster of x: its column ranges (pass 1)
+  const int32_t* col_ptr;    // exclusive scan of runs (pass 2)
+  int32_t* col_ranges;
+  int64_t cap_c;             // column ranges provided for
+  unsigned long long* pairs; // kept (i, j) pairs
+};
+struct ClusterCall {
+  const float* x;
+  const float* y;
+  int64_t M, N;
+  int D;
+  double cell, reach2;
+  int32_t* order_x;
+  int32_t* order_y;
+  int32_t* row_ranges;   // M x 2 (clusters beyond the count: empty)
+  int32_t* col_ptr;      // M + 1
+  int32_t* col_ranges;   // col_cap x 2
+  int64_t col_cap;
+  int64_t* counts;       // 4: clusters of x, column ranges, pairs, overflow
+};
+size_t cluster_scratch_bytes(int64_t M, int64_t N);
+hipError_t build_cluster_pattern(const ClusterCall& c, void* scratch, size_t bytes, hipStream_t s);
+// dst[i] = src[index[i]] (inverse: dst[index[i]] = src[i]), rows of `width` floats
+hipError_t launch_gather_rows(const float* src, const int32_t* index, int64_t n, int width,
+                              int inverse, float* dst, hipStream_t s);
+
 hipError_t launch_fill(float* out, int64_t count, float value, hipStream_t s);
 hipError_t launch_fill2(float* out, int64_t count, float v0, float v1, hipStream_t s);
 

@@ -77,6 +77,11 @@ def load():
                                                    vp]
         lib.kred_validate_backward_ranges.argtypes = [pp, i64, i64, i32, i32, vp, vp, vp, vp, vp,
                                                       vp, vp, i32, vp, vp, vp, i32, vp, vp, vp]
+        lib.kred_cluster_pattern.argtypes = [vp, i64, i64, i32, vp, vp, ctypes.c_double,
+                                             ctypes.c_double, vp, vp, vp, vp, vp, i64, vp, vp]
+        lib.kred_cluster_pattern.restype = ctypes.c_int
+        lib.kred_gather_rows.argtypes = [vp, i64, i32, vp, vp, vp, i32, vp]
+        lib.kred_gather_rows.restype = ctypes.c_int
         lib.kred_strerror.argtypes = [ctypes.c_int]
         lib.kred_strerror.restype = ctypes.c_char_p
         lib.kred_version.restype = i32
@@ -290,6 +295,63 @@ class Context:
         if st != 0:
             raise KredError(st, "kred_run(%s, %s, M=%d, N=%d, D=%d, E=%d)" % (formula, reduction,
                                                                              M, N, D, E))
+        return out
+
+    def cluster_pattern(self, x, y, cell, cutoff, col_cap=None, stream=None):
+        """Block-sparse truncation pattern built on the GPU (kred_cluster_pattern).
+
+        x (M, D), y (N, D): contiguous float32 on the context's GPU.  Returns a
+        dict of int32 GPU tensors order_x (M,), order_y (N,), row_ranges (M, 2),
+        col_ptr (M + 1,), col_ranges (nnz, 2) and the int64 GPU tensor counts
+        (clusters of x, column ranges, pairs, overflow).  With col_cap None a
+        first call with no room for column ranges sizes them (one read of the
+        counts), then the second fills them; otherwise col_ranges has col_cap
+        rows and nothing is read back (check counts[3] for overflow).
+        """
+        import torch
+        M, D = x.shape
+        N = y.shape[0]
+        if y.dim() != 2 or y.shape[1] != D:
+            raise ValueError("y must be (N, D) with the same D as x")
+        s = (stream if stream is not None else torch.cuda.current_stream(x.device)).cuda_stream
+        dev = x.device
+        i32 = dict(dtype=torch.int32, device=dev)
+        t = dict(order_x=torch.empty(M, **i32), order_y=torch.empty(N, **i32),
+                 row_ranges=torch.empty((M, 2), **i32), col_ptr=torch.empty(M + 1, **i32),
+                 counts=torch.empty(4, dtype=torch.int64, device=dev))
+
+        def call(cap, cr):
+            st = load().kred_cluster_pattern(
+                self._h, M, N, D, self._dev_ptr(x, "x", torch.float32),
+                self._dev_ptr(y, "y", torch.float32), float(cell), float(cutoff),
+                t["order_x"].data_ptr(), t["order_y"].data_ptr(), t["row_ranges"].data_ptr(),
+                t["col_ptr"].data_ptr(), cr.data_ptr() if cap > 0 else None, cap,
+                t["counts"].data_ptr(), s)
+            if st != 0:
+                raise KredError(st, "kred_cluster_pattern(M=%d, N=%d, D=%d)" % (M, N, D))
+
+        if col_cap is None:
+            call(0, None)
+            col_cap = int(t["counts"][1].item())
+        t["col_ranges"] = torch.empty((max(col_cap, 1), 2), **i32)
+        call(col_cap, t["col_ranges"])
+        t["col_ranges"] = t["col_ranges"][:col_cap]
+        return t
+
+    def gather_rows(self, src, index, inverse=False, out=None, stream=None):
+        """Row permutation on the GPU (kred_gather_rows): out[i] = src[index[i]],
+        or out[index[i]] = src[i] with inverse.  src (n, w) float32, index (n,) int32."""
+        import torch
+        n = src.shape[0]
+        w = 1 if src.dim() == 1 else src.shape[1]
+        if out is None:
+            out = torch.empty_like(src)
+        s = (stream if stream is not None else torch.cuda.current_stream(src.device)).cuda_stream
+        st = load().kred_gather_rows(self._h, n, w, self._dev_ptr(src, "src", torch.float32),
+                                     self._dev_ptr(index, "index", torch.int32),
+                                     self._dev_ptr(out, "out", torch.float32), 1 if inverse else 0, s)
+        if st != 0:
+            raise KredError(st, "kred_gather_rows(n=%d, width=%d)" % (n, w))
         return out
 
     def gauss_backward_ranges(self, x, y, b, e, pattern, transposed, sigma=1.0, gx=True,
