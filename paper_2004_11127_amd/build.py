@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "libkred.so")
 PROBE_LIB = os.path.join(PKG, "libkred_probe.so")
 
 SOURCES = ["kred_api.cpp", "k_direct.hip", "k_combine.hip", "k_mfma.hip", "k_mfma64.hip",
-           "k_small_mfma.hip", "k_small.hip", "k_cluster.hip"]
+           "k_knn.hip", "k_small_mfma.hip", "k_small.hip", "k_cluster.hip"]
 PROBE_SOURCES = ["peak_probe.hip"]   # sustained-rate microbenchmarks (bench.py), not the library
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -38,11 +38,16 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
 # sources whose arithmetic must round every operation on its own (the device
 # clustering repeats a host construction bit for bit): no fused multiply-adds
 NO_CONTRACT = {"k_cluster.hip"}
+# sources whose values are never NaN: IEEE mode off, so that fp64 minimum and
+# maximum need no quieting of their operands
+NO_IEEE = {"k_knn.hip"}
 
 
 def flags_for(src: str):
     if src in NO_CONTRACT:
         return [f if f != "-ffp-contract=fast" else "-ffp-contract=off" for f in FLAGS]
+    if src in NO_IEEE:
+        return FLAGS + ["-fno-honor-nans", "-mno-amdgpu-ieee", "-Wno-nan-infinity-disabled"]
     return FLAGS
 
 

@@ -1,6 +1,7 @@
-// Large-D (16 < D <= 256) prologue, the split-bf16 sum kernel, the exact bf16
-// arg-K-min kernel, the centre and the large-D gradient kernels, and the
-// launchers of the fp32 matrix-core kernel (its template is in k_mfma_kernel.h).
+// Large-D (16 < D <= 256) prologue, the exactness guard of the bf16 arg-K-min
+// kernel (the kernel is in k_knn.hip), the split-bf16 sum kernel, the centre
+// and the large-D gradient kernels, and the launchers of the fp32 matrix-core
+// kernel (its template is in k_mfma_kernel.h).
 #include "k_mfma_kernel.h"
 
 #include <climits>
@@ -196,226 +197,6 @@ __global__ __launch_bounds__(256) void exact_check_kernel(const float* __restric
 }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-
-constexpr int bf16_tile_cols(int DP) { return DP <= 64 ? 128 : (DP <= 128 ? 64 : 32); }
-
-// Arg-K-min on the bf16 matrix cores, for data the guard has shown to be
-// exact there: T[j][i] = ny_j + sum_d (-2 y_jd) x_id with one
-// v_mfma_f32_16x16x32_bf16 per 32 coordinates of a 16 x 16 block.  The
-// ranking, ties, lists and partial layout are those of the fp32 kernel.
-// bf16 16x16x32 operand layout (lane l = 16 g + li): A (16 x 32): lane l
-// supplies A[li][8 g .. 8 g + 7]; B (32 x 16): lane l supplies
-// B[8 g .. 8 g + 7][li]; D as for the fp32 product, lane l holds
-// D[4 g + r][li].  With A = Y rows and B = X rows, lane l ranks column
-// j = 4 g + r for row i = li.  Coordinates d = 32 ch + 8 g + t.
-// Waves per SIMD the exact kernel is compiled for.  Dense, at 64 coordinates
-// and 4 <= K <= 10, its natural allocation (about 160 VGPRs) gives 3 waves;
-// held to 128 it spills 24-120 bytes per lane and the fourth wave is worth
-// more (10 nearest of 1e6 points for 1e5 queries: 21.0 -> 18.3 ms, 4 nearest
-// 17.4 -> 15.6 ms).  Elsewhere the compiler chooses.
-constexpr int knn_bf16_waves(int NCH, int KP, bool SP) {
-  return (!SP && NCH == 2 && KP >= 4 && KP <= 10) ? 4 : 1;
-}
-
-template <int NCH, int RB, int KP, bool SP>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(knn_bf16_waves(NCH, KP, SP))))
-void knn_bf16_kernel(MfmaArgs a) {
-  if (!exact_ok(a.exact, a.D)) return;   // the fp32 kernel does the work
-  constexpr int DP = 32 * NCH;
-  constexpr int TJ = bf16_tile_cols(DP);
-  constexpr int RU = DP / 8 + 1;           // uint4 per LDS row: DP bf16 and 8 of padding
-  constexpr int TU = TJ * (DP / 8);        // uint4 of y per tile
-  constexpr int YL = (TU + 255) / 256;     // per thread
-
-  __shared__ uint4 ys[2][TJ * RU];
-  __shared__ float4 ns[2][TJ / 4];
-
-  const MItem it = mitem<SP>(a, 64 * RB);
-  if (!it.live) return;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int li = lane & 15, g = lane >> 4;
-  const int c = it.c;
-  const int64_t rend = it.row_end;
-  const float pad_ny = a.pad_ny;
-  const int64_t i0 = it.row0 + wave * (16 * RB);
-
-  bf16x8 xb[RB][NCH];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int64_t row = i0 + 16 * rb + li;
-    const bool ok = row < rend;
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch)
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const int d = 32 * ch + 8 * g + t;
-        xb[rb][ch][t] = (__bf16)((ok && d < a.D) ? a.x[row * a.D + d] : 0.0f);
-      }
-  }
-
-  // per row block the lane's sorted keys (see key_insert) and the distance
-  // part of its last one
-  double kk[RB][KP];
-  float dlast[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    dlast[rb] = __builtin_inff();
-#pragma unroll
-    for (int p = 0; p < KP; ++p) kk[rb][p] = __builtin_inf();
-  }
-
-  // Filter shared by the 4 lanes of a row (each lists its own quarter of the
-  // columns): any value with at least KP of the row's candidates at or below
-  // it bounds the row's K-th nearest in this column block, so a column above
-  // it cannot be among them; ties pass (<=) for the lowest-index rule.  Two
-  // such bounds: the smallest of the 4 lanes' KP-th values, and the largest
-  // of their ceil(KP/4)-th values (4 ceil(KP/4) >= KP candidates).  It is
-  // refreshed once per tile; a stale value is only looser.
-  float thr[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) thr[rb] = __builtin_inff();
-
-  uint4 ystage[YL];
-  float4 nstage;
-  // the tile at column jt (16-aligned), its columns outside [lo, hi) masked
-  auto fetch = [&](int64_t jt, int64_t lo, int64_t hi) {
-    // y of masked columns is loaded as is (inside the padded array): their
-    // padding norm (+infinity) keeps them out of every list
-    const int ncol = (int)min((int64_t)TJ, ((hi + 15) & ~(int64_t)15) - jt);
-    const uint4* ysrc = reinterpret_cast<const uint4*>(a.ybf + jt * DP);
-#pragma unroll
-    for (int k = 0; k < YL; ++k) {
-      const int f = tid + k * 256;
-      ystage[k] = (f < TU && f < ncol * (DP / 8)) ? ysrc[f] : uint4{0u, 0u, 0u, 0u};
-    }
-    if (tid < TJ / 4) {
-      if constexpr (SP) nstage = masked_ny(a.ny, pad_ny, jt + 4 * tid, lo, hi);
-      else nstage = (tid * 4 < ncol) ? reinterpret_cast<const float4*>(a.ny + jt)[tid]
-                                     : float4{0.f, 0.f, 0.f, 0.f};
-    }
-  };
-  auto put = [&](int buf) {
-#pragma unroll
-    for (int k = 0; k < YL; ++k) {
-      const int f = tid + k * 256;
-      if (f < TU) ys[buf][(f / (DP / 8)) * RU + f % (DP / 8)] = ystage[k];
-    }
-    if (tid < TJ / 4) ns[buf][tid] = nstage;
-  };
-
-  auto segment = [&](int64_t a0, int64_t a1) {
-  const int64_t base = a0 & ~(int64_t)15;
-  const int64_t ntiles = (a1 - base + TJ - 1) / TJ;
-  fetch(base, a0, a1);
-  put(0);
-  __syncthreads();
-  for (int64_t t = 0; t < ntiles; ++t) {
-    const int64_t jt = base + t * TJ;
-    const int buf = (int)(t & 1);
-    const int nblk = (int)((min((int64_t)TJ, a1 - jt) + 15) / 16);
-    if (t + 1 < ntiles) fetch(jt + TJ, a0, a1);
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      float v = dlast[rb];
-      v = fminf(v, __shfl_xor(v, 16));
-      v = fminf(v, __shfl_xor(v, 32));
-      float u = key_d(kk[rb][(KP + 3) / 4 - 1]);
-      u = fmaxf(u, __shfl_xor(u, 16));
-      u = fmaxf(u, __shfl_xor(u, 32));
-      thr[rb] = fminf(v, u);
-    }
-    for (int blk = 0; blk < nblk; ++blk) {
-      bf16x8 ya[NCH];
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch)
-        ya[ch] = __builtin_bit_cast(bf16x8, ys[buf][(blk * 16 + li) * RU + 4 * ch + g]);
-      const float4 nyv = ns[buf][blk * 4 + g];
-      // all row blocks' products first (independent chains overlap), then
-      // every filter test, and only then the branches: no branch sits between
-      // an MFMA and the first read of its result
-      f4 acc[RB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        acc[rb] = f4{nyv.x, nyv.y, nyv.z, nyv.w};
-#pragma unroll
-        for (int ch = 0; ch < NCH; ++ch)
-          acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ya[ch], xb[rb][ch], acc[rb], 0, 0, 0);
-      }
-      bool any[RB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const float th = thr[rb];
-        any[rb] = fminf(fminf(acc[rb][0], acc[rb][1]), fminf(acc[rb][2], acc[rb][3])) <= th;
-      }
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        if (__builtin_expect(any[rb], 0)) {
-          const int jb = (int)(jt + blk * 16 + 4 * g);
-          // columns arrive in index order, so a distance equal to the last
-          // entry's loses the tie
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (acc[rb][r] < dlast[rb]) {
-              key_insert<KP>(kk[rb], __builtin_fma((double)acc[rb][r], kKeyScale, (double)(jb + r)));
-              dlast[rb] = key_d(kk[rb][KP - 1]);
-            }
-        }
-      }
-    }
-    // buffer (t+1)&1 was last read in iteration t-1, which ended with a barrier
-    if (t + 1 < ntiles) put((int)((t + 1) & 1));
-    __syncthreads();
-  }
-  };
-  if constexpr (SP) for_segments(a, it, segment);
-  else if (it.w0 < it.w1) segment(it.w0, it.w1);
-
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    float part = 0.0f;   // the row norm (exact: integers below 2^24)
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch)
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const float v = (float)xb[rb][ch][t];
-        part = __builtin_fmaf(v, v, part);
-      }
-    part += __shfl_xor(part, 16);
-    part += __shfl_xor(part, 32);
-    const int64_t row = i0 + 16 * rb + li;
-    if (row >= rend) continue;
-    float* q = a.part + (((int64_t)c * 4 + g) * a.M + row) * (2 * KP);
-#pragma unroll
-    for (int p = 0; p < KP; ++p) {
-      const double key = kk[rb][p];
-      const double d = __builtin_floor(key * kKeyInv);
-      const bool empty = key == __builtin_inf();
-      q[2 * p] = empty ? __builtin_inff() : (float)d + part;
-      q[2 * p + 1] = __int_as_float(empty ? INT_MAX : (int)(key - d * kKeyScale));
-    }
-  }
-}
-
-// rows per workgroup as in the fp32 kernel, so both share one grid and one
-// block-sparse workgroup map
-constexpr int bf16_rows_blocks(int NCH, int KP) { return (NCH >= 8 || KP >= 64) ? 1 : 2; }
-
-template <int NCH, bool SP>
-hipError_t launch_knn_bf16_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
-  switch (a.KP) {
-#define KRED_KNN_BF16(KPV)                                                                     \
-  case KPV:                                                                                     \
-    hipLaunchKernelGGL((knn_bf16_kernel<NCH, bf16_rows_blocks(NCH, KPV), KPV, SP>), grid, dim3(256), \
-                       0, s, a);                                                                \
-    break;
-    KRED_KNN_BF16(1) KRED_KNN_BF16(4) KRED_KNN_BF16(8) KRED_KNN_BF16(10) KRED_KNN_BF16(12)
-    KRED_KNN_BF16(16) KRED_KNN_BF16(64)
-#undef KRED_KNN_BF16
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
 
 // ------------------------------------------------ sums, split bf16 products
 // The Gaussian sum of mfma_kernel with the inner product on the bf16 matrix
@@ -1042,18 +823,6 @@ hipError_t launch_exact_check(const float* x, int64_t M, const float* y, int64_t
   hipLaunchKernelGGL(exact_check_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, M * D, y,
                      N * D, g);
   return hipGetLastError();
-}
-
-hipError_t launch_knn_bf16(const MfmaArgs& a, hipStream_t s) {
-  const int rows = mfma_rows_per_block(a.DP, a.KP);
-  const dim3 grid((unsigned)(mfma_row_groups(a, rows) * a.C));
-  switch (a.DP) {
-    case 32: return a.nr > 0 ? launch_knn_bf16_n<1, true>(a, grid, s) : launch_knn_bf16_n<1, false>(a, grid, s);
-    case 64: return a.nr > 0 ? launch_knn_bf16_n<2, true>(a, grid, s) : launch_knn_bf16_n<2, false>(a, grid, s);
-    case 128: return a.nr > 0 ? launch_knn_bf16_n<4, true>(a, grid, s) : launch_knn_bf16_n<4, false>(a, grid, s);
-    case 256: return a.nr > 0 ? launch_knn_bf16_n<8, true>(a, grid, s) : launch_knn_bf16_n<8, false>(a, grid, s);
-    default: return hipErrorInvalidValue;
-  }
 }
 
 hipError_t launch_mfma_split(const MfmaArgs& a, hipStream_t s) {

@@ -21,12 +21,12 @@ import pytest
 from paper_2004_11127_amd import build
 
 MIN_SLOTS = 6
-SOURCES = ["k_small_mfma.hip", "k_mfma.hip", "k_mfma64.hip", "k_small.hip"]
+SOURCES = ["k_small_mfma.hip", "k_mfma.hip", "k_mfma64.hip", "k_knn.hip", "k_small.hip"]
 
 
 def _asm(src, tmp_path):
     out = os.path.join(tmp_path, src + ".s")
-    cmd = [build.HIPCC] + build.FLAGS + ["--cuda-device-only", "-S",
+    cmd = [build.HIPCC] + build.flags_for(src) + ["--cuda-device-only", "-S",
                                          os.path.join(build.CSRC, src), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
