@@ -108,7 +108,7 @@ LIST_K = {"knn3": 10}   # K of the arg-K-min workloads drawn by a generator with
 KERNEL_SOURCES = {"sum_kernel": "k_direct.hip", "gradx_kernel": "k_direct.hip",
                   "lse_kernel": "k_direct.hip", "knn_kernel": "k_direct.hip",
                   "vjp_kernel": "k_direct.hip", "mfma_kernel": "k_mfma.hip",
-                  "mfma_split_kernel": "k_mfma.hip", "knn_bf16_kernel": "k_mfma.hip",
+                  "mfma_split_kernel": "k_mfma.hip", "knn_bf16_kernel": "k_knn.hip",
                   "fast_kernel": "k_small_mfma.hip", "small_kernel": "k_small.hip"}
 
 
