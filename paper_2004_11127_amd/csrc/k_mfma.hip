@@ -130,8 +130,11 @@ __global__ __launch_bounds__(256) void mfma_norm_kernel(MfmaPackArgs a) {
   }
   if (a.spread != nullptr) {
     // the centred forms: ny = fl32(-|Y|^2 (+ g')) with Y = fl32(s (y - m)) the
-    // coordinates the contraction uses, the sum in fp64 and one rounding
-    for (int64_t j = wave; j < a.N16; j += waves) {
+    // coordinates the contraction uses, the sum in fp64 and one rounding; the
+    // split kernel also reads 16 padding norms after the N16 columns (the
+    // source of its masked columns' norms; the buffer is sized for fp64)
+    const int64_t nend = a.N16 + (a.ysp != nullptr ? 16 : 0);
+    for (int64_t j = wave; j < nend; j += waves) {
       double s = 0.0;
       if (j < a.N)
         for (int d = lane; d < a.D; d += 64) {
@@ -197,6 +200,7 @@ __global__ __launch_bounds__(256) void exact_check_kernel(const float* __restric
 }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f16v __attribute__((ext_vector_type(16)));
 
 // ------------------------------------------------ sums, split bf16 products
 // The Gaussian sum of mfma_kernel with the inner product on the bf16 matrix
@@ -214,13 +218,15 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 // of each block (P[i = li][j = 4 g + r], the exponent's own D layout) are the 8
 // K values k = 8 g + 4 h + r of one v_mfma_f32_16x16x32_bf16, split into three
 // bf16 parts like the coordinates, and the signal is stored by the prologue as
-// three bf16 planes in the matching K order (bsplit_index), so six products
+// three bf16 planes in the matching K order (mfma_pack_kernel), so six products
 // per 32 columns replace eight v_mfma_f32_16x16x4_f32 (48 matrix-core cycles
 // per 16 columns instead of 128).  Wider D keeps the fp32 P . B.
+// DP = 64 and 128 take mfma_split_kernel below (32 x 32 tiles); this kernel
+// serves DP = 32 and 256.
 constexpr int split_tile_cols(int DP) { return DP <= 64 ? 64 : (DP <= 128 ? 32 : 16); }
 
 template <int NCH, int RB, int EB, bool SP>
-__global__ __launch_bounds__(256) void mfma_split_kernel(MfmaArgs a) {
+__global__ __launch_bounds__(256) void mfma_split16_kernel(MfmaArgs a) {
   constexpr int DP = 32 * NCH;
   constexpr int TJ = split_tile_cols(DP);
   constexpr bool PAIR = TJ % 32 == 0;          // P . B on the bf16 matrix cores
@@ -520,13 +526,377 @@ hipError_t launch_split_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   // the fp64 contraction, launched beside this one
   if (a.epi != 0) return hipSuccess;
   switch (a.EB) {
-    case 1: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, 1, SP>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, 2, SP>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((mfma_split_kernel<NCH, RB, 4, SP>), grid, dim3(256), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((mfma_split16_kernel<NCH, RB, 1, SP>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((mfma_split16_kernel<NCH, RB, 2, SP>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((mfma_split16_kernel<NCH, RB, 4, SP>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
+
+// ------------------------------------ sums, split bf16 products, 32x32 tiles
+// The same split sum for DP = 64 and 128 with the exponent on
+// v_mfma_f32_32x32x16_bf16: one wave owns 32 rows, and each 32-column tile is
+// one 32 x 32 block of T, six instructions per 16 coordinates (hh, hm, mh into
+// one chain, mm, hl, lh into the other, both from zero).  The instruction adds
+// its products in groups of 8 exactly as the 16x16x32 form does (in-bounds
+// probes: one group's 2^24 + 1 + 1 is exact, two groups give 2^24, the same
+// roundings of 1 +- 2^-24 (1 + 2^-7)), so the split form's error bound is
+// unchanged; its matrix-core rate is the higher one (two chains per wave come
+// near the dense bf16 peak where the 16x16x32 form needs many more).
+// Lane l = 32 h + i supplies column i of the tile's y and row i of x, each at
+// coordinates 16 ch + 8 h .. + 7, and holds T[i][j] for the 16 columns
+// j = 8 q + 4 h + r (q, r < 4).  P . B stays on v_mfma_f32_16x16x32_bf16 (E is
+// 16 per block, a 32-wide B would be half empty): the lane's p values of
+// q = 0, 2 (U) and q = 1, 3 (V) pass through one permlane32 and one permlane16
+// swap, which leaves in every lane group g of 16 lanes the 8 K values
+// k = 8 g + t (column 16 (t / 4) + 4 g + t % 4, the prologue's b order) of
+// rows 0-15 (first register) and rows 16-31 (second).
+// Workgroups of 8 waves (256 rows, two waves per SIMD) halve the y traffic
+// per row against 4.  Every part of a tile (y planes, norms, b planes) goes
+// from memory straight into LDS, two tiles ahead, into four sets of buffers
+// that are distinct arrays indexed statically (the loop is unrolled by 4):
+// the compiler then sees that no read aliases an outstanding direct load and
+// waits for none; the waits are explicit (the newest tile's loads stay in
+// flight) and the barrier orders LDS only.  With 16 signal columns the
+// exponent's products of tile t are issued together with the vector work of
+// tile t - 1 (norms, 2^T, swaps, splits) and its P . B, so that neither unit
+// waits for the other inside a wave.
+
+// v0, v1 -> packed bf16 pairs h, m, l with v = h + m + l exactly (each part
+// rounded to nearest; the remainders are exact in fp32)
+__device__ __forceinline__ void split3x2(float v0, float v1, unsigned& h, unsigned& m, unsigned& l) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  h = __builtin_bit_cast(unsigned, __builtin_convertvector((f2{v0, v1}), bf16x2));
+  const float r0 = v0 - __builtin_bit_cast(float, h << 16);
+  const float r1 = v1 - __builtin_bit_cast(float, h & 0xffff0000u);
+  m = __builtin_bit_cast(unsigned, __builtin_convertvector((f2{r0, r1}), bf16x2));
+  const float s0 = r0 - __builtin_bit_cast(float, m << 16);
+  const float s1 = r1 - __builtin_bit_cast(float, m & 0xffff0000u);
+  l = __builtin_bit_cast(unsigned, __builtin_convertvector((f2{s0, s1}), bf16x2));
+}
+
+// the fewest direct loads one of nwv waves makes per tile: y windows
+// round-robin, b windows round-robin, and the norms by the last wave
+constexpr int split32_min_loads(int yw, int bo, int nwv) {
+  int best = 1 << 30;
+  for (int w = 0; w < nwv; ++w) {
+    int n = 0;
+    for (int o = w; o < yw; o += nwv) ++n;
+    for (int o = w; o < bo; o += nwv) ++n;
+    if (w == nwv - 1) ++n;
+    best = n < best ? n : best;
+  }
+  return best;
+}
+
+template <int NC, int EB, bool SP>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void mfma_split_kernel(MfmaArgs a) {
+  constexpr int NWV = 8;                      // waves per workgroup, 32 rows each
+  constexpr int DP = 16 * NC;
+  constexpr int TJ = 32;
+  constexpr int PU = DP / 8;                  // uint4 per plane of a column
+  constexpr int TU = TJ * 3 * PU;             // uint4 of y planes per tile
+  static_assert(TU % 64 == 0, "whole wave loads per tile");
+  constexpr int YI = (TU / 64 + NWV - 1) / NWV;   // direct loads per wave and tile (at most)
+  constexpr int YMIN = (TU / 64) / NWV;           // ... made by every wave
+  static_assert(YMIN >= 1 && YI <= 3, "tile shape");
+  constexpr int W = 16 * EB;
+  constexpr int BO = (15 * W + 63) / 64;      // wave loads of a slot's b planes
+  constexpr int BI = (BO + NWV - 1) / NWV;
+  // direct loads per wave and tile, the fewest over the waves (y, b, norms)
+  constexpr int VKEEP = split32_min_loads(TU / 64, BO, NWV);
+  static_assert(VKEEP >= 1 && VKEEP <= 15, "wait count");
+
+  // four buffers of a tile: y planes as in HBM, uint4 q of column c at
+  // position q ^ (c & (PU - 1)) within its plane (16 consecutive columns on
+  // distinct bank groups), the norms, and the b planes (rows of 5 uint4);
+  // distinct arrays, indexed statically, so that the compiler knows that the
+  // direct loads into one buffer never alias the reads of another
+  __shared__ uint4 ys0[TU], ys1[TU], ys2[TU], ys3[TU];
+  __shared__ float4 ns0[TJ / 4], ns1[TJ / 4], ns2[TJ / 4], ns3[TJ / 4];
+  __shared__ uint4 bq0[15 * W], bq1[15 * W], bq2[15 * W], bq3[15 * W];
+
+  if (wide64(a.spread, a.wide_c, a.wide_limit)) return;   // the fp64 contraction does the work
+  const MItem it = mitem<SP>(a, 32 * NWV);
+  if (!it.live) return;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int li = lane & 15, g = lane >> 4;    // P . B lanes
+  const int i32 = lane & 31, h = lane >> 5;   // exponent lanes
+  const int c = it.c;
+  const int64_t rend = it.row_end;
+  const float pad_ny = a.pad_ny;
+  const int64_t i0 = it.row0 + wave * 32;
+
+  // planes of x[i32][16 ch + 8 h + t]; X = fl32(s (x - m)) formed in fp64 and
+  // nx = -fl32(|X|^2) summed in fp64
+  bf16x8 xh[NC], xm[NC], xl[NC];
+  float nx;
+  {
+    const int64_t row = i0 + i32;
+    const bool ok = row < rend;
+    double part = 0.0;
+#pragma unroll
+    for (int ch = 0; ch < NC; ++ch)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int d = 16 * ch + 8 * h + t;
+        const float v =
+            (ok && d < a.D) ? (float)(((double)a.x[row * a.D + d] -
+                                       (double)(a.xc != nullptr ? a.xc[d] : 0.0f)) * a.xscale64)
+                            : 0.0f;
+        __bf16 vh, vm, vl;
+        split3(v, vh, vm, vl);
+        xh[ch][t] = vh;
+        xm[ch][t] = vm;
+        xl[ch][t] = vl;
+        part = __builtin_fma((double)v, (double)v, part);
+      }
+    part += __shfl_xor(part, 32);
+    nx = -(float)part;
+  }
+
+  f4 tot[2][EB];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int eb = 0; eb < EB; ++eb) tot[u][eb] = f4{0.f, 0.f, 0.f, 0.f};
+
+  // source of the uint4 this lane loads into slot k of a whole tile
+  int yoff[YI];
+#pragma unroll
+  for (int k = 0; k < YI; ++k) {
+    const int sl = 64 * (NWV * k + wave) + lane;
+    const int cc = sl / (3 * PU), qq = sl - cc * 3 * PU;
+    yoff[k] = cc * 3 * PU + (qq ^ (cc & (PU - 1)));
+  }
+
+  // the tile at column jt (32-aligned) into buffers yd, nd, bd, every
+  // part straight from memory into LDS (lane l of a wave writes the 4 or 16
+  // bytes at the window's base + l times that; each lane loads what belongs
+  // at its position): the norms (a column outside [lo, hi) or past the
+  // loaded 16-column blocks reads a padding norm), the b planes (the row
+  // padding slots read any b), and the y planes (a column past the loaded
+  // blocks reads a copy of the last loaded one: finite, removed by its norm)
+  auto fetch = [&](uint4 (&yd)[TU], float4 (&nd)[TJ / 4], uint4 (&bd)[15 * W], int64_t jt, int64_t lo,
+                   int64_t hi) __attribute__((always_inline)) {
+    const int ncol = (int)min((int64_t)TJ, ((hi + 15) & ~(int64_t)15) - jt);
+    if (wave == NWV - 1 && lane < TJ) {
+      const int64_t col = jt + lane;
+      const bool live = SP ? (col >= lo && col < hi) : (lane < ncol);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.ny + (live ? col : a.N16)),
+                                       (__attribute__((address_space(3))) void*)(&nd[0]), 4, 0, 0);
+    }
+    const uint4* bsrc = reinterpret_cast<const uint4*>(a.bpk) + (jt / 32) * (12 * W);
+#pragma unroll
+    for (int k = 0; k < BI; ++k) {
+      const int o = NWV * k + wave;   // the wave's window of the slot
+      if (o >= BO) break;             // wave-uniform
+      const int sl = 64 * o + lane, row = sl / 5, kc = sl - row * 5;
+      if (sl < 15 * W)
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(bsrc + row * 4 + (kc < 4 ? kc : 0)),
+                                         (__attribute__((address_space(3))) void*)(&bd[64 * o]), 16, 0, 0);
+    }
+    const uint4* ysrc = reinterpret_cast<const uint4*>(a.ysp + jt * 3 * DP);
+#pragma unroll
+    for (int k = 0; k < YI; ++k) {
+      const int s0 = 64 * (NWV * k + wave);
+      if (k >= YMIN && s0 >= TU) break;   // wave-uniform
+      int src = yoff[k];
+      if (ncol < TJ) {
+        const int sl = s0 + lane;
+        const int cc = sl / (3 * PU), qq = sl - cc * 3 * PU;
+        src = min(cc, ncol - 1) * 3 * PU + (qq ^ (cc & (PU - 1)));
+      }
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(ysrc + src),
+                                       (__attribute__((address_space(3))) void*)(&yd[s0]), 16, 0, 0);
+    }
+  };
+  // vector-memory waits: the newest tile's direct loads (at least VKEEP per
+  // wave, issued last) may stay in flight, or none
+  auto wait_vm_keep = [&]() { __builtin_amdgcn_s_waitcnt((VKEEP & 15) | (0x7 << 4) | (0xf << 8)); };
+  auto wait_vm_all = [&]() { __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xf << 8)); };
+  // workgroup barrier ordering LDS only (vector-memory waits are explicit)
+  auto barrier = [&]() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  };
+
+  // the tile's T less the norms: acc (hh, hm, mh) and acc2 (mm, hl, lh)
+  auto exponent = [&](const uint4 (&yc)[TU], f16v& acc, f16v& acc2) __attribute__((always_inline)) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = acc2[r] = 0.0f;
+    const uint4* col = &yc[i32 * 3 * PU];
+    const int sw = i32 & (PU - 1);
+#pragma unroll
+    for (int ch = 0; ch < NC; ++ch) {
+      const int q = (2 * ch + h) ^ sw;
+      const bf16x8 yh = __builtin_bit_cast(bf16x8, col[q]);
+      const bf16x8 ym = __builtin_bit_cast(bf16x8, col[PU + q]);
+      const bf16x8 yl = __builtin_bit_cast(bf16x8, col[2 * PU + q]);
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ym, xm[ch], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ym, xh[ch], acc, 0, 0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yl, xh[ch], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yh, xm[ch], acc, 0, 0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yh, xl[ch], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yh, xh[ch], acc, 0, 0, 0);
+    }
+  };
+
+  // p = 2^T of a tile from its fl(acc + acc2) and its norms nd, and p . b
+  // (b planes bd) into tot
+  auto finish = [&](const float4 (&nd)[TJ / 4], const uint4 (&bd)[15 * W], const f16v& ap)
+                    __attribute__((always_inline)) {
+    // T = fl(fl(acc + acc2) + fl(nx + ny)), p = 2^T; column 8 q + 4 h + r
+    float p[16];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 nyv = nd[2 * q + h];
+      p[4 * q + 0] = __builtin_amdgcn_exp2f(ap[4 * q + 0] + (nx + nyv.x));
+      p[4 * q + 1] = __builtin_amdgcn_exp2f(ap[4 * q + 1] + (nx + nyv.y));
+      p[4 * q + 2] = __builtin_amdgcn_exp2f(ap[4 * q + 2] + (nx + nyv.z));
+      p[4 * q + 3] = __builtin_amdgcn_exp2f(ap[4 * q + 3] + (nx + nyv.w));
+    }
+    // U = q 0, 2 and V = q 1, 3 -> rows 0-15 (u = 0) and 16-31 (u = 1)
+    float pr[2][8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int ru = t < 4 ? t : t + 4, rv = ru + 4;
+      const auto s1 = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, p[ru]),
+                                                       __builtin_bit_cast(unsigned, p[rv]), false, false);
+      const auto s2 = __builtin_amdgcn_permlane16_swap(s1[0], s1[1], false, false);
+      pr[0][t] = __builtin_bit_cast(float, (unsigned)s2[0]);
+      pr[1][t] = __builtin_bit_cast(float, (unsigned)s2[1]);
+    }
+    bf16x8 ph[2], pm[2], pl[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      unsigned hw[4], mw[4], lw[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) split3x2(pr[u][2 * k], pr[u][2 * k + 1], hw[k], mw[k], lw[k]);
+      ph[u] = __builtin_bit_cast(bf16x8, uint4{hw[0], hw[1], hw[2], hw[3]});
+      pm[u] = __builtin_bit_cast(bf16x8, uint4{mw[0], mw[1], mw[2], mw[3]});
+      pl[u] = __builtin_bit_cast(bf16x8, uint4{lw[0], lw[1], lw[2], lw[3]});
+    }
+#pragma unroll
+    for (int eb = 0; eb < EB; ++eb) {
+      // B planes: b[j(k)][e = 16 eb + li] for k = 8 g .. 8 g + 7
+      const uint4* brow = &bd[(16 * eb + li) * 5 + g];
+      const bf16x8 bh = __builtin_bit_cast(bf16x8, brow[0]);
+      const bf16x8 bm = __builtin_bit_cast(bf16x8, brow[5 * W]);
+      const bf16x8 bl = __builtin_bit_cast(bf16x8, brow[10 * W]);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        // smallest partial products first, from zero; then into the total
+        f4 o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pm[u], bm, f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+        o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[u], bh, o, 0, 0, 0);
+        o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[u], bl, o, 0, 0, 0);
+        o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pm[u], bh, o, 0, 0, 0);
+        o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[u], bm, o, 0, 0, 0);
+        o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[u], bh, o, 0, 0, 0);
+        tot[u][eb] += o;
+      }
+    }
+  };
+
+  // Pipeline per tile t (buffers t % 4): at its start tile t has landed and
+  // tile t + 1 may be in flight; it prefetches tile t + 2 (into the buffers
+  // tile t - 2 used), forms tile t's products and finishes tile t - 1 (its
+  // buffers stay untouched until tile t + 3's prefetch; without PIPE, tile t),
+  // and waits for tile t + 1.  Each segment ends with a barrier, as the next one starts over at
+  // buffers 0.
+  // (with 32 or 64 signal columns the registers do not hold two tiles: each tile is
+  // finished right after its products)
+  constexpr bool PIPE = EB == 1;
+  f16v accp;   // fl(acc + acc2) of the pending tile
+  auto step = [&](int t, int ntiles, int64_t base, int64_t a0, int64_t a1, const uint4 (&yc)[TU],
+                  const float4 (&nc)[TJ / 4], const uint4 (&bc)[15 * W], const float4 (&nf)[TJ / 4],
+                  const uint4 (&bf)[15 * W], uint4 (&yn)[TU], float4 (&nn)[TJ / 4],
+                  uint4 (&bn)[15 * W]) __attribute__((always_inline)) {
+    const bool more = t + 2 < ntiles;
+    if (more) fetch(yn, nn, bn, base + (int64_t)(t + 2) * TJ, a0, a1);
+    f16v acc, acc2;
+    exponent(yc, acc, acc2);
+    if constexpr (PIPE) {
+      if (t > 0) finish(nf, bf, accp);
+      accp = acc + acc2;
+    } else {
+      finish(nc, bc, acc + acc2);
+    }
+    if (more) wait_vm_keep();   // tile t + 1 has landed
+    else wait_vm_all();
+    barrier();
+  };
+  auto segment = [&](int64_t a0, int64_t a1) {
+    const int64_t base = a0 & ~(int64_t)31;
+    const int ntiles = (int)((a1 - base + TJ - 1) / TJ);
+    fetch(ys0, ns0, bq0, base, a0, a1);
+    if (ntiles > 1) {
+      fetch(ys1, ns1, bq1, base + TJ, a0, a1);
+      wait_vm_keep();   // tile 0 has landed
+    } else {
+      wait_vm_all();
+    }
+    barrier();
+    step(0, ntiles, base, a0, a1, ys0, ns0, bq0, ns3, bq3, ys2, ns2, bq2);   // (no tile -1)
+    for (int t = 1; t < ntiles; t += 4) {
+      step(t, ntiles, base, a0, a1, ys1, ns1, bq1, ns0, bq0, ys3, ns3, bq3);
+      if (t + 1 < ntiles) step(t + 1, ntiles, base, a0, a1, ys2, ns2, bq2, ns1, bq1, ys0, ns0, bq0);
+      if (t + 2 < ntiles) step(t + 2, ntiles, base, a0, a1, ys3, ns3, bq3, ns2, bq2, ys1, ns1, bq1);
+      if (t + 3 < ntiles) step(t + 3, ntiles, base, a0, a1, ys0, ns0, bq0, ns3, bq3, ys2, ns2, bq2);
+    }
+    if constexpr (PIPE) {
+      switch ((ntiles - 1) & 3) {
+        case 0: finish(ns0, bq0, accp); break;
+        case 1: finish(ns1, bq1, accp); break;
+        case 2: finish(ns2, bq2, accp); break;
+        default: finish(ns3, bq3, accp); break;
+      }
+    }
+    barrier();
+  };
+  if constexpr (SP) for_segments(a, it, segment);
+  else if (it.w0 < it.w1) segment(it.w0, it.w1);
+
+  // lane holds out[i = 16 u + 4 g + r][e = 16 eb + li]
+  const int Ec = min(W, a.E - a.e0);
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int eb = 0; eb < EB; ++eb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = i0 + 16 * u + 4 * g + r;
+        const int e = 16 * eb + li;
+        if (row >= rend) continue;
+        if (a.C == 1) {
+          if (e < Ec) static_cast<float*>(a.out)[row * a.E + a.e0 + e] = tot[u][eb][r];
+        } else {
+          a.part[((int64_t)c * a.M + row) * W + e] = tot[u][eb][r];
+        }
+      }
+}
+
+// rows per workgroup of mfma_split_kernel
+constexpr int kSplitRows = 256;
+
+template <int NC, bool SP>
+hipError_t launch_split32_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
+  if (a.epi != 0) return hipSuccess;   // as launch_split_n
+  switch (a.EB) {
+    case 1: hipLaunchKernelGGL((mfma_split_kernel<NC, 1, SP>), grid, dim3(512), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((mfma_split_kernel<NC, 2, SP>), grid, dim3(512), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((mfma_split_kernel<NC, 4, SP>), grid, dim3(512), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 
 template <int Q>
 constexpr int rows_blocks() { return Q >= 64 ? 1 : 2; }
@@ -596,6 +966,10 @@ int mfma_knn_pad_k(int K) {
 int mfma_rows_per_block(int DP, int KP) {
   const int Q = DP / 4;
   return 64 * ((Q >= 64 || KP == 64) ? 1 : 2);
+}
+
+int mfma_split_rows_per_block(int DP) {
+  return (DP == 64 || DP == 128) ? kSplitRows : mfma_rows_per_block(DP, 0);
 }
 
 // ------------------------------------------ centre; fused gradient, large D
@@ -826,12 +1200,12 @@ hipError_t launch_exact_check(const float* x, int64_t M, const float* y, int64_t
 }
 
 hipError_t launch_mfma_split(const MfmaArgs& a, hipStream_t s) {
-  const int rows = mfma_rows_per_block(a.DP, 0);
+  const int rows = mfma_split_rows_per_block(a.DP);
   const dim3 grid((unsigned)(mfma_row_groups(a, rows) * a.C));
   switch (a.DP) {
     case 32: return a.nr > 0 ? launch_split_n<1, true>(a, grid, s) : launch_split_n<1, false>(a, grid, s);
-    case 64: return a.nr > 0 ? launch_split_n<2, true>(a, grid, s) : launch_split_n<2, false>(a, grid, s);
-    case 128: return a.nr > 0 ? launch_split_n<4, true>(a, grid, s) : launch_split_n<4, false>(a, grid, s);
+    case 64: return a.nr > 0 ? launch_split32_n<4, true>(a, grid, s) : launch_split32_n<4, false>(a, grid, s);
+    case 128: return a.nr > 0 ? launch_split32_n<8, true>(a, grid, s) : launch_split32_n<8, false>(a, grid, s);
     case 256: return a.nr > 0 ? launch_split_n<8, true>(a, grid, s) : launch_split_n<8, false>(a, grid, s);
     default: return hipErrorInvalidValue;
   }

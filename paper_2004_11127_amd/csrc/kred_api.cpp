@@ -383,9 +383,14 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   const bool split_sum = q.epi <= 2 && exact_eligible(p->flags, M, N);
   q.wide_limit = !(q.epi == 0 || q.epi == 4 || q.epi == 6 || q.epi == 9) ? -1.0f
                  : split_sum ? wide_limit_split(D) : wide_limit_f32(D);
-  const int rows = mfma_rows_per_block(q.DP, q.KP);
+  const int rows = (split_sum && q.epi == 0) ? mfma_split_rows_per_block(q.DP)
+                                            : mfma_rows_per_block(q.DP, q.KP);
   const int64_t row_blocks = std::max<int64_t>(1, (M + rows - 1) / rows);
   int C = choose_col_blocks(row_blocks, q.N16, num_cus, p->col_blocks);
+  // the split sum kernel with 4 to 7 column blocks: 8, one per XCD (blockIdx
+  // mod 8 picks both), so that each XCD's L2 serves one stream of y tiles
+  // (c4: 51.3 ms against 52.4 at the 6 chosen above)
+  if (split_sum && q.epi == 0 && p->col_blocks <= 0 && C >= 4 && C < 8 && q.N16 >= 8 * 128) C = 8;
   int64_t jpb = (q.N16 + C - 1) / C;
   jpb = (jpb + q.TJ - 1) / q.TJ * q.TJ;
   q.jpb = jpb;
@@ -540,7 +545,6 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   MPlan pl;
   if (!make_mplan(f, r, p, M, N, D, E, ctx->num_cus, &pl)) return KRED_ERR_UNSUPPORTED;
   if (rg) pl.C = std::max(1, std::min(p->col_blocks, KRED_MAX_COL_BLOCKS));   // chunks per cluster
-  const int64_t rows_wg = mfma_rows_per_block(pl.DP, pl.KP);
   const bool knn = (r == KRED_R_ARGKMIN);
   const bool lse = (r == KRED_R_LSE);
   const bool ext = is_extreme(r);
@@ -551,6 +555,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   // sums: the split bf16 kernel replaces the fp32 one; log-sum-exp: fp32 only
   const bool exact = knn && exact_knn_eligible(p->flags, M, N);
   const bool split = !knn && !lse && !ext && exact_eligible(p->flags, M, N);
+  const int64_t rows_wg = split ? mfma_split_rows_per_block(pl.DP) : mfma_rows_per_block(pl.DP, pl.KP);
   const int64_t ybf_bytes = mfma_bf16_bytes(pl, knn, p->flags, M, N);
   if (rg) {   // partials of every chunk (rows outside the clusters read the empty value)
     pl.part_bytes = knn ? align_up((int64_t)4 * pl.C * M * 2 * pl.KP * (int64_t)sizeof(float))
