@@ -128,6 +128,8 @@ def matrix_flops_per_pair(kernel, w, reduction, formula=None):
         widths = [min(64, w.D + 1 - c) for c in range(0, w.D + 1, 64)]
     ebs = [1 if e <= 16 else (2 if e <= 32 else 4) for e in widths]
     if kernel == "mfma_split_kernel":     # 6 split products per coordinate
+        if reduction == "lse":            # the log-sum-exp has no P . B
+            return {"bf16": 12 * dp}
         if dp <= 128:                     # P . B: 6 bf16 16x16x32 products per 32 x 16 pairs
             return {"bf16": 12 * dp * len(ebs) + sum(192 * eb for eb in ebs)}
         return {"bf16": 12 * dp * len(ebs), "f32": sum(32 * eb for eb in ebs)}

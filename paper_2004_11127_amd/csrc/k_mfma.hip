@@ -591,7 +591,7 @@ constexpr int split32_min_loads(int yw, int bo, int nwv) {
   return best;
 }
 
-template <int NC, int EB, bool SP>
+template <int NC, int EB, int EPI, bool SP>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void mfma_split_kernel(MfmaArgs a) {
   constexpr int NWV = 8;                      // waves per workgroup, 32 rows each
@@ -603,8 +603,10 @@ void mfma_split_kernel(MfmaArgs a) {
   constexpr int YI = (TU / 64 + NWV - 1) / NWV;   // direct loads per wave and tile (at most)
   constexpr int YMIN = (TU / 64) / NWV;           // ... made by every wave
   static_assert(YMIN >= 1 && YI <= 3, "tile shape");
+  constexpr bool LSE = EPI == 4;              // log-sum-exp (E = 1, no b planes)
   constexpr int W = 16 * EB;
-  constexpr int BO = (15 * W + 63) / 64;      // wave loads of a slot's b planes
+  constexpr int BQ = LSE ? 1 : 15 * W;        // uint4 of a slot's b planes
+  constexpr int BO = LSE ? 0 : (BQ + 63) / 64;   // wave loads of a slot's b planes
   constexpr int BI = (BO + NWV - 1) / NWV;
   // direct loads per wave and tile, the fewest over the waves (y, b, norms)
   constexpr int VKEEP = split32_min_loads(TU / 64, BO, NWV);
@@ -617,7 +619,7 @@ void mfma_split_kernel(MfmaArgs a) {
   // direct loads into one buffer never alias the reads of another
   __shared__ uint4 ys0[TU], ys1[TU], ys2[TU], ys3[TU];
   __shared__ float4 ns0[TJ / 4], ns1[TJ / 4], ns2[TJ / 4], ns3[TJ / 4];
-  __shared__ uint4 bq0[15 * W], bq1[15 * W], bq2[15 * W], bq3[15 * W];
+  __shared__ uint4 bq0[BQ], bq1[BQ], bq2[BQ], bq3[BQ];
 
   if (wide64(a.spread, a.wide_c, a.wide_limit)) return;   // the fp64 contraction does the work
   const MItem it = mitem<SP>(a, 32 * NWV);
@@ -682,7 +684,7 @@ void mfma_split_kernel(MfmaArgs a) {
   // loaded 16-column blocks reads a padding norm), the b planes (the row
   // padding slots read any b), and the y planes (a column past the loaded
   // blocks reads a copy of the last loaded one: finite, removed by its norm)
-  auto fetch = [&](uint4 (&yd)[TU], float4 (&nd)[TJ / 4], uint4 (&bd)[15 * W], int64_t jt, int64_t lo,
+  auto fetch = [&](uint4 (&yd)[TU], float4 (&nd)[TJ / 4], uint4 (&bd)[BQ], int64_t jt, int64_t lo,
                    int64_t hi) __attribute__((always_inline)) {
     const int ncol = (int)min((int64_t)TJ, ((hi + 15) & ~(int64_t)15) - jt);
     if (wave == NWV - 1 && lane < TJ) {
@@ -691,7 +693,7 @@ void mfma_split_kernel(MfmaArgs a) {
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.ny + (live ? col : a.N16)),
                                        (__attribute__((address_space(3))) void*)(&nd[0]), 4, 0, 0);
     }
-    const uint4* bsrc = reinterpret_cast<const uint4*>(a.bpk) + (jt / 32) * (12 * W);
+    const uint4* bsrc = LSE ? nullptr : reinterpret_cast<const uint4*>(a.bpk) + (jt / 32) * (12 * W);
 #pragma unroll
     for (int k = 0; k < BI; ++k) {
       const int o = NWV * k + wave;   // the wave's window of the slot
@@ -750,8 +752,37 @@ void mfma_split_kernel(MfmaArgs a) {
 
   // p = 2^T of a tile from its fl(acc + acc2) and its norms nd, and p . b
   // (b planes bd) into tot
-  auto finish = [&](const float4 (&nd)[TJ / 4], const uint4 (&bd)[15 * W], const f16v& ap)
+  // log-sum-exp: per lane the running maximum lm of its row's s (= T, log2
+  // units) and the sum ls of 2^(s - lm), rescaled when lm moves (as the fp32
+  // kernel; lm starts finite, so an empty start never forms inf - inf)
+  float lm = -3.0e38f, ls = 0.0f;
+  auto finish = [&](const float4 (&nd)[TJ / 4], const uint4 (&bd)[BQ], const f16v& ap)
                     __attribute__((always_inline)) {
+    if constexpr (LSE) {
+      float sv[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 nyv = nd[2 * q + h];
+        sv[4 * q + 0] = ap[4 * q + 0] + (nx + nyv.x);
+        sv[4 * q + 1] = ap[4 * q + 1] + (nx + nyv.y);
+        sv[4 * q + 2] = ap[4 * q + 2] + (nx + nyv.z);
+        sv[4 * q + 3] = ap[4 * q + 3] + (nx + nyv.w);
+      }
+      float mb = sv[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mb = fmaxf(mb, sv[r]);
+      const float nm = fmaxf(lm, mb);
+      float e[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(sv[r] - nm);
+#pragma unroll
+      for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+        for (int r = 0; r < w; ++r) e[r] += e[r + w];
+      ls = ls * __builtin_amdgcn_exp2f(lm - nm) + e[0];
+      lm = nm;
+      return;
+    }
     // T = fl(fl(acc + acc2) + fl(nx + ny)), p = 2^T; column 8 q + 4 h + r
     float p[16];
 #pragma unroll
@@ -815,9 +846,9 @@ void mfma_split_kernel(MfmaArgs a) {
   constexpr bool PIPE = EB == 1;
   f16v accp;   // fl(acc + acc2) of the pending tile
   auto step = [&](int t, int ntiles, int64_t base, int64_t a0, int64_t a1, const uint4 (&yc)[TU],
-                  const float4 (&nc)[TJ / 4], const uint4 (&bc)[15 * W], const float4 (&nf)[TJ / 4],
-                  const uint4 (&bf)[15 * W], uint4 (&yn)[TU], float4 (&nn)[TJ / 4],
-                  uint4 (&bn)[15 * W]) __attribute__((always_inline)) {
+                  const float4 (&nc)[TJ / 4], const uint4 (&bc)[BQ], const float4 (&nf)[TJ / 4],
+                  const uint4 (&bf)[BQ], uint4 (&yn)[TU], float4 (&nn)[TJ / 4],
+                  uint4 (&bn)[BQ]) __attribute__((always_inline)) {
     const bool more = t + 2 < ntiles;
     if (more) fetch(yn, nn, bn, base + (int64_t)(t + 2) * TJ, a0, a1);
     f16v acc, acc2;
@@ -863,6 +894,24 @@ void mfma_split_kernel(MfmaArgs a) {
   if constexpr (SP) for_segments(a, it, segment);
   else if (it.w0 < it.w1) segment(it.w0, it.w1);
 
+  if constexpr (LSE) {
+    // merge the row's two lanes (h = 0, 1): (m, s) + (m', s') relative to max(m, m')
+    const float m2 = __shfl_xor(lm, 32), s2 = __shfl_xor(ls, 32);
+    const float nm = fmaxf(lm, m2);
+    const float t = ls * __builtin_amdgcn_exp2f(lm - nm) + s2 * __builtin_amdgcn_exp2f(m2 - nm);
+    const int64_t row = i0 + i32;
+    if (h == 0 && row < rend) {
+      if (a.C == 1) {
+        // an empty row (t = 0) gives -infinity
+        static_cast<float*>(a.out)[row] = (nm + __builtin_amdgcn_logf(t)) * kLn2;
+      } else {
+        float* pp = a.part + ((int64_t)c * a.M + row) * 2;   // the (m, s) pair the combine merges
+        pp[0] = t > 0.0f ? nm : -__builtin_inff();
+        pp[1] = t;
+      }
+    }
+    return;
+  }
   // lane holds out[i = 16 u + 4 g + r][e = 16 eb + li]
   const int Ec = min(W, a.E - a.e0);
 #pragma unroll
@@ -887,11 +936,15 @@ constexpr int kSplitRows = 256;
 
 template <int NC, bool SP>
 hipError_t launch_split32_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
+  if (a.epi == 4) {   // the Gaussian and Sinkhorn log-sum-exp
+    hipLaunchKernelGGL((mfma_split_kernel<NC, 1, 4, SP>), grid, dim3(512), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.epi != 0) return hipSuccess;   // as launch_split_n
   switch (a.EB) {
-    case 1: hipLaunchKernelGGL((mfma_split_kernel<NC, 1, SP>), grid, dim3(512), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((mfma_split_kernel<NC, 2, SP>), grid, dim3(512), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((mfma_split_kernel<NC, 4, SP>), grid, dim3(512), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((mfma_split_kernel<NC, 1, 0, SP>), grid, dim3(512), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((mfma_split_kernel<NC, 2, 0, SP>), grid, dim3(512), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((mfma_split_kernel<NC, 4, 0, SP>), grid, dim3(512), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

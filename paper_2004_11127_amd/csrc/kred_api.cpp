@@ -381,16 +381,19 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   // fp64 contraction; arg-K-min ranks in fp32 and is re-ranked exactly
   // (sums take the split bf16 kernel where it is eligible, with its own bound)
   const bool split_sum = q.epi <= 2 && exact_eligible(p->flags, M, N);
+  // the Gaussian and Sinkhorn log-sum-exp on the 32x32-tile split kernel (DP
+  // 64 and 128), under the split contraction's bound
+  const bool split_lse = q.epi == 4 && split_lse_dp(q.DP) && exact_eligible(p->flags, M, N);
   q.wide_limit = !(q.epi == 0 || q.epi == 4 || q.epi == 6 || q.epi == 9) ? -1.0f
-                 : split_sum ? wide_limit_split(D) : wide_limit_f32(D);
-  const int rows = (split_sum && q.epi == 0) ? mfma_split_rows_per_block(q.DP)
-                                            : mfma_rows_per_block(q.DP, q.KP);
+                 : (split_sum || split_lse) ? wide_limit_split(D) : wide_limit_f32(D);
+  const bool split32 = (split_sum && q.epi == 0) || split_lse;
+  const int rows = split32 ? mfma_split_rows_per_block(q.DP) : mfma_rows_per_block(q.DP, q.KP);
   const int64_t row_blocks = std::max<int64_t>(1, (M + rows - 1) / rows);
   int C = choose_col_blocks(row_blocks, q.N16, num_cus, p->col_blocks);
   // the split sum kernel with 4 to 7 column blocks: 8, one per XCD (blockIdx
   // mod 8 picks both), so that each XCD's L2 serves one stream of y tiles
   // (c4: 51.3 ms against 52.4 at the 6 chosen above)
-  if (split_sum && q.epi == 0 && p->col_blocks <= 0 && C >= 4 && C < 8 && q.N16 >= 8 * 128) C = 8;
+  if (split32 && p->col_blocks <= 0 && C >= 4 && C < 8 && q.N16 >= 8 * 128) C = 8;
   int64_t jpb = (q.N16 + C - 1) / C;
   jpb = (jpb + q.TJ - 1) / q.TJ * q.TJ;
   q.jpb = jpb;
@@ -552,9 +555,11 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   // for the bare squared distance; the signal is then a column of ones
   const bool unit_b = ext && (f == KRED_F_SINKHORN || b == nullptr);
   // arg-K-min: the exact bf16 kernel is a candidate (the device decides);
-  // sums: the split bf16 kernel replaces the fp32 one; log-sum-exp: fp32 only
+  // sums, and the Gaussian / Sinkhorn log-sum-exp at DP = 64, 128: the split
+  // bf16 kernel replaces the fp32 one
   const bool exact = knn && exact_knn_eligible(p->flags, M, N);
-  const bool split = !knn && !lse && !ext && exact_eligible(p->flags, M, N);
+  const bool split = !knn && !ext && exact_eligible(p->flags, M, N) &&
+                     (!lse || (pl.epi == 4 && split_lse_dp(pl.DP)));
   const int64_t rows_wg = split ? mfma_split_rows_per_block(pl.DP) : mfma_rows_per_block(pl.DP, pl.KP);
   const int64_t ybf_bytes = mfma_bf16_bytes(pl, knn, p->flags, M, N);
   if (rg) {   // partials of every chunk (rows outside the clusters read the empty value)

@@ -94,6 +94,8 @@ def test_matrix_work_per_pair_follows_the_mfma_shapes():
     assert bench.matrix_flops_per_pair("small_kernel", _W(3), "sum") == {"f32": 8}
     # fp32 log-sum-exp at D = 64: the inner product only, no signal product
     assert bench.matrix_flops_per_pair("mfma_kernel", _W(64), "lse") == {"f32": 2 * 64}
+    # the split log-sum-exp: six bf16 products per coordinate, no P . B
+    assert bench.matrix_flops_per_pair("mfma_split_kernel", _W(64), "lse") == {"bf16": 12 * 64}
     # the fused gradient at D = 128 runs 129 signal columns in three chunks
     mx = bench.matrix_flops_per_pair("mfma_split_kernel", _W(128, 1), "sum", "gauss_gradx")
     assert mx == {"bf16": 3 * 6 * 4 * per32 + 192 * (4 + 4 + 1)}

@@ -283,3 +283,36 @@ def test_large_d_knn_values_re_ranked(ctx, D, K, C):
     # the values are the direct-form fp32 distances of the returned indices
     # (a sum of D non-negative terms: relative error below (D + 1) 2^-24)
     assert (np.abs(kd.astype(np.float64) - got) <= (D + 2) * U * got + 1e-30).all()
+
+
+@pytest.mark.parametrize("D", [40, 64, 100, 128])
+@pytest.mark.parametrize("side", [0.97, 1.02])
+def test_split_lse_guard_sides(ctx, D, side):
+    # the Sinkhorn log-sum-exp on the split kernel (KRED_FLAG_FAST, D = 33..128):
+    # at 97% of the split limit it runs there and meets the bar on data where
+    # its rounding is largest; at 102% the fp64 contraction takes it
+    from paper_2004_11127_amd import kred
+    rng = np.random.default_rng(D + 7)
+    M, N = 400, 1500
+    x, y = two_clusters(rng, M, N, D, std=0.3 / np.sqrt(D))
+    g = rng.standard_normal((N, 1)).astype(np.float32)
+    c = side * limit(D, True) / guard_L(x, y, 1.0)
+    eps = LOG2E / c
+    out, name = _profiled(ctx, "sinkhorn", "lse", dev(x), dev(y), dev(g), eps=eps, flags=kred.FLAG_FAST)
+    assert name == ("mfma_f64_kernel" if side > 1 else "mfma_split_kernel")
+    ref, m = oracle.sinkhorn_lse(x, y, g, eps)
+    assert lse_err(out[:, 0], ref, m) <= LSE_TOL
+
+
+def test_lse_d64_data_on_the_split_kernel(ctx):
+    # the lse_d64 workload's data with KRED_FLAG_FAST (as at its full size):
+    # inside the split limit, on the split kernel, at the bar
+    from paper_2004_11127_amd import inputs, kred
+    w = inputs.sinkhorn_lse(M=3000, N=3000, D=64, eps=1.0, seed=3)
+    assert not expect_fp64(64, guard_L(w.x, w.y, LOG2E), split=True)
+    g = w.b.reshape(-1, 1)
+    out, name = _profiled(ctx, "sinkhorn", "lse", dev(w.x), dev(w.y), dev(g), eps=1.0,
+                          flags=kred.FLAG_FAST)
+    assert name == "mfma_split_kernel"
+    ref, m = oracle.sinkhorn_lse(w.x, w.y, g, 1.0)
+    assert lse_err(out[:, 0], ref, m) <= LSE_TOL

@@ -1,4 +1,4 @@
-"""GPU parity of the 32x32-tile split sum kernel (33 <= D <= 128) at every tile count.
+"""GPU parity of the 32x32-tile split kernel (33 <= D <= 128) at every tile count: sums and log-sum-exp.
 
 The kernel walks each column block in 32-column tiles through four sets of
 LDS buffers (the loop unrolled by four, two tiles in flight, the pending
@@ -6,7 +6,8 @@ tile finished one step later with 16 signal columns and in place with 32
 or 64), so a column block of 1 to 9 tiles meets every entry and exit of that
 loop; N not a multiple of 16 or 32 leaves a partial last tile.  Workgroups
 hold 256 rows, so M = 300 leaves a ragged second one.  Same bar as the other
-sum tests: error normalised by sum_j |k_ij b_j| at most 1e-4 against the fp64
+sum and log-sum-exp tests: error normalised by sum_j |k_ij b_j| (sums), or
+absolute in the log domain (log-sum-exp), at most 1e-4 against the fp64
 oracle, and the kernel that ran is asserted.
 """
 import numpy as np
@@ -96,3 +97,76 @@ def test_split_kernel_segments_restart(ctx):
         ref, norm = oracle.ranges_reduce("sum", x, y, b, rr, cp, cr, formula="gauss", sigma=1.0)
         assert norm_err(out, ref, norm) <= SUM_TOL
         assert (out[300:310] == 0).all()   # rows in no cluster
+
+
+# ------------------------------------------------------------- log-sum-exp
+# The Gaussian and Sinkhorn log-sum-exp take the same kernel at D = 33..128
+# (bar: 1e-4 absolute in the log domain, as every LSE test)
+def _lse_data(M, N, D, seed):
+    # uniform in a box of side sqrt(32 / D) (the squared spread of the unit
+    # cube at D = 32), so that the guard's L stays well inside the split
+    # limit at every D here (about 15 against 24 at D = 128)
+    spread = float(np.sqrt(32.0 / D))
+    rng = np.random.default_rng(seed)
+    x = (spread * rng.uniform(size=(M, D))).astype(np.float32)
+    y = (spread * rng.uniform(size=(N, D))).astype(np.float32)
+    y[:, 0] += 0.3
+    g = rng.standard_normal((N, 1)).astype(np.float32)
+    return x, y, g
+
+
+@pytest.mark.parametrize("N", [1, 17, 32, 33, 95, 160, 257, 288])
+@pytest.mark.parametrize("formula,D", [("sinkhorn", 64), ("sinkhorn", 128), ("gauss", 100), ("sinkhorn", 40)])
+def test_split_lse_tile_counts(ctx, formula, D, N):
+    from paper_2004_11127_amd import kred
+    from helpers import LSE_TOL, lse_err
+    M = 300
+    x, y, g = _lse_data(M, N, D, seed=D + N)
+    kw = dict(eps=1.0) if formula == "sinkhorn" else dict(sigma=0.7)
+    ctx.profile_collect()
+    out = host(ctx.run(formula, "lse", dev(x), dev(y), dev(g), col_blocks=1,
+                       flags=kred.FLAG_FAST | kred.FLAG_PROFILE, **kw))
+    assert ctx.profile_collect()[2] == "mfma_split_kernel"
+    ref, m = (oracle.sinkhorn_lse(x, y, g, 1.0) if formula == "sinkhorn"
+              else oracle.kernel_lse("gauss", x, y, g, 0.7))
+    assert lse_err(out[:, 0], ref, m) <= LSE_TOL
+
+
+@pytest.mark.parametrize("C", [0, 2, 8])
+@pytest.mark.parametrize("D", [64, 128])
+def test_split_lse_column_blocks(ctx, D, C):
+    from paper_2004_11127_amd import kred
+    from helpers import LSE_TOL, lse_err
+    M, N = 530, 1100
+    x, y, g = _lse_data(M, N, D, seed=3 * C + D)
+    ctx.profile_collect()
+    out = host(ctx.run("sinkhorn", "lse", dev(x), dev(y), dev(g), eps=0.8, col_blocks=C,
+                       flags=kred.FLAG_FAST | kred.FLAG_PROFILE))
+    assert ctx.profile_collect()[2] == "mfma_split_kernel"
+    ref, m = oracle.sinkhorn_lse(x, y, g, 0.8)
+    assert lse_err(out[:, 0], ref, m) <= LSE_TOL
+
+
+def test_split_lse_segments_and_empty_rows(ctx):
+    # block-sparse: many short segments per cluster; rows in no cluster are -inf
+    from paper_2004_11127_amd import kred
+    from helpers import LSE_TOL, lse_err
+    M, N, D = 600, 1500, 64
+    x, y, g = _lse_data(M, N, D, seed=5)
+    rr = np.array([[0, 260], [260, 300], [310, 600]], dtype=np.int32)
+    rng = np.random.default_rng(12)
+    cuts = np.sort(rng.choice(np.arange(1, N), size=24, replace=False))
+    edges = np.concatenate([[0], cuts, [N]])
+    spans = [(int(edges[k]), int(edges[k + 1])) for k in range(len(edges) - 1)]
+    keep = [[s for k, s in enumerate(spans) if (k + i) % 3 != 0] for i in range(len(rr))]
+    cp = np.cumsum([0] + [len(k) for k in keep]).astype(np.int32)
+    cr = np.array([s for k in keep for s in k], dtype=np.int32)
+    for C in (1, 3):
+        ctx.profile_collect()
+        out = host(ctx.run_ranges("sinkhorn", "lse", dev(x), dev(y), dev(g), dev(rr), dev(cp), dev(cr),
+                                  eps=0.5, col_blocks=C, flags=kred.FLAG_FAST | kred.FLAG_PROFILE))
+        assert ctx.profile_collect()[2] == "mfma_split_kernel"
+        ref, m = oracle.ranges_reduce("lse", x, y, g, rr, cp, cr, eps=0.5)
+        live = np.isfinite(ref)
+        assert lse_err(out[live, 0], ref[live], m[live]) <= LSE_TOL, C
+        assert np.isneginf(out[300:310, 0]).all()
