@@ -49,6 +49,8 @@ CASES = [
     ("gauss", "sum", 64, 16, dict(sigma=1.0, flags=4), (1500, 2500), (500, 600)),      # large D, split bf16 kernel
     ("gauss_gradx", "sum", 40, 1, dict(sigma=1.0), (1200, 2000), (300, 500)),          # large D, signal chunks
     ("sinkhorn", "lse", 48, 1, dict(eps=1.0), (1200, 2000), (300, 500)),
+    ("sinkhorn", "lse", 48, 1, dict(eps=1.0, flags=4), (1200, 2000), (300, 500)),      # large D, split log-sum-exp
+    ("gauss", "sum", 128, 40, dict(sigma=1.0, flags=4), (900, 1300), (300, 400)),      # split, 64 signal columns
     ("gauss", "max", 24, 3, dict(sigma=1.0), (800, 1500), (200, 300)),
 ]
 
