@@ -387,7 +387,7 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   q.wide_limit = !(q.epi == 0 || q.epi == 4 || q.epi == 6 || q.epi == 9) ? -1.0f
                  : (split_sum || split_lse) ? wide_limit_split(D) : wide_limit_f32(D);
   const bool split32 = (split_sum && q.epi == 0) || split_lse;
-  const int rows = split32 ? mfma_split_rows_per_block(q.DP) : mfma_rows_per_block(q.DP, q.KP);
+  const int rows = split32 ? mfma_split_rows_per_block(q.DP, q.epi) : mfma_rows_per_block(q.DP, q.KP);
   const int64_t row_blocks = std::max<int64_t>(1, (M + rows - 1) / rows);
   int C = choose_col_blocks(row_blocks, q.N16, num_cus, p->col_blocks);
   // the split sum kernel with 4 to 7 column blocks: 8, one per XCD (blockIdx
@@ -560,7 +560,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   const bool exact = knn && exact_knn_eligible(p->flags, M, N);
   const bool split = !knn && !ext && exact_eligible(p->flags, M, N) &&
                      (!lse || (pl.epi == 4 && split_lse_dp(pl.DP)));
-  const int64_t rows_wg = split ? mfma_split_rows_per_block(pl.DP) : mfma_rows_per_block(pl.DP, pl.KP);
+  const int64_t rows_wg = split ? mfma_split_rows_per_block(pl.DP, pl.epi) : mfma_rows_per_block(pl.DP, pl.KP);
   const int64_t ybf_bytes = mfma_bf16_bytes(pl, knn, p->flags, M, N);
   if (rg) {   // partials of every chunk (rows outside the clusters read the empty value)
     pl.part_bytes = knn ? align_up((int64_t)4 * pl.C * M * 2 * pl.KP * (int64_t)sizeof(float))

@@ -352,7 +352,7 @@ int mfma_pad_d(int D);               // DP for D > 16 (0 if D > 256)
 int mfma_tile_cols(int DP);          // columns per LDS tile
 int mfma_knn_pad_k(int K);           // list length of the matrix-core arg-K-min kernels
 int mfma_rows_per_block(int DP, int KP);
-int mfma_split_rows_per_block(int DP);   // rows per workgroup of the split sum kernels
+int mfma_split_rows_per_block(int DP, int epi);   // rows per workgroup of the split kernels
 // the padded widths at which the log-sum-exp takes the split kernel (32x32 tiles)
 inline bool split_lse_dp(int DP) { return DP == 64 || DP == 128; }
 int64_t mfma_row_groups(const MfmaArgs& a, int rows);   // row-block slots of the grid
