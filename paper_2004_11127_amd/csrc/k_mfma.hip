@@ -534,9 +534,10 @@ hipError_t launch_split_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   return hipGetLastError();
 }
 
-// ------------------------------------ sums, split bf16 products, 32x32 tiles
-// The same split sum for DP = 64 and 128 with the exponent on
-// v_mfma_f32_32x32x16_bf16: one wave owns 32 rows, and each 32-column tile is
+// ---------------------- sums and log-sum-exp, split bf16 products, 32x32 tiles
+// The same split sum for DP = 64 and 128 (and the Gaussian / Sinkhorn
+// log-sum-exp, EPI 4: a running maximum and rescaled sum per lane instead of
+// P . B) with the exponent on v_mfma_f32_32x32x16_bf16: one wave owns 32 rows, and each 32-column tile is
 // one 32 x 32 block of T, six instructions per 16 coordinates (hh, hm, mh into
 // one chain, mm, hl, lh into the other, both from zero).  The instruction adds
 // its products in groups of 8 exactly as the 16x16x32 form does (in-bounds
@@ -554,8 +555,9 @@ hipError_t launch_split_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
 // rows 0-15 (first register) and rows 16-31 (second).
 // Workgroups of 8 waves (256 rows, two waves per SIMD) halve the y traffic
 // per row against 4-wave ones; the log-sum-exp at DP = 64 (158 VGPRs) runs
-// 4-wave workgroups, three waves per SIMD, instead.  Every part of a tile (y planes, norms, b planes) goes
-// from memory straight into LDS, two tiles ahead, into four sets of buffers
+// 4-wave workgroups, three waves per SIMD, instead.  Every part of a tile
+// (y planes, norms, b planes) goes from memory straight into LDS, two tiles
+// ahead, into four sets of buffers
 // that are distinct arrays indexed statically (the loop is unrolled by 4):
 // the compiler then sees that no read aliases an outstanding direct load and
 // waits for none; the waits are explicit (the newest tile's loads stay in
@@ -632,7 +634,6 @@ void mfma_split_kernel(MfmaArgs a) {
   const int i32 = lane & 31, h = lane >> 5;   // exponent lanes
   const int c = it.c;
   const int64_t rend = it.row_end;
-  const float pad_ny = a.pad_ny;
   const int64_t i0 = it.row0 + wave * 32;
 
   // planes of x[i32][16 ch + 8 h + t]; X = fl32(s (x - m)) formed in fp64 and
