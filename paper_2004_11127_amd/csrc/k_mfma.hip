@@ -221,8 +221,8 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 // three bf16 planes in the matching K order (mfma_pack_kernel), so six products
 // per 32 columns replace eight v_mfma_f32_16x16x4_f32 (48 matrix-core cycles
 // per 16 columns instead of 128).  Wider D keeps the fp32 P . B.
-// DP = 64 and 128 take mfma_split_kernel below (32 x 32 tiles); this kernel
-// serves DP = 32 and 256.
+// DP = 32, 64 and 128 take mfma_split_kernel below (32 x 32 tiles); this
+// kernel serves DP = 256.
 constexpr int split_tile_cols(int DP) { return DP <= 64 ? 64 : (DP <= 128 ? 32 : 16); }
 
 template <int NCH, int RB, int EB, bool SP>
@@ -535,7 +535,7 @@ hipError_t launch_split_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
 }
 
 // ---------------------- sums and log-sum-exp, split bf16 products, 32x32 tiles
-// The same split sum for DP = 64 and 128 (and the Gaussian / Sinkhorn
+// The same split sum for DP = 32, 64 and 128 (and the Gaussian / Sinkhorn
 // log-sum-exp, EPI 4: a running maximum and rescaled sum per lane instead of
 // P . B) with the exponent on v_mfma_f32_32x32x16_bf16: one wave owns 32 rows, and each 32-column tile is
 // one 32 x 32 block of T, six instructions per 16 coordinates (hh, hm, mh into
@@ -555,7 +555,8 @@ hipError_t launch_split_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
 // rows 0-15 (first register) and rows 16-31 (second).
 // Workgroups of 8 waves (256 rows, two waves per SIMD) halve the y traffic
 // per row against 4-wave ones; the log-sum-exp at DP = 64 (158 VGPRs) runs
-// 4-wave workgroups, three waves per SIMD, instead.  Every part of a tile
+// 4-wave workgroups, three waves per SIMD, instead, and so does DP = 32
+// (a tile there is six wave loads).  Every part of a tile
 // (y planes, norms, b planes) goes from memory straight into LDS, two tiles
 // ahead, into four sets of buffers
 // that are distinct arrays indexed statically (the loop is unrolled by 4):
@@ -935,8 +936,9 @@ void mfma_split_kernel(MfmaArgs a) {
 
 // waves per workgroup of mfma_split_kernel: 8 (two per SIMD); the
 // log-sum-exp at DP = 64 holds 158 VGPRs and runs three per SIMD in
-// workgroups of 4 (lse_d64: 4.5% faster than with 8)
-constexpr int split32_waves(int NC, int EPI) { return (EPI == 4 && NC <= 4) ? 4 : 8; }
+// workgroups of 4 (lse_d64: 4.5% faster than with 8), and DP = 32 takes
+// workgroups of 4 as well (the whole tile is six wave loads)
+constexpr int split32_waves(int NC, int EPI) { return (NC <= 2 || (EPI == 4 && NC <= 4)) ? 4 : 8; }
 
 template <int NC, bool SP>
 hipError_t launch_split32_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
@@ -1028,7 +1030,7 @@ int mfma_rows_per_block(int DP, int KP) {
 }
 
 int mfma_split_rows_per_block(int DP, int epi) {
-  if (DP == 64 || DP == 128) return 32 * (epi == 4 ? split32_waves(DP / 16, 4) : split32_waves(DP / 16, 0));
+  if (DP == 32 || DP == 64 || DP == 128) return 32 * (epi == 4 ? split32_waves(DP / 16, 4) : split32_waves(DP / 16, 0));
   return mfma_rows_per_block(DP, 0);
 }
 
@@ -1263,7 +1265,7 @@ hipError_t launch_mfma_split(const MfmaArgs& a, hipStream_t s) {
   const int rows = mfma_split_rows_per_block(a.DP, a.epi);
   const dim3 grid((unsigned)(mfma_row_groups(a, rows) * a.C));
   switch (a.DP) {
-    case 32: return a.nr > 0 ? launch_split_n<1, true>(a, grid, s) : launch_split_n<1, false>(a, grid, s);
+    case 32: return a.nr > 0 ? launch_split32_n<2, true>(a, grid, s) : launch_split32_n<2, false>(a, grid, s);
     case 64: return a.nr > 0 ? launch_split32_n<4, true>(a, grid, s) : launch_split32_n<4, false>(a, grid, s);
     case 128: return a.nr > 0 ? launch_split32_n<8, true>(a, grid, s) : launch_split32_n<8, false>(a, grid, s);
     case 256: return a.nr > 0 ? launch_split_n<8, true>(a, grid, s) : launch_split_n<8, false>(a, grid, s);

@@ -382,7 +382,7 @@ bool make_mplan(kred_formula f, kred_reduction r, const kred_params* p, int64_t 
   // (sums take the split bf16 kernel where it is eligible, with its own bound)
   const bool split_sum = q.epi <= 2 && exact_eligible(p->flags, M, N);
   // the Gaussian and Sinkhorn log-sum-exp on the 32x32-tile split kernel (DP
-  // 64 and 128), under the split contraction's bound
+  // 32, 64 and 128), under the split contraction's bound
   const bool split_lse = q.epi == 4 && split_lse_dp(q.DP) && exact_eligible(p->flags, M, N);
   q.wide_limit = !(q.epi == 0 || q.epi == 4 || q.epi == 6 || q.epi == 9) ? -1.0f
                  : (split_sum || split_lse) ? wide_limit_split(D) : wide_limit_f32(D);

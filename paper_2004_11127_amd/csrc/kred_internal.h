@@ -354,7 +354,7 @@ int mfma_knn_pad_k(int K);           // list length of the matrix-core arg-K-min
 int mfma_rows_per_block(int DP, int KP);
 int mfma_split_rows_per_block(int DP, int epi);   // rows per workgroup of the split kernels
 // the padded widths at which the log-sum-exp takes the split kernel (32x32 tiles)
-inline bool split_lse_dp(int DP) { return DP == 64 || DP == 128; }
+inline bool split_lse_dp(int DP) { return DP == 32 || DP == 64 || DP == 128; }
 int64_t mfma_row_groups(const MfmaArgs& a, int rows);   // row-block slots of the grid
 
 struct FastPackArgs {

@@ -1,11 +1,12 @@
-"""GPU parity of the 32x32-tile split kernel (33 <= D <= 128) at every tile count: sums and log-sum-exp.
+"""GPU parity of the 32x32-tile split kernel (17 <= D <= 128) at every tile count: sums and log-sum-exp.
 
 The kernel walks each column block in 32-column tiles through four sets of
 LDS buffers (the loop unrolled by four, two tiles in flight, the pending
 tile finished one step later with 16 signal columns and in place with 32
 or 64), so a column block of 1 to 9 tiles meets every entry and exit of that
 loop; N not a multiple of 16 or 32 leaves a partial last tile.  Workgroups
-hold 256 rows, so M = 300 leaves a ragged second one.  Same bar as the other
+hold 256 rows (128 at D <= 32 and for the log-sum-exp at D <= 64), so M = 300
+leaves a ragged last one.  Same bar as the other
 sum and log-sum-exp tests: error normalised by sum_j |k_ij b_j| (sums), or
 absolute in the log domain (log-sum-exp), at most 1e-4 against the fp64
 oracle, and the kernel that ran is asserted.
@@ -37,8 +38,8 @@ def _data(M, N, D, E, seed):
 
 
 # (D, E): 16 signal columns (pipelined), 32 and 64 (finished in place), E
-# below a block; D = 128 and 64 (the two padded widths), and odd D
-WIDTHS = [(128, 16), (128, 40), (100, 64), (64, 16), (64, 20), (40, 3)]
+# below a block; D = 128, 64 and 32 (the three padded widths), and odd D
+WIDTHS = [(128, 16), (128, 40), (100, 64), (64, 16), (64, 20), (40, 3), (32, 16), (32, 64), (24, 1)]
 # columns: 1 to 9 tiles, full and partial last tiles
 COLS = [1, 17, 32, 33, 64, 95, 128, 129, 160, 200, 257, 288]
 
@@ -59,7 +60,7 @@ def test_split_kernel_tile_counts(ctx, D, E, N):
 
 
 @pytest.mark.parametrize("C", [2, 3, 8])
-@pytest.mark.parametrize("D,E", [(128, 16), (128, 64), (64, 16)])
+@pytest.mark.parametrize("D,E", [(128, 16), (128, 64), (64, 16), (32, 16)])
 def test_split_kernel_column_blocks(ctx, D, E, C):
     # several column blocks (partials combined in a second pass), each with a
     # few tiles; C = 8 is the one-block-per-XCD choice
@@ -100,7 +101,7 @@ def test_split_kernel_segments_restart(ctx):
 
 
 # ------------------------------------------------------------- log-sum-exp
-# The Gaussian and Sinkhorn log-sum-exp take the same kernel at D = 33..128
+# The Gaussian and Sinkhorn log-sum-exp take the same kernel at D = 17..128
 # (bar: 1e-4 absolute in the log domain, as every LSE test)
 def _lse_data(M, N, D, seed):
     # uniform in a box of side sqrt(32 / D) (the squared spread of the unit
@@ -116,7 +117,8 @@ def _lse_data(M, N, D, seed):
 
 
 @pytest.mark.parametrize("N", [1, 17, 32, 33, 95, 160, 257, 288])
-@pytest.mark.parametrize("formula,D", [("sinkhorn", 64), ("sinkhorn", 128), ("gauss", 100), ("sinkhorn", 40)])
+@pytest.mark.parametrize("formula,D", [("sinkhorn", 64), ("sinkhorn", 128), ("gauss", 100), ("sinkhorn", 40),
+                                           ("sinkhorn", 32), ("gauss", 20)])
 def test_split_lse_tile_counts(ctx, formula, D, N):
     from paper_2004_11127_amd import kred
     from helpers import LSE_TOL, lse_err
@@ -133,7 +135,7 @@ def test_split_lse_tile_counts(ctx, formula, D, N):
 
 
 @pytest.mark.parametrize("C", [0, 2, 8])
-@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("D", [32, 64, 128])
 def test_split_lse_column_blocks(ctx, D, C):
     from paper_2004_11127_amd import kred
     from helpers import LSE_TOL, lse_err
