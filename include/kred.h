@@ -89,7 +89,7 @@ typedef enum kred_status {
                                  the exact bf16 one */
 #define KRED_FLAG_FAST 4u     /* D <= 4: use the matrix-core exponent whatever the problem size (the
                                  accuracy guard still falls back to the direct form).  D > 16
-                                 sums (and LSE at 33 <= D <= 128): the split bf16 products whatever
+                                 sums (and LSE at 17 <= D <= 128): the split bf16 products whatever
                                  the size (same guard).  D > 16
                                  arg-K-min: consider the exact bf16 kernel whatever the size (it
                                  runs only when every coordinate is an integer with |v| <= 256 and
@@ -170,7 +170,7 @@ kred_status kred_destroy(kred_ctx* ctx);
  * guard (computed on the device, no host synchronisation): with L = c (max_i
  * |x_i - m|^2 + max_j |y_j - m|^2), the Gaussian and Sinkhorn forms use fp32
  * products (KRED_FLAG_DIRECT or below 2^28 pairs; error in the exponent below
- * (D + 10) 2^-24 L) or, for the sums and (at 33 <= D <= 128) the LSE, split
+ * (D + 10) 2^-24 L) or, for the sums and (at 17 <= D <= 128) the LSE, split
  * bf16 products (error below (D / 2 + 18) 2^-24 L; from 2^28 pairs, or with
  * KRED_FLAG_FAST) while that bound stays within 1.2e-4 in log2 units,
  * and the fp64 contraction beyond it; the Laplacian forms and the squared
