@@ -397,7 +397,8 @@ def cpu_baseline(w, formula, reduction, out_gpu, seconds, pattern=None):
             return val, scale
         return oracle.kernel_sum(formula, w.x, w.y, w.b, sigma=w.sigma, rows=rows)
 
-    probe = inputs.sample_rows(w.M, min(w.M, 32), seed=777)
+    # a probe large enough that thread start-up does not dominate its time
+    probe = inputs.sample_rows(w.M, min(w.M, 256), seed=777)
     t0 = time.perf_counter()
     run(probe)
     t_probe = time.perf_counter() - t0
