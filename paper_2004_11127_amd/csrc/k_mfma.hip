@@ -595,7 +595,7 @@ constexpr int split32_min_loads(int yw, int bo, int nwv) {
   return best;
 }
 
-template <int NC, int EB, int EPI, int NWV, bool SP>
+template <int NC, int EB, int EPI, int NWV, bool SP, bool XC = false>
 __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV == 4 ? 3 : 2, NWV == 4 ? 3 : 2)))
 void mfma_split_kernel(MfmaArgs a) {
   // NWV waves per workgroup, 32 rows each
@@ -615,6 +615,10 @@ void mfma_split_kernel(MfmaArgs a) {
   // direct loads per wave and tile, the fewest over the waves (y, b, norms)
   constexpr int VKEEP = split32_min_loads(TU / 64, BO, NWV);
   static_assert(VKEEP >= 1 && VKEEP <= 15, "wait count");
+  // XC: one more signal column (fp32, a.xb) summed per lane on the vector ALU;
+  // its tile of 32 values sits after the norms in the same buffer
+  static_assert(!XC || (!LSE && EB == 4 && NWV >= 2), "extra column with 64 signal columns");
+  constexpr int NQ = XC ? TJ / 2 : TJ / 4;   // float4 of a slot's norms (and extra column)
 
   // four buffers of a tile: y planes as in HBM, uint4 q of column c at
   // position q ^ (c & (PU - 1)) within its plane (16 consecutive columns on
@@ -622,9 +626,10 @@ void mfma_split_kernel(MfmaArgs a) {
   // distinct arrays, indexed statically, so that the compiler knows that the
   // direct loads into one buffer never alias the reads of another
   __shared__ uint4 ys0[TU], ys1[TU], ys2[TU], ys3[TU];
-  __shared__ float4 ns0[TJ / 4], ns1[TJ / 4], ns2[TJ / 4], ns3[TJ / 4];
+  __shared__ float4 ns0[NQ], ns1[NQ], ns2[NQ], ns3[NQ];
   __shared__ uint4 bq0[BQ], bq1[BQ], bq2[BQ], bq3[BQ];
 
+  if (a.xskip) return;   // (summed with the previous launch)
   if (wide64(a.spread, a.wide_c, a.wide_limit)) return;   // the fp64 contraction does the work
   const MItem it = mitem<SP>(a, 32 * NWV);
   if (!it.live) return;
@@ -687,7 +692,7 @@ void mfma_split_kernel(MfmaArgs a) {
   // loaded 16-column blocks reads a padding norm), the b planes (the row
   // padding slots read any b), and the y planes (a column past the loaded
   // blocks reads a copy of the last loaded one: finite, removed by its norm)
-  auto fetch = [&](uint4 (&yd)[TU], float4 (&nd)[TJ / 4], uint4 (&bd)[BQ], int64_t jt, int64_t lo,
+  auto fetch = [&](uint4 (&yd)[TU], float4 (&nd)[NQ], uint4 (&bd)[BQ], int64_t jt, int64_t lo,
                    int64_t hi) __attribute__((always_inline)) {
     const int ncol = (int)min((int64_t)TJ, ((hi + 15) & ~(int64_t)15) - jt);
     if (wave == NWV - 1 && lane < TJ) {
@@ -695,6 +700,15 @@ void mfma_split_kernel(MfmaArgs a) {
       const bool live = SP ? (col >= lo && col < hi) : (lane < ncol);
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.ny + (live ? col : a.N16)),
                                        (__attribute__((address_space(3))) void*)(&nd[0]), 4, 0, 0);
+    }
+    if constexpr (XC) {
+      // the extra column's values (a masked column reads the zero at N16)
+      if (wave == NWV - 2 && lane < TJ) {
+        const int64_t col = jt + lane;
+        const bool live = SP ? (col >= lo && col < hi) : (lane < ncol);
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.xb + (live ? col : a.N16)),
+                                         (__attribute__((address_space(3))) void*)(&nd[TJ / 4]), 4, 0, 0);
+      }
     }
     const uint4* bsrc = LSE ? nullptr : reinterpret_cast<const uint4*>(a.bpk) + (jt / 32) * (12 * W);
 #pragma unroll
@@ -759,7 +773,8 @@ void mfma_split_kernel(MfmaArgs a) {
   // units) and the sum ls of 2^(s - lm), rescaled when lm moves (as the fp32
   // kernel; lm starts finite, so an empty start never forms inf - inf)
   float lm = -3.0e38f, ls = 0.0f;
-  auto finish = [&](const float4 (&nd)[TJ / 4], const uint4 (&bd)[BQ], const f16v& ap)
+  float xacc = 0.0f;   // the extra column: this lane's share of its row's sum
+  auto finish = [&](const float4 (&nd)[NQ], const uint4 (&bd)[BQ], const f16v& ap)
                     __attribute__((always_inline)) {
     if constexpr (LSE) {
       float sv[16];
@@ -788,6 +803,7 @@ void mfma_split_kernel(MfmaArgs a) {
     }
     // T = fl(fl(acc + acc2) + fl(nx + ny)), p = 2^T; column 8 q + 4 h + r
     float p[16];
+    float xq[4];   // XC: p times the extra column over each group of 4 columns
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const float4 nyv = nd[2 * q + h];
@@ -795,7 +811,16 @@ void mfma_split_kernel(MfmaArgs a) {
       p[4 * q + 1] = __builtin_amdgcn_exp2f(ap[4 * q + 1] + (nx + nyv.y));
       p[4 * q + 2] = __builtin_amdgcn_exp2f(ap[4 * q + 2] + (nx + nyv.z));
       p[4 * q + 3] = __builtin_amdgcn_exp2f(ap[4 * q + 3] + (nx + nyv.w));
+      if constexpr (XC) {
+        const float4 xv = nd[TJ / 4 + 2 * q + h];
+        xq[q] = __builtin_fmaf(p[4 * q + 3], xv.w,
+                               __builtin_fmaf(p[4 * q + 2], xv.z,
+                                              __builtin_fmaf(p[4 * q + 1], xv.y, p[4 * q + 0] * xv.x)));
+      }
     }
+    // the tile's 16 columns into the running sum once (one rounding per tile,
+    // as P . B)
+    if constexpr (XC) xacc += (xq[0] + xq[1]) + (xq[2] + xq[3]);
     // U = q 0, 2 and V = q 1, 3 -> rows 0-15 (u = 0) and 16-31 (u = 1)
     float pr[2][8];
 #pragma unroll
@@ -849,8 +874,8 @@ void mfma_split_kernel(MfmaArgs a) {
   constexpr bool PIPE = EB == 1;
   f16v accp;   // fl(acc + acc2) of the pending tile
   auto step = [&](int t, int ntiles, int64_t base, int64_t a0, int64_t a1, const uint4 (&yc)[TU],
-                  const float4 (&nc)[TJ / 4], const uint4 (&bc)[BQ], const float4 (&nf)[TJ / 4],
-                  const uint4 (&bf)[BQ], uint4 (&yn)[TU], float4 (&nn)[TJ / 4],
+                  const float4 (&nc)[NQ], const uint4 (&bc)[BQ], const float4 (&nf)[NQ],
+                  const uint4 (&bf)[BQ], uint4 (&yn)[TU], float4 (&nn)[NQ],
                   uint4 (&bn)[BQ]) __attribute__((always_inline)) {
     const bool more = t + 2 < ntiles;
     if (more) fetch(yn, nn, bn, base + (int64_t)(t + 2) * TJ, a0, a1);
@@ -915,6 +940,15 @@ void mfma_split_kernel(MfmaArgs a) {
     }
     return;
   }
+  if constexpr (XC) {
+    // the row's two lanes (h = 0, 1) hold halves of its extra-column sum
+    const float xs = xacc + __shfl_xor(xacc, 32);
+    const int64_t row = i0 + i32;
+    if (h == 0 && row < rend) {
+      if (a.C == 1) a.xout[row] = xs;
+      else a.xpart[(int64_t)c * a.M + row] = xs;
+    }
+  }
   // lane holds out[i = 16 u + 4 g + r][e = 16 eb + li]
   const int Ec = min(W, a.E - a.e0);
 #pragma unroll
@@ -952,7 +986,10 @@ hipError_t launch_split32_n(const MfmaArgs& a, dim3 grid, hipStream_t s) {
   switch (a.EB) {
     case 1: hipLaunchKernelGGL((mfma_split_kernel<NC, 1, 0, NW, SP>), grid, dim3(64 * NW), 0, s, a); break;
     case 2: hipLaunchKernelGGL((mfma_split_kernel<NC, 2, 0, NW, SP>), grid, dim3(64 * NW), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((mfma_split_kernel<NC, 4, 0, NW, SP>), grid, dim3(64 * NW), 0, s, a); break;
+    case 4:
+      if (a.xb) hipLaunchKernelGGL((mfma_split_kernel<NC, 4, 0, NW, SP, true>), grid, dim3(64 * NW), 0, s, a);
+      else hipLaunchKernelGGL((mfma_split_kernel<NC, 4, 0, NW, SP>), grid, dim3(64 * NW), 0, s, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

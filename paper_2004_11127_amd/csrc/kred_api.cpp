@@ -530,10 +530,22 @@ int64_t mfma_bf16_bytes(const MPlan& pl, bool knn, uint32_t flags, int64_t M, in
   return align_up(pl.N16 * (knn ? 1 : 3) * pl.DP * (int64_t)sizeof(uint16_t));
 }
 
+// One more signal column of a Gaussian sum with 64 columns on the 32x32-tile
+// split kernel (summed there on the vector ALU): xb its values (N16 + 1, zero
+// from N on), xout its output column (M floats).  skip: the call that would
+// sum that column alone, after such a call with the same arguments; its
+// split kernel returns at once and it runs with one column block, so that
+// only the fp64 contraction (when the guard picks it) writes xout.
+struct XCol {
+  const float* xb = nullptr;
+  float* xout = nullptr;
+  bool skip = false;
+};
+
 kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred_params* p,
                      int64_t M, int64_t N, int32_t D, int32_t E, const float* x, const float* y,
                      const float* b, void* out, hipStream_t s, int kvalues,
-                     const Ranges* rg = nullptr) {
+                     const Ranges* rg = nullptr, const XCol* xcol = nullptr) {
   kred_params pr;
   if (rg && p->col_blocks == 0) {
     // chunks of each cluster's columns: enough workgroups for every CU, the
@@ -561,6 +573,13 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   const bool split = !knn && !ext && exact_eligible(p->flags, M, N) &&
                      (!lse || (pl.epi == 4 && split_lse_dp(pl.DP)));
   const int64_t rows_wg = split ? mfma_split_rows_per_block(pl.DP, pl.epi) : mfma_rows_per_block(pl.DP, pl.KP);
+  // the extra column needs the 32x32-tile split sum with 64 columns (or, to
+  // skip it, one column block)
+  const bool xon = xcol && xcol->xb;
+  if (xon && !(split && pl.epi == 0 && pl.DP <= 128 && pl.EB == 4)) return KRED_ERR_UNSUPPORTED;
+  if (xcol && xcol->skip && (!split || pl.epi != 0 || pl.DP > 128 || pl.C != 1))
+    return KRED_ERR_UNSUPPORTED;
+  const int64_t xpart_bytes = (xon && pl.C > 1) ? align_up((int64_t)pl.C * M * (int64_t)sizeof(float)) : 0;
   const int64_t ybf_bytes = mfma_bf16_bytes(pl, knn, p->flags, M, N);
   if (rg) {   // partials of every chunk (rows outside the clusters read the empty value)
     pl.part_bytes = knn ? align_up((int64_t)4 * pl.C * M * 2 * pl.KP * (int64_t)sizeof(float))
@@ -581,7 +600,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   const kred_status gs = buffer(ctx, BUF_SCRATCH,
                                 (size_t)(pl.yop_bytes + pl.ny_bytes + pl.b_bytes + pl.part_bytes +
                                          ybf_bytes + bstart_bytes + cen_bytes + sg_bytes +
-                                         bstart64_bytes), &sp);
+                                         bstart64_bytes + xpart_bytes), &sp);
   if (gs != KRED_OK) return gs;
   void* gp = nullptr;
   if (exact) {
@@ -611,6 +630,9 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
                         : reinterpret_cast<SpreadGuard*>(reinterpret_cast<char*>(cen) + cen_bytes);
   int* bstart64 = bstart64_bytes ? reinterpret_cast<int*>(reinterpret_cast<char*>(sg) + sg_bytes)
                                  : nullptr;
+  float* xpart = xpart_bytes ? reinterpret_cast<float*>(reinterpret_cast<char*>(sg) + sg_bytes +
+                                                        bstart64_bytes)
+                             : nullptr;
   const float wide_c = (float)(pl.sc64 * pl.sc64);
   if (cen && launch_centre(y, N, D, cen, s) != hipSuccess) return KRED_ERR_HIP;
   if (sg && launch_spread(x, M, y, N, D, cen, sg, s) != hipSuccess) return KRED_ERR_HIP;
@@ -633,6 +655,7 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
     if (!knn && !lse && !ext && pl.C > 1 &&
         launch_fill(part, (int64_t)pl.C * M * pl.W, 0.0f, s) != hipSuccess)
       return KRED_ERR_HIP;
+    if (xpart && launch_fill(xpart, (int64_t)pl.C * M, 0.0f, s) != hipSuccess) return KRED_ERR_HIP;
   }
 
   MfmaPackArgs pa{};
@@ -701,6 +724,12 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
   ma.wide_c = wide_c;
   ma.wide_limit = pl.wide_limit;
   ma.xscale64 = pl.sc64;
+  if (xon) {
+    ma.xb = xcol->xb;
+    ma.xout = xcol->xout;
+    ma.xpart = xpart;
+  }
+  ma.xskip = (xcol && xcol->skip) ? 1 : 0;
   if (rg) {
     ma.nr = rg->nr;
     ma.rr = rg->rr;
@@ -806,6 +835,13 @@ kred_status run_mfma(kred_ctx* ctx, kred_formula f, kred_reduction r, const kred
       ca.rD = D;
     }
     if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
+    if (xpart) {   // the extra column's partials, the same sum
+      ca.E = 1;
+      ca.EP = 1;
+      ca.part = xpart;
+      ca.out = xcol->xout;
+      if (launch_combine(ca, s) != hipSuccess) return KRED_ERR_HIP;
+    }
   }
   return KRED_OK;
 }
@@ -835,7 +871,16 @@ int64_t gradx_wide_bytes(int64_t M, int64_t N, int32_t D, int32_t E = 1) {
   const int64_t W = (int64_t)E * (D + 1);
   return align_up((int64_t)D * (int64_t)sizeof(float)) +
          align_up(N * std::min<int64_t>(64, W) * (int64_t)sizeof(float)) +
-         align_up(M * W * (int64_t)sizeof(float));
+         align_up(M * W * (int64_t)sizeof(float)) +
+         align_up(((N + 15) / 16 * 16 + 16) * (int64_t)sizeof(float));
+}
+
+// W = 64 q + 1 signal columns on the 32x32-tile split kernel: the last column
+// rides with the first 64 (summed on the vector ALU) instead of a launch of
+// its own
+bool gradx_extra_col(uint32_t flags, int64_t M, int64_t N, int32_t D, int32_t E) {
+  const int64_t W = (int64_t)E * (D + 1);
+  return W > 64 && W % 64 == 1 && exact_eligible(flags, M, N) && mfma_pad_d(D) <= 128;
 }
 
 // Gaussian x-gradients for 16 < D <= 256 (validated, M, N > 0) as one Gaussian
@@ -856,14 +901,33 @@ kred_status run_gradx_wide(kred_ctx* ctx, const kred_params* p, int64_t M, int64
   float* sig = reinterpret_cast<float*>(base + align_up((int64_t)D * (int64_t)sizeof(float)));
   float* T = reinterpret_cast<float*>(reinterpret_cast<char*>(sig) +
                                       align_up(N * std::min(64, W) * (int64_t)sizeof(float)));
+  float* xsig = reinterpret_cast<float*>(reinterpret_cast<char*>(T) +
+                                         align_up(M * W * (int64_t)sizeof(float)));
+  const int64_t N16 = (N + 15) / 16 * 16;
   // rows outside every cluster read zero sums (a zero value and gradient)
   if (rg && launch_fill(T, M * W, 0.0f, s) != hipSuccess) return KRED_ERR_HIP;
   if (launch_centre(y, N, D, m, s) != hipSuccess) return KRED_ERR_HIP;
+  const bool xc = gradx_extra_col(p->flags, M, N, D, E);
+  XCol xadd, xskip;
+  kred_params p1 = *p;   // the last column's own call, when it rides with the first
+  if (xc) {
+    if (launch_gradx_signal(y, b, N, D, E, m, W - 1, 1, xsig, s) != hipSuccess ||
+        launch_fill(xsig + N, N16 + 16 - N, 0.0f, s) != hipSuccess)
+      return KRED_ERR_HIP;
+    xadd.xb = xsig;
+    xadd.xout = T + (int64_t)(W - 1) * M;
+    xskip.skip = true;
+    p1.col_blocks = 1;
+  }
   for (int c0 = 0; c0 < W; c0 += 64) {
     const int Ec = std::min(64, W - c0);
-    if (launch_gradx_signal(y, b, N, D, E, m, c0, Ec, sig, s) != hipSuccess) return KRED_ERR_HIP;
-    const kred_status st = run_mfma(ctx, KRED_F_GAUSS, KRED_R_SUM, p, M, N, D, Ec, x, y, sig,
-                                    T + (int64_t)c0 * M, s, 0, rg);
+    const bool last1 = xc && c0 == W - 1;
+    if (!last1 && launch_gradx_signal(y, b, N, D, E, m, c0, Ec, sig, s) != hipSuccess)
+      return KRED_ERR_HIP;
+    // (the skipped call's signal: the same column, already in xsig)
+    const kred_status st = run_mfma(ctx, KRED_F_GAUSS, KRED_R_SUM, last1 ? &p1 : p, M, N, D, Ec, x,
+                                    y, last1 ? xsig : sig, T + (int64_t)c0 * M, s, 0, rg,
+                                    !xc ? nullptr : c0 == 0 ? &xadd : last1 ? &xskip : nullptr);
     if (st != KRED_OK) return st;
   }
   const double sg = (double)p->sigma;
@@ -1475,11 +1539,13 @@ int64_t scratch_need(kred_formula f, kred_reduction r, const kred_params* p, int
     if (!make_mplan(wide ? KRED_F_GAUSS : f, r, p, M, N, D, wide ? std::min(64, D + 1) : E,
                     num_cus, &mp))
       return -1;
+    const bool xc = wide && gradx_extra_col(p->flags, M, N, D, 1);
     return mp.yop_bytes + mp.ny_bytes + mp.b_bytes + mp.part_bytes +
            mfma_bf16_bytes(mp, r == KRED_R_ARGKMIN, p->flags, M, N) +
            (r == KRED_R_ARGKMIN ? 0 : align_up((int64_t)D * (int64_t)sizeof(float)) +
                                           align_up(sizeof(SpreadGuard))) +
-           (wide ? gradx_wide_bytes(M, N, D) : 0);
+           (wide ? gradx_wide_bytes(M, N, D) : 0) +
+           ((xc && mp.C > 1) ? align_up((int64_t)mp.C * M * (int64_t)sizeof(float)) : 0);
   }
   const int epi = fast_epi(f, r, M, N, D, E, p->flags, p->K);
   Plan pl;

@@ -328,6 +328,15 @@ struct MfmaArgs {
   const SpreadGuard* spread;   // the guard choosing the fp32 or the fp64 contraction (null: fp32)
   float wide_c, wide_limit;    // c of the prescale, and the limit on L
   double xscale64;             // the row prescale in fp64 (fp64 contraction)
+  // one more signal column summed on the vector ALU by the 32x32-tile split
+  // sum with 64 columns: its fp32 values per column (N16 + 1 of them, zero
+  // from N on), the output column (M floats) and its C x M partials; xskip:
+  // the split kernel returns at once (that column was summed with the
+  // previous launch; the fp64 contraction still runs when the guard picks it)
+  const float* xb;
+  float* xout;
+  float* xpart;
+  int xskip;
 };
 hipError_t launch_mfma(const MfmaArgs& a, hipStream_t s);
 // The same reductions with the contraction in fp64 (runs only when the guard

@@ -127,3 +127,72 @@ def test_backward_ranges_large_d(ctx, E):
     assert norm_err(host(gx), rx, nx) <= SUM_TOL
     assert norm_err(host(gy), ry, ny) <= SUM_TOL
     assert norm_err(host(gb), rb, nb) <= SUM_TOL
+
+
+# With 64 q + 1 signal columns on the 32x32-tile split kernel (D + 1 = 65 or
+# 129), the last column is summed on the vector ALU by the first launch; its
+# own call then only lets the fp64 contraction run when the guard picks it
+@pytest.mark.parametrize("C", [1, 2, 8])
+@pytest.mark.parametrize("M,N,D", [(700, 1500, 64), (520, 1100, 128), (300, 65, 64)])
+def test_gradx_last_column_with_the_first_launch(ctx, M, N, D, C):
+    from paper_2004_11127_amd import kred
+    x, y, b = _data(D + C + N, M, N, D, offset=1.5)
+    for _ in range(2):   # the second call finds the first one's partials
+        ctx.profile_collect()
+        out = host(ctx.run("gauss_gradx", "sum", dev(x), dev(y), dev(b), sigma=1.0, col_blocks=C,
+                           flags=kred.FLAG_FAST | kred.FLAG_PROFILE))
+        assert ctx.profile_collect()[2] == "mfma_split_kernel"
+        ref, norm = oracle.gauss_gradx(x, y, b, 1.0)
+        assert norm_err(out, ref, norm) <= SUM_TOL
+        # the last coordinate's gradient comes from the extra column alone
+        assert norm_err(out[:, -1:], ref[:, -1:], norm[:, -1:]) <= SUM_TOL
+
+
+def test_vjp_last_column_with_the_first_launch(ctx):
+    # E (D + 1) = 3 x 43 = 129 signal columns: the vector-Jacobian product
+    from paper_2004_11127_amd import kred
+    M, N, D, E = 400, 900, 42, 3
+    x, y, b = _data(5, M, N, D, offset=0.5, E=E)
+    e = np.random.default_rng(6).standard_normal((M, E)).astype(np.float32)
+    gx, gy, gb = ctx.gauss_backward(dev(x), dev(y), dev(b), dev(e), sigma=1.0, flags=kred.FLAG_FAST)
+    ref, norm = oracle.gauss_vjp(x, y, b, e, 1.0)
+    assert norm_err(host(gx), ref, norm) <= SUM_TOL
+    ref, norm = oracle.gauss_vjp(y, x, e, b, 1.0)
+    assert norm_err(host(gy), ref, norm) <= SUM_TOL
+
+
+def test_gradx_last_column_ranges(ctx):
+    # block-sparse, D = 64: segments restart the extra column's buffers too;
+    # rows in no cluster stay zero
+    from paper_2004_11127_amd import kred
+    from test_gpu_ranges import random_pattern
+    rng = np.random.default_rng(9)
+    M, N, D = 900, 1400, 64
+    x, y, b = _data(8, M, N, D, offset=1.0)
+    rows, ptr, cr = random_pattern(rng, M, N, 10, 8)
+    for C in (1, 3):
+        out = host(ctx.run_ranges("gauss_gradx", "sum", dev(x), dev(y), dev(b), dev(rows), dev(ptr),
+                                  dev(cr), sigma=1.0, col_blocks=C, flags=kred.FLAG_FAST))
+        ref, norm = oracle.ranges_reduce("gradx", x, y, b, rows, ptr, cr, sigma=1.0)
+        assert norm_err(out, ref, norm) <= SUM_TOL, C
+        assert (out[norm.sum(1) == 0] == 0).all()
+
+
+@pytest.mark.parametrize("C", [1, 4])
+def test_gradx_last_column_beyond_the_guard(ctx, C):
+    # data past the split kernel's limit: the fp64 contraction takes every
+    # launch, the last column's own call included
+    from paper_2004_11127_amd import kred
+    from test_gpu_large_d_guard import LOG2E, guard_L, limit, two_clusters
+    rng = np.random.default_rng(31)
+    M, N, D = 300, 800, 64
+    x, y = two_clusters(rng, M, N, D, std=0.3 / np.sqrt(D))
+    b = rng.standard_normal((N, 1)).astype(np.float32)
+    c = 1.05 * limit(D, True) / guard_L(x, y, 1.0)
+    sigma = float(np.sqrt(LOG2E / (2 * c)))
+    ctx.profile_collect()
+    out = host(ctx.run("gauss_gradx", "sum", dev(x), dev(y), dev(b), sigma=sigma, col_blocks=C,
+                       flags=kred.FLAG_FAST | kred.FLAG_PROFILE))
+    assert ctx.profile_collect()[2] == "mfma_f64_kernel"
+    ref, norm = oracle.gauss_gradx(x, y, b, sigma)
+    assert norm_err(out, ref, norm) <= SUM_TOL
