@@ -51,8 +51,9 @@ WORKLOADS = {
     "c4": ("highdim_gauss", dict(M=200_000, N=200_000, D=128, E=16, sigma=1.0), "gauss", "sum",
            291, "mfma", "gaussian kernel sum, N(0, I/128), 2e5 x 2e5, D=128, E=16"),
     # the fused value + x-gradient at D = 128: one Gaussian sum with D + 1 = 129
-    # signal columns [b, b (y - m)] on the matrix cores (three launches of up to
-    # 64 columns); 2D + 3 flops for the exponent and 2 (D + 1) for the sums
+    # signal columns [b, b (y - m)] on the matrix cores (two launches of 64
+    # columns, the first also summing the 129th on the vector ALU); 2D + 3
+    # flops for the exponent and 2 (D + 1) for the sums
     "gradx_d128": ("highdim_gauss", dict(M=200_000, N=200_000, D=128, E=1, sigma=1.0),
                    "gauss_gradx", "sum", 2 * 128 + 3 + 2 * 129, "mfma",
                    "gaussian kernel sum + x-gradient (fused), N(0, I/128), 2e5 x 2e5, D=128"),
@@ -131,6 +132,10 @@ def matrix_flops_per_pair(kernel, w, reduction, formula=None):
         if reduction == "lse":            # the log-sum-exp has no P . B
             return {"bf16": 12 * dp}
         if dp <= 128:                     # P . B: 6 bf16 16x16x32 products per 32 x 16 pairs
+            if len(widths) > 1 and widths[-1] == 1:
+                # a last single column is summed on the vector ALU by the first
+                # launch (its own launch returns at once)
+                ebs = ebs[:-1]
             return {"bf16": 12 * dp * len(ebs) + sum(192 * eb for eb in ebs)}
         return {"bf16": 12 * dp * len(ebs), "f32": sum(32 * eb for eb in ebs)}
     if kernel == "mfma_kernel":

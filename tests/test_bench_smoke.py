@@ -96,9 +96,13 @@ def test_matrix_work_per_pair_follows_the_mfma_shapes():
     assert bench.matrix_flops_per_pair("mfma_kernel", _W(64), "lse") == {"f32": 2 * 64}
     # the split log-sum-exp: six bf16 products per coordinate, no P . B
     assert bench.matrix_flops_per_pair("mfma_split_kernel", _W(64), "lse") == {"bf16": 12 * 64}
-    # the fused gradient at D = 128 runs 129 signal columns in three chunks
+    # the fused gradient at D = 128 runs 129 signal columns in two launches of
+    # 64 on the matrix cores (the 129th on the vector ALU)
     mx = bench.matrix_flops_per_pair("mfma_split_kernel", _W(128, 1), "sum", "gauss_gradx")
-    assert mx == {"bf16": 3 * 6 * 4 * per32 + 192 * (4 + 4 + 1)}
+    assert mx == {"bf16": 2 * 6 * 4 * per32 + 192 * (4 + 4)}
+    # D = 256 (257 columns, the 16x16x32 kernel): five launches
+    mx = bench.matrix_flops_per_pair("mfma_split_kernel", _W(256, 1), "sum", "gauss_gradx")
+    assert len(mx) == 2 and mx["f32"] == 32 * (4 + 4 + 4 + 4 + 1)
     assert bench.matrix_flops_per_pair("sum_kernel", _W(3), "sum") == {}
 
 
