@@ -51,6 +51,7 @@ CASES = [
     ("sinkhorn", "lse", 48, 1, dict(eps=1.0), (1200, 2000), (300, 500)),
     ("sinkhorn", "lse", 48, 1, dict(eps=1.0, flags=4), (1200, 2000), (300, 500)),      # large D, split log-sum-exp
     ("gauss", "sum", 128, 40, dict(sigma=1.0, flags=4), (900, 1300), (300, 400)),      # split, 64 signal columns
+    ("gauss_gradx", "sum", 64, 1, dict(sigma=1.0, flags=4), (1500, 2500), (400, 600)),  # 65th column in the first launch
     ("gauss", "max", 24, 3, dict(sigma=1.0), (800, 1500), (200, 300)),
 ]
 
