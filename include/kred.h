@@ -343,8 +343,9 @@ int64_t kred_scratch_bytes(kred_formula f, kred_reduction r, const kred_params* 
  * and p->K are ignored.  Ranges: 0 <= M, N <= 2^31 - 1, 1 <= D <= KRED_MAX_D,
  * 1 <= E <= KRED_MAX_E.  For D > 16, gx and gy run as one Gaussian sum with
  * the E (D + 1) signal columns [b_e, b_e (y - m)] (m a centre of y), 64
- * columns per matrix-core launch, contracted with the cotangent; scratch
- * grows by about (M + 64 N) E (D + 1) floats.  With M = 0 or N = 0
+ * columns per matrix-core launch (on the split kernel at D <= 128 a last
+ * single column is summed by the first launch), contracted with the
+ * cotangent; scratch grows by about (M + 64 N) E (D + 1) floats.  With M = 0 or N = 0
  * the requested outputs are filled with zeros.  x, y and e are required, and
  * b too for gx or gy, whenever M, N > 0 and an output is requested.  Same
  * error and asynchrony rules as kred_run: on any argument error nothing runs.
