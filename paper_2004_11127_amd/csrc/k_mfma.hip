@@ -692,11 +692,17 @@ void mfma_split_kernel(MfmaArgs a) {
   // loaded 16-column blocks reads a padding norm), the b planes (the row
   // padding slots read any b), and the y planes (a column past the loaded
   // blocks reads a copy of the last loaded one: finite, removed by its norm)
+  // (with XC the per-lane load offsets pass through an empty asm statement
+  // each tile, so that the compiler recomputes their 64-bit addresses instead
+  // of keeping them across the loop: at DP = 128, 64 signal columns, that
+  // spilled them, 79.4 ms per launch against 74.4 without)
   auto fetch = [&](uint4 (&yd)[TU], float4 (&nd)[NQ], uint4 (&bd)[BQ], int64_t jt, int64_t lo,
                    int64_t hi) __attribute__((always_inline)) {
     const int ncol = (int)min((int64_t)TJ, ((hi + 15) & ~(int64_t)15) - jt);
     if (wave == NWV - 1 && lane < TJ) {
-      const int64_t col = jt + lane;
+      int ln = lane;
+      if constexpr (XC) asm volatile("" : "+v"(ln));
+      const int64_t col = jt + ln;
       const bool live = SP ? (col >= lo && col < hi) : (lane < ncol);
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.ny + (live ? col : a.N16)),
                                        (__attribute__((address_space(3))) void*)(&nd[0]), 4, 0, 0);
@@ -704,7 +710,9 @@ void mfma_split_kernel(MfmaArgs a) {
     if constexpr (XC) {
       // the extra column's values (a masked column reads the zero at N16)
       if (wave == NWV - 2 && lane < TJ) {
-        const int64_t col = jt + lane;
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int64_t col = jt + ln;
         const bool live = SP ? (col >= lo && col < hi) : (lane < ncol);
         __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.xb + (live ? col : a.N16)),
                                          (__attribute__((address_space(3))) void*)(&nd[TJ / 4]), 4, 0, 0);
@@ -716,8 +724,10 @@ void mfma_split_kernel(MfmaArgs a) {
       const int o = NWV * k + wave;   // the wave's window of the slot
       if (o >= BO) break;             // wave-uniform
       const int sl = 64 * o + lane, row = sl / 5, kc = sl - row * 5;
+      int bo = row * 4 + (kc < 4 ? kc : 0);
+      if constexpr (XC) asm volatile("" : "+v"(bo));
       if (sl < 15 * W)
-        __builtin_amdgcn_global_load_lds(static_cast<const void*>(bsrc + row * 4 + (kc < 4 ? kc : 0)),
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(bsrc + bo),
                                          (__attribute__((address_space(3))) void*)(&bd[64 * o]), 16, 0, 0);
     }
     const uint4* ysrc = reinterpret_cast<const uint4*>(a.ysp + jt * 3 * DP);
@@ -726,6 +736,7 @@ void mfma_split_kernel(MfmaArgs a) {
       const int s0 = 64 * (NWV * k + wave);
       if (k >= YMIN && s0 >= TU) break;   // wave-uniform
       int src = yoff[k];
+      if constexpr (XC) asm volatile("" : "+v"(src));
       if (ncol < TJ) {
         const int sl = s0 + lane;
         const int cc = sl / (3 * PU), qq = sl - cc * 3 * PU;
