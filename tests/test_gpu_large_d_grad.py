@@ -133,7 +133,8 @@ def test_backward_ranges_large_d(ctx, E):
 # 129), the last column is summed on the vector ALU by the first launch; its
 # own call then only lets the fp64 contraction run when the guard picks it
 @pytest.mark.parametrize("C", [1, 2, 8])
-@pytest.mark.parametrize("M,N,D", [(700, 1500, 64), (520, 1100, 128), (300, 65, 64)])
+@pytest.mark.parametrize("M,N,D", [(700, 1500, 64), (520, 1100, 128), (300, 65, 64), (1, 1, 64),
+                                   (37, 31, 128)])
 def test_gradx_last_column_with_the_first_launch(ctx, M, N, D, C):
     from paper_2004_11127_amd import kred
     x, y, b = _data(D + C + N, M, N, D, offset=1.5)
